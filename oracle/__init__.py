@@ -1,0 +1,178 @@
+"""SparCML reference oracle -- TEST INFRASTRUCTURE ONLY.
+
+Python (ctypes + numpy) front end of ``liboracle.so``, the plain sequential C
+implementation of the SparCML definitions (arXiv 1802.08021).  Only the
+tests, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
+``bench.py`` may import this package.  It shares no code with the HIP path.
+
+Functions follow the paper:
+  * ``sparse_reduce``  -- §5.1 sparse streams, switch rule, pairwise sum;
+                          §5.3.1 recursive doubling order.
+  * ``topk``           -- §2.2 Top-k sparsification, Alg. 1 error update.
+  * ``quantize``       -- §2.2 / §6 QSGD stochastic quantization.
+  * ``dequantize``, ``densify``, ``philox4x32_10``.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "liboracle.so")
+_SOURCES = [os.path.join(_HERE, "oracle.c")]
+
+
+def build(force: bool = True) -> str:
+    """Compile liboracle.so with gcc (no contraction, no fast-math)."""
+    if not force and os.path.exists(LIB_PATH):
+        return LIB_PATH
+    tmp = LIB_PATH + ".tmp"
+    cmd = ["gcc", "-O2", "-std=c11", "-ffp-contract=off", "-fno-fast-math",
+           "-fPIC", "-shared", "-o", tmp] + _SOURCES + ["-lm"]
+    subprocess.run(cmd, check=True)
+    os.replace(tmp, LIB_PATH)
+    return LIB_PATH
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            build()
+        L = ctypes.CDLL(LIB_PATH)
+        u32p = ctypes.POINTER(ctypes.c_uint32)
+        vp = ctypes.c_void_p
+        L.orc_philox4x32_10.argtypes = [u32p, u32p, u32p]
+        L.orc_philox4x32_10.restype = None
+        L.orc_sparse_reduce.argtypes = [
+            ctypes.c_int, vp, vp, vp, ctypes.c_uint64, ctypes.c_double,
+            vp, ctypes.c_uint64, vp, vp, vp, vp, vp]
+        L.orc_sparse_reduce.restype = ctypes.c_int
+        L.orc_topk.argtypes = [ctypes.c_int, vp, ctypes.c_uint64, ctypes.c_uint64, vp, vp, vp]
+        L.orc_topk.restype = ctypes.c_int
+        L.orc_quantize.argtypes = [ctypes.c_int, vp, vp, ctypes.c_int, ctypes.c_uint64, vp, vp, vp]
+        L.orc_quantize.restype = ctypes.c_int
+        L.orc_dequantize.argtypes = [vp, ctypes.c_float, ctypes.c_int, ctypes.c_uint64, vp]
+        L.orc_dequantize.restype = ctypes.c_int
+        L.orc_densify.argtypes = [vp, vp, ctypes.c_uint64, ctypes.c_uint64, vp]
+        L.orc_densify.restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+class OracleError(RuntimeError):
+    pass
+
+
+def _ptr(a: np.ndarray) -> int:
+    return a.ctypes.data if a.size else 0
+
+
+def _ptr_table(arrs):
+    return (ctypes.c_void_p * len(arrs))(*[_ptr(a) for a in arrs])
+
+
+def philox4x32_10(ctr, key):
+    """One Philox4x32-10 block (Salmon et al., SC'11)."""
+    c = (ctypes.c_uint32 * 4)(*[int(v) & 0xFFFFFFFF for v in ctr])
+    k = (ctypes.c_uint32 * 2)(*[int(v) & 0xFFFFFFFF for v in key])
+    o = (ctypes.c_uint32 * 4)()
+    lib().orc_philox4x32_10(c, k, o)
+    return [int(v) for v in o]
+
+
+def threshold(N: int, delta: float) -> int:
+    """Sparse-item threshold: floor(delta * N) in double (§5.1)."""
+    return int(np.floor(np.float64(delta) * np.float64(N)))
+
+
+def sparse_reduce(idx_list, val_list, N: int, delta: float):
+    """Recursive-doubling sparse allreduce with the dense switch.
+
+    Returns dict(idx, val, nnz, dense, node_nnz, node_dense); for a dense root
+    ``val`` holds all N values and ``idx`` is None.
+    """
+    P = len(idx_list)
+    idx_list = [np.ascontiguousarray(a, dtype=np.uint32) for a in idx_list]
+    val_list = [np.ascontiguousarray(a, dtype=np.float32) for a in val_list]
+    nnz = np.array([a.size for a in idx_list], dtype=np.uint64)
+    cap = int(min(nnz.sum(), N)) if P else 0
+    out_idx = np.zeros(max(cap, 1), dtype=np.uint32)
+    out_val = np.zeros(N, dtype=np.float32)
+    out_nnz = np.zeros(1, dtype=np.uint64)
+    out_dense = np.zeros(1, dtype=np.int32)
+    node_nnz = np.zeros(max(P - 1, 1), dtype=np.uint64)
+    node_dense = np.zeros(max(P - 1, 1), dtype=np.uint8)
+    rc = lib().orc_sparse_reduce(
+        P, _ptr_table(idx_list), _ptr_table(val_list), nnz.ctypes.data, N, float(delta),
+        out_idx.ctypes.data, cap, out_val.ctypes.data, out_nnz.ctypes.data,
+        out_dense.ctypes.data, node_nnz.ctypes.data, node_dense.ctypes.data)
+    if rc != 0:
+        raise OracleError(f"orc_sparse_reduce returned {rc}")
+    n = int(out_nnz[0])
+    dense = bool(out_dense[0])
+    return {
+        "idx": None if dense else out_idx[:n].copy(),
+        "val": out_val if dense else out_val[:n].copy(),
+        "nnz": n,
+        "dense": dense,
+        "node_nnz": node_nnz[: P - 1].copy(),
+        "node_dense": node_dense[: P - 1].copy(),
+    }
+
+
+def topk(x: np.ndarray, k: int, residual: bool = False):
+    """Exact per-row top-k by magnitude of x[P, N] by a full sort."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    P, N = x.shape
+    out_idx = np.zeros((P, max(k, 1)), dtype=np.uint32)
+    out_val = np.zeros((P, max(k, 1)), dtype=np.float32)
+    res = x.copy() if residual else None
+    rc = lib().orc_topk(P, x.ctypes.data, N, k, out_idx.ctypes.data, out_val.ctypes.data,
+                        res.ctypes.data if residual else None)
+    if rc != 0:
+        raise OracleError(f"orc_topk returned {rc}")
+    return out_idx[:, :k].copy(), out_val[:, :k].copy(), res
+
+
+def quantize(val_list, bits: int, seed: int):
+    """QSGD per stream.  Returns (codes list, scales[P], dequantized list)."""
+    P = len(val_list)
+    val_list = [np.ascontiguousarray(a, dtype=np.float32) for a in val_list]
+    nnz = np.array([a.size for a in val_list], dtype=np.uint64)
+    per_byte = 8 // bits
+    q = [np.zeros(max((a.size + per_byte - 1) // per_byte, 1), dtype=np.uint8) for a in val_list]
+    deq = [np.zeros(max(a.size, 1), dtype=np.float32) for a in val_list]
+    scale = np.zeros(P, dtype=np.float32)
+    rc = lib().orc_quantize(P, _ptr_table(val_list), nnz.ctypes.data, bits, seed & (2**64 - 1),
+                            _ptr_table(q), scale.ctypes.data, _ptr_table(deq))
+    if rc != 0:
+        raise OracleError(f"orc_quantize returned {rc}")
+    nb = [(a.size + per_byte - 1) // per_byte for a in val_list]
+    return ([qq[:n].copy() for qq, n in zip(q, nb)], scale,
+            [d[: a.size].copy() for d, a in zip(deq, val_list)])
+
+
+def dequantize(q: np.ndarray, scale: float, bits: int, n: int) -> np.ndarray:
+    q = np.ascontiguousarray(q, dtype=np.uint8)
+    out = np.zeros(max(n, 1), dtype=np.float32)
+    rc = lib().orc_dequantize(_ptr(q), ctypes.c_float(scale), bits, n, out.ctypes.data)
+    if rc != 0:
+        raise OracleError(f"orc_dequantize returned {rc}")
+    return out[:n].copy()
+
+
+def densify(idx: np.ndarray, val: np.ndarray, N: int) -> np.ndarray:
+    idx = np.ascontiguousarray(idx, dtype=np.uint32)
+    val = np.ascontiguousarray(val, dtype=np.float32)
+    out = np.zeros(N, dtype=np.float32)
+    rc = lib().orc_densify(_ptr(idx), _ptr(val), idx.size, N, out.ctypes.data)
+    if rc != 0:
+        raise OracleError(f"orc_densify returned {rc}")
+    return out

@@ -1,0 +1,401 @@
+/*
+ * SparCML reference oracle -- TEST INFRASTRUCTURE ONLY (see oracle.h).
+ *
+ * Each function restates, in the plainest sequential form, a definition from
+ * Renggli et al., "SparCML", arXiv 1802.08021.  Nothing here is blocked,
+ * fused or reordered beyond what the definition states; the only library
+ * primitives used are qsort (top-k by full sort) and sqrt.  Values are fp32
+ * (the value type of the sparse streams, §5.1 "Vector Representations");
+ * the QSGD norm, which the paper leaves unspecified, is accumulated in fp64.
+ *
+ * Build: gcc -O2 -std=c11 -ffp-contract=off -fno-fast-math -shared -fPIC.
+ */
+#include "oracle.h"
+
+#include <math.h>
+#include <stdlib.h>
+#include <string.h>
+
+/* ------------------------------------------------------------------------ */
+/* Philox4x32-10 (Salmon et al., SC'11).  State: four 32-bit words; key: two.
+ * One round multiplies words 0 and 2 by the two Philox constants, splits
+ * each 64-bit product into high/low halves and mixes the high halves with
+ * words 1 and 3 and the round key; the key is bumped by the two Weyl
+ * constants between rounds. */
+void orc_philox4x32_10(const uint32_t ctr[4], const uint32_t key[2], uint32_t out[4])
+{
+    const uint32_t M0 = 0xD2511F53u, M1 = 0xCD9E8D57u;
+    const uint32_t W0 = 0x9E3779B9u, W1 = 0xBB67AE85u;
+    uint32_t x0 = ctr[0], x1 = ctr[1], x2 = ctr[2], x3 = ctr[3];
+    uint32_t k0 = key[0], k1 = key[1];
+    for (int round = 0; round < 10; ++round) {
+        if (round > 0) {
+            k0 += W0;
+            k1 += W1;
+        }
+        uint64_t p0 = (uint64_t)M0 * (uint64_t)x0;
+        uint64_t p1 = (uint64_t)M1 * (uint64_t)x2;
+        uint32_t hi0 = (uint32_t)(p0 >> 32), lo0 = (uint32_t)p0;
+        uint32_t hi1 = (uint32_t)(p1 >> 32), lo1 = (uint32_t)p1;
+        uint32_t y0 = hi1 ^ x1 ^ k0;
+        uint32_t y1 = lo1;
+        uint32_t y2 = hi0 ^ x3 ^ k1;
+        uint32_t y3 = lo0;
+        x0 = y0; x1 = y1; x2 = y2; x3 = y3;
+    }
+    out[0] = x0; out[1] = x1; out[2] = x2; out[3] = x3;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Sparse streams and their pairwise sum (§5.1).                            */
+
+typedef struct {
+    int dense;      /* representation flag (§5.1 "Switching to a Dense Format") */
+    uint64_t nnz;   /* sparse: number of pairs; dense: N */
+    uint32_t* idx;  /* sparse only */
+    float* val;     /* sparse: nnz values; dense: N values */
+    int owned;      /* buffers belong to the oracle (freed after use) */
+} onode;
+
+static int is_pow2(int p) { return p >= 1 && (p & (p - 1)) == 0; }
+
+static void node_free(onode* n)
+{
+    if (n->owned) {
+        free(n->idx);
+        free(n->val);
+    }
+    n->idx = NULL;
+    n->val = NULL;
+}
+
+/* Both sparse, result sparse: ordered merge of the two index lists; an index
+ * present in both gets the fp32 sum of the two values. */
+static int sum_sparse_sparse(const onode* a, const onode* b, onode* o)
+{
+    uint64_t cap = a->nnz + b->nnz;
+    o->dense = 0;
+    o->owned = 1;
+    o->idx = (uint32_t*)malloc((cap ? cap : 1) * sizeof(uint32_t));
+    o->val = (float*)malloc((cap ? cap : 1) * sizeof(float));
+    if (!o->idx || !o->val) return -4;
+    uint64_t i = 0, j = 0, n = 0;
+    while (i < a->nnz || j < b->nnz) {
+        if (j >= b->nnz || (i < a->nnz && a->idx[i] < b->idx[j])) {
+            o->idx[n] = a->idx[i];
+            o->val[n] = a->val[i];
+            ++i;
+        } else if (i >= a->nnz || b->idx[j] < a->idx[i]) {
+            o->idx[n] = b->idx[j];
+            o->val[n] = b->val[j];
+            ++j;
+        } else {
+            o->idx[n] = a->idx[i];
+            o->val[n] = a->val[i] + b->val[j];
+            ++i;
+            ++j;
+        }
+        ++n;
+    }
+    o->nnz = n;
+    return 0;
+}
+
+/* Add every pair of a sparse stream into a dense vector. */
+static void scatter_add(float* D, const onode* s)
+{
+    for (uint64_t i = 0; i < s->nnz; ++i) D[s->idx[i]] += s->val[i];
+}
+
+/* One node of the reduction tree: the four cases of §5.1 "Efficient
+ * Summation" for overlapping index sets, with the switch rule: two sparse
+ * inputs whose nnz upper bound |H1|+|H2| exceeds the threshold give a dense
+ * result. */
+static int sum_pair(const onode* L, const onode* R, uint64_t N, uint64_t thr, onode* o)
+{
+    if (!L->dense && !R->dense) {
+        if (L->nnz + R->nnz <= thr) return sum_sparse_sparse(L, R, o);
+        o->dense = 1;
+        o->owned = 1;
+        o->nnz = N;
+        o->idx = NULL;
+        o->val = (float*)calloc(N, sizeof(float)); /* all +0.0 */
+        if (!o->val) return -4;
+        scatter_add(o->val, L);
+        scatter_add(o->val, R);
+        return 0;
+    }
+    if (L->dense && R->dense) {
+        /* dense + dense: elementwise sum (into a fresh vector) */
+        o->dense = 1;
+        o->owned = 1;
+        o->nnz = N;
+        o->idx = NULL;
+        o->val = (float*)malloc(N * sizeof(float));
+        if (!o->val) return -4;
+        for (uint64_t j = 0; j < N; ++j) o->val[j] = L->val[j] + R->val[j];
+        return 0;
+    }
+    /* one dense, one sparse: copy the dense one, add the sparse pairs */
+    const onode* D = L->dense ? L : R;
+    const onode* S = L->dense ? R : L;
+    o->dense = 1;
+    o->owned = 1;
+    o->nnz = N;
+    o->idx = NULL;
+    o->val = (float*)malloc(N * sizeof(float));
+    if (!o->val) return -4;
+    memcpy(o->val, D->val, N * sizeof(float));
+    scatter_add(o->val, S);
+    return 0;
+}
+
+int orc_sparse_reduce(int P, const uint32_t* const* idx, const float* const* val,
+                      const uint64_t* nnz, uint64_t N, double delta,
+                      uint32_t* out_idx, uint64_t out_cap, float* out_val,
+                      uint64_t* out_nnz, int* out_dense,
+                      uint64_t* node_nnz, uint8_t* node_dense)
+{
+    if (!is_pow2(P) || N == 0 || N > 0xFFFFFFFFull || !(delta > 0.0)) return -1;
+    if (!idx || !val || !nnz || !out_val || !out_nnz || !out_dense) return -1;
+    /* threshold on the number of sparse items (§5.1), as a fraction of N */
+    double t = floor(delta * (double)N);
+    uint64_t thr = t >= 18446744073709551615.0 ? UINT64_MAX : (uint64_t)t;
+
+    for (int r = 0; r < P; ++r) {
+        if (nnz[r] > N) return -2;
+        if (nnz[r] && (!idx[r] || !val[r])) return -1;
+        for (uint64_t i = 0; i < nnz[r]; ++i) {
+            if (idx[r][i] >= N) return -2;
+            if (i > 0 && idx[r][i] <= idx[r][i - 1]) return -2;
+        }
+    }
+
+    onode* cur = (onode*)calloc((size_t)P, sizeof(onode));
+    if (!cur) return -4;
+    for (int r = 0; r < P; ++r) {
+        cur[r].dense = 0;
+        cur[r].nnz = nnz[r];
+        cur[r].idx = (uint32_t*)idx[r];
+        cur[r].val = (float*)val[r];
+        cur[r].owned = 0;
+    }
+
+    int rc = 0;
+    if (P == 1 && nnz[0] > thr) {
+        /* a single stream with more than thr items cannot stay sparse */
+        onode d = {1, N, NULL, (float*)calloc(N, sizeof(float)), 1};
+        if (!d.val) { free(cur); return -4; }
+        scatter_add(d.val, &cur[0]);
+        cur[0] = d;
+    }
+
+    /* Recursive doubling (§5.3.1): in round t the partners at distance
+     * 2^(t-1) hold the sums of adjacent blocks of 2^(t-1) ranks; their sum is
+     * node g of level t, made of nodes 2g and 2g+1 of level t-1. */
+    int width = P;
+    uint64_t node_base = 0;
+    while (width > 1) {
+        int half = width / 2;
+        onode* next = (onode*)calloc((size_t)half, sizeof(onode));
+        if (!next) { rc = -4; break; }
+        for (int g = 0; g < half && rc == 0; ++g) {
+            rc = sum_pair(&cur[2 * g], &cur[2 * g + 1], N, thr, &next[g]);
+            if (rc) break;
+            if (node_nnz) node_nnz[node_base + g] = next[g].nnz;
+            if (node_dense) node_dense[node_base + g] = (uint8_t)next[g].dense;
+            node_free(&cur[2 * g]);
+            node_free(&cur[2 * g + 1]);
+        }
+        if (rc) {
+            for (int g = 0; g < half; ++g) node_free(&next[g]);
+            free(next);
+            break;
+        }
+        free(cur);
+        cur = next;
+        node_base += (uint64_t)half;
+        width = half;
+    }
+    if (rc) {
+        for (int r = 0; r < width; ++r) node_free(&cur[r]);
+        free(cur);
+        return rc;
+    }
+
+    onode* root = &cur[0];
+    if (root->dense) {
+        memcpy(out_val, root->val, N * sizeof(float));
+        *out_nnz = N;
+        *out_dense = 1;
+    } else {
+        if (root->nnz > out_cap) {
+            node_free(root);
+            free(cur);
+            return -3;
+        }
+        if (root->nnz) {
+            memcpy(out_idx, root->idx, root->nnz * sizeof(uint32_t));
+            memcpy(out_val, root->val, root->nnz * sizeof(float));
+        }
+        *out_nnz = root->nnz;
+        *out_dense = 0;
+    }
+    node_free(root);
+    free(cur);
+    return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Top-k by magnitude (§2.2, Alg. 1).                                        */
+
+typedef struct {
+    uint32_t key;
+    uint32_t idx;
+} okv;
+
+static uint32_t mag_key(float v)
+{
+    uint32_t b;
+    memcpy(&b, &v, sizeof b);
+    return b & 0x7FFFFFFFu; /* |v| as an ordered integer */
+}
+
+static int cmp_key_desc_idx_asc(const void* pa, const void* pb)
+{
+    const okv* a = (const okv*)pa;
+    const okv* b = (const okv*)pb;
+    if (a->key != b->key) return a->key > b->key ? -1 : 1;
+    if (a->idx != b->idx) return a->idx < b->idx ? -1 : 1;
+    return 0;
+}
+
+static int cmp_u32(const void* pa, const void* pb)
+{
+    uint32_t a = *(const uint32_t*)pa, b = *(const uint32_t*)pb;
+    return a < b ? -1 : (a > b ? 1 : 0);
+}
+
+int orc_topk(int P, const float* x, uint64_t N, uint64_t k,
+             uint32_t* out_idx, float* out_val, float* residual)
+{
+    if (P < 1 || N == 0 || N > 0xFFFFFFFFull || k > N || !x) return -1;
+    if (k && (!out_idx || !out_val)) return -1;
+    okv* all = (okv*)malloc(N * sizeof(okv));
+    if (!all) return -4;
+    for (int r = 0; r < P; ++r) {
+        const float* row = x + (uint64_t)r * N;
+        for (uint64_t j = 0; j < N; ++j) {
+            all[j].key = mag_key(row[j]);
+            all[j].idx = (uint32_t)j;
+        }
+        qsort(all, N, sizeof(okv), cmp_key_desc_idx_asc);
+        uint32_t* sel = out_idx + (uint64_t)r * k;
+        for (uint64_t i = 0; i < k; ++i) sel[i] = all[i].idx;
+        qsort(sel, k, sizeof(uint32_t), cmp_u32);
+        float* v = out_val + (uint64_t)r * k;
+        for (uint64_t i = 0; i < k; ++i) v[i] = row[sel[i]];
+        if (residual) {
+            float* res = residual + (uint64_t)r * N;
+            if (res != row) memcpy(res, row, N * sizeof(float));
+            for (uint64_t i = 0; i < k; ++i) res[sel[i]] = 0.0f;
+        }
+    }
+    free(all);
+    return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* QSGD stochastic quantization (§2.2, §6).                                  */
+
+static int valid_bits(int bits) { return bits == 2 || bits == 4 || bits == 8; }
+
+int orc_quantize(int P, const float* const* val, const uint64_t* nnz, int bits,
+                 uint64_t seed, uint8_t* const* out_q, float* out_scale,
+                 float* const* out_deq)
+{
+    if (P < 1 || !valid_bits(bits) || !val || !nnz || !out_q || !out_scale) return -1;
+    const uint32_t s = (1u << (bits - 1)) - 1u; /* magnitude levels 0..s */
+    const int per_byte = 8 / bits;
+    const uint32_t key[2] = {(uint32_t)(seed & 0xFFFFFFFFu), (uint32_t)(seed >> 32)};
+    for (int r = 0; r < P; ++r) {
+        const uint64_t n = nnz[r];
+        const float* v = val[r];
+        uint8_t* q = out_q[r];
+        if (n && (!v || !q)) return -1;
+
+        /* L2 norm: squares summed by an adjacent-pair binary tree in fp64,
+         * zero-padded to a power of two. */
+        uint64_t m = 1;
+        while (m < n) m <<= 1;
+        double* t = (double*)calloc(m, sizeof(double));
+        if (!t) return -4;
+        for (uint64_t j = 0; j < n; ++j) t[j] = (double)v[j] * (double)v[j];
+        for (uint64_t w = m; w > 1; w >>= 1)
+            for (uint64_t i = 0; i < w / 2; ++i) t[i] = t[2 * i] + t[2 * i + 1];
+        double norm2 = n ? t[0] : 0.0;
+        free(t);
+        float scale = (float)sqrt(norm2);
+        out_scale[r] = scale;
+
+        uint64_t nbytes = (n + per_byte - 1) / per_byte;
+        if (nbytes) memset(q, 0, nbytes);
+        float* deq = out_deq ? out_deq[r] : NULL;
+        if (scale == 0.0f) {
+            if (deq)
+                for (uint64_t j = 0; j < n; ++j) deq[j] = 0.0f;
+            continue;
+        }
+        const float inv = (float)s / scale;  /* levels per unit of norm */
+        const float unit = scale / (float)s; /* value of one level */
+        for (uint64_t j = 0; j < n; ++j) {
+            float a = fabsf(v[j]) * inv;
+            uint32_t l = (uint32_t)a; /* floor, a >= 0 */
+            float f = a - (float)l;   /* exact */
+            uint32_t ctr[4] = {(uint32_t)(j >> 2), (uint32_t)r, 0u, 0u};
+            uint32_t word[4];
+            orc_philox4x32_10(ctr, key, word);
+            float u = (float)(word[j & 3] >> 8) * 0x1p-24f; /* uniform [0,1) */
+            if (u < f) l += 1u; /* round up with probability f */
+            if (l > s) l = s;
+            uint32_t sign = (v[j] < 0.0f && l > 0u) ? 1u : 0u;
+            uint32_t code = (sign << (bits - 1)) | l;
+            q[j / per_byte] |= (uint8_t)(code << ((j % per_byte) * bits));
+            if (deq) {
+                float mag = (float)l * unit;
+                deq[j] = l == 0u ? 0.0f : (sign ? -mag : mag);
+            }
+        }
+    }
+    return 0;
+}
+
+int orc_dequantize(const uint8_t* q, float scale, int bits, uint64_t n, float* out)
+{
+    if (!valid_bits(bits) || (n && (!q || !out))) return -1;
+    const uint32_t s = (1u << (bits - 1)) - 1u;
+    const int per_byte = 8 / bits;
+    const uint32_t lmask = s, smask = 1u << (bits - 1);
+    const float unit = scale / (float)s;
+    for (uint64_t j = 0; j < n; ++j) {
+        uint32_t code = (q[j / per_byte] >> ((j % per_byte) * bits)) & ((1u << bits) - 1u);
+        uint32_t l = code & lmask;
+        float mag = (float)l * unit;
+        out[j] = l == 0u ? 0.0f : ((code & smask) ? -mag : mag);
+    }
+    return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+
+int orc_densify(const uint32_t* idx, const float* val, uint64_t nnz, uint64_t N,
+                float* dense)
+{
+    if (N == 0 || !dense || (nnz && (!idx || !val))) return -1;
+    for (uint64_t j = 0; j < N; ++j) dense[j] = 0.0f;
+    for (uint64_t i = 0; i < nnz; ++i) {
+        if (idx[i] >= N) return -2;
+        dense[idx[i]] = val[i];
+    }
+    return 0;
+}
