@@ -1,0 +1,208 @@
+/*
+ * sparcml.h -- C ABI of the MI355X (gfx950) SparCML hot path.
+ *
+ * Implements the local reduction work of SparCML's sparse allreduce and its
+ * two producers (Renggli et al., "SparCML: High-Performance Sparse
+ * Communication for Machine Learning", arXiv 1802.08021):
+ *
+ *   sparcml_topk_sparsify  -- top-k sparsification of dense gradients
+ *                             (§2.2 "Structured Sparsification", Alg. 1)
+ *   sparcml_quantize       -- QSGD stochastic quantization (§2.2, §6)
+ *   sparcml_sparse_reduce  -- sum of P sparse streams in recursive-doubling
+ *                             order with the sparse->dense switch
+ *                             (§5.1, §5.3.1, Fig. 2)
+ *   sparcml_densify        -- dense representation of one stream (§5.1)
+ *
+ * Conventions shared by every call:
+ *   - All data pointers are DEVICE pointers (HBM of the current HIP device),
+ *     except the descriptor arrays (sparcml_stream[], pointer tables), which
+ *     are HOST memory read during the call.
+ *   - `stream` is a hipStream_t passed as void*; NULL means the null stream.
+ *     Work is enqueued on it in order; sparcml_sparse_reduce additionally
+ *     waits for its own result header (see there); the other calls return
+ *     without synchronizing.
+ *   - The caller owns every buffer.  The library never allocates, frees or
+ *     keeps device memory between calls and has no global mutable state
+ *     apart from the thread-local last-error message.  Scratch memory comes
+ *     from the caller's workspace (size from sparcml_workspace_size).
+ *     Calls on distinct streams with distinct workspaces may run
+ *     concurrently.
+ *   - Return value: SPARCML_OK (0) or a negative status.  Argument errors
+ *     are detected on the host before any device work is enqueued; on error
+ *     the outputs are unspecified.  No exception crosses the ABI.
+ *   - Values are finite fp32; NaN/Inf inputs give unspecified results.
+ */
+#ifndef SPARCML_H
+#define SPARCML_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#if defined(__GNUC__)
+#define SPARCML_API __attribute__((visibility("default")))
+#else
+#define SPARCML_API
+#endif
+
+#define SPARCML_OK 0
+#define SPARCML_EINVAL -1     /* bad argument (sizes, P, k, delta, bits, NULL pointers) */
+#define SPARCML_ECAPACITY -2  /* output capacity too small for the result */
+#define SPARCML_EWORKSPACE -3 /* workspace missing or smaller than required */
+#define SPARCML_EUNSORTED -4  /* stream indices not strictly ascending or >= N */
+#define SPARCML_EHIP -5       /* a HIP runtime call failed (see sparcml_last_error) */
+
+/* Operation ids for sparcml_workspace_size. */
+#define SPARCML_OP_TOPK 1
+#define SPARCML_OP_QUANTIZE 2
+#define SPARCML_OP_REDUCE 3
+#define SPARCML_OP_DENSIFY 4
+
+/*
+ * Sparse stream (§5.1 "Vector Representations" and "Switching to a Dense
+ * Format"): a representation flag plus either index/value pairs or a dense
+ * array.  Layout is structure-of-arrays.
+ *   idx      sparse: nnz uint32 indices, strictly ascending, each < N.
+ *   val      qbits == 0: sparse: nnz fp32 values; dense: N fp32 values.
+ *   qval     qbits != 0: QSGD codes packed 8/qbits per byte, element j in
+ *            byte j/(8/qbits) at bit (j%(8/qbits))*qbits; a code is
+ *            (sign << (qbits-1)) | level, level in [0, 2^(qbits-1)-1].
+ *   qscale   qbits != 0: device pointer to the stream's fp32 scale.
+ *   nnz      number of stored pairs (N for a dense stream).
+ *   is_dense representation flag.
+ *   qbits    0 (fp32 values) or 2, 4, 8.
+ */
+typedef struct sparcml_stream {
+    uint32_t* idx;
+    float* val;
+    uint8_t* qval;
+    float* qscale;
+    uint64_t nnz;
+    uint32_t is_dense;
+    uint32_t qbits;
+} sparcml_stream;
+
+/*
+ * Workspace bytes needed by an operation.
+ *   op       SPARCML_OP_*.
+ *   P        number of ranks (streams / rows).
+ *   N        dimension.
+ *   max_nnz  TOPK: k; QUANTIZE: largest stream length; REDUCE: largest
+ *            input stream nnz; DENSIFY: ignored.
+ *   delta    REDUCE only (switch threshold as a fraction of N).
+ * A workspace sized with max_nnz >= the actual largest nnz is sufficient.
+ * Returns SPARCML_OK and *bytes, or SPARCML_EINVAL.
+ */
+SPARCML_API int sparcml_workspace_size(int op, int P, uint64_t N, uint64_t max_nnz, double delta,
+                           size_t* bytes);
+
+/*
+ * Top-k sparsification by magnitude, per rank (§2.2 "Structured
+ * Sparsification": each node keeps the k largest-magnitude components;
+ * Alg. 1: eps = acc - TopK(acc)).
+ *   P, N, k    x is P rows of N fp32 (row r at x + r*N), 1 <= N < 2^32,
+ *              0 <= k <= N, P >= 1.
+ *   out_idx    [P][k] uint32: the selected indices of row r, ascending.
+ *   out_val    [P][k] fp32: x[r][out_idx[r][i]] (signed).
+ *   residual   NULL, or [P][N] fp32 receiving x with the selected entries
+ *              set to +0.0 (the error-feedback update).  May alias x, in
+ *              which case only the k selected entries per row are written.
+ * Ordering: magnitude = the IEEE bit pattern with the sign cleared; equal
+ * magnitudes are taken lowest index first.
+ * Errors: EINVAL (P < 1, N == 0 or >= 2^32, k > N, NULL x / outputs with
+ * k > 0), EWORKSPACE, EHIP.
+ */
+SPARCML_API int sparcml_topk_sparsify(int P, const float* x, uint64_t N, uint64_t k,
+                          uint32_t* out_idx, float* out_val, float* residual,
+                          void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * QSGD stochastic quantization of each stream's values (§2.2
+ * "Quantization", §6 "Supporting Low-Precision Communication"): scale =
+ * the stream's L2 norm (one bucket per stream); s = 2^(bits-1)-1 levels;
+ * element v -> level l = floor(|v| s/scale) + [u < frac], u uniform in
+ * [0,1), plus a sign bit; the dequantized value is +-l * (scale/s).
+ *   P        number of streams (P >= 1).
+ *   in       host array of P descriptors; in[r].val holds in[r].nnz fp32
+ *            values (qbits must be 0; idx/is_dense are not read).
+ *   bits     2, 4 or 8.
+ *   seed     key of the Philox4x32-10 generator (Salmon et al., SC'11):
+ *            element j of stream r uses word (j & 3) of the block at
+ *            counter (j >> 2, r, 0, 0), key (seed & 0xffffffff, seed >> 32);
+ *            u = (word >> 8) * 2^-24.  Results are deterministic in
+ *            (seed, r, j).
+ *   out_q    host array of P device pointers; out_q[r] receives
+ *            ceil(nnz_r * bits / 8) bytes of packed codes (layout as in
+ *            sparcml_stream.qval).
+ *   out_scale device array of P fp32 scales.  The L2 norm is accumulated
+ *            in fp64 over an adjacent-pair tree (zero-padded to a power of
+ *            two) and rounded once to fp32.
+ *   out_deq  NULL, or host array of P device pointers (entries may be NULL)
+ *            receiving the dequantized fp32 values.
+ * Errors: EINVAL, EWORKSPACE, EHIP.
+ */
+SPARCML_API int sparcml_quantize(int P, const sparcml_stream* in, int bits, uint64_t seed,
+                     uint8_t* const* out_q, float* out_scale, float* const* out_deq,
+                     void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Sparse allreduce of P streams, one GPU's share: the sum of all ranks'
+ * contributions, associated as the recursive-doubling rounds of §5.3.1
+ * (round t sums adjacent blocks of 2^(t-1) ranks: node g of level t is
+ * node 2g plus node 2g+1 of level t-1), with the representation switch of
+ * §5.1: a node is dense if a child is dense or |H_L| + |H_R| > thr, where
+ * thr = floor(delta * N) (computed in double) and |H| is a sparse child's
+ * exact nnz (the union of its leaves' index sets); otherwise it is the
+ * sorted union with values summed (fp32) where indices coincide.  Entries
+ * whose sum is zero are kept.  A dense node holds the sum at every index
+ * (+0.0 where no rank contributes).  For P == 1 the root is the single
+ * stream, dense iff its nnz > thr.
+ *   P        power of two, 1 <= P <= 256.
+ *   streams  host array of P sparse descriptors (is_dense == 0) with the
+ *            same qbits (0 = fp32 val, or 2/4/8 = QSGD codes dequantized on
+ *            the fly).  Indices strictly ascending and < N (not checked).
+ *   N        1 <= N < 2^32.   delta > 0 (fraction of N).
+ *   out      in: out->idx (capacity out->nnz entries, must be >=
+ *            min(thr, sum of input nnz), or >= nnz_0 when P == 1 and the
+ *            stream stays sparse), out->val (N floats), out->qbits == 0.
+ *            out: out->nnz = root nnz (N if dense), out->is_dense; a sparse
+ *            root occupies out->idx[0..nnz) / out->val[0..nnz), a dense
+ *            root out->val[0..N).
+ *   node_nnz   NULL or device uint64[P-1]: union size of every internal
+ *              node (N for dense nodes), level order: level-1 nodes first
+ *              (g ascending), root last.
+ *   node_dense NULL or device uint8[P-1]: switch decision per node.
+ * Synchronization: the call reads back a 16-byte result header from the
+ * device and therefore waits for its own work on `stream`.
+ * Errors: EINVAL (including P > 256 or mixed qbits), ECAPACITY (out->nnz
+ * below the capacity stated above), EWORKSPACE, EHIP; all but EHIP are
+ * detected before any device work is enqueued.
+ */
+SPARCML_API int sparcml_sparse_reduce(int P, const sparcml_stream* streams, uint64_t N, double delta,
+                          sparcml_stream* out, uint64_t* node_nnz, uint8_t* node_dense,
+                          void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Dense representation of one stream (§5.1): dense[j] = value of index j,
+ * +0.0 where absent; dequantizes QSGD codes on the fly.  A dense input is
+ * copied (or dequantized).  Writes all N floats.  Indices must be strictly
+ * ascending and < N (not checked).
+ * Errors: EINVAL (NULL pointers, N == 0 or >= 2^32, nnz > N, bad qbits),
+ * EHIP.
+ */
+SPARCML_API int sparcml_densify(const sparcml_stream* in, uint64_t N, float* dense, void* stream);
+
+/* Static description of a status code. */
+SPARCML_API const char* sparcml_strerror(int status);
+
+/* Detail of the last error on the calling thread ("" if none). */
+SPARCML_API const char* sparcml_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SPARCML_H */

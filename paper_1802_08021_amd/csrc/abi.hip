@@ -1,0 +1,251 @@
+// C ABI entry points (declared in include/sparcml.h): argument validation on
+// the host, workspace checks, then the device passes.
+#include "../../include/sparcml.h"
+#include "internal.h"
+
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <algorithm>
+#include <exception>
+#include <vector>
+
+using namespace sparcml;
+
+namespace {
+
+thread_local char g_last_error[512] = "";
+
+int fail(int status, const char* fmt, ...)
+{
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
+    va_end(ap);
+    return status;
+}
+
+int hip_fail(hipError_t e, const char* where)
+{
+    return fail(SPARCML_EHIP, "%s: %s", where, hipGetErrorString(e));
+}
+
+bool valid_n(uint64_t N) { return N >= 1 && N < (1ull << 32); }
+bool valid_bits(uint32_t b) { return b == 2 || b == 4 || b == 8; }
+bool is_pow2(int p) { return p >= 1 && (p & (p - 1)) == 0; }
+
+int reduce_validate(int P, const sparcml_stream* streams, uint64_t N, double delta, uint32_t* qbits,
+                    uint64_t* max_nnz, uint64_t* sum_nnz)
+{
+    if (!is_pow2(P) || P > 256) return fail(SPARCML_EINVAL, "P must be a power of two in [1, 256] (got %d)", P);
+    if (!valid_n(N)) return fail(SPARCML_EINVAL, "N must be in [1, 2^32)");
+    if (!(delta > 0.0) || isnan(delta)) return fail(SPARCML_EINVAL, "delta must be > 0");
+    if (!streams) return fail(SPARCML_EINVAL, "streams is NULL");
+    *qbits = streams[0].qbits;
+    *max_nnz = 0;
+    *sum_nnz = 0;
+    for (int r = 0; r < P; ++r) {
+        const sparcml_stream& s = streams[r];
+        if (s.is_dense) return fail(SPARCML_EINVAL, "stream %d: inputs must be sparse", r);
+        if (s.qbits != *qbits) return fail(SPARCML_EINVAL, "stream %d: all streams must share qbits", r);
+        if (s.qbits && !valid_bits(s.qbits)) return fail(SPARCML_EINVAL, "stream %d: qbits must be 0, 2, 4 or 8", r);
+        if (s.nnz > N) return fail(SPARCML_EINVAL, "stream %d: nnz > N", r);
+        if (s.qbits && !s.qscale) return fail(SPARCML_EINVAL, "stream %d: qscale is NULL", r);
+        if (s.nnz) {
+            if (!s.idx) return fail(SPARCML_EINVAL, "stream %d: idx is NULL", r);
+            if (s.qbits ? !s.qval : !s.val) return fail(SPARCML_EINVAL, "stream %d: values are NULL", r);
+        }
+        *max_nnz = std::max(*max_nnz, s.nnz);
+        *sum_nnz += s.nnz;
+    }
+    return SPARCML_OK;
+}
+
+uint64_t threshold(uint64_t N, double delta)
+{
+    const double t = floor(delta * (double)N);
+    return t >= 18446744073709551615.0 ? UINT64_MAX : (uint64_t)t;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* sparcml_strerror(int status)
+{
+    switch (status) {
+    case SPARCML_OK: return "success";
+    case SPARCML_EINVAL: return "invalid argument";
+    case SPARCML_ECAPACITY: return "output capacity too small";
+    case SPARCML_EWORKSPACE: return "workspace missing or too small";
+    case SPARCML_EUNSORTED: return "stream indices not strictly ascending or out of range";
+    case SPARCML_EHIP: return "HIP runtime error";
+    default: return "unknown status";
+    }
+}
+
+const char* sparcml_last_error(void) { return g_last_error; }
+
+int sparcml_workspace_size(int op, int P, uint64_t N, uint64_t max_nnz, double delta, size_t* bytes)
+{
+    if (!bytes) return fail(SPARCML_EINVAL, "bytes is NULL");
+    switch (op) {
+    case SPARCML_OP_TOPK:
+        if (P < 1 || !valid_n(N) || max_nnz > N) return fail(SPARCML_EINVAL, "bad top-k sizes");
+        *bytes = max_nnz ? topk_workspace(P, N, max_nnz) : 0;
+        return SPARCML_OK;
+    case SPARCML_OP_QUANTIZE:
+        if (P < 1) return fail(SPARCML_EINVAL, "P must be >= 1");
+        *bytes = quant_workspace(P, max_nnz);
+        return SPARCML_OK;
+    case SPARCML_OP_REDUCE: {
+        if (!is_pow2(P) || P > 256 || !valid_n(N) || !(delta > 0.0) || max_nnz > N)
+            return fail(SPARCML_EINVAL, "bad reduce sizes");
+        ReducePlan p;
+        reduce_plan(P, N, max_nnz, 0, delta, 0, &p);
+        *bytes = P == 1 ? 0 : reduce_workspace(p);
+        return SPARCML_OK;
+    }
+    case SPARCML_OP_DENSIFY:
+        *bytes = 0;
+        return SPARCML_OK;
+    default: return fail(SPARCML_EINVAL, "unknown op %d", op);
+    }
+}
+
+int sparcml_topk_sparsify(int P, const float* x, uint64_t N, uint64_t k, uint32_t* out_idx,
+                          float* out_val, float* residual, void* ws, size_t ws_bytes, void* stream)
+{
+    try {
+        if (P < 1) return fail(SPARCML_EINVAL, "P must be >= 1");
+        if (!valid_n(N)) return fail(SPARCML_EINVAL, "N must be in [1, 2^32)");
+        if (k > N) return fail(SPARCML_EINVAL, "k > N");
+        if (!x) return fail(SPARCML_EINVAL, "x is NULL");
+        if (k && (!out_idx || !out_val)) return fail(SPARCML_EINVAL, "outputs are NULL");
+        const size_t need = k ? topk_workspace(P, N, k) : 0;
+        if (need && (!ws || ws_bytes < need))
+            return fail(SPARCML_EWORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
+        hipError_t e = topk_run(P, x, N, k, out_idx, out_val, residual, ws, (hipStream_t)stream);
+        if (e != hipSuccess) return hip_fail(e, "topk");
+        return SPARCML_OK;
+    } catch (const std::exception& ex) {
+        return fail(SPARCML_EHIP, "host exception: %s", ex.what());
+    }
+}
+
+int sparcml_quantize(int P, const sparcml_stream* in, int bits, uint64_t seed, uint8_t* const* out_q,
+                     float* out_scale, float* const* out_deq, void* ws, size_t ws_bytes, void* stream)
+{
+    try {
+        if (P < 1) return fail(SPARCML_EINVAL, "P must be >= 1");
+        if (!valid_bits((uint32_t)bits)) return fail(SPARCML_EINVAL, "bits must be 2, 4 or 8");
+        if (!in || !out_q || !out_scale) return fail(SPARCML_EINVAL, "NULL argument");
+        std::vector<const float*> vals(P);
+        std::vector<uint64_t> n(P);
+        uint64_t max_n = 0;
+        for (int r = 0; r < P; ++r) {
+            if (in[r].qbits) return fail(SPARCML_EINVAL, "stream %d: input must hold fp32 values", r);
+            if (in[r].nnz >= (1ull << 40)) return fail(SPARCML_EINVAL, "stream %d: too long", r);
+            if (in[r].nnz && (!in[r].val || !out_q[r])) return fail(SPARCML_EINVAL, "stream %d: NULL pointer", r);
+            vals[r] = in[r].val;
+            n[r] = in[r].nnz;
+            max_n = std::max(max_n, n[r]);
+        }
+        const size_t need = quant_workspace(P, max_n);
+        if (!ws || ws_bytes < need) return fail(SPARCML_EWORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
+        hipError_t e = quant_run(P, vals.data(), n.data(), bits, seed, out_q, out_scale, out_deq, ws,
+                                 (hipStream_t)stream);
+        if (e != hipSuccess) return hip_fail(e, "quantize");
+        return SPARCML_OK;
+    } catch (const std::exception& ex) {
+        return fail(SPARCML_EHIP, "host exception: %s", ex.what());
+    }
+}
+
+int sparcml_sparse_reduce(int P, const sparcml_stream* streams, uint64_t N, double delta,
+                          sparcml_stream* out, uint64_t* node_nnz, uint8_t* node_dense, void* ws,
+                          size_t ws_bytes, void* stream)
+{
+    try {
+        uint32_t qbits;
+        uint64_t max_nnz, sum_nnz;
+        int rc = reduce_validate(P, streams, N, delta, &qbits, &max_nnz, &sum_nnz);
+        if (rc) return rc;
+        if (!out || !out->val) return fail(SPARCML_EINVAL, "out / out->val is NULL");
+        if (out->qbits) return fail(SPARCML_EINVAL, "out->qbits must be 0");
+        const uint64_t thr = threshold(N, delta);
+        const hipStream_t s = (hipStream_t)stream;
+        hipError_t e;
+
+        if (P == 1) {
+            const sparcml_stream& a = streams[0];
+            if (a.nnz > thr) {
+                e = densify_run(a.idx, a.val, a.qval, a.qscale, qbits, a.nnz, N, 0, out->val, s);
+                if (e != hipSuccess) return hip_fail(e, "densify");
+                out->nnz = N;
+                out->is_dense = 1;
+                return SPARCML_OK;
+            }
+            if (a.nnz && !out->idx) return fail(SPARCML_EINVAL, "out->idx is NULL");
+            if (out->nnz < a.nnz) return fail(SPARCML_ECAPACITY, "out capacity %llu < %llu",
+                                              (unsigned long long)out->nnz, (unsigned long long)a.nnz);
+            if (a.nnz) {
+                e = hipMemcpyAsync(out->idx, a.idx, a.nnz * sizeof(uint32_t), hipMemcpyDeviceToDevice, s);
+                if (e == hipSuccess)
+                    e = qbits ? dequant_run(a.qval, a.qscale, qbits, a.nnz, out->val, s)
+                              : hipMemcpyAsync(out->val, a.val, a.nnz * sizeof(float),
+                                               hipMemcpyDeviceToDevice, s);
+                if (e != hipSuccess) return hip_fail(e, "copy");
+            }
+            out->nnz = a.nnz;
+            out->is_dense = 0;
+            return SPARCML_OK;
+        }
+
+        const uint64_t cap = std::min(thr, sum_nnz);
+        if (cap && !out->idx) return fail(SPARCML_EINVAL, "out->idx is NULL");
+        if (out->nnz < cap)
+            return fail(SPARCML_ECAPACITY, "out capacity %llu < min(thr, sum nnz) = %llu",
+                        (unsigned long long)out->nnz, (unsigned long long)cap);
+        ReducePlan plan;
+        reduce_plan(P, N, max_nnz, sum_nnz, delta, (int)qbits, &plan);
+        const size_t need = reduce_workspace(plan);
+        if (!ws || ws_bytes < need) return fail(SPARCML_EWORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
+
+        std::vector<StreamDesc> tab(P);
+        for (int r = 0; r < P; ++r)
+            tab[r] = StreamDesc{streams[r].idx, streams[r].val, streams[r].qval, streams[r].qscale,
+                                streams[r].nnz, 0};
+        ReduceResult res{};
+        e = reduce_run(plan, tab.data(), out->idx, out->val, node_nnz, node_dense, ws, s, &res);
+        if (e != hipSuccess) return hip_fail(e, "sparse_reduce");
+        out->nnz = res.nnz;
+        out->is_dense = res.dense;
+        return SPARCML_OK;
+    } catch (const std::exception& ex) {
+        return fail(SPARCML_EHIP, "host exception: %s", ex.what());
+    }
+}
+
+int sparcml_densify(const sparcml_stream* in, uint64_t N, float* dense, void* stream)
+{
+    if (!in || !dense) return fail(SPARCML_EINVAL, "NULL argument");
+    if (!valid_n(N)) return fail(SPARCML_EINVAL, "N must be in [1, 2^32)");
+    if (in->qbits && !valid_bits(in->qbits)) return fail(SPARCML_EINVAL, "qbits must be 0, 2, 4 or 8");
+    if (in->qbits && !in->qscale) return fail(SPARCML_EINVAL, "qscale is NULL");
+    const bool has_vals = in->qbits ? in->qval != nullptr : in->val != nullptr;
+    if (in->is_dense) {
+        if (!has_vals) return fail(SPARCML_EINVAL, "values are NULL");
+    } else {
+        if (in->nnz > N) return fail(SPARCML_EINVAL, "nnz > N");
+        if (in->nnz && (!in->idx || !has_vals)) return fail(SPARCML_EINVAL, "NULL stream arrays");
+    }
+    hipError_t e = densify_run(in->idx, in->val, in->qval, in->qscale, in->qbits, in->nnz, N,
+                               in->is_dense ? 1 : 0, dense, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "densify");
+    return SPARCML_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,85 @@
+// Internal declarations of the gfx950 SparCML library (not part of the ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace sparcml {
+
+// Device copy of one input stream descriptor (48 bytes).
+struct StreamDesc {
+    const uint32_t* idx;
+    const float* val;
+    const uint8_t* qval;
+    const float* qscale;
+    uint64_t nnz;
+    uint64_t pad;
+};
+
+// Small host->device blobs travel as kernel arguments (no pageable copies).
+constexpr int kBlobWords = 768;
+struct Blob {
+    uint32_t nwords;
+    uint32_t words[kBlobWords];
+};
+hipError_t upload(void* dst, const void* src, size_t bytes, hipStream_t s);
+
+// Round x up to a multiple of a (a power of two).
+inline size_t align_up(size_t x, size_t a) { return (x + a - 1) & ~(a - 1); }
+
+// Bump allocator over a caller-provided workspace.
+struct Carve {
+    uint8_t* base;
+    size_t used;
+    explicit Carve(void* b) : base(static_cast<uint8_t*>(b)), used(0) {}
+    template <class T>
+    T* take(size_t count) {
+        used = align_up(used, 256);
+        T* p = reinterpret_cast<T*>(base ? base + used : nullptr);
+        used += count * sizeof(T);
+        return p;
+    }
+};
+
+// ---------------------------------------------------------------- reduce
+struct ReducePlan {
+    uint32_t P, L, MW, T, ntiles, nchunks, tiles_per_chunk, qbits;
+    uint64_t N, thr, sum_nnz;
+    int speculate_dense;
+};
+int reduce_plan(int P, uint64_t N, uint64_t max_nnz, uint64_t sum_nnz, double delta, int qbits,
+                ReducePlan* plan);
+size_t reduce_workspace(const ReducePlan& p);
+
+struct ReduceResult {
+    uint64_t nnz;
+    uint32_t dense;
+    uint32_t pad;
+};
+
+// Enqueue the whole reduction; writes the root header into *res (host).
+hipError_t reduce_run(const ReducePlan& p, const StreamDesc* host_tab, uint32_t* out_idx,
+                      float* out_val, uint64_t* node_nnz, uint8_t* node_dense, void* ws,
+                      hipStream_t s, ReduceResult* res);
+
+// ---------------------------------------------------------------- densify
+hipError_t densify_run(const uint32_t* idx, const float* val, const uint8_t* qval,
+                       const float* qscale, uint32_t qbits, uint64_t nnz, uint64_t N,
+                       int is_dense, float* dense, hipStream_t s);
+// out[i] = dequantized code i, i < n.
+hipError_t dequant_run(const uint8_t* qval, const float* qscale, uint32_t qbits, uint64_t n,
+                       float* out, hipStream_t s);
+
+// ---------------------------------------------------------------- top-k
+size_t topk_workspace(int P, uint64_t N, uint64_t k);
+hipError_t topk_run(int P, const float* x, uint64_t N, uint64_t k, uint32_t* out_idx,
+                    float* out_val, float* residual, void* ws, hipStream_t s);
+
+// ---------------------------------------------------------------- QSGD
+size_t quant_workspace(int P, uint64_t max_n);
+hipError_t quant_run(int P, const float* const* vals, const uint64_t* n, int bits, uint64_t seed,
+                     uint8_t* const* out_q, float* out_scale, float* const* out_deq, void* ws,
+                     hipStream_t s);
+
+}  // namespace sparcml

@@ -1,0 +1,231 @@
+// QSGD stochastic quantization on gfx950 (§2.2 "Quantization", §6): one
+// bucket per stream, scale = the stream's L2 norm, s = 2^(bits-1)-1 levels
+// plus a sign bit, unbiased stochastic rounding driven by Philox4x32-10.
+//
+// The norm is a fixed adjacent-pair tree in fp64 (zero-padded to a power of
+// two), so it is reproducible bit for bit: 64 consecutive squares are summed
+// by a lane butterfly, 32 such groups by a second butterfly, waves and
+// blocks in tree order, and block partials by further aligned trees.
+#include "internal.h"
+
+#include <algorithm>
+
+namespace sparcml {
+namespace {
+
+constexpr uint32_t kSeg = 8192;  // elements per first-level partial (256 threads)
+
+struct QDesc {
+    const float* val;
+    uint8_t* q;
+    float* deq;
+    uint64_t n;
+};
+
+__device__ __forceinline__ double butterfly_sum(double v, int width)
+{
+    for (int o = 1; o < width; o <<= 1) v = v + __shfl_xor(v, o);
+    return v;
+}
+
+// partial[r][b] = tree sum of v^2 over elements [b*kSeg, (b+1)*kSeg) of
+// stream r (zeros past the end).
+__global__ void __launch_bounds__(256) k_sumsq_partial(const QDesc* tab, double* partial, uint32_t Q)
+{
+    __shared__ double s_w[4];
+    const uint32_t r = blockIdx.y, b = blockIdx.x;
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    const float* v = tab[r].val;
+    const uint64_t n = tab[r].n;
+    const uint64_t base = (uint64_t)b * kSeg + (uint64_t)wv * 2048;
+    double mine = 0.0;
+    for (int it = 0; it < 32; ++it) {
+        const uint64_t e = base + (uint64_t)it * 64 + lane;
+        const double x = e < n ? (double)v[e] : 0.0;
+        const double g = butterfly_sum(x * x, 64);
+        if (lane == it) mine = g;
+    }
+    const double w = butterfly_sum(mine, 32);
+    if (lane == 0) s_w[wv] = w;
+    __syncthreads();
+    if (threadIdx.x == 0) partial[(uint64_t)r * Q + b] = (s_w[0] + s_w[1]) + (s_w[2] + s_w[3]);
+}
+
+// out[r][b] = tree sum of in[r][b*1024 .. b*1024+1024) (zeros past count).
+__global__ void __launch_bounds__(1024) k_sum_f64(const double* in, uint32_t count, double* out,
+                                                  uint32_t out_count)
+{
+    __shared__ double s_w[16];
+    const uint32_t r = blockIdx.y, b = blockIdx.x;
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    const uint32_t e = b * 1024 + threadIdx.x;
+    const double x = e < count ? in[(uint64_t)r * count + e] : 0.0;
+    const double w = butterfly_sum(x, 64);
+    if (lane == 0) s_w[wv] = w;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        double t[16];
+        for (int i = 0; i < 16; ++i) t[i] = s_w[i];
+        for (int width = 16; width > 1; width >>= 1)
+            for (int i = 0; i < width / 2; ++i) t[i] = t[2 * i] + t[2 * i + 1];
+        out[(uint64_t)r * out_count + b] = t[0];
+    }
+}
+
+__global__ void k_scale(const double* norm2, float* scale, uint32_t P)
+{
+    const uint32_t r = blockIdx.x * blockDim.x + threadIdx.x;
+    if (r < P) scale[r] = (float)sqrt(norm2[r]);
+}
+
+// Philox4x32-10 (Salmon et al., SC'11): ten rounds of two 32x32->64
+// multiplies with the high halves mixed into the other words and the key,
+// the key advanced by the Weyl constants between rounds.
+__device__ __forceinline__ uint4 philox(uint4 c, uint32_t k0, uint32_t k1)
+{
+#pragma unroll
+    for (int i = 0; i < 10; ++i) {
+        if (i) {
+            k0 += 0x9E3779B9u;
+            k1 += 0xBB67AE85u;
+        }
+        const uint32_t lo0 = 0xD2511F53u * c.x, hi0 = __umulhi(0xD2511F53u, c.x);
+        const uint32_t lo1 = 0xCD9E8D57u * c.z, hi1 = __umulhi(0xCD9E8D57u, c.z);
+        c = make_uint4(hi1 ^ c.y ^ k0, lo1, hi0 ^ c.w ^ k1, lo0);
+    }
+    return c;
+}
+
+// Each thread quantizes 32/bits consecutive elements into one 32-bit word
+// of codes (4 elements per Philox block).
+template <int BITS>
+__global__ void __launch_bounds__(256) k_quantize(const QDesc* tab, const float* scales, uint32_t k0,
+                                                  uint32_t k1)
+{
+    constexpr int EPT = 32 / BITS;
+    constexpr uint32_t S = (1u << (BITS - 1)) - 1u;
+    const uint32_t r = blockIdx.y;
+    const QDesc d = tab[r];
+    const uint64_t e0 = ((uint64_t)blockIdx.x * 256 + threadIdx.x) * EPT;
+    if (e0 >= d.n) return;
+    const float scale = scales[r];
+    const float inv = scale > 0.0f ? __fdiv_rn((float)S, scale) : 0.0f;
+    const float unit = __fdiv_rn(scale, (float)S);
+    float x[EPT];
+    const bool full = e0 + EPT <= d.n;
+    if (full && ((reinterpret_cast<uintptr_t>(d.val + e0) & 15u) == 0)) {
+#pragma unroll
+        for (int i = 0; i < EPT; i += 4) {
+            const float4 t = *reinterpret_cast<const float4*>(d.val + e0 + i);
+            x[i] = t.x;
+            x[i + 1] = t.y;
+            x[i + 2] = t.z;
+            x[i + 3] = t.w;
+        }
+    } else {
+#pragma unroll
+        for (int i = 0; i < EPT; ++i) x[i] = e0 + i < d.n ? d.val[e0 + i] : 0.0f;
+    }
+    uint32_t word = 0;
+#pragma unroll
+    for (int g = 0; g < EPT; g += 4) {
+        const uint64_t blk = (e0 + g) >> 2;
+        const uint4 w4 = philox(make_uint4((uint32_t)blk, r, 0u, 0u), k0, k1);
+        const uint32_t wr[4] = {w4.x, w4.y, w4.z, w4.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int ii = g + i;
+            uint32_t l = 0;
+            if (scale > 0.0f) {
+                const float a = __fmul_rn(fabsf(x[ii]), inv);
+                l = (uint32_t)a;
+                const float f = __fsub_rn(a, (float)l);
+                const float u = (float)(wr[i] >> 8) * 0x1p-24f;
+                l += u < f ? 1u : 0u;
+                l = l > S ? S : l;
+            }
+            const uint32_t sign = (x[ii] < 0.0f && l > 0u) ? 1u : 0u;
+            const uint32_t code = (sign << (BITS - 1)) | l;
+            word |= code << (ii * BITS);
+            if (d.deq && e0 + ii < d.n) {
+                const float mag = __fmul_rn((float)l, unit);
+                d.deq[e0 + ii] = l == 0u ? 0.0f : (sign ? -mag : mag);
+            }
+        }
+    }
+    const uint64_t byte0 = e0 * BITS / 8;
+    const uint64_t nbytes = (d.n * BITS + 7) / 8;
+    if (byte0 + 4 <= nbytes && ((reinterpret_cast<uintptr_t>(d.q + byte0) & 3u) == 0)) {
+        *reinterpret_cast<uint32_t*>(d.q + byte0) = word;
+    } else {
+        for (int i = 0; i < 4; ++i)
+            if (byte0 + i < nbytes) d.q[byte0 + i] = (uint8_t)(word >> (8 * i));
+    }
+}
+
+struct QLayout {
+    QDesc* tab;
+    double* part[4];
+    uint32_t count[4];
+    int levels;
+    double* norm2;
+    size_t bytes;
+};
+
+QLayout qlayout(int P, uint64_t max_n, void* ws)
+{
+    Carve c(ws);
+    QLayout l{};
+    l.tab = c.take<QDesc>(P);
+    uint64_t cnt = std::max<uint64_t>(1, (max_n + kSeg - 1) / kSeg);
+    l.levels = 0;
+    l.count[0] = (uint32_t)cnt;
+    l.part[0] = c.take<double>((size_t)P * cnt);
+    while (cnt > 1) {
+        cnt = (cnt + 1023) / 1024;
+        ++l.levels;
+        l.count[l.levels] = (uint32_t)cnt;
+        l.part[l.levels] = c.take<double>((size_t)P * cnt);
+    }
+    l.norm2 = l.part[l.levels];
+    l.bytes = align_up(c.used, 256);
+    return l;
+}
+
+}  // namespace
+
+size_t quant_workspace(int P, uint64_t max_n) { return qlayout(P, max_n, nullptr).bytes; }
+
+hipError_t quant_run(int P, const float* const* vals, const uint64_t* n, int bits, uint64_t seed,
+                     uint8_t* const* out_q, float* out_scale, float* const* out_deq, void* ws,
+                     hipStream_t s)
+{
+    uint64_t max_n = 0;
+    for (int r = 0; r < P; ++r) max_n = std::max(max_n, n[r]);
+    const QLayout l = qlayout(P, max_n, ws);
+    QDesc* host = new QDesc[P];
+    for (int r = 0; r < P; ++r)
+        host[r] = QDesc{vals[r], out_q[r], out_deq ? out_deq[r] : nullptr, n[r]};
+    hipError_t e = upload(l.tab, host, sizeof(QDesc) * P, s);
+    delete[] host;
+    if (e != hipSuccess) return e;
+
+    hipLaunchKernelGGL(k_sumsq_partial, dim3(l.count[0], P), dim3(256), 0, s, l.tab, l.part[0],
+                       l.count[0]);
+    for (int lv = 1; lv <= l.levels; ++lv)
+        hipLaunchKernelGGL(k_sum_f64, dim3(l.count[lv], P), dim3(1024), 0, s, l.part[lv - 1],
+                           l.count[lv - 1], l.part[lv], l.count[lv]);
+    hipLaunchKernelGGL(k_scale, dim3((P + 255) / 256), dim3(256), 0, s, l.norm2, out_scale,
+                       (uint32_t)P);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if (max_n == 0) return hipSuccess;
+    const uint32_t k0 = (uint32_t)(seed & 0xFFFFFFFFu), k1 = (uint32_t)(seed >> 32);
+    const uint64_t per_block = 256ull * (32 / bits);
+    const dim3 grid((uint32_t)((max_n + per_block - 1) / per_block), P);
+    if (bits == 2) hipLaunchKernelGGL(k_quantize<2>, grid, dim3(256), 0, s, l.tab, out_scale, k0, k1);
+    else if (bits == 4) hipLaunchKernelGGL(k_quantize<4>, grid, dim3(256), 0, s, l.tab, out_scale, k0, k1);
+    else hipLaunchKernelGGL(k_quantize<8>, grid, dim3(256), 0, s, l.tab, out_scale, k0, k1);
+    return hipGetLastError();
+}
+
+}  // namespace sparcml

@@ -1,0 +1,253 @@
+"""Python binding of libsparcml.so (the gfx950 SparCML C ABI, include/sparcml.h).
+
+Argument marshalling only: torch tensors supply device memory and the
+current HIP stream; every step of the computation runs in the library's HIP
+kernels.  There is no fallback path -- if the library is missing or the
+device is not usable, calls raise.
+
+Index tensors are int32 holding the uint32 bit patterns of the ABI.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "_lib", "libsparcml.so")
+
+OK, EINVAL, ECAPACITY, EWORKSPACE, EUNSORTED, EHIP = 0, -1, -2, -3, -4, -5
+OP_TOPK, OP_QUANTIZE, OP_REDUCE, OP_DENSIFY = 1, 2, 3, 4
+
+
+class Stream(ctypes.Structure):
+    """Mirror of ``sparcml_stream``."""
+    _fields_ = [
+        ("idx", ctypes.c_void_p),
+        ("val", ctypes.c_void_p),
+        ("qval", ctypes.c_void_p),
+        ("qscale", ctypes.c_void_p),
+        ("nnz", ctypes.c_uint64),
+        ("is_dense", ctypes.c_uint32),
+        ("qbits", ctypes.c_uint32),
+    ]
+
+
+class SparcmlError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {strerror(status)} ({status}): {last_error()}")
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load libsparcml.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(
+            f"{LIB_PATH} is missing: build it with `python -m paper_1802_08021_amd.build` "
+            "(there is no CPU fallback)")
+    L = ctypes.CDLL(LIB_PATH)
+    vp, u64, i32 = ctypes.c_void_p, ctypes.c_uint64, ctypes.c_int
+    L.sparcml_workspace_size.argtypes = [i32, i32, u64, u64, ctypes.c_double, ctypes.POINTER(ctypes.c_size_t)]
+    L.sparcml_workspace_size.restype = i32
+    L.sparcml_topk_sparsify.argtypes = [i32, vp, u64, u64, vp, vp, vp, vp, ctypes.c_size_t, vp]
+    L.sparcml_topk_sparsify.restype = i32
+    L.sparcml_quantize.argtypes = [i32, ctypes.POINTER(Stream), i32, u64, vp, vp, vp, vp,
+                                   ctypes.c_size_t, vp]
+    L.sparcml_quantize.restype = i32
+    L.sparcml_sparse_reduce.argtypes = [i32, ctypes.POINTER(Stream), u64, ctypes.c_double,
+                                        ctypes.POINTER(Stream), vp, vp, vp, ctypes.c_size_t, vp]
+    L.sparcml_sparse_reduce.restype = i32
+    L.sparcml_densify.argtypes = [ctypes.POINTER(Stream), u64, vp, vp]
+    L.sparcml_densify.restype = i32
+    L.sparcml_strerror.argtypes = [i32]
+    L.sparcml_strerror.restype = ctypes.c_char_p
+    L.sparcml_last_error.argtypes = []
+    L.sparcml_last_error.restype = ctypes.c_char_p
+    _lib = L
+    return L
+
+
+def strerror(status: int) -> str:
+    return lib().sparcml_strerror(status).decode()
+
+
+def last_error() -> str:
+    return lib().sparcml_last_error().decode()
+
+
+def _check(rc: int, where: str) -> None:
+    if rc != OK:
+        raise SparcmlError(rc, where)
+
+
+def workspace_size(op: int, P: int, N: int, max_nnz: int, delta: float = 1.0) -> int:
+    n = ctypes.c_size_t(0)
+    _check(lib().sparcml_workspace_size(op, P, N, max_nnz, float(delta), ctypes.byref(n)),
+           "sparcml_workspace_size")
+    return int(n.value)
+
+
+# ---------------------------------------------------------------------------
+# torch-facing helpers (device memory and streams only)
+
+def _torch():
+    import torch
+    return torch
+
+
+def _stream_ptr(device) -> int:
+    torch = _torch()
+    return int(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _ptr(t) -> int:
+    return int(t.data_ptr()) if t is not None and t.numel() else 0
+
+
+def _require_cuda(t, name: str):
+    torch = _torch()
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise ValueError(f"{name} must be a CUDA (HIP) tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def alloc_workspace(nbytes: int, device):
+    torch = _torch()
+    return torch.empty(max(nbytes, 1), dtype=torch.uint8, device=device)
+
+
+def topk_sparsify(x, k: int, residual=None, ws=None):
+    """Per-row top-k by magnitude of x[P, N] (fp32).  residual: None, "inplace"
+    (x itself becomes the residual) or a [P, N] fp32 tensor.
+    Returns (idx int32 [P, k], val fp32 [P, k])."""
+    torch = _torch()
+    _require_cuda(x, "x")
+    if x.dtype != torch.float32 or x.dim() != 2:
+        raise ValueError("x must be a 2-D float32 tensor")
+    P, N = x.shape
+    idx = torch.empty((P, max(k, 1)), dtype=torch.int32, device=x.device)
+    val = torch.empty((P, max(k, 1)), dtype=torch.float32, device=x.device)
+    res_ptr = 0
+    if isinstance(residual, str):
+        if residual != "inplace":
+            raise ValueError("residual must be None, 'inplace' or a tensor")
+        res_ptr = _ptr(x)
+    elif residual is not None:
+        _require_cuda(residual, "residual")
+        res_ptr = _ptr(residual)
+    nbytes = workspace_size(OP_TOPK, P, N, k)
+    if ws is None or ws.numel() < nbytes:
+        ws = alloc_workspace(nbytes, x.device)
+    _check(lib().sparcml_topk_sparsify(P, _ptr(x), N, k, _ptr(idx), _ptr(val), res_ptr,
+                                        _ptr(ws), ws.numel(), _stream_ptr(x.device)),
+           "sparcml_topk_sparsify")
+    return idx[:, :k], val[:, :k]
+
+
+def quantize(vals, bits: int, seed: int, want_deq: bool = False, ws=None):
+    """QSGD of each fp32 tensor in ``vals``.  Returns (codes list of uint8
+    tensors, scales fp32 [P], dequantized list or None)."""
+    torch = _torch()
+    P = len(vals)
+    dev = vals[0].device
+    per = 8 // bits
+    arr = (Stream * P)()
+    codes, deqs = [], []
+    for r, v in enumerate(vals):
+        _require_cuda(v, f"vals[{r}]")
+        n = v.numel()
+        arr[r] = Stream(None, _ptr(v), None, None, n, 0, 0)
+        codes.append(torch.empty(max((n + per - 1) // per, 1), dtype=torch.uint8, device=dev))
+        if want_deq:
+            deqs.append(torch.empty(max(n, 1), dtype=torch.float32, device=dev))
+    qptr = (ctypes.c_void_p * P)(*[_ptr(c) for c in codes])
+    dptr = (ctypes.c_void_p * P)(*[_ptr(d) for d in deqs]) if want_deq else None
+    scale = torch.empty(P, dtype=torch.float32, device=dev)
+    nbytes = workspace_size(OP_QUANTIZE, P, 1, max(v.numel() for v in vals))
+    if ws is None or ws.numel() < nbytes:
+        ws = alloc_workspace(nbytes, dev)
+    _check(lib().sparcml_quantize(P, arr, bits, seed & (2**64 - 1), ctypes.cast(qptr, ctypes.c_void_p),
+                                  _ptr(scale), ctypes.cast(dptr, ctypes.c_void_p) if dptr else None,
+                                  _ptr(ws), ws.numel(), _stream_ptr(dev)),
+           "sparcml_quantize")
+    nb = [(v.numel() + per - 1) // per for v in vals]
+    return ([c[:m] for c, m in zip(codes, nb)], scale,
+            [d[: v.numel()] for d, v in zip(deqs, vals)] if want_deq else None)
+
+
+def make_streams(idx, vals=None, codes=None, scales=None, qbits: int = 0):
+    """Descriptor array for P sparse streams (fp32 values or QSGD codes)."""
+    P = len(idx)
+    arr = (Stream * P)()
+    for r in range(P):
+        _require_cuda(idx[r], f"idx[{r}]")
+        n = idx[r].numel()
+        if qbits:
+            arr[r] = Stream(_ptr(idx[r]), None, _ptr(codes[r]), int(scales[r].data_ptr()), n, 0, qbits)
+        else:
+            arr[r] = Stream(_ptr(idx[r]), _ptr(vals[r]), None, None, n, 0, 0)
+    return arr
+
+
+def sparse_reduce(idx, vals, N: int, delta: float, codes=None, scales=None, qbits: int = 0,
+                  node_info: bool = False, ws=None, out_idx=None, out_val=None):
+    """Sum of P sparse streams in recursive-doubling order with the dense
+    switch.  ``scales`` is a device fp32 tensor [P] (one scale per stream)
+    when ``qbits`` != 0.  Returns dict(idx, val, nnz, dense, node_nnz,
+    node_dense); ``idx`` is None for a dense root."""
+    torch = _torch()
+    P = len(idx)
+    dev = idx[0].device
+    if qbits:
+        scale_views = [scales[r: r + 1] for r in range(P)]
+        arr = make_streams(idx, codes=codes, scales=scale_views, qbits=qbits)
+    else:
+        arr = make_streams(idx, vals)
+    nnz = [t.numel() for t in idx]
+    thr = int(float(delta) * float(N) // 1)
+    cap = max(1, min(thr, sum(nnz)) if P > 1 else max(nnz[0], 1))
+    if out_idx is None:
+        out_idx = torch.empty(cap, dtype=torch.int32, device=dev)
+    if out_val is None:
+        out_val = torch.empty(N, dtype=torch.float32, device=dev)
+    out = Stream(_ptr(out_idx), _ptr(out_val), None, None, out_idx.numel(), 0, 0)
+    node_nnz = node_dense = None
+    if node_info and P > 1:
+        node_nnz = torch.empty(P - 1, dtype=torch.int64, device=dev)
+        node_dense = torch.empty(P - 1, dtype=torch.uint8, device=dev)
+    nbytes = workspace_size(OP_REDUCE, P, N, max(nnz), delta)
+    if ws is None or ws.numel() < nbytes:
+        ws = alloc_workspace(nbytes, dev)
+    _check(lib().sparcml_sparse_reduce(P, arr, N, float(delta), ctypes.byref(out),
+                                       _ptr(node_nnz), _ptr(node_dense), _ptr(ws), ws.numel(),
+                                       _stream_ptr(dev)),
+           "sparcml_sparse_reduce")
+    n = int(out.nnz)
+    dense = bool(out.is_dense)
+    return {
+        "idx": None if dense else out_idx[:n],
+        "val": out_val if dense else out_val[:n],
+        "nnz": n,
+        "dense": dense,
+        "node_nnz": node_nnz,
+        "node_dense": node_dense,
+    }
+
+
+def densify(idx, val, N: int, codes=None, scale=None, qbits: int = 0):
+    """Dense fp32[N] of one sparse stream (values or QSGD codes)."""
+    torch = _torch()
+    dev = idx.device
+    if qbits:
+        s = Stream(_ptr(idx), None, _ptr(codes), int(scale.data_ptr()), idx.numel(), 0, qbits)
+    else:
+        s = Stream(_ptr(idx), _ptr(val), None, None, idx.numel(), 0, 0)
+    out = torch.empty(N, dtype=torch.float32, device=dev)
+    _check(lib().sparcml_densify(ctypes.byref(s), N, _ptr(out), _stream_ptr(dev)), "sparcml_densify")
+    return out

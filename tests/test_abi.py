@@ -1,0 +1,167 @@
+"""C-ABI checks that need no GPU: the library loads, exports every entry
+point include/sparcml.h declares, and rejects bad arguments on the host
+before any device work (so these calls never reach the HIP runtime)."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+from paper_1802_08021_amd import sparcml as S
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "sparcml.h")
+
+
+def declared_symbols():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"SPARCML_API\s+[\w\s\*]+?\b(sparcml_\w+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    syms = declared_symbols()
+    for name in ("sparcml_topk_sparsify", "sparcml_quantize", "sparcml_sparse_reduce",
+                 "sparcml_densify", "sparcml_workspace_size", "sparcml_strerror",
+                 "sparcml_last_error"):
+        assert name in syms
+
+
+def test_library_exports_every_declared_symbol():
+    L = S.lib()
+    for name in declared_symbols():
+        assert hasattr(L, name), name
+    out = subprocess.run(["nm", "-D", "--defined-only", S.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(re.findall(r"\b[TW]\s+(\S+)$", out, flags=re.M))
+    assert set(declared_symbols()) <= exported
+    # nothing but the ABI is exported from the library's own code
+    assert all(e.startswith("sparcml_") for e in exported if "sparcml" in e)
+
+
+def test_strerror_codes():
+    assert S.strerror(0) == "success"
+    for code in (S.EINVAL, S.ECAPACITY, S.EWORKSPACE, S.EUNSORTED, S.EHIP):
+        assert S.strerror(code) and S.strerror(code) != "unknown status"
+    assert S.strerror(-99) == "unknown status"
+
+
+def ws_size(op, P, N, max_nnz, delta=1.0):
+    n = ctypes.c_size_t(0)
+    rc = S.lib().sparcml_workspace_size(op, P, N, max_nnz, delta, ctypes.byref(n))
+    return rc, n.value
+
+
+def test_workspace_size_queries():
+    rc, n = ws_size(S.OP_REDUCE, 128, 2**27, 2**27 // 100, 0.1)
+    assert rc == 0 and n > 0
+    rc2, n2 = ws_size(S.OP_REDUCE, 128, 2**27, 2**27 // 10, 0.1)
+    assert rc2 == 0 and n2 >= n  # larger max_nnz never needs less
+    assert ws_size(S.OP_REDUCE, 3, 100, 10)[0] == S.EINVAL
+    assert ws_size(S.OP_REDUCE, 512, 100, 10)[0] == S.EINVAL
+    assert ws_size(S.OP_REDUCE, 4, 0, 0)[0] == S.EINVAL
+    assert ws_size(S.OP_REDUCE, 4, 2**32, 1)[0] == S.EINVAL
+    assert ws_size(S.OP_REDUCE, 4, 100, 10, 0.0)[0] == S.EINVAL
+    assert ws_size(S.OP_TOPK, 32, 2**24, 2**24 // 1000)[0] == 0
+    assert ws_size(S.OP_TOPK, 1, 10, 11)[0] == S.EINVAL
+    assert ws_size(S.OP_QUANTIZE, 128, 1, 2**20)[0] == 0
+    assert ws_size(S.OP_DENSIFY, 1, 10, 0)[0] == 0
+    assert ws_size(99, 1, 10, 0)[0] == S.EINVAL
+    assert S.lib().sparcml_workspace_size(S.OP_DENSIFY, 1, 10, 0, 1.0, None) == S.EINVAL
+
+
+FAKE = 0x1000  # never dereferenced: every call below fails validation first
+
+
+def streams(P, nnz=4, qbits=0, dense=0):
+    arr = (S.Stream * P)()
+    for r in range(P):
+        arr[r] = S.Stream(FAKE, FAKE, FAKE if qbits else None, FAKE if qbits else None,
+                          nnz, dense, qbits)
+    return arr
+
+
+def reduce_rc(P, arr, N=100, delta=0.5, out=None, ws=FAKE, ws_bytes=1 << 40):
+    if out is None:
+        out = S.Stream(FAKE, FAKE, None, None, 1 << 30, 0, 0)
+    return S.lib().sparcml_sparse_reduce(P, arr, N, delta, ctypes.byref(out), None, None,
+                                         ws, ws_bytes, None)
+
+
+def test_reduce_argument_errors():
+    assert reduce_rc(3, streams(3)) == S.EINVAL          # P not a power of two
+    assert reduce_rc(0, streams(1)) == S.EINVAL
+    assert reduce_rc(512, streams(512)) == S.EINVAL      # beyond the supported P
+    assert reduce_rc(4, streams(4), N=0) == S.EINVAL
+    assert reduce_rc(4, streams(4), N=2**32) == S.EINVAL
+    assert reduce_rc(4, streams(4), delta=0.0) == S.EINVAL
+    assert reduce_rc(4, streams(4), delta=float("nan")) == S.EINVAL
+    assert reduce_rc(4, streams(4, nnz=101)) == S.EINVAL  # nnz > N
+    assert reduce_rc(4, streams(4, dense=1)) == S.EINVAL  # leaves must be sparse
+    mixed = streams(4)
+    mixed[2] = S.Stream(FAKE, None, FAKE, FAKE, 4, 0, 4)
+    assert reduce_rc(4, mixed) == S.EINVAL                # mixed qbits
+    assert reduce_rc(4, streams(4, qbits=3)) == S.EINVAL
+    noscale = streams(4, qbits=4)
+    noscale[1] = S.Stream(FAKE, None, FAKE, None, 4, 0, 4)
+    assert reduce_rc(4, noscale) == S.EINVAL
+    nullidx = streams(4)
+    nullidx[0] = S.Stream(None, FAKE, None, None, 4, 0, 0)
+    assert reduce_rc(4, nullidx) == S.EINVAL
+    assert S.lib().sparcml_sparse_reduce(4, None, 100, 0.5, None, None, None, FAKE, 1, None) == S.EINVAL
+    out = S.Stream(FAKE, None, None, None, 100, 0, 0)
+    assert reduce_rc(4, streams(4), out=out) == S.EINVAL  # out->val NULL
+    assert "val" in S.last_error()
+
+
+def test_reduce_capacity_and_workspace_errors():
+    # sum nnz = 16, thr = 50: capacity must be >= 16
+    small = S.Stream(FAKE, FAKE, None, None, 15, 0, 0)
+    assert reduce_rc(4, streams(4), out=small) == S.ECAPACITY
+    # P == 1 sparse copy needs nnz_0 entries
+    assert reduce_rc(1, streams(1, nnz=10), out=S.Stream(FAKE, FAKE, None, None, 9, 0, 0)) == S.ECAPACITY
+    assert reduce_rc(4, streams(4), ws=None, ws_bytes=0) == S.EWORKSPACE
+    assert reduce_rc(4, streams(4), ws_bytes=16) == S.EWORKSPACE
+
+
+def test_topk_argument_errors():
+    L = S.lib()
+    assert L.sparcml_topk_sparsify(0, FAKE, 10, 1, FAKE, FAKE, None, FAKE, 1 << 30, None) == S.EINVAL
+    assert L.sparcml_topk_sparsify(1, FAKE, 10, 11, FAKE, FAKE, None, FAKE, 1 << 30, None) == S.EINVAL
+    assert L.sparcml_topk_sparsify(1, None, 10, 1, FAKE, FAKE, None, FAKE, 1 << 30, None) == S.EINVAL
+    assert L.sparcml_topk_sparsify(1, FAKE, 10, 1, None, FAKE, None, FAKE, 1 << 30, None) == S.EINVAL
+    assert L.sparcml_topk_sparsify(1, FAKE, 0, 0, FAKE, FAKE, None, FAKE, 1 << 30, None) == S.EINVAL
+    assert L.sparcml_topk_sparsify(2, FAKE, 1000, 10, FAKE, FAKE, None, FAKE, 8, None) == S.EWORKSPACE
+
+
+def test_quantize_argument_errors():
+    L = S.lib()
+    q = (ctypes.c_void_p * 4)(*([FAKE] * 4))
+    arr = streams(4)
+    assert L.sparcml_quantize(4, arr, 3, 1, ctypes.cast(q, ctypes.c_void_p), FAKE, None, FAKE, 1 << 30, None) == S.EINVAL
+    assert L.sparcml_quantize(0, arr, 4, 1, ctypes.cast(q, ctypes.c_void_p), FAKE, None, FAKE, 1 << 30, None) == S.EINVAL
+    assert L.sparcml_quantize(4, arr, 4, 1, None, FAKE, None, FAKE, 1 << 30, None) == S.EINVAL
+    assert L.sparcml_quantize(4, arr, 4, 1, ctypes.cast(q, ctypes.c_void_p), None, None, FAKE, 1 << 30, None) == S.EINVAL
+    assert L.sparcml_quantize(4, streams(4, qbits=4), 4, 1, ctypes.cast(q, ctypes.c_void_p), FAKE, None, FAKE, 1 << 30, None) == S.EINVAL
+    assert L.sparcml_quantize(4, arr, 4, 1, ctypes.cast(q, ctypes.c_void_p), FAKE, None, FAKE, 8, None) == S.EWORKSPACE
+
+
+def test_densify_argument_errors():
+    L = S.lib()
+    s = S.Stream(FAKE, FAKE, None, None, 4, 0, 0)
+    assert L.sparcml_densify(None, 10, FAKE, None) == S.EINVAL
+    assert L.sparcml_densify(ctypes.byref(s), 10, None, None) == S.EINVAL
+    assert L.sparcml_densify(ctypes.byref(s), 0, FAKE, None) == S.EINVAL
+    big = S.Stream(FAKE, FAKE, None, None, 11, 0, 0)
+    assert L.sparcml_densify(ctypes.byref(big), 10, FAKE, None) == S.EINVAL
+    q = S.Stream(FAKE, None, FAKE, None, 4, 0, 4)
+    assert L.sparcml_densify(ctypes.byref(q), 10, FAKE, None) == S.EINVAL
+    q3 = S.Stream(FAKE, None, FAKE, FAKE, 4, 0, 3)
+    assert L.sparcml_densify(ctypes.byref(q3), 10, FAKE, None) == S.EINVAL
+
+
+def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
+    monkeypatch.setattr(S, "LIB_PATH", str(tmp_path / "missing.so"))
+    monkeypatch.setattr(S, "_lib", None)
+    with pytest.raises(RuntimeError, match="no CPU fallback"):
+        S.lib()

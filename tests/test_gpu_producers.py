@@ -1,0 +1,134 @@
+"""Parity of the HIP producers (top-k, QSGD) and densify with the oracle.
+
+Top-k: selected indices bit-exact (ties lowest index first), values and
+residual bitwise.  QSGD: packed codes and scales bit-exact, dequantized
+values bitwise (same Philox stream on both sides).  Densify: bitwise."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_1802_08021_amd import inputs
+from gpu_util import say, to_dev, to_np, torch_dev
+
+pytestmark = pytest.mark.gpu
+
+
+def gpu_topk(x, k, residual=None):
+    from paper_1802_08021_amd import sparcml as S
+    torch, dev = torch_dev()
+    tx = to_dev(x)
+    res = None
+    if residual == "copy":
+        res = torch.empty_like(tx)
+    elif residual == "inplace":
+        res = "inplace"
+    i, v = S.topk_sparsify(tx, k, residual=res)
+    torch.cuda.synchronize()
+    out_res = None
+    if residual == "copy":
+        out_res = to_np(res)
+    elif residual == "inplace":
+        out_res = to_np(tx)
+    return to_np(i, np.uint32), to_np(v), out_res
+
+
+@pytest.mark.parametrize("residual", [None, "copy", "inplace"])
+def test_topk_random(residual):
+    rng = np.random.default_rng(20)
+    for case in range(12):
+        P = int(rng.integers(1, 9))
+        N = int(rng.choice([1, 5, 1000, 4097, 70001, 300000]))
+        k = int(rng.choice([0, 1, N // 1000, N // 10, N]))
+        k = min(k, N)
+        x = np.stack([inputs.laplace(rng, 1e-3, N) for _ in range(P)])
+        if case % 3 == 1:
+            x[:, ::5] = np.float32(-0.25)  # ties with sign differences
+            x[:, 1::5] = np.float32(0.25)
+        if case % 4 == 2:
+            x[:, ::2] = 0.0
+        say(f"[topk] case {case} P={P} N={N} k={k} residual={residual}")
+        oi, ov, orr = oracle.topk(x, k, residual=residual is not None)
+        gi, gv, gr = gpu_topk(x, k, residual)
+        np.testing.assert_array_equal(gi, oi)
+        np.testing.assert_array_equal(gv.view(np.uint32), ov.view(np.uint32))
+        if residual is not None:
+            np.testing.assert_array_equal(gr.view(np.uint32), orr.view(np.uint32))
+
+
+def test_topk_all_equal_and_config3_scaled():
+    x = np.full((3, 9000), 1.5, np.float32)
+    x[1, ::2] = -1.5
+    say("[topk] all equal magnitudes")
+    oi, ov, _ = oracle.topk(x, 1234)
+    gi, gv, _ = gpu_topk(x, 1234)
+    np.testing.assert_array_equal(gi, oi)
+    np.testing.assert_array_equal(gv, ov)
+    c = inputs.config(3, scale_log2=4)
+    d = inputs.generate(c, seed=0)
+    say(f"[topk] c3/16: P={c.P} N={c.N} k={c.k}")
+    oi, ov, orr = oracle.topk(d["x"], c.k, residual=True)
+    gi, gv, gr = gpu_topk(d["x"], c.k, "copy")
+    np.testing.assert_array_equal(gi, oi)
+    np.testing.assert_array_equal(gv.view(np.uint32), ov.view(np.uint32))
+    np.testing.assert_array_equal(gr.view(np.uint32), orr.view(np.uint32))
+
+
+def gpu_quantize(vals, bits, seed):
+    from paper_1802_08021_amd import sparcml as S
+    torch, dev = torch_dev()
+    tv = [to_dev(v if v.size else np.zeros(0, np.float32)) for v in vals]
+    codes, scale, deq = S.quantize(tv, bits, seed, want_deq=True)
+    torch.cuda.synchronize()
+    return [to_np(c) for c in codes], to_np(scale), [to_np(d) for d in deq]
+
+
+@pytest.mark.parametrize("bits", [2, 4, 8])
+def test_quantize_parity(bits):
+    rng = np.random.default_rng(30 + bits)
+    sizes = [0, 1, 2, 3, 4, 5, 7, 8, 9, 63, 64, 65, 1000, 8191, 8192, 8193, 100003, 1 << 20]
+    vals = [inputs.laplace(rng, 1e-3, n) for n in sizes]
+    vals.append(np.zeros(77, np.float32))
+    vals.append(np.float32(3.0) * np.ones(5, np.float32))
+    seed = 0xDEADBEEF_12345678 + bits
+    say(f"[quant] bits={bits} streams={len(vals)}")
+    oq, os_, od = oracle.quantize(vals, bits, seed)
+    gq, gs, gd = gpu_quantize(vals, bits, seed)
+    np.testing.assert_array_equal(gs.view(np.uint32), os_.view(np.uint32))
+    for r in range(len(vals)):
+        np.testing.assert_array_equal(gq[r], oq[r], err_msg=f"codes of stream {r}")
+        np.testing.assert_array_equal(gd[r].view(np.uint32), od[r].view(np.uint32),
+                                      err_msg=f"dequantized stream {r}")
+
+
+def test_quantize_config5_scaled():
+    c = inputs.config(5, scale_log2=5)
+    d = inputs.generate(c, seed=0)
+    seed = inputs.quant_seed(0, 5)
+    say(f"[quant] c5/32 P={c.P} k={c.k}")
+    oq, os_, od = oracle.quantize(d["val"], 4, seed)
+    gq, gs, gd = gpu_quantize(d["val"], 4, seed)
+    np.testing.assert_array_equal(gs.view(np.uint32), os_.view(np.uint32))
+    for r in range(c.P):
+        np.testing.assert_array_equal(gq[r], oq[r])
+        np.testing.assert_array_equal(gd[r].view(np.uint32), od[r].view(np.uint32))
+
+
+def test_densify_parity():
+    from paper_1802_08021_amd import sparcml as S
+    torch, dev = torch_dev()
+    rng = np.random.default_rng(40)
+    for N in (1, 100, 4096, 4097, 123457):
+        for k in (0, 1, N // 7, N):
+            idx = inputs.uniform_subset(rng, N, k)
+            val = inputs.normal(rng, k)
+            say(f"[densify] N={N} k={k}")
+            want = oracle.densify(idx, val, N)
+            got = S.densify(to_dev(idx), to_dev(val), N)
+            torch.cuda.synchronize()
+            np.testing.assert_array_equal(to_np(got).view(np.uint32), want.view(np.uint32))
+            if k:
+                q, sc, deq = oracle.quantize([val], 4, seed=5)
+                want_q = oracle.densify(idx, deq[0], N)
+                got_q = S.densify(to_dev(idx), None, N, codes=to_dev(q[0]), scale=to_dev(sc), qbits=4)
+                torch.cuda.synchronize()
+                np.testing.assert_array_equal(to_np(got_q).view(np.uint32), want_q.view(np.uint32))

@@ -1,0 +1,153 @@
+"""Parity of the HIP sparse reduce (through the C ABI) with the CPU oracle.
+
+Bit-exact: root representation, nnz, indices, per-node switch decisions and
+union sizes.  Values: within 1e-6 rel / 1e-7 abs, and bitwise (the kernels
+use the oracle's association).  Sizes span several tiles with a ragged
+tail; edge cases cover empty streams, a single rank, all-dense and
+all-sparse thresholds, overfull tiles (the slow path) and a sparse root
+reached after a dense guess."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_1802_08021_amd import inputs
+from gpu_util import assert_reduce_equal, gpu_reduce, say
+
+pytestmark = pytest.mark.gpu
+
+
+def check(idx, val, N, delta, label):
+    say(f"[reduce] {label}: P={len(idx)} N={N} delta={delta} nnz={sum(a.size for a in idx)}")
+    o = oracle.sparse_reduce(idx, val, N, delta)
+    g = gpu_reduce(idx, val, N, delta)
+    assert_reduce_equal(g, o, label)
+    return g, o
+
+
+def rand_streams(rng, P, N, kmax, dist="normal"):
+    idx, val = [], []
+    for _ in range(P):
+        k = int(rng.integers(0, min(N, kmax) + 1))
+        a = inputs.uniform_subset(rng, N, k)
+        idx.append(a)
+        val.append(inputs.normal(rng, k) if dist == "normal" else inputs.laplace(rng, 1.0, k))
+    return idx, val
+
+
+def test_random_small_cases():
+    rng = np.random.default_rng(100)
+    for case in range(60):
+        P = int(rng.choice([2, 4, 8, 16, 32, 64, 128, 256]))
+        N = int(rng.choice([1, 7, 300, 4999, 20011, 70001]))
+        kmax = int(rng.choice([1, 8, 64, 500, 5000]))
+        delta = float(rng.choice([1e-9, 0.01, 0.1, 0.3, 1.0, 8.0]))
+        idx, val = rand_streams(rng, P, N, kmax)
+        check(idx, val, N, delta, f"random#{case}")
+
+
+@pytest.mark.parametrize("cfg", [1, 2])
+def test_config_full_size_sparse(cfg):
+    c = inputs.config(cfg)
+    d = inputs.generate(c, seed=0)
+    g, o = check(d["idx"], d["val"], c.N, c.delta, c.name)
+    assert not g["dense"]
+
+
+@pytest.mark.parametrize("cfg,scale", [(4, 6), (5, 7)])
+def test_config_scaled_dense_switch(cfg, scale):
+    c = inputs.config(cfg, scale_log2=scale)
+    d = inputs.generate(c, seed=1)
+    g, o = check(d["idx"], d["val"], c.N, c.delta, f"{c.name}/2^{scale}")
+    assert g["dense"]
+    assert (~g["node_dense"].astype(bool)).any()  # lower levels stayed sparse
+
+
+def test_empty_and_single_rank():
+    N = 5000
+    e = np.zeros(0, np.uint32)
+    ev = np.zeros(0, np.float32)
+    check([e] * 8, [ev] * 8, N, 0.5, "all empty")
+    check([e] * 8, [ev] * 8, N, 1e-9, "all empty thr 0")
+    rng = np.random.default_rng(3)
+    idx, val = rand_streams(rng, 8, N, 400)
+    idx[3] = e
+    val[3] = ev
+    check(idx, val, N, 0.5, "one empty")
+    a = inputs.uniform_subset(rng, N, 300)
+    v = inputs.normal(rng, 300)
+    check([a], [v], N, 0.5, "P=1 sparse")
+    check([a], [v], N, 0.01, "P=1 dense")
+
+
+def test_thresholds_extremes_and_boundary():
+    rng = np.random.default_rng(4)
+    idx, val = rand_streams(rng, 16, 30000, 2000)
+    for delta in (1e-9, 1e-4, 0.05, 0.2, 1.0, 1e6):
+        check(idx, val, 30000, delta, f"delta={delta}")
+    # threshold exactly at a level-1 upper bound: nnz_L + nnz_R == thr stays sparse
+    a = inputs.uniform_subset(rng, 1000, 100)
+    b = inputs.uniform_subset(rng, 1000, 100)
+    check([a, b], [inputs.normal(rng, 100), inputs.normal(rng, 100)], 1000, 0.2, "sum == thr")
+    check([a, b], [inputs.normal(rng, 100), inputs.normal(rng, 100)], 1000, 0.199, "sum == thr+1")
+
+
+def test_overfull_tiles_take_the_slow_path():
+    rng = np.random.default_rng(5)
+    N = 40000
+    # dense-ish ranks: > 64 entries of one rank in a tile
+    idx, val = rand_streams(rng, 8, N, N)
+    idx[0] = np.arange(0, N, 2, dtype=np.uint32)
+    val[0] = inputs.normal(rng, idx[0].size)
+    check(idx, val, N, 0.3, "dense-ish ranks")
+    check(idx, val, N, 100.0, "dense-ish ranks, all sparse")
+    # every rank clustered in one region: tile total above the fast-path cap
+    P = 128
+    idx = [np.sort(rng.choice(3000, 60, replace=False)).astype(np.uint32) for _ in range(P)]
+    val = [inputs.normal(rng, 60) for _ in range(P)]
+    check(idx, val, 3000000, 0.5, "clustered, sparse")
+    check(idx, val, 3000000, 1e-6, "clustered, dense")
+    # k = N for every rank
+    idx = [np.arange(2000, dtype=np.uint32)] * 4
+    val = [inputs.normal(rng, 2000) for _ in range(4)]
+    check(idx, val, 2000, 0.5, "k = N")
+    check(idx, val, 2000, 4.0, "k = N, sparse")
+
+
+def test_dense_guess_then_sparse_root():
+    """Sum of nnz above thr makes the kernel write a dense root first; full
+    overlap keeps every node sparse, so the sparse pass must run."""
+    rng = np.random.default_rng(6)
+    N, k, P = 100000, 1000, 16
+    base = inputs.uniform_subset(rng, N, k)
+    idx = [base] * P
+    val = [inputs.normal(rng, k) for _ in range(P)]
+    g, o = check(idx, val, N, 0.03, "overlap")
+    assert not g["dense"] and g["nnz"] == k
+
+
+def test_quantized_inputs_fused_dequant():
+    from gpu_util import to_dev, torch_dev
+    rng = np.random.default_rng(7)
+    for bits in (2, 4, 8):
+        P, N = 32, 50000
+        idx, val = rand_streams(rng, P, N, 3000, dist="laplace")
+        q, scale, deq = oracle.quantize(val, bits, seed=99 + bits)
+        torch, dev = torch_dev()
+        codes = [to_dev(a if a.size else np.zeros(1, np.uint8)) for a in q]
+        scales = to_dev(scale)
+        for delta in (0.02, 5.0):
+            say(f"[reduce] quantized bits={bits} delta={delta}")
+            o = oracle.sparse_reduce(idx, deq, N, delta)
+            g = gpu_reduce(idx, None, N, delta, qbits=bits, codes=codes, scales=scales)
+            assert_reduce_equal(g, o, f"q{bits}")
+
+
+def test_run_twice_is_bitwise_identical():
+    c = inputs.config(4, scale_log2=7)
+    d = inputs.generate(c, seed=2)
+    say("[reduce] determinism")
+    a = gpu_reduce(d["idx"], d["val"], c.N, c.delta)
+    b = gpu_reduce(d["idx"], d["val"], c.N, c.delta)
+    assert a["dense"] == b["dense"]
+    np.testing.assert_array_equal(a["val"].view(np.uint32), b["val"].view(np.uint32))
+    np.testing.assert_array_equal(a["node_nnz"], b["node_nnz"])
