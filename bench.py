@@ -1,0 +1,362 @@
+#!/usr/bin/env python3
+"""Benchmark of the SparCML hot path on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload c5]
+
+A step is one pass of the hot path over one batch of synthetic input held
+in HBM.  The headline workload is c5, the largest configuration: 128 ranks x
+1,342,177 uniform indices of N = 2^27 with Laplace(0, 1e-3) values, QSGD
+4-bit quantization (per-rank L2 scale, Philox) followed by the
+recursive-doubling sparse reduce with fused dequantization and the dense
+switch (delta = 0.1).  value = reduce input nnz per second of step time.
+
+Besides the headline line the JSON carries:
+  roofline      the dominant kernel's algorithmic bytes per launch over its
+                average duration (HIP events on the launch stream, recorded
+                by the library during the timed steps), against 8 TB/s;
+                traffic = measured HBM bytes per launch from rocprofv3
+                FETCH_SIZE/WRITE_SIZE runs (profiles/), or null when the
+                kernel source changed since they were taken;
+  cpu_baseline  the CPU oracle timed on a bounded sample of the workload;
+  per_config    the other configurations (c1..c4; c3 = top-k then reduce).
+
+Only one GPU is used; --gpus above 1 exits with a message.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "sparse-reduce input nnz/s + achieved HBM GB/s (% of MI355X peak)"
+HBM_PEAK_GBS = 8000.0
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "reduce_tiles_c5_traffic.json")
+
+
+def log(msg: str) -> None:
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=20)
+    p.add_argument("--warmup", type=int, default=3)
+    p.add_argument("--workload", default="c5", choices=["c1", "c2", "c3", "c4", "c5"])
+    p.add_argument("--seed", type=int, default=0)
+    p.add_argument("--no-per-config", action="store_true")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--calibrate-copy", action="store_true",
+                   help="only run a plain 1 GiB device copy (3 times): the reference for "
+                        "scaling rocprofv3 FETCH_SIZE / WRITE_SIZE to bytes")
+    return p.parse_args()
+
+
+def calibrate_copy(torch) -> int:
+    x = torch.empty(1 << 28, dtype=torch.float32, device="cuda:0").fill_(1.0)
+    y = torch.empty_like(x)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        y.copy_(x)
+    torch.cuda.synchronize()
+    log("copied 1 GiB three times")
+    return 0
+
+
+def arena(arrays, dtype, torch, dev, align=64):
+    """One device allocation holding every rank's array, each slice starting
+    on a 256-byte boundary; returns (arena, per-rank views)."""
+    offs, tot = [], 0
+    for a in arrays:
+        offs.append(tot)
+        tot += (a.size + align - 1) // align * align
+    host = np.zeros(max(tot, 1), dtype=arrays[0].dtype)
+    for a, o in zip(arrays, offs):
+        host[o: o + a.size] = a
+    dev_arena = torch.from_numpy(host).to(dev)
+    return dev_arena, [dev_arena[o: o + a.size] for a, o in zip(arrays, offs)]
+
+
+def empty_arena(sizes, dtype, torch, dev, align=256):
+    offs, tot = [], 0
+    for n in sizes:
+        offs.append(tot)
+        tot += (max(n, 1) + align - 1) // align * align
+    t = torch.empty(max(tot, 1), dtype=dtype, device=dev)
+    return t, [t[o: o + n] for n, o in zip(sizes, offs)]
+
+
+class Workload:
+    """Device-resident inputs, prepared calls and byte accounting of one config."""
+
+    def __init__(self, name, cfg, seed, torch, dev):
+        from paper_1802_08021_amd import inputs
+        from paper_1802_08021_amd import sparcml as S
+        self.name, self.c = name, cfg
+        c = cfg
+        t0 = time.time()
+        d = inputs.generate(c, seed)
+        log(f"{name}: generated inputs in {time.time() - t0:.1f}s")
+        self.groups = [S.TIMER_REDUCE_PASS, S.TIMER_REDUCE_SLOW, S.TIMER_REDUCE_WRITE]
+        self.kernel_bytes = {}
+        if c.kind == "topk":
+            x = torch.from_numpy(d["x"]).to(dev)
+            del d
+            self.topk = S.TopkCall(x, c.k)
+            idx = [self.topk.idx[r] for r in range(c.P)]
+            vals = [self.topk.val[r] for r in range(c.P)]
+            self.nnz = c.P * c.k
+            self.reduce = S.ReduceCall(idx, c.N, c.delta, vals=vals)
+            self.groups += [S.TIMER_TOPK_SELECT, S.TIMER_TOPK_WRITE]
+            # compulsory bytes: one read of x (selection), x read + k pairs
+            # written (compaction); the passes re-read x, which the roofline
+            # fraction then shows as lost bandwidth
+            self.kernel_bytes[S.TIMER_TOPK_SELECT] = c.P * c.N * 4
+            self.kernel_bytes[S.TIMER_TOPK_WRITE] = c.P * c.N * 4 + c.P * c.k * 8
+            self._steps = [self.topk.run, self.reduce.run]
+        else:
+            self.nnz = sum(a.size for a in d["idx"])
+            _, idx = arena([a.view(np.int32) for a in d["idx"]], None, torch, dev)
+            if c.qbits:
+                _, vals = arena(d["val"], None, torch, dev)
+                per = 8 // c.qbits
+                code_bytes = [(a.size + per - 1) // per for a in d["idx"]]
+                _, codes = empty_arena(code_bytes, torch.uint8, torch, dev)
+                scale = torch.empty(c.P, dtype=torch.float32, device=dev)
+                self.quant = S.QuantizeCall(vals, codes, scale, c.qbits, inputs.quant_seed(seed, c.cfg))
+                self.reduce = S.ReduceCall(idx, c.N, c.delta, codes=codes, scales=scale, qbits=c.qbits)
+                self.groups += [S.TIMER_QUANT_NORM, S.TIMER_QUANT_CODES]
+                cb = sum(code_bytes)
+                self.kernel_bytes[S.TIMER_QUANT_NORM] = self.nnz * 4
+                self.kernel_bytes[S.TIMER_QUANT_CODES] = self.nnz * 4 + cb
+                self.in_bytes = self.nnz * 4 + cb
+                self.quant_bytes = self.nnz * 4 + cb
+                self._steps = [self.quant.run, self.reduce.run]
+            else:
+                _, vals = arena(d["val"], None, torch, dev)
+                self.reduce = S.ReduceCall(idx, c.N, c.delta, vals=vals)
+                self.in_bytes = self.nnz * 8
+                self.quant_bytes = 0
+                self._steps = [self.reduce.run]
+        self.d_host = d if cfg.cfg == 5 else None
+
+    def step(self):
+        out = None
+        for f in self._steps:
+            out = f()
+        return out
+
+    def finish_bytes(self, root_nnz, dense):
+        """Algorithmic bytes once the root representation is known."""
+        from paper_1802_08021_amd import sparcml as S
+        c = self.c
+        out_bytes = c.N * 4 if dense else root_nnz * 8
+        if c.kind == "topk":
+            red_in = self.nnz * 8
+        else:
+            red_in = self.in_bytes
+        # first tile pass: reads the streams; a dense root is written there
+        self.kernel_bytes[S.TIMER_REDUCE_PASS] = red_in + (c.N * 4 if dense else 0)
+        if not dense:
+            self.kernel_bytes[S.TIMER_REDUCE_WRITE] = red_in + out_bytes
+        if c.kind == "topk":
+            self.step_bytes = c.P * c.N * 4 + c.P * c.k * 8 + red_in + out_bytes
+        else:
+            self.step_bytes = self.quant_bytes + red_in + out_bytes
+
+
+def time_steps(w, K, W, torch):
+    from paper_1802_08021_amd import sparcml as S
+    res = None
+    for _ in range(W):
+        res = w.step()
+    torch.cuda.synchronize()
+    S.timing_enable(True)
+    durs = {g: [] for g in w.groups}
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    start.record()
+    for _ in range(K):
+        res = w.step()
+        for g in w.groups:
+            v = S.timing_read(g)
+            if v is not None:
+                durs[g].append(v)
+    end.record()
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - wall0) * 1e3 / K
+    S.timing_enable(False)
+    ms = start.elapsed_time(end) / K
+    nnz, dense = res
+    w.finish_bytes(nnz, dense)
+    return ms, wall, {g: float(np.mean(v)) for g, v in durs.items() if v}, nnz, dense
+
+
+GROUP_NAMES = {0: "reduce_tiles", 1: "reduce_write", 2: "reduce_slow", 3: "qsgd_norm",
+               4: "qsgd_codes", 5: "topk_select", 6: "topk_write", 7: "densify"}
+
+
+def source_hash() -> str:
+    h = hashlib.sha256()
+    for f in ("reduce.hip", "qsgd_device.h", "internal.h"):
+        with open(os.path.join(ROOT, "paper_1802_08021_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def traffic_for(kernel: str, workload: str):
+    """Measured HBM bytes per launch from the committed rocprofv3 counters,
+    only while the kernel source is unchanged since they were taken."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if t.get("kernel") != kernel or t.get("workload") != workload:
+        return None
+    if t.get("source_sha256") != source_hash():
+        return None
+    return t.get("bytes_per_launch")
+
+
+def cpu_baseline(d, c, seed, frac_log2=2):
+    """Oracle (quantize + reduce) on the coordinate slice [0, N/2^frac_log2)
+    of the same streams: same P, density, threshold fraction and tree."""
+    import oracle
+    from paper_1802_08021_amd import inputs
+    Ns = c.N >> frac_log2
+    idx, val = [], []
+    for a, v in zip(d["idx"], d["val"]):
+        n = int(np.searchsorted(a, Ns))
+        idx.append(a[:n])
+        val.append(v[:n])
+    nnz = sum(a.size for a in idx)
+    t0 = time.perf_counter()
+    if c.qbits:
+        _, _, deq = oracle.quantize(val, c.qbits, inputs.quant_seed(seed, c.cfg))
+    else:
+        deq = val
+    oracle.sparse_reduce(idx, deq, Ns, c.delta)
+    dt = time.perf_counter() - t0
+    return {"value": nnz / dt, "unit": "nnz/s", "cores": 1, "kind": "oracle",
+            "sample": f"{c.name} streams restricted to indices < N/{2**frac_log2} "
+                      f"({nnz} input nnz, N'={Ns}); quantize + reduce, single thread, {dt:.2f} s"}
+
+
+def describe(c) -> str:
+    q = f", QSGD {c.qbits}-bit" if c.qbits else ""
+    kind = {"uniform": "uniform indices", "zipf": "Zipf(1.1) permuted indices",
+            "topk": "top-k of dense Laplace rows"}[c.kind]
+    return f"{c.name}: P={c.P}, N={c.N}, k={c.k}, {kind}{q}, delta={c.delta}"
+
+
+def main() -> int:
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU's share of the reduction; runs on more than one GPU "
+              "are not part of this build (use --gpus 1).", file=sys.stderr)
+        return 2
+    import torch
+    from paper_1802_08021_amd import inputs, sparcml as S
+    if not torch.cuda.is_available():
+        print("bench.py needs a HIP device", file=sys.stderr)
+        return 2
+    if args.calibrate_copy:
+        return calibrate_copy(torch)
+    S.lib()
+    dev = torch.device("cuda:0")
+
+    head_cfg = inputs.config(int(args.workload[1]))
+    w = Workload(args.workload, head_cfg, args.seed, torch, dev)
+    ms, wall, kdur, root_nnz, dense = time_steps(w, args.steps, args.warmup, torch)
+    log(f"{args.workload}: {ms:.3f} ms/step (wall {wall:.3f}), kernels {kdur}")
+    value = w.nnz / (ms * 1e-3)
+    step_gbs = w.step_bytes / (ms * 1e-3) / 1e9
+
+    # dominant kernel and its roofline
+    dom = max(kdur, key=lambda g: kdur[g])
+    dom_bytes = w.kernel_bytes.get(dom)
+    achieved = dom_bytes / (kdur[dom] * 1e-3) / 1e9 if dom_bytes else None
+    roofline = {
+        "bound": "hbm",
+        "kernel": GROUP_NAMES[dom],
+        "achieved": achieved,
+        "peak": HBM_PEAK_GBS,
+        "unit": "GB/s",
+        "frac": achieved / HBM_PEAK_GBS if achieved else None,
+        "traffic": traffic_for(GROUP_NAMES[dom], args.workload),
+        "bytes_per_launch": dom_bytes,
+        "avg_ms": kdur[dom],
+    }
+    kernels = {GROUP_NAMES[g]: {"avg_ms": v, "bytes": w.kernel_bytes.get(g),
+                                "GB/s": (w.kernel_bytes[g] / (v * 1e-3) / 1e9) if w.kernel_bytes.get(g) else None}
+               for g, v in kdur.items()}
+
+    cpu = None
+    if not args.no_cpu_baseline and w.d_host is not None:
+        log("timing the CPU oracle on a bounded sample")
+        cpu = cpu_baseline(w.d_host, head_cfg, args.seed)
+    w = None
+    torch.cuda.empty_cache()
+
+    per_config = {}
+    if not args.no_per_config:
+        for name in ("c1", "c2", "c3", "c4", "c5"):
+            if name == args.workload:
+                continue
+            c = inputs.config(int(name[1]))
+            pw = Workload(name, c, args.seed, torch, dev)
+            pms, pwall, pk, pn, pd = time_steps(pw, max(5, args.steps // 2), 2, torch)
+            per_config[name] = {
+                "workload": describe(c), "ms_per_step": pms, "input_nnz_per_s": pw.nnz / (pms * 1e-3),
+                "step_GB/s": pw.step_bytes / (pms * 1e-3) / 1e9,
+                "step_frac_of_hbm_peak": pw.step_bytes / (pms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                "root_nnz": pn, "root_dense": pd,
+                "kernels": {GROUP_NAMES[g]: {"avg_ms": v, "GB/s": (pw.kernel_bytes[g] / (v * 1e-3) / 1e9)
+                                             if pw.kernel_bytes.get(g) else None} for g, v in pk.items()},
+            }
+            log(f"{name}: {pms:.3f} ms/step")
+            pw = None
+            torch.cuda.empty_cache()
+
+    line = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "nnz/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": describe(head_cfg), "P": head_cfg.P, "N": head_cfg.N, "k": head_cfg.k,
+                   "delta": head_cfg.delta, "qbits": head_cfg.qbits, "seed": args.seed,
+                   "root_nnz": root_nnz, "root_dense": dense},
+        "step_GB/s": step_gbs,
+        "roofline": roofline,
+        "kernels": kernels,
+        "cpu_baseline": cpu,
+        "wall_ms_per_step": wall,
+        "per_config": per_config,
+    }
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

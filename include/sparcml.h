@@ -195,6 +195,25 @@ SPARCML_API int sparcml_sparse_reduce(int P, const sparcml_stream* streams, uint
  */
 SPARCML_API int sparcml_densify(const sparcml_stream* in, uint64_t N, float* dense, void* stream);
 
+/*
+ * Kernel timing for benchmarks and profiling (off by default; per calling
+ * thread).  While enabled, each call records HIP events on its stream
+ * around its main kernels; sparcml_timing_read returns the duration (ms) of
+ * the most recent launch of one kernel group, waiting for its stop event.
+ * Groups: SPARCML_TIMER_*.  Enabling or disabling forgets earlier records.
+ * sparcml_timing_read returns EINVAL when the group has no record.
+ */
+#define SPARCML_TIMER_REDUCE_PASS 0  /* first tile pass of sparse_reduce */
+#define SPARCML_TIMER_REDUCE_WRITE 1 /* sparse-output tile pass */
+#define SPARCML_TIMER_REDUCE_SLOW 2  /* pass over tiles too full for the first pass */
+#define SPARCML_TIMER_QUANT_NORM 3   /* QSGD norm partials */
+#define SPARCML_TIMER_QUANT_CODES 4  /* QSGD coding */
+#define SPARCML_TIMER_TOPK_SELECT 5  /* top-k radix-select histogram passes */
+#define SPARCML_TIMER_TOPK_WRITE 6   /* top-k count, scan and write */
+#define SPARCML_TIMER_DENSIFY 7
+SPARCML_API int sparcml_timing_enable(int on);
+SPARCML_API int sparcml_timing_read(int group, float* ms);
+
 /* Static description of a status code. */
 SPARCML_API const char* sparcml_strerror(int status);
 

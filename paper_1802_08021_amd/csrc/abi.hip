@@ -88,6 +88,16 @@ const char* sparcml_strerror(int status)
 
 const char* sparcml_last_error(void) { return g_last_error; }
 
+int sparcml_timing_enable(int on) { return timer_enable(on); }
+
+int sparcml_timing_read(int group, float* ms)
+{
+    const int rc = timer_read(group, ms);
+    if (rc == -1) return fail(SPARCML_EINVAL, "no timing record for group %d", group);
+    if (rc != 0) return fail(SPARCML_EHIP, "event query failed");
+    return SPARCML_OK;
+}
+
 int sparcml_workspace_size(int op, int P, uint64_t N, uint64_t max_nnz, double delta, size_t* bytes)
 {
     if (!bytes) return fail(SPARCML_EINVAL, "bytes is NULL");
@@ -104,7 +114,9 @@ int sparcml_workspace_size(int op, int P, uint64_t N, uint64_t max_nnz, double d
         if (!is_pow2(P) || P > 256 || !valid_n(N) || !(delta > 0.0) || max_nnz > N)
             return fail(SPARCML_EINVAL, "bad reduce sizes");
         ReducePlan p;
-        reduce_plan(P, N, max_nnz, 0, delta, 0, &p);
+        // the call's sum of nnz is at most P * max_nnz, which never needs a
+        // smaller workspace than the call itself
+        reduce_plan(P, N, max_nnz, (uint64_t)P * max_nnz, delta, 0, &p);
         *bytes = P == 1 ? 0 : reduce_workspace(p);
         return SPARCML_OK;
     }

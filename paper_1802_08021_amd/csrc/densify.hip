@@ -75,8 +75,10 @@ hipError_t densify_run(const uint32_t* idx, const float* val, const uint8_t* qva
         return hipMemcpyAsync(dense, val, N * sizeof(float), hipMemcpyDeviceToDevice, s);
     }
     const uint64_t tiles = (N + kTile - 1) / kTile;
+    timer_begin(kTDensify, s);
     hipLaunchKernelGGL(k_densify, dim3((uint32_t)tiles), dim3(256), 0, s, idx, val, qval, qscale,
                        qbits, (uint32_t)nnz, N, dense);
+    timer_end(kTDensify, s);
     return hipGetLastError();
 }
 

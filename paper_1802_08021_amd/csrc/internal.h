@@ -25,6 +25,24 @@ struct Blob {
 };
 hipError_t upload(void* dst, const void* src, size_t bytes, hipStream_t s);
 
+// Optional kernel timing (see sparcml_timing_enable): HIP events recorded
+// on the launch stream around the main kernels of each call.
+enum TimerSlot {
+    kTReducePass = 0,   // first tile pass of sparse_reduce (count or dense)
+    kTReduceWrite = 1,  // sparse-output tile pass
+    kTReduceSlow = 2,   // deferred-tile pass following the first tile pass
+    kTQuantNorm = 3,    // QSGD norm partials
+    kTQuantCodes = 4,   // QSGD coding pass
+    kTTopkSelect = 5,   // top-k histogram passes
+    kTTopkWrite = 6,    // top-k count + scan + write
+    kTDensify = 7,
+    kTSlots = 8
+};
+void timer_begin(int slot, hipStream_t s);
+void timer_end(int slot, hipStream_t s);
+int timer_enable(int on);
+int timer_read(int slot, float* ms);
+
 // Round x up to a multiple of a (a power of two).
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) & ~(a - 1); }
 

@@ -210,8 +210,10 @@ hipError_t quant_run(int P, const float* const* vals, const uint64_t* n, int bit
     delete[] host;
     if (e != hipSuccess) return e;
 
+    timer_begin(kTQuantNorm, s);
     hipLaunchKernelGGL(k_sumsq_partial, dim3(l.count[0], P), dim3(256), 0, s, l.tab, l.part[0],
                        l.count[0]);
+    timer_end(kTQuantNorm, s);
     for (int lv = 1; lv <= l.levels; ++lv)
         hipLaunchKernelGGL(k_sum_f64, dim3(l.count[lv], P), dim3(1024), 0, s, l.part[lv - 1],
                            l.count[lv - 1], l.part[lv], l.count[lv]);
@@ -222,9 +224,11 @@ hipError_t quant_run(int P, const float* const* vals, const uint64_t* n, int bit
     const uint32_t k0 = (uint32_t)(seed & 0xFFFFFFFFu), k1 = (uint32_t)(seed >> 32);
     const uint64_t per_block = 256ull * (32 / bits);
     const dim3 grid((uint32_t)((max_n + per_block - 1) / per_block), P);
+    timer_begin(kTQuantCodes, s);
     if (bits == 2) hipLaunchKernelGGL(k_quantize<2>, grid, dim3(256), 0, s, l.tab, out_scale, k0, k1);
     else if (bits == 4) hipLaunchKernelGGL(k_quantize<4>, grid, dim3(256), 0, s, l.tab, out_scale, k0, k1);
     else hipLaunchKernelGGL(k_quantize<8>, grid, dim3(256), 0, s, l.tab, out_scale, k0, k1);
+    timer_end(kTQuantCodes, s);
     return hipGetLastError();
 }
 

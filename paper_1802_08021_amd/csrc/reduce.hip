@@ -33,21 +33,32 @@ namespace sparcml {
 namespace {
 
 enum Mode { kCount = 0, kDense = 1, kSparseWrite = 2 };
+
+// Pointers that live in memory (descriptor tables, LDS) are generic unless
+// marked: generic (FLAT) loads also count against the LDS wait counter and
+// would serialize the LDS work behind every HBM access.
+typedef const uint32_t __attribute__((address_space(1))) g_u32;
+typedef const uint8_t __attribute__((address_space(1))) g_u8;
+typedef const float __attribute__((address_space(1))) g_f32;
 constexpr uint32_t kCap = 4096;  // entries per tile on the fast path
 constexpr uint32_t kWin = 64;    // entries read per rank per tile (one wave)
 constexpr int kSlowNT = 256;
 constexpr int kSlowTS = 1024;    // coordinates per slow-path sub-tile
 
+// MW = 32-bit rank-mask words per coordinate = ceil(P / 32).  Every fast
+// tile kernel has 256 threads; TMAX coordinates of masks take 16 KB of LDS;
+// CAP entries per tile fit the fast path.  Ranks are read in pairs: one
+// 64-lane load covers a 32-entry window of two ranks.
 template <int MW>
-struct Shape;  // MW = 32-bit mask words per coordinate = ceil(P / 32)
-template <>
-struct Shape<1> { static constexpr int NT = 256, TMAX = 4096, LMAX = 5; };
-template <>
-struct Shape<2> { static constexpr int NT = 256, TMAX = 4096, LMAX = 6; };
-template <>
-struct Shape<4> { static constexpr int NT = 256, TMAX = 2048, LMAX = 7; };
-template <>
-struct Shape<8> { static constexpr int NT = 512, TMAX = 1024, LMAX = 8; };
+struct Shape {
+    static constexpr int NT = 256, NW = 4;
+    static constexpr int TMAX = 4096 / MW;
+    static constexpr int LMAX = MW == 1 ? 5 : (MW == 2 ? 6 : (MW == 4 ? 7 : 8));
+    static constexpr int PMAX = 32 * MW;
+    static constexpr int CAP = 2048;
+    static constexpr int SLOTS = PMAX / 2 / NW;  // rank pairs per wave
+};
+constexpr uint32_t kHalf = 32;  // window per rank per tile
 
 struct Args {
     const StreamDesc* tab;
@@ -73,6 +84,41 @@ __device__ __forceinline__ uint32_t lower_bound(const uint32_t* a, uint32_t lo, 
     return lo;
 }
 
+// The MW rank-mask words of index j (vector LDS access where possible).
+template <int MW>
+__device__ __forceinline__ void load_mask(const uint32_t* m, uint32_t j, uint32_t (&w)[MW])
+{
+    if constexpr (MW == 1) {
+        w[0] = m[j];
+    } else if constexpr (MW == 2) {
+        const uint2 v = reinterpret_cast<const uint2*>(m)[j];
+        w[0] = v.x;
+        w[1] = v.y;
+    } else {
+#pragma unroll
+        for (int k = 0; k < MW / 4; ++k) {
+            const uint4 v = reinterpret_cast<const uint4*>(m)[j * (MW / 4) + k];
+            w[4 * k] = v.x;
+            w[4 * k + 1] = v.y;
+            w[4 * k + 2] = v.z;
+            w[4 * k + 3] = v.w;
+        }
+    }
+}
+
+template <int MW>
+__device__ __forceinline__ void clear_mask(uint32_t* m, uint32_t j)
+{
+    if constexpr (MW == 1) {
+        m[j] = 0u;
+    } else if constexpr (MW == 2) {
+        reinterpret_cast<uint2*>(m)[j] = make_uint2(0u, 0u);
+    } else {
+#pragma unroll
+        for (int k = 0; k < MW / 4; ++k) reinterpret_cast<uint4*>(m)[j * (MW / 4) + k] = make_uint4(0u, 0u, 0u, 0u);
+    }
+}
+
 // Level t (1-based) and group g of internal node `node` in level order.
 __device__ __forceinline__ void node_coords(uint32_t node, uint32_t P, uint32_t* t, uint32_t* g)
 {
@@ -85,16 +131,21 @@ __device__ __forceinline__ void node_coords(uint32_t node, uint32_t P, uint32_t*
     *g = node - base;
 }
 
-// Turn per-(rank, depth) counts into node union sizes and add them to the
-// global counters.  E[r][d] = entries of rank r that open new groups at
-// levels 1..d; node (t,g) counts the entries of its ranks with depth >= t.
+// Turn per-rank counts into node union sizes and add them to the global
+// counters.  E[r][d], d < L: entries of rank r whose predecessor (next lower
+// rank present at the same index) first differs from r at bit d -- such an
+// entry opens a new group at levels 1..d; E[r][L]: all entries of rank r,
+// of which those without predecessor open new groups at every level.
+// Node (t, g) counts the entries of its ranks that open a group at level t.
 template <int NT>
 __device__ void flush_counts(uint32_t* E, const Args& a)
 {
     const uint32_t P = a.P, L = a.L, W = L + 1;
     for (uint32_t r = threadIdx.x; r < P; r += NT) {
-        uint32_t acc = 0;
-        for (int d = (int)L; d >= 1; --d) {
+        uint32_t acc = E[r * W + L];
+        for (uint32_t d = 0; d < L; ++d) acc -= E[r * W + d];
+        E[r * W + L] = acc;
+        for (int d = (int)L - 1; d >= 1; --d) {
             acc += E[r * W + d];
             E[r * W + d] = acc;
         }
@@ -110,103 +161,138 @@ __device__ void flush_counts(uint32_t* E, const Args& a)
 }
 
 // ------------------------------------------------------------------------
-// Fast tile pass.  One workgroup walks a chunk of consecutive tiles; wave w
-// owns ranks [w*RPW, (w+1)*RPW) and reads a 64-entry window of each per
-// tile.  Tiles where a rank has >= 64 entries or the tile has > kCap entries
-// are deferred to the slow pass.
+// Fast tile pass.  One workgroup walks a chunk of consecutive tiles of T
+// indices.  Per tile:
+//   A  each wave reads a 32-entry window of two ranks per 64-lane load and
+//      counts, by ballot, how many fall in the tile;
+//   B  the entries are compacted into LDS (rank-major) and their rank bits
+//      set in the per-index masks;
+//   2  per index: ranks present (popcount), exclusive scan -> where each
+//      index's values start, in rank order;
+//   3  per entry: value placed at its index's start plus the number of lower
+//      ranks present; entries with a predecessor counted by split level;
+//   4  per thread: a flat walk over its indices' values, summing each index
+//      with the tree's association, then one write of the tile.
+// Tiles where a rank fills its window or with more than CAP entries go to
+// the slow pass.
 template <int MW, int MODE, bool QUANT>
-__global__ void __launch_bounds__(Shape<MW>::NT) k_tiles(Args a)
+__global__ void __launch_bounds__(256) k_tiles(Args a)
 {
-    constexpr int NT = Shape<MW>::NT, NW = NT / 64, TMAX = Shape<MW>::TMAX;
-    constexpr int LMAX = Shape<MW>::LMAX, PMAX = 32 * MW, RPW = PMAX / NW;
-    __shared__ uint32_t s_mask[TMAX * MW];
-    __shared__ float s_vals[MODE == kCount ? 1 : kCap];
+    using S = Shape<MW>;
+    constexpr int NT = S::NT, NW = S::NW, TMAX = S::TMAX, LMAX = S::LMAX, PMAX = S::PMAX;
+    constexpr int CAP = S::CAP, SLOTS = S::SLOTS, CPTMAX = TMAX / NT;
+    __shared__ uint4 s_mask4[TMAX * MW / 4];
+    __shared__ uint32_t s_ent[2 * CAP];  // [0,CAP): index<<8 | rank; [CAP,2CAP): value bits
+    __shared__ float s_vals[MODE == kCount ? 1 : CAP];
     __shared__ uint16_t s_bin[MODE == kCount ? 1 : TMAX];
     __shared__ uint32_t s_E[MODE == kSparseWrite ? 1 : PMAX * (LMAX + 1)];
-    __shared__ uint32_t s_cur[PMAX], s_end[PMAX], s_cnt[PMAX];
+    __shared__ uint32_t s_cur[PMAX], s_end[PMAX], s_cnt[PMAX], s_last[PMAX];
+    __shared__ g_u32* s_ip[PMAX];
+    __shared__ g_u32* s_vp[PMAX];  // fp32 bits, or packed codes (byte-addressed)
     __shared__ float s_unit[QUANT ? PMAX : 1];
-    __shared__ uint32_t s_wsum[NW];
-    __shared__ uint32_t s_total, s_slow;
+    __shared__ uint32_t s_wsum[CPTMAX * NW];
+    __shared__ uint32_t s_slow;
+    uint32_t* s_mask = reinterpret_cast<uint32_t*>(s_mask4);
+    uint32_t* s_entv = s_ent + CAP;
+    float* s_out = reinterpret_cast<float*>(s_ent);  // phase 4 only (T <= 2*CAP)
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const uint32_t P = a.P, L = a.L, T = a.T, CPT = T / NT;
+    const uint32_t half = (uint32_t)lane >> 5, sl = (uint32_t)lane & 31u;
+    const uint32_t P = a.P, L = a.L, T = a.T, CPT = T / NT, W = L + 1;
     const uint32_t chunk = blockIdx.x, stride = a.nchunks + 1;
     const uint32_t t0 = chunk * a.tpc, t1 = min(t0 + a.tpc, a.ntiles);
+    const uint32_t RPL = P > 64 ? P / 64 : 1;  // ranks per lane in the rank scan
 
     for (uint32_t r = tid; r < P; r += NT) {
+        const StreamDesc* d = &a.tab[r];
         s_cur[r] = a.off[r * stride + chunk];
         s_end[r] = a.off[r * stride + chunk + 1];
-        if (QUANT)
-            s_unit[r] = level_unit(*a.tab[r].qscale, a.qbits);
+        // empty streams read (and discard) a word of the descriptor table
+        const bool empty = d->nnz == 0;
+        s_last[r] = empty ? 0u : (uint32_t)(d->nnz - 1);
+        const void* ip = empty ? static_cast<const void*>(a.tab) : static_cast<const void*>(d->idx);
+        const void* vp = empty ? static_cast<const void*>(a.tab)
+                               : (QUANT ? static_cast<const void*>(d->qval) : static_cast<const void*>(d->val));
+        s_ip[r] = (g_u32*)ip;
+        s_vp[r] = (g_u32*)vp;
+        if (QUANT) s_unit[r] = level_unit(*d->qscale, a.qbits);
     }
     if (MODE != kSparseWrite)
-        for (uint32_t i = tid; i < P * (L + 1); i += NT) s_E[i] = 0;
+        for (uint32_t i = tid; i < P * W; i += NT) s_E[i] = 0;
+    for (uint32_t i = tid; i < TMAX * MW / 4; i += NT) s_mask4[i] = make_uint4(0u, 0u, 0u, 0u);
 
     for (uint32_t tile = t0; tile < t1; ++tile) {
         const uint32_t tlo = tile * T;
         const uint32_t thi = (uint32_t)min((uint64_t)tlo + T, (uint64_t)a.N);
         __syncthreads();
-        for (uint32_t i = tid; i < T * MW / 4; i += NT)
-            reinterpret_cast<uint4*>(s_mask)[i] = make_uint4(0u, 0u, 0u, 0u);
-        if (tid == 0) {
-            s_total = 0;
-            s_slow = 0;
-        }
-        __syncthreads();
+        if (tid == 0) s_slow = 0;
 
-        // Phase 1: windows, rank bits, per-rank counts.
-        uint32_t xs[RPW], vs[RPW], inmask = 0;
+        // A: windows of two ranks per load.  Straight-line code: every load
+        // is issued before any is used (ranks past P read rank P-1 and are
+        // masked out afterwards).
+        uint32_t xs[SLOTS], vs[SLOTS], okbits = 0;
 #pragma unroll
-        for (int s = 0; s < RPW; ++s) {
-            const uint32_t r = wv * RPW + s;
-            xs[s] = 0xFFFFFFFFu;
-            vs[s] = 0u;
-            if (r < P) {
-                const uint32_t i = s_cur[r] + lane;
-                if (i < s_end[r]) {
-                    const StreamDesc* d = &a.tab[r];
-                    xs[s] = d->idx[i];
-                    vs[s] = QUANT ? load_code(d->qval, i, a.qbits) : __float_as_uint(d->val[i]);
-                }
+        for (int q = 0; q < SLOTS; ++q) {
+            const uint32_t r = 2 * (uint32_t)(wv * SLOTS + q) + half;
+            const uint32_t rr = min(r, P - 1);
+            const uint32_t i = s_cur[rr] + sl;
+            const uint32_t ic = min(i, s_last[rr]);
+            xs[q] = s_ip[rr][ic];
+            if (QUANT) {
+                const uint32_t plog = a.qbits == 8u ? 0u : (a.qbits == 4u ? 1u : 2u);
+                const uint32_t byte = ((g_u8*)s_vp[rr])[ic >> plog];
+                vs[q] = (byte >> ((ic & ((1u << plog) - 1u)) * a.qbits)) & ((1u << a.qbits) - 1u);
+            } else {
+                vs[q] = s_vp[rr][ic];
             }
+            okbits |= (uint32_t)(r < P && i < s_end[rr]) << q;
         }
+        uint32_t inbits = 0;
 #pragma unroll
-        for (int s = 0; s < RPW; ++s) {
-            const uint32_t r = wv * RPW + s;
-            if (r < P) {
-                const bool in = xs[s] >= tlo && xs[s] < thi;
-                const uint64_t bal = __ballot(in);
-                if (in) {
-                    atomicOr(&s_mask[(xs[s] - tlo) * MW + (r >> 5)], 1u << (r & 31u));
-                    inmask |= 1u << s;
-                }
-                if (lane == 0) {
-                    const uint32_t c = (uint32_t)__popcll(bal);
-                    s_cnt[r] = c;
-                    atomicAdd(&s_total, c);
-                    if (c == kWin) s_slow = 1u;
-                }
+        for (int q = 0; q < SLOTS; ++q) {
+            const bool in = ((okbits >> q) & 1u) && xs[q] >= tlo && xs[q] < thi;
+            inbits |= (uint32_t)in << q;
+            const uint64_t bal = __ballot(in);
+            const uint32_t c = (uint32_t)__popc((uint32_t)(bal >> (32 * half)));
+            if (sl == 0) {
+                s_cnt[2 * (uint32_t)(wv * SLOTS + q) + half] = c;
+                if (c == kHalf) s_slow = 1u;
             }
         }
         __syncthreads();
 
-        if (s_slow || s_total > kCap) {
-            // Defer the tile; move every cursor past it (a rank may hold more
-            // than one window's worth of entries here).
-            for (int s = 0; s < RPW; ++s) {
-                const uint32_t r = wv * RPW + s;
+        // Every wave scans the per-rank counts itself (RPL ranks per lane).
+        uint32_t lsum = 0;
+        for (uint32_t k = 0; k < RPL; ++k) {
+            const uint32_t r = (uint32_t)lane * RPL + k;
+            lsum += r < P ? s_cnt[r] : 0u;
+        }
+        uint32_t lincl = lsum;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+            const uint32_t y = __shfl_up(lincl, o);
+            if (lane >= o) lincl += y;
+        }
+        const uint32_t total = __shfl(lincl, 63);
+        const uint32_t lexcl = lincl - lsum;
+
+        if (s_slow || total > (uint32_t)CAP) {
+            // Defer the tile and move every cursor past it (a rank may hold
+            // more than one window's worth of entries here).
+            for (int k = 0; k < 2 * SLOTS; ++k) {
+                const uint32_t r = (uint32_t)(wv * 2 * SLOTS + k);
                 if (r >= P) break;
                 uint32_t n = s_cnt[r];
-                if (n == kWin) {
-                    const uint32_t* idx = a.tab[r].idx;
+                if (n == kHalf) {
+                    g_u32* idx = s_ip[r];
                     const uint32_t base = s_cur[r], end = s_end[r];
                     for (;;) {
                         const uint32_t i = base + n + lane;
                         const bool in = i < end && idx[i] < thi;
                         const uint32_t c = (uint32_t)__popcll(__ballot(in));
                         n += c;
-                        if (c < kWin) break;
+                        if (c < 64) break;
                     }
                 }
                 if (lane == 0) s_cur[r] += n;
@@ -217,133 +303,186 @@ __global__ void __launch_bounds__(Shape<MW>::NT) k_tiles(Args a)
             }
             continue;
         }
-        for (uint32_t r = tid; r < P; r += NT) s_cur[r] += s_cnt[r];
 
-        // Phase 2: per-coordinate rank counts; exclusive scan packs
-        // (entries below 16 bits, non-empty coordinates above).
-        const uint32_t j0 = tid * CPT;
-        uint32_t acc = 0;
-        for (uint32_t q = 0; q < CPT; ++q) {
-            uint32_t m = 0;
+        // B: compact the entries (rank-major) and set the rank bits.
 #pragma unroll
-            for (int w = 0; w < MW; ++w) m += __popc(s_mask[(j0 + q) * MW + w]);
-            acc += m | ((m != 0u) << 16);
+        for (int q = 0; q < SLOTS; ++q) {
+            const uint32_t u = (uint32_t)(wv * SLOTS + q);
+            if (2 * u < P) {
+                const uint32_t r = 2 * u + half;
+                const uint32_t lr = r / RPL;
+                uint32_t base = __shfl(lexcl, (int)lr);
+                for (uint32_t k = lr * RPL; k < r; ++k) base += s_cnt[k];
+                if ((inbits >> q) & 1u) {
+                    const uint32_t j = xs[q] - tlo;
+                    s_ent[base + sl] = (j << 8) | r;
+                    s_entv[base + sl] = vs[q];
+                    atomicOr(&s_mask[j * MW + (r >> 5)], 1u << (r & 31u));
+                }
+            }
         }
-        uint32_t incl = acc;
-#pragma unroll
-        for (int o = 1; o < 64; o <<= 1) {
-            const uint32_t y = __shfl_up(incl, o);
-            if (lane >= o) incl += y;
-        }
-        if (lane == 63) s_wsum[wv] = incl;
+        if (MODE != kSparseWrite)
+            for (uint32_t r = tid; r < P; r += NT) s_E[r * W + L] += s_cnt[r];
+        for (uint32_t r = tid; r < P; r += NT) s_cur[r] += s_cnt[r];
         __syncthreads();
-        uint32_t excl = incl - acc, total = 0;
+
+        // 2: ranks per index.  Thread t owns indices q*NT + t (q < CPT), so
+        // per-lane LDS accesses are consecutive (no bank conflicts) and the
+        // dense write coalesces.  Exclusive scan over indices in order: one
+        // wave scan per round q, the wave totals of all rounds exchanged
+        // through LDS at once; packed (entries low 16 bits, non-empty high).
+        uint32_t pk[CPTMAX], ex[CPTMAX];
 #pragma unroll
-        for (int w = 0; w < NW; ++w) {
-            const uint32_t v = s_wsum[w];
-            if (w < wv) excl += v;
-            total += v;
-        }
-        if (MODE != kSparseWrite && tid == 0) a.tile_cnt[tile] = total >> 16;
-        if (MODE != kCount) {
-            uint32_t run = excl;
-            for (uint32_t q = 0; q < CPT; ++q) {
+        for (int q = 0; q < CPTMAX; ++q) {
+            pk[q] = 0;
+            ex[q] = 0;
+            if ((uint32_t)q < CPT) {
+                uint32_t w[MW];
+                load_mask<MW>(s_mask, (uint32_t)q * NT + tid, w);
                 uint32_t m = 0;
 #pragma unroll
-                for (int w = 0; w < MW; ++w) m += __popc(s_mask[(j0 + q) * MW + w]);
-                s_bin[j0 + q] = (uint16_t)(run & 0xFFFFu);
-                run += m | ((m != 0u) << 16);
+                for (int k = 0; k < MW; ++k) m += __popc(w[k]);
+                pk[q] = m | ((m != 0u) << 16);
+                uint32_t incl = pk[q];
+#pragma unroll
+                for (int o = 1; o < 64; o <<= 1) {
+                    const uint32_t y = __shfl_up(incl, o);
+                    if (lane >= o) incl += y;
+                }
+                ex[q] = incl - pk[q];
+                if (lane == 63) s_wsum[q * NW + wv] = incl;
             }
         }
         __syncthreads();
-
-        // Phase 3: place values in rank order; count node memberships.
+        uint32_t run = 0;
 #pragma unroll
-        for (int s = 0; s < RPW; ++s) {
-            const uint32_t r = wv * RPW + s;
-            if (r < P && ((inmask >> s) & 1u)) {
-                const uint32_t j = xs[s] - tlo;
-                uint32_t w[MW];
+        for (int q = 0; q < CPTMAX; ++q) {
+            if ((uint32_t)q < CPT) {
+                uint32_t before = 0, rtot = 0;
 #pragma unroll
-                for (int k = 0; k < MW; ++k) w[k] = s_mask[j * MW + k];
-                const uint32_t rw = r >> 5, lowbits = (1u << (r & 31u)) - 1u;
-                if (MODE != kCount) {
-                    uint32_t below = 0;
-#pragma unroll
-                    for (int k = 0; k < MW; ++k)
-                        below += (uint32_t)k < rw ? __popc(w[k])
-                                                  : ((uint32_t)k == rw ? __popc(w[k] & lowbits) : 0u);
-                    const float v = QUANT ? dequant(vs[s], a.qbits, s_unit[r]) : __uint_as_float(vs[s]);
-                    s_vals[s_bin[j] + below] = v;
+                for (int w = 0; w < NW; ++w) {
+                    const uint32_t v = s_wsum[q * NW + w];
+                    if (w < wv) before += v;
+                    rtot += v;
                 }
-                if (MODE != kSparseWrite) {
-                    int prev = -1;
-#pragma unroll
-                    for (int k = MW - 1; k >= 0; --k) {
-                        const uint32_t cand = (uint32_t)k < rw ? w[k]
-                                                               : ((uint32_t)k == rw ? (w[k] & lowbits) : 0u);
-                        if (prev < 0 && cand) prev = k * 32 + 31 - (int)__clz(cand);
-                    }
-                    const uint32_t depth = prev < 0 ? L : (31u - (uint32_t)__clz(r ^ (uint32_t)prev));
-                    if (depth) atomicAdd(&s_E[r * (L + 1) + depth], 1u);
-                }
+                ex[q] += run + before;
+                run += rtot;
+                if (MODE != kCount) s_bin[(uint32_t)q * NT + tid] = (uint16_t)(ex[q] & 0xFFFFu);
             }
         }
-        if (MODE == kCount) continue;
+        if (MODE != kSparseWrite && tid == 0) a.tile_cnt[tile] = run >> 16;
         __syncthreads();
 
-        // Phase 4: tree sum per coordinate, write the tile once.
-        uint32_t run = excl;
-        for (uint32_t q = 0; q < CPT; ++q) {
-            const uint32_t j = j0 + q;
-            uint32_t w[MW], m = 0;
+        // 3: per entry -- rank-ordered placement and split-level counts.
+        for (uint32_t e = tid; e < total; e += NT) {
+            const uint32_t ent = s_ent[e];
+            const uint32_t r = ent & 0xFFu, j = ent >> 8;
+            uint32_t w[MW];
+            load_mask<MW>(s_mask, j, w);
+            const uint32_t rw = r >> 5, lowbits = (1u << (r & 31u)) - 1u;
+            if (MODE != kCount) {
+                uint32_t below = 0;
+#pragma unroll
+                for (int k = 0; k < MW; ++k)
+                    below += (uint32_t)k < rw ? __popc(w[k])
+                                              : ((uint32_t)k == rw ? __popc(w[k] & lowbits) : 0u);
+                const uint32_t vb = s_entv[e];
+                const float v = QUANT ? dequant(vb, a.qbits, s_unit[r]) : __uint_as_float(vb);
+                s_vals[s_bin[j] + below] = v;
+            }
+            if (MODE != kSparseWrite) {
+                int prev = -1;
+#pragma unroll
+                for (int k = MW - 1; k >= 0; --k) {
+                    const uint32_t cand = (uint32_t)k < rw ? w[k]
+                                                           : ((uint32_t)k == rw ? (w[k] & lowbits) : 0u);
+                    if (prev < 0 && cand) prev = k * 32 + 31 - (int)__clz(cand);
+                }
+                if (prev >= 0) atomicAdd(&s_E[r * W + (31u - (uint32_t)__clz(r ^ (uint32_t)prev))], 1u);
+            }
+        }
+        __syncthreads();
+        if (MODE == kCount) {
+            for (uint32_t q = 0; q < CPT; ++q) clear_mask<MW>(s_mask, q * NT + tid);
+            continue;
+        }
+
+        // 4: flat walk over this thread's entries, index by index (q order),
+        // summing each index's values with the tree's association.
+        uint32_t nent = 0;
+#pragma unroll
+        for (int q = 0; q < CPTMAX; ++q) nent += pk[q] & 0xFFFFu;
+        if (MODE == kDense)
+            for (uint32_t q = 0; q < CPT; ++q) s_out[q * NT + tid] = 0.0f;
+        uint32_t q = 0, bits[MW];
+        load_mask<MW>(s_mask, tid, bits);
+        uint32_t pos = s_bin[tid];
+        float slot[LMAX];
+#pragma unroll
+        for (int l = 0; l < LMAX; ++l) slot[l] = 0.0f;
+        float cur = 0.0f;
+        uint32_t pend = 0;
+        int last = -1;
+        for (uint32_t it = 0; it < nent; ++it) {
+            for (;;) {  // next index with ranks left (nent guarantees one)
+                uint32_t any = 0;
+#pragma unroll
+                for (int k = 0; k < MW; ++k) any |= bits[k];
+                if (any) break;
+                ++q;
+                load_mask<MW>(s_mask, q * NT + tid, bits);
+                pos = s_bin[q * NT + tid];
+            }
+            int r = -1;
 #pragma unroll
             for (int k = 0; k < MW; ++k) {
-                w[k] = s_mask[j * MW + k];
-                m += __popc(w[k]);
-            }
-            float sum = 0.0f;
-            if (m) {
-                uint32_t pos = run & 0xFFFFu, pend = 0;
-                float slot[LMAX];
-#pragma unroll
-                for (int l = 0; l < LMAX; ++l) slot[l] = 0.0f;
-                float cur = 0.0f;
-                int last = -1;
-#pragma unroll
-                for (int k = 0; k < MW; ++k) {
-                    uint32_t bits = w[k];
-                    while (bits) {
-                        const int r = k * 32 + (__ffs(bits) - 1);
-                        bits &= bits - 1u;
-                        const float v = s_vals[pos++];
-                        if (last >= 0) {
-                            const int sep = 31 - (int)__clz((uint32_t)(r ^ last));
-#pragma unroll
-                            for (int l = 0; l < LMAX; ++l)
-                                if (l < sep && ((pend >> l) & 1u)) cur = slot[l] + cur;
-                            pend = (pend & ~((1u << sep) - 1u)) | (1u << sep);
-#pragma unroll
-                            for (int l = 0; l < LMAX; ++l)
-                                if (l == sep) slot[l] = cur;
-                        }
-                        cur = v;
-                        last = r;
-                    }
+                if (r < 0 && bits[k]) {
+                    r = k * 32 + (__ffs(bits[k]) - 1);
+                    bits[k] &= bits[k] - 1u;
                 }
+            }
+            const float v = s_vals[pos++];
+            if (last >= 0) {
+                const int sep = 31 - (int)__clz((uint32_t)(r ^ last));
+#pragma unroll
+                for (int l = 0; l < LMAX; ++l)
+                    if (l < sep && ((pend >> l) & 1u)) cur = slot[l] + cur;
+                pend = (pend & ~((1u << sep) - 1u)) | (1u << sep);
+#pragma unroll
+                for (int l = 0; l < LMAX; ++l)
+                    if (l == sep) slot[l] = cur;
+            }
+            cur = v;
+            last = r;
+            uint32_t left = 0;
+#pragma unroll
+            for (int k = 0; k < MW; ++k) left |= bits[k];
+            if (!left) {  // index q*NT + tid complete
 #pragma unroll
                 for (int l = 0; l < LMAX; ++l)
                     if ((pend >> l) & 1u) cur = slot[l] + cur;
-                sum = cur;
+                const uint32_t j = q * NT + tid;
+                if (MODE == kDense) {
+                    s_out[j] = cur + 0.0f;
+                } else {
+                    uint32_t nz = 0;
+#pragma unroll
+                    for (int qq = 0; qq < CPTMAX; ++qq)
+                        if ((uint32_t)qq == q) nz = ex[qq] >> 16;
+                    const uint32_t o = a.tile_off[tile] + nz;
+                    a.out_idx[o] = tlo + j;
+                    a.out_val[o] = cur;
+                }
+                pend = 0;
+                last = -1;
             }
-            if (MODE == kDense) {
-                if ((uint64_t)tlo + j < thi) a.out_val[(uint64_t)tlo + j] = m ? sum + 0.0f : 0.0f;
-            } else if (m) {
-                const uint32_t o = a.tile_off[tile] + (run >> 16);
-                a.out_idx[o] = tlo + j;
-                a.out_val[o] = sum;
+        }
+        for (uint32_t k = 0; k < CPT; ++k) clear_mask<MW>(s_mask, k * NT + tid);
+        if (MODE == kDense) {
+            for (uint32_t k = 0; k < CPT; ++k) {
+                const uint32_t j = k * NT + tid;
+                if ((uint64_t)tlo + j < thi) a.out_val[(uint64_t)tlo + j] = s_out[j];
             }
-            run += m | ((m != 0u) << 16);
         }
     }
     __syncthreads();
@@ -398,16 +537,23 @@ __global__ void __launch_bounds__(kSlowNT) k_slow(Args a)
                 const uint32_t lo = s_lo[r], hi = s_hi[r];
                 if (lo == hi) continue;
                 const StreamDesc* d = &a.tab[r];
+                g_u32* gidx = (g_u32*)d->idx;
+                g_f32* gval = (g_f32*)d->val;
+                g_u8* gq = (g_u8*)d->qval;
                 for (uint32_t i = lo + tid; i < hi; i += NT) {
-                    const uint32_t j = d->idx[i] - (uint32_t)sub;
+                    const uint32_t j = gidx[i] - (uint32_t)sub;
                     if (j >= width) continue;
-                    const float v = QUANT ? dequant(load_code(d->qval, i, a.qbits), a.qbits, s_unit[r])
-                                          : d->val[i];
-                    const int last = s_last[j];
-                    uint32_t depth;
-                    if (last < 0) {
-                        depth = L;
+                    float v;
+                    if (QUANT) {
+                        const uint32_t plog = a.qbits == 8u ? 0u : (a.qbits == 4u ? 1u : 2u);
+                        const uint32_t byte = gq[i >> plog];
+                        const uint32_t code = (byte >> ((i & ((1u << plog) - 1u)) * a.qbits)) & ((1u << a.qbits) - 1u);
+                        v = dequant(code, a.qbits, s_unit[r]);
                     } else {
+                        v = gval[i];
+                    }
+                    const int last = s_last[j];
+                    if (last >= 0) {
                         const uint32_t sep = 31u - (uint32_t)__clz(r ^ (uint32_t)last);
                         float cur = s_curv[j];
                         uint32_t pend = s_pend[j];
@@ -417,12 +563,12 @@ __global__ void __launch_bounds__(kSlowNT) k_slow(Args a)
                         pend = (pend & ~((1u << sep) - 1u)) | (1u << sep);
                         s_slot[sep][j] = cur;
                         s_pend[j] = (uint16_t)pend;
-                        depth = sep;
+                        if (MODE != kSparseWrite) atomicAdd(&s_E[r * (L + 1) + sep], 1u);
                     }
                     s_curv[j] = v;
                     s_last[j] = (int16_t)r;
-                    if (MODE != kSparseWrite && depth) atomicAdd(&s_E[r * (L + 1) + depth], 1u);
                 }
+                if (MODE != kSparseWrite && tid == 0) s_E[r * (L + 1) + L] += hi - lo;
                 __syncthreads();
             }
             __syncthreads();
@@ -563,12 +709,17 @@ __global__ void __launch_bounds__(1024) k_scan_tiles(const uint32_t* cnt, uint32
 template <int MW, int MODE>
 hipError_t launch_tiles_q(const Args& a, bool quant, hipStream_t s)
 {
-    const dim3 grid(a.nchunks), block(Shape<MW>::NT);
+    const dim3 grid(a.nchunks), block(256);
+    const int slot = MODE == kSparseWrite ? kTReduceWrite : kTReducePass;
+    timer_begin(slot, s);
     if (quant) hipLaunchKernelGGL((k_tiles<MW, MODE, true>), grid, block, 0, s, a);
     else hipLaunchKernelGGL((k_tiles<MW, MODE, false>), grid, block, 0, s, a);
+    timer_end(slot, s);
     const uint32_t sg = std::min<uint32_t>(a.ntiles, 256u);
+    if (MODE != kSparseWrite) timer_begin(kTReduceSlow, s);
     if (quant) hipLaunchKernelGGL((k_slow<MW, MODE, true>), dim3(sg), dim3(kSlowNT), 0, s, a);
     else hipLaunchKernelGGL((k_slow<MW, MODE, false>), dim3(sg), dim3(kSlowNT), 0, s, a);
+    if (MODE != kSparseWrite) timer_end(kTReduceSlow, s);
     return hipGetLastError();
 }
 
@@ -617,24 +768,21 @@ int reduce_plan(int P, uint64_t N, uint64_t max_nnz, uint64_t sum_nnz, double de
     p.L = 0;
     while ((1u << p.L) < p.P) ++p.L;
     p.MW = p.P <= 32 ? 1u : p.P / 32u;
-    const uint32_t NT = p.MW == 8 ? 512u : 256u;
-    const uint32_t TMAX = p.MW == 1 ? 4096u : (p.MW == 2 ? 4096u : (p.MW == 4 ? 2048u : 1024u));
-    // Aim for about 32 entries per rank per tile (half a window) so that a
-    // rank rarely fills its 64-entry window.
-    uint64_t T = TMAX;
-    if (max_nnz > 0) {
-        const uint64_t want = (32u * N) / max_nnz;
-        uint64_t t = NT;
-        while (t * 2 <= want && t * 2 <= TMAX) t *= 2;
-        T = t;
-    }
+    const uint64_t NT = 256, TMAX = 4096 / p.MW, CAP = 2048;
+    // Tile size: the largest power of two (256 .. TMAX) for which a tile
+    // holds on average at most 70% of CAP entries and a rank at most half of
+    // its 32-entry window, so that the slow pass stays rare.
+    uint64_t T = NT;
+    const double want_total = sum_nnz ? 0.7 * (double)CAP * (double)N / (double)sum_nnz : 1e30;
+    const double want_rank = max_nnz ? 16.0 * (double)N / (double)max_nnz : 1e30;
+    while (T * 2 <= TMAX && (double)(T * 2) <= want_total && (double)(T * 2) <= want_rank) T *= 2;
     uint64_t Np2 = NT;
     while (Np2 < N) Np2 *= 2;
     if (T > Np2) T = Np2;
     p.T = (uint32_t)T;
     p.N = N;
     p.ntiles = (uint32_t)((N + T - 1) / T);
-    uint32_t nch = std::min<uint32_t>(p.ntiles, 512u);
+    uint32_t nch = std::min<uint32_t>(p.ntiles, 768u);
     p.tiles_per_chunk = (p.ntiles + nch - 1) / nch;
     p.nchunks = (p.ntiles + p.tiles_per_chunk - 1) / p.tiles_per_chunk;
     const double t = std::floor(delta * (double)N);

@@ -272,17 +272,21 @@ hipError_t topk_run(int P, const float* x, uint64_t N, uint64_t k, uint32_t* out
                        (uint32_t)P, k, l.hist);
     const uint32_t hb = (uint32_t)std::min<uint64_t>(kHistBlocksPerRank, (N + 4095) / 4096);
     const dim3 hgrid(hb, P);
+    timer_begin(kTTopkSelect, s);
     hipLaunchKernelGGL(k_hist<0>, hgrid, dim3(256), 0, s, x, N, l.st, l.hist);
     hipLaunchKernelGGL(k_select<0>, dim3(P), dim3(256), 0, s, l.st, l.hist);
     hipLaunchKernelGGL(k_hist<1>, hgrid, dim3(256), 0, s, x, N, l.st, l.hist);
     hipLaunchKernelGGL(k_select<1>, dim3(P), dim3(256), 0, s, l.st, l.hist);
     hipLaunchKernelGGL(k_hist<2>, hgrid, dim3(256), 0, s, x, N, l.st, l.hist);
     hipLaunchKernelGGL(k_select<2>, dim3(P), dim3(256), 0, s, l.st, l.hist);
+    timer_end(kTTopkSelect, s);
+    timer_begin(kTTopkWrite, s);
     const dim3 ugrid((l.U + 3) / 4, P);
     hipLaunchKernelGGL(k_count, ugrid, dim3(256), 0, s, x, N, l.U, l.st, l.cgt, l.ceq);
     hipLaunchKernelGGL(k_unit_scan, dim3(P), dim3(1024), 0, s, l.U, l.st, l.cgt, l.ceq, l.beq, l.bout);
     hipLaunchKernelGGL(k_write, ugrid, dim3(256), 0, s, x, N, k, l.U, l.st, l.beq, l.bout, out_idx,
                        out_val, residual);
+    timer_end(kTTopkWrite, s);
     return hipGetLastError();
 }
 

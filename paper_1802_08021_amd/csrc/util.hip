@@ -36,4 +36,52 @@ hipError_t upload(void* dst, const void* src, size_t bytes, hipStream_t s)
     return hipSuccess;
 }
 
+namespace {
+
+struct Timers {
+    bool enabled = false;
+    bool created = false;
+    hipEvent_t ev[kTSlots][2];
+    bool recorded[kTSlots] = {};
+};
+thread_local Timers g_timers;
+
+}  // namespace
+
+void timer_begin(int slot, hipStream_t s)
+{
+    Timers& t = g_timers;
+    if (!t.enabled) return;
+    if (!t.created) {
+        for (int i = 0; i < kTSlots; ++i)
+            for (int j = 0; j < 2; ++j)
+                if (hipEventCreate(&t.ev[i][j]) != hipSuccess) return;
+        t.created = true;
+    }
+    hipEventRecord(t.ev[slot][0], s);
+}
+
+void timer_end(int slot, hipStream_t s)
+{
+    Timers& t = g_timers;
+    if (!t.enabled || !t.created) return;
+    hipEventRecord(t.ev[slot][1], s);
+    t.recorded[slot] = true;
+}
+
+int timer_enable(int on)
+{
+    g_timers.enabled = on != 0;
+    for (bool& r : g_timers.recorded) r = false;
+    return 0;
+}
+
+int timer_read(int slot, float* ms)
+{
+    Timers& t = g_timers;
+    if (slot < 0 || slot >= kTSlots || !ms || !t.created || !t.recorded[slot]) return -1;
+    if (hipEventSynchronize(t.ev[slot][1]) != hipSuccess) return -5;
+    return hipEventElapsedTime(ms, t.ev[slot][0], t.ev[slot][1]) == hipSuccess ? 0 : -5;
+}
+
 }  // namespace sparcml

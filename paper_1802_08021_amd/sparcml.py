@@ -64,12 +64,31 @@ def lib() -> ctypes.CDLL:
     L.sparcml_sparse_reduce.restype = i32
     L.sparcml_densify.argtypes = [ctypes.POINTER(Stream), u64, vp, vp]
     L.sparcml_densify.restype = i32
+    L.sparcml_timing_enable.argtypes = [i32]
+    L.sparcml_timing_enable.restype = i32
+    L.sparcml_timing_read.argtypes = [i32, ctypes.POINTER(ctypes.c_float)]
+    L.sparcml_timing_read.restype = i32
     L.sparcml_strerror.argtypes = [i32]
     L.sparcml_strerror.restype = ctypes.c_char_p
     L.sparcml_last_error.argtypes = []
     L.sparcml_last_error.restype = ctypes.c_char_p
     _lib = L
     return L
+
+
+TIMER_REDUCE_PASS, TIMER_REDUCE_WRITE, TIMER_REDUCE_SLOW = 0, 1, 2
+TIMER_QUANT_NORM, TIMER_QUANT_CODES, TIMER_TOPK_SELECT, TIMER_TOPK_WRITE, TIMER_DENSIFY = 3, 4, 5, 6, 7
+
+
+def timing_enable(on: bool) -> None:
+    lib().sparcml_timing_enable(1 if on else 0)
+
+
+def timing_read(group: int):
+    """Duration (ms) of the last launch of a kernel group, or None."""
+    ms = ctypes.c_float(0.0)
+    rc = lib().sparcml_timing_read(group, ctypes.byref(ms))
+    return float(ms.value) if rc == OK else None
 
 
 def strerror(status: int) -> str:
@@ -251,3 +270,92 @@ def densify(idx, val, N: int, codes=None, scale=None, qbits: int = 0):
     out = torch.empty(N, dtype=torch.float32, device=dev)
     _check(lib().sparcml_densify(ctypes.byref(s), N, _ptr(out), _stream_ptr(dev)), "sparcml_densify")
     return out
+
+
+# ---------------------------------------------------------------------------
+# Prepared calls: descriptors and buffers built once, each run() is a single
+# C-ABI call (used by the benchmark so that Python marshalling stays out of
+# the timed loop).
+
+class QuantizeCall:
+    """Repeated QSGD of fixed device arrays into fixed code buffers."""
+
+    def __init__(self, vals, codes, scale, bits: int, seed: int, deq=None):
+        self.P = len(vals)
+        self.bits, self.seed = bits, seed & (2**64 - 1)
+        self.dev = vals[0].device
+        self.arr = (Stream * self.P)()
+        for r, v in enumerate(vals):
+            _require_cuda(v, f"vals[{r}]")
+            self.arr[r] = Stream(None, _ptr(v), None, None, v.numel(), 0, 0)
+        self.qptr = (ctypes.c_void_p * self.P)(*[_ptr(c) for c in codes])
+        self.dptr = (ctypes.c_void_p * self.P)(*[_ptr(d) for d in deq]) if deq else None
+        self.scale = scale
+        nbytes = workspace_size(OP_QUANTIZE, self.P, 1, max(v.numel() for v in vals))
+        self.ws = alloc_workspace(nbytes, self.dev)
+        self._keep = (vals, codes, deq)
+
+    def run(self) -> None:
+        _check(lib().sparcml_quantize(
+            self.P, self.arr, self.bits, self.seed, ctypes.cast(self.qptr, ctypes.c_void_p),
+            _ptr(self.scale), ctypes.cast(self.dptr, ctypes.c_void_p) if self.dptr else None,
+            _ptr(self.ws), self.ws.numel(), _stream_ptr(self.dev)), "sparcml_quantize")
+
+
+class ReduceCall:
+    """Repeated sparse reduce of fixed device streams into fixed outputs."""
+
+    def __init__(self, idx, N: int, delta: float, vals=None, codes=None, scales=None,
+                 qbits: int = 0, node_info: bool = False):
+        self.P = len(idx)
+        self.N, self.delta = N, float(delta)
+        self.dev = idx[0].device
+        torch = _torch()
+        if qbits:
+            self.arr = make_streams(idx, codes=codes, scales=[scales[r: r + 1] for r in range(self.P)],
+                                    qbits=qbits)
+        else:
+            self.arr = make_streams(idx, vals)
+        nnz = [t.numel() for t in idx]
+        thr = int(self.delta * float(N) // 1)
+        cap = max(1, min(thr, sum(nnz)) if self.P > 1 else max(nnz[0], 1))
+        self.out_idx = torch.empty(cap, dtype=torch.int32, device=self.dev)
+        self.out_val = torch.empty(N, dtype=torch.float32, device=self.dev)
+        self.node_nnz = self.node_dense = None
+        if node_info and self.P > 1:
+            self.node_nnz = torch.empty(self.P - 1, dtype=torch.int64, device=self.dev)
+            self.node_dense = torch.empty(self.P - 1, dtype=torch.uint8, device=self.dev)
+        nbytes = workspace_size(OP_REDUCE, self.P, N, max(nnz), self.delta)
+        self.ws = alloc_workspace(nbytes, self.dev)
+        self.out = Stream(_ptr(self.out_idx), _ptr(self.out_val), None, None, self.out_idx.numel(), 0, 0)
+        self._keep = (idx, vals, codes, scales)
+
+    def run(self):
+        """Returns (nnz, dense)."""
+        self.out.nnz = self.out_idx.numel()
+        _check(lib().sparcml_sparse_reduce(
+            self.P, self.arr, self.N, self.delta, ctypes.byref(self.out), _ptr(self.node_nnz),
+            _ptr(self.node_dense), _ptr(self.ws), self.ws.numel(), _stream_ptr(self.dev)),
+            "sparcml_sparse_reduce")
+        return int(self.out.nnz), bool(self.out.is_dense)
+
+
+class TopkCall:
+    """Repeated top-k of a fixed device matrix into fixed outputs."""
+
+    def __init__(self, x, k: int, residual=None):
+        torch = _torch()
+        _require_cuda(x, "x")
+        self.x, self.k = x, k
+        self.P, self.N = x.shape
+        self.idx = torch.empty((self.P, max(k, 1)), dtype=torch.int32, device=x.device)
+        self.val = torch.empty((self.P, max(k, 1)), dtype=torch.float32, device=x.device)
+        self.res_ptr = _ptr(residual) if residual is not None else 0
+        nbytes = workspace_size(OP_TOPK, self.P, self.N, k)
+        self.ws = alloc_workspace(nbytes, x.device)
+        self._keep = residual
+
+    def run(self) -> None:
+        _check(lib().sparcml_topk_sparsify(
+            self.P, _ptr(self.x), self.N, self.k, _ptr(self.idx), _ptr(self.val), self.res_ptr,
+            _ptr(self.ws), self.ws.numel(), _stream_ptr(self.x.device)), "sparcml_topk_sparsify")
