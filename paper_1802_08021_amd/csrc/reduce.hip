@@ -28,6 +28,7 @@
 #include "qsgd_device.h"
 
 #include <algorithm>
+#include <cmath>
 
 namespace sparcml {
 namespace {
@@ -52,11 +53,13 @@ constexpr int kSlowTS = 1024;    // coordinates per slow-path sub-tile
 template <int MW>
 struct Shape {
     static constexpr int NT = 256, NW = 4;
-    static constexpr int TMAX = 4096 / MW;
+    static constexpr int TMAX = MW <= 2 ? 2048 : 4096 / MW;
     static constexpr int LMAX = MW == 1 ? 5 : (MW == 2 ? 6 : (MW == 4 ? 7 : 8));
     static constexpr int PMAX = 32 * MW;
-    static constexpr int CAP = 2048;
     static constexpr int SLOTS = PMAX / 2 / NW;  // rank pairs per wave
+    // per tile: values past the second of an index, and rank-ordered values
+    // of indices with five or more ranks
+    static constexpr uint32_t OVCAP = TMAX / 2, BINCAP = TMAX / 2;
 };
 constexpr uint32_t kHalf = 32;  // window per rank per tile
 
@@ -163,38 +166,51 @@ __device__ void flush_counts(uint32_t* E, const Args& a)
 // ------------------------------------------------------------------------
 // Fast tile pass.  One workgroup walks a chunk of consecutive tiles of T
 // indices.  Per tile:
-//   A  each wave reads a 32-entry window of two ranks per 64-lane load and
-//      counts, by ballot, how many fall in the tile;
-//   B  the entries are compacted into LDS (rank-major) and their rank bits
-//      set in the per-index masks;
-//   2  per index: ranks present (popcount), exclusive scan -> where each
-//      index's values start, in rank order;
-//   3  per entry: value placed at its index's start plus the number of lower
-//      ranks present; entries with a predecessor counted by split level;
-//   4  per thread: a flat walk over its indices' values, summing each index
-//      with the tree's association, then one write of the tile.
-// Tiles where a rank fills its window or with more than CAP entries go to
-// the slow pass.
+//   1  insertion -- each wave holds a 32-entry window of two ranks per 64-lane
+//      register (prefetched during the previous tile); every entry inside
+//      the tile sets its rank bit in the index's mask and takes an arrival
+//      number; the first two values of an index go to a pair slot, later
+//      ones to an overflow chain.  All atomics of all windows are issued
+//      before any result is used (lanes outside the tile hit per-lane dummy
+//      words), so their latencies overlap;
+//   2  per index (thread t owns indices q*NT + t): with at most two ranks the
+//      sum needs no ordering (v0 + v1 is commutative) and is written here;
+//   3  three or four ranks: values sorted by rank in registers and summed
+//      with the tree's association, which for a sorted run of ranks is
+//      decided by the separators (highest differing bit of neighbours): the
+//      largest separator is the top split;
+//   4  five or more ranks: values placed in rank order (popcount of the lower
+//      rank bits) and summed by a stack keyed by separator level.
+// Union sizes of the tree nodes are counted on the side: an entry whose
+// predecessor (next lower rank present at the index) first differs from it
+// at bit h opens a group at levels 1..h; one without predecessor opens a
+// group at every level.  Tiles whose overflow values or rank-ordered values
+// would not fit go to the slow pass.
 template <int MW, int MODE, bool QUANT>
 __global__ void __launch_bounds__(256) k_tiles(Args a)
 {
     using S = Shape<MW>;
     constexpr int NT = S::NT, NW = S::NW, TMAX = S::TMAX, LMAX = S::LMAX, PMAX = S::PMAX;
-    constexpr int CAP = S::CAP, SLOTS = S::SLOTS, CPTMAX = TMAX / NT;
-    __shared__ uint4 s_mask4[TMAX * MW / 4];
-    __shared__ uint32_t s_ent[2 * CAP];  // [0,CAP): index<<8 | rank; [CAP,2CAP): value bits
-    __shared__ float s_vals[MODE == kCount ? 1 : CAP];
-    __shared__ uint16_t s_bin[MODE == kCount ? 1 : TMAX];
+    constexpr int SLOTS = S::SLOTS, CPTMAX = TMAX / NT;
+    constexpr uint32_t OVCAP = S::OVCAP, BINCAP = S::BINCAP;
+    constexpr uint32_t kNone = 0xFFFFu;
+    __shared__ uint4 s_mask4[(TMAX + 64) * MW / 4];  // + one dummy index per lane
+    __shared__ uint32_t s_cnt[TMAX + 64];  // arrivals (low 16 bits); sparse position (high)
+    __shared__ float2 s_pv[TMAX];          // first two values
+    __shared__ uint32_t s_pr[TMAX];        // their ranks: r0 | r1 << 8
+    __shared__ uint32_t s_head[TMAX];      // overflow chain head
+    __shared__ uint2 s_ov[OVCAP];          // {value bits, rank | next << 16}
+    __shared__ float s_bins[MODE == kCount ? 1 : BINCAP];
+    __shared__ uint32_t s_list[TMAX];      // [0, nA): 3-4 ranks; from the top: 5+ ranks
     __shared__ uint32_t s_E[MODE == kSparseWrite ? 1 : PMAX * (LMAX + 1)];
-    __shared__ uint32_t s_cur[PMAX], s_end[PMAX], s_cnt[PMAX], s_last[PMAX];
+    __shared__ uint32_t s_rcnt[PMAX];
+    __shared__ uint32_t s_cur[PMAX], s_end[PMAX], s_last[PMAX];
     __shared__ g_u32* s_ip[PMAX];
-    __shared__ g_u32* s_vp[PMAX];  // fp32 bits, or packed codes (byte-addressed)
+    __shared__ g_u32* s_vp[PMAX];
     __shared__ float s_unit[QUANT ? PMAX : 1];
     __shared__ uint32_t s_wsum[CPTMAX * NW];
-    __shared__ uint32_t s_slow;
+    __shared__ uint32_t s_ovn, s_bsum, s_nA, s_nB, s_binn;
     uint32_t* s_mask = reinterpret_cast<uint32_t*>(s_mask4);
-    uint32_t* s_entv = s_ent + CAP;
-    float* s_out = reinterpret_cast<float*>(s_ent);  // phase 4 only (T <= 2*CAP)
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -202,7 +218,9 @@ __global__ void __launch_bounds__(256) k_tiles(Args a)
     const uint32_t P = a.P, L = a.L, T = a.T, CPT = T / NT, W = L + 1;
     const uint32_t chunk = blockIdx.x, stride = a.nchunks + 1;
     const uint32_t t0 = chunk * a.tpc, t1 = min(t0 + a.tpc, a.ntiles);
-    const uint32_t RPL = P > 64 ? P / 64 : 1;  // ranks per lane in the rank scan
+    const uint32_t plog = a.qbits == 8u ? 0u : (a.qbits == 4u ? 1u : 2u);
+    const uint32_t cmask = QUANT ? (1u << a.qbits) - 1u : 0u;
+    const uint64_t ltmask = (1ull << lane) - 1ull;
 
     for (uint32_t r = tid; r < P; r += NT) {
         const StreamDesc* d = &a.tab[r];
@@ -220,83 +238,126 @@ __global__ void __launch_bounds__(256) k_tiles(Args a)
     }
     if (MODE != kSparseWrite)
         for (uint32_t i = tid; i < P * W; i += NT) s_E[i] = 0;
-    for (uint32_t i = tid; i < TMAX * MW / 4; i += NT) s_mask4[i] = make_uint4(0u, 0u, 0u, 0u);
+    __syncthreads();
+
+    // Window of rank r (this lane's half) starting at stream position `pos`;
+    // positions at or past `end` read as index 0xFFFFFFFF (in no tile).
+    auto load_window = [&](uint32_t r, uint32_t pos, uint32_t end, uint32_t& x, uint32_t& v) {
+        const uint32_t i = pos + sl;
+        const uint32_t ic = min(i, s_last[r]);
+        const uint32_t xi = s_ip[r][ic];
+        if (QUANT) {
+            const uint32_t byte = ((g_u8*)s_vp[r])[ic >> plog];
+            v = (byte >> ((ic & ((1u << plog) - 1u)) * a.qbits)) & cmask;
+        } else {
+            v = s_vp[r][ic];
+        }
+        x = i < end ? xi : 0xFFFFFFFFu;
+    };
+    auto value_of = [&](uint32_t vbits, uint32_t r) -> float {
+        return QUANT ? dequant(vbits, a.qbits, s_unit[r]) : __uint_as_float(vbits);
+    };
+
+    uint32_t xs[SLOTS], vs[SLOTS];
+#pragma unroll
+    for (int q = 0; q < SLOTS; ++q) {
+        const uint32_t r = 2 * (uint32_t)(wv * SLOTS + q) + half;
+        const uint32_t rr = min(r, P - 1);
+        load_window(rr, s_cur[rr], r < P ? s_end[rr] : 0u, xs[q], vs[q]);
+    }
 
     for (uint32_t tile = t0; tile < t1; ++tile) {
         const uint32_t tlo = tile * T;
         const uint32_t thi = (uint32_t)min((uint64_t)tlo + T, (uint64_t)a.N);
-        __syncthreads();
-        if (tid == 0) s_slow = 0;
 
-        // A: windows of two ranks per load.  Straight-line code: every load
-        // is issued before any is used (ranks past P read rank P-1 and are
-        // masked out afterwards).
-        uint32_t xs[SLOTS], vs[SLOTS], okbits = 0;
+        // Reset this thread's indices and the tile counters once every reader
+        // of the previous tile is done.
+        __syncthreads();
+        for (uint32_t k = 0; k < CPT; ++k) {
+            const uint32_t j = k * NT + tid;
+            clear_mask<MW>(s_mask, j);
+            s_cnt[j] = 0u;
+            s_pr[j] = 0u;
+            s_head[j] = kNone;
+        }
+        if (tid == 0) {
+            s_ovn = 0;
+            s_bsum = 0;
+            s_nA = 0;
+            s_nB = 0;
+            s_binn = 0;
+        }
+        __syncthreads();
+
+        // 1: insertion.  Sweep A issues every atomic; sweep B stores values.
+        uint32_t arr[SLOTS], inb = 0;
 #pragma unroll
         for (int q = 0; q < SLOTS; ++q) {
-            const uint32_t r = 2 * (uint32_t)(wv * SLOTS + q) + half;
-            const uint32_t rr = min(r, P - 1);
-            const uint32_t i = s_cur[rr] + sl;
-            const uint32_t ic = min(i, s_last[rr]);
-            xs[q] = s_ip[rr][ic];
-            if (QUANT) {
-                const uint32_t plog = a.qbits == 8u ? 0u : (a.qbits == 4u ? 1u : 2u);
-                const uint32_t byte = ((g_u8*)s_vp[rr])[ic >> plog];
-                vs[q] = (byte >> ((ic & ((1u << plog) - 1u)) * a.qbits)) & ((1u << a.qbits) - 1u);
+            const uint32_t u = (uint32_t)(wv * SLOTS + q);
+            const uint32_t r = 2 * u + half;
+            const bool in = 2 * u < P && xs[q] >= tlo && xs[q] < thi;
+            const uint32_t j = in ? xs[q] - tlo : (uint32_t)TMAX + (uint32_t)lane;
+            atomicOr(&s_mask[j * MW + (r >> 5)], 1u << (r & 31u));
+            arr[q] = atomicAdd(&s_cnt[j], 1u);
+            inb |= (uint32_t)in << q;
+        }
+        auto store_value = [&](uint32_t j, uint32_t r, uint32_t k, float v) {
+            if (k < 2u) {
+                if (k == 0u) s_pv[j].x = v;
+                else s_pv[j].y = v;
+                atomicOr(&s_pr[j], r << (8u * k));
             } else {
-                vs[q] = s_vp[rr][ic];
+                const uint32_t o = atomicAdd(&s_ovn, 1u);
+                if (o < OVCAP) {
+                    const uint32_t prev = atomicExch(&s_head[j], o);
+                    s_ov[o] = make_uint2(__float_as_uint(v), r | (prev << 16));
+                }
             }
-            okbits |= (uint32_t)(r < P && i < s_end[rr]) << q;
-        }
-        uint32_t inbits = 0;
+        };
 #pragma unroll
         for (int q = 0; q < SLOTS; ++q) {
-            const bool in = ((okbits >> q) & 1u) && xs[q] >= tlo && xs[q] < thi;
-            inbits |= (uint32_t)in << q;
-            const uint64_t bal = __ballot(in);
-            const uint32_t c = (uint32_t)__popc((uint32_t)(bal >> (32 * half)));
-            if (sl == 0) {
-                s_cnt[2 * (uint32_t)(wv * SLOTS + q) + half] = c;
-                if (c == kHalf) s_slow = 1u;
+            if ((inb >> q) & 1u) {
+                const uint32_t r = 2 * (uint32_t)(wv * SLOTS + q) + half;
+                store_value(xs[q] - tlo, r, arr[q], value_of(vs[q], r));
+            }
+        }
+        // Counts, the rare continuation of a window that was entirely inside
+        // the tile, and the prefetch of the next tile's windows.
+#pragma unroll
+        for (int q = 0; q < SLOTS; ++q) {
+            const uint32_t u = (uint32_t)(wv * SLOTS + q);
+            if (2 * u < P) {
+                const uint32_t r = 2 * u + half;
+                const uint64_t bal = __ballot((inb >> q) & 1u);
+                uint32_t n = (uint32_t)__popc((uint32_t)(bal >> (32 * half)));
+                const uint32_t end = s_end[r];
+                uint32_t pos = s_cur[r];
+                bool more = n == kHalf;
+                while (__ballot(more)) {
+                    uint32_t x = 0xFFFFFFFFu, v = 0u;
+                    if (more) load_window(r, pos + n, end, x, v);
+                    const bool in = more && x >= tlo && x < thi;
+                    if (in) {
+                        const uint32_t j = x - tlo;
+                        atomicOr(&s_mask[j * MW + (r >> 5)], 1u << (r & 31u));
+                        const uint32_t k = atomicAdd(&s_cnt[j], 1u);
+                        store_value(j, r, k, value_of(v, r));
+                    }
+                    const uint64_t b2 = __ballot(in);
+                    const uint32_t c = (uint32_t)__popc((uint32_t)(b2 >> (32 * half)));
+                    n += c;
+                    more = more && c == kHalf;
+                }
+                pos += n;
+                if (sl == 0) {
+                    s_cur[r] = pos;
+                    s_rcnt[r] = n;
+                }
+                load_window(r, pos, end, xs[q], vs[q]);
             }
         }
         __syncthreads();
-
-        // Every wave scans the per-rank counts itself (RPL ranks per lane).
-        uint32_t lsum = 0;
-        for (uint32_t k = 0; k < RPL; ++k) {
-            const uint32_t r = (uint32_t)lane * RPL + k;
-            lsum += r < P ? s_cnt[r] : 0u;
-        }
-        uint32_t lincl = lsum;
-#pragma unroll
-        for (int o = 1; o < 64; o <<= 1) {
-            const uint32_t y = __shfl_up(lincl, o);
-            if (lane >= o) lincl += y;
-        }
-        const uint32_t total = __shfl(lincl, 63);
-        const uint32_t lexcl = lincl - lsum;
-
-        if (s_slow || total > (uint32_t)CAP) {
-            // Defer the tile and move every cursor past it (a rank may hold
-            // more than one window's worth of entries here).
-            for (int k = 0; k < 2 * SLOTS; ++k) {
-                const uint32_t r = (uint32_t)(wv * 2 * SLOTS + k);
-                if (r >= P) break;
-                uint32_t n = s_cnt[r];
-                if (n == kHalf) {
-                    g_u32* idx = s_ip[r];
-                    const uint32_t base = s_cur[r], end = s_end[r];
-                    for (;;) {
-                        const uint32_t i = base + n + lane;
-                        const bool in = i < end && idx[i] < thi;
-                        const uint32_t c = (uint32_t)__popcll(__ballot(in));
-                        n += c;
-                        if (c < 64) break;
-                    }
-                }
-                if (lane == 0) s_cur[r] += n;
-            }
+        if (s_ovn > OVCAP) {
             if (tid == 0) {
                 const uint32_t k = atomicAdd(a.slow_count, 1u);
                 a.slow_list[k] = tile;
@@ -304,56 +365,31 @@ __global__ void __launch_bounds__(256) k_tiles(Args a)
             continue;
         }
 
-        // B: compact the entries (rank-major) and set the rank bits.
-#pragma unroll
-        for (int q = 0; q < SLOTS; ++q) {
-            const uint32_t u = (uint32_t)(wv * SLOTS + q);
-            if (2 * u < P) {
-                const uint32_t r = 2 * u + half;
-                const uint32_t lr = r / RPL;
-                uint32_t base = __shfl(lexcl, (int)lr);
-                for (uint32_t k = lr * RPL; k < r; ++k) base += s_cnt[k];
-                if ((inbits >> q) & 1u) {
-                    const uint32_t j = xs[q] - tlo;
-                    s_ent[base + sl] = (j << 8) | r;
-                    s_entv[base + sl] = vs[q];
-                    atomicOr(&s_mask[j * MW + (r >> 5)], 1u << (r & 31u));
-                }
-            }
-        }
-        if (MODE != kSparseWrite)
-            for (uint32_t r = tid; r < P; r += NT) s_E[r * W + L] += s_cnt[r];
-        for (uint32_t r = tid; r < P; r += NT) s_cur[r] += s_cnt[r];
-        __syncthreads();
-
-        // 2: ranks per index.  Thread t owns indices q*NT + t (q < CPT), so
-        // per-lane LDS accesses are consecutive (no bank conflicts) and the
-        // dense write coalesces.  Exclusive scan over indices in order: one
-        // wave scan per round q, the wave totals of all rounds exchanged
-        // through LDS at once; packed (entries low 16 bits, non-empty high).
-        uint32_t pk[CPTMAX], ex[CPTMAX];
+        // 2a: ranks per index; non-empty indices counted in index order; the
+        // 5+ rank indices' value count checked against the bin capacity.
+        uint32_t ms[CPTMAX], nzb[CPTMAX];
 #pragma unroll
         for (int q = 0; q < CPTMAX; ++q) {
-            pk[q] = 0;
-            ex[q] = 0;
+            ms[q] = 0;
+            nzb[q] = 0;
             if ((uint32_t)q < CPT) {
-                uint32_t w[MW];
-                load_mask<MW>(s_mask, (uint32_t)q * NT + tid, w);
-                uint32_t m = 0;
-#pragma unroll
-                for (int k = 0; k < MW; ++k) m += __popc(w[k]);
-                pk[q] = m | ((m != 0u) << 16);
-                uint32_t incl = pk[q];
-#pragma unroll
-                for (int o = 1; o < 64; o <<= 1) {
-                    const uint32_t y = __shfl_up(incl, o);
-                    if (lane >= o) incl += y;
-                }
-                ex[q] = incl - pk[q];
-                if (lane == 63) s_wsum[q * NW + wv] = incl;
+                ms[q] = s_cnt[(uint32_t)q * NT + tid] & 0xFFFFu;
+                const uint64_t b = __ballot(ms[q] != 0u);
+                nzb[q] = (uint32_t)__popcll(b & ltmask);
+                if (lane == 0) s_wsum[q * NW + wv] = (uint32_t)__popcll(b);
+                if (ms[q] >= 5u) atomicAdd(&s_bsum, ms[q]);
             }
         }
         __syncthreads();
+        if (s_bsum > BINCAP) {
+            if (tid == 0) {
+                const uint32_t k = atomicAdd(a.slow_count, 1u);
+                a.slow_list[k] = tile;
+            }
+            continue;
+        }
+        if (MODE != kSparseWrite)
+            for (uint32_t r = tid; r < P; r += NT) s_E[r * W + L] += s_rcnt[r];
         uint32_t run = 0;
 #pragma unroll
         for (int q = 0; q < CPTMAX; ++q) {
@@ -361,127 +397,198 @@ __global__ void __launch_bounds__(256) k_tiles(Args a)
                 uint32_t before = 0, rtot = 0;
 #pragma unroll
                 for (int w = 0; w < NW; ++w) {
-                    const uint32_t v = s_wsum[q * NW + w];
-                    if (w < wv) before += v;
-                    rtot += v;
+                    const uint32_t c = s_wsum[q * NW + w];
+                    if (w < wv) before += c;
+                    rtot += c;
                 }
-                ex[q] += run + before;
+                nzb[q] += run + before;
                 run += rtot;
-                if (MODE != kCount) s_bin[(uint32_t)q * NT + tid] = (uint16_t)(ex[q] & 0xFFFFu);
             }
         }
-        if (MODE != kSparseWrite && tid == 0) a.tile_cnt[tile] = run >> 16;
-        __syncthreads();
+        if (MODE != kSparseWrite && tid == 0) a.tile_cnt[tile] = run;
 
-        // 3: per entry -- rank-ordered placement and split-level counts.
-        for (uint32_t e = tid; e < total; e += NT) {
-            const uint32_t ent = s_ent[e];
-            const uint32_t r = ent & 0xFFu, j = ent >> 8;
+        // 2b: at most two ranks: finish here; more: to the lists.
+        const uint32_t toff = MODE == kSparseWrite ? a.tile_off[tile] : 0u;
+#pragma unroll
+        for (int q = 0; q < CPTMAX; ++q) {
+            if ((uint32_t)q < CPT) {
+                const uint32_t j = (uint32_t)q * NT + tid;
+                const uint32_t m = ms[q];
+                if (m == 2u && MODE != kSparseWrite) {
+                    const uint32_t pr = s_pr[j];
+                    const uint32_t r0 = pr & 0xFFu, r1 = (pr >> 8) & 0xFFu;
+                    atomicAdd(&s_E[max(r0, r1) * W + (31u - (uint32_t)__clz(r0 ^ r1))], 1u);
+                }
+                if (MODE != kCount) {
+                    float sum = 0.0f;
+                    if (m != 0u && m <= 2u) {
+                        const float2 pv = s_pv[j];
+                        sum = m == 1u ? pv.x : pv.x + pv.y;
+                    }
+                    if (MODE == kDense) {
+                        if (m <= 2u && (uint64_t)tlo + j < thi) a.out_val[(uint64_t)tlo + j] = m ? sum + 0.0f : 0.0f;
+                    } else if (m != 0u && m <= 2u) {
+                        a.out_idx[toff + nzb[q]] = tlo + j;
+                        a.out_val[toff + nzb[q]] = sum;
+                    }
+                }
+                const bool la = m == 3u || m == 4u, lb = m >= 5u;
+                const uint64_t ba = __ballot(la), bb = __ballot(lb);
+                uint32_t pa = 0, pb = 0;
+                if (lane == 0) {
+                    if (ba) pa = atomicAdd(&s_nA, (uint32_t)__popcll(ba));
+                    if (bb) pb = atomicAdd(&s_nB, (uint32_t)__popcll(bb));
+                }
+                pa = __shfl(pa, 0) + (uint32_t)__popcll(ba & ltmask);
+                pb = __shfl(pb, 0) + (uint32_t)__popcll(bb & ltmask);
+                const uint32_t item = j | (nzb[q] << 16);
+                if (la) s_list[pa] = item;
+                if (lb) s_list[(uint32_t)TMAX - 1u - pb] = item;
+            }
+        }
+        __syncthreads();
+        const uint32_t nA = s_nA, nB = s_nB;
+
+        // 3: three or four ranks, in registers.
+        for (uint32_t wi = tid; wi < nA; wi += NT) {
+            const uint32_t item = s_list[wi];
+            const uint32_t j = item & 0xFFFFu;
+            const uint32_t m = s_cnt[j] & 0xFFFFu;
+            const uint32_t pr = s_pr[j];
+            uint32_t rk[4];
+            float vv[4];
+            rk[0] = pr & 0xFFu;
+            rk[1] = (pr >> 8) & 0xFFu;
+            if (MODE != kCount) {
+                const float2 pv = s_pv[j];
+                vv[0] = pv.x;
+                vv[1] = pv.y;
+            } else {
+                vv[0] = vv[1] = 0.0f;
+            }
+            const uint2 o2 = s_ov[s_head[j]];
+            rk[2] = o2.y & 0xFFFFu;
+            vv[2] = __uint_as_float(o2.x);
+            rk[3] = 0x100u;  // sentinel above every rank
+            vv[3] = 0.0f;
+            if (m == 4u) {
+                const uint2 o3 = s_ov[o2.y >> 16];
+                rk[3] = o3.y & 0xFFFFu;
+                vv[3] = __uint_as_float(o3.x);
+            }
+            auto cswap = [&](int x, int y) {
+                const bool s = rk[x] > rk[y];
+                const uint32_t tr = rk[x];
+                const float tv = vv[x];
+                rk[x] = s ? rk[y] : rk[x];
+                rk[y] = s ? tr : rk[y];
+                vv[x] = s ? vv[y] : vv[x];
+                vv[y] = s ? tv : vv[y];
+            };
+            cswap(0, 1);
+            cswap(2, 3);
+            cswap(0, 2);
+            cswap(1, 3);
+            cswap(1, 2);
+            const uint32_t c1 = 31u - (uint32_t)__clz(rk[0] ^ rk[1]);
+            const uint32_t c2 = 31u - (uint32_t)__clz(rk[1] ^ rk[2]);
+            if (MODE != kSparseWrite) {
+                atomicAdd(&s_E[rk[1] * W + c1], 1u);
+                atomicAdd(&s_E[rk[2] * W + c2], 1u);
+            }
+            uint32_t c3 = 0;
+            if (m == 4u) {
+                c3 = 31u - (uint32_t)__clz(rk[2] ^ rk[3]);
+                if (MODE != kSparseWrite) atomicAdd(&s_E[rk[3] * W + c3], 1u);
+            }
+            if (MODE != kCount) {
+                float sum;
+                const float t012 = c1 < c2 ? (vv[0] + vv[1]) + vv[2] : vv[0] + (vv[1] + vv[2]);
+                if (m == 3u) {
+                    sum = t012;
+                } else if (c2 > c1 && c2 > c3) {
+                    sum = (vv[0] + vv[1]) + (vv[2] + vv[3]);
+                } else if (c1 > c3) {
+                    sum = vv[0] + (c2 < c3 ? (vv[1] + vv[2]) + vv[3] : vv[1] + (vv[2] + vv[3]));
+                } else {
+                    sum = t012 + vv[3];
+                }
+                if (MODE == kDense) {
+                    a.out_val[(uint64_t)tlo + j] = sum + 0.0f;
+                } else {
+                    a.out_idx[toff + (item >> 16)] = tlo + j;
+                    a.out_val[toff + (item >> 16)] = sum;
+                }
+            }
+        }
+
+        // 4: five or more ranks: rank-ordered values, stack walk.
+        for (uint32_t wi = tid; wi < nB; wi += NT) {
+            const uint32_t item = s_list[(uint32_t)TMAX - 1u - wi];
+            const uint32_t j = item & 0xFFFFu;
+            const uint32_t m = s_cnt[j] & 0xFFFFu;
             uint32_t w[MW];
             load_mask<MW>(s_mask, j, w);
-            const uint32_t rw = r >> 5, lowbits = (1u << (r & 31u)) - 1u;
+            uint32_t start = 0;
             if (MODE != kCount) {
-                uint32_t below = 0;
+                start = atomicAdd(&s_binn, m);
+                auto place = [&](uint32_t r, float v) {
+                    const uint32_t rw = r >> 5, low = (1u << (r & 31u)) - 1u;
+                    uint32_t below = 0;
 #pragma unroll
-                for (int k = 0; k < MW; ++k)
-                    below += (uint32_t)k < rw ? __popc(w[k])
-                                              : ((uint32_t)k == rw ? __popc(w[k] & lowbits) : 0u);
-                const uint32_t vb = s_entv[e];
-                const float v = QUANT ? dequant(vb, a.qbits, s_unit[r]) : __uint_as_float(vb);
-                s_vals[s_bin[j] + below] = v;
-            }
-            if (MODE != kSparseWrite) {
-                int prev = -1;
-#pragma unroll
-                for (int k = MW - 1; k >= 0; --k) {
-                    const uint32_t cand = (uint32_t)k < rw ? w[k]
-                                                           : ((uint32_t)k == rw ? (w[k] & lowbits) : 0u);
-                    if (prev < 0 && cand) prev = k * 32 + 31 - (int)__clz(cand);
+                    for (int k = 0; k < MW; ++k)
+                        below += (uint32_t)k < rw ? __popc(w[k]) : ((uint32_t)k == rw ? __popc(w[k] & low) : 0u);
+                    s_bins[start + below] = v;
+                };
+                const float2 pv = s_pv[j];
+                const uint32_t pr = s_pr[j];
+                place(pr & 0xFFu, pv.x);
+                place((pr >> 8) & 0xFFu, pv.y);
+                for (uint32_t o = s_head[j]; o != kNone;) {
+                    const uint2 it = s_ov[o];
+                    place(it.y & 0xFFFFu, __uint_as_float(it.x));
+                    o = it.y >> 16;
                 }
-                if (prev >= 0) atomicAdd(&s_E[r * W + (31u - (uint32_t)__clz(r ^ (uint32_t)prev))], 1u);
             }
-        }
-        __syncthreads();
-        if (MODE == kCount) {
-            for (uint32_t q = 0; q < CPT; ++q) clear_mask<MW>(s_mask, q * NT + tid);
-            continue;
-        }
-
-        // 4: flat walk over this thread's entries, index by index (q order),
-        // summing each index's values with the tree's association.
-        uint32_t nent = 0;
+            float slot[LMAX];
 #pragma unroll
-        for (int q = 0; q < CPTMAX; ++q) nent += pk[q] & 0xFFFFu;
-        if (MODE == kDense)
-            for (uint32_t q = 0; q < CPT; ++q) s_out[q * NT + tid] = 0.0f;
-        uint32_t q = 0, bits[MW];
-        load_mask<MW>(s_mask, tid, bits);
-        uint32_t pos = s_bin[tid];
-        float slot[LMAX];
-#pragma unroll
-        for (int l = 0; l < LMAX; ++l) slot[l] = 0.0f;
-        float cur = 0.0f;
-        uint32_t pend = 0;
-        int last = -1;
-        for (uint32_t it = 0; it < nent; ++it) {
-            for (;;) {  // next index with ranks left (nent guarantees one)
-                uint32_t any = 0;
-#pragma unroll
-                for (int k = 0; k < MW; ++k) any |= bits[k];
-                if (any) break;
-                ++q;
-                load_mask<MW>(s_mask, q * NT + tid, bits);
-                pos = s_bin[q * NT + tid];
-            }
-            int r = -1;
+            for (int l = 0; l < LMAX; ++l) slot[l] = 0.0f;
+            float cur = 0.0f;
+            uint32_t pend = 0, pos = start;
+            int last = -1;
 #pragma unroll
             for (int k = 0; k < MW; ++k) {
-                if (r < 0 && bits[k]) {
-                    r = k * 32 + (__ffs(bits[k]) - 1);
-                    bits[k] &= bits[k] - 1u;
+                uint32_t bits = w[k];
+                while (bits) {
+                    const int r = k * 32 + (__ffs(bits) - 1);
+                    bits &= bits - 1u;
+                    if (last >= 0) {
+                        const int sep = 31 - (int)__clz((uint32_t)(r ^ last));
+                        if (MODE != kSparseWrite) atomicAdd(&s_E[(uint32_t)r * W + (uint32_t)sep], 1u);
+                        if (MODE != kCount) {
+#pragma unroll
+                            for (int l = 0; l < LMAX; ++l)
+                                if (l < sep && ((pend >> l) & 1u)) cur = slot[l] + cur;
+                            pend = (pend & ~((1u << sep) - 1u)) | (1u << sep);
+#pragma unroll
+                            for (int l = 0; l < LMAX; ++l)
+                                if (l == sep) slot[l] = cur;
+                        }
+                    }
+                    if (MODE != kCount) cur = s_bins[pos++];
+                    last = r;
                 }
             }
-            const float v = s_vals[pos++];
-            if (last >= 0) {
-                const int sep = 31 - (int)__clz((uint32_t)(r ^ last));
-#pragma unroll
-                for (int l = 0; l < LMAX; ++l)
-                    if (l < sep && ((pend >> l) & 1u)) cur = slot[l] + cur;
-                pend = (pend & ~((1u << sep) - 1u)) | (1u << sep);
-#pragma unroll
-                for (int l = 0; l < LMAX; ++l)
-                    if (l == sep) slot[l] = cur;
-            }
-            cur = v;
-            last = r;
-            uint32_t left = 0;
-#pragma unroll
-            for (int k = 0; k < MW; ++k) left |= bits[k];
-            if (!left) {  // index q*NT + tid complete
+            if (MODE != kCount) {
 #pragma unroll
                 for (int l = 0; l < LMAX; ++l)
                     if ((pend >> l) & 1u) cur = slot[l] + cur;
-                const uint32_t j = q * NT + tid;
                 if (MODE == kDense) {
-                    s_out[j] = cur + 0.0f;
+                    a.out_val[(uint64_t)tlo + j] = cur + 0.0f;
                 } else {
-                    uint32_t nz = 0;
-#pragma unroll
-                    for (int qq = 0; qq < CPTMAX; ++qq)
-                        if ((uint32_t)qq == q) nz = ex[qq] >> 16;
-                    const uint32_t o = a.tile_off[tile] + nz;
-                    a.out_idx[o] = tlo + j;
-                    a.out_val[o] = cur;
+                    a.out_idx[toff + (item >> 16)] = tlo + j;
+                    a.out_val[toff + (item >> 16)] = cur;
                 }
-                pend = 0;
-                last = -1;
-            }
-        }
-        for (uint32_t k = 0; k < CPT; ++k) clear_mask<MW>(s_mask, k * NT + tid);
-        if (MODE == kDense) {
-            for (uint32_t k = 0; k < CPT; ++k) {
-                const uint32_t j = k * NT + tid;
-                if ((uint64_t)tlo + j < thi) a.out_val[(uint64_t)tlo + j] = s_out[j];
             }
         }
     }
@@ -768,14 +875,26 @@ int reduce_plan(int P, uint64_t N, uint64_t max_nnz, uint64_t sum_nnz, double de
     p.L = 0;
     while ((1u << p.L) < p.P) ++p.L;
     p.MW = p.P <= 32 ? 1u : p.P / 32u;
-    const uint64_t NT = 256, TMAX = 4096 / p.MW, CAP = 2048;
-    // Tile size: the largest power of two (256 .. TMAX) for which a tile
-    // holds on average at most 70% of CAP entries and a rank at most half of
-    // its 32-entry window, so that the slow pass stays rare.
-    uint64_t T = NT;
-    const double want_total = sum_nnz ? 0.7 * (double)CAP * (double)N / (double)sum_nnz : 1e30;
+    const uint64_t NT = 256;
+    const uint64_t TMAX = p.MW <= 2 ? 2048 : 4096 / p.MW;
+    // Tile size: the largest power of two (256 .. TMAX) for which, with the
+    // entries spread uniformly, a rank fills at most half of its 32-entry
+    // window and the expected overflow values, worklist indices and
+    // rank-ordered values stay under half of their per-tile capacity
+    // (Poisson model of the ranks present per index, mean lambda).
+    const double lam = (double)sum_nnz / (double)N;
+    const double e = std::exp(-lam);
+    const double p4 = 1.0 - e * (1.0 + lam + lam * lam / 2 + lam * lam * lam / 6);  // P(m >= 5)
+    const double ovf = std::max(0.0, lam - 2.0 + 2.0 * e + lam * e);              // E[(m-2)+]
+    const double bins = std::max(0.0, lam - e * lam * (1.0 + lam + lam * lam / 2 + lam * lam * lam / 6));  // E[m; m >= 5]
+    // capacities are TMAX/2 values each; aim for a quarter of TMAX in expectation
     const double want_rank = max_nnz ? 16.0 * (double)N / (double)max_nnz : 1e30;
-    while (T * 2 <= TMAX && (double)(T * 2) <= want_total && (double)(T * 2) <= want_rank) T *= 2;
+    const double want_ov = ovf > 0 ? 0.25 * (double)TMAX / ovf : 1e30;
+    const double want_bins = bins > 0 ? 0.25 * (double)TMAX / bins : 1e30;
+    (void)p4;
+    const double want = std::min(want_rank, std::min(want_ov, want_bins));
+    uint64_t T = NT;
+    while (T * 2 <= TMAX && (double)(T * 2) <= want) T *= 2;
     uint64_t Np2 = NT;
     while (Np2 < N) Np2 *= 2;
     if (T > Np2) T = Np2;
