@@ -62,7 +62,7 @@ struct Carve {
 
 // ---------------------------------------------------------------- reduce
 struct ReducePlan {
-    uint32_t P, L, MW, T, ntiles, nchunks, tiles_per_chunk, qbits;
+    uint32_t P, L, PK, T, ntiles, nchunks, tiles_per_chunk, qbits;  // PK: rank class 16/32/64/128/256
     uint64_t N, thr, sum_nnz;
     int speculate_dense;
 };

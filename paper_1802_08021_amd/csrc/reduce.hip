@@ -25,6 +25,10 @@
 // fast path's LDS budget -> decide (switch rule over the node counts) ->
 // [scan of per-tile union sizes -> SPARSE_WRITE tile and slow passes].
 #include "internal.h"
+
+#include <map>
+#include <mutex>
+#include <tuple>
 #include "qsgd_device.h"
 
 #include <algorithm>
@@ -35,33 +39,44 @@ namespace {
 
 enum Mode { kCount = 0, kDense = 1, kSparseWrite = 2 };
 
-// Pointers that live in memory (descriptor tables, LDS) are generic unless
-// marked: generic (FLAT) loads also count against the LDS wait counter and
-// would serialize the LDS work behind every HBM access.
+// Pointers that live in memory are generic unless marked: generic (FLAT)
+// loads also count against the LDS wait counter and would serialize LDS
+// work behind every HBM access.  The descriptor table is read through the
+// constant address space so that its uniform loads become scalar loads.
 typedef const uint32_t __attribute__((address_space(1))) g_u32;
 typedef const uint8_t __attribute__((address_space(1))) g_u8;
 typedef const float __attribute__((address_space(1))) g_f32;
-constexpr uint32_t kCap = 4096;  // entries per tile on the fast path
-constexpr uint32_t kWin = 64;    // entries read per rank per tile (one wave)
-constexpr int kSlowNT = 256;
-constexpr int kSlowTS = 1024;    // coordinates per slow-path sub-tile
+typedef const StreamDesc __attribute__((address_space(4)))* c_desc;
 
-// MW = 32-bit rank-mask words per coordinate = ceil(P / 32).  Every fast
-// tile kernel has 256 threads; TMAX coordinates of masks take 16 KB of LDS;
-// CAP entries per tile fit the fast path.  Ranks are read in pairs: one
-// 64-lane load covers a 32-entry window of two ranks.
+constexpr int kSlowNT = 256;
+constexpr int kSlowTS = 1024;  // coordinates per slow-path sub-tile
+
+// Tree levels for up to 32*MW ranks (slow pass).
 template <int MW>
-struct Shape {
-    static constexpr int NT = 256, NW = 4;
-    static constexpr int TMAX = MW <= 2 ? 2048 : 4096 / MW;
-    static constexpr int LMAX = MW == 1 ? 5 : (MW == 2 ? 6 : (MW == 4 ? 7 : 8));
+struct SlowShape {
     static constexpr int PMAX = 32 * MW;
-    static constexpr int SLOTS = PMAX / 2 / NW;  // rank pairs per wave
-    // per tile: values past the second of an index, and rank-ordered values
-    // of indices with five or more ranks
-    static constexpr uint32_t OVCAP = TMAX / 2, BINCAP = TMAX / 2;
+    static constexpr int LMAX = MW == 1 ? 5 : (MW == 2 ? 6 : (MW == 4 ? 7 : 8));
 };
-constexpr uint32_t kHalf = 32;  // window per rank per tile
+
+// Fast tile pass for up to PMAX ranks.  A wave owns SLMAX ranks ("slots");
+// per tile it reads a 64-entry window of each slot's stream (one entry per
+// lane).  TMAX coordinates per tile; CAP staged entries (those of indices
+// held by three or more ranks); SIDE entries of windows that had to be
+// continued because all 64 entries fell inside the tile.
+template <int PMAX>
+struct Fast {
+    static constexpr int NT = PMAX > 128 ? 512 : 256;
+    static constexpr int NW = NT / 64;
+    static constexpr int SLMAX = PMAX / NW;
+    static constexpr int TMAX = 4096;
+    static constexpr int CPTMAX = TMAX / NT;
+    static constexpr uint32_t CAP = 4096;
+    static constexpr uint32_t LCAP = CAP / 3 + 1;
+    static constexpr uint32_t SIDE = 512;
+    static constexpr int LMAX = PMAX <= 16 ? 4 : (PMAX <= 32 ? 5 : (PMAX <= 64 ? 6 : (PMAX <= 128 ? 7 : 8)));
+    static constexpr int MW = PMAX <= 32 ? 1 : PMAX / 32;
+};
+constexpr uint32_t kWin = 64;  // window entries per rank per tile
 
 struct Args {
     const StreamDesc* tab;
@@ -74,6 +89,7 @@ struct Args {
     uint32_t* out_idx;
     float* out_val;
     uint32_t P, L, N, T, ntiles, nchunks, tpc, qbits;
+    uint32_t out_vec;          // out_val is 16-byte aligned
 };
 
 __device__ __forceinline__ uint32_t lower_bound(const uint32_t* a, uint32_t lo, uint32_t hi,
@@ -85,41 +101,6 @@ __device__ __forceinline__ uint32_t lower_bound(const uint32_t* a, uint32_t lo, 
         else hi = mid;
     }
     return lo;
-}
-
-// The MW rank-mask words of index j (vector LDS access where possible).
-template <int MW>
-__device__ __forceinline__ void load_mask(const uint32_t* m, uint32_t j, uint32_t (&w)[MW])
-{
-    if constexpr (MW == 1) {
-        w[0] = m[j];
-    } else if constexpr (MW == 2) {
-        const uint2 v = reinterpret_cast<const uint2*>(m)[j];
-        w[0] = v.x;
-        w[1] = v.y;
-    } else {
-#pragma unroll
-        for (int k = 0; k < MW / 4; ++k) {
-            const uint4 v = reinterpret_cast<const uint4*>(m)[j * (MW / 4) + k];
-            w[4 * k] = v.x;
-            w[4 * k + 1] = v.y;
-            w[4 * k + 2] = v.z;
-            w[4 * k + 3] = v.w;
-        }
-    }
-}
-
-template <int MW>
-__device__ __forceinline__ void clear_mask(uint32_t* m, uint32_t j)
-{
-    if constexpr (MW == 1) {
-        m[j] = 0u;
-    } else if constexpr (MW == 2) {
-        reinterpret_cast<uint2*>(m)[j] = make_uint2(0u, 0u);
-    } else {
-#pragma unroll
-        for (int k = 0; k < MW / 4; ++k) reinterpret_cast<uint4*>(m)[j * (MW / 4) + k] = make_uint4(0u, 0u, 0u, 0u);
-    }
 }
 
 // Level t (1-based) and group g of internal node `node` in level order.
@@ -163,437 +144,528 @@ __device__ void flush_counts(uint32_t* E, const Args& a)
     }
 }
 
+// Raw buffer resource over `bytes` bytes at `base`: lanes past the end read
+// zero instead of faulting (the fourth word selects 32-bit raw accesses on
+// the gfx9 family).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_at(const void* base, uint32_t bytes)
+{
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, (int)bytes, 0x00020000);
+}
+
+// Inclusive prefix sum over the 64 lanes of a wave: shifts within rows of
+// 16 lanes, then the row broadcasts.
+__device__ __forceinline__ uint32_t wave_scan(uint32_t v)
+{
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x111, 0xF, 0xF, true);  // row_shr:1
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x112, 0xF, 0xF, true);  // row_shr:2
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x114, 0xF, 0xF, true);  // row_shr:4
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x118, 0xF, 0xF, true);  // row_shr:8
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x142, 0xA, 0xF, false); // row_bcast:15
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x143, 0xC, 0xF, false); // row_bcast:31
+    return v;
+}
+
+// Level at which ranks a != b first meet: their highest differing bit
+// (the | 1 keeps equal ranks, which valid streams never produce, in range).
+__device__ __forceinline__ uint32_t sep_level(uint32_t a, uint32_t b)
+{
+    return 31u - (uint32_t)__clz((a ^ b) | 1u);
+}
+
 // ------------------------------------------------------------------------
 // Fast tile pass.  One workgroup walks a chunk of consecutive tiles of T
-// indices.  Per tile:
-//   1  insertion -- each wave holds a 32-entry window of two ranks per 64-lane
-//      register (prefetched during the previous tile); every entry inside
-//      the tile sets its rank bit in the index's mask and takes an arrival
-//      number; the first two values of an index go to a pair slot, later
-//      ones to an overflow chain.  All atomics of all windows are issued
-//      before any result is used (lanes outside the tile hit per-lane dummy
-//      words), so their latencies overlap;
-//   2  per index (thread t owns indices q*NT + t): with at most two ranks the
-//      sum needs no ordering (v0 + v1 is commutative) and is written here;
-//   3  three or four ranks: values sorted by rank in registers and summed
-//      with the tree's association, which for a sorted run of ranks is
-//      decided by the separators (highest differing bit of neighbours): the
-//      largest separator is the top split;
-//   4  five or more ranks: values placed in rank order (popcount of the lower
-//      rank bits) and summed by a stack keyed by separator level.
-// Union sizes of the tree nodes are counted on the side: an entry whose
-// predecessor (next lower rank present at the index) first differs from it
-// at bit h opens a group at levels 1..h; one without predecessor opens a
-// group at every level.  Tiles whose overflow values or rank-ordered values
-// would not fit go to the slow pass.
-template <int MW, int MODE, bool QUANT>
-__global__ void __launch_bounds__(256) k_tiles(Args a)
+// coordinates; per tile:
+//   P1  every window entry inside the tile takes an arrival number at its
+//       coordinate (LDS atomic); the first arrival leaves its rank and
+//       value there.  A window that lies entirely inside the tile is
+//       continued (rare) into the side buffer.  The next tile's windows are
+//       then requested, so their loads overlap the rest of this tile.
+//   scan  per coordinate: m ranks; coordinates with m >= 3 get a staging
+//       range and a list slot (m = 3..4 and m >= 5 apart); non-empty ones
+//       their output position (sparse output).
+//   P2  m = 1: done (the first value stands); m = 2: the second arrival adds
+//       its value to the first -- a single addition is the same in either
+//       order -- and counts its pair for the node sizes; m >= 3: the entry
+//       is staged at its coordinate's range.
+//   walk  m = 3..4: ranks sorted in registers, sum with the association the
+//       separators dictate; m >= 5: staged entries put in rank order, then a
+//       stack keyed by separator level adds them in tree order.
+//   store (dense result) the tile leaves LDS in 16-byte stores.
+// Union sizes of the tree nodes are counted on the side (flush_counts).
+// Tiles whose staged entries, side entries or total entries exceed the LDS
+// budget are deferred to the slow pass.
+template <int PMAX, int MODE, bool QUANT>
+__global__ void __launch_bounds__(Fast<PMAX>::NT, 2) k_tiles(Args a)
 {
-    using S = Shape<MW>;
-    constexpr int NT = S::NT, NW = S::NW, TMAX = S::TMAX, LMAX = S::LMAX, PMAX = S::PMAX;
-    constexpr int SLOTS = S::SLOTS, CPTMAX = TMAX / NT;
-    constexpr uint32_t OVCAP = S::OVCAP, BINCAP = S::BINCAP;
-    constexpr uint32_t kNone = 0xFFFFu;
-    __shared__ uint4 s_mask4[(TMAX + 64) * MW / 4];  // + one dummy index per lane
-    __shared__ uint32_t s_cnt[TMAX + 64];  // arrivals (low 16 bits); sparse position (high)
-    __shared__ float2 s_pv[TMAX];          // first two values
-    __shared__ uint32_t s_pr[TMAX];        // their ranks: r0 | r1 << 8
-    __shared__ uint32_t s_head[TMAX];      // overflow chain head
-    __shared__ uint2 s_ov[OVCAP];          // {value bits, rank | next << 16}
-    __shared__ float s_bins[MODE == kCount ? 1 : BINCAP];
-    __shared__ uint32_t s_list[TMAX];      // [0, nA): 3-4 ranks; from the top: 5+ ranks
-    __shared__ uint32_t s_E[MODE == kSparseWrite ? 1 : PMAX * (LMAX + 1)];
-    __shared__ uint32_t s_rcnt[PMAX];
-    __shared__ uint32_t s_cur[PMAX], s_end[PMAX], s_last[PMAX];
-    __shared__ g_u32* s_ip[PMAX];
-    __shared__ g_u32* s_vp[PMAX];
-    __shared__ float s_unit[QUANT ? PMAX : 1];
-    __shared__ uint32_t s_wsum[CPTMAX * NW];
-    __shared__ uint32_t s_ovn, s_bsum, s_nA, s_nB, s_binn;
-    uint32_t* s_mask = reinterpret_cast<uint32_t*>(s_mask4);
+    using F = Fast<PMAX>;
+    constexpr int NT = F::NT, NW = F::NW, SLMAX = F::SLMAX, TMAX = F::TMAX, CPTMAX = F::CPTMAX;
+    constexpr uint32_t CAP = F::CAP, SIDE = F::SIDE;
+    constexpr int LMAX = F::LMAX, MW = F::MW;
+    constexpr bool VALS = MODE != kCount, CNTS = MODE != kSparseWrite;
 
-    const int tid = threadIdx.x, lane = tid & 63;
-    const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const uint32_t half = (uint32_t)lane >> 5, sl = (uint32_t)lane & 31u;
-    const uint32_t P = a.P, L = a.L, T = a.T, CPT = T / NT, W = L + 1;
+    __shared__ __align__(16) uint32_t s_cnt[TMAX];         // ranks per index; then m | aux << 9
+    __shared__ __align__(16) float s_out[VALS ? TMAX : 4];  // first value; dense: the sum
+    __shared__ uint8_t s_r0[TMAX];                         // rank of the first arrival
+    __shared__ float s_sv[VALS ? CAP : 1];                 // staged values
+    __shared__ uint8_t s_sr[CAP];                          // staged ranks
+    __shared__ uint2 s_list[F::LCAP];                      // {j | nzpos << 16, start | m << 16}
+    __shared__ uint32_t s_E[CNTS ? PMAX * (LMAX + 1) : 1];
+    __shared__ uint2 s_side[SIDE];                         // {j | r << 12 | k << 20, value}
+    __shared__ uint32_t s_wtot[2 * NW];
+    __shared__ uint32_t s_nside, s_flag, s_total;
+
+    const uint32_t tid = threadIdx.x, lane = tid & 63u;
+    const uint32_t wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const uint32_t P = a.P, L = a.L, W = L + 1, T = a.T, CPT = T / NT;
     const uint32_t chunk = blockIdx.x, stride = a.nchunks + 1;
     const uint32_t t0 = chunk * a.tpc, t1 = min(t0 + a.tpc, a.ntiles);
-    const uint32_t plog = a.qbits == 8u ? 0u : (a.qbits == 4u ? 1u : 2u);
-    const uint32_t cmask = QUANT ? (1u << a.qbits) - 1u : 0u;
-    const uint64_t ltmask = (1ull << lane) - 1ull;
+    const uint32_t SL = (P + NW - 1) / NW;
+    const uint32_t qbits = a.qbits;
+    const uint32_t plog = qbits == 8u ? 0u : (qbits == 4u ? 1u : 2u), pm = (1u << plog) - 1u;
+    const c_desc tab = (c_desc)a.tab;
 
-    for (uint32_t r = tid; r < P; r += NT) {
-        const StreamDesc* d = &a.tab[r];
-        s_cur[r] = a.off[r * stride + chunk];
-        s_end[r] = a.off[r * stride + chunk + 1];
-        // empty streams read (and discard) a word of the descriptor table
-        const bool empty = d->nnz == 0;
-        s_last[r] = empty ? 0u : (uint32_t)(d->nnz - 1);
-        const void* ip = empty ? static_cast<const void*>(a.tab) : static_cast<const void*>(d->idx);
-        const void* vp = empty ? static_cast<const void*>(a.tab)
-                               : (QUANT ? static_cast<const void*>(d->qval) : static_cast<const void*>(d->val));
-        s_ip[r] = (g_u32*)ip;
-        s_vp[r] = (g_u32*)vp;
-        if (QUANT) s_unit[r] = level_unit(*d->qscale, a.qbits);
-    }
-    if (MODE != kSparseWrite)
-        for (uint32_t i = tid; i < P * W; i += NT) s_E[i] = 0;
-    __syncthreads();
+    // Rank of slot s.  Slots past the last rank keep an empty window (their
+    // chunk end equals their position) and read rank P-1's stream harmlessly,
+    // so that every slot runs the same straight-line code.
+    auto slot_rank = [&](int s) -> uint32_t { return min(wv * SL + (uint32_t)s, P - 1u); };
+    // Per-slot scalars (descriptor fields, lane reads of the slot state) are
+    // loop invariant; left alone the compiler would hoist all of them out of
+    // the tile loop and run out of scalar registers.  An opaque copy of the
+    // slot number keeps them next to their use.
+    auto opaque = [](uint32_t v) -> uint32_t {
+        asm volatile("" : "+s"(v));
+        return v;
+    };
 
-    // Window of rank r (this lane's half) starting at stream position `pos`;
-    // positions at or past `end` read as index 0xFFFFFFFF (in no tile).
-    auto load_window = [&](uint32_t r, uint32_t pos, uint32_t end, uint32_t& x, uint32_t& v) {
-        const uint32_t i = pos + sl;
-        const uint32_t ic = min(i, s_last[r]);
-        const uint32_t xi = s_ip[r][ic];
-        if (QUANT) {
-            const uint32_t byte = ((g_u8*)s_vp[r])[ic >> plog];
-            v = (byte >> ((ic & ((1u << plog) - 1u)) * a.qbits)) & cmask;
+    // Window of rank r at stream position pos: raw index and raw value
+    // word (fp32 bits, or the byte holding the entry's code).
+    auto load_win = [&](uint32_t r, uint32_t pos, uint32_t& x, uint32_t& v) {
+        r = opaque(r);
+        const uint64_t nnz = tab[r].nnz;
+        const uint32_t rem = pos < nnz ? (uint32_t)min(nnz - pos, (uint64_t)kWin) : 0u;
+        x = __builtin_amdgcn_raw_buffer_load_b32(buffer_at(tab[r].idx + pos, rem * 4u), (int)(lane * 4u), 0, 0);
+        if (VALS) {
+            if (QUANT) {
+                const uint64_t nb = (nnz * qbits + 7u) / 8u;
+                const uint32_t b0 = pos >> plog;
+                const uint32_t remb = b0 < nb ? (uint32_t)min(nb - b0, (uint64_t)kWin) : 0u;
+                v = __builtin_amdgcn_raw_buffer_load_b8(buffer_at(tab[r].qval + b0, remb),
+                                                        (int)((lane + (pos & pm)) >> plog), 0, 0);
+            } else {
+                v = __builtin_amdgcn_raw_buffer_load_b32(buffer_at(tab[r].val + pos, rem * 4u),
+                                                         (int)(lane * 4u), 0, 0);
+            }
         } else {
-            v = s_vp[r][ic];
+            v = 0u;
         }
-        x = i < end ? xi : 0xFFFFFFFFu;
     };
-    auto value_of = [&](uint32_t vbits, uint32_t r) -> float {
-        return QUANT ? dequant(vbits, a.qbits, s_unit[r]) : __uint_as_float(vbits);
+    auto decode = [&](uint32_t v, uint32_t pos, float unit) -> float {
+        if (QUANT) {
+            const uint32_t code = (v >> (((lane + (pos & pm)) & pm) * qbits)) & ((1u << qbits) - 1u);
+            return dequant(code, qbits, unit);
+        }
+        return __uint_as_float(v);
+    };
+    auto first_arrival = [&](uint32_t j, uint32_t r, float v) {
+        s_r0[j] = (uint8_t)r;
+        if (VALS) s_out[j] = MODE == kDense ? v + 0.0f : v;
     };
 
-    uint32_t xs[SLOTS], vs[SLOTS];
-#pragma unroll
-    for (int q = 0; q < SLOTS; ++q) {
-        const uint32_t r = 2 * (uint32_t)(wv * SLOTS + q) + half;
-        const uint32_t rr = min(r, P - 1);
-        load_window(rr, s_cur[rr], r < P ? s_end[rr] : 0u, xs[q], vs[q]);
+    // Per-slot state in lanes: lane s holds slot s's stream position, chunk
+    // end, level unit and this tile's entry count.
+    uint32_t posv = 0u, endv = 0u, ntv = 0u;
+    float unitv = 0.0f;
+    if (lane < SL && wv * SL + lane < P) {
+        const uint32_t r = wv * SL + lane;
+        posv = a.off[r * stride + chunk];
+        endv = a.off[r * stride + chunk + 1];
+        if (QUANT && VALS) unitv = level_unit(*a.tab[r].qscale, qbits);
     }
+    auto rl = [&](uint32_t v, int s) -> uint32_t { return (uint32_t)__builtin_amdgcn_readlane((int)v, s); };
+
+    for (uint32_t i = tid; i < TMAX; i += NT) {
+        s_cnt[i] = 0u;
+        if (VALS) s_out[i] = 0.0f;
+    }
+    if (CNTS)
+        for (uint32_t i = tid; i < P * W; i += NT) s_E[i] = 0u;
+    if (tid == 0) {
+        s_nside = 0u;
+        s_flag = 0u;
+        s_total = 0u;
+    }
+
+    // xr: raw window index, then (entry in the tile) j | arrival << 12, or
+    // ~0 for an entry outside the tile; vr: raw value word, then the value.
+    uint32_t xr[SLMAX], vr[SLMAX];
+#pragma unroll
+    for (int s = 0; s < SLMAX; ++s) {
+        load_win(slot_rank(s), rl(posv, s), xr[s], vr[s]);
+    }
+    __syncthreads();
 
     for (uint32_t tile = t0; tile < t1; ++tile) {
         const uint32_t tlo = tile * T;
-        const uint32_t thi = (uint32_t)min((uint64_t)tlo + T, (uint64_t)a.N);
+        const uint32_t TT = (uint32_t)min((uint64_t)T, (uint64_t)a.N - tlo);  // tile width
 
-        // Reset this thread's indices and the tile counters once every reader
-        // of the previous tile is done.
-        __syncthreads();
-        for (uint32_t k = 0; k < CPT; ++k) {
-            const uint32_t j = k * NT + tid;
-            clear_mask<MW>(s_mask, j);
-            s_cnt[j] = 0u;
-            s_pr[j] = 0u;
-            s_head[j] = kNone;
-        }
-        if (tid == 0) {
-            s_ovn = 0;
-            s_bsum = 0;
-            s_nA = 0;
-            s_nB = 0;
-            s_binn = 0;
-        }
-        __syncthreads();
-
-        // 1: insertion.  Sweep A issues every atomic; sweep B stores values.
-        uint32_t arr[SLOTS], inb = 0;
+        // P1: arrival numbers, first values.
+        uint32_t full = 0u, wtot = 0u;
 #pragma unroll
-        for (int q = 0; q < SLOTS; ++q) {
-            const uint32_t u = (uint32_t)(wv * SLOTS + q);
-            const uint32_t r = 2 * u + half;
-            const bool in = 2 * u < P && xs[q] >= tlo && xs[q] < thi;
-            const uint32_t j = in ? xs[q] - tlo : (uint32_t)TMAX + (uint32_t)lane;
-            atomicOr(&s_mask[j * MW + (r >> 5)], 1u << (r & 31u));
-            arr[q] = atomicAdd(&s_cnt[j], 1u);
-            inb |= (uint32_t)in << q;
+        for (int s = 0; s < SLMAX; ++s) {
+            const int so = (int)opaque((uint32_t)s);
+            const uint32_t pos = rl(posv, so), avail = rl(endv, so) - pos;
+            const uint32_t j = xr[s] - tlo;
+            const bool in = j < TT && lane < avail;
+            uint32_t k = ~0u;
+            if (in) k = atomicAdd(&s_cnt[j], 1u);
+            if (VALS) vr[s] = __float_as_uint(decode(vr[s], pos, __uint_as_float(rl(__float_as_uint(unitv), so))));
+            const uint32_t n = (uint32_t)__popcll(__ballot(in));
+            posv = lane == (uint32_t)s ? pos + n : posv;
+            ntv = lane == (uint32_t)s ? n : ntv;
+            full |= (n == kWin ? 1u : 0u) << s;
+            wtot += n;
+            xr[s] = in ? j | k << 12 : ~0u;
         }
-        auto store_value = [&](uint32_t j, uint32_t r, uint32_t k, float v) {
-            if (k < 2u) {
-                if (k == 0u) s_pv[j].x = v;
-                else s_pv[j].y = v;
-                atomicOr(&s_pr[j], r << (8u * k));
+#pragma unroll
+        for (int s = 0; s < SLMAX; ++s)
+            if (xr[s] < (1u << 12)) first_arrival(xr[s], slot_rank(s), __uint_as_float(vr[s]));
+
+        // Windows entirely inside the tile: continue them into the side buffer.
+        while (full) {
+            const int s = __builtin_ctz(full);
+            full &= full - 1u;
+            const uint32_t r = wv * SL + (uint32_t)s;
+            const float unit = __uint_as_float(rl(__float_as_uint(unitv), s));
+            uint32_t n;
+            do {
+                const uint32_t pos = rl(posv, s), avail = rl(endv, s) - pos;
+                uint32_t x, v;
+                load_win(r, pos, x, v);
+                const uint32_t j = x - tlo;
+                const bool in = j < TT && lane < avail;
+                const uint64_t bal = __ballot(in);
+                n = (uint32_t)__popcll(bal);
+                uint32_t k = ~0u;
+                if (in) k = atomicAdd(&s_cnt[j], 1u);
+                const float val = VALS ? decode(v, pos, unit) : 0.0f;
+                uint32_t base = 0u;
+                if (lane == 0u && n) base = atomicAdd(&s_nside, n);
+                base = (uint32_t)__builtin_amdgcn_readfirstlane((int)base);
+                if (in) {
+                    if (k == 0u) first_arrival(j, r, val);
+                    const uint32_t at = base + (uint32_t)__popcll(bal & ((1ull << lane) - 1ull));
+                    if (at < SIDE) s_side[at] = make_uint2(j | r << 12 | k << 20, __float_as_uint(val));
+                }
+                if (lane == 0u && base + n > SIDE) s_flag = 1u;
+                posv = lane == (uint32_t)s ? pos + n : posv;
+                ntv = lane == (uint32_t)s ? ntv + n : ntv;
+                wtot += n;
+            } while (n == kWin);
+        }
+        if (lane == 0u && wtot) atomicAdd(&s_total, wtot);
+
+        // Request the next tile's windows.
+        uint32_t xn[SLMAX], vn[SLMAX];
+#pragma unroll
+        for (int s = 0; s < SLMAX; ++s) {
+            load_win(slot_rank(s), rl(posv, (int)opaque((uint32_t)s)), xn[s], vn[s]);
+        }
+        __syncthreads();
+
+        // Scan over this thread's CPT consecutive coordinates.
+        const uint32_t jb = tid * CPT;
+        uint32_t mc[CPTMAX];
+#pragma unroll
+        for (int c = 0; c < CPTMAX; c += 4) {
+            if ((uint32_t)c < CPT) {
+                const uint4 q = *reinterpret_cast<const uint4*>(&s_cnt[jb + c]);
+                mc[c] = q.x;
+                mc[c + 1] = q.y;
+                mc[c + 2] = q.z;
+                mc[c + 3] = q.w;
             } else {
-                const uint32_t o = atomicAdd(&s_ovn, 1u);
-                if (o < OVCAP) {
-                    const uint32_t prev = atomicExch(&s_head[j], o);
-                    s_ov[o] = make_uint2(__float_as_uint(v), r | (prev << 16));
-                }
-            }
-        };
-#pragma unroll
-        for (int q = 0; q < SLOTS; ++q) {
-            if ((inb >> q) & 1u) {
-                const uint32_t r = 2 * (uint32_t)(wv * SLOTS + q) + half;
-                store_value(xs[q] - tlo, r, arr[q], value_of(vs[q], r));
+                mc[c] = mc[c + 1] = mc[c + 2] = mc[c + 3] = 0u;
             }
         }
-        // Counts, the rare continuation of a window that was entirely inside
-        // the tile, and the prefetch of the next tile's windows.
+        uint32_t st = 0u, ne = 0u, na = 0u, nb = 0u;
 #pragma unroll
-        for (int q = 0; q < SLOTS; ++q) {
-            const uint32_t u = (uint32_t)(wv * SLOTS + q);
-            if (2 * u < P) {
-                const uint32_t r = 2 * u + half;
-                const uint64_t bal = __ballot((inb >> q) & 1u);
-                uint32_t n = (uint32_t)__popc((uint32_t)(bal >> (32 * half)));
-                const uint32_t end = s_end[r];
-                uint32_t pos = s_cur[r];
-                bool more = n == kHalf;
-                while (__ballot(more)) {
-                    uint32_t x = 0xFFFFFFFFu, v = 0u;
-                    if (more) load_window(r, pos + n, end, x, v);
-                    const bool in = more && x >= tlo && x < thi;
-                    if (in) {
-                        const uint32_t j = x - tlo;
-                        atomicOr(&s_mask[j * MW + (r >> 5)], 1u << (r & 31u));
-                        const uint32_t k = atomicAdd(&s_cnt[j], 1u);
-                        store_value(j, r, k, value_of(v, r));
-                    }
-                    const uint64_t b2 = __ballot(in);
-                    const uint32_t c = (uint32_t)__popc((uint32_t)(b2 >> (32 * half)));
-                    n += c;
-                    more = more && c == kHalf;
-                }
-                pos += n;
-                if (sl == 0) {
-                    s_cur[r] = pos;
-                    s_rcnt[r] = n;
-                }
-                load_window(r, pos, end, xs[q], vs[q]);
-            }
+        for (int c = 0; c < CPTMAX; ++c) {
+            const uint32_t m = mc[c];
+            ne += m != 0u ? 1u : 0u;
+            st += m >= 3u ? m : 0u;
+            na += m - 3u < 2u ? 1u : 0u;
+            nb += m >= 5u ? 1u : 0u;
+        }
+        const uint32_t p1 = st | ne << 16, p2 = na | nb << 16;
+        const uint32_t i1 = wave_scan(p1), i2 = wave_scan(p2);
+        if (lane == 63u) {
+            s_wtot[wv] = i1;
+            s_wtot[NW + wv] = i2;
         }
         __syncthreads();
-        if (s_ovn > OVCAP) {
+        uint32_t b1 = 0u, b2 = 0u, g1 = 0u, g2 = 0u;
+#pragma unroll
+        for (int w = 0; w < NW; ++w) {
+            const uint32_t c1 = s_wtot[w], c2 = s_wtot[NW + w];
+            if ((uint32_t)w < wv) {
+                b1 += c1;
+                b2 += c2;
+            }
+            g1 += c1;
+            g2 += c2;
+        }
+        // every entry of the tile is counted at its coordinate, so with at
+        // most 65535 of them no packed field can overflow
+        const bool defer = s_flag != 0u || s_total > 65535u || (g1 & 0xFFFFu) > CAP;
+        const uint32_t NE = g1 >> 16, NA = g2 & 0xFFFFu, NB = g2 >> 16;
+        if (!defer) {
+            if (CNTS && tid == 0) a.tile_cnt[tile] = NE;
+            const uint32_t e1 = i1 - p1 + b1, e2 = i2 - p2 + b2;
+            uint32_t srun = e1 & 0xFFFFu, nrun = e1 >> 16, arun = e2 & 0xFFFFu, brun = NA + (e2 >> 16);
+#pragma unroll
+            for (int c = 0; c < CPTMAX; ++c) {
+                if ((uint32_t)c < CPT) {
+                    const uint32_t m = mc[c], j = jb + (uint32_t)c;
+                    uint32_t aux = MODE == kSparseWrite ? nrun : 0u;
+                    if (m >= 3u) {
+                        aux = srun;
+                        const uint2 item = make_uint2(j | nrun << 16, srun | m << 16);
+                        if (m <= 4u) s_list[arun++] = item;
+                        else s_list[brun++] = item;
+                        srun += m;
+                    }
+                    nrun += m != 0u ? 1u : 0u;
+                    mc[c] = m | aux << 9;
+                }
+            }
+#pragma unroll
+            for (int c = 0; c < CPTMAX; c += 4)
+                if ((uint32_t)c < CPT)
+                    *reinterpret_cast<uint4*>(&s_cnt[jb + c]) = make_uint4(mc[c], mc[c + 1], mc[c + 2], mc[c + 3]);
+        } else {
+#pragma unroll
+            for (int c = 0; c < CPTMAX; c += 4) {
+                if ((uint32_t)c < CPT) {
+                    *reinterpret_cast<uint4*>(&s_cnt[jb + c]) = make_uint4(0u, 0u, 0u, 0u);
+                    if (VALS) *reinterpret_cast<float4*>(&s_out[jb + c]) = make_float4(0.f, 0.f, 0.f, 0.f);
+                }
+            }
             if (tid == 0) {
                 const uint32_t k = atomicAdd(a.slow_count, 1u);
                 a.slow_list[k] = tile;
             }
-            continue;
-        }
-
-        // 2a: ranks per index; non-empty indices counted in index order; the
-        // 5+ rank indices' value count checked against the bin capacity.
-        uint32_t ms[CPTMAX], nzb[CPTMAX];
-#pragma unroll
-        for (int q = 0; q < CPTMAX; ++q) {
-            ms[q] = 0;
-            nzb[q] = 0;
-            if ((uint32_t)q < CPT) {
-                ms[q] = s_cnt[(uint32_t)q * NT + tid] & 0xFFFFu;
-                const uint64_t b = __ballot(ms[q] != 0u);
-                nzb[q] = (uint32_t)__popcll(b & ltmask);
-                if (lane == 0) s_wsum[q * NW + wv] = (uint32_t)__popcll(b);
-                if (ms[q] >= 5u) atomicAdd(&s_bsum, ms[q]);
-            }
         }
         __syncthreads();
-        if (s_bsum > BINCAP) {
-            if (tid == 0) {
-                const uint32_t k = atomicAdd(a.slow_count, 1u);
-                a.slow_list[k] = tile;
-            }
-            continue;
-        }
-        if (MODE != kSparseWrite)
-            for (uint32_t r = tid; r < P; r += NT) s_E[r * W + L] += s_rcnt[r];
-        uint32_t run = 0;
-#pragma unroll
-        for (int q = 0; q < CPTMAX; ++q) {
-            if ((uint32_t)q < CPT) {
-                uint32_t before = 0, rtot = 0;
-#pragma unroll
-                for (int w = 0; w < NW; ++w) {
-                    const uint32_t c = s_wsum[q * NW + w];
-                    if (w < wv) before += c;
-                    rtot += c;
-                }
-                nzb[q] += run + before;
-                run += rtot;
-            }
-        }
-        if (MODE != kSparseWrite && tid == 0) a.tile_cnt[tile] = run;
 
-        // 2b: at most two ranks: finish here; more: to the lists.
-        const uint32_t toff = MODE == kSparseWrite ? a.tile_off[tile] : 0u;
-#pragma unroll
-        for (int q = 0; q < CPTMAX; ++q) {
-            if ((uint32_t)q < CPT) {
-                const uint32_t j = (uint32_t)q * NT + tid;
-                const uint32_t m = ms[q];
-                if (m == 2u && MODE != kSparseWrite) {
-                    const uint32_t pr = s_pr[j];
-                    const uint32_t r0 = pr & 0xFFu, r1 = (pr >> 8) & 0xFFu;
-                    atomicAdd(&s_E[max(r0, r1) * W + (31u - (uint32_t)__clz(r0 ^ r1))], 1u);
-                }
-                if (MODE != kCount) {
-                    float sum = 0.0f;
-                    if (m != 0u && m <= 2u) {
-                        const float2 pv = s_pv[j];
-                        sum = m == 1u ? pv.x : pv.x + pv.y;
-                    }
-                    if (MODE == kDense) {
-                        if (m <= 2u && (uint64_t)tlo + j < thi) a.out_val[(uint64_t)tlo + j] = m ? sum + 0.0f : 0.0f;
-                    } else if (m != 0u && m <= 2u) {
-                        a.out_idx[toff + nzb[q]] = tlo + j;
-                        a.out_val[toff + nzb[q]] = sum;
-                    }
-                }
-                const bool la = m == 3u || m == 4u, lb = m >= 5u;
-                const uint64_t ba = __ballot(la), bb = __ballot(lb);
-                uint32_t pa = 0, pb = 0;
-                if (lane == 0) {
-                    if (ba) pa = atomicAdd(&s_nA, (uint32_t)__popcll(ba));
-                    if (bb) pb = atomicAdd(&s_nB, (uint32_t)__popcll(bb));
-                }
-                pa = __shfl(pa, 0) + (uint32_t)__popcll(ba & ltmask);
-                pb = __shfl(pb, 0) + (uint32_t)__popcll(bb & ltmask);
-                const uint32_t item = j | (nzb[q] << 16);
-                if (la) s_list[pa] = item;
-                if (lb) s_list[(uint32_t)TMAX - 1u - pb] = item;
-            }
-        }
-        __syncthreads();
-        const uint32_t nA = s_nA, nB = s_nB;
-
-        // 3: three or four ranks, in registers.
-        for (uint32_t wi = tid; wi < nA; wi += NT) {
-            const uint32_t item = s_list[wi];
-            const uint32_t j = item & 0xFFFFu;
-            const uint32_t m = s_cnt[j] & 0xFFFFu;
-            const uint32_t pr = s_pr[j];
-            uint32_t rk[4];
-            float vv[4];
-            rk[0] = pr & 0xFFu;
-            rk[1] = (pr >> 8) & 0xFFu;
-            if (MODE != kCount) {
-                const float2 pv = s_pv[j];
-                vv[0] = pv.x;
-                vv[1] = pv.y;
-            } else {
-                vv[0] = vv[1] = 0.0f;
-            }
-            const uint2 o2 = s_ov[s_head[j]];
-            rk[2] = o2.y & 0xFFFFu;
-            vv[2] = __uint_as_float(o2.x);
-            rk[3] = 0x100u;  // sentinel above every rank
-            vv[3] = 0.0f;
-            if (m == 4u) {
-                const uint2 o3 = s_ov[o2.y >> 16];
-                rk[3] = o3.y & 0xFFFFu;
-                vv[3] = __uint_as_float(o3.x);
-            }
-            auto cswap = [&](int x, int y) {
-                const bool s = rk[x] > rk[y];
-                const uint32_t tr = rk[x];
-                const float tv = vv[x];
-                rk[x] = s ? rk[y] : rk[x];
-                rk[y] = s ? tr : rk[y];
-                vv[x] = s ? vv[y] : vv[x];
-                vv[y] = s ? tv : vv[y];
-            };
-            cswap(0, 1);
-            cswap(2, 3);
-            cswap(0, 2);
-            cswap(1, 3);
-            cswap(1, 2);
-            const uint32_t c1 = 31u - (uint32_t)__clz(rk[0] ^ rk[1]);
-            const uint32_t c2 = 31u - (uint32_t)__clz(rk[1] ^ rk[2]);
-            if (MODE != kSparseWrite) {
-                atomicAdd(&s_E[rk[1] * W + c1], 1u);
-                atomicAdd(&s_E[rk[2] * W + c2], 1u);
-            }
-            uint32_t c3 = 0;
-            if (m == 4u) {
-                c3 = 31u - (uint32_t)__clz(rk[2] ^ rk[3]);
-                if (MODE != kSparseWrite) atomicAdd(&s_E[rk[3] * W + c3], 1u);
-            }
-            if (MODE != kCount) {
-                float sum;
-                const float t012 = c1 < c2 ? (vv[0] + vv[1]) + vv[2] : vv[0] + (vv[1] + vv[2]);
-                if (m == 3u) {
-                    sum = t012;
-                } else if (c2 > c1 && c2 > c3) {
-                    sum = (vv[0] + vv[1]) + (vv[2] + vv[3]);
-                } else if (c1 > c3) {
-                    sum = vv[0] + (c2 < c3 ? (vv[1] + vv[2]) + vv[3] : vv[1] + (vv[2] + vv[3]));
-                } else {
-                    sum = t012 + vv[3];
-                }
-                if (MODE == kDense) {
-                    a.out_val[(uint64_t)tlo + j] = sum + 0.0f;
-                } else {
-                    a.out_idx[toff + (item >> 16)] = tlo + j;
-                    a.out_val[toff + (item >> 16)] = sum;
-                }
-            }
-        }
-
-        // 4: five or more ranks: rank-ordered values, stack walk.
-        for (uint32_t wi = tid; wi < nB; wi += NT) {
-            const uint32_t item = s_list[(uint32_t)TMAX - 1u - wi];
-            const uint32_t j = item & 0xFFFFu;
-            const uint32_t m = s_cnt[j] & 0xFFFFu;
-            uint32_t w[MW];
-            load_mask<MW>(s_mask, j, w);
-            uint32_t start = 0;
-            if (MODE != kCount) {
-                start = atomicAdd(&s_binn, m);
-                auto place = [&](uint32_t r, float v) {
-                    const uint32_t rw = r >> 5, low = (1u << (r & 31u)) - 1u;
-                    uint32_t below = 0;
-#pragma unroll
-                    for (int k = 0; k < MW; ++k)
-                        below += (uint32_t)k < rw ? __popc(w[k]) : ((uint32_t)k == rw ? __popc(w[k] & low) : 0u);
-                    s_bins[start + below] = v;
-                };
-                const float2 pv = s_pv[j];
-                const uint32_t pr = s_pr[j];
-                place(pr & 0xFFu, pv.x);
-                place((pr >> 8) & 0xFFu, pv.y);
-                for (uint32_t o = s_head[j]; o != kNone;) {
-                    const uint2 it = s_ov[o];
-                    place(it.y & 0xFFFFu, __uint_as_float(it.x));
-                    o = it.y >> 16;
-                }
-            }
-            float slot[LMAX];
-#pragma unroll
-            for (int l = 0; l < LMAX; ++l) slot[l] = 0.0f;
-            float cur = 0.0f;
-            uint32_t pend = 0, pos = start;
-            int last = -1;
-#pragma unroll
-            for (int k = 0; k < MW; ++k) {
-                uint32_t bits = w[k];
-                while (bits) {
-                    const int r = k * 32 + (__ffs(bits) - 1);
-                    bits &= bits - 1u;
-                    if (last >= 0) {
-                        const int sep = 31 - (int)__clz((uint32_t)(r ^ last));
-                        if (MODE != kSparseWrite) atomicAdd(&s_E[(uint32_t)r * W + (uint32_t)sep], 1u);
-                        if (MODE != kCount) {
-#pragma unroll
-                            for (int l = 0; l < LMAX; ++l)
-                                if (l < sep && ((pend >> l) & 1u)) cur = slot[l] + cur;
-                            pend = (pend & ~((1u << sep) - 1u)) | (1u << sep);
-#pragma unroll
-                            for (int l = 0; l < LMAX; ++l)
-                                if (l == sep) slot[l] = cur;
+        if (!defer) {
+            // P2
+            if (CNTS && lane < SL && wv * SL + lane < P) s_E[(wv * SL + lane) * W + L] += ntv;
+            const uint32_t toff = MODE == kSparseWrite ? a.tile_off[tile] : 0u;
+            auto entry = [&](uint32_t j, uint32_t r, uint32_t k, float v) {
+                const uint32_t sc = s_cnt[j], m = sc & 0x1FFu, aux = sc >> 9;
+                if (m >= 3u) {
+                    const uint32_t at = aux + k;
+                    s_sr[at] = (uint8_t)r;
+                    if (VALS) s_sv[at] = v;
+                } else if (m == 2u) {
+                    if (k == 1u) {
+                        const uint32_t r0 = s_r0[j];
+                        if (CNTS) atomicAdd(&s_E[max(r0, r) * W + sep_level(r0, r)], 1u);
+                        if (VALS) {
+                            const float sum = s_out[j] + v;
+                            if (MODE == kDense) {
+                                s_out[j] = sum;
+                            } else {
+                                a.out_idx[toff + aux] = tlo + j;
+                                a.out_val[toff + aux] = sum;
+                            }
                         }
                     }
-                    if (MODE != kCount) cur = s_bins[pos++];
-                    last = r;
+                } else if (MODE == kSparseWrite) {
+                    a.out_idx[toff + aux] = tlo + j;
+                    a.out_val[toff + aux] = v;
                 }
-            }
-            if (MODE != kCount) {
+            };
 #pragma unroll
-                for (int l = 0; l < LMAX; ++l)
-                    if ((pend >> l) & 1u) cur = slot[l] + cur;
-                if (MODE == kDense) {
-                    a.out_val[(uint64_t)tlo + j] = cur + 0.0f;
-                } else {
-                    a.out_idx[toff + (item >> 16)] = tlo + j;
-                    a.out_val[toff + (item >> 16)] = cur;
+            for (int s = 0; s < SLMAX; ++s)
+                if (xr[s] != ~0u) entry(xr[s] & 0xFFFu, slot_rank(s), xr[s] >> 12, __uint_as_float(vr[s]));
+            const uint32_t nside = min(s_nside, SIDE);
+            for (uint32_t i = tid; i < nside; i += NT) {
+                const uint2 e = s_side[i];
+                entry(e.x & 0xFFFu, (e.x >> 12) & 0xFFu, e.x >> 20, __uint_as_float(e.y));
+            }
+            __syncthreads();
+
+            // Walk: indices with three or four ranks.
+            for (uint32_t i = tid; i < NA; i += NT) {
+                const uint2 item = s_list[i];
+                const uint32_t j = item.x & 0xFFFFu, nz = item.x >> 16;
+                const uint32_t st0 = item.y & 0xFFFFu, m = item.y >> 16;
+                uint32_t rk[4];
+                float vv[4];
+#pragma unroll
+                for (int e = 0; e < 3; ++e) {
+                    rk[e] = s_sr[st0 + e];
+                    vv[e] = VALS ? s_sv[st0 + e] : 0.0f;
+                }
+                rk[3] = 0x100u;  // above every rank
+                vv[3] = 0.0f;
+                if (m == 4u) {
+                    rk[3] = s_sr[st0 + 3];
+                    if (VALS) vv[3] = s_sv[st0 + 3];
+                }
+                auto cswap = [&](int x, int y) {
+                    const bool sw = rk[x] > rk[y];
+                    const uint32_t tr = rk[x];
+                    const float tv = vv[x];
+                    rk[x] = sw ? rk[y] : rk[x];
+                    rk[y] = sw ? tr : rk[y];
+                    vv[x] = sw ? vv[y] : vv[x];
+                    vv[y] = sw ? tv : vv[y];
+                };
+                cswap(0, 1);
+                cswap(2, 3);
+                cswap(0, 2);
+                cswap(1, 3);
+                cswap(1, 2);
+                const uint32_t c1 = sep_level(rk[0], rk[1]), c2 = sep_level(rk[1], rk[2]);
+                const uint32_t c3 = m == 4u ? sep_level(rk[2], rk[3]) : 0u;
+                if (CNTS) {
+                    atomicAdd(&s_E[rk[1] * W + c1], 1u);
+                    atomicAdd(&s_E[rk[2] * W + c2], 1u);
+                    if (m == 4u) atomicAdd(&s_E[rk[3] * W + c3], 1u);
+                }
+                if (VALS) {
+                    float sum;
+                    const float t012 = c1 < c2 ? (vv[0] + vv[1]) + vv[2] : vv[0] + (vv[1] + vv[2]);
+                    if (m == 3u) sum = t012;
+                    else if (c2 > c1 && c2 > c3) sum = (vv[0] + vv[1]) + (vv[2] + vv[3]);
+                    else if (c1 > c3) sum = vv[0] + (c2 < c3 ? (vv[1] + vv[2]) + vv[3] : vv[1] + (vv[2] + vv[3]));
+                    else sum = t012 + vv[3];
+                    if (MODE == kDense) {
+                        s_out[j] = sum + 0.0f;
+                    } else {
+                        a.out_idx[toff + nz] = tlo + j;
+                        a.out_val[toff + nz] = sum;
+                    }
                 }
             }
+            // Walk: indices with five or more ranks.
+            for (uint32_t i = NA + tid; i < NA + NB; i += NT) {
+                const uint2 item = s_list[i];
+                const uint32_t j = item.x & 0xFFFFu, nz = item.x >> 16;
+                const uint32_t st0 = item.y & 0xFFFFu, m = item.y >> 16;
+                uint32_t w[MW];
+#pragma unroll
+                for (int q = 0; q < MW; ++q) w[q] = 0u;
+                for (uint32_t e = 0; e < m; ++e) {
+                    const uint32_t r = s_sr[st0 + e];
+#pragma unroll
+                    for (int q = 0; q < MW; ++q) w[q] |= (r >> 5) == (uint32_t)q ? 1u << (r & 31u) : 0u;
+                }
+                if (VALS) {
+                    // rank order: entry of rank r goes to the number of
+                    // present ranks below r (cycle placement, in place)
+                    auto rank_pos = [&](uint32_t r) -> uint32_t {
+                        uint32_t below = 0u;
+#pragma unroll
+                        for (int q = 0; q < MW; ++q)
+                            below += (uint32_t)q < (r >> 5) ? (uint32_t)__popc(w[q])
+                                     : ((uint32_t)q == (r >> 5) ? (uint32_t)__popc(w[q] & ((1u << (r & 31u)) - 1u)) : 0u);
+                        return below;
+                    };
+                    for (uint32_t e = 0; e < m; ++e) {
+                        uint32_t r = s_sr[st0 + e];
+                        float v = s_sv[st0 + e];
+                        uint32_t p = rank_pos(r);
+                        for (uint32_t guard = 0; p != e && guard < m; ++guard) {
+                            const uint32_t r2 = s_sr[st0 + p];
+                            const float v2 = s_sv[st0 + p];
+                            s_sr[st0 + p] = (uint8_t)r;
+                            s_sv[st0 + p] = v;
+                            r = r2;
+                            v = v2;
+                            p = rank_pos(r);
+                        }
+                        s_sr[st0 + e] = (uint8_t)r;
+                        s_sv[st0 + e] = v;
+                    }
+                }
+                float slot[LMAX];
+#pragma unroll
+                for (int l = 0; l < LMAX; ++l) slot[l] = 0.0f;
+                float cur = 0.0f;
+                uint32_t pend = 0u, at = st0;
+                int last = -1;
+#pragma unroll
+                for (int q = 0; q < MW; ++q) {
+                    uint32_t bits = w[q];
+                    while (bits) {
+                        const int r = q * 32 + (__ffs(bits) - 1);
+                        bits &= bits - 1u;
+                        if (last >= 0) {
+                            const uint32_t sep = sep_level((uint32_t)r, (uint32_t)last);
+                            if (CNTS) atomicAdd(&s_E[(uint32_t)r * W + sep], 1u);
+                            if (VALS) {
+#pragma unroll
+                                for (int l = 0; l < LMAX; ++l)
+                                    if ((uint32_t)l < sep && ((pend >> l) & 1u)) cur = slot[l] + cur;
+                                pend = (pend & ~((1u << sep) - 1u)) | (1u << sep);
+#pragma unroll
+                                for (int l = 0; l < LMAX; ++l)
+                                    if ((uint32_t)l == sep) slot[l] = cur;
+                            }
+                        }
+                        if (VALS) cur = s_sv[at++];
+                        last = r;
+                    }
+                }
+                if (VALS) {
+#pragma unroll
+                    for (int l = 0; l < LMAX; ++l)
+                        if ((pend >> l) & 1u) cur = slot[l] + cur;
+                    if (MODE == kDense) {
+                        s_out[j] = cur + 0.0f;
+                    } else {
+                        a.out_idx[toff + nz] = tlo + j;
+                        a.out_val[toff + nz] = cur;
+                    }
+                }
+            }
+            __syncthreads();
+
+            // Store the dense tile; clear the tile state.
+            for (uint32_t c = tid * 4u; c < T; c += NT * 4u) {
+                if (MODE == kDense) {
+                    const float4 v = *reinterpret_cast<const float4*>(&s_out[c]);
+                    *reinterpret_cast<float4*>(&s_out[c]) = make_float4(0.f, 0.f, 0.f, 0.f);
+                    const uint64_t g = (uint64_t)tlo + c;
+                    if (a.out_vec && c + 4u <= TT) {
+                        *reinterpret_cast<float4*>(a.out_val + g) = v;
+                    } else {
+                        if (c < TT) a.out_val[g] = v.x;
+                        if (c + 1u < TT) a.out_val[g + 1] = v.y;
+                        if (c + 2u < TT) a.out_val[g + 2] = v.z;
+                        if (c + 3u < TT) a.out_val[g + 3] = v.w;
+                    }
+                }
+                *reinterpret_cast<uint4*>(&s_cnt[c]) = make_uint4(0u, 0u, 0u, 0u);
+            }
+        }
+        if (tid == 0) {
+            s_nside = 0u;
+            s_flag = 0u;
+            s_total = 0u;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int s = 0; s < SLMAX; ++s) {
+            xr[s] = xn[s];
+            vr[s] = vn[s];
         }
     }
     __syncthreads();
-    if (MODE != kSparseWrite) flush_counts<NT>(s_E, a);
+    if (CNTS) flush_counts<NT>(s_E, a);
 }
 
 // ------------------------------------------------------------------------
@@ -603,7 +675,7 @@ __global__ void __launch_bounds__(256) k_tiles(Args a)
 template <int MW, int MODE, bool QUANT>
 __global__ void __launch_bounds__(kSlowNT) k_slow(Args a)
 {
-    constexpr int NT = kSlowNT, TS = kSlowTS, LMAX = Shape<MW>::LMAX, PMAX = 32 * MW;
+    constexpr int NT = kSlowNT, TS = kSlowTS, LMAX = SlowShape<MW>::LMAX, PMAX = 32 * MW;
     __shared__ float s_slot[LMAX][TS];
     __shared__ float s_curv[TS];
     __shared__ int16_t s_last[TS];
@@ -813,31 +885,85 @@ __global__ void __launch_bounds__(1024) k_scan_tiles(const uint32_t* cnt, uint32
     if (tid == 0) *slow_count = 0u;
 }
 
-template <int MW, int MODE>
+template <int PMAX, int MODE>
 hipError_t launch_tiles_q(const Args& a, bool quant, hipStream_t s)
 {
-    const dim3 grid(a.nchunks), block(256);
+    constexpr int SMW = PMAX <= 32 ? 1 : PMAX / 32;
+    const dim3 grid(a.nchunks), block(Fast<PMAX>::NT);
     const int slot = MODE == kSparseWrite ? kTReduceWrite : kTReducePass;
     timer_begin(slot, s);
-    if (quant) hipLaunchKernelGGL((k_tiles<MW, MODE, true>), grid, block, 0, s, a);
-    else hipLaunchKernelGGL((k_tiles<MW, MODE, false>), grid, block, 0, s, a);
+    if (quant) hipLaunchKernelGGL((k_tiles<PMAX, MODE, true>), grid, block, 0, s, a);
+    else hipLaunchKernelGGL((k_tiles<PMAX, MODE, false>), grid, block, 0, s, a);
     timer_end(slot, s);
     const uint32_t sg = std::min<uint32_t>(a.ntiles, 256u);
     if (MODE != kSparseWrite) timer_begin(kTReduceSlow, s);
-    if (quant) hipLaunchKernelGGL((k_slow<MW, MODE, true>), dim3(sg), dim3(kSlowNT), 0, s, a);
-    else hipLaunchKernelGGL((k_slow<MW, MODE, false>), dim3(sg), dim3(kSlowNT), 0, s, a);
+    if (quant) hipLaunchKernelGGL((k_slow<SMW, MODE, true>), dim3(sg), dim3(kSlowNT), 0, s, a);
+    else hipLaunchKernelGGL((k_slow<SMW, MODE, false>), dim3(sg), dim3(kSlowNT), 0, s, a);
     if (MODE != kSparseWrite) timer_end(kTReduceSlow, s);
     return hipGetLastError();
 }
 
-template <int MODE>
-hipError_t launch_pass(const Args& a, uint32_t MW, bool quant, hipStream_t s)
+// Workgroups of the tile pass that the current device holds at once (the
+// fewest over the three modes), 0 if it cannot be queried.
+template <int PMAX, bool QUANT>
+int tiles_occupancy()
 {
-    switch (MW) {
-    case 1: return launch_tiles_q<1, MODE>(a, quant, s);
-    case 2: return launch_tiles_q<2, MODE>(a, quant, s);
-    case 4: return launch_tiles_q<4, MODE>(a, quant, s);
-    default: return launch_tiles_q<8, MODE>(a, quant, s);
+    constexpr int NT = Fast<PMAX>::NT;
+    int best = 1 << 30, n = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_tiles<PMAX, kCount, QUANT>, NT, 0) != hipSuccess)
+        return 0;
+    best = std::min(best, n);
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_tiles<PMAX, kDense, QUANT>, NT, 0) != hipSuccess)
+        return 0;
+    best = std::min(best, n);
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_tiles<PMAX, kSparseWrite, QUANT>, NT, 0) != hipSuccess)
+        return 0;
+    return std::min(best, n);
+}
+
+// Chunks of the tile pass: as many as workgroups fit on the device at once,
+// so that the grid runs as a single wave of equal chunks.  Without a device
+// (size queries on a host with no GPU) a fixed 512.
+uint32_t resident_chunks(uint32_t pk, bool quant)
+{
+    static std::mutex mu;
+    static std::map<std::tuple<int, uint32_t, bool>, uint32_t> cache;
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0) {
+        (void)hipGetLastError();
+        return 512u;
+    }
+    std::lock_guard<std::mutex> g(mu);
+    const auto key = std::make_tuple(dev, pk, quant);
+    const auto it = cache.find(key);
+    if (it != cache.end()) return it->second;
+    int occ = 0;
+    switch (pk) {
+    case 16: occ = quant ? tiles_occupancy<16, true>() : tiles_occupancy<16, false>(); break;
+    case 32: occ = quant ? tiles_occupancy<32, true>() : tiles_occupancy<32, false>(); break;
+    case 64: occ = quant ? tiles_occupancy<64, true>() : tiles_occupancy<64, false>(); break;
+    case 128: occ = quant ? tiles_occupancy<128, true>() : tiles_occupancy<128, false>(); break;
+    default: occ = quant ? tiles_occupancy<256, true>() : tiles_occupancy<256, false>(); break;
+    }
+    if (occ <= 0) {
+        (void)hipGetLastError();
+        occ = 1;
+    }
+    const uint32_t n = (uint32_t)occ * (uint32_t)cus;
+    cache[key] = n;
+    return n;
+}
+
+template <int MODE>
+hipError_t launch_pass(const Args& a, uint32_t pk, bool quant, hipStream_t s)
+{
+    switch (pk) {
+    case 16: return launch_tiles_q<16, MODE>(a, quant, s);
+    case 32: return launch_tiles_q<32, MODE>(a, quant, s);
+    case 64: return launch_tiles_q<64, MODE>(a, quant, s);
+    case 128: return launch_tiles_q<128, MODE>(a, quant, s);
+    default: return launch_tiles_q<256, MODE>(a, quant, s);
     }
 }
 
@@ -874,34 +1000,23 @@ int reduce_plan(int P, uint64_t N, uint64_t max_nnz, uint64_t sum_nnz, double de
     p.P = (uint32_t)P;
     p.L = 0;
     while ((1u << p.L) < p.P) ++p.L;
-    p.MW = p.P <= 32 ? 1u : p.P / 32u;
-    const uint64_t NT = 256;
-    const uint64_t TMAX = p.MW <= 2 ? 2048 : 4096 / p.MW;
-    // Tile size: the largest power of two (256 .. TMAX) for which, with the
-    // entries spread uniformly, a rank fills at most half of its 32-entry
-    // window and the expected overflow values, worklist indices and
-    // rank-ordered values stay under half of their per-tile capacity
-    // (Poisson model of the ranks present per index, mean lambda).
+    p.PK = p.P <= 16 ? 16u : (p.P <= 32 ? 32u : (p.P <= 64 ? 64u : (p.P <= 128 ? 128u : 256u)));
+    // Tile size: the largest multiple of 4*NT up to 4096 for which the
+    // densest stream puts at most 42 entries of a 64-entry window into a
+    // tile and, with the entries spread uniformly (Poisson model of the
+    // ranks present per index, mean lambda), the entries of indices held by
+    // three or more ranks fill at most half of the staging capacity.
+    const uint64_t NTq = p.PK > 128 ? 512 : 256, TMIN = 4 * NTq, TMAXq = 4096;
     const double lam = (double)sum_nnz / (double)N;
     const double e = std::exp(-lam);
-    const double p4 = 1.0 - e * (1.0 + lam + lam * lam / 2 + lam * lam * lam / 6);  // P(m >= 5)
-    const double ovf = std::max(0.0, lam - 2.0 + 2.0 * e + lam * e);              // E[(m-2)+]
-    const double bins = std::max(0.0, lam - e * lam * (1.0 + lam + lam * lam / 2 + lam * lam * lam / 6));  // E[m; m >= 5]
-    // capacities are TMAX/2 values each; aim for a quarter of TMAX in expectation
-    const double want_rank = max_nnz ? 16.0 * (double)N / (double)max_nnz : 1e30;
-    const double want_ov = ovf > 0 ? 0.25 * (double)TMAX / ovf : 1e30;
-    const double want_bins = bins > 0 ? 0.25 * (double)TMAX / bins : 1e30;
-    (void)p4;
-    const double want = std::min(want_rank, std::min(want_ov, want_bins));
-    uint64_t T = NT;
-    while (T * 2 <= TMAX && (double)(T * 2) <= want) T *= 2;
-    uint64_t Np2 = NT;
-    while (Np2 < N) Np2 *= 2;
-    if (T > Np2) T = Np2;
+    const double staged = std::max(0.0, lam - lam * e - lam * lam * e);  // E[m; m >= 3]
+    const double dens = (double)max_nnz / (double)N;
+    uint64_t T = TMAXq;
+    while (T > TMIN && ((double)T * dens > 42.0 || (double)T * staged > 2048.0)) T -= TMIN;
     p.T = (uint32_t)T;
     p.N = N;
     p.ntiles = (uint32_t)((N + T - 1) / T);
-    uint32_t nch = std::min<uint32_t>(p.ntiles, 768u);
+    uint32_t nch = std::min<uint32_t>(p.ntiles, resident_chunks(p.PK, qbits != 0));
     p.tiles_per_chunk = (p.ntiles + nch - 1) / nch;
     p.nchunks = (p.ntiles + p.tiles_per_chunk - 1) / p.tiles_per_chunk;
     const double t = std::floor(delta * (double)N);
@@ -946,10 +1061,11 @@ hipError_t reduce_run(const ReducePlan& p, const StreamDesc* host_tab, uint32_t*
     a.nchunks = p.nchunks;
     a.tpc = p.tiles_per_chunk;
     a.qbits = p.qbits;
+    a.out_vec = (reinterpret_cast<uintptr_t>(out_val) & 15u) == 0 ? 1u : 0u;
     const bool quant = p.qbits != 0;
 
-    e = p.speculate_dense ? launch_pass<kDense>(a, p.MW, quant, s)
-                          : launch_pass<kCount>(a, p.MW, quant, s);
+    e = p.speculate_dense ? launch_pass<kDense>(a, p.PK, quant, s)
+                          : launch_pass<kCount>(a, p.PK, quant, s);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(k_decide, dim3(1), dim3(64), 0, s, l.tab, l.node_cnt, p.P, p.N, p.thr,
                        node_nnz, node_dense, l.hdr);
@@ -966,7 +1082,7 @@ hipError_t reduce_run(const ReducePlan& p, const StreamDesc* host_tab, uint32_t*
     hipLaunchKernelGGL(k_scan_tiles, dim3(1), dim3(1024), 0, s, l.tile_cnt, l.tile_off, p.ntiles,
                        l.slow_count);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    if ((e = launch_pass<kSparseWrite>(a, p.MW, quant, s)) != hipSuccess) return e;
+    if ((e = launch_pass<kSparseWrite>(a, p.PK, quant, s)) != hipSuccess) return e;
     if ((e = hipMemcpyAsync(res, l.hdr, sizeof(ReduceResult), hipMemcpyDeviceToHost, s)) !=
         hipSuccess)
         return e;
