@@ -60,23 +60,26 @@ struct SlowShape {
 
 // Fast tile pass for up to PMAX ranks.  A wave owns SLMAX ranks ("slots");
 // per tile it reads a 64-entry window of each slot's stream (one entry per
-// lane).  TMAX coordinates per tile; CAP staged entries (those of indices
+// lane).  Two workgroups share a CU (LDS), so the wave count per SIMD and
+// with it the register budget follow from NT.  TMAX coordinates per tile; CAP staged entries (those of indices
 // held by three or more ranks); SIDE entries of windows that had to be
 // continued because all 64 entries fell inside the tile.
 template <int PMAX>
 struct Fast {
-    static constexpr int NT = PMAX > 128 ? 512 : 256;
+    static constexpr int NT = PMAX <= 32 ? 256 : (PMAX <= 128 ? 512 : 1024);
+    static constexpr int WPE = NT == 256 ? 2 : 4;  // waves per SIMD (LDS and registers)
     static constexpr int NW = NT / 64;
     static constexpr int SLMAX = PMAX / NW;
     static constexpr int TMAX = 4096;
     static constexpr int CPTMAX = TMAX / NT;
-    static constexpr uint32_t CAP = 4096;
+    static constexpr uint32_t CAP = 3584;
     static constexpr uint32_t LCAP = CAP / 3 + 1;
-    static constexpr uint32_t SIDE = 512;
+    static constexpr uint32_t SIDE = 256;
     static constexpr int LMAX = PMAX <= 16 ? 4 : (PMAX <= 32 ? 5 : (PMAX <= 64 ? 6 : (PMAX <= 128 ? 7 : 8)));
     static constexpr int MW = PMAX <= 32 ? 1 : PMAX / 32;
 };
 constexpr uint32_t kWin = 64;  // window entries per rank per tile
+constexpr double kStageCap = 3584.0;  // Fast<>::CAP
 
 struct Args {
     const StreamDesc* tab;
@@ -195,22 +198,33 @@ __device__ __forceinline__ uint32_t sep_level(uint32_t a, uint32_t b)
 // Tiles whose staged entries, side entries or total entries exceed the LDS
 // budget are deferred to the slow pass.
 template <int PMAX, int MODE, bool QUANT>
-__global__ void __launch_bounds__(Fast<PMAX>::NT, 2) k_tiles(Args a)
+__global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args a)
 {
     using F = Fast<PMAX>;
     constexpr int NT = F::NT, NW = F::NW, SLMAX = F::SLMAX, TMAX = F::TMAX, CPTMAX = F::CPTMAX;
     constexpr uint32_t CAP = F::CAP, SIDE = F::SIDE;
     constexpr int LMAX = F::LMAX, MW = F::MW;
     constexpr bool VALS = MODE != kCount, CNTS = MODE != kSparseWrite;
+    constexpr uint32_t EW = PMAX * (LMAX + 1);  // node-count words; 64 dummies follow
 
-    __shared__ __align__(16) uint32_t s_cnt[TMAX];         // ranks per index; then m | aux << 9
-    __shared__ __align__(16) float s_out[VALS ? TMAX : 4];  // first value; dense: the sum
-    __shared__ uint8_t s_r0[TMAX];                         // rank of the first arrival
-    __shared__ float s_sv[VALS ? CAP : 1];                 // staged values
-    __shared__ uint8_t s_sr[CAP];                          // staged ranks
-    __shared__ uint2 s_list[F::LCAP];                      // {j | nzpos << 16, start | m << 16}
-    __shared__ uint32_t s_E[CNTS ? PMAX * (LMAX + 1) : 1];
-    __shared__ uint2 s_side[SIDE];                         // {j | r << 12 | k << 20, value}
+    // Every array has 64 dummy words past its end: lanes with nothing to do
+    // aim their (unconditional) LDS accesses there, which keeps the slot
+    // loops free of branches so that their LDS latencies overlap.
+    __shared__ __align__(16) uint32_t s_cnt[TMAX + 64];         // ranks per index; then m | aux << 9
+    __shared__ __align__(16) float s_out[VALS ? TMAX + 64 : 4];  // first value; dense: the sum
+    __shared__ uint8_t s_r0[TMAX + 64];                         // rank of the first arrival
+    __shared__ float s_sv[VALS ? CAP + 64 : 1];                 // staged values
+    __shared__ uint8_t s_sr[CAP + 64];                          // staged ranks
+    __shared__ uint2 s_list[F::LCAP];                           // {j | nzpos << 16, start | m << 16}
+    __shared__ uint32_t s_E[CNTS ? EW + 64 : 1];
+    __shared__ uint2 s_side[SIDE];                              // {j | r << 12 | k << 20, value}
+    // Per rank (slot) state: {stream position, entries in this tile},
+    // {chunk end, last readable entry}, {index base, value base}, level unit.
+    // Ranks past P have an empty window over a readable dummy address.
+    __shared__ uint64_t s_pn[PMAX];  // position | tile count << 32
+    __shared__ uint2 s_el[PMAX];
+    __shared__ uint4 s_base[PMAX];
+    __shared__ float s_unit[PMAX];
     __shared__ uint32_t s_wtot[2 * NW];
     __shared__ uint32_t s_nside, s_flag, s_total;
 
@@ -219,126 +233,146 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, 2) k_tiles(Args a)
     const uint32_t P = a.P, L = a.L, W = L + 1, T = a.T, CPT = T / NT;
     const uint32_t chunk = blockIdx.x, stride = a.nchunks + 1;
     const uint32_t t0 = chunk * a.tpc, t1 = min(t0 + a.tpc, a.ntiles);
-    const uint32_t SL = (P + NW - 1) / NW;
     const uint32_t qbits = a.qbits;
     const uint32_t plog = qbits == 8u ? 0u : (qbits == 4u ? 1u : 2u), pm = (1u << plog) - 1u;
-    const c_desc tab = (c_desc)a.tab;
 
-    // Rank of slot s.  Slots past the last rank keep an empty window (their
-    // chunk end equals their position) and read rank P-1's stream harmlessly,
-    // so that every slot runs the same straight-line code.
-    auto slot_rank = [&](int s) -> uint32_t { return min(wv * SL + (uint32_t)s, P - 1u); };
-    // Per-slot scalars (descriptor fields, lane reads of the slot state) are
-    // loop invariant; left alone the compiler would hoist all of them out of
-    // the tile loop and run out of scalar registers.  An opaque copy of the
-    // slot number keeps them next to their use.
+    // Slot s of wave wv is rank s*NW + wv (waves interleave, so small P
+    // still spreads over all waves).
+    // Loop-invariant values (the per-rank LDS state of every slot, LDS
+    // addresses of a thread's coordinates) would be hoisted out of the tile
+    // loop and held in registers or spilled; opaque copies of the rank
+    // (scalar) and thread number (vector) keep them next to their use.
     auto opaque = [](uint32_t v) -> uint32_t {
         asm volatile("" : "+s"(v));
         return v;
     };
+    auto opaque_v = [](uint32_t v) -> uint32_t {
+        asm volatile("" : "+v"(v));
+        return v;
+    };
+    auto slot_rank = [&](int s) -> uint32_t { return opaque((uint32_t)s * NW + wv); };
+    // A slot's {position, tile count} is written by lane 0 of its wave and
+    // read by all lanes with no barrier in between.  Plain accesses would let
+    // the compiler forward a lane's own earlier read (in its per-thread view
+    // nobody else writes), leaving lanes 1..63 on a stale position; relaxed
+    // atomic accesses always go to LDS, where the wave's operations are
+    // ordered.
+    auto pn_get = [&](uint32_t r) -> uint2 {
+        const uint64_t v = __hip_atomic_load(&s_pn[r], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WAVEFRONT);
+        return make_uint2((uint32_t)v, (uint32_t)(v >> 32));
+    };
+    auto pn_set = [&](uint32_t r, uint32_t pos, uint32_t cnt) {
+        __hip_atomic_store(&s_pn[r], (uint64_t)pos | (uint64_t)cnt << 32, __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_WAVEFRONT);
+    };
 
-    // Window of rank r at stream position pos: raw index and raw value
-    // word (fp32 bits, or the byte holding the entry's code).
-    auto load_win = [&](uint32_t r, uint32_t pos, uint32_t& x, uint32_t& v) {
-        r = opaque(r);
-        const uint64_t nnz = tab[r].nnz;
-        const uint32_t rem = pos < nnz ? (uint32_t)min(nnz - pos, (uint64_t)kWin) : 0u;
-        x = __builtin_amdgcn_raw_buffer_load_b32(buffer_at(tab[r].idx + pos, rem * 4u), (int)(lane * 4u), 0, 0);
-        if (VALS) {
-            if (QUANT) {
-                const uint64_t nb = (nnz * qbits + 7u) / 8u;
-                const uint32_t b0 = pos >> plog;
-                const uint32_t remb = b0 < nb ? (uint32_t)min(nb - b0, (uint64_t)kWin) : 0u;
-                v = __builtin_amdgcn_raw_buffer_load_b8(buffer_at(tab[r].qval + b0, remb),
-                                                        (int)((lane + (pos & pm)) >> plog), 0, 0);
-            } else {
-                v = __builtin_amdgcn_raw_buffer_load_b32(buffer_at(tab[r].val + pos, rem * 4u),
-                                                         (int)(lane * 4u), 0, 0);
+    for (uint32_t r = tid; r < (uint32_t)PMAX; r += NT) {
+        uint2 pn = make_uint2(0u, 0u), el = make_uint2(0u, 0u);
+        uint64_t ib = reinterpret_cast<uint64_t>(a.tab), vb = ib;  // readable dummy
+        float unit = 0.0f;
+        if (r < P) {
+            const StreamDesc& d = a.tab[r];
+            pn.x = a.off[r * stride + chunk];
+            el.x = a.off[r * stride + chunk + 1];
+            if (d.nnz) {
+                el.y = (uint32_t)(d.nnz - 1u);
+                ib = reinterpret_cast<uint64_t>(d.idx);
+                vb = reinterpret_cast<uint64_t>(QUANT ? static_cast<const void*>(d.qval)
+                                                      : static_cast<const void*>(d.val));
             }
-        } else {
-            v = 0u;
+            if (QUANT && VALS) unit = level_unit(*d.qscale, qbits);
         }
-    };
-    auto decode = [&](uint32_t v, uint32_t pos, float unit) -> float {
-        if (QUANT) {
-            const uint32_t code = (v >> (((lane + (pos & pm)) & pm) * qbits)) & ((1u << qbits) - 1u);
-            return dequant(code, qbits, unit);
-        }
-        return __uint_as_float(v);
-    };
-    auto first_arrival = [&](uint32_t j, uint32_t r, float v) {
-        s_r0[j] = (uint8_t)r;
-        if (VALS) s_out[j] = MODE == kDense ? v + 0.0f : v;
-    };
-
-    // Per-slot state in lanes: lane s holds slot s's stream position, chunk
-    // end, level unit and this tile's entry count.
-    uint32_t posv = 0u, endv = 0u, ntv = 0u;
-    float unitv = 0.0f;
-    if (lane < SL && wv * SL + lane < P) {
-        const uint32_t r = wv * SL + lane;
-        posv = a.off[r * stride + chunk];
-        endv = a.off[r * stride + chunk + 1];
-        if (QUANT && VALS) unitv = level_unit(*a.tab[r].qscale, qbits);
+        s_pn[r] = (uint64_t)pn.x | (uint64_t)pn.y << 32;
+        s_el[r] = el;
+        s_base[r] = make_uint4((uint32_t)ib, (uint32_t)(ib >> 32), (uint32_t)vb, (uint32_t)(vb >> 32));
+        s_unit[r] = unit;
     }
-    auto rl = [&](uint32_t v, int s) -> uint32_t { return (uint32_t)__builtin_amdgcn_readlane((int)v, s); };
-
-    for (uint32_t i = tid; i < TMAX; i += NT) {
+    for (uint32_t i = tid; i < TMAX + 64; i += NT) {
         s_cnt[i] = 0u;
         if (VALS) s_out[i] = 0.0f;
     }
     if (CNTS)
-        for (uint32_t i = tid; i < P * W; i += NT) s_E[i] = 0u;
+        for (uint32_t i = tid; i < EW + 64; i += NT) s_E[i] = 0u;
     if (tid == 0) {
         s_nside = 0u;
         s_flag = 0u;
         s_total = 0u;
     }
+    __syncthreads();
+
+    // Window of rank r at stream position pos: raw index and raw value word
+    // (fp32 bits, or the byte holding the entry's code).  Positions past the
+    // stream's end read its last entry (they lie past the chunk end too).
+    auto load_win = [&](uint32_t r, uint32_t pos, uint32_t& x, uint32_t& v) {
+        const uint4 b = s_base[r];
+        const uint32_t i = min(pos + lane, s_el[r].y);
+        const uint64_t ib = ((uint64_t)b.y << 32) | b.x;
+        x = *reinterpret_cast<g_u32*>(ib + 4ull * i);
+        v = 0u;
+        if (VALS) {
+            const uint64_t vb = ((uint64_t)b.w << 32) | b.z;
+            if (QUANT) v = *reinterpret_cast<g_u8*>(vb + (i >> plog));
+            else v = *reinterpret_cast<g_u32*>(vb + 4ull * i);
+        }
+    };
+    auto decode = [&](uint32_t v, uint32_t pos, float unit) -> float {
+        if (QUANT) {
+            const uint32_t code = (v >> (((lane + pos) & pm) * qbits)) & ((1u << qbits) - 1u);
+            return dequant(code, qbits, unit);
+        }
+        return __uint_as_float(v);
+    };
 
     // xr: raw window index, then (entry in the tile) j | arrival << 12, or
     // ~0 for an entry outside the tile; vr: raw value word, then the value.
     uint32_t xr[SLMAX], vr[SLMAX];
 #pragma unroll
-    for (int s = 0; s < SLMAX; ++s) {
-        load_win(slot_rank(s), rl(posv, s), xr[s], vr[s]);
-    }
-    __syncthreads();
+    for (int s = 0; s < SLMAX; ++s) load_win(slot_rank(s), pn_get(slot_rank(s)).x, xr[s], vr[s]);
 
     for (uint32_t tile = t0; tile < t1; ++tile) {
         const uint32_t tlo = tile * T;
         const uint32_t TT = (uint32_t)min((uint64_t)T, (uint64_t)a.N - tlo);  // tile width
 
-        // P1: arrival numbers, first values.
+        // P1: arrival numbers (all atomics issued before any result is
+        // used), then the first arrivals' ranks and values.
         uint32_t full = 0u, wtot = 0u;
+        uint32_t kk[SLMAX];
 #pragma unroll
         for (int s = 0; s < SLMAX; ++s) {
-            const int so = (int)opaque((uint32_t)s);
-            const uint32_t pos = rl(posv, so), avail = rl(endv, so) - pos;
+            const uint32_t r = slot_rank(s);
+            const uint32_t pos = pn_get(r).x;
+            const uint32_t avail = s_el[r].x - pos;
             const uint32_t j = xr[s] - tlo;
             const bool in = j < TT && lane < avail;
-            uint32_t k = ~0u;
-            if (in) k = atomicAdd(&s_cnt[j], 1u);
-            if (VALS) vr[s] = __float_as_uint(decode(vr[s], pos, __uint_as_float(rl(__float_as_uint(unitv), so))));
+            const uint32_t jd = in ? j : (uint32_t)TMAX + lane;
+            kk[s] = atomicAdd(&s_cnt[jd], 1u);
+            if (VALS) vr[s] = __float_as_uint(decode(vr[s], pos, s_unit[r]));
             const uint32_t n = (uint32_t)__popcll(__ballot(in));
-            posv = lane == (uint32_t)s ? pos + n : posv;
-            ntv = lane == (uint32_t)s ? n : ntv;
+            if (lane == 0u) pn_set(r, pos + n, n);
             full |= (n == kWin ? 1u : 0u) << s;
             wtot += n;
-            xr[s] = in ? j | k << 12 : ~0u;
+            xr[s] = jd;
         }
 #pragma unroll
-        for (int s = 0; s < SLMAX; ++s)
-            if (xr[s] < (1u << 12)) first_arrival(xr[s], slot_rank(s), __uint_as_float(vr[s]));
+        for (int s = 0; s < SLMAX; ++s) {
+            const bool in = xr[s] < (uint32_t)TMAX;
+            const bool first = in && kk[s] == 0u;
+            const uint32_t jf = first ? xr[s] : (uint32_t)TMAX + lane;
+            s_r0[jf] = (uint8_t)slot_rank(s);
+            if (VALS) s_out[jf] = MODE == kDense ? __uint_as_float(vr[s]) + 0.0f : __uint_as_float(vr[s]);
+            xr[s] = in ? xr[s] | kk[s] << 12 : ~0u;
+        }
 
         // Windows entirely inside the tile: continue them into the side buffer.
         while (full) {
             const int s = __builtin_ctz(full);
             full &= full - 1u;
-            const uint32_t r = wv * SL + (uint32_t)s;
-            const float unit = __uint_as_float(rl(__float_as_uint(unitv), s));
+            const uint32_t r = slot_rank(s);
+            const float unit = s_unit[r];
             uint32_t n;
             do {
-                const uint32_t pos = rl(posv, s), avail = rl(endv, s) - pos;
+                const uint2 pn = pn_get(r);
+                const uint32_t pos = pn.x, avail = s_el[r].x - pos;
                 uint32_t x, v;
                 load_win(r, pos, x, v);
                 const uint32_t j = x - tlo;
@@ -352,28 +386,26 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, 2) k_tiles(Args a)
                 if (lane == 0u && n) base = atomicAdd(&s_nside, n);
                 base = (uint32_t)__builtin_amdgcn_readfirstlane((int)base);
                 if (in) {
-                    if (k == 0u) first_arrival(j, r, val);
+                    if (k == 0u) {
+                        s_r0[j] = (uint8_t)r;
+                        if (VALS) s_out[j] = MODE == kDense ? val + 0.0f : val;
+                    }
                     const uint32_t at = base + (uint32_t)__popcll(bal & ((1ull << lane) - 1ull));
                     if (at < SIDE) s_side[at] = make_uint2(j | r << 12 | k << 20, __float_as_uint(val));
                 }
-                if (lane == 0u && base + n > SIDE) s_flag = 1u;
-                posv = lane == (uint32_t)s ? pos + n : posv;
-                ntv = lane == (uint32_t)s ? ntv + n : ntv;
+                if (lane == 0u) {
+                    if (base + n > SIDE) s_flag = 1u;
+                    pn_set(r, pos + n, pn.y + n);
+                }
                 wtot += n;
             } while (n == kWin);
         }
         if (lane == 0u && wtot) atomicAdd(&s_total, wtot);
 
-        // Request the next tile's windows.
-        uint32_t xn[SLMAX], vn[SLMAX];
-#pragma unroll
-        for (int s = 0; s < SLMAX; ++s) {
-            load_win(slot_rank(s), rl(posv, (int)opaque((uint32_t)s)), xn[s], vn[s]);
-        }
         __syncthreads();
 
         // Scan over this thread's CPT consecutive coordinates.
-        const uint32_t jb = tid * CPT;
+        const uint32_t jb = opaque_v(tid) * CPT;
         uint32_t mc[CPTMAX];
 #pragma unroll
         for (int c = 0; c < CPTMAX; c += 4) {
@@ -454,15 +486,72 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, 2) k_tiles(Args a)
                 const uint32_t k = atomicAdd(a.slow_count, 1u);
                 a.slow_list[k] = tile;
             }
+#pragma unroll
+            for (int s = 0; s < SLMAX; ++s) load_win(slot_rank(s), pn_get(slot_rank(s)).x, xr[s], vr[s]);
         }
         __syncthreads();
 
         if (!defer) {
             // P2
-            if (CNTS && lane < SL && wv * SL + lane < P) s_E[(wv * SL + lane) * W + L] += ntv;
+            if (CNTS)
+                for (uint32_t r = tid; r < P; r += NT) s_E[r * W + L] += pn_get(r).y;
             const uint32_t toff = MODE == kSparseWrite ? a.tile_off[tile] : 0u;
+            // Slots in groups of G: (a) the counts of every entry's index,
+            // all reads in flight at once; (b) staging of entries at indices
+            // with >= 3 ranks, and the first value and rank fetched for the
+            // second of two; (c) the pairs' node counts and sums.
+            constexpr int G = 4;
+#pragma unroll
+            for (int g0 = 0; g0 < SLMAX; g0 += G) {
+                uint32_t sc[G], r0s[G];
+                float o0s[G];
+#pragma unroll
+                for (int q = 0; q < G; ++q) sc[q] = s_cnt[xr[g0 + q] & 0xFFFu];
+#pragma unroll
+                for (int q = 0; q < G; ++q) {
+                    const int s = g0 + q;
+                    const bool valid = xr[s] != ~0u;
+                    const uint32_t j = xr[s] & 0xFFFu, k = xr[s] >> 12;
+                    const uint32_t m = sc[q] & 0x1FFu, aux = sc[q] >> 9;
+                    const uint32_t at = valid && m >= 3u ? aux + k : CAP + lane;
+                    s_sr[at] = (uint8_t)slot_rank(s);
+                    if (VALS) s_sv[at] = __uint_as_float(vr[s]);
+                    const bool pair = valid && m == 2u && k == 1u;
+                    const uint32_t pj = pair ? j : (uint32_t)TMAX + lane;
+                    r0s[q] = s_r0[pj];
+                    o0s[q] = VALS ? s_out[pj] : 0.0f;
+                    if (MODE == kSparseWrite && valid && m == 1u) {
+                        a.out_idx[toff + aux] = tlo + j;
+                        a.out_val[toff + aux] = __uint_as_float(vr[s]);
+                    }
+                }
+#pragma unroll
+                for (int q = 0; q < G; ++q) {
+                    const int s = g0 + q;
+                    const bool valid = xr[s] != ~0u;
+                    const uint32_t j = xr[s] & 0xFFFu, k = xr[s] >> 12;
+                    const uint32_t m = sc[q] & 0x1FFu, aux = sc[q] >> 9;
+                    const uint32_t r = slot_rank(s);
+                    const bool pair = valid && m == 2u && k == 1u;
+                    if (CNTS) {
+                        const uint32_t e = pair ? max(r0s[q], r) * W + sep_level(r0s[q], r) : EW + lane;
+                        atomicAdd(&s_E[e], 1u);
+                    }
+                    if (MODE == kDense) {
+                        s_out[pair ? j : (uint32_t)TMAX + lane] = o0s[q] + __uint_as_float(vr[s]);
+                    } else if (MODE == kSparseWrite && pair) {
+                        a.out_idx[toff + aux] = tlo + j;
+                        a.out_val[toff + aux] = o0s[q] + __uint_as_float(vr[s]);
+                    }
+                }
+                // this group's entries are done: request its next windows
+                // (they overlap the walk and the next tile's start)
+#pragma unroll
+                for (int q = 0; q < G; ++q) load_win(slot_rank(g0 + q), pn_get(slot_rank(g0 + q)).x, xr[g0 + q], vr[g0 + q]);
+            }
+            // continued windows' entries
             auto entry = [&](uint32_t j, uint32_t r, uint32_t k, float v) {
-                const uint32_t sc = s_cnt[j], m = sc & 0x1FFu, aux = sc >> 9;
+                const uint32_t sc1 = s_cnt[j], m = sc1 & 0x1FFu, aux = sc1 >> 9;
                 if (m >= 3u) {
                     const uint32_t at = aux + k;
                     s_sr[at] = (uint8_t)r;
@@ -486,9 +575,6 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, 2) k_tiles(Args a)
                     a.out_val[toff + aux] = v;
                 }
             };
-#pragma unroll
-            for (int s = 0; s < SLMAX; ++s)
-                if (xr[s] != ~0u) entry(xr[s] & 0xFFFu, slot_rank(s), xr[s] >> 12, __uint_as_float(vr[s]));
             const uint32_t nside = min(s_nside, SIDE);
             for (uint32_t i = tid; i < nside; i += NT) {
                 const uint2 e = s_side[i];
@@ -504,15 +590,13 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, 2) k_tiles(Args a)
                 uint32_t rk[4];
                 float vv[4];
 #pragma unroll
-                for (int e = 0; e < 3; ++e) {
+                for (int e = 0; e < 4; ++e) {
                     rk[e] = s_sr[st0 + e];
                     vv[e] = VALS ? s_sv[st0 + e] : 0.0f;
                 }
-                rk[3] = 0x100u;  // above every rank
-                vv[3] = 0.0f;
-                if (m == 4u) {
-                    rk[3] = s_sr[st0 + 3];
-                    if (VALS) vv[3] = s_sv[st0 + 3];
+                if (m == 3u) {
+                    rk[3] = 0x100u;  // above every rank
+                    vv[3] = 0.0f;
                 }
                 auto cswap = [&](int x, int y) {
                     const bool sw = rk[x] > rk[y];
@@ -533,7 +617,7 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, 2) k_tiles(Args a)
                 if (CNTS) {
                     atomicAdd(&s_E[rk[1] * W + c1], 1u);
                     atomicAdd(&s_E[rk[2] * W + c2], 1u);
-                    if (m == 4u) atomicAdd(&s_E[rk[3] * W + c3], 1u);
+                    atomicAdd(&s_E[m == 4u ? rk[3] * W + c3 : EW + lane], 1u);
                 }
                 if (VALS) {
                     float sum;
@@ -635,7 +719,7 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, 2) k_tiles(Args a)
             __syncthreads();
 
             // Store the dense tile; clear the tile state.
-            for (uint32_t c = tid * 4u; c < T; c += NT * 4u) {
+            for (uint32_t c = opaque_v(tid) * 4u; c < T; c += NT * 4u) {
                 if (MODE == kDense) {
                     const float4 v = *reinterpret_cast<const float4*>(&s_out[c]);
                     *reinterpret_cast<float4*>(&s_out[c]) = make_float4(0.f, 0.f, 0.f, 0.f);
@@ -658,11 +742,6 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, 2) k_tiles(Args a)
             s_total = 0u;
         }
         __syncthreads();
-#pragma unroll
-        for (int s = 0; s < SLMAX; ++s) {
-            xr[s] = xn[s];
-            vr[s] = vn[s];
-        }
     }
     __syncthreads();
     if (CNTS) flush_counts<NT>(s_E, a);
@@ -1005,14 +1084,14 @@ int reduce_plan(int P, uint64_t N, uint64_t max_nnz, uint64_t sum_nnz, double de
     // densest stream puts at most 42 entries of a 64-entry window into a
     // tile and, with the entries spread uniformly (Poisson model of the
     // ranks present per index, mean lambda), the entries of indices held by
-    // three or more ranks fill at most half of the staging capacity.
-    const uint64_t NTq = p.PK > 128 ? 512 : 256, TMIN = 4 * NTq, TMAXq = 4096;
+    // three or more ranks fill at most 60% of the staging capacity.
+    const uint64_t NTq = p.PK <= 32 ? 256 : (p.PK <= 128 ? 512 : 1024), TMIN = 4 * NTq, TMAXq = 4096;
     const double lam = (double)sum_nnz / (double)N;
     const double e = std::exp(-lam);
     const double staged = std::max(0.0, lam - lam * e - lam * lam * e);  // E[m; m >= 3]
     const double dens = (double)max_nnz / (double)N;
     uint64_t T = TMAXq;
-    while (T > TMIN && ((double)T * dens > 42.0 || (double)T * staged > 2048.0)) T -= TMIN;
+    while (T > TMIN && ((double)T * dens > 42.0 || (double)T * staged > 0.6 * kStageCap)) T -= TMIN;
     p.T = (uint32_t)T;
     p.N = N;
     p.ntiles = (uint32_t)((N + T - 1) / T);
