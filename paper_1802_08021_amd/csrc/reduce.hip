@@ -337,21 +337,34 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
         // used), then the first arrivals' ranks and values.
         uint32_t full = 0u, wtot = 0u;
         uint32_t kk[SLMAX];
+        // slots in groups: the group's state reads are issued together
+        constexpr int G1 = SLMAX < 8 ? SLMAX : 8;
 #pragma unroll
-        for (int s = 0; s < SLMAX; ++s) {
-            const uint32_t r = slot_rank(s);
-            const uint32_t pos = pn_get(r).x;
-            const uint32_t avail = s_el[r].x - pos;
-            const uint32_t j = xr[s] - tlo;
-            const bool in = j < TT && lane < avail;
-            const uint32_t jd = in ? j : (uint32_t)TMAX + lane;
-            kk[s] = atomicAdd(&s_cnt[jd], 1u);
-            if (VALS) vr[s] = __float_as_uint(decode(vr[s], pos, s_unit[r]));
-            const uint32_t n = (uint32_t)__popcll(__ballot(in));
-            if (lane == 0u) pn_set(r, pos + n, n);
-            full |= (n == kWin ? 1u : 0u) << s;
-            wtot += n;
-            xr[s] = jd;
+        for (int g0 = 0; g0 < SLMAX; g0 += G1) {
+            uint32_t ps[G1], es[G1];
+            float us[G1];
+#pragma unroll
+            for (int q = 0; q < G1; ++q) {
+                const uint32_t r = slot_rank(g0 + q);
+                ps[q] = pn_get(r).x;
+                es[q] = s_el[r].x;
+                us[q] = QUANT && VALS ? s_unit[r] : 0.0f;
+            }
+#pragma unroll
+            for (int q = 0; q < G1; ++q) {
+                const int s = g0 + q;
+                const uint32_t pos = ps[q], avail = es[q] - pos;
+                const uint32_t j = xr[s] - tlo;
+                const bool in = j < TT && lane < avail;
+                const uint32_t jd = in ? j : (uint32_t)TMAX + lane;
+                kk[s] = atomicAdd(&s_cnt[jd], 1u);
+                if (VALS) vr[s] = __float_as_uint(decode(vr[s], pos, us[q]));
+                const uint32_t n = (uint32_t)__popcll(__ballot(in));
+                if (lane == 0u) pn_set(slot_rank(s), pos + n, n);
+                full |= (n == kWin ? 1u : 0u) << s;
+                wtot += n;
+                xr[s] = jd;
+            }
         }
 #pragma unroll
         for (int s = 0; s < SLMAX; ++s) {
@@ -435,17 +448,15 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
             s_wtot[NW + wv] = i2;
         }
         __syncthreads();
-        uint32_t b1 = 0u, b2 = 0u, g1 = 0u, g2 = 0u;
-#pragma unroll
-        for (int w = 0; w < NW; ++w) {
-            const uint32_t c1 = s_wtot[w], c2 = s_wtot[NW + w];
-            if ((uint32_t)w < wv) {
-                b1 += c1;
-                b2 += c2;
-            }
-            g1 += c1;
-            g2 += c2;
-        }
+        // wave totals: lane w < NW holds wave w's; prefix below this wave and
+        // the tile totals by one more wave scan
+        const uint32_t w1 = lane < (uint32_t)NW ? s_wtot[lane] : 0u;
+        const uint32_t w2 = lane < (uint32_t)NW ? s_wtot[NW + lane] : 0u;
+        const uint32_t x1 = wave_scan(w1), x2 = wave_scan(w2);
+        const uint32_t b1 = (uint32_t)__builtin_amdgcn_readlane((int)(x1 - w1), (int)wv);
+        const uint32_t b2 = (uint32_t)__builtin_amdgcn_readlane((int)(x2 - w2), (int)wv);
+        const uint32_t g1 = (uint32_t)__builtin_amdgcn_readlane((int)x1, NW - 1);
+        const uint32_t g2 = (uint32_t)__builtin_amdgcn_readlane((int)x2, NW - 1);
         // every entry of the tile is counted at its coordinate, so with at
         // most 65535 of them no packed field can overflow
         const bool defer = s_flag != 0u || s_total > 65535u || (g1 & 0xFFFFu) > CAP;
@@ -456,24 +467,19 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
             uint32_t srun = e1 & 0xFFFFu, nrun = e1 >> 16, arun = e2 & 0xFFFFu, brun = NA + (e2 >> 16);
 #pragma unroll
             for (int c = 0; c < CPTMAX; ++c) {
-                if ((uint32_t)c < CPT) {
-                    const uint32_t m = mc[c], j = jb + (uint32_t)c;
-                    uint32_t aux = MODE == kSparseWrite ? nrun : 0u;
-                    if (m >= 3u) {
-                        aux = srun;
-                        const uint2 item = make_uint2(j | nrun << 16, srun | m << 16);
-                        if (m <= 4u) s_list[arun++] = item;
-                        else s_list[brun++] = item;
-                        srun += m;
-                    }
-                    nrun += m != 0u ? 1u : 0u;
-                    mc[c] = m | aux << 9;
+                const uint32_t m = mc[c], j = jb + (uint32_t)c;
+                if (m >= 3u) {
+                    // staging range and list slot; s_cnt keeps m | start << 9
+                    const uint2 item = make_uint2(j | nrun << 16, srun | m << 16);
+                    if (m <= 4u) s_list[arun++] = item;
+                    else s_list[brun++] = item;
+                    s_cnt[j] = m | srun << 9;
+                    srun += m;
+                } else if (MODE == kSparseWrite && m != 0u) {
+                    s_cnt[j] = m | nrun << 9;  // output position
                 }
+                nrun += m != 0u ? 1u : 0u;
             }
-#pragma unroll
-            for (int c = 0; c < CPTMAX; c += 4)
-                if ((uint32_t)c < CPT)
-                    *reinterpret_cast<uint4*>(&s_cnt[jb + c]) = make_uint4(mc[c], mc[c + 1], mc[c + 2], mc[c + 3]);
         } else {
 #pragma unroll
             for (int c = 0; c < CPTMAX; c += 4) {
@@ -639,6 +645,68 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
                 const uint2 item = s_list[i];
                 const uint32_t j = item.x & 0xFFFFu, nz = item.x >> 16;
                 const uint32_t st0 = item.y & 0xFFFFu, m = item.y >> 16;
+                if (m <= 8u) {
+                    // up to eight: all reads at once, a sorting network (ranks
+                    // past m are distinct sentinels above every rank), then
+                    // the separator stack over the sorted run
+                    uint32_t rk[8];
+                    float vv[8];
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) {
+                        const uint32_t rr = s_sr[st0 + e];
+                        const float v = VALS ? s_sv[st0 + e] : 0.0f;
+                        rk[e] = (uint32_t)e < m ? rr : 0x100u + (uint32_t)e;
+                        vv[e] = v;
+                    }
+                    auto cswap = [&](int x, int y) {
+                        const bool sw = rk[x] > rk[y];
+                        const uint32_t tr = rk[x];
+                        const float tv = vv[x];
+                        rk[x] = sw ? rk[y] : rk[x];
+                        rk[y] = sw ? tr : rk[y];
+                        vv[x] = sw ? vv[y] : vv[x];
+                        vv[y] = sw ? tv : vv[y];
+                    };
+                    cswap(0, 2); cswap(1, 3); cswap(4, 6); cswap(5, 7);
+                    cswap(0, 4); cswap(1, 5); cswap(2, 6); cswap(3, 7);
+                    cswap(0, 1); cswap(2, 3); cswap(4, 5); cswap(6, 7);
+                    cswap(2, 4); cswap(3, 5); cswap(1, 4); cswap(3, 6);
+                    cswap(1, 2); cswap(3, 4); cswap(5, 6);
+                    float slot[LMAX];
+#pragma unroll
+                    for (int l = 0; l < LMAX; ++l) slot[l] = 0.0f;
+                    float cur = vv[0];
+                    uint32_t pend = 0u;
+#pragma unroll
+                    for (int e = 1; e < 8; ++e) {
+                        if ((uint32_t)e < m) {
+                            const uint32_t sep = sep_level(rk[e - 1], rk[e]);
+                            if (CNTS) atomicAdd(&s_E[rk[e] * W + sep], 1u);
+                            if (VALS) {
+#pragma unroll
+                                for (int l = 0; l < LMAX; ++l)
+                                    if ((uint32_t)l < sep && ((pend >> l) & 1u)) cur = slot[l] + cur;
+                                pend = (pend & ~((1u << sep) - 1u)) | (1u << sep);
+#pragma unroll
+                                for (int l = 0; l < LMAX; ++l)
+                                    if ((uint32_t)l == sep) slot[l] = cur;
+                                cur = vv[e];
+                            }
+                        }
+                    }
+                    if (VALS) {
+#pragma unroll
+                        for (int l = 0; l < LMAX; ++l)
+                            if ((pend >> l) & 1u) cur = slot[l] + cur;
+                        if (MODE == kDense) {
+                            s_out[j] = cur + 0.0f;
+                        } else {
+                            a.out_idx[toff + nz] = tlo + j;
+                            a.out_val[toff + nz] = cur;
+                        }
+                    }
+                    continue;
+                }
                 uint32_t w[MW];
 #pragma unroll
                 for (int q = 0; q < MW; ++q) w[q] = 0u;
