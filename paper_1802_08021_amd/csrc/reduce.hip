@@ -60,26 +60,24 @@ struct SlowShape {
 
 // Fast tile pass for up to PMAX ranks.  A wave owns SLMAX ranks ("slots");
 // per tile it reads a 64-entry window of each slot's stream (one entry per
-// lane).  Two workgroups share a CU (LDS), so the wave count per SIMD and
-// with it the register budget follow from NT.  TMAX coordinates per tile; CAP staged entries (those of indices
-// held by three or more ranks); SIDE entries of windows that had to be
-// continued because all 64 entries fell inside the tile.
+// lane) and compacts the entries inside the tile into its own region of at
+// most ECAP entries.  TMAX coordinates per tile; CAP staged entries (those
+// of indices held by three or more ranks).  Up to 128 ranks: two 512-thread
+// workgroups per CU (LDS), four waves per SIMD.
 template <int PMAX>
 struct Fast {
-    static constexpr int NT = PMAX <= 32 ? 256 : (PMAX <= 128 ? 512 : 1024);
-    static constexpr int WPE = NT == 256 ? 2 : 4;  // waves per SIMD (LDS and registers)
+    static constexpr int NT = PMAX <= 32 ? 512 : 1024;
+    static constexpr int WPE = 4;                   // waves per SIMD (LDS and registers)
     static constexpr int NW = NT / 64;
-    static constexpr int SLMAX = PMAX / NW;
-    static constexpr int TMAX = 4096;
-    static constexpr int CPTMAX = TMAX / NT;
-    static constexpr uint32_t CAP = 3584;
+    static constexpr int SLMAX = PMAX / NW < 1 ? 1 : PMAX / NW;
+    static constexpr int TMAX = PMAX <= 32 ? 2048 : 4096;
+    static constexpr int CPT = TMAX / NT;           // coordinates per thread (4)
+    static constexpr uint32_t CAP = TMAX * 7 / 8;   // staged entries
     static constexpr uint32_t LCAP = CAP / 3 + 1;
-    static constexpr uint32_t SIDE = 256;
+    static constexpr uint32_t ECAP = 448;           // compacted entries per wave
     static constexpr int LMAX = PMAX <= 16 ? 4 : (PMAX <= 32 ? 5 : (PMAX <= 64 ? 6 : (PMAX <= 128 ? 7 : 8)));
-    static constexpr int MW = PMAX <= 32 ? 1 : PMAX / 32;
 };
 constexpr uint32_t kWin = 64;  // window entries per rank per tile
-constexpr double kStageCap = 3584.0;  // Fast<>::CAP
 
 struct Args {
     const StreamDesc* tab;
@@ -201,23 +199,20 @@ template <int PMAX, int MODE, bool QUANT>
 __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args a)
 {
     using F = Fast<PMAX>;
-    constexpr int NT = F::NT, NW = F::NW, SLMAX = F::SLMAX, TMAX = F::TMAX, CPTMAX = F::CPTMAX;
-    constexpr uint32_t CAP = F::CAP, SIDE = F::SIDE;
-    constexpr int LMAX = F::LMAX, MW = F::MW;
+    constexpr int NT = F::NT, NW = F::NW, SLMAX = F::SLMAX, TMAX = F::TMAX, CPT = F::CPT;
+    constexpr uint32_t CAP = F::CAP, ECAP = F::ECAP;
+    constexpr int LMAX = F::LMAX;
     constexpr bool VALS = MODE != kCount, CNTS = MODE != kSparseWrite;
     constexpr uint32_t EW = PMAX * (LMAX + 1);  // node-count words; 64 dummies follow
 
-    // Every array has 64 dummy words past its end: lanes with nothing to do
-    // aim their (unconditional) LDS accesses there, which keeps the slot
-    // loops free of branches so that their LDS latencies overlap.
-    __shared__ __align__(16) uint32_t s_cnt[TMAX + 64];         // ranks per index; then m | aux << 9
-    __shared__ __align__(16) float s_out[VALS ? TMAX + 64 : 4];  // first value; dense: the sum
-    __shared__ uint8_t s_r0[TMAX + 64];                         // rank of the first arrival
-    __shared__ float s_sv[VALS ? CAP + 64 : 1];                 // staged values
-    __shared__ uint8_t s_sr[CAP + 64];                          // staged ranks
-    __shared__ uint2 s_list[F::LCAP];                           // {j | nzpos << 16, start | m << 16}
+    __shared__ __align__(16) uint32_t s_cnt[TMAX];         // ranks per index; then m | aux << 9
+    __shared__ __align__(16) float s_out[VALS ? TMAX : 4];  // first value; dense: the sum
+    __shared__ uint8_t s_r0[TMAX];                         // rank of the first arrival
+    __shared__ uint2 s_ent[NW * ECAP];                     // per wave: the tile's entries
+    __shared__ float s_sv[VALS ? CAP + 8 : 1];             // staged values (8 readable past the end)
+    __shared__ uint8_t s_sr[CAP + 8];                      // staged ranks
+    __shared__ uint2 s_list[F::LCAP];                      // {j | nzpos << 16, start | m << 16}
     __shared__ uint32_t s_E[CNTS ? EW + 64 : 1];
-    __shared__ uint2 s_side[SIDE];                              // {j | r << 12 | k << 20, value}
     // Per rank (slot) state: {stream position, entries in this tile},
     // {chunk end, last readable entry}, {index base, value base}, level unit.
     // Ranks past P have an empty window over a readable dummy address.
@@ -226,18 +221,21 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
     __shared__ uint4 s_base[PMAX];
     __shared__ float s_unit[PMAX];
     __shared__ uint32_t s_wtot[2 * NW];
-    __shared__ uint32_t s_nside, s_flag, s_total;
+    __shared__ uint32_t s_flag;
+    constexpr int PW = (PMAX + 31) / 32;                   // rank-mask words
+    __shared__ float s_wv[VALS ? NW * PMAX : 1];           // per wave: values by rank
+    __shared__ uint32_t s_wp[NW * PW];                     // per wave: ranks present
 
     const uint32_t tid = threadIdx.x, lane = tid & 63u;
     const uint32_t wv = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const uint32_t P = a.P, L = a.L, W = L + 1, T = a.T, CPT = T / NT;
+    const uint32_t P = a.P, L = a.L, W = L + 1, T = a.T;
     const uint32_t chunk = blockIdx.x, stride = a.nchunks + 1;
     const uint32_t t0 = chunk * a.tpc, t1 = min(t0 + a.tpc, a.ntiles);
     const uint32_t qbits = a.qbits;
     const uint32_t plog = qbits == 8u ? 0u : (qbits == 4u ? 1u : 2u), pm = (1u << plog) - 1u;
+    const uint32_t EB = wv * ECAP;  // this wave's entry region
+    const uint64_t below = (1ull << lane) - 1ull;
 
-    // Slot s of wave wv is rank s*NW + wv (waves interleave, so small P
-    // still spreads over all waves).
     // Loop-invariant values (the per-rank LDS state of every slot, LDS
     // addresses of a thread's coordinates) would be hoisted out of the tile
     // loop and held in registers or spilled; opaque copies of the rank
@@ -250,6 +248,8 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
         asm volatile("" : "+v"(v));
         return v;
     };
+    // Slot s of wave wv is rank s*NW + wv (waves interleave, so small P
+    // still spreads over all waves).
     auto slot_rank = [&](int s) -> uint32_t { return opaque((uint32_t)s * NW + wv); };
     // A slot's {position, tile count} is written by lane 0 of its wave and
     // read by all lanes with no barrier in between.  Plain accesses would let
@@ -287,22 +287,30 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
         s_base[r] = make_uint4((uint32_t)ib, (uint32_t)(ib >> 32), (uint32_t)vb, (uint32_t)(vb >> 32));
         s_unit[r] = unit;
     }
-    for (uint32_t i = tid; i < TMAX + 64; i += NT) {
+    for (uint32_t i = tid; i < TMAX; i += NT) {
         s_cnt[i] = 0u;
         if (VALS) s_out[i] = 0.0f;
     }
     if (CNTS)
         for (uint32_t i = tid; i < EW + 64; i += NT) s_E[i] = 0u;
-    if (tid == 0) {
-        s_nside = 0u;
-        s_flag = 0u;
-        s_total = 0u;
-    }
+    for (uint32_t i = tid; i < (uint32_t)(NW * PW); i += NT) s_wp[i] = 0u;
+    if (tid == 0) s_flag = 0u;
     __syncthreads();
 
-    // Window of rank r at stream position pos: raw index and raw value word
-    // (fp32 bits, or the byte holding the entry's code).  Positions past the
+    // Window of a stream at position pos: raw index and raw value word (fp32
+    // bits, or the byte holding the entry's code).  Positions past the
     // stream's end read its last entry (they lie past the chunk end too).
+    auto load_win_at = [&](const uint4& b, uint32_t last, uint32_t pos, uint32_t& x, uint32_t& v) {
+        const uint32_t i = min(pos + lane, last);
+        const uint64_t ib = ((uint64_t)b.y << 32) | b.x;
+        x = *reinterpret_cast<g_u32*>(ib + 4ull * i);
+        v = 0u;
+        if (VALS) {
+            const uint64_t vb = ((uint64_t)b.w << 32) | b.z;
+            if (QUANT) v = *reinterpret_cast<g_u8*>(vb + (i >> plog));
+            else v = *reinterpret_cast<g_u32*>(vb + 4ull * i);
+        }
+    };
     auto load_win = [&](uint32_t r, uint32_t pos, uint32_t& x, uint32_t& v) {
         const uint4 b = s_base[r];
         const uint32_t i = min(pos + lane, s_el[r].y);
@@ -315,16 +323,16 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
             else v = *reinterpret_cast<g_u32*>(vb + 4ull * i);
         }
     };
-    auto decode = [&](uint32_t v, uint32_t pos, float unit) -> float {
-        if (QUANT) {
-            const uint32_t code = (v >> (((lane + pos) & pm) * qbits)) & ((1u << qbits) - 1u);
-            return dequant(code, qbits, unit);
+    // Append the in-tile entries of a window to this wave's entry region:
+    // {j | rank << 12 | code position in its byte << 20, raw value word}.
+    auto compact = [&](bool in, uint64_t bal, uint32_t base, uint32_t j, uint32_t r, uint32_t pos, uint32_t v) {
+        if (in) {
+            const uint32_t at = base + (uint32_t)__popcll(bal & below);
+            if (at < ECAP) s_ent[EB + at] = make_uint2(j | r << 12 | ((lane + pos) & pm) << 20, v);
         }
-        return __uint_as_float(v);
     };
 
-    // xr: raw window index, then (entry in the tile) j | arrival << 12, or
-    // ~0 for an entry outside the tile; vr: raw value word, then the value.
+    // xr, vr: raw window words of every slot (in flight during a tile).
     uint32_t xr[SLMAX], vr[SLMAX];
 #pragma unroll
     for (int s = 0; s < SLMAX; ++s) load_win(slot_rank(s), pn_get(slot_rank(s)).x, xr[s], vr[s]);
@@ -333,115 +341,111 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
         const uint32_t tlo = tile * T;
         const uint32_t TT = (uint32_t)min((uint64_t)T, (uint64_t)a.N - tlo);  // tile width
 
-        // P1: arrival numbers (all atomics issued before any result is
-        // used), then the first arrivals' ranks and values.
-        uint32_t full = 0u, wtot = 0u;
-        uint32_t kk[SLMAX];
-        // slots in groups: the group's state reads are issued together
-        constexpr int G1 = SLMAX < 8 ? SLMAX : 8;
+        // P1w: the in-tile entries of every window, compacted into this
+        // wave's region (no other wave touches it, so no barrier follows).
+        // A window entirely inside the tile is continued at once; then the
+        // slot's next window is requested, so that its load overlaps the
+        // rest of this tile.
+        uint32_t nent = 0u;
+        // This tile's windows were requested a whole tile ago: wait for all of
+        // them here, once (vmcnt(0)), so that no later use waits behind the
+        // next tile's requests issued below.
+        __builtin_amdgcn_s_waitcnt(0x0F70);
+        constexpr int G1 = SLMAX < 4 ? SLMAX : 4;
 #pragma unroll
         for (int g0 = 0; g0 < SLMAX; g0 += G1) {
-            uint32_t ps[G1], es[G1];
-            float us[G1];
+            uint2 pe[G1], el[G1];
+            uint4 bs[G1];
 #pragma unroll
             for (int q = 0; q < G1; ++q) {
                 const uint32_t r = slot_rank(g0 + q);
-                ps[q] = pn_get(r).x;
-                es[q] = s_el[r].x;
-                us[q] = QUANT && VALS ? s_unit[r] : 0.0f;
+                pe[q] = pn_get(r);
+                el[q] = s_el[r];
+                bs[q] = s_base[r];
             }
 #pragma unroll
             for (int q = 0; q < G1; ++q) {
                 const int s = g0 + q;
-                const uint32_t pos = ps[q], avail = es[q] - pos;
+                const uint32_t r = slot_rank(s);
+                uint32_t pos = pe[q].x;
                 const uint32_t j = xr[s] - tlo;
-                const bool in = j < TT && lane < avail;
-                const uint32_t jd = in ? j : (uint32_t)TMAX + lane;
-                kk[s] = atomicAdd(&s_cnt[jd], 1u);
-                if (VALS) vr[s] = __float_as_uint(decode(vr[s], pos, us[q]));
-                const uint32_t n = (uint32_t)__popcll(__ballot(in));
-                if (lane == 0u) pn_set(slot_rank(s), pos + n, n);
-                full |= (n == kWin ? 1u : 0u) << s;
-                wtot += n;
-                xr[s] = jd;
+                const bool in = j < TT && lane < el[q].x - pos;
+                const uint64_t bal = __ballot(in);
+                uint32_t n = (uint32_t)__popcll(bal);
+                compact(in, bal, nent, j, r, pos, vr[s]);
+                nent += n;
+                pos += n;
+                uint32_t cnt = n;
+                if (n == kWin) {  // rare: continue the window
+                    do {
+                        uint32_t x2, v2;
+                        load_win_at(bs[q], el[q].y, pos, x2, v2);
+                        const uint32_t j2 = x2 - tlo;
+                        const bool in2 = j2 < TT && lane < el[q].x - pos;
+                        const uint64_t bal2 = __ballot(in2);
+                        n = (uint32_t)__popcll(bal2);
+                        compact(in2, bal2, nent, j2, r, pos, v2);
+                        nent += n;
+                        pos += n;
+                        cnt += n;
+                    } while (n == kWin);
+                }
+                if (lane == 0u) pn_set(r, pos, cnt);
+                load_win_at(bs[q], el[q].y, pos, xr[s], vr[s]);
             }
         }
-#pragma unroll
-        for (int s = 0; s < SLMAX; ++s) {
-            const bool in = xr[s] < (uint32_t)TMAX;
-            const bool first = in && kk[s] == 0u;
-            const uint32_t jf = first ? xr[s] : (uint32_t)TMAX + lane;
-            s_r0[jf] = (uint8_t)slot_rank(s);
-            if (VALS) s_out[jf] = MODE == kDense ? __uint_as_float(vr[s]) + 0.0f : __uint_as_float(vr[s]);
-            xr[s] = in ? xr[s] | kk[s] << 12 : ~0u;
-        }
+        if (nent > ECAP && lane == 0u) s_flag = 1u;
+        const uint32_t ne_w = min(nent, ECAP);
 
-        // Windows entirely inside the tile: continue them into the side buffer.
-        while (full) {
-            const int s = __builtin_ctz(full);
-            full &= full - 1u;
-            const uint32_t r = slot_rank(s);
-            const float unit = s_unit[r];
-            uint32_t n;
-            do {
-                const uint2 pn = pn_get(r);
-                const uint32_t pos = pn.x, avail = s_el[r].x - pos;
-                uint32_t x, v;
-                load_win(r, pos, x, v);
-                const uint32_t j = x - tlo;
-                const bool in = j < TT && lane < avail;
-                const uint64_t bal = __ballot(in);
-                n = (uint32_t)__popcll(bal);
-                uint32_t k = ~0u;
-                if (in) k = atomicAdd(&s_cnt[j], 1u);
-                const float val = VALS ? decode(v, pos, unit) : 0.0f;
-                uint32_t base = 0u;
-                if (lane == 0u && n) base = atomicAdd(&s_nside, n);
-                base = (uint32_t)__builtin_amdgcn_readfirstlane((int)base);
-                if (in) {
-                    if (k == 0u) {
-                        s_r0[j] = (uint8_t)r;
-                        if (VALS) s_out[j] = MODE == kDense ? val + 0.0f : val;
-                    }
-                    const uint32_t at = base + (uint32_t)__popcll(bal & ((1ull << lane) - 1ull));
-                    if (at < SIDE) s_side[at] = make_uint2(j | r << 12 | k << 20, __float_as_uint(val));
+        // P1e: arrival numbers of this wave's entries; the first arrival
+        // leaves its rank and value at the index.  The entry keeps its
+        // arrival number and decoded value.  (Lanes now read entries other
+        // lanes of the wave wrote: the fence orders them for the compiler.)
+        __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+        for (uint32_t e = lane; e < ne_w; e += 64u) {
+            const uint2 en = s_ent[EB + e];
+            const uint32_t j = en.x & 0xFFFu, r = (en.x >> 12) & 0xFFu;
+            const uint32_t k = atomicAdd(&s_cnt[j], 1u);
+            float v = 0.0f;
+            if (VALS) {
+                if (QUANT) {
+                    const uint32_t code = (en.y >> (((en.x >> 20) & 3u) * qbits)) & ((1u << qbits) - 1u);
+                    v = dequant(code, qbits, s_unit[r]);
+                } else {
+                    v = __uint_as_float(en.y);
                 }
-                if (lane == 0u) {
-                    if (base + n > SIDE) s_flag = 1u;
-                    pn_set(r, pos + n, pn.y + n);
-                }
-                wtot += n;
-            } while (n == kWin);
+            }
+            if (k == 0u) {
+                s_r0[j] = (uint8_t)r;
+                if (VALS) s_out[j] = MODE == kDense ? v + 0.0f : v;
+            }
+            s_ent[EB + e] = make_uint2((en.x & 0xFFFFFu) | k << 20, __float_as_uint(v));
         }
-        if (lane == 0u && wtot) atomicAdd(&s_total, wtot);
-
         __syncthreads();
 
         // Scan over this thread's CPT consecutive coordinates.
         const uint32_t jb = opaque_v(tid) * CPT;
-        uint32_t mc[CPTMAX];
+        uint32_t mc[CPT];
 #pragma unroll
-        for (int c = 0; c < CPTMAX; c += 4) {
-            if ((uint32_t)c < CPT) {
-                const uint4 q = *reinterpret_cast<const uint4*>(&s_cnt[jb + c]);
-                mc[c] = q.x;
-                mc[c + 1] = q.y;
-                mc[c + 2] = q.z;
-                mc[c + 3] = q.w;
-            } else {
-                mc[c] = mc[c + 1] = mc[c + 2] = mc[c + 3] = 0u;
-            }
+        for (int c = 0; c < CPT; c += 4) {
+            const uint4 q = *reinterpret_cast<const uint4*>(&s_cnt[jb + c]);
+            mc[c] = q.x;
+            mc[c + 1] = q.y;
+            mc[c + 2] = q.z;
+            mc[c + 3] = q.w;
         }
-        uint32_t st = 0u, ne = 0u, na = 0u, nb = 0u;
+        uint32_t st = 0u, ne = 0u, na = 0u, nb = 0u, nc = 0u;
 #pragma unroll
-        for (int c = 0; c < CPTMAX; ++c) {
+        for (int c = 0; c < CPT; ++c) {
             const uint32_t m = mc[c];
             ne += m != 0u ? 1u : 0u;
             st += m >= 3u ? m : 0u;
             na += m - 3u < 2u ? 1u : 0u;
-            nb += m >= 5u ? 1u : 0u;
+            nb += m - 5u < 4u ? 1u : 0u;
+            nc += m > 8u ? 1u : 0u;
         }
-        const uint32_t p1 = st | ne << 16, p2 = na | nb << 16;
+        // with at most CAP staged entries: na < 2^11, nb < 2^10, nc < 2^9
+        const uint32_t p1 = st | ne << 16, p2 = na | nb << 11 | nc << 21;
         const uint32_t i1 = wave_scan(p1), i2 = wave_scan(p2);
         if (lane == 63u) {
             s_wtot[wv] = i1;
@@ -457,22 +461,23 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
         const uint32_t b2 = (uint32_t)__builtin_amdgcn_readlane((int)(x2 - w2), (int)wv);
         const uint32_t g1 = (uint32_t)__builtin_amdgcn_readlane((int)x1, NW - 1);
         const uint32_t g2 = (uint32_t)__builtin_amdgcn_readlane((int)x2, NW - 1);
-        // every entry of the tile is counted at its coordinate, so with at
-        // most 65535 of them no packed field can overflow
-        const bool defer = s_flag != 0u || s_total > 65535u || (g1 & 0xFFFFu) > CAP;
-        const uint32_t NE = g1 >> 16, NA = g2 & 0xFFFFu, NB = g2 >> 16;
+        // at most NW*ECAP (< 65536) entries: no packed field overflows
+        const bool defer = s_flag != 0u || (g1 & 0xFFFFu) > CAP;
+        const uint32_t NE = g1 >> 16, NA = g2 & 0x7FFu, NB = (g2 >> 11) & 0x3FFu, NC = g2 >> 21;
         if (!defer) {
             if (CNTS && tid == 0) a.tile_cnt[tile] = NE;
             const uint32_t e1 = i1 - p1 + b1, e2 = i2 - p2 + b2;
-            uint32_t srun = e1 & 0xFFFFu, nrun = e1 >> 16, arun = e2 & 0xFFFFu, brun = NA + (e2 >> 16);
+            uint32_t srun = e1 & 0xFFFFu, nrun = e1 >> 16;
+            uint32_t arun = e2 & 0x7FFu, brun = NA + ((e2 >> 11) & 0x3FFu), crun = NA + NB + (e2 >> 21);
 #pragma unroll
-            for (int c = 0; c < CPTMAX; ++c) {
+            for (int c = 0; c < CPT; ++c) {
                 const uint32_t m = mc[c], j = jb + (uint32_t)c;
                 if (m >= 3u) {
                     // staging range and list slot; s_cnt keeps m | start << 9
                     const uint2 item = make_uint2(j | nrun << 16, srun | m << 16);
                     if (m <= 4u) s_list[arun++] = item;
-                    else s_list[brun++] = item;
+                    else if (m <= 8u) s_list[brun++] = item;
+                    else s_list[crun++] = item;
                     s_cnt[j] = m | srun << 9;
                     srun += m;
                 } else if (MODE == kSparseWrite && m != 0u) {
@@ -482,86 +487,34 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
             }
         } else {
 #pragma unroll
-            for (int c = 0; c < CPTMAX; c += 4) {
-                if ((uint32_t)c < CPT) {
-                    *reinterpret_cast<uint4*>(&s_cnt[jb + c]) = make_uint4(0u, 0u, 0u, 0u);
-                    if (VALS) *reinterpret_cast<float4*>(&s_out[jb + c]) = make_float4(0.f, 0.f, 0.f, 0.f);
-                }
+            for (int c = 0; c < CPT; c += 4) {
+                *reinterpret_cast<uint4*>(&s_cnt[jb + c]) = make_uint4(0u, 0u, 0u, 0u);
+                if (VALS) *reinterpret_cast<float4*>(&s_out[jb + c]) = make_float4(0.f, 0.f, 0.f, 0.f);
             }
             if (tid == 0) {
                 const uint32_t k = atomicAdd(a.slow_count, 1u);
                 a.slow_list[k] = tile;
             }
-#pragma unroll
-            for (int s = 0; s < SLMAX; ++s) load_win(slot_rank(s), pn_get(slot_rank(s)).x, xr[s], vr[s]);
         }
         __syncthreads();
 
         if (!defer) {
-            // P2
+            // P2: per entry of this wave: m = 1 done (the first value
+            // stands); m = 2: the second arrival adds its value to the first
+            // -- a single addition is the same in either order -- and counts
+            // the pair for the node sizes; m >= 3: staged at its index's
+            // range in arrival order.
             if (CNTS)
                 for (uint32_t r = tid; r < P; r += NT) s_E[r * W + L] += pn_get(r).y;
             const uint32_t toff = MODE == kSparseWrite ? a.tile_off[tile] : 0u;
-            // Slots in groups of G: (a) the counts of every entry's index,
-            // all reads in flight at once; (b) staging of entries at indices
-            // with >= 3 ranks, and the first value and rank fetched for the
-            // second of two; (c) the pairs' node counts and sums.
-            constexpr int G = 4;
-#pragma unroll
-            for (int g0 = 0; g0 < SLMAX; g0 += G) {
-                uint32_t sc[G], r0s[G];
-                float o0s[G];
-#pragma unroll
-                for (int q = 0; q < G; ++q) sc[q] = s_cnt[xr[g0 + q] & 0xFFFu];
-#pragma unroll
-                for (int q = 0; q < G; ++q) {
-                    const int s = g0 + q;
-                    const bool valid = xr[s] != ~0u;
-                    const uint32_t j = xr[s] & 0xFFFu, k = xr[s] >> 12;
-                    const uint32_t m = sc[q] & 0x1FFu, aux = sc[q] >> 9;
-                    const uint32_t at = valid && m >= 3u ? aux + k : CAP + lane;
-                    s_sr[at] = (uint8_t)slot_rank(s);
-                    if (VALS) s_sv[at] = __uint_as_float(vr[s]);
-                    const bool pair = valid && m == 2u && k == 1u;
-                    const uint32_t pj = pair ? j : (uint32_t)TMAX + lane;
-                    r0s[q] = s_r0[pj];
-                    o0s[q] = VALS ? s_out[pj] : 0.0f;
-                    if (MODE == kSparseWrite && valid && m == 1u) {
-                        a.out_idx[toff + aux] = tlo + j;
-                        a.out_val[toff + aux] = __uint_as_float(vr[s]);
-                    }
-                }
-#pragma unroll
-                for (int q = 0; q < G; ++q) {
-                    const int s = g0 + q;
-                    const bool valid = xr[s] != ~0u;
-                    const uint32_t j = xr[s] & 0xFFFu, k = xr[s] >> 12;
-                    const uint32_t m = sc[q] & 0x1FFu, aux = sc[q] >> 9;
-                    const uint32_t r = slot_rank(s);
-                    const bool pair = valid && m == 2u && k == 1u;
-                    if (CNTS) {
-                        const uint32_t e = pair ? max(r0s[q], r) * W + sep_level(r0s[q], r) : EW + lane;
-                        atomicAdd(&s_E[e], 1u);
-                    }
-                    if (MODE == kDense) {
-                        s_out[pair ? j : (uint32_t)TMAX + lane] = o0s[q] + __uint_as_float(vr[s]);
-                    } else if (MODE == kSparseWrite && pair) {
-                        a.out_idx[toff + aux] = tlo + j;
-                        a.out_val[toff + aux] = o0s[q] + __uint_as_float(vr[s]);
-                    }
-                }
-                // this group's entries are done: request its next windows
-                // (they overlap the walk and the next tile's start)
-#pragma unroll
-                for (int q = 0; q < G; ++q) load_win(slot_rank(g0 + q), pn_get(slot_rank(g0 + q)).x, xr[g0 + q], vr[g0 + q]);
-            }
-            // continued windows' entries
-            auto entry = [&](uint32_t j, uint32_t r, uint32_t k, float v) {
-                const uint32_t sc1 = s_cnt[j], m = sc1 & 0x1FFu, aux = sc1 >> 9;
+            for (uint32_t e = lane; e < ne_w; e += 64u) {
+                const uint2 en = s_ent[EB + e];
+                const uint32_t j = en.x & 0xFFFu, r = (en.x >> 12) & 0xFFu, k = en.x >> 20;
+                const float v = __uint_as_float(en.y);
+                const uint32_t sc = s_cnt[j], m = sc & 0x1FFu, aux = sc >> 9;
                 if (m >= 3u) {
-                    const uint32_t at = aux + k;
-                    s_sr[at] = (uint8_t)r;
-                    if (VALS) s_sv[at] = v;
+                    s_sr[aux + k] = (uint8_t)r;
+                    if (VALS) s_sv[aux + k] = v;
                 } else if (m == 2u) {
                     if (k == 1u) {
                         const uint32_t r0 = s_r0[j];
@@ -580,11 +533,6 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
                     a.out_idx[toff + aux] = tlo + j;
                     a.out_val[toff + aux] = v;
                 }
-            };
-            const uint32_t nside = min(s_nside, SIDE);
-            for (uint32_t i = tid; i < nside; i += NT) {
-                const uint2 e = s_side[i];
-                entry(e.x & 0xFFFu, (e.x >> 12) & 0xFFu, e.x >> 20, __uint_as_float(e.y));
             }
             __syncthreads();
 
@@ -640,136 +588,57 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
                     }
                 }
             }
-            // Walk: indices with five or more ranks.
+            // Walk: indices with five to eight ranks, one per thread.
             for (uint32_t i = NA + tid; i < NA + NB; i += NT) {
                 const uint2 item = s_list[i];
                 const uint32_t j = item.x & 0xFFFFu, nz = item.x >> 16;
                 const uint32_t st0 = item.y & 0xFFFFu, m = item.y >> 16;
-                if (m <= 8u) {
-                    // up to eight: all reads at once, a sorting network (ranks
-                    // past m are distinct sentinels above every rank), then
-                    // the separator stack over the sorted run
-                    uint32_t rk[8];
-                    float vv[8];
+                // up to eight: all reads at once, a sorting network (ranks
+                // past m are distinct sentinels above every rank), then
+                // the separator stack over the sorted run
+                uint32_t rk[8];
+                float vv[8];
 #pragma unroll
-                    for (int e = 0; e < 8; ++e) {
-                        const uint32_t rr = s_sr[st0 + e];
-                        const float v = VALS ? s_sv[st0 + e] : 0.0f;
-                        rk[e] = (uint32_t)e < m ? rr : 0x100u + (uint32_t)e;
-                        vv[e] = v;
-                    }
-                    auto cswap = [&](int x, int y) {
-                        const bool sw = rk[x] > rk[y];
-                        const uint32_t tr = rk[x];
-                        const float tv = vv[x];
-                        rk[x] = sw ? rk[y] : rk[x];
-                        rk[y] = sw ? tr : rk[y];
-                        vv[x] = sw ? vv[y] : vv[x];
-                        vv[y] = sw ? tv : vv[y];
-                    };
-                    cswap(0, 2); cswap(1, 3); cswap(4, 6); cswap(5, 7);
-                    cswap(0, 4); cswap(1, 5); cswap(2, 6); cswap(3, 7);
-                    cswap(0, 1); cswap(2, 3); cswap(4, 5); cswap(6, 7);
-                    cswap(2, 4); cswap(3, 5); cswap(1, 4); cswap(3, 6);
-                    cswap(1, 2); cswap(3, 4); cswap(5, 6);
-                    float slot[LMAX];
-#pragma unroll
-                    for (int l = 0; l < LMAX; ++l) slot[l] = 0.0f;
-                    float cur = vv[0];
-                    uint32_t pend = 0u;
-#pragma unroll
-                    for (int e = 1; e < 8; ++e) {
-                        if ((uint32_t)e < m) {
-                            const uint32_t sep = sep_level(rk[e - 1], rk[e]);
-                            if (CNTS) atomicAdd(&s_E[rk[e] * W + sep], 1u);
-                            if (VALS) {
-#pragma unroll
-                                for (int l = 0; l < LMAX; ++l)
-                                    if ((uint32_t)l < sep && ((pend >> l) & 1u)) cur = slot[l] + cur;
-                                pend = (pend & ~((1u << sep) - 1u)) | (1u << sep);
-#pragma unroll
-                                for (int l = 0; l < LMAX; ++l)
-                                    if ((uint32_t)l == sep) slot[l] = cur;
-                                cur = vv[e];
-                            }
-                        }
-                    }
-                    if (VALS) {
-#pragma unroll
-                        for (int l = 0; l < LMAX; ++l)
-                            if ((pend >> l) & 1u) cur = slot[l] + cur;
-                        if (MODE == kDense) {
-                            s_out[j] = cur + 0.0f;
-                        } else {
-                            a.out_idx[toff + nz] = tlo + j;
-                            a.out_val[toff + nz] = cur;
-                        }
-                    }
-                    continue;
+                for (int e = 0; e < 8; ++e) {
+                    const uint32_t rr = s_sr[st0 + e];
+                    const float v = VALS ? s_sv[st0 + e] : 0.0f;
+                    rk[e] = (uint32_t)e < m ? rr : 0x100u + (uint32_t)e;
+                    vv[e] = v;
                 }
-                uint32_t w[MW];
-#pragma unroll
-                for (int q = 0; q < MW; ++q) w[q] = 0u;
-                for (uint32_t e = 0; e < m; ++e) {
-                    const uint32_t r = s_sr[st0 + e];
-#pragma unroll
-                    for (int q = 0; q < MW; ++q) w[q] |= (r >> 5) == (uint32_t)q ? 1u << (r & 31u) : 0u;
-                }
-                if (VALS) {
-                    // rank order: entry of rank r goes to the number of
-                    // present ranks below r (cycle placement, in place)
-                    auto rank_pos = [&](uint32_t r) -> uint32_t {
-                        uint32_t below = 0u;
-#pragma unroll
-                        for (int q = 0; q < MW; ++q)
-                            below += (uint32_t)q < (r >> 5) ? (uint32_t)__popc(w[q])
-                                     : ((uint32_t)q == (r >> 5) ? (uint32_t)__popc(w[q] & ((1u << (r & 31u)) - 1u)) : 0u);
-                        return below;
-                    };
-                    for (uint32_t e = 0; e < m; ++e) {
-                        uint32_t r = s_sr[st0 + e];
-                        float v = s_sv[st0 + e];
-                        uint32_t p = rank_pos(r);
-                        for (uint32_t guard = 0; p != e && guard < m; ++guard) {
-                            const uint32_t r2 = s_sr[st0 + p];
-                            const float v2 = s_sv[st0 + p];
-                            s_sr[st0 + p] = (uint8_t)r;
-                            s_sv[st0 + p] = v;
-                            r = r2;
-                            v = v2;
-                            p = rank_pos(r);
-                        }
-                        s_sr[st0 + e] = (uint8_t)r;
-                        s_sv[st0 + e] = v;
-                    }
-                }
+                auto cswap = [&](int x, int y) {
+                    const bool sw = rk[x] > rk[y];
+                    const uint32_t tr = rk[x];
+                    const float tv = vv[x];
+                    rk[x] = sw ? rk[y] : rk[x];
+                    rk[y] = sw ? tr : rk[y];
+                    vv[x] = sw ? vv[y] : vv[x];
+                    vv[y] = sw ? tv : vv[y];
+                };
+                cswap(0, 2); cswap(1, 3); cswap(4, 6); cswap(5, 7);
+                cswap(0, 4); cswap(1, 5); cswap(2, 6); cswap(3, 7);
+                cswap(0, 1); cswap(2, 3); cswap(4, 5); cswap(6, 7);
+                cswap(2, 4); cswap(3, 5); cswap(1, 4); cswap(3, 6);
+                cswap(1, 2); cswap(3, 4); cswap(5, 6);
                 float slot[LMAX];
 #pragma unroll
                 for (int l = 0; l < LMAX; ++l) slot[l] = 0.0f;
-                float cur = 0.0f;
-                uint32_t pend = 0u, at = st0;
-                int last = -1;
+                float cur = vv[0];
+                uint32_t pend = 0u;
 #pragma unroll
-                for (int q = 0; q < MW; ++q) {
-                    uint32_t bits = w[q];
-                    while (bits) {
-                        const int r = q * 32 + (__ffs(bits) - 1);
-                        bits &= bits - 1u;
-                        if (last >= 0) {
-                            const uint32_t sep = sep_level((uint32_t)r, (uint32_t)last);
-                            if (CNTS) atomicAdd(&s_E[(uint32_t)r * W + sep], 1u);
-                            if (VALS) {
+                for (int e = 1; e < 8; ++e) {
+                    if ((uint32_t)e < m) {
+                        const uint32_t sep = sep_level(rk[e - 1], rk[e]);
+                        if (CNTS) atomicAdd(&s_E[rk[e] * W + sep], 1u);
+                        if (VALS) {
 #pragma unroll
-                                for (int l = 0; l < LMAX; ++l)
-                                    if ((uint32_t)l < sep && ((pend >> l) & 1u)) cur = slot[l] + cur;
-                                pend = (pend & ~((1u << sep) - 1u)) | (1u << sep);
+                            for (int l = 0; l < LMAX; ++l)
+                                if ((uint32_t)l < sep && ((pend >> l) & 1u)) cur = slot[l] + cur;
+                            pend = (pend & ~((1u << sep) - 1u)) | (1u << sep);
 #pragma unroll
-                                for (int l = 0; l < LMAX; ++l)
-                                    if ((uint32_t)l == sep) slot[l] = cur;
-                            }
+                            for (int l = 0; l < LMAX; ++l)
+                                if ((uint32_t)l == sep) slot[l] = cur;
+                            cur = vv[e];
                         }
-                        if (VALS) cur = s_sv[at++];
-                        last = r;
                     }
                 }
                 if (VALS) {
@@ -783,6 +652,82 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
                         a.out_val[toff + nz] = cur;
                     }
                 }
+            }
+            // Walk: indices with more than eight ranks, one per wave.  The
+            // values are laid out by rank (lane l holds ranks l*K .. l*K+K-1)
+            // and the tree is evaluated level by level: a node is the sum of
+            // its two children when both hold a value, else the one that
+            // does -- the recursive doubling of the ranks present.
+            for (uint32_t i = NA + NB + wv; i < NA + NB + NC; i += NW) {
+                const uint2 item = s_list[i];
+                const uint32_t j = item.x & 0xFFFFu, nz = item.x >> 16;
+                const uint32_t st0 = item.y & 0xFFFFu, m = item.y >> 16;
+                float* wval = s_wv + wv * PMAX;
+                uint32_t* wpre = s_wp + wv * PW;
+                for (uint32_t e = lane; e < m; e += 64u) {
+                    const uint32_t r = s_sr[st0 + e];
+                    if (VALS) wval[r] = s_sv[st0 + e];
+                    atomicOr(&wpre[r >> 5], 1u << (r & 31u));
+                }
+                __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+                uint32_t pw[PW];
+#pragma unroll
+                for (int q = 0; q < PW; ++q) pw[q] = wpre[q];
+                constexpr int K = PMAX > 64 ? PMAX / 64 : 1;
+                float lv[K];
+                bool lp[K];
+#pragma unroll
+                for (int q = 0; q < K; ++q) {
+                    const uint32_t r = lane * K + (uint32_t)q;
+                    uint32_t word = 0u;
+#pragma unroll
+                    for (int w2 = 0; w2 < PW; ++w2) word = (uint32_t)w2 == (r >> 5) ? pw[w2] : word;
+                    lp[q] = r < (uint32_t)PMAX && ((word >> (r & 31u)) & 1u);
+                    lv[q] = VALS && lp[q] ? wval[r] : 0.0f;
+                    if (CNTS && lp[q]) {
+                        // predecessor: the highest present rank below r
+                        int pred = -1;
+#pragma unroll
+                        for (int w2 = 0; w2 < PW; ++w2) {
+                            const uint32_t mk = (uint32_t)w2 < (r >> 5) ? pw[w2]
+                                              : ((uint32_t)w2 == (r >> 5) ? pw[w2] & ((1u << (r & 31u)) - 1u) : 0u);
+                            if (mk) pred = w2 * 32 + 31 - (int)__clz(mk);
+                        }
+                        if (pred >= 0) atomicAdd(&s_E[r * W + sep_level((uint32_t)pred, r)], 1u);
+                    }
+                }
+                if (VALS) {
+                    // levels inside the lane, then across lanes
+#pragma unroll
+                    for (int h = 1; h < K; h <<= 1) {
+#pragma unroll
+                        for (int q = 0; q < K; q += 2 * h) {
+                            lv[q] = lp[q] && lp[q + h] ? lv[q] + lv[q + h] : (lp[q] ? lv[q] : lv[q + h]);
+                            lp[q] = lp[q] || lp[q + h];
+                        }
+                    }
+                    float v = lv[0];
+                    uint32_t pr = lp[0] ? 1u : 0u;
+#pragma unroll
+                    for (uint32_t sh = 1; sh < 64u; sh <<= 1) {
+                        const float ov = __shfl_down(v, sh);
+                        const uint32_t op = (uint32_t)__shfl_down((int)pr, sh);
+                        if ((lane & (2u * sh - 1u)) == 0u) {
+                            v = pr && op ? v + ov : (pr ? v : ov);
+                            pr |= op;
+                        }
+                    }
+                    if (lane == 0u) {
+                        if (MODE == kDense) {
+                            s_out[j] = v + 0.0f;
+                        } else {
+                            a.out_idx[toff + nz] = tlo + j;
+                            a.out_val[toff + nz] = v;
+                        }
+                    }
+                }
+                if (lane < (uint32_t)PW) wpre[lane] = 0u;
+                __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
             }
             __syncthreads();
 
@@ -804,11 +749,7 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
                 *reinterpret_cast<uint4*>(&s_cnt[c]) = make_uint4(0u, 0u, 0u, 0u);
             }
         }
-        if (tid == 0) {
-            s_nside = 0u;
-            s_flag = 0u;
-            s_total = 0u;
-        }
+        if (tid == 0) s_flag = 0u;
         __syncthreads();
     }
     __syncthreads();
@@ -1148,18 +1089,8 @@ int reduce_plan(int P, uint64_t N, uint64_t max_nnz, uint64_t sum_nnz, double de
     p.L = 0;
     while ((1u << p.L) < p.P) ++p.L;
     p.PK = p.P <= 16 ? 16u : (p.P <= 32 ? 32u : (p.P <= 64 ? 64u : (p.P <= 128 ? 128u : 256u)));
-    // Tile size: the largest multiple of 4*NT up to 4096 for which the
-    // densest stream puts at most 42 entries of a 64-entry window into a
-    // tile and, with the entries spread uniformly (Poisson model of the
-    // ranks present per index, mean lambda), the entries of indices held by
-    // three or more ranks fill at most 60% of the staging capacity.
-    const uint64_t NTq = p.PK <= 32 ? 256 : (p.PK <= 128 ? 512 : 1024), TMIN = 4 * NTq, TMAXq = 4096;
-    const double lam = (double)sum_nnz / (double)N;
-    const double e = std::exp(-lam);
-    const double staged = std::max(0.0, lam - lam * e - lam * lam * e);  // E[m; m >= 3]
-    const double dens = (double)max_nnz / (double)N;
-    uint64_t T = TMAXq;
-    while (T > TMIN && ((double)T * dens > 42.0 || (double)T * staged > 0.6 * kStageCap)) T -= TMIN;
+    // Tile size: fixed per rank class (the LDS layout of the tile pass).
+    const uint64_t T = p.PK <= 32 ? 2048 : 4096;
     p.T = (uint32_t)T;
     p.N = N;
     p.ntiles = (uint32_t)((N + T - 1) / T);

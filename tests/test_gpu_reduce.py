@@ -151,3 +151,40 @@ def test_run_twice_is_bitwise_identical():
     assert a["dense"] == b["dense"]
     np.testing.assert_array_equal(a["val"].view(np.uint32), b["val"].view(np.uint32))
     np.testing.assert_array_equal(a["node_nnz"], b["node_nnz"])
+
+
+@pytest.mark.parametrize("P", [16, 64, 128, 256])
+def test_heavy_overlap_many_ranks(P):
+    """Indices shared by many ranks, up to all P: every per-index path (two,
+    three-four, five-eight and more than eight ranks) in one reduce."""
+    rng = np.random.default_rng(700 + P)
+    N = 50021
+    core = inputs.uniform_subset(rng, N, 300)
+    idx, val = [], []
+    for _ in range(P):
+        keep = core[rng.random(core.size) < rng.uniform(0.3, 1.0)]
+        extra = inputs.uniform_subset(rng, N, int(rng.integers(0, 2000)))
+        a = np.union1d(keep, extra).astype(np.uint32)
+        idx.append(a)
+        val.append(inputs.normal(rng, a.size))
+    for delta in (1.0, 0.02):
+        check(idx, val, N, delta, f"overlap P={P} delta={delta}")
+
+
+@pytest.mark.parametrize("P", [4, 32, 128])
+def test_runs_of_consecutive_indices(P):
+    """Streams with long runs of consecutive indices: a rank's whole
+    64-entry window falls inside one tile and has to be continued."""
+    rng = np.random.default_rng(800 + P)
+    N = 300007
+    idx, val = [], []
+    for _ in range(P):
+        parts = [inputs.uniform_subset(rng, N, int(rng.integers(0, 500)))]
+        for _ in range(int(rng.integers(1, 4))):
+            start = int(rng.integers(0, N - 700))
+            parts.append(np.arange(start, start + int(rng.integers(64, 700)), dtype=np.uint32))
+        a = np.unique(np.concatenate(parts)).astype(np.uint32)
+        idx.append(a)
+        val.append(inputs.normal(rng, a.size))
+    for delta in (1.0, 0.05):
+        check(idx, val, N, delta, f"runs P={P} delta={delta}")
