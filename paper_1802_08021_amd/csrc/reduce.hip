@@ -122,17 +122,19 @@ __device__ __forceinline__ void node_coords(uint32_t node, uint32_t P, uint32_t*
 // entry opens a new group at levels 1..d; E[r][L]: all entries of rank r,
 // of which those without predecessor open new groups at every level.
 // Node (t, g) counts the entries of its ranks that open a group at level t.
-template <int NT>
+template <int NT, int RS>
 __device__ void flush_counts(uint32_t* E, const Args& a)
 {
     const uint32_t P = a.P, L = a.L, W = L + 1;
+    // E[r][d] lives at d * RS + r (rank-contiguous rows) or r * W + d.
+    auto at = [&](uint32_t r, uint32_t d) -> uint32_t { return RS ? d * RS + r : r * W + d; };
     for (uint32_t r = threadIdx.x; r < P; r += NT) {
-        uint32_t acc = E[r * W + L];
-        for (uint32_t d = 0; d < L; ++d) acc -= E[r * W + d];
-        E[r * W + L] = acc;
+        uint32_t acc = E[at(r, L)];
+        for (uint32_t d = 0; d < L; ++d) acc -= E[at(r, d)];
+        E[at(r, L)] = acc;
         for (int d = (int)L - 1; d >= 1; --d) {
-            acc += E[r * W + d];
-            E[r * W + d] = acc;
+            acc += E[at(r, (uint32_t)d)];
+            E[at(r, (uint32_t)d)] = acc;
         }
     }
     __syncthreads();
@@ -140,17 +142,9 @@ __device__ void flush_counts(uint32_t* E, const Args& a)
         uint32_t t, g;
         node_coords(node, P, &t, &g);
         uint32_t sum = 0;
-        for (uint32_t r = g << t; r < ((g + 1) << t); ++r) sum += E[r * W + t];
+        for (uint32_t r = g << t; r < ((g + 1) << t); ++r) sum += E[at(r, t)];
         if (sum) atomicAdd(&a.node_cnt[node], sum);
     }
-}
-
-// Raw buffer resource over `bytes` bytes at `base`: lanes past the end read
-// zero instead of faulting (the fourth word selects 32-bit raw accesses on
-// the gfx9 family).
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_at(const void* base, uint32_t bytes)
-{
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, (int)bytes, 0x00020000);
 }
 
 // Inclusive prefix sum over the 64 lanes of a wave: shifts within rows of
@@ -228,10 +222,10 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
 
     const uint32_t tid = threadIdx.x, lane = tid & 63u;
     const uint32_t wv = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const uint32_t P = a.P, L = a.L, W = L + 1, T = a.T;
+    const uint32_t P = a.P, L = a.L, T = a.T;
     const uint32_t chunk = blockIdx.x, stride = a.nchunks + 1;
     const uint32_t t0 = chunk * a.tpc, t1 = min(t0 + a.tpc, a.ntiles);
-    const uint32_t qbits = a.qbits;
+    const uint32_t qbits = a.qbits, qlog = qbits == 8u ? 3u : (qbits == 4u ? 2u : 1u);
     const uint32_t plog = qbits == 8u ? 0u : (qbits == 4u ? 1u : 2u), pm = (1u << plog) - 1u;
     const uint32_t EB = wv * ECAP;  // this wave's entry region
     const uint64_t below = (1ull << lane) - 1ull;
@@ -402,14 +396,13 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
         // arrival number and decoded value.  (Lanes now read entries other
         // lanes of the wave wrote: the fence orders them for the compiler.)
         __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
-        for (uint32_t e = lane; e < ne_w; e += 64u) {
-            const uint2 en = s_ent[EB + e];
+        auto arrive = [&](uint2 en, uint32_t e) {
             const uint32_t j = en.x & 0xFFFu, r = (en.x >> 12) & 0xFFu;
             const uint32_t k = atomicAdd(&s_cnt[j], 1u);
             float v = 0.0f;
             if (VALS) {
                 if (QUANT) {
-                    const uint32_t code = (en.y >> (((en.x >> 20) & 3u) * qbits)) & ((1u << qbits) - 1u);
+                    const uint32_t code = (en.y >> (((en.x >> 20) & 3u) << qlog)) & ((1u << qbits) - 1u);
                     v = dequant(code, qbits, s_unit[r]);
                 } else {
                     v = __uint_as_float(en.y);
@@ -420,6 +413,14 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
                 if (VALS) s_out[j] = MODE == kDense ? v + 0.0f : v;
             }
             s_ent[EB + e] = make_uint2((en.x & 0xFFFFFu) | k << 20, __float_as_uint(v));
+        };
+        // two entries per lane and step, so that their LDS round trips overlap
+        for (uint32_t e = lane; e < ne_w; e += 128u) {
+            const bool two = e + 64u < ne_w;
+            const uint2 en0 = s_ent[EB + e];
+            const uint2 en1 = s_ent[EB + (two ? e + 64u : e)];
+            arrive(en0, e);
+            if (two) arrive(en1, e + 64u);
         }
         __syncthreads();
 
@@ -505,20 +506,19 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
             // the pair for the node sizes; m >= 3: staged at its index's
             // range in arrival order.
             if (CNTS)
-                for (uint32_t r = tid; r < P; r += NT) s_E[r * W + L] += pn_get(r).y;
+                for (uint32_t r = tid; r < P; r += NT) s_E[L * PMAX + r] += pn_get(r).y;
             const uint32_t toff = MODE == kSparseWrite ? a.tile_off[tile] : 0u;
-            for (uint32_t e = lane; e < ne_w; e += 64u) {
-                const uint2 en = s_ent[EB + e];
+            auto place = [&](uint2 en, uint32_t sc) {
                 const uint32_t j = en.x & 0xFFFu, r = (en.x >> 12) & 0xFFu, k = en.x >> 20;
                 const float v = __uint_as_float(en.y);
-                const uint32_t sc = s_cnt[j], m = sc & 0x1FFu, aux = sc >> 9;
+                const uint32_t m = sc & 0x1FFu, aux = sc >> 9;
                 if (m >= 3u) {
                     s_sr[aux + k] = (uint8_t)r;
                     if (VALS) s_sv[aux + k] = v;
                 } else if (m == 2u) {
                     if (k == 1u) {
                         const uint32_t r0 = s_r0[j];
-                        if (CNTS) atomicAdd(&s_E[max(r0, r) * W + sep_level(r0, r)], 1u);
+                        if (CNTS) atomicAdd(&s_E[sep_level(r0, r) * PMAX + max(r0, r)], 1u);
                         if (VALS) {
                             const float sum = s_out[j] + v;
                             if (MODE == kDense) {
@@ -533,6 +533,15 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
                     a.out_idx[toff + aux] = tlo + j;
                     a.out_val[toff + aux] = v;
                 }
+            };
+            // two entries per lane and step, reads first
+            for (uint32_t e = lane; e < ne_w; e += 128u) {
+                const bool two = e + 64u < ne_w;
+                const uint2 en0 = s_ent[EB + e];
+                const uint2 en1 = s_ent[EB + (two ? e + 64u : e)];
+                const uint32_t sc0 = s_cnt[en0.x & 0xFFFu], sc1 = s_cnt[en1.x & 0xFFFu];
+                place(en0, sc0);
+                if (two) place(en1, sc1);
             }
             __syncthreads();
 
@@ -569,9 +578,9 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
                 const uint32_t c1 = sep_level(rk[0], rk[1]), c2 = sep_level(rk[1], rk[2]);
                 const uint32_t c3 = m == 4u ? sep_level(rk[2], rk[3]) : 0u;
                 if (CNTS) {
-                    atomicAdd(&s_E[rk[1] * W + c1], 1u);
-                    atomicAdd(&s_E[rk[2] * W + c2], 1u);
-                    atomicAdd(&s_E[m == 4u ? rk[3] * W + c3 : EW + lane], 1u);
+                    atomicAdd(&s_E[c1 * PMAX + rk[1]], 1u);
+                    atomicAdd(&s_E[c2 * PMAX + rk[2]], 1u);
+                    atomicAdd(&s_E[m == 4u ? c3 * PMAX + rk[3] : EW + lane], 1u);
                 }
                 if (VALS) {
                     float sum;
@@ -589,7 +598,10 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
                 }
             }
             // Walk: indices with five to eight ranks, one per thread.
-            for (uint32_t i = NA + tid; i < NA + NB; i += NT) {
+            // (five to eight ranks take the threads from the top down and more
+            // than eight the waves from the last one down, so that they share
+            // as few waves as possible with the three-four rank indices)
+            for (uint32_t i = NA + (NT - 1u - tid); i < NA + NB; i += NT) {
                 const uint2 item = s_list[i];
                 const uint32_t j = item.x & 0xFFFFu, nz = item.x >> 16;
                 const uint32_t st0 = item.y & 0xFFFFu, m = item.y >> 16;
@@ -628,7 +640,7 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
                 for (int e = 1; e < 8; ++e) {
                     if ((uint32_t)e < m) {
                         const uint32_t sep = sep_level(rk[e - 1], rk[e]);
-                        if (CNTS) atomicAdd(&s_E[rk[e] * W + sep], 1u);
+                        if (CNTS) atomicAdd(&s_E[sep * PMAX + rk[e]], 1u);
                         if (VALS) {
 #pragma unroll
                             for (int l = 0; l < LMAX; ++l)
@@ -658,7 +670,7 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
             // and the tree is evaluated level by level: a node is the sum of
             // its two children when both hold a value, else the one that
             // does -- the recursive doubling of the ranks present.
-            for (uint32_t i = NA + NB + wv; i < NA + NB + NC; i += NW) {
+            for (uint32_t i = NA + NB + (NW - 1u - wv); i < NA + NB + NC; i += NW) {
                 const uint2 item = s_list[i];
                 const uint32_t j = item.x & 0xFFFFu, nz = item.x >> 16;
                 const uint32_t st0 = item.y & 0xFFFFu, m = item.y >> 16;
@@ -693,7 +705,7 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
                                               : ((uint32_t)w2 == (r >> 5) ? pw[w2] & ((1u << (r & 31u)) - 1u) : 0u);
                             if (mk) pred = w2 * 32 + 31 - (int)__clz(mk);
                         }
-                        if (pred >= 0) atomicAdd(&s_E[r * W + sep_level((uint32_t)pred, r)], 1u);
+                        if (pred >= 0) atomicAdd(&s_E[sep_level((uint32_t)pred, r) * PMAX + r], 1u);
                     }
                 }
                 if (VALS) {
@@ -753,7 +765,7 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
         __syncthreads();
     }
     __syncthreads();
-    if (CNTS) flush_counts<NT>(s_E, a);
+    if (CNTS) flush_counts<NT, PMAX>(s_E, a);
 }
 
 // ------------------------------------------------------------------------
@@ -895,7 +907,7 @@ __global__ void __launch_bounds__(kSlowNT) k_slow(Args a)
         if (MODE != kSparseWrite && tid == 0) a.tile_cnt[tile] = tile_nz;
     }
     __syncthreads();
-    if (MODE != kSparseWrite) flush_counts<NT>(s_E, a);
+    if (MODE != kSparseWrite) flush_counts<NT, 0>(s_E, a);
 }
 
 // ------------------------------------------------------------------------
