@@ -176,3 +176,26 @@ def densify(idx: np.ndarray, val: np.ndarray, N: int) -> np.ndarray:
     if rc != 0:
         raise OracleError(f"orc_densify returned {rc}")
     return out
+
+
+def topk_by_threshold(x: np.ndarray, k: int):
+    """Exact per-row top-k with the same selection as topk (magnitude key =
+    the float's bits without the sign, larger first; equal keys by smaller
+    index; result in index order), found from the k-th largest key by a
+    partition instead of a full sort -- for rows too long to sort quickly.
+    §2.2 (top-k sparsification)."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    P, N = x.shape
+    out_idx = np.zeros((P, k), dtype=np.uint32)
+    out_val = np.zeros((P, k), dtype=np.float32)
+    if k == 0:
+        return out_idx, out_val
+    for r in range(P):
+        key = x[r].view(np.uint32) & np.uint32(0x7FFFFFFF)
+        kth = np.partition(key, N - k)[N - k]
+        above = np.nonzero(key > kth)[0]
+        ties = np.nonzero(key == kth)[0][: k - above.size]
+        sel = np.sort(np.concatenate([above, ties])).astype(np.uint32)
+        out_idx[r] = sel
+        out_val[r] = x[r][sel]
+    return out_idx, out_val

@@ -29,7 +29,11 @@ __device__ __forceinline__ double butterfly_sum(double v, int width)
 }
 
 // partial[r][b] = tree sum of v^2 over elements [b*kSeg, (b+1)*kSeg) of
-// stream r (zeros past the end).
+// stream r (zeros past the end).  A wave covers 2048 consecutive elements
+// in eight steps of 256: each lane squares four consecutive elements and
+// adds them pairwise, a lane butterfly joins the 64 lanes' subtrees, and the
+// eight step sums are joined pairwise at the end -- the same adjacent-pair
+// tree, with the eight independent butterflies in flight together.
 __global__ void __launch_bounds__(256) k_sumsq_partial(const QDesc* tab, double* partial, uint32_t Q)
 {
     __shared__ double s_w[4];
@@ -38,14 +42,25 @@ __global__ void __launch_bounds__(256) k_sumsq_partial(const QDesc* tab, double*
     const float* v = tab[r].val;
     const uint64_t n = tab[r].n;
     const uint64_t base = (uint64_t)b * kSeg + (uint64_t)wv * 2048;
-    double mine = 0.0;
-    for (int it = 0; it < 32; ++it) {
-        const uint64_t e = base + (uint64_t)it * 64 + lane;
-        const double x = e < n ? (double)v[e] : 0.0;
-        const double g = butterfly_sum(x * x, 64);
-        if (lane == it) mine = g;
+    const bool vec = (reinterpret_cast<uintptr_t>(v) & 15u) == 0;
+    double part[8];
+#pragma unroll
+    for (int it = 0; it < 8; ++it) {
+        const uint64_t e = base + (uint64_t)it * 256 + (uint64_t)lane * 4;
+        float4 x;
+        if (vec && e + 4 <= n) {
+            x = *reinterpret_cast<const float4*>(v + e);
+        } else {
+            x.x = e < n ? v[e] : 0.0f;
+            x.y = e + 1 < n ? v[e + 1] : 0.0f;
+            x.z = e + 2 < n ? v[e + 2] : 0.0f;
+            x.w = e + 3 < n ? v[e + 3] : 0.0f;
+        }
+        const double sq = ((double)x.x * (double)x.x + (double)x.y * (double)x.y) +
+                          ((double)x.z * (double)x.z + (double)x.w * (double)x.w);
+        part[it] = butterfly_sum(sq, 64);
     }
-    const double w = butterfly_sum(mine, 32);
+    const double w = ((part[0] + part[1]) + (part[2] + part[3])) + ((part[4] + part[5]) + (part[6] + part[7]));
     if (lane == 0) s_w[wv] = w;
     __syncthreads();
     if (threadIdx.x == 0) partial[(uint64_t)r * Q + b] = (s_w[0] + s_w[1]) + (s_w[2] + s_w[3]);

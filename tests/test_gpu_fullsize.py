@@ -1,0 +1,104 @@
+"""Parity at the full workload sizes, in the launch configuration the
+benchmark times: bench.Workload builds the same arena-resident inputs and
+prepared calls, one step runs the whole path, and its outputs are compared
+with the oracle on the same seeded inputs.
+
+  c3  P=32, N=2^24 dense rows: top-k (k = N/1000) of every rank, then the
+      sparse reduce of the selected streams;
+  c4  P=64, N=2^26, Zipf-overlapping supports: reduce to a dense root;
+  c5  P=128, N=2^27: 4-bit QSGD of every rank (codes and scales), then the
+      reduce of the dequantized streams to a dense root.
+
+Bar: indices, nnz, per-node union sizes and switch decisions, codes and
+scales bit-exact; values within 1e-6 rel / 1e-7 abs and bitwise."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_1802_08021_amd import inputs
+from gpu_util import assert_reduce_equal, assert_values, say, to_np, torch_dev
+
+pytestmark = pytest.mark.gpu
+
+
+def _workload(cfg, seed=0):
+    import bench
+    torch, dev = torch_dev()
+    c = inputs.config(cfg)
+    say(f"[full] {c.name}: P={c.P} N={c.N} generating inputs and device buffers")
+    return c, bench.Workload(c.name, c, seed, torch, dev), torch
+
+
+def _gpu_result(call, torch):
+    """The reduce outputs of one timed step, plus per-node union sizes and
+    decisions from the same prepared inputs."""
+    from paper_1802_08021_amd import sparcml as S
+    nnz, dense = call.run()
+    torch.cuda.synchronize()
+    idx, vals, codes, scales = call._keep
+    node = S.ReduceCall(idx, call.N, call.delta, vals=vals, codes=codes, scales=scales,
+                        qbits=0 if codes is None else call.arr[0].qbits, node_info=True)
+    n2, d2 = node.run()
+    torch.cuda.synchronize()
+    assert (n2, d2) == (nnz, dense)
+    out = {
+        "dense": dense,
+        "nnz": nnz,
+        "idx": None if dense else to_np(call.out_idx, np.uint32)[:nnz].copy(),
+        "val": to_np(call.out_val).copy() if dense else to_np(call.out_val)[:nnz].copy(),
+        "node_nnz": to_np(node.node_nnz).astype(np.uint64),
+        "node_dense": to_np(node.node_dense),
+    }
+    del node
+    return out
+
+
+@pytest.mark.timeout(900)
+def test_c5_full_quantize_and_reduce():
+    c, w, torch = _workload(5)
+    w.quant.run()
+    torch.cuda.synchronize()
+    g = _gpu_result(w.reduce, torch)
+    say(f"[full] c5: GPU root nnz={g['nnz']} dense={g['dense']}")
+    d = w.d_host
+    say("[full] c5: oracle quantize")
+    q, scale, deq = oracle.quantize(d["val"], c.qbits, inputs.quant_seed(0, c.cfg))
+    codes, gscale = w.quant._keep[1], to_np(w.quant.scale)
+    np.testing.assert_array_equal(gscale.view(np.uint32), scale.view(np.uint32), err_msg="scales")
+    for r in range(c.P):
+        np.testing.assert_array_equal(to_np(codes[r]), q[r], err_msg=f"codes of rank {r}")
+    say("[full] c5: codes and scales equal; oracle reduce")
+    o = oracle.sparse_reduce(d["idx"], deq, c.N, c.delta)
+    assert_reduce_equal(g, o, "c5 full")
+    assert g["dense"]
+
+
+@pytest.mark.timeout(600)
+def test_c4_full_reduce():
+    c, w, torch = _workload(4)
+    g = _gpu_result(w.reduce, torch)
+    say(f"[full] c4: GPU root nnz={g['nnz']} dense={g['dense']}; regenerating host inputs")
+    d = inputs.generate(c, 0)
+    o = oracle.sparse_reduce(d["idx"], d["val"], c.N, c.delta)
+    assert_reduce_equal(g, o, "c4 full")
+    assert g["dense"]
+    assert (~g["node_dense"].astype(bool)).any()  # the lower levels stayed sparse
+
+
+@pytest.mark.timeout(600)
+def test_c3_full_topk_and_reduce():
+    c, w, torch = _workload(3)
+    w.topk.run()
+    torch.cuda.synchronize()
+    gi = to_np(w.topk.idx, np.uint32)
+    gv = to_np(w.topk.val)
+    g = _gpu_result(w.reduce, torch)
+    say(f"[full] c3: GPU root nnz={g['nnz']} dense={g['dense']}; oracle top-k")
+    x = inputs.generate(c, 0)["x"]
+    oi, ov = oracle.topk_by_threshold(x, c.k)
+    np.testing.assert_array_equal(gi, oi, err_msg="top-k indices")
+    assert_values(gv.ravel(), ov.ravel(), "top-k values")
+    say("[full] c3: top-k equal; oracle reduce")
+    o = oracle.sparse_reduce([oi[r] for r in range(c.P)], [ov[r] for r in range(c.P)], c.N, c.delta)
+    assert_reduce_equal(g, o, "c3 full")
+    assert not g["dense"]

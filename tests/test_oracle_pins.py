@@ -506,3 +506,19 @@ def test_full_size_c1_vs_brute_force():
     c = inputs.config(1)
     d = inputs.generate(c, seed=0, workers=1)
     check_reduce_against_brute(d["idx"], d["val"], c.N, c.delta)
+
+
+def test_topk_by_threshold_matches_full_sort():
+    """The partition-based top-k picks exactly what the full sort picks,
+    ties (equal magnitudes, +-0, +-x) included."""
+    rng = np.random.default_rng(51)
+    for N, k in ((1, 1), (17, 5), (1000, 1), (1000, 999), (4096, 300), (5000, 5000)):
+        x = rng.normal(size=(3, N)).astype(np.float32)
+        x[1] = np.round(x[1] * 2.0) / 2.0          # many equal magnitudes
+        x[1, ::7] = -x[1, ::7]
+        x[2, : N // 2] = 0.0
+        x[2, N // 4: N // 2] = -0.0
+        i1, v1, _ = oracle.topk(x, k)
+        i2, v2 = oracle.topk_by_threshold(x, k)
+        np.testing.assert_array_equal(i1, i2)
+        np.testing.assert_array_equal(v1.view(np.uint32), v2.view(np.uint32))
