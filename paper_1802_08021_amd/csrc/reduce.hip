@@ -72,9 +72,10 @@ struct Fast {
     static constexpr int SLMAX = PMAX / NW < 1 ? 1 : PMAX / NW;
     static constexpr int TMAX = PMAX <= 32 ? 2048 : 4096;
     static constexpr int CPT = TMAX / NT;           // coordinates per thread (4)
-    static constexpr uint32_t CAP = TMAX * 7 / 8;   // staged entries
-    static constexpr uint32_t LCAP = CAP / 3 + 1;
-    static constexpr uint32_t ECAP = 448;           // compacted entries per wave
+    static constexpr uint32_t CAP = TMAX * 3 / 4;   // staged later arrivals
+    static constexpr uint32_t CWC = 128;            // indices with three or more ranks per wave
+    static constexpr uint32_t CCAP = NW * CWC;
+    static constexpr uint32_t ECAP = PMAX >= 256 ? 384 : 448;  // compacted entries per wave
     static constexpr int LMAX = PMAX <= 16 ? 4 : (PMAX <= 32 ? 5 : (PMAX <= 64 ? 6 : (PMAX <= 128 ? 7 : 8)));
 };
 constexpr uint32_t kWin = 64;  // window entries per rank per tile
@@ -160,6 +161,25 @@ __device__ __forceinline__ uint32_t wave_scan(uint32_t v)
     return v;
 }
 
+// A tree node: the sum of its two children when both hold a value, else the
+// one that does (px, py: whether x, y hold one).
+__device__ __forceinline__ float tree_join(float x, uint32_t px, float y, uint32_t py)
+{
+    return px && py ? x + y : (px ? x : y);
+}
+
+// One level of a tree over the lanes of rows of 16: lane i (a multiple of
+// 2H) joins lane i + H (DPP row_shl:H).  All lanes must be active.
+template <int H>
+__device__ __forceinline__ void tree_level(float& v, uint32_t& pr, uint32_t lane)
+{
+    const float ov = __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x100 + H, 0xF, 0xF, true));
+    const uint32_t op = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)pr, 0x100 + H, 0xF, 0xF, true);
+    const bool at = (lane & (2u * H - 1u)) == 0u;
+    v = at ? tree_join(v, pr, ov, op) : v;
+    pr = at ? (pr | op) : pr;
+}
+
 // Level at which ranks a != b first meet: their highest differing bit
 // (the | 1 keeps equal ranks, which valid streams never produce, in range).
 __device__ __forceinline__ uint32_t sep_level(uint32_t a, uint32_t b)
@@ -194,31 +214,44 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
 {
     using F = Fast<PMAX>;
     constexpr int NT = F::NT, NW = F::NW, SLMAX = F::SLMAX, TMAX = F::TMAX, CPT = F::CPT;
-    constexpr uint32_t CAP = F::CAP, ECAP = F::ECAP;
+    constexpr uint32_t CAP = F::CAP, ECAP = F::ECAP, ERGN = ECAP + 64, CWC = F::CWC, CCAP = F::CCAP;
     constexpr int LMAX = F::LMAX;
     constexpr bool VALS = MODE != kCount, CNTS = MODE != kSparseWrite;
     constexpr uint32_t EW = PMAX * (LMAX + 1);  // node-count words; 64 dummies follow
+    constexpr int PW = (PMAX + 31) / 32;        // rank-mask words
+    static_assert(NW * PMAX + NW * PW <= 2 * NW * (int)ERGN, "walk buffers alias the entry regions");
 
-    __shared__ __align__(16) uint32_t s_cnt[TMAX];         // ranks per index; then m | aux << 9
+    // Per index: arrivals (sparse output: m | output position << 9 once the
+    // positions are known), the first arrival's value and rank, the staging
+    // start of the later arrivals of an index with three or more.
+    __shared__ __align__(16) uint32_t s_cnt[TMAX + 64];  // 64 dummies for idle lanes
     __shared__ __align__(16) float s_out[VALS ? TMAX : 4];  // first value; dense: the sum
-    __shared__ uint8_t s_r0[TMAX];                         // rank of the first arrival
-    __shared__ uint2 s_ent[NW * ECAP];                     // per wave: the tile's entries
-    __shared__ float s_sv[VALS ? CAP + 8 : 1];             // staged values (8 readable past the end)
-    __shared__ uint8_t s_sr[CAP + 8];                      // staged ranks
-    __shared__ uint2 s_list[F::LCAP];                      // {j | nzpos << 16, start | m << 16}
+    __shared__ uint8_t s_r0[TMAX];
+    __shared__ uint16_t s_start[TMAX];
+    // Per wave: the tile's entries {j | rank << 12 | code position << 20, raw
+    // value word}, then its later arrivals {j | rank << 12 | arrival number
+    // << 20, value}.  The walk of indices with more than eight ranks reuses
+    // the space.
+    __shared__ __align__(16) uint2 s_ent[NW * ERGN];
+    __shared__ float s_sv[VALS ? CAP + 8 : 1];             // later values by index, arrival order
+    __shared__ uint8_t s_sr[CAP + 8];                      // and their ranks
+    __shared__ uint16_t s_cands[CCAP];                     // per wave: indices with three or more ranks
+    __shared__ uint32_t s_lista[CCAP];                     // 3-4 ranks: j | start << 12
+    __shared__ uint32_t s_listb[CCAP];                     // 5-8 from the bottom, > 8 from the top
     __shared__ uint32_t s_E[CNTS ? EW + 64 : 1];
-    // Per rank (slot) state: {stream position, entries in this tile},
-    // {chunk end, last readable entry}, {index base, value base}, level unit.
-    // Ranks past P have an empty window over a readable dummy address.
-    __shared__ uint64_t s_pn[PMAX];  // position | tile count << 32
-    __shared__ uint2 s_el[PMAX];
-    __shared__ uint4 s_base[PMAX];
-    __shared__ float s_unit[PMAX];
-    __shared__ uint32_t s_wtot[2 * NW];
-    __shared__ uint32_t s_flag;
-    constexpr int PW = (PMAX + 31) / 32;                   // rank-mask words
-    __shared__ float s_wv[VALS ? NW * PMAX : 1];           // per wave: values by rank
-    __shared__ uint32_t s_wp[NW * PW];                     // per wave: ranks present
+    // Per wave and slot: {stream position, entries in this tile, chunk end,
+    // last readable entry}, {index base, value base}, {level unit}.  Slot s
+    // of wave w is rank s*NW + w (waves interleave, so small P still spreads
+    // over all waves); ranks past P have an empty window over a readable
+    // dummy address.  A wave reads its slots at fixed offsets.
+    __shared__ uint4 s_slot[NW * SLMAX * 3];
+    __shared__ uint32_t s_wtot[NW];
+    // tile counters: staged values | list A << 16 | list B << 32 | list C << 48
+    // (each below 2^16), non-empty indices, overflow flag
+    __shared__ uint64_t s_alloc;
+    __shared__ uint32_t s_ne, s_flag;
+    float* const s_wv = reinterpret_cast<float*>(s_ent);                  // per wave: values by rank
+    uint32_t* const s_wp = reinterpret_cast<uint32_t*>(s_ent) + NW * PMAX;  // per wave: ranks present
 
     const uint32_t tid = threadIdx.x, lane = tid & 63u;
     const uint32_t wv = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -227,41 +260,26 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
     const uint32_t t0 = chunk * a.tpc, t1 = min(t0 + a.tpc, a.ntiles);
     const uint32_t qbits = a.qbits, qlog = qbits == 8u ? 3u : (qbits == 4u ? 2u : 1u);
     const uint32_t plog = qbits == 8u ? 0u : (qbits == 4u ? 1u : 2u), pm = (1u << plog) - 1u;
-    const uint32_t EB = wv * ECAP;  // this wave's entry region
+    const uint32_t EB = wv * ERGN;  // this wave's entry region
     const uint64_t below = (1ull << lane) - 1ull;
 
-    // Loop-invariant values (the per-rank LDS state of every slot, LDS
-    // addresses of a thread's coordinates) would be hoisted out of the tile
-    // loop and held in registers or spilled; opaque copies of the rank
-    // (scalar) and thread number (vector) keep them next to their use.
-    auto opaque = [](uint32_t v) -> uint32_t {
-        asm volatile("" : "+s"(v));
-        return v;
-    };
+    // Loop-invariant values (LDS addresses of a thread's coordinates) would
+    // be hoisted out of the tile loop and held in registers or spilled; an
+    // opaque copy of the thread number keeps them next to their use.
     auto opaque_v = [](uint32_t v) -> uint32_t {
         asm volatile("" : "+v"(v));
         return v;
     };
-    // Slot s of wave wv is rank s*NW + wv (waves interleave, so small P
-    // still spreads over all waves).
-    auto slot_rank = [&](int s) -> uint32_t { return opaque((uint32_t)s * NW + wv); };
-    // A slot's {position, tile count} is written by lane 0 of its wave and
-    // read by all lanes with no barrier in between.  Plain accesses would let
-    // the compiler forward a lane's own earlier read (in its per-thread view
-    // nobody else writes), leaving lanes 1..63 on a stale position; relaxed
-    // atomic accesses always go to LDS, where the wave's operations are
-    // ordered.
-    auto pn_get = [&](uint32_t r) -> uint2 {
-        const uint64_t v = __hip_atomic_load(&s_pn[r], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WAVEFRONT);
-        return make_uint2((uint32_t)v, (uint32_t)(v >> 32));
-    };
-    auto pn_set = [&](uint32_t r, uint32_t pos, uint32_t cnt) {
-        __hip_atomic_store(&s_pn[r], (uint64_t)pos | (uint64_t)cnt << 32, __ATOMIC_RELAXED,
-                           __HIP_MEMORY_SCOPE_WAVEFRONT);
+    uint4* const sw = s_slot + 3u * SLMAX * wv;  // this wave's slots
+    // entries of rank r in the current tile
+    auto rank_count = [&](uint32_t r) -> uint32_t { return s_slot[3u * ((r % NW) * SLMAX + r / NW)].y; };
+    auto reset_counters = [&]() {
+        s_alloc = 0u;
+        s_ne = s_flag = 0u;
     };
 
     for (uint32_t r = tid; r < (uint32_t)PMAX; r += NT) {
-        uint2 pn = make_uint2(0u, 0u), el = make_uint2(0u, 0u);
+        uint2 pn = make_uint2(0u, 0u), el = make_uint2(0u, 0u);  // {position, count}, {end, last}
         uint64_t ib = reinterpret_cast<uint64_t>(a.tab), vb = ib;  // readable dummy
         float unit = 0.0f;
         if (r < P) {
@@ -276,19 +294,18 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
             }
             if (QUANT && VALS) unit = level_unit(*d.qscale, qbits);
         }
-        s_pn[r] = (uint64_t)pn.x | (uint64_t)pn.y << 32;
-        s_el[r] = el;
-        s_base[r] = make_uint4((uint32_t)ib, (uint32_t)(ib >> 32), (uint32_t)vb, (uint32_t)(vb >> 32));
-        s_unit[r] = unit;
+        uint4* const sl = s_slot + 3u * ((r % NW) * SLMAX + r / NW);
+        sl[0] = make_uint4(pn.x, pn.y, el.x, el.y);
+        sl[1] = make_uint4((uint32_t)ib, (uint32_t)(ib >> 32), (uint32_t)vb, (uint32_t)(vb >> 32));
+        sl[2] = make_uint4(__float_as_uint(unit), 0u, 0u, 0u);
     }
-    for (uint32_t i = tid; i < TMAX; i += NT) {
+    for (uint32_t i = tid; i < TMAX + 64; i += NT) {
         s_cnt[i] = 0u;
         if (VALS) s_out[i] = 0.0f;
     }
     if (CNTS)
         for (uint32_t i = tid; i < EW + 64; i += NT) s_E[i] = 0u;
-    for (uint32_t i = tid; i < (uint32_t)(NW * PW); i += NT) s_wp[i] = 0u;
-    if (tid == 0) s_flag = 0u;
+    if (tid == 0) reset_counters();
     __syncthreads();
 
     // Window of a stream at position pos: raw index and raw value word (fp32
@@ -305,35 +322,34 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
             else v = *reinterpret_cast<g_u32*>(vb + 4ull * i);
         }
     };
-    auto load_win = [&](uint32_t r, uint32_t pos, uint32_t& x, uint32_t& v) {
-        const uint4 b = s_base[r];
-        const uint32_t i = min(pos + lane, s_el[r].y);
-        const uint64_t ib = ((uint64_t)b.y << 32) | b.x;
-        x = *reinterpret_cast<g_u32*>(ib + 4ull * i);
-        v = 0u;
-        if (VALS) {
-            const uint64_t vb = ((uint64_t)b.w << 32) | b.z;
-            if (QUANT) v = *reinterpret_cast<g_u8*>(vb + (i >> plog));
-            else v = *reinterpret_cast<g_u32*>(vb + 4ull * i);
-        }
+    // Value bits of a window entry at stream position pos + lane: the fp32
+    // word, or the entry's code (its bits of the byte) dequantized.
+    // (+-level * unit, level 0 giving +0, as the signed level times the unit.)
+    auto decode = [&](uint32_t v, uint32_t pos, float unit) -> uint32_t {
+        if (!QUANT) return v;
+        const uint32_t code = __builtin_amdgcn_ubfe(v, ((lane + pos) & pm) << qlog, qbits);
+        const uint32_t lev = code & ((1u << (qbits - 1u)) - 1u);
+        const int sl = (code >> (qbits - 1u)) ? -(int)lev : (int)lev;
+        return lev ? __float_as_uint(__fmul_rn((float)sl, unit)) : 0u;
     };
-    // Append the in-tile entries of a window to this wave's entry region:
-    // {j | rank << 12 | code position in its byte << 20, raw value word}.
-    auto compact = [&](bool in, uint64_t bal, uint32_t base, uint32_t j, uint32_t r, uint32_t pos, uint32_t v) {
-        if (in) {
-            const uint32_t at = base + (uint32_t)__popcll(bal & below);
-            if (at < ECAP) s_ent[EB + at] = make_uint2(j | r << 12 | ((lane + pos) & pm) << 20, v);
-        }
+    // Append a window to this wave's entry region as {j | rank << 12, value
+    // bits}: the in-tile entries of a window are a prefix of it (streams are
+    // ascending), so lane i goes to position base + i; the lanes past the
+    // prefix write slack that the next window or the region's 64 spare
+    // entries take.  Nothing is written once the region is full.
+    auto append = [&](uint32_t base, uint32_t jr, uint32_t v) {
+        if (base <= ECAP) s_ent[EB + base + lane] = make_uint2(jr, v);
     };
 
     // xr, vr: raw window words of every slot (in flight during a tile).
     uint32_t xr[SLMAX], vr[SLMAX];
 #pragma unroll
-    for (int s = 0; s < SLMAX; ++s) load_win(slot_rank(s), pn_get(slot_rank(s)).x, xr[s], vr[s]);
+    for (int s = 0; s < SLMAX; ++s) load_win_at(sw[3 * s + 1], sw[3 * s].w, sw[3 * s].x, xr[s], vr[s]);
 
     for (uint32_t tile = t0; tile < t1; ++tile) {
         const uint32_t tlo = tile * T;
         const uint32_t TT = (uint32_t)min((uint64_t)T, (uint64_t)a.N - tlo);  // tile width
+        const uint32_t toff = MODE == kSparseWrite ? a.tile_off[tile] : 0u;
 
         // P1w: the in-tile entries of every window, compacted into this
         // wave's region (no other wave touches it, so no barrier follows).
@@ -348,289 +364,308 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
         constexpr int G1 = SLMAX < 4 ? SLMAX : 4;
 #pragma unroll
         for (int g0 = 0; g0 < SLMAX; g0 += G1) {
-            uint2 pe[G1], el[G1];
-            uint4 bs[G1];
+            uint4 st[G1], bs[G1];
+            float un[G1];
 #pragma unroll
             for (int q = 0; q < G1; ++q) {
-                const uint32_t r = slot_rank(g0 + q);
-                pe[q] = pn_get(r);
-                el[q] = s_el[r];
-                bs[q] = s_base[r];
+                st[q] = sw[3 * (g0 + q)];
+                bs[q] = sw[3 * (g0 + q) + 1];
+                un[q] = QUANT && VALS ? __uint_as_float(sw[3 * (g0 + q) + 2].x) : 0.0f;
             }
 #pragma unroll
             for (int q = 0; q < G1; ++q) {
                 const int s = g0 + q;
-                const uint32_t r = slot_rank(s);
-                uint32_t pos = pe[q].x;
-                const uint32_t j = xr[s] - tlo;
-                const bool in = j < TT && lane < el[q].x - pos;
-                const uint64_t bal = __ballot(in);
-                uint32_t n = (uint32_t)__popcll(bal);
-                compact(in, bal, nent, j, r, pos, vr[s]);
+                // (j | rank << 12) of an in-tile entry x is x plus this
+                const uint32_t jr0 = (((uint32_t)s * NW + wv) << 12) - tlo;
+                uint32_t pos = st[q].x;
+                const uint32_t end = st[q].z, last = st[q].w;
+                const bool in = xr[s] - tlo < TT && lane < end - pos;
+                uint32_t n = (uint32_t)__popcll(__ballot(in));
+                append(nent, xr[s] + jr0, VALS ? decode(vr[s], pos, un[q]) : 0u);
                 nent += n;
                 pos += n;
                 uint32_t cnt = n;
                 if (n == kWin) {  // rare: continue the window
                     do {
                         uint32_t x2, v2;
-                        load_win_at(bs[q], el[q].y, pos, x2, v2);
-                        const uint32_t j2 = x2 - tlo;
-                        const bool in2 = j2 < TT && lane < el[q].x - pos;
-                        const uint64_t bal2 = __ballot(in2);
-                        n = (uint32_t)__popcll(bal2);
-                        compact(in2, bal2, nent, j2, r, pos, v2);
+                        load_win_at(bs[q], last, pos, x2, v2);
+                        const bool in2 = x2 - tlo < TT && lane < end - pos;
+                        n = (uint32_t)__popcll(__ballot(in2));
+                        append(nent, x2 + jr0, VALS ? decode(v2, pos, un[q]) : 0u);
                         nent += n;
                         pos += n;
                         cnt += n;
                     } while (n == kWin);
                 }
-                if (lane == 0u) pn_set(r, pos, cnt);
-                load_win_at(bs[q], el[q].y, pos, xr[s], vr[s]);
+                // every lane stores the same {position, count}
+                *reinterpret_cast<uint2*>(&sw[3 * s]) = make_uint2(pos, cnt);
+                load_win_at(bs[q], last, pos, xr[s], vr[s]);
             }
         }
         if (nent > ECAP && lane == 0u) s_flag = 1u;
         const uint32_t ne_w = min(nent, ECAP);
-
-        // P1e: arrival numbers of this wave's entries; the first arrival
-        // leaves its rank and value at the index.  The entry keeps its
-        // arrival number and decoded value.  (Lanes now read entries other
-        // lanes of the wave wrote: the fence orders them for the compiler.)
+        // P1e: arrival numbers of this wave's entries, two per lane and step
+        // so that their LDS round trips overlap (idle lanes count at dummy
+        // words).  The first arrival leaves its rank and value at the index;
+        // the later ones are compacted, with their arrival number, to the
+        // front of the wave's region (never past what the wave has read), and
+        // the third lists its index as one with three or more ranks.  The next
+        // step's entries, which this step never overwrites, are read ahead.
+        // (Lanes read entries other lanes of the wave wrote: the fence orders
+        // them for the compiler.)
         __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
-        auto arrive = [&](uint2 en, uint32_t e) {
-            const uint32_t j = en.x & 0xFFFu, r = (en.x >> 12) & 0xFFu;
-            const uint32_t k = atomicAdd(&s_cnt[j], 1u);
-            float v = 0.0f;
-            if (VALS) {
-                if (QUANT) {
-                    const uint32_t code = (en.y >> (((en.x >> 20) & 3u) << qlog)) & ((1u << qbits) - 1u);
-                    v = dequant(code, qbits, s_unit[r]);
-                } else {
-                    v = __uint_as_float(en.y);
+        const uint32_t CB = wv * CWC;  // this wave's candidate region
+        uint32_t nlat = 0u, ncw = 0u, nfirst = 0u;
+        uint2 nx0 = s_ent[EB + lane], nx1 = s_ent[EB + 64u + lane];
+        for (uint32_t b = 0; b < ne_w; b += 128u) {
+            const uint2 en0 = nx0, en1 = nx1;
+            const bool ok0 = b + lane < ne_w, ok1 = b + 64u + lane < ne_w;
+            const uint32_t j0 = en0.x & 0xFFFu, j1 = en1.x & 0xFFFu;
+            const uint32_t k0 = atomicAdd(&s_cnt[ok0 ? j0 : TMAX + lane], 1u);
+            const uint32_t k1 = atomicAdd(&s_cnt[ok1 ? j1 : TMAX + lane], 1u);
+            nx0 = s_ent[EB + min(b + 128u + lane, ECAP - 1u)];
+            nx1 = s_ent[EB + min(b + 192u + lane, ECAP - 1u)];
+            const bool f0 = ok0 && k0 == 0u, f1 = ok1 && k1 == 0u;
+            const bool l0 = ok0 && k0 != 0u, l1 = ok1 && k1 != 0u;
+            const bool c0 = ok0 && k0 == 2u, c1 = ok1 && k1 == 2u;
+            if (f0) {
+                s_r0[j0] = (uint8_t)(en0.x >> 12);
+                if (VALS) s_out[j0] = MODE == kDense ? __uint_as_float(en0.y) + 0.0f : __uint_as_float(en0.y);
+            }
+            if (f1) {
+                s_r0[j1] = (uint8_t)(en1.x >> 12);
+                if (VALS) s_out[j1] = MODE == kDense ? __uint_as_float(en1.y) + 0.0f : __uint_as_float(en1.y);
+            }
+            const uint64_t L0 = __ballot(l0), L1 = __ballot(l1);
+            const uint64_t C0 = __ballot(c0), C1 = __ballot(c1);
+            if (CNTS) nfirst += (uint32_t)__popcll(__ballot(f0)) + (uint32_t)__popcll(__ballot(f1));
+            if (l0) s_ent[EB + nlat + (uint32_t)__popcll(L0 & below)] = make_uint2(en0.x | k0 << 20, en0.y);
+            nlat += (uint32_t)__popcll(L0);
+            if (l1) s_ent[EB + nlat + (uint32_t)__popcll(L1 & below)] = make_uint2(en1.x | k1 << 20, en1.y);
+            nlat += (uint32_t)__popcll(L1);
+            const uint32_t q0 = ncw + (uint32_t)__popcll(C0 & below);
+            if (c0 && q0 < CWC) s_cands[CB + q0] = (uint16_t)j0;
+            ncw += (uint32_t)__popcll(C0);
+            const uint32_t q1 = ncw + (uint32_t)__popcll(C1 & below);
+            if (c1 && q1 < CWC) s_cands[CB + q1] = (uint16_t)j1;
+            ncw += (uint32_t)__popcll(C1);
+        }
+        if (lane == 0u) {
+            if (CNTS && nfirst) atomicAdd(&s_ne, nfirst);
+            if (ncw > CWC) s_flag = 1u;
+        }
+        __syncthreads();
+
+        const bool over = s_flag != 0u;
+        if (!over) {
+            if (MODE == kSparseWrite) {
+                // output position (index order) of every non-empty index; a
+                // single value is written out here
+                const uint32_t jb = opaque_v(tid) * CPT;
+                uint32_t mc[CPT];
+#pragma unroll
+                for (int c = 0; c < CPT; c += 4) {
+                    const uint4 q = *reinterpret_cast<const uint4*>(&s_cnt[jb + c]);
+                    mc[c] = q.x;
+                    mc[c + 1] = q.y;
+                    mc[c + 2] = q.z;
+                    mc[c + 3] = q.w;
+                }
+                uint32_t ne = 0u;
+#pragma unroll
+                for (int c = 0; c < CPT; ++c) ne += mc[c] != 0u ? 1u : 0u;
+                const uint32_t incl = wave_scan(ne);
+                if (lane == 63u) s_wtot[wv] = incl;
+                __syncthreads();
+                const uint32_t wt = lane < (uint32_t)NW ? s_wtot[lane] : 0u;
+                const uint32_t xs = wave_scan(wt);
+                uint32_t nrun = incl - ne + (uint32_t)__builtin_amdgcn_readlane((int)(xs - wt), (int)wv);
+#pragma unroll
+                for (int c = 0; c < CPT; ++c) {
+                    const uint32_t m = mc[c], j = jb + (uint32_t)c;
+                    if (m == 1u) {
+                        a.out_idx[toff + nrun] = tlo + j;
+                        a.out_val[toff + nrun] = s_out[j];
+                    } else if (m != 0u) {
+                        s_cnt[j] = m | nrun << 9;
+                    }
+                    nrun += m != 0u ? 1u : 0u;
+                }
+                __syncthreads();
+            }
+            // Candidates of this wave, one per lane: the staging range of the
+            // later arrivals and the walk list by rank count.
+            for (uint32_t b = 0; b < ncw; b += 64u) {
+                const uint32_t i = b + lane;
+                const bool act = i < ncw;
+                const uint32_t j = act ? (uint32_t)s_cands[CB + i] : 0u;
+                const uint32_t m = act ? s_cnt[j] & 0x1FFu : 0u;
+                const uint32_t ext = act ? m - 1u : 0u;
+                const uint32_t incl = wave_scan(ext);
+                const bool ca = act && m <= 4u, cb = act && m - 5u < 4u, cc = act && m > 8u;
+                const uint64_t BA = __ballot(ca), BB = __ballot(cb), BC = __ballot(cc);
+                // one reservation for the staging range and the three lists
+                const uint64_t want = (uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)incl, 63) |
+                                      (uint64_t)__popcll(BA) << 16 | (uint64_t)__popcll(BB) << 32 |
+                                      (uint64_t)__popcll(BC) << 48;
+                uint64_t got = 0u;
+                if (lane == 0u) got = atomicAdd(&s_alloc, want);
+                const uint32_t glo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)got);
+                const uint32_t ghi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(got >> 32));
+                const uint32_t start = (glo & 0xFFFFu) + incl - ext;
+                const uint32_t pa = (glo >> 16) + (uint32_t)__popcll(BA & below);
+                const uint32_t pb = (ghi & 0xFFFFu) + (uint32_t)__popcll(BB & below);
+                const uint32_t pc = (ghi >> 16) + (uint32_t)__popcll(BC & below);
+                if (act && start + ext <= CAP) {
+                    s_start[j] = (uint16_t)start;
+                    const uint32_t item = j | start << 12;
+                    if (ca) s_lista[pa] = item;
+                    if (cb) s_listb[pb] = item;
+                    if (cc) s_listb[CCAP - 1u - pc] = item;
                 }
             }
-            if (k == 0u) {
-                s_r0[j] = (uint8_t)r;
-                if (VALS) s_out[j] = MODE == kDense ? v + 0.0f : v;
-            }
-            s_ent[EB + e] = make_uint2((en.x & 0xFFFFFu) | k << 20, __float_as_uint(v));
-        };
-        // two entries per lane and step, so that their LDS round trips overlap
-        for (uint32_t e = lane; e < ne_w; e += 128u) {
-            const bool two = e + 64u < ne_w;
-            const uint2 en0 = s_ent[EB + e];
-            const uint2 en1 = s_ent[EB + (two ? e + 64u : e)];
-            arrive(en0, e);
-            if (two) arrive(en1, e + 64u);
         }
         __syncthreads();
+        const uint64_t al = s_alloc;
+        const bool defer = over || (uint32_t)(al & 0xFFFFu) > CAP;
+        const uint32_t NE = s_ne, NA = (uint32_t)(al >> 16) & 0xFFFFu;
+        const uint32_t NB = (uint32_t)(al >> 32) & 0xFFFFu, NC = (uint32_t)(al >> 48);
 
-        // Scan over this thread's CPT consecutive coordinates.
-        const uint32_t jb = opaque_v(tid) * CPT;
-        uint32_t mc[CPT];
-#pragma unroll
-        for (int c = 0; c < CPT; c += 4) {
-            const uint4 q = *reinterpret_cast<const uint4*>(&s_cnt[jb + c]);
-            mc[c] = q.x;
-            mc[c + 1] = q.y;
-            mc[c + 2] = q.z;
-            mc[c + 3] = q.w;
-        }
-        uint32_t st = 0u, ne = 0u, na = 0u, nb = 0u, nc = 0u;
-#pragma unroll
-        for (int c = 0; c < CPT; ++c) {
-            const uint32_t m = mc[c];
-            ne += m != 0u ? 1u : 0u;
-            st += m >= 3u ? m : 0u;
-            na += m - 3u < 2u ? 1u : 0u;
-            nb += m - 5u < 4u ? 1u : 0u;
-            nc += m > 8u ? 1u : 0u;
-        }
-        // with at most CAP staged entries: na < 2^11, nb < 2^10, nc < 2^9
-        const uint32_t p1 = st | ne << 16, p2 = na | nb << 11 | nc << 21;
-        const uint32_t i1 = wave_scan(p1), i2 = wave_scan(p2);
-        if (lane == 63u) {
-            s_wtot[wv] = i1;
-            s_wtot[NW + wv] = i2;
-        }
-        __syncthreads();
-        // wave totals: lane w < NW holds wave w's; prefix below this wave and
-        // the tile totals by one more wave scan
-        const uint32_t w1 = lane < (uint32_t)NW ? s_wtot[lane] : 0u;
-        const uint32_t w2 = lane < (uint32_t)NW ? s_wtot[NW + lane] : 0u;
-        const uint32_t x1 = wave_scan(w1), x2 = wave_scan(w2);
-        const uint32_t b1 = (uint32_t)__builtin_amdgcn_readlane((int)(x1 - w1), (int)wv);
-        const uint32_t b2 = (uint32_t)__builtin_amdgcn_readlane((int)(x2 - w2), (int)wv);
-        const uint32_t g1 = (uint32_t)__builtin_amdgcn_readlane((int)x1, NW - 1);
-        const uint32_t g2 = (uint32_t)__builtin_amdgcn_readlane((int)x2, NW - 1);
-        // at most NW*ECAP (< 65536) entries: no packed field overflows
-        const bool defer = s_flag != 0u || (g1 & 0xFFFFu) > CAP;
-        const uint32_t NE = g1 >> 16, NA = g2 & 0x7FFu, NB = (g2 >> 11) & 0x3FFu, NC = g2 >> 21;
         if (!defer) {
             if (CNTS && tid == 0) a.tile_cnt[tile] = NE;
-            const uint32_t e1 = i1 - p1 + b1, e2 = i2 - p2 + b2;
-            uint32_t srun = e1 & 0xFFFFu, nrun = e1 >> 16;
-            uint32_t arun = e2 & 0x7FFu, brun = NA + ((e2 >> 11) & 0x3FFu), crun = NA + NB + (e2 >> 21);
-#pragma unroll
-            for (int c = 0; c < CPT; ++c) {
-                const uint32_t m = mc[c], j = jb + (uint32_t)c;
-                if (m >= 3u) {
-                    // staging range and list slot; s_cnt keeps m | start << 9
-                    const uint2 item = make_uint2(j | nrun << 16, srun | m << 16);
-                    if (m <= 4u) s_list[arun++] = item;
-                    else if (m <= 8u) s_list[brun++] = item;
-                    else s_list[crun++] = item;
-                    s_cnt[j] = m | srun << 9;
-                    srun += m;
-                } else if (MODE == kSparseWrite && m != 0u) {
-                    s_cnt[j] = m | nrun << 9;  // output position
-                }
-                nrun += m != 0u ? 1u : 0u;
-            }
-        } else {
-#pragma unroll
-            for (int c = 0; c < CPT; c += 4) {
-                *reinterpret_cast<uint4*>(&s_cnt[jb + c]) = make_uint4(0u, 0u, 0u, 0u);
-                if (VALS) *reinterpret_cast<float4*>(&s_out[jb + c]) = make_float4(0.f, 0.f, 0.f, 0.f);
-            }
-            if (tid == 0) {
-                const uint32_t k = atomicAdd(a.slow_count, 1u);
-                a.slow_list[k] = tile;
-            }
-        }
-        __syncthreads();
-
-        if (!defer) {
-            // P2: per entry of this wave: m = 1 done (the first value
-            // stands); m = 2: the second arrival adds its value to the first
-            // -- a single addition is the same in either order -- and counts
-            // the pair for the node sizes; m >= 3: staged at its index's
-            // range in arrival order.
             if (CNTS)
-                for (uint32_t r = tid; r < P; r += NT) s_E[L * PMAX + r] += pn_get(r).y;
-            const uint32_t toff = MODE == kSparseWrite ? a.tile_off[tile] : 0u;
-            auto place = [&](uint2 en, uint32_t sc) {
-                const uint32_t j = en.x & 0xFFFu, r = (en.x >> 12) & 0xFFu, k = en.x >> 20;
-                const float v = __uint_as_float(en.y);
-                const uint32_t m = sc & 0x1FFu, aux = sc >> 9;
-                if (m >= 3u) {
-                    s_sr[aux + k] = (uint8_t)r;
-                    if (VALS) s_sv[aux + k] = v;
-                } else if (m == 2u) {
-                    if (k == 1u) {
-                        const uint32_t r0 = s_r0[j];
-                        if (CNTS) atomicAdd(&s_E[sep_level(r0, r) * PMAX + max(r0, r)], 1u);
-                        if (VALS) {
-                            const float sum = s_out[j] + v;
-                            if (MODE == kDense) {
-                                s_out[j] = sum;
-                            } else {
-                                a.out_idx[toff + aux] = tlo + j;
-                                a.out_val[toff + aux] = sum;
-                            }
+                for (uint32_t r = tid; r < P; r += NT) s_E[L * PMAX + r] += rank_count(r);
+            // P2, per later arrival of this wave: an index with two ranks is
+            // finished here -- a single addition is the same in either order --
+            // and counts its pair for the node sizes; otherwise the value is
+            // staged at its index's range in arrival order.
+            // Two entries per lane and step; every read of a step comes before
+            // its writes (no two entries of a step finish the same pair).
+            auto place = [&](uint2 en, uint32_t sc, uint32_t r0, uint32_t st, float first) {
+                const uint32_t jj = en.x & 0xFFFu, r = (en.x >> 12) & 0xFFu, k = en.x >> 20;
+                if ((sc & 0x1FFu) == 2u) {
+                    if (CNTS) atomicAdd(&s_E[sep_level(r0, r) * PMAX + max(r0, r)], 1u);
+                    if (VALS) {
+                        const float sum = first + __uint_as_float(en.y);
+                        if (MODE == kDense) {
+                            s_out[jj] = sum;
+                        } else {
+                            a.out_idx[toff + (sc >> 9)] = tlo + jj;
+                            a.out_val[toff + (sc >> 9)] = sum;
                         }
                     }
-                } else if (MODE == kSparseWrite) {
-                    a.out_idx[toff + aux] = tlo + j;
-                    a.out_val[toff + aux] = v;
+                } else {
+                    const uint32_t at = st + k - 1u;
+                    s_sr[at] = (uint8_t)r;
+                    if (VALS) s_sv[at] = __uint_as_float(en.y);
                 }
             };
-            // two entries per lane and step, reads first
-            for (uint32_t e = lane; e < ne_w; e += 128u) {
-                const bool two = e + 64u < ne_w;
-                const uint2 en0 = s_ent[EB + e];
-                const uint2 en1 = s_ent[EB + (two ? e + 64u : e)];
-                const uint32_t sc0 = s_cnt[en0.x & 0xFFFu], sc1 = s_cnt[en1.x & 0xFFFu];
-                place(en0, sc0);
-                if (two) place(en1, sc1);
+            for (uint32_t i = lane; i < nlat; i += 128u) {
+                const bool two = i + 64u < nlat;
+                const uint2 e0 = s_ent[EB + i];
+                const uint2 e1 = s_ent[EB + (two ? i + 64u : i)];
+                const uint32_t ja = e0.x & 0xFFFu, jb = e1.x & 0xFFFu;
+                const uint32_t sa = s_cnt[ja], sb = s_cnt[jb];
+                const uint32_t ra = s_r0[ja], rb = s_r0[jb];
+                const uint32_t ta = s_start[ja], tb = s_start[jb];
+                const float oa = VALS ? s_out[ja] : 0.0f, ob = VALS ? s_out[jb] : 0.0f;
+                place(e0, sa, ra, ta, oa);
+                if (two) place(e1, sb, rb, tb, ob);
             }
             __syncthreads();
+            if (tid == 0) reset_counters();  // every thread has read them
 
-            // Walk: indices with three or four ranks.
-            for (uint32_t i = tid; i < NA; i += NT) {
-                const uint2 item = s_list[i];
-                const uint32_t j = item.x & 0xFFFFu, nz = item.x >> 16;
-                const uint32_t st0 = item.y & 0xFFFFu, m = item.y >> 16;
+            auto emit = [&](uint32_t jj, float sum) {
+                if (MODE == kDense) {
+                    s_out[jj] = sum + 0.0f;
+                } else {
+                    const uint32_t nz = s_cnt[jj] >> 9;
+                    a.out_idx[toff + nz] = tlo + jj;
+                    a.out_val[toff + nz] = sum;
+                }
+            };
+            auto cswap_rv = [](uint32_t* rk, float* vv, int x, int y) {
+                const bool sw = rk[x] > rk[y];
+                const uint32_t tr = rk[x];
+                const float tv = vv[x];
+                rk[x] = sw ? rk[y] : rk[x];
+                rk[y] = sw ? tr : rk[y];
+                vv[x] = sw ? vv[y] : vv[x];
+                vv[y] = sw ? tv : vv[y];
+            };
+            // Waves 4q + s run on SIMD s (round-robin placement).  The walks of
+            // three or four ranks fill the waves of SIMDs 0-2 first and those
+            // of more than eight ranks take them from the other end, so that
+            // the top wave, which walks the indices with five to eight ranks,
+            // shares its SIMD with little else.
+            constexpr uint32_t G3 = (NW / 4) * 3;
+            static_assert(NW % 4 == 0, "four SIMDs");
+            const uint32_t wslot = (wv & 3u) != 3u ? (wv >> 2) * 3u + (wv & 3u) : G3 + (wv >> 2);
+            // Walk: indices with three or four ranks -- sorted by a network,
+            // summed with the association their separators dictate.
+            for (uint32_t i = wslot * 64u + lane; i < NA; i += NT) {
+                const uint32_t item = s_lista[i];
+                const uint32_t jj = item & 0xFFFu, st0 = item >> 12;
+                const uint32_t mm = s_cnt[jj] & 0x1FFu;
                 uint32_t rk[4];
                 float vv[4];
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    rk[e] = s_sr[st0 + e];
-                    vv[e] = VALS ? s_sv[st0 + e] : 0.0f;
+                rk[0] = s_r0[jj];
+                rk[1] = s_sr[st0];
+                rk[2] = s_sr[st0 + 1];
+                rk[3] = mm == 4u ? (uint32_t)s_sr[st0 + 2] : 0x100u;  // above every rank
+                if (VALS) {
+                    vv[0] = s_out[jj];
+                    vv[1] = s_sv[st0];
+                    vv[2] = s_sv[st0 + 1];
+                    vv[3] = mm == 4u ? s_sv[st0 + 2] : 0.0f;
+                } else {
+                    vv[0] = vv[1] = vv[2] = vv[3] = 0.0f;
                 }
-                if (m == 3u) {
-                    rk[3] = 0x100u;  // above every rank
-                    vv[3] = 0.0f;
-                }
-                auto cswap = [&](int x, int y) {
-                    const bool sw = rk[x] > rk[y];
-                    const uint32_t tr = rk[x];
-                    const float tv = vv[x];
-                    rk[x] = sw ? rk[y] : rk[x];
-                    rk[y] = sw ? tr : rk[y];
-                    vv[x] = sw ? vv[y] : vv[x];
-                    vv[y] = sw ? tv : vv[y];
-                };
-                cswap(0, 1);
-                cswap(2, 3);
-                cswap(0, 2);
-                cswap(1, 3);
-                cswap(1, 2);
+                cswap_rv(rk, vv, 0, 1);
+                cswap_rv(rk, vv, 2, 3);
+                cswap_rv(rk, vv, 0, 2);
+                cswap_rv(rk, vv, 1, 3);
+                cswap_rv(rk, vv, 1, 2);
                 const uint32_t c1 = sep_level(rk[0], rk[1]), c2 = sep_level(rk[1], rk[2]);
-                const uint32_t c3 = m == 4u ? sep_level(rk[2], rk[3]) : 0u;
+                const uint32_t c3 = mm == 4u ? sep_level(rk[2], rk[3]) : 0u;
                 if (CNTS) {
                     atomicAdd(&s_E[c1 * PMAX + rk[1]], 1u);
                     atomicAdd(&s_E[c2 * PMAX + rk[2]], 1u);
-                    atomicAdd(&s_E[m == 4u ? c3 * PMAX + rk[3] : EW + lane], 1u);
+                    atomicAdd(&s_E[mm == 4u ? c3 * PMAX + rk[3] : EW + lane], 1u);
                 }
                 if (VALS) {
                     float sum;
                     const float t012 = c1 < c2 ? (vv[0] + vv[1]) + vv[2] : vv[0] + (vv[1] + vv[2]);
-                    if (m == 3u) sum = t012;
+                    if (mm == 3u) sum = t012;
                     else if (c2 > c1 && c2 > c3) sum = (vv[0] + vv[1]) + (vv[2] + vv[3]);
                     else if (c1 > c3) sum = vv[0] + (c2 < c3 ? (vv[1] + vv[2]) + vv[3] : vv[1] + (vv[2] + vv[3]));
                     else sum = t012 + vv[3];
-                    if (MODE == kDense) {
-                        s_out[j] = sum + 0.0f;
-                    } else {
-                        a.out_idx[toff + nz] = tlo + j;
-                        a.out_val[toff + nz] = sum;
-                    }
+                    emit(jj, sum);
                 }
             }
-            // Walk: indices with five to eight ranks, one per thread.
-            // (five to eight ranks take the threads from the top down and more
-            // than eight the waves from the last one down, so that they share
-            // as few waves as possible with the three-four rank indices)
-            for (uint32_t i = NA + (NT - 1u - tid); i < NA + NB; i += NT) {
-                const uint2 item = s_list[i];
-                const uint32_t j = item.x & 0xFFFFu, nz = item.x >> 16;
-                const uint32_t st0 = item.y & 0xFFFFu, m = item.y >> 16;
-                // up to eight: all reads at once, a sorting network (ranks
-                // past m are distinct sentinels above every rank), then
-                // the separator stack over the sorted run
+            // Walk: indices with five to eight ranks, one per thread (from the
+            // top thread down, so that they share few waves with the above):
+            // a sorting network (ranks past m are distinct sentinels above
+            // every rank), then a stack keyed by separator level.
+            for (uint32_t i = NT - 1u - tid; i < NB; i += NT) {
+                const uint32_t item = s_listb[i];
+                const uint32_t jj = item & 0xFFFu, st0 = item >> 12;
+                const uint32_t mm = s_cnt[jj] & 0x1FFu;
                 uint32_t rk[8];
                 float vv[8];
+                rk[0] = s_r0[jj];
+                vv[0] = VALS ? s_out[jj] : 0.0f;
 #pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    const uint32_t rr = s_sr[st0 + e];
-                    const float v = VALS ? s_sv[st0 + e] : 0.0f;
-                    rk[e] = (uint32_t)e < m ? rr : 0x100u + (uint32_t)e;
-                    vv[e] = v;
+                for (int e = 1; e < 8; ++e) {
+                    const uint32_t rr = s_sr[st0 + e - 1];
+                    vv[e] = VALS ? s_sv[st0 + e - 1] : 0.0f;
+                    rk[e] = (uint32_t)e < mm ? rr : 0x100u + (uint32_t)e;
                 }
-                auto cswap = [&](int x, int y) {
-                    const bool sw = rk[x] > rk[y];
-                    const uint32_t tr = rk[x];
-                    const float tv = vv[x];
-                    rk[x] = sw ? rk[y] : rk[x];
-                    rk[y] = sw ? tr : rk[y];
-                    vv[x] = sw ? vv[y] : vv[x];
-                    vv[y] = sw ? tv : vv[y];
-                };
-                cswap(0, 2); cswap(1, 3); cswap(4, 6); cswap(5, 7);
-                cswap(0, 4); cswap(1, 5); cswap(2, 6); cswap(3, 7);
-                cswap(0, 1); cswap(2, 3); cswap(4, 5); cswap(6, 7);
-                cswap(2, 4); cswap(3, 5); cswap(1, 4); cswap(3, 6);
-                cswap(1, 2); cswap(3, 4); cswap(5, 6);
+                cswap_rv(rk, vv, 0, 2); cswap_rv(rk, vv, 1, 3); cswap_rv(rk, vv, 4, 6); cswap_rv(rk, vv, 5, 7);
+                cswap_rv(rk, vv, 0, 4); cswap_rv(rk, vv, 1, 5); cswap_rv(rk, vv, 2, 6); cswap_rv(rk, vv, 3, 7);
+                cswap_rv(rk, vv, 0, 1); cswap_rv(rk, vv, 2, 3); cswap_rv(rk, vv, 4, 5); cswap_rv(rk, vv, 6, 7);
+                cswap_rv(rk, vv, 2, 4); cswap_rv(rk, vv, 3, 5); cswap_rv(rk, vv, 1, 4); cswap_rv(rk, vv, 3, 6);
+                cswap_rv(rk, vv, 1, 2); cswap_rv(rk, vv, 3, 4); cswap_rv(rk, vv, 5, 6);
                 float slot[LMAX];
 #pragma unroll
                 for (int l = 0; l < LMAX; ++l) slot[l] = 0.0f;
@@ -638,7 +673,7 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
                 uint32_t pend = 0u;
 #pragma unroll
                 for (int e = 1; e < 8; ++e) {
-                    if ((uint32_t)e < m) {
+                    if ((uint32_t)e < mm) {
                         const uint32_t sep = sep_level(rk[e - 1], rk[e]);
                         if (CNTS) atomicAdd(&s_E[sep * PMAX + rk[e]], 1u);
                         if (VALS) {
@@ -657,28 +692,25 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
 #pragma unroll
                     for (int l = 0; l < LMAX; ++l)
                         if ((pend >> l) & 1u) cur = slot[l] + cur;
-                    if (MODE == kDense) {
-                        s_out[j] = cur + 0.0f;
-                    } else {
-                        a.out_idx[toff + nz] = tlo + j;
-                        a.out_val[toff + nz] = cur;
-                    }
+                    emit(jj, cur);
                 }
             }
-            // Walk: indices with more than eight ranks, one per wave.  The
-            // values are laid out by rank (lane l holds ranks l*K .. l*K+K-1)
-            // and the tree is evaluated level by level: a node is the sum of
-            // its two children when both hold a value, else the one that
-            // does -- the recursive doubling of the ranks present.
-            for (uint32_t i = NA + NB + (NW - 1u - wv); i < NA + NB + NC; i += NW) {
-                const uint2 item = s_list[i];
-                const uint32_t j = item.x & 0xFFFFu, nz = item.x >> 16;
-                const uint32_t st0 = item.y & 0xFFFFu, m = item.y >> 16;
-                float* wval = s_wv + wv * PMAX;
-                uint32_t* wpre = s_wp + wv * PW;
-                for (uint32_t e = lane; e < m; e += 64u) {
-                    const uint32_t r = s_sr[st0 + e];
-                    if (VALS) wval[r] = s_sv[st0 + e];
+            // Walk: indices with more than eight ranks, one per wave.  The values are laid out by rank (lane l holds
+            // ranks l*K .. l*K+K-1) and the tree is evaluated level by level:
+            // a node is the sum of its two children when both hold a value,
+            // else the one that does -- the recursive doubling of the ranks
+            // present.
+            float* const wval = s_wv + wv * PMAX;
+            uint32_t* const wpre = s_wp + wv * PW;
+            for (uint32_t i = wslot < G3 ? G3 - 1u - wslot : wslot; i < NC; i += NW) {
+                const uint32_t item = s_listb[CCAP - 1u - i];
+                const uint32_t jj = item & 0xFFFu, st0 = item >> 12;
+                const uint32_t mm = s_cnt[jj] & 0x1FFu;
+                if (lane < (uint32_t)PW) wpre[lane] = 0u;
+                __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+                for (uint32_t e = lane; e < mm; e += 64u) {
+                    const uint32_t r = e == 0u ? (uint32_t)s_r0[jj] : (uint32_t)s_sr[st0 + e - 1u];
+                    if (VALS) wval[r] = e == 0u ? s_out[jj] : s_sv[st0 + e - 1u];
                     atomicOr(&wpre[r >> 5], 1u << (r & 31u));
                 }
                 __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
@@ -720,25 +752,22 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
                     }
                     float v = lv[0];
                     uint32_t pr = lp[0] ? 1u : 0u;
+                    tree_level<1>(v, pr, lane);
+                    tree_level<2>(v, pr, lane);
+                    tree_level<4>(v, pr, lane);
+                    tree_level<8>(v, pr, lane);
+                    // the four row results (lanes 0, 16, 32, 48)
+                    float rv[4];
+                    uint32_t rp[4];
 #pragma unroll
-                    for (uint32_t sh = 1; sh < 64u; sh <<= 1) {
-                        const float ov = __shfl_down(v, sh);
-                        const uint32_t op = (uint32_t)__shfl_down((int)pr, sh);
-                        if ((lane & (2u * sh - 1u)) == 0u) {
-                            v = pr && op ? v + ov : (pr ? v : ov);
-                            pr |= op;
-                        }
+                    for (int q = 0; q < 4; ++q) {
+                        rv[q] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16 * q));
+                        rp[q] = (uint32_t)__builtin_amdgcn_readlane((int)pr, 16 * q);
                     }
-                    if (lane == 0u) {
-                        if (MODE == kDense) {
-                            s_out[j] = v + 0.0f;
-                        } else {
-                            a.out_idx[toff + nz] = tlo + j;
-                            a.out_val[toff + nz] = v;
-                        }
-                    }
+                    const float lo = tree_join(rv[0], rp[0], rv[1], rp[1]);
+                    const float hi = tree_join(rv[2], rp[2], rv[3], rp[3]);
+                    if (lane == 0u) emit(jj, tree_join(lo, rp[0] | rp[1], hi, rp[2] | rp[3]));
                 }
-                if (lane < (uint32_t)PW) wpre[lane] = 0u;
                 __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
             }
             __syncthreads();
@@ -760,8 +789,18 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
                 }
                 *reinterpret_cast<uint4*>(&s_cnt[c]) = make_uint4(0u, 0u, 0u, 0u);
             }
+        } else {
+            __syncthreads();  // every thread has read the counters
+            if (tid == 0) {
+                reset_counters();
+                const uint32_t k = atomicAdd(a.slow_count, 1u);
+                a.slow_list[k] = tile;
+            }
+            for (uint32_t c = opaque_v(tid) * 4u; c < T; c += NT * 4u) {
+                *reinterpret_cast<uint4*>(&s_cnt[c]) = make_uint4(0u, 0u, 0u, 0u);
+                if (VALS) *reinterpret_cast<float4*>(&s_out[c]) = make_float4(0.f, 0.f, 0.f, 0.f);
+            }
         }
-        if (tid == 0) s_flag = 0u;
         __syncthreads();
     }
     __syncthreads();

@@ -188,3 +188,29 @@ def test_runs_of_consecutive_indices(P):
         val.append(inputs.normal(rng, a.size))
     for delta in (1.0, 0.05):
         check(idx, val, N, delta, f"runs P={P} delta={delta}")
+
+
+@pytest.mark.parametrize("P,density,bits", [(128, 0.0125, 4), (64, 0.025, 0), (32, 0.05, 2), (256, 0.006, 0)])
+def test_wave_regions_near_capacity(P, density, bits):
+    """Per-wave entry counts per tile near the wave's entry region (each wave
+    collects its ranks' in-tile entries, up to a few hundred): the arrival
+    loop runs all its steps, and tiles past the region take the slow path."""
+    from gpu_util import to_dev, torch_dev
+    rng = np.random.default_rng(900 + P)
+    N = 50021
+    k = int(density * N)
+    idx = [inputs.uniform_subset(rng, N, k) for _ in range(P)]
+    val = [inputs.laplace(rng, 1.0, k) for _ in range(P)]
+    if bits:
+        q, scale, deq = oracle.quantize(val, bits, seed=5 + bits)
+        torch, dev = torch_dev()
+        codes = [to_dev(a) for a in q]
+        scales = to_dev(scale)
+        for delta in (1.0, 0.01):
+            say(f"[reduce] near capacity P={P} bits={bits} delta={delta}")
+            o = oracle.sparse_reduce(idx, deq, N, delta)
+            g = gpu_reduce(idx, None, N, delta, qbits=bits, codes=codes, scales=scales)
+            assert_reduce_equal(g, o, f"near capacity P={P} q{bits}")
+    else:
+        for delta in (1.0, 0.01):
+            check(idx, val, N, delta, f"near capacity P={P} delta={delta}")
