@@ -161,6 +161,28 @@ __device__ __forceinline__ uint32_t wave_scan(uint32_t v)
     return v;
 }
 
+// Mask of the active lanes whose predicate holds.
+__device__ __forceinline__ uint64_t ballot(bool p)
+{
+    return __builtin_amdgcn_ballot_w64(p);
+}
+
+// Masks of the active lanes where a == b, a < b (unsigned): one compare each.
+__device__ __forceinline__ uint64_t lanes_eq(uint32_t a, uint32_t b)
+{
+    return __builtin_amdgcn_uicmp(a, b, 32);  // ICMP_EQ
+}
+__device__ __forceinline__ uint64_t lanes_lt(uint32_t a, uint32_t b)
+{
+    return __builtin_amdgcn_uicmp(a, b, 36);  // ICMP_ULT
+}
+
+// base + the number of lanes below this one set in m.
+__device__ __forceinline__ uint32_t below_count(uint64_t m, uint32_t base)
+{
+    return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, base));
+}
+
 // A tree node: the sum of its two children when both hold a value, else the
 // one that does (px, py: whether x, y hold one).
 __device__ __forceinline__ float tree_join(float x, uint32_t px, float y, uint32_t py)
@@ -225,8 +247,8 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
     // positions are known), the first arrival's value and rank, the staging
     // start of the later arrivals of an index with three or more.
     __shared__ __align__(16) uint32_t s_cnt[TMAX + 64];  // 64 dummies for idle lanes
-    __shared__ __align__(16) float s_out[VALS ? TMAX : 4];  // first value; dense: the sum
-    __shared__ uint8_t s_r0[TMAX];
+    __shared__ __align__(16) float s_out[VALS ? TMAX + 64 : 4];  // first value; dense: the sum
+    __shared__ uint8_t s_r0[TMAX + 64];
     __shared__ uint16_t s_start[TMAX];
     // Per wave: the tile's entries {j | rank << 12 | code position << 20, raw
     // value word}, then its later arrivals {j | rank << 12 | arrival number
@@ -235,7 +257,7 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
     __shared__ __align__(16) uint2 s_ent[NW * ERGN];
     __shared__ float s_sv[VALS ? CAP + 8 : 1];             // later values by index, arrival order
     __shared__ uint8_t s_sr[CAP + 8];                      // and their ranks
-    __shared__ uint16_t s_cands[CCAP];                     // per wave: indices with three or more ranks
+    __shared__ uint16_t s_cands[NW * (CWC + 64)];          // per wave: indices with three or more ranks
     __shared__ uint32_t s_lista[CCAP];                     // 3-4 ranks: j | start << 12
     __shared__ uint32_t s_listb[CCAP];                     // 5-8 from the bottom, > 8 from the top
     __shared__ uint32_t s_E[CNTS ? EW + 64 : 1];
@@ -259,9 +281,8 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
     const uint32_t chunk = blockIdx.x, stride = a.nchunks + 1;
     const uint32_t t0 = chunk * a.tpc, t1 = min(t0 + a.tpc, a.ntiles);
     const uint32_t qbits = a.qbits, qlog = qbits == 8u ? 3u : (qbits == 4u ? 2u : 1u);
-    const uint32_t plog = qbits == 8u ? 0u : (qbits == 4u ? 1u : 2u), pm = (1u << plog) - 1u;
+    const uint32_t plog = qbits == 8u ? 0u : (qbits == 4u ? 1u : 2u);
     const uint32_t EB = wv * ERGN;  // this wave's entry region
-    const uint64_t below = (1ull << lane) - 1ull;
 
     // Loop-invariant values (LDS addresses of a thread's coordinates) would
     // be hoisted out of the tile loop and held in registers or spilled; an
@@ -324,13 +345,16 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
     };
     // Value bits of a window entry at stream position pos + lane: the fp32
     // word, or the entry's code (its bits of the byte) dequantized.
-    // (+-level * unit, level 0 giving +0, as the signed level times the unit.)
+    // (+-level * unit, level 0 giving +0: the sign bit set on a nonzero
+    // level negates the product.)
+    const uint32_t hbit = 1u << (qbits - 1u);
     auto decode = [&](uint32_t v, uint32_t pos, float unit) -> uint32_t {
         if (!QUANT) return v;
-        const uint32_t code = __builtin_amdgcn_ubfe(v, ((lane + pos) & pm) << qlog, qbits);
-        const uint32_t lev = code & ((1u << (qbits - 1u)) - 1u);
-        const int sl = (code >> (qbits - 1u)) ? -(int)lev : (int)lev;
-        return lev ? __float_as_uint(__fmul_rn((float)sl, unit)) : 0u;
+        const uint32_t code = __builtin_amdgcn_ubfe(v, ((lane + pos) << qlog) & 7u, qbits);
+        const uint32_t lev = code & (hbit - 1u);
+        const float mag = __fmul_rn((float)lev, unit);
+        const float val = code > hbit ? -mag : mag;
+        return lev ? __float_as_uint(val) : 0u;
     };
     // Append a window to this wave's entry region as {j | rank << 12, value
     // bits}: the in-tile entries of a window are a prefix of it (streams are
@@ -379,8 +403,7 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
                 const uint32_t jr0 = (((uint32_t)s * NW + wv) << 12) - tlo;
                 uint32_t pos = st[q].x;
                 const uint32_t end = st[q].z, last = st[q].w;
-                const bool in = xr[s] - tlo < TT && lane < end - pos;
-                uint32_t n = (uint32_t)__popcll(__ballot(in));
+                uint32_t n = (uint32_t)__popcll(lanes_lt(xr[s] - tlo, TT) & lanes_lt(lane, end - pos));
                 append(nent, xr[s] + jr0, VALS ? decode(vr[s], pos, un[q]) : 0u);
                 nent += n;
                 pos += n;
@@ -389,8 +412,7 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
                     do {
                         uint32_t x2, v2;
                         load_win_at(bs[q], last, pos, x2, v2);
-                        const bool in2 = x2 - tlo < TT && lane < end - pos;
-                        n = (uint32_t)__popcll(__ballot(in2));
+                        n = (uint32_t)__popcll(lanes_lt(x2 - tlo, TT) & lanes_lt(lane, end - pos));
                         append(nent, x2 + jr0, VALS ? decode(v2, pos, un[q]) : 0u);
                         nent += n;
                         pos += n;
@@ -414,7 +436,7 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
         // (Lanes read entries other lanes of the wave wrote: the fence orders
         // them for the compiler.)
         __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
-        const uint32_t CB = wv * CWC;  // this wave's candidate region
+        const uint32_t CB = wv * (CWC + 64u);  // this wave's candidate region
         uint32_t nlat = 0u, ncw = 0u, nfirst = 0u;
         uint2 nx0 = s_ent[EB + lane], nx1 = s_ent[EB + 64u + lane];
         for (uint32_t b = 0; b < ne_w; b += 128u) {
@@ -428,27 +450,31 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
             const bool f0 = ok0 && k0 == 0u, f1 = ok1 && k1 == 0u;
             const bool l0 = ok0 && k0 != 0u, l1 = ok1 && k1 != 0u;
             const bool c0 = ok0 && k0 == 2u, c1 = ok1 && k1 == 2u;
-            if (f0) {
-                s_r0[j0] = (uint8_t)(en0.x >> 12);
-                if (VALS) s_out[j0] = MODE == kDense ? __uint_as_float(en0.y) + 0.0f : __uint_as_float(en0.y);
-            }
-            if (f1) {
-                s_r0[j1] = (uint8_t)(en1.x >> 12);
-                if (VALS) s_out[j1] = MODE == kDense ? __uint_as_float(en1.y) + 0.0f : __uint_as_float(en1.y);
-            }
-            const uint64_t L0 = __ballot(l0), L1 = __ballot(l1);
-            const uint64_t C0 = __ballot(c0), C1 = __ballot(c1);
-            if (CNTS) nfirst += (uint32_t)__popcll(__ballot(f0)) + (uint32_t)__popcll(__ballot(f1));
-            if (l0) s_ent[EB + nlat + (uint32_t)__popcll(L0 & below)] = make_uint2(en0.x | k0 << 20, en0.y);
+            // Writes are unconditional: a lane with nothing to write aims at
+            // a dummy word (past the tile, the region's slack, the list's end).
+            const uint32_t fj0 = f0 ? j0 : TMAX + lane, fj1 = f1 ? j1 : TMAX + lane;
+            s_r0[fj0] = (uint8_t)(en0.x >> 12);
+            if (VALS) s_out[fj0] = MODE == kDense ? __uint_as_float(en0.y) + 0.0f : __uint_as_float(en0.y);
+            s_r0[fj1] = (uint8_t)(en1.x >> 12);
+            if (VALS) s_out[fj1] = MODE == kDense ? __uint_as_float(en1.y) + 0.0f : __uint_as_float(en1.y);
+            // lane masks from single comparisons, combined on the scalar unit
+            const uint64_t OK0 = lanes_lt(b + lane, ne_w), OK1 = lanes_lt(b + 64u + lane, ne_w);
+            const uint64_t Z0 = lanes_eq(k0, 0u), Z1 = lanes_eq(k1, 0u);
+            const uint64_t L0 = OK0 & ~Z0, L1 = OK1 & ~Z1;
+            const uint64_t C0 = OK0 & lanes_eq(k0, 2u), C1 = OK1 & lanes_eq(k1, 2u);
+            if (CNTS) nfirst += (uint32_t)__popcll(OK0 & Z0) + (uint32_t)__popcll(OK1 & Z1);
+            const uint32_t p0 = below_count(L0, nlat);
             nlat += (uint32_t)__popcll(L0);
-            if (l1) s_ent[EB + nlat + (uint32_t)__popcll(L1 & below)] = make_uint2(en1.x | k1 << 20, en1.y);
+            const uint32_t p1 = below_count(L1, nlat);
             nlat += (uint32_t)__popcll(L1);
-            const uint32_t q0 = ncw + (uint32_t)__popcll(C0 & below);
-            if (c0 && q0 < CWC) s_cands[CB + q0] = (uint16_t)j0;
+            const uint32_t q0 = below_count(C0, ncw);
             ncw += (uint32_t)__popcll(C0);
-            const uint32_t q1 = ncw + (uint32_t)__popcll(C1 & below);
-            if (c1 && q1 < CWC) s_cands[CB + q1] = (uint16_t)j1;
+            const uint32_t q1 = below_count(C1, ncw);
             ncw += (uint32_t)__popcll(C1);
+            s_ent[EB + (l0 ? p0 : ECAP + lane)] = make_uint2(en0.x | k0 << 20, en0.y);
+            s_ent[EB + (l1 ? p1 : ECAP + lane)] = make_uint2(en1.x | k1 << 20, en1.y);
+            s_cands[CB + (c0 && q0 < CWC ? q0 : CWC + lane)] = (uint16_t)j0;
+            s_cands[CB + (c1 && q1 < CWC ? q1 : CWC + lane)] = (uint16_t)j1;
         }
         if (lane == 0u) {
             if (CNTS && nfirst) atomicAdd(&s_ne, nfirst);
@@ -503,7 +529,8 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
                 const uint32_t ext = act ? m - 1u : 0u;
                 const uint32_t incl = wave_scan(ext);
                 const bool ca = act && m <= 4u, cb = act && m - 5u < 4u, cc = act && m > 8u;
-                const uint64_t BA = __ballot(ca), BB = __ballot(cb), BC = __ballot(cc);
+                const uint64_t ACT = lanes_lt(i, ncw);
+                const uint64_t BA = ACT & lanes_lt(m, 5u), BB = ACT & lanes_lt(m - 5u, 4u), BC = ACT & ~lanes_lt(m, 9u);
                 // one reservation for the staging range and the three lists
                 const uint64_t want = (uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)incl, 63) |
                                       (uint64_t)__popcll(BA) << 16 | (uint64_t)__popcll(BB) << 32 |
@@ -513,9 +540,9 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
                 const uint32_t glo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)got);
                 const uint32_t ghi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(got >> 32));
                 const uint32_t start = (glo & 0xFFFFu) + incl - ext;
-                const uint32_t pa = (glo >> 16) + (uint32_t)__popcll(BA & below);
-                const uint32_t pb = (ghi & 0xFFFFu) + (uint32_t)__popcll(BB & below);
-                const uint32_t pc = (ghi >> 16) + (uint32_t)__popcll(BC & below);
+                const uint32_t pa = below_count(BA, glo >> 16);
+                const uint32_t pb = below_count(BB, ghi & 0xFFFFu);
+                const uint32_t pc = below_count(BC, ghi >> 16);
                 if (act && start + ext <= CAP) {
                     s_start[j] = (uint16_t)start;
                     const uint32_t item = j | start << 12;
