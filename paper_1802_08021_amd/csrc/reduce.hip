@@ -243,13 +243,14 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
     constexpr int PW = (PMAX + 31) / 32;        // rank-mask words
     static_assert(NW * PMAX + NW * PW <= 2 * NW * (int)ERGN, "walk buffers alias the entry regions");
 
-    // Per index: arrivals (sparse output: m | output position << 9 once the
-    // positions are known), the first arrival's value and rank, the staging
-    // start of the later arrivals of an index with three or more.
+    // Per index: arrivals, then m | aux << 9 with aux the staging start of an
+    // index with three or more ranks (sparse output: the output position of
+    // every non-empty index, the staging start apart); the first arrival's
+    // value and rank.
     __shared__ __align__(16) uint32_t s_cnt[TMAX + 64];  // 64 dummies for idle lanes
     __shared__ __align__(16) float s_out[VALS ? TMAX + 64 : 4];  // first value; dense: the sum
     __shared__ uint8_t s_r0[TMAX + 64];
-    __shared__ uint16_t s_start[TMAX];
+    __shared__ uint16_t s_start[MODE == kSparseWrite ? TMAX : 1];  // staging start (sparse output)
     // Per wave: the tile's entries {j | rank << 12 | code position << 20, raw
     // value word}, then its later arrivals {j | rank << 12 | arrival number
     // << 20, value}.  The walk of indices with more than eight ranks reuses
@@ -544,7 +545,8 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
                 const uint32_t pb = below_count(BB, ghi & 0xFFFFu);
                 const uint32_t pc = below_count(BC, ghi >> 16);
                 if (act && start + ext <= CAP) {
-                    s_start[j] = (uint16_t)start;
+                    if (MODE == kSparseWrite) s_start[j] = (uint16_t)start;
+                    else s_cnt[j] = m | start << 9;
                     const uint32_t item = j | start << 12;
                     if (ca) s_lista[pa] = item;
                     if (cb) s_listb[pb] = item;
@@ -594,7 +596,8 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
                 const uint32_t ja = e0.x & 0xFFFu, jb = e1.x & 0xFFFu;
                 const uint32_t sa = s_cnt[ja], sb = s_cnt[jb];
                 const uint32_t ra = s_r0[ja], rb = s_r0[jb];
-                const uint32_t ta = s_start[ja], tb = s_start[jb];
+                const uint32_t ta = MODE == kSparseWrite ? (uint32_t)s_start[ja] : sa >> 9;
+                const uint32_t tb = MODE == kSparseWrite ? (uint32_t)s_start[jb] : sb >> 9;
                 const float oa = VALS ? s_out[ja] : 0.0f, ob = VALS ? s_out[jb] : 0.0f;
                 place(e0, sa, ra, ta, oa);
                 if (two) place(e1, sb, rb, tb, ob);
@@ -995,32 +998,47 @@ __global__ void k_partition(const StreamDesc* tab, uint32_t* off, uint32_t P, ui
 
 // Switch rule over the tree (§5.1): node dense iff a child is dense or the
 // children's nnz sum exceeds thr; a sparse node's nnz is its union size.
-__global__ void k_decide(const StreamDesc* tab, const uint32_t* node_cnt, uint32_t P, uint64_t N,
-                         uint64_t thr, uint64_t* node_nnz, uint8_t* node_dense, ReduceResult* hdr)
+__global__ void __launch_bounds__(256) k_decide(const StreamDesc* tab, const uint32_t* node_cnt, uint32_t P,
+                                                uint64_t N, uint64_t thr, uint64_t* node_nnz,
+                                                uint8_t* node_dense, ReduceResult* hdr)
 {
-    __shared__ uint64_t s_n[256];
+    // Stream sizes and node union sizes are read by all threads at once; one
+    // thread then applies the rule level by level in LDS; all threads store.
+    __shared__ uint64_t s_n[256];    // per group of the current level
     __shared__ uint8_t s_d[256];
-    if (threadIdx.x != 0) return;
-    for (uint32_t r = 0; r < P; ++r) {
-        s_n[r] = tab[r].nnz;
-        s_d[r] = 0;
+    __shared__ uint32_t s_c[256];    // union sizes, level order
+    __shared__ uint64_t s_nn[256];   // decided node sizes
+    __shared__ uint8_t s_nd[256];
+    const uint32_t t = threadIdx.x;
+    if (t < P) {
+        s_n[t] = tab[t].nnz;
+        s_d[t] = 0;
     }
-    uint32_t width = P, node = 0;
-    while (width > 1) {
-        for (uint32_t g = 0; g < width / 2; ++g) {
-            const bool dense = s_d[2 * g] || s_d[2 * g + 1] || (s_n[2 * g] + s_n[2 * g + 1] > thr);
-            const uint64_t nnz = dense ? N : (uint64_t)node_cnt[node];
-            if (node_nnz) node_nnz[node] = nnz;
-            if (node_dense) node_dense[node] = dense ? 1 : 0;
-            s_n[g] = nnz;
-            s_d[g] = dense ? 1 : 0;
-            ++node;
+    if (t + 1 < P) s_c[t] = node_cnt[t];
+    __syncthreads();
+    if (t == 0) {
+        uint32_t width = P, node = 0;
+        while (width > 1) {
+            for (uint32_t g = 0; g < width / 2; ++g) {
+                const bool dense = s_d[2 * g] || s_d[2 * g + 1] || (s_n[2 * g] + s_n[2 * g + 1] > thr);
+                const uint64_t nnz = dense ? N : (uint64_t)s_c[node];
+                s_nn[node] = nnz;
+                s_nd[node] = dense ? 1 : 0;
+                s_n[g] = nnz;
+                s_d[g] = dense ? 1 : 0;
+                ++node;
+            }
+            width /= 2;
         }
-        width /= 2;
+        hdr->nnz = s_n[0];
+        hdr->dense = s_d[0];
+        hdr->pad = 0;
     }
-    hdr->nnz = s_n[0];
-    hdr->dense = s_d[0];
-    hdr->pad = 0;
+    __syncthreads();
+    if (t + 1 < P) {
+        if (node_nnz) node_nnz[t] = s_nn[t];
+        if (node_dense) node_dense[t] = s_nd[t];
+    }
 }
 
 // Exclusive scan of the per-tile root union sizes (one workgroup); also
@@ -1223,7 +1241,7 @@ hipError_t reduce_run(const ReducePlan& p, const StreamDesc* host_tab, uint32_t*
     e = p.speculate_dense ? launch_pass<kDense>(a, p.PK, quant, s)
                           : launch_pass<kCount>(a, p.PK, quant, s);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_decide, dim3(1), dim3(64), 0, s, l.tab, l.node_cnt, p.P, p.N, p.thr,
+    hipLaunchKernelGGL(k_decide, dim3(1), dim3(256), 0, s, l.tab, l.node_cnt, p.P, p.N, p.thr,
                        node_nnz, node_dense, l.hdr);
     if ((e = hipGetLastError()) != hipSuccess) return e;
 
