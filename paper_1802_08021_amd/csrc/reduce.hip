@@ -161,12 +161,6 @@ __device__ __forceinline__ uint32_t wave_scan(uint32_t v)
     return v;
 }
 
-// Mask of the active lanes whose predicate holds.
-__device__ __forceinline__ uint64_t ballot(bool p)
-{
-    return __builtin_amdgcn_ballot_w64(p);
-}
-
 // Masks of the active lanes where a == b, a < b (unsigned): one compare each.
 __device__ __forceinline__ uint64_t lanes_eq(uint32_t a, uint32_t b)
 {
@@ -200,6 +194,19 @@ __device__ __forceinline__ void tree_level(float& v, uint32_t& pr, uint32_t lane
     const bool at = (lane & (2u * H - 1u)) == 0u;
     v = at ? tree_join(v, pr, ov, op) : v;
     pr = at ? (pr | op) : pr;
+}
+
+// Tree sums of three and four values in rank order, given the separator
+// levels between neighbours (distinct within the run): the root splits at the
+// largest separator.
+__device__ __forceinline__ float tree3(float a, float b, float c, uint32_t x, uint32_t y)
+{
+    return x < y ? (a + b) + c : a + (b + c);
+}
+__device__ __forceinline__ float tree4(float a, float b, float c, float d, uint32_t x, uint32_t y, uint32_t z)
+{
+    if (y > x && y > z) return (a + b) + (c + d);
+    return x > z ? a + tree3(b, c, d, y, z) : tree3(a, b, c, x, y) + d;
 }
 
 // Level at which ranks a != b first meet: their highest differing bit
@@ -241,7 +248,9 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
     constexpr bool VALS = MODE != kCount, CNTS = MODE != kSparseWrite;
     constexpr uint32_t EW = PMAX * (LMAX + 1);  // node-count words; 64 dummies follow
     constexpr int PW = (PMAX + 31) / 32;        // rank-mask words
-    static_assert(NW * PMAX + NW * PW <= 2 * NW * (int)ERGN, "walk buffers alias the entry regions");
+    constexpr uint32_t RROWS = PMAX >= 256 ? 2u : 4u;  // indices per wave in the row walk
+    constexpr uint32_t RK = PMAX / 16;                  // ranks per lane in the row walk
+    static_assert(NW * RROWS * (PMAX + PW) <= 2 * NW * (int)ERGN, "walk buffers alias the entry regions");
 
     // Per index: arrivals, then m | aux << 9 with aux the staging start of an
     // index with three or more ranks (sparse output: the output position of
@@ -260,7 +269,7 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
     __shared__ uint8_t s_sr[CAP + 8];                      // and their ranks
     __shared__ uint16_t s_cands[NW * (CWC + 64)];          // per wave: indices with three or more ranks
     __shared__ uint32_t s_lista[CCAP];                     // 3-4 ranks: j | start << 12
-    __shared__ uint32_t s_listb[CCAP];                     // 5-8 from the bottom, > 8 from the top
+    __shared__ uint32_t s_listb[CCAP];                     // 6+ ranks from the bottom, 5 from the top
     __shared__ uint32_t s_E[CNTS ? EW + 64 : 1];
     // Per wave and slot: {stream position, entries in this tile, chunk end,
     // last readable entry}, {index base, value base}, {level unit}.  Slot s
@@ -269,12 +278,13 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
     // dummy address.  A wave reads its slots at fixed offsets.
     __shared__ uint4 s_slot[NW * SLMAX * 3];
     __shared__ uint32_t s_wtot[NW];
-    // tile counters: staged values | list A << 16 | list B << 32 | list C << 48
-    // (each below 2^16), non-empty indices, overflow flag
+    // tile counters: staged values | list A << 16 | list B << 32 | five-rank
+    // list << 48 (each below 2^16), non-empty indices, overflow flag
     __shared__ uint64_t s_alloc;
     __shared__ uint32_t s_ne, s_flag;
-    float* const s_wv = reinterpret_cast<float*>(s_ent);                  // per wave: values by rank
-    uint32_t* const s_wp = reinterpret_cast<uint32_t*>(s_ent) + NW * PMAX;  // per wave: ranks present
+    // per wave and row of the row walk: values by rank, ranks present
+    float* const s_wv = reinterpret_cast<float*>(s_ent);
+    uint32_t* const s_wp = reinterpret_cast<uint32_t*>(s_ent) + NW * RROWS * PMAX;
 
     const uint32_t tid = threadIdx.x, lane = tid & 63u;
     const uint32_t wv = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -529,13 +539,13 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
                 const uint32_t m = act ? s_cnt[j] & 0x1FFu : 0u;
                 const uint32_t ext = act ? m - 1u : 0u;
                 const uint32_t incl = wave_scan(ext);
-                const bool ca = act && m <= 4u, cb = act && m - 5u < 4u, cc = act && m > 8u;
+                const bool ca = act && m <= 4u, cb = act && m > 5u, c5 = act && m == 5u;
                 const uint64_t ACT = lanes_lt(i, ncw);
-                const uint64_t BA = ACT & lanes_lt(m, 5u), BB = ACT & lanes_lt(m - 5u, 4u), BC = ACT & ~lanes_lt(m, 9u);
+                const uint64_t BA = ACT & lanes_lt(m, 5u), BB = ACT & ~lanes_lt(m, 6u), B5 = ACT & lanes_eq(m, 5u);
                 // one reservation for the staging range and the three lists
                 const uint64_t want = (uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)incl, 63) |
                                       (uint64_t)__popcll(BA) << 16 | (uint64_t)__popcll(BB) << 32 |
-                                      (uint64_t)__popcll(BC) << 48;
+                                      (uint64_t)__popcll(B5) << 48;
                 uint64_t got = 0u;
                 if (lane == 0u) got = atomicAdd(&s_alloc, want);
                 const uint32_t glo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)got);
@@ -543,14 +553,14 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
                 const uint32_t start = (glo & 0xFFFFu) + incl - ext;
                 const uint32_t pa = below_count(BA, glo >> 16);
                 const uint32_t pb = below_count(BB, ghi & 0xFFFFu);
-                const uint32_t pc = below_count(BC, ghi >> 16);
+                const uint32_t p5 = below_count(B5, ghi >> 16);
                 if (act && start + ext <= CAP) {
                     if (MODE == kSparseWrite) s_start[j] = (uint16_t)start;
                     else s_cnt[j] = m | start << 9;
                     const uint32_t item = j | start << 12;
                     if (ca) s_lista[pa] = item;
                     if (cb) s_listb[pb] = item;
-                    if (cc) s_listb[CCAP - 1u - pc] = item;
+                    if (c5) s_listb[CCAP - 1u - p5] = item;
                 }
             }
         }
@@ -558,7 +568,7 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
         const uint64_t al = s_alloc;
         const bool defer = over || (uint32_t)(al & 0xFFFFu) > CAP;
         const uint32_t NE = s_ne, NA = (uint32_t)(al >> 16) & 0xFFFFu;
-        const uint32_t NB = (uint32_t)(al >> 32) & 0xFFFFu, NC = (uint32_t)(al >> 48);
+        const uint32_t NB = (uint32_t)(al >> 32) & 0xFFFFu, N5 = (uint32_t)(al >> 48);
 
         if (!defer) {
             if (CNTS && tid == 0) a.tile_cnt[tile] = NE;
@@ -623,11 +633,11 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
                 vv[x] = sw ? vv[y] : vv[x];
                 vv[y] = sw ? tv : vv[y];
             };
-            // Waves 4q + s run on SIMD s (round-robin placement).  The walks of
-            // three or four ranks fill the waves of SIMDs 0-2 first and those
-            // of more than eight ranks take them from the other end, so that
-            // the top wave, which walks the indices with five to eight ranks,
-            // shares its SIMD with little else.
+            // Waves 4q + s run on SIMD s (round-robin placement).  The walk of
+            // three or four ranks fills the waves of SIMDs 0-2 from the first,
+            // the row walk takes waves from the other end (those of SIMDs 0-2
+            // from the last, then SIMD 3's), so that the two spread over the
+            // four SIMDs.
             constexpr uint32_t G3 = (NW / 4) * 3;
             static_assert(NW % 4 == 0, "four SIMDs");
             const uint32_t wslot = (wv & 3u) != 3u ? (wv >> 2) * 3u + (wv & 3u) : G3 + (wv >> 2);
@@ -663,142 +673,122 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
                     atomicAdd(&s_E[c2 * PMAX + rk[2]], 1u);
                     atomicAdd(&s_E[mm == 4u ? c3 * PMAX + rk[3] : EW + lane], 1u);
                 }
-                if (VALS) {
-                    float sum;
-                    const float t012 = c1 < c2 ? (vv[0] + vv[1]) + vv[2] : vv[0] + (vv[1] + vv[2]);
-                    if (mm == 3u) sum = t012;
-                    else if (c2 > c1 && c2 > c3) sum = (vv[0] + vv[1]) + (vv[2] + vv[3]);
-                    else if (c1 > c3) sum = vv[0] + (c2 < c3 ? (vv[1] + vv[2]) + vv[3] : vv[1] + (vv[2] + vv[3]));
-                    else sum = t012 + vv[3];
-                    emit(jj, sum);
-                }
+                if (VALS) emit(jj, mm == 3u ? tree3(vv[0], vv[1], vv[2], c1, c2)
+                                            : tree4(vv[0], vv[1], vv[2], vv[3], c1, c2, c3));
             }
-            // Walk: indices with five to eight ranks, one per thread (from the
-            // top thread down, so that they share few waves with the above):
-            // a sorting network (ranks past m are distinct sentinels above
-            // every rank), then a stack keyed by separator level.
-            for (uint32_t i = NT - 1u - tid; i < NB; i += NT) {
-                const uint32_t item = s_listb[i];
+            // Walk: indices with five ranks, one per thread (from the top
+            // thread down, so that they share few waves with the above): a
+            // sorting network, then the root splits at the largest separator
+            // into parts of at most four, summed by the forms above.
+            for (uint32_t i = NT - 1u - tid; i < N5; i += NT) {
+                const uint32_t item = s_listb[CCAP - 1u - i];
                 const uint32_t jj = item & 0xFFFu, st0 = item >> 12;
-                const uint32_t mm = s_cnt[jj] & 0x1FFu;
-                uint32_t rk[8];
-                float vv[8];
+                uint32_t rk[5];
+                float vv[5];
                 rk[0] = s_r0[jj];
                 vv[0] = VALS ? s_out[jj] : 0.0f;
 #pragma unroll
-                for (int e = 1; e < 8; ++e) {
-                    const uint32_t rr = s_sr[st0 + e - 1];
+                for (int e = 1; e < 5; ++e) {
+                    rk[e] = s_sr[st0 + e - 1];
                     vv[e] = VALS ? s_sv[st0 + e - 1] : 0.0f;
-                    rk[e] = (uint32_t)e < mm ? rr : 0x100u + (uint32_t)e;
                 }
-                cswap_rv(rk, vv, 0, 2); cswap_rv(rk, vv, 1, 3); cswap_rv(rk, vv, 4, 6); cswap_rv(rk, vv, 5, 7);
-                cswap_rv(rk, vv, 0, 4); cswap_rv(rk, vv, 1, 5); cswap_rv(rk, vv, 2, 6); cswap_rv(rk, vv, 3, 7);
-                cswap_rv(rk, vv, 0, 1); cswap_rv(rk, vv, 2, 3); cswap_rv(rk, vv, 4, 5); cswap_rv(rk, vv, 6, 7);
-                cswap_rv(rk, vv, 2, 4); cswap_rv(rk, vv, 3, 5); cswap_rv(rk, vv, 1, 4); cswap_rv(rk, vv, 3, 6);
-                cswap_rv(rk, vv, 1, 2); cswap_rv(rk, vv, 3, 4); cswap_rv(rk, vv, 5, 6);
-                float slot[LMAX];
-#pragma unroll
-                for (int l = 0; l < LMAX; ++l) slot[l] = 0.0f;
-                float cur = vv[0];
-                uint32_t pend = 0u;
-#pragma unroll
-                for (int e = 1; e < 8; ++e) {
-                    if ((uint32_t)e < mm) {
-                        const uint32_t sep = sep_level(rk[e - 1], rk[e]);
-                        if (CNTS) atomicAdd(&s_E[sep * PMAX + rk[e]], 1u);
-                        if (VALS) {
-#pragma unroll
-                            for (int l = 0; l < LMAX; ++l)
-                                if ((uint32_t)l < sep && ((pend >> l) & 1u)) cur = slot[l] + cur;
-                            pend = (pend & ~((1u << sep) - 1u)) | (1u << sep);
-#pragma unroll
-                            for (int l = 0; l < LMAX; ++l)
-                                if ((uint32_t)l == sep) slot[l] = cur;
-                            cur = vv[e];
-                        }
-                    }
+                cswap_rv(rk, vv, 0, 3); cswap_rv(rk, vv, 1, 4); cswap_rv(rk, vv, 0, 2);
+                cswap_rv(rk, vv, 1, 3); cswap_rv(rk, vv, 0, 1); cswap_rv(rk, vv, 2, 4);
+                cswap_rv(rk, vv, 1, 2); cswap_rv(rk, vv, 3, 4); cswap_rv(rk, vv, 2, 3);
+                const uint32_t c1 = sep_level(rk[0], rk[1]), c2 = sep_level(rk[1], rk[2]);
+                const uint32_t c3 = sep_level(rk[2], rk[3]), c4 = sep_level(rk[3], rk[4]);
+                if (CNTS) {
+                    atomicAdd(&s_E[c1 * PMAX + rk[1]], 1u);
+                    atomicAdd(&s_E[c2 * PMAX + rk[2]], 1u);
+                    atomicAdd(&s_E[c3 * PMAX + rk[3]], 1u);
+                    atomicAdd(&s_E[c4 * PMAX + rk[4]], 1u);
                 }
                 if (VALS) {
-#pragma unroll
-                    for (int l = 0; l < LMAX; ++l)
-                        if ((pend >> l) & 1u) cur = slot[l] + cur;
-                    emit(jj, cur);
+                    const float t012 = tree3(vv[0], vv[1], vv[2], c1, c2);
+                    const float t234 = tree3(vv[2], vv[3], vv[4], c3, c4);
+                    const float t0123 = tree4(vv[0], vv[1], vv[2], vv[3], c1, c2, c3);
+                    const float t1234 = tree4(vv[1], vv[2], vv[3], vv[4], c2, c3, c4);
+                    const uint32_t top = max(max(c1, c2), max(c3, c4));
+                    float sum;
+                    if (c1 == top) sum = vv[0] + t1234;
+                    else if (c2 == top) sum = (vv[0] + vv[1]) + t234;
+                    else if (c3 == top) sum = t012 + (vv[3] + vv[4]);
+                    else sum = t0123 + vv[4];
+                    emit(jj, sum);
                 }
             }
-            // Walk: indices with more than eight ranks, one per wave.  The values are laid out by rank (lane l holds
-            // ranks l*K .. l*K+K-1) and the tree is evaluated level by level:
-            // a node is the sum of its two children when both hold a value,
-            // else the one that does -- the recursive doubling of the ranks
-            // present.
-            float* const wval = s_wv + wv * PMAX;
-            uint32_t* const wpre = s_wp + wv * PW;
-            for (uint32_t i = wslot < G3 ? G3 - 1u - wslot : wslot; i < NC; i += NW) {
-                const uint32_t item = s_listb[CCAP - 1u - i];
-                const uint32_t jj = item & 0xFFFu, st0 = item >> 12;
-                const uint32_t mm = s_cnt[jj] & 0x1FFu;
-                if (lane < (uint32_t)PW) wpre[lane] = 0u;
-                __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
-                for (uint32_t e = lane; e < mm; e += 64u) {
-                    const uint32_t r = e == 0u ? (uint32_t)s_r0[jj] : (uint32_t)s_sr[st0 + e - 1u];
-                    if (VALS) wval[r] = e == 0u ? s_out[jj] : s_sv[st0 + e - 1u];
-                    atomicOr(&wpre[r >> 5], 1u << (r & 31u));
-                }
-                __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
-                uint32_t pw[PW];
-#pragma unroll
-                for (int q = 0; q < PW; ++q) pw[q] = wpre[q];
-                constexpr int K = PMAX > 64 ? PMAX / 64 : 1;
-                float lv[K];
-                bool lp[K];
-#pragma unroll
-                for (int q = 0; q < K; ++q) {
-                    const uint32_t r = lane * K + (uint32_t)q;
-                    uint32_t word = 0u;
-#pragma unroll
-                    for (int w2 = 0; w2 < PW; ++w2) word = (uint32_t)w2 == (r >> 5) ? pw[w2] : word;
-                    lp[q] = r < (uint32_t)PMAX && ((word >> (r & 31u)) & 1u);
-                    lv[q] = VALS && lp[q] ? wval[r] : 0.0f;
-                    if (CNTS && lp[q]) {
-                        // predecessor: the highest present rank below r
-                        int pred = -1;
-#pragma unroll
-                        for (int w2 = 0; w2 < PW; ++w2) {
-                            const uint32_t mk = (uint32_t)w2 < (r >> 5) ? pw[w2]
-                                              : ((uint32_t)w2 == (r >> 5) ? pw[w2] & ((1u << (r & 31u)) - 1u) : 0u);
-                            if (mk) pred = w2 * 32 + 31 - (int)__clz(mk);
-                        }
-                        if (pred >= 0) atomicAdd(&s_E[sep_level((uint32_t)pred, r) * PMAX + r], 1u);
+            // Walk: indices with six or more ranks, one per row of 16 lanes
+            // (ROWS per wave and pass).  Lane l of a row holds ranks l*K ..
+            // l*K+K-1 of its index: the values are scattered by rank to the
+            // row's region and the tree is evaluated level by level, within
+            // the lane and then across the row (DPP) -- a node is the sum of its
+            // two children when both hold a value, else the one that does: the
+            // recursive doubling of the ranks present.  A present rank's
+            // predecessor (for the node sizes) is the previous present one in
+            // its lane, else the highest present one in the row's lower lanes.
+            {
+                const uint32_t row = min(lane >> 4, RROWS - 1u), l16 = lane & 15u;
+                float* const rval = s_wv + (wv * RROWS + row) * PMAX;
+                uint32_t* const rpre = s_wp + (wv * RROWS + row) * PW;
+                const uint32_t base = l16 * RK;
+                for (uint32_t b0 = (wslot < G3 ? G3 - 1u - wslot : wslot) * RROWS; b0 < NB; b0 += RROWS * NW) {
+                    const uint32_t i = b0 + row;
+                    const bool act = (lane >> 4) < RROWS && i < NB;
+                    const uint32_t item = act ? s_listb[i] : 0u;
+                    const uint32_t jj = item & 0xFFFu, st0 = item >> 12;
+                    const uint32_t mm = act ? s_cnt[jj] & 0x1FFu : 0u;
+                    if ((lane >> 4) < RROWS && l16 < (uint32_t)PW) rpre[l16] = 0u;
+                    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+                    for (uint32_t e = l16; e < mm; e += 16u) {
+                        const uint32_t r = e == 0u ? (uint32_t)s_r0[jj] : (uint32_t)s_sr[st0 + e - 1u];
+                        if (VALS) rval[r] = e == 0u ? s_out[jj] : s_sv[st0 + e - 1u];
+                        atomicOr(&rpre[r >> 5], 1u << (r & 31u));
                     }
-                }
-                if (VALS) {
-                    // levels inside the lane, then across lanes
+                    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+                    const uint32_t bits = act ? (rpre[base >> 5] >> (base & 31u)) & (RK == 32 ? ~0u : (1u << RK) - 1u) : 0u;
+                    if (CNTS) {
+                        // (rank + 1) of the highest present rank in lower lanes of the row
+                        uint32_t top = bits ? base + 32u - (uint32_t)__clz(bits) : 0u;
+                        top = max(top, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)top, 0x111, 0xF, 0xF, true));
+                        top = max(top, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)top, 0x112, 0xF, 0xF, true));
+                        top = max(top, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)top, 0x114, 0xF, 0xF, true));
+                        top = max(top, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)top, 0x118, 0xF, 0xF, true));
+                        uint32_t prev = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)top, 0x111, 0xF, 0xF, true);
 #pragma unroll
-                    for (int h = 1; h < K; h <<= 1) {
-#pragma unroll
-                        for (int q = 0; q < K; q += 2 * h) {
-                            lv[q] = lp[q] && lp[q + h] ? lv[q] + lv[q + h] : (lp[q] ? lv[q] : lv[q + h]);
-                            lp[q] = lp[q] || lp[q + h];
+                        for (uint32_t q = 0; q < RK; ++q) {
+                            if ((bits >> q) & 1u) {
+                                const uint32_t r = base + q;
+                                if (prev) atomicAdd(&s_E[sep_level(prev - 1u, r) * PMAX + r], 1u);
+                                prev = r + 1u;
+                            }
                         }
                     }
-                    float v = lv[0];
-                    uint32_t pr = lp[0] ? 1u : 0u;
-                    tree_level<1>(v, pr, lane);
-                    tree_level<2>(v, pr, lane);
-                    tree_level<4>(v, pr, lane);
-                    tree_level<8>(v, pr, lane);
-                    // the four row results (lanes 0, 16, 32, 48)
-                    float rv[4];
-                    uint32_t rp[4];
+                    if (VALS) {
+                        float lv[RK];
+                        bool lp[RK];
 #pragma unroll
-                    for (int q = 0; q < 4; ++q) {
-                        rv[q] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16 * q));
-                        rp[q] = (uint32_t)__builtin_amdgcn_readlane((int)pr, 16 * q);
+                        for (uint32_t q = 0; q < RK; ++q) {
+                            lp[q] = (bits >> q) & 1u;
+                            lv[q] = lp[q] ? rval[base + q] : 0.0f;
+                        }
+#pragma unroll
+                        for (uint32_t h = 1; h < RK; h <<= 1) {
+#pragma unroll
+                            for (uint32_t q = 0; q < RK; q += 2 * h) {
+                                lv[q] = tree_join(lv[q], lp[q], lv[q + h], lp[q + h]);
+                                lp[q] = lp[q] || lp[q + h];
+                            }
+                        }
+                        float v = lv[0];
+                        uint32_t pr = lp[0] ? 1u : 0u;
+                        tree_level<1>(v, pr, lane);
+                        tree_level<2>(v, pr, lane);
+                        tree_level<4>(v, pr, lane);
+                        tree_level<8>(v, pr, lane);
+                        if (act && l16 == 0u) emit(jj, v);
                     }
-                    const float lo = tree_join(rv[0], rp[0], rv[1], rp[1]);
-                    const float hi = tree_join(rv[2], rp[2], rv[3], rp[3]);
-                    if (lane == 0u) emit(jj, tree_join(lo, rp[0] | rp[1], hi, rp[2] | rp[3]));
+                    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
                 }
-                __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
             }
             __syncthreads();
 
