@@ -43,6 +43,19 @@ void timer_end(int slot, hipStream_t s);
 int timer_enable(int on);
 int timer_read(int slot, float* ms);
 
+// Inclusive prefix sum over the 64 lanes of a wave: shifts within rows of
+// 16 lanes, then the row broadcasts.
+__device__ __forceinline__ uint32_t wave_scan(uint32_t v)
+{
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x111, 0xF, 0xF, true);  // row_shr:1
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x112, 0xF, 0xF, true);  // row_shr:2
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x114, 0xF, 0xF, true);  // row_shr:4
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x118, 0xF, 0xF, true);  // row_shr:8
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x142, 0xA, 0xF, false); // row_bcast:15
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x143, 0xC, 0xF, false); // row_bcast:31
+    return v;
+}
+
 // Round x up to a multiple of a (a power of two).
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) & ~(a - 1); }
 

@@ -148,19 +148,6 @@ __device__ void flush_counts(uint32_t* E, const Args& a)
     }
 }
 
-// Inclusive prefix sum over the 64 lanes of a wave: shifts within rows of
-// 16 lanes, then the row broadcasts.
-__device__ __forceinline__ uint32_t wave_scan(uint32_t v)
-{
-    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x111, 0xF, 0xF, true);  // row_shr:1
-    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x112, 0xF, 0xF, true);  // row_shr:2
-    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x114, 0xF, 0xF, true);  // row_shr:4
-    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x118, 0xF, 0xF, true);  // row_shr:8
-    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x142, 0xA, 0xF, false); // row_bcast:15
-    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x143, 0xC, 0xF, false); // row_bcast:31
-    return v;
-}
-
 // Masks of the active lanes where a == b, a < b (unsigned): one compare each.
 __device__ __forceinline__ uint64_t lanes_eq(uint32_t a, uint32_t b)
 {

@@ -1,12 +1,17 @@
 // Top-k sparsification by magnitude on gfx950 (§2.2 "Structured
 // Sparsification"; Alg. 1: TopK and the error update eps = acc - TopK(acc)).
 //
-// Exact radix select on the 31-bit magnitude key (IEEE bits, sign cleared):
-// three histogram passes (11 + 10 + 10 bits) narrow the k-th largest key K*
-// and how many entries equal to K* are still needed; a count pass and a scan
-// over 4096-element wave units then give every unit its output offset, and a
-// write pass compacts the selection in index order (equal keys: lowest index
-// first) with wave ballots, optionally zeroing the residual.
+// Exact radix select on the 31-bit magnitude key (IEEE bits, sign cleared),
+// three passes over the data: a histogram of the top 11 key bits finds the
+// bin holding the k-th largest key; a filter pass counts, per 4096-element
+// wave unit, the keys above that bin and gathers the keys inside it; the
+// k-th largest key K* and how many entries equal to it are still needed
+// follow from the gathered keys alone (two more 10-bit histograms), which
+// also complete the unit counts.  A scan over the units gives every unit its
+// output offset, and a write pass compacts the selection in index order
+// (equal keys: lowest index first) with wave ballots, optionally zeroing the
+// residual.  A row with a unit holding more than kSlots keys of the boundary
+// bin takes two more histogram passes and a count pass over its data instead.
 #include "internal.h"
 
 #include <algorithm>
@@ -15,15 +20,52 @@ namespace sparcml {
 namespace {
 
 constexpr uint32_t kUnit = 4096;  // elements per wave unit (64 iterations of 64 lanes)
+constexpr uint32_t kSlots = 16;   // gathered keys per unit
 constexpr int kHistBlocksPerRank = 64;
+
+__device__ __forceinline__ uint32_t mag_key(float v) { return __float_as_uint(v) & 0x7FFFFFFFu; }
 
 struct RankState {
     uint32_t prefix;  // key bits fixed so far
-    uint32_t pad;
+    uint32_t full;    // 0: K* from the gathered keys; 1: refined by passes over the data
     uint64_t krem;    // entries still to take from keys matching the prefix
 };
 
-__device__ __forceinline__ uint32_t mag_key(float v) { return __float_as_uint(v) & 0x7FFFFFFFu; }
+// Keys of row r from element lo to hi (lo a multiple of 4), in float4 loads
+// where the row is 16-byte aligned; f(element, key) in any order.
+template <typename F>
+__device__ __forceinline__ void for_keys(const float* row, uint64_t lo, uint64_t hi, uint32_t t,
+                                         uint32_t nt, F&& f)
+{
+    if ((reinterpret_cast<uintptr_t>(row) & 15u) == 0u) {
+        // batches of four float4 loads per thread, all issued before use
+        const uint64_t step = 16ull * nt, hb = lo + ((hi - lo) / step) * step;
+        for (uint64_t e = lo + 4ull * t; e < hb; e += step) {
+            float4 v[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) v[q] = *reinterpret_cast<const float4*>(row + e + 4ull * nt * q);
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const uint64_t b = e + 4ull * nt * q;
+                f(b, mag_key(v[q].x));
+                f(b + 1, mag_key(v[q].y));
+                f(b + 2, mag_key(v[q].z));
+                f(b + 3, mag_key(v[q].w));
+            }
+        }
+        const uint64_t hv = hb + ((hi - hb) & ~3ull);
+        for (uint64_t e = hb + 4ull * t; e < hv; e += 4ull * nt) {
+            const float4 v = *reinterpret_cast<const float4*>(row + e);
+            f(e, mag_key(v.x));
+            f(e + 1, mag_key(v.y));
+            f(e + 2, mag_key(v.z));
+            f(e + 3, mag_key(v.w));
+        }
+        for (uint64_t e = hv + t; e < hi; e += nt) f(e, mag_key(row[e]));
+    } else {
+        for (uint64_t e = lo + t; e < hi; e += nt) f(e, mag_key(row[e]));
+    }
+}
 
 // PASS 0: bins = key >> 20 (2048); PASS 1: (key >> 10) & 1023 among keys
 // whose top 11 bits match; PASS 2: key & 1023 among keys whose top 21 bits
@@ -37,16 +79,16 @@ __global__ void __launch_bounds__(256) k_hist(const float* x, uint64_t N, const 
     constexpr int PSHIFT = PASS == 1 ? 20 : 10;
     __shared__ uint32_t s_h[NB];
     const uint32_t r = blockIdx.y;
+    if (PASS != 0 && st[r].full == 0u) return;  // row settled by its gathered keys
     for (uint32_t i = threadIdx.x; i < NB; i += 256) s_h[i] = 0;
     __syncthreads();
     const uint32_t prefix = PASS == 0 ? 0u : st[r].prefix;
     const float* row = x + (uint64_t)r * N;
-    const uint64_t per = (N + gridDim.x - 1) / gridDim.x;
-    const uint64_t lo = (uint64_t)blockIdx.x * per, hi = min(lo + per, N);
-    for (uint64_t e = lo + threadIdx.x; e < hi; e += 256) {
-        const uint32_t key = mag_key(row[e]);
+    const uint64_t per = ((N + gridDim.x - 1) / gridDim.x + 3) & ~3ull;
+    const uint64_t lo = min((uint64_t)blockIdx.x * per, N), hi = min(lo + per, N);
+    for_keys(row, lo, hi, threadIdx.x, 256u, [&](uint64_t, uint32_t key) {
         if (PASS == 0 || (key >> PSHIFT) == prefix) atomicAdd(&s_h[(key >> SHIFT) & (NB - 1)], 1u);
-    }
+    });
     __syncthreads();
     for (uint32_t i = threadIdx.x; i < NB; i += 256)
         if (s_h[i]) atomicAdd(&hist[(uint64_t)r * 2048 + i], s_h[i]);
@@ -61,6 +103,7 @@ __global__ void __launch_bounds__(256) k_select(RankState* st, uint32_t* hist)
     constexpr int BITS = PASS == 0 ? 11 : 10;
     __shared__ uint64_t s_w[4];
     const uint32_t r = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    if (PASS != 0 && st[r].full == 0u) return;
     // read the state before the barrier below; one thread rewrites it after
     const uint64_t krem = st[r].krem;
     const uint32_t prefix = st[r].prefix;
@@ -96,40 +139,16 @@ __global__ void __launch_bounds__(256) k_select(RankState* st, uint32_t* hist)
     for (uint32_t i = 0; i < PER; ++i) h[lo + i] = 0;
 }
 
-__global__ void k_init(RankState* st, uint32_t P, uint64_t k, uint32_t* hist)
+__global__ void k_init(RankState* st, uint32_t P, uint64_t k, uint32_t* hist, uint32_t* overflow)
 {
     const uint64_t gid = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (gid < P) {
         st[gid].prefix = 0;
+        st[gid].full = 0;
         st[gid].krem = k;
+        overflow[gid] = 0;
     }
     if (gid < (uint64_t)P * 2048) hist[gid] = 0;
-}
-
-// Per wave unit: entries with key > K* and key == K*.
-__global__ void __launch_bounds__(256) k_count(const float* x, uint64_t N, uint32_t U,
-                                               const RankState* st, uint32_t* cgt, uint32_t* ceq)
-{
-    const uint32_t r = blockIdx.y, lane = threadIdx.x & 63;
-    const uint32_t u = blockIdx.x * 4 + (threadIdx.x >> 6);
-    if (u >= U) return;
-    const uint32_t K = st[r].prefix;
-    const float* row = x + (uint64_t)r * N;
-    const uint64_t lo = (uint64_t)u * kUnit, hi = min(lo + kUnit, N);
-    uint32_t gt = 0, eq = 0;
-    for (uint64_t e = lo + lane; e < hi; e += 64) {
-        const uint32_t key = mag_key(row[e]);
-        gt += key > K;
-        eq += key == K;
-    }
-    for (int o = 32; o > 0; o >>= 1) {
-        gt += __shfl_xor(gt, o);
-        eq += __shfl_xor(eq, o);
-    }
-    if (lane == 0) {
-        cgt[(uint64_t)r * U + u] = gt;
-        ceq[(uint64_t)r * U + u] = eq;
-    }
 }
 
 __device__ __forceinline__ uint32_t block_excl_scan(uint32_t v, uint32_t* s_w, uint32_t* total)
@@ -151,6 +170,162 @@ __device__ __forceinline__ uint32_t block_excl_scan(uint32_t v, uint32_t* s_w, u
     *total = t;
     return ex;
 }
+
+// Per wave unit: keys above the boundary bin (top 11 bits) counted, keys in
+// it gathered as {element, key} into the unit's kSlots slots (a unit with
+// more flags its row for the passes over the data); the unit's tie count
+// starts at zero.
+__global__ void __launch_bounds__(256) k_filter(const float* x, uint64_t N, uint32_t U, const RankState* st,
+                                                uint32_t* cgt, uint32_t* ceq, uint2* cand, uint32_t* ccnt,
+                                                uint32_t* overflow)
+{
+    const uint32_t r = blockIdx.y, lane = threadIdx.x & 63;
+    const uint32_t u = blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (u >= U) return;
+    const uint32_t bin = st[r].prefix;
+    const float* row = x + (uint64_t)r * N;
+    const uint64_t lo = (uint64_t)u * kUnit, hi = min(lo + kUnit, N);
+    uint2* cu = cand + ((uint64_t)r * U + u) * kSlots;
+    uint32_t gt = 0, nc = 0;
+    auto gather = [&](bool in, uint64_t e, uint32_t key) {
+        const uint64_t m = __ballot(in);
+        if (m) {
+            const uint32_t at = nc + (uint32_t)__popcll(m & ((1ull << lane) - 1ull));
+            if (in && at < kSlots) cu[at] = make_uint2((uint32_t)e, key);
+            nc += (uint32_t)__popcll(m);
+        }
+    };
+    if ((reinterpret_cast<uintptr_t>(row) & 15u) == 0u && hi - lo == kUnit) {
+        // the unit's 16 float4 per lane, all requested before use
+        float4 vs[kUnit / 256];
+#pragma unroll
+        for (uint32_t q = 0; q < kUnit / 256; ++q)
+            vs[q] = *reinterpret_cast<const float4*>(row + lo + 256u * q + 4u * lane);
+#pragma unroll
+        for (uint32_t q = 0; q < kUnit / 256; ++q) {
+            const uint64_t e = lo + 256u * q + 4u * lane;
+            const float4 v = vs[q];
+            const uint32_t k0 = mag_key(v.x), k1 = mag_key(v.y), k2 = mag_key(v.z), k3 = mag_key(v.w);
+            gt += ((k0 >> 20) > bin) + ((k1 >> 20) > bin) + ((k2 >> 20) > bin) + ((k3 >> 20) > bin);
+            gather((k0 >> 20) == bin, e, k0);
+            gather((k1 >> 20) == bin, e + 1, k1);
+            gather((k2 >> 20) == bin, e + 2, k2);
+            gather((k3 >> 20) == bin, e + 3, k3);
+        }
+    } else {
+        for (uint64_t e0 = lo; e0 < hi; e0 += 64) {
+            const uint64_t e = e0 + lane;
+            const uint32_t key = e < hi ? mag_key(row[e]) : 0u;
+            gt += e < hi && (key >> 20) > bin;
+            gather(e < hi && (key >> 20) == bin, e, key);
+        }
+    }
+    for (int o = 32; o > 0; o >>= 1) gt += __shfl_xor(gt, o);
+    if (lane == 0) {
+        cgt[(uint64_t)r * U + u] = gt;
+        ceq[(uint64_t)r * U + u] = 0;
+        ccnt[(uint64_t)r * U + u] = nc;
+        if (nc > kSlots) atomicOr(&overflow[r], 1u);
+    }
+}
+
+// Bin (of NB, ordered from the top) holding the krem-th largest key of a
+// histogram held one bin per thread (thread t: bin NB-1-t); returns the bin
+// and, through *rem, krem less the keys in the bins above it.
+__device__ uint32_t block_find(uint32_t cnt, uint64_t krem, uint32_t NB, uint64_t* rem, uint32_t* s_w,
+                               uint32_t* s_res)
+{
+    uint32_t total;
+    const uint32_t above = block_excl_scan(cnt, s_w, &total);
+    if (above < krem && above + cnt >= krem) {
+        s_res[0] = NB - 1u - threadIdx.x;
+        s_res[1] = (uint32_t)(krem - above);
+    }
+    __syncthreads();
+    *rem = s_res[1];
+    return s_res[0];
+}
+
+// K* and the ties still needed from the gathered keys of row r (its
+// boundary bin), then the unit counts of keys above K* and equal to it.
+// Thread t takes units t, t + 1024, ...
+__global__ void __launch_bounds__(1024) k_cand_select(uint32_t U, RankState* st, const uint2* cand,
+                                                      const uint32_t* ccnt, const uint32_t* overflow,
+                                                      uint32_t* cgt, uint32_t* ceq)
+{
+    __shared__ uint32_t s_h[1024];
+    __shared__ uint32_t s_w[16];
+    __shared__ uint32_t s_res[2];
+    const uint32_t r = blockIdx.x, t = threadIdx.x;
+    if (overflow[r]) {  // too many to gather: refine by passes over the data
+        if (t == 0) st[r].full = 1u;
+        return;
+    }
+    const uint2* cr = cand + (uint64_t)r * U * kSlots;
+    const uint32_t* cn = ccnt + (uint64_t)r * U;
+    const uint32_t bin = st[r].prefix;
+    uint64_t krem = st[r].krem;
+    // bits 19..10, then bits 9..0 among the keys matching so far
+    s_h[t] = 0;
+    __syncthreads();
+    for (uint32_t u = t; u < U; u += 1024)
+        for (uint32_t i = 0; i < cn[u]; ++i) atomicAdd(&s_h[(cr[u * kSlots + i].y >> 10) & 1023u], 1u);
+    __syncthreads();
+    const uint32_t b2 = block_find(s_h[1023u - t], krem, 1024u, &krem, s_w, s_res);
+    const uint32_t p21 = bin << 10 | b2;
+    __syncthreads();
+    s_h[t] = 0;
+    __syncthreads();
+    for (uint32_t u = t; u < U; u += 1024)
+        for (uint32_t i = 0; i < cn[u]; ++i) {
+            const uint32_t key = cr[u * kSlots + i].y;
+            if ((key >> 10) == p21) atomicAdd(&s_h[key & 1023u], 1u);
+        }
+    __syncthreads();
+    const uint32_t b3 = block_find(s_h[1023u - t], krem, 1024u, &krem, s_w, s_res);
+    const uint32_t K = p21 << 10 | b3;
+    for (uint32_t u = t; u < U; u += 1024) {
+        uint32_t g = 0, q = 0;
+        for (uint32_t i = 0; i < cn[u]; ++i) {
+            const uint32_t key = cr[u * kSlots + i].y;
+            g += key > K;
+            q += key == K;
+        }
+        cgt[(uint64_t)r * U + u] += g;
+        ceq[(uint64_t)r * U + u] = q;
+    }
+    if (t == 0) {
+        st[r].prefix = K;
+        st[r].krem = krem;
+    }
+}
+
+// Per wave unit: entries with key > K* and key == K*.
+__global__ void __launch_bounds__(256) k_count(const float* x, uint64_t N, uint32_t U,
+                                               const RankState* st, uint32_t* cgt, uint32_t* ceq)
+{
+    const uint32_t r = blockIdx.y, lane = threadIdx.x & 63;
+    const uint32_t u = blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (u >= U || st[r].full == 0u) return;
+    const uint32_t K = st[r].prefix;
+    const float* row = x + (uint64_t)r * N;
+    const uint64_t lo = (uint64_t)u * kUnit, hi = min(lo + kUnit, N);
+    uint32_t gt = 0, eq = 0;
+    for (uint64_t e = lo + lane; e < hi; e += 64) {
+        const uint32_t key = mag_key(row[e]);
+        gt += key > K;
+        eq += key == K;
+    }
+    for (int o = 32; o > 0; o >>= 1) {
+        gt += __shfl_xor(gt, o);
+        eq += __shfl_xor(eq, o);
+    }
+    if (lane == 0) {
+        cgt[(uint64_t)r * U + u] = gt;
+        ceq[(uint64_t)r * U + u] = eq;
+    }
+}
+
 
 // Unit offsets: equal keys are taken in index order until `need` of them.
 __global__ void __launch_bounds__(1024) k_unit_scan(uint32_t U, const RankState* st, const uint32_t* cgt,
@@ -205,6 +380,64 @@ __global__ void __launch_bounds__(256) k_write(const float* x, uint64_t N, uint6
     uint32_t out_run = bout[(uint64_t)r * U + u];
     const uint64_t lo = (uint64_t)u * kUnit, hi = min(lo + kUnit, N);
     const uint64_t lt = (1ull << lane) - 1ull;
+    const bool res_vec = res == nullptr || inplace || (reinterpret_cast<uintptr_t>(res) & 15u) == 0u;
+    if ((reinterpret_cast<uintptr_t>(row) & 15u) == 0u && res_vec && hi - lo == kUnit) {
+        // The unit's 16 float4 per lane, all requested before use; per 256
+        // elements (lane i: elements 4i..4i+3) ties and selections are placed
+        // in index order by wave scans of the per-lane counts.
+        float4 vs[kUnit / 256];
+#pragma unroll
+        for (uint32_t q = 0; q < kUnit / 256; ++q)
+            vs[q] = *reinterpret_cast<const float4*>(row + lo + 256u * q + 4u * lane);
+#pragma unroll
+        for (uint32_t q = 0; q < kUnit / 256; ++q) {
+            const uint64_t e = lo + 256u * q + 4u * lane;
+            const float v4[4] = {vs[q].x, vs[q].y, vs[q].z, vs[q].w};
+            uint32_t neq = 0;
+            bool isq[4], gt[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const uint32_t key = mag_key(v4[i]);
+                isq[i] = key == K;
+                gt[i] = key > K;
+                neq += isq[i] ? 1u : 0u;
+            }
+            const uint32_t eincl = wave_scan(neq);
+            uint64_t eb = eq_run + (eincl - neq);  // ties before this lane's first
+            bool sel[4];
+            uint32_t nsel = 0;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                sel[i] = gt[i] || (isq[i] && eb < need);
+                eb += isq[i] ? 1u : 0u;
+                nsel += sel[i] ? 1u : 0u;
+            }
+            const uint32_t sincl = wave_scan(nsel);
+            uint32_t o = out_run + (sincl - nsel);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                if (sel[i]) {
+                    oi[o] = (uint32_t)(e + i);
+                    ov[o] = v4[i];
+                    ++o;
+                }
+            }
+            if (res) {
+                if (inplace) {
+#pragma unroll
+                    for (int i = 0; i < 4; ++i)
+                        if (sel[i]) res[e + i] = 0.0f;
+                } else {
+                    *reinterpret_cast<float4*>(res + e) =
+                        make_float4(sel[0] ? 0.0f : v4[0], sel[1] ? 0.0f : v4[1], sel[2] ? 0.0f : v4[2],
+                                    sel[3] ? 0.0f : v4[3]);
+                }
+            }
+            eq_run += (uint32_t)__builtin_amdgcn_readlane((int)eincl, 63);
+            out_run += (uint32_t)__builtin_amdgcn_readlane((int)sincl, 63);
+        }
+        return;
+    }
     for (uint64_t e0 = lo; e0 < hi; e0 += 64) {
         const uint64_t e = e0 + lane;
         const bool valid = e < hi;
@@ -234,7 +467,8 @@ __global__ void __launch_bounds__(256) k_write(const float* x, uint64_t N, uint6
 
 struct TLayout {
     RankState* st;
-    uint32_t *hist, *cgt, *ceq, *beq, *bout;
+    uint32_t *hist, *cgt, *ceq, *beq, *bout, *ccnt, *overflow;
+    uint2* cand;
     uint32_t U;
     size_t bytes;
 };
@@ -245,6 +479,9 @@ TLayout tlayout(int P, uint64_t N, void* ws)
     TLayout l{};
     l.U = (uint32_t)((N + kUnit - 1) / kUnit);
     l.st = c.take<RankState>(P);
+    l.overflow = c.take<uint32_t>(P);
+    l.ccnt = c.take<uint32_t>((size_t)P * l.U);
+    l.cand = c.take<uint2>((size_t)P * l.U * kSlots);
     l.hist = c.take<uint32_t>((size_t)P * 2048);
     l.cgt = c.take<uint32_t>((size_t)P * l.U);
     l.ceq = c.take<uint32_t>((size_t)P * l.U);
@@ -269,19 +506,23 @@ hipError_t topk_run(int P, const float* x, uint64_t N, uint64_t k, uint32_t* out
     const TLayout l = tlayout(P, N, ws);
     const uint64_t ninit = (uint64_t)P * 2048;
     hipLaunchKernelGGL(k_init, dim3((uint32_t)((ninit + 255) / 256)), dim3(256), 0, s, l.st,
-                       (uint32_t)P, k, l.hist);
+                       (uint32_t)P, k, l.hist, l.overflow);
     const uint32_t hb = (uint32_t)std::min<uint64_t>(kHistBlocksPerRank, (N + 4095) / 4096);
-    const dim3 hgrid(hb, P);
+    const dim3 hgrid(hb, P), ugrid((l.U + 3) / 4, P);
     timer_begin(kTTopkSelect, s);
     hipLaunchKernelGGL(k_hist<0>, hgrid, dim3(256), 0, s, x, N, l.st, l.hist);
     hipLaunchKernelGGL(k_select<0>, dim3(P), dim3(256), 0, s, l.st, l.hist);
+    hipLaunchKernelGGL(k_filter, ugrid, dim3(256), 0, s, x, N, l.U, l.st, l.cgt, l.ceq, l.cand, l.ccnt,
+                       l.overflow);
+    hipLaunchKernelGGL(k_cand_select, dim3(P), dim3(1024), 0, s, l.U, l.st, l.cand, l.ccnt, l.overflow,
+                       l.cgt, l.ceq);
+    // rows whose boundary bin overflowed the gather buffer (the others return at once)
     hipLaunchKernelGGL(k_hist<1>, hgrid, dim3(256), 0, s, x, N, l.st, l.hist);
     hipLaunchKernelGGL(k_select<1>, dim3(P), dim3(256), 0, s, l.st, l.hist);
     hipLaunchKernelGGL(k_hist<2>, hgrid, dim3(256), 0, s, x, N, l.st, l.hist);
     hipLaunchKernelGGL(k_select<2>, dim3(P), dim3(256), 0, s, l.st, l.hist);
     timer_end(kTTopkSelect, s);
     timer_begin(kTTopkWrite, s);
-    const dim3 ugrid((l.U + 3) / 4, P);
     hipLaunchKernelGGL(k_count, ugrid, dim3(256), 0, s, x, N, l.U, l.st, l.cgt, l.ceq);
     hipLaunchKernelGGL(k_unit_scan, dim3(P), dim3(1024), 0, s, l.U, l.st, l.cgt, l.ceq, l.beq, l.bout);
     hipLaunchKernelGGL(k_write, ugrid, dim3(256), 0, s, x, N, k, l.U, l.st, l.beq, l.bout, out_idx,

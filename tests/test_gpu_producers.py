@@ -73,6 +73,28 @@ def test_topk_all_equal_and_config3_scaled():
     np.testing.assert_array_equal(gr.view(np.uint32), orr.view(np.uint32))
 
 
+def test_topk_boundary_bin_at_gather_capacity():
+    """The k-th largest key's 11-bit bin holding 16 keys (as many as a
+    4096-element unit gathers) in every unit of the first row, and 17 in one
+    unit of the second: the first row is settled by its gathered keys, the
+    second by the extra passes over its data."""
+    rng = np.random.default_rng(31)
+    N, k, unit = 1 << 18, 500, 4096
+    x = np.stack([inputs.laplace(rng, 1e-3, N) for _ in range(2)])
+    for r in range(2):
+        for u in range(N // unit):
+            cnt = 17 if (r == 1 and u == 7) else 16
+            pos = u * unit + rng.choice(unit, size=cnt, replace=False)
+            x[r, pos] = np.float32(1.0) if r == 0 else np.float32(-1.0)
+            x[r, pos[::5]] = np.float32(1.0009765625)  # same bin, a larger key
+    say(f"[topk] gather capacity P=2 N={N} k={k}")
+    oi, ov, orr = oracle.topk(x, k, residual=True)
+    gi, gv, gr = gpu_topk(x, k, "copy")
+    np.testing.assert_array_equal(gi, oi)
+    np.testing.assert_array_equal(gv.view(np.uint32), ov.view(np.uint32))
+    np.testing.assert_array_equal(gr.view(np.uint32), orr.view(np.uint32))
+
+
 def gpu_quantize(vals, bits, seed):
     from paper_1802_08021_amd import sparcml as S
     torch, dev = torch_dev()
