@@ -979,8 +979,8 @@ __global__ void __launch_bounds__(256) k_decide(const StreamDesc* tab, const uin
                                                 uint64_t N, uint64_t thr, uint64_t* node_nnz,
                                                 uint8_t* node_dense, ReduceResult* hdr)
 {
-    // Stream sizes and node union sizes are read by all threads at once; one
-    // thread then applies the rule level by level in LDS; all threads store.
+    // Stream sizes and node union sizes are read by all threads at once, the
+    // rule is applied level by level in LDS, and all threads store.
     __shared__ uint64_t s_n[256];    // per group of the current level
     __shared__ uint8_t s_d[256];
     __shared__ uint32_t s_c[256];    // union sizes, level order
@@ -993,20 +993,27 @@ __global__ void __launch_bounds__(256) k_decide(const StreamDesc* tab, const uin
     }
     if (t + 1 < P) s_c[t] = node_cnt[t];
     __syncthreads();
-    if (t == 0) {
-        uint32_t width = P, node = 0;
-        while (width > 1) {
-            for (uint32_t g = 0; g < width / 2; ++g) {
-                const bool dense = s_d[2 * g] || s_d[2 * g + 1] || (s_n[2 * g] + s_n[2 * g + 1] > thr);
-                const uint64_t nnz = dense ? N : (uint64_t)s_c[node];
-                s_nn[node] = nnz;
-                s_nd[node] = dense ? 1 : 0;
-                s_n[g] = nnz;
-                s_d[g] = dense ? 1 : 0;
-                ++node;
-            }
-            width /= 2;
+    // level by level (children of group g at 2g, 2g+1), one thread per node
+    uint32_t node = 0;
+    for (uint32_t width = P; width > 1; width /= 2) {
+        const uint32_t g = t;
+        bool dense = false;
+        uint64_t nnz = 0;
+        if (g < width / 2) {
+            dense = s_d[2 * g] || s_d[2 * g + 1] || (s_n[2 * g] + s_n[2 * g + 1] > thr);
+            nnz = dense ? N : (uint64_t)s_c[node + g];
+            s_nn[node + g] = nnz;
+            s_nd[node + g] = dense ? 1 : 0;
         }
+        __syncthreads();
+        if (g < width / 2) {
+            s_n[g] = nnz;
+            s_d[g] = dense ? 1 : 0;
+        }
+        __syncthreads();
+        node += width / 2;
+    }
+    if (t == 0) {
         hdr->nnz = s_n[0];
         hdr->dense = s_d[0];
         hdr->pad = 0;
