@@ -239,13 +239,13 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
     constexpr uint32_t RK = PMAX / 16;                  // ranks per lane in the row walk
     static_assert(NW * RROWS * (PMAX + PW) <= 2 * NW * (int)ERGN, "walk buffers alias the entry regions");
 
-    // Per index: arrivals, then m | aux << 9 with aux the staging start of an
-    // index with three or more ranks (sparse output: the output position of
-    // every non-empty index, the staging start apart); the first arrival's
-    // value and rank.
+    // Per index: arrivals | (sum of the arrived ranks) << 16 -- the second
+    // arrival reads the first one's rank there -- then m | aux << 9 with aux
+    // the staging start of an index with three or more ranks (sparse output:
+    // the output position of every non-empty index, the staging start apart);
+    // the first arrival's value (dense: then the result).
     __shared__ __align__(16) uint32_t s_cnt[TMAX + 64];  // 64 dummies for idle lanes
     __shared__ __align__(16) float s_out[VALS ? TMAX + 64 : 4];  // first value; dense: the sum
-    __shared__ uint8_t s_r0[TMAX + 64];
     __shared__ uint16_t s_start[MODE == kSparseWrite ? TMAX : 1];  // staging start (sparse output)
     // Per wave: the tile's entries {j | rank << 12 | code position << 20, raw
     // value word}, then its later arrivals {j | rank << 12 | arrival number
@@ -426,11 +426,12 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
         const uint32_t ne_w = min(nent, ECAP);
         // P1e: arrival numbers of this wave's entries, two per lane and step
         // so that their LDS round trips overlap (idle lanes count at dummy
-        // words).  The first arrival leaves its rank and value at the index;
-        // the later ones are compacted, with their arrival number, to the
-        // front of the wave's region (never past what the wave has read), and
-        // the third lists its index as one with three or more ranks.  The next
-        // step's entries, which this step never overwrites, are read ahead.
+        // words).  The first arrival leaves its value at the index; the later
+        // ones are compacted to the front of the wave's region (never past
+        // what the wave has read) with their arrival number -- the second
+        // with the first one's rank instead, and a flag -- and the third
+        // lists its index as one with three or more ranks.  The next step's
+        // entries, which this step never overwrites, are read ahead.
         // (Lanes read entries other lanes of the wave wrote: the fence orders
         // them for the compiler.)
         __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
@@ -441,8 +442,9 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
             const uint2 en0 = nx0, en1 = nx1;
             const bool ok0 = b + lane < ne_w, ok1 = b + 64u + lane < ne_w;
             const uint32_t j0 = en0.x & 0xFFFu, j1 = en1.x & 0xFFFu;
-            const uint32_t k0 = atomicAdd(&s_cnt[ok0 ? j0 : TMAX + lane], 1u);
-            const uint32_t k1 = atomicAdd(&s_cnt[ok1 ? j1 : TMAX + lane], 1u);
+            const uint32_t w0 = atomicAdd(&s_cnt[ok0 ? j0 : TMAX + lane], 1u + ((en0.x >> 12) << 16));
+            const uint32_t w1 = atomicAdd(&s_cnt[ok1 ? j1 : TMAX + lane], 1u + ((en1.x >> 12) << 16));
+            const uint32_t k0 = w0 & 0xFFFFu, k1 = w1 & 0xFFFFu;
             nx0 = s_ent[EB + min(b + 128u + lane, ECAP - 1u)];
             nx1 = s_ent[EB + min(b + 192u + lane, ECAP - 1u)];
             const bool f0 = ok0 && k0 == 0u, f1 = ok1 && k1 == 0u;
@@ -451,9 +453,7 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
             // Writes are unconditional: a lane with nothing to write aims at
             // a dummy word (past the tile, the region's slack, the list's end).
             const uint32_t fj0 = f0 ? j0 : TMAX + lane, fj1 = f1 ? j1 : TMAX + lane;
-            s_r0[fj0] = (uint8_t)(en0.x >> 12);
             if (VALS) s_out[fj0] = MODE == kDense ? __uint_as_float(en0.y) + 0.0f : __uint_as_float(en0.y);
-            s_r0[fj1] = (uint8_t)(en1.x >> 12);
             if (VALS) s_out[fj1] = MODE == kDense ? __uint_as_float(en1.y) + 0.0f : __uint_as_float(en1.y);
             // lane masks from single comparisons, combined on the scalar unit
             const uint64_t OK0 = lanes_lt(b + lane, ne_w), OK1 = lanes_lt(b + 64u + lane, ne_w);
@@ -469,8 +469,10 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
             ncw += (uint32_t)__popcll(C0);
             const uint32_t q1 = below_count(C1, ncw);
             ncw += (uint32_t)__popcll(C1);
-            s_ent[EB + (l0 ? p0 : ECAP + lane)] = make_uint2(en0.x | k0 << 20, en0.y);
-            s_ent[EB + (l1 ? p1 : ECAP + lane)] = make_uint2(en1.x | k1 << 20, en1.y);
+            // {j | rank << 12 | (k, or for k = 1 the first rank | 1 << 8) << 20, value}
+            const uint32_t t0 = k0 == 1u ? (w0 >> 16) | 0x100u : k0, t1 = k1 == 1u ? (w1 >> 16) | 0x100u : k1;
+            s_ent[EB + (l0 ? p0 : ECAP + lane)] = make_uint2(en0.x | t0 << 20, en0.y);
+            s_ent[EB + (l1 ? p1 : ECAP + lane)] = make_uint2(en1.x | t1 << 20, en1.y);
             s_cands[CB + (c0 && q0 < CWC ? q0 : CWC + lane)] = (uint16_t)j0;
             s_cands[CB + (c1 && q1 < CWC ? q1 : CWC + lane)] = (uint16_t)j1;
         }
@@ -506,7 +508,7 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
                 uint32_t nrun = incl - ne + (uint32_t)__builtin_amdgcn_readlane((int)(xs - wt), (int)wv);
 #pragma unroll
                 for (int c = 0; c < CPT; ++c) {
-                    const uint32_t m = mc[c], j = jb + (uint32_t)c;
+                    const uint32_t m = mc[c] & 0xFFFFu, j = jb + (uint32_t)c;
                     if (m == 1u) {
                         a.out_idx[toff + nrun] = tlo + j;
                         a.out_val[toff + nrun] = s_out[j];
@@ -524,7 +526,7 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
                 const bool act = i < ncw;
                 const uint32_t j = act ? (uint32_t)s_cands[CB + i] : 0u;
                 const uint32_t m = act ? s_cnt[j] & 0x1FFu : 0u;
-                const uint32_t ext = act ? m - 1u : 0u;
+                const uint32_t ext = m;  // all m values, the first staged by the second arrival
                 const uint32_t incl = wave_scan(ext);
                 const bool ca = act && m <= 4u, cb = act && m > 5u, c5 = act && m == 5u;
                 const uint64_t ACT = lanes_lt(i, ncw);
@@ -564,11 +566,14 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
             // P2, per later arrival of this wave: an index with two ranks is
             // finished here -- a single addition is the same in either order --
             // and counts its pair for the node sizes; otherwise the value is
-            // staged at its index's range in arrival order.
+            // staged at its index's range in arrival order, the second arrival
+            // staging the first one's value and rank as well.
             // Two entries per lane and step; every read of a step comes before
             // its writes (no two entries of a step finish the same pair).
-            auto place = [&](uint2 en, uint32_t sc, uint32_t r0, uint32_t st, float first) {
-                const uint32_t jj = en.x & 0xFFFu, r = (en.x >> 12) & 0xFFu, k = en.x >> 20;
+            auto place = [&](uint2 en, uint32_t sc, uint32_t st, float first) {
+                const uint32_t jj = en.x & 0xFFFu, r = (en.x >> 12) & 0xFFu, t = en.x >> 20;
+                const bool second = t >= 0x100u;
+                const uint32_t r0 = t & 0xFFu;  // the first rank (second arrival)
                 if ((sc & 0x1FFu) == 2u) {
                     if (CNTS) atomicAdd(&s_E[sep_level(r0, r) * PMAX + max(r0, r)], 1u);
                     if (VALS) {
@@ -581,9 +586,13 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
                         }
                     }
                 } else {
-                    const uint32_t at = st + k - 1u;
+                    const uint32_t at = st + (second ? 1u : t);
                     s_sr[at] = (uint8_t)r;
                     if (VALS) s_sv[at] = __uint_as_float(en.y);
+                    if (second) {
+                        s_sr[st] = (uint8_t)r0;
+                        if (VALS) s_sv[st] = first;
+                    }
                 }
             };
             for (uint32_t i = lane; i < nlat; i += 128u) {
@@ -592,12 +601,11 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
                 const uint2 e1 = s_ent[EB + (two ? i + 64u : i)];
                 const uint32_t ja = e0.x & 0xFFFu, jb = e1.x & 0xFFFu;
                 const uint32_t sa = s_cnt[ja], sb = s_cnt[jb];
-                const uint32_t ra = s_r0[ja], rb = s_r0[jb];
                 const uint32_t ta = MODE == kSparseWrite ? (uint32_t)s_start[ja] : sa >> 9;
                 const uint32_t tb = MODE == kSparseWrite ? (uint32_t)s_start[jb] : sb >> 9;
                 const float oa = VALS ? s_out[ja] : 0.0f, ob = VALS ? s_out[jb] : 0.0f;
-                place(e0, sa, ra, ta, oa);
-                if (two) place(e1, sb, rb, tb, ob);
+                place(e0, sa, ta, oa);
+                if (two) place(e1, sb, tb, ob);
             }
             __syncthreads();
             if (tid == 0) reset_counters();  // every thread has read them
@@ -636,15 +644,15 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
                 const uint32_t mm = s_cnt[jj] & 0x1FFu;
                 uint32_t rk[4];
                 float vv[4];
-                rk[0] = s_r0[jj];
-                rk[1] = s_sr[st0];
-                rk[2] = s_sr[st0 + 1];
-                rk[3] = mm == 4u ? (uint32_t)s_sr[st0 + 2] : 0x100u;  // above every rank
+                rk[0] = s_sr[st0];
+                rk[1] = s_sr[st0 + 1];
+                rk[2] = s_sr[st0 + 2];
+                rk[3] = mm == 4u ? (uint32_t)s_sr[st0 + 3] : 0x100u;  // above every rank
                 if (VALS) {
-                    vv[0] = s_out[jj];
-                    vv[1] = s_sv[st0];
-                    vv[2] = s_sv[st0 + 1];
-                    vv[3] = mm == 4u ? s_sv[st0 + 2] : 0.0f;
+                    vv[0] = s_sv[st0];
+                    vv[1] = s_sv[st0 + 1];
+                    vv[2] = s_sv[st0 + 2];
+                    vv[3] = mm == 4u ? s_sv[st0 + 3] : 0.0f;
                 } else {
                     vv[0] = vv[1] = vv[2] = vv[3] = 0.0f;
                 }
@@ -672,12 +680,10 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
                 const uint32_t jj = item & 0xFFFu, st0 = item >> 12;
                 uint32_t rk[5];
                 float vv[5];
-                rk[0] = s_r0[jj];
-                vv[0] = VALS ? s_out[jj] : 0.0f;
 #pragma unroll
-                for (int e = 1; e < 5; ++e) {
-                    rk[e] = s_sr[st0 + e - 1];
-                    vv[e] = VALS ? s_sv[st0 + e - 1] : 0.0f;
+                for (int e = 0; e < 5; ++e) {
+                    rk[e] = s_sr[st0 + e];
+                    vv[e] = VALS ? s_sv[st0 + e] : 0.0f;
                 }
                 cswap_rv(rk, vv, 0, 3); cswap_rv(rk, vv, 1, 4); cswap_rv(rk, vv, 0, 2);
                 cswap_rv(rk, vv, 1, 3); cswap_rv(rk, vv, 0, 1); cswap_rv(rk, vv, 2, 4);
@@ -727,8 +733,8 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
                     if ((lane >> 4) < RROWS && l16 < (uint32_t)PW) rpre[l16] = 0u;
                     __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
                     for (uint32_t e = l16; e < mm; e += 16u) {
-                        const uint32_t r = e == 0u ? (uint32_t)s_r0[jj] : (uint32_t)s_sr[st0 + e - 1u];
-                        if (VALS) rval[r] = e == 0u ? s_out[jj] : s_sv[st0 + e - 1u];
+                        const uint32_t r = s_sr[st0 + e];
+                        if (VALS) rval[r] = s_sv[st0 + e];
                         atomicOr(&rpre[r >> 5], 1u << (r & 31u));
                     }
                     __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
