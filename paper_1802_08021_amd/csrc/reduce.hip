@@ -561,8 +561,6 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
 
         if (!defer) {
             if (CNTS && tid == 0) a.tile_cnt[tile] = NE;
-            if (CNTS)
-                for (uint32_t r = tid; r < P; r += NT) s_E[L * PMAX + r] += rank_count(r);
             // P2, per later arrival of this wave: an index with two ranks is
             // finished here -- a single addition is the same in either order --
             // and counts its pair for the node sizes; otherwise the value is
@@ -804,6 +802,9 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
             }
         } else {
             __syncthreads();  // every thread has read the counters
+            // the slow pass counts this tile's entries of every rank
+            if (CNTS)
+                for (uint32_t r = tid; r < P; r += NT) s_E[L * PMAX + r] -= rank_count(r);
             if (tid == 0) {
                 reset_counters();
                 const uint32_t k = atomicAdd(a.slow_count, 1u);
@@ -817,7 +818,14 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
         __syncthreads();
     }
     __syncthreads();
-    if (CNTS) flush_counts<NT, PMAX>(s_E, a);
+    if (CNTS) {
+        // all entries of the chunk's streams (less those of deferred tiles,
+        // subtracted above)
+        for (uint32_t r = tid; r < P; r += NT)
+            s_E[L * PMAX + r] += a.off[r * stride + chunk + 1] - a.off[r * stride + chunk];
+        __syncthreads();
+        flush_counts<NT, PMAX>(s_E, a);
+    }
 }
 
 // ------------------------------------------------------------------------
