@@ -18,7 +18,13 @@ Besides the headline line the JSON carries:
                 FETCH_SIZE/WRITE_SIZE runs (profiles/), or null when the
                 kernel source changed since they were taken;
   cpu_baseline  the CPU oracle timed on a bounded sample of the workload;
-  per_config    the other configurations (c1..c4; c3 = top-k then reduce).
+  cold_ms_per_step  the step with the 256 MB Infinity Cache evicted first
+                (median of 5);
+  seeds         the step over seeds s..s+4 (fresh inputs): per-seed ms,
+                median and quartiles;
+  copy_ceiling  a plain 1 GiB device copy's bandwidth, the streaming ceiling;
+  per_config    the other configurations (c1..c4; c3 = top-k then reduce,
+                with the top-k input elements per second).
 
 Only one GPU is used; --gpus above 1 exits with a message.
 """
@@ -70,6 +76,55 @@ def calibrate_copy(torch) -> int:
     torch.cuda.synchronize()
     log("copied 1 GiB three times")
     return 0
+
+
+def copy_ceiling(torch, reps=5):
+    """A plain 1 GiB device copy (torch copy_): bytes read + written over its
+    time, the bandwidth a streaming kernel can reach on this device."""
+    x = torch.empty(1 << 28, dtype=torch.float32, device="cuda:0").fill_(1.0)
+    y = torch.empty_like(x)
+    y.copy_(x)
+    torch.cuda.synchronize()
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(reps):
+        y.copy_(x)
+    end.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(end) / reps
+    gbs = 2 * (1 << 30) / (ms * 1e-3) / 1e9
+    del x, y
+    return {"GB/s": gbs, "frac_of_peak": gbs / HBM_PEAK_GBS, "bytes": 2 << 30, "ms": ms}
+
+
+def time_cold(w, n, torch):
+    """Steps with the 256 MB Infinity Cache evicted first (a 512 MB buffer is
+    written before each); median ms of the step alone."""
+    flush = torch.empty(1 << 27, dtype=torch.float32, device="cuda:0")
+    times = []
+    for _ in range(n):
+        flush.fill_(0.0)
+        start = torch.cuda.Event(enable_timing=True)
+        end = torch.cuda.Event(enable_timing=True)
+        start.record()
+        w.step()
+        end.record()
+        torch.cuda.synchronize()
+        times.append(start.elapsed_time(end))
+    del flush
+    return float(np.median(times))
+
+
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 def arena(arrays, dtype, torch, dev, align=64):
@@ -251,7 +306,8 @@ def cpu_baseline(d, c, seed, frac_log2=2):
     dt = time.perf_counter() - t0
     return {"value": nnz / dt, "unit": "nnz/s", "cores": 1, "kind": "oracle",
             "sample": f"{c.name} streams restricted to indices < N/{2**frac_log2} "
-                      f"({nnz} input nnz, N'={Ns}); quantize + reduce, single thread, {dt:.2f} s"}
+                      f"({nnz} input nnz, N'={Ns}); quantize + reduce, single thread, {dt:.2f} s; "
+                      f"host {cpu_model()}, {os.cpu_count()} logical CPUs"}
 
 
 def describe(c) -> str:
@@ -304,12 +360,31 @@ def main() -> int:
                                 "GB/s": (w.kernel_bytes[g] / (v * 1e-3) / 1e9) if w.kernel_bytes.get(g) else None}
                for g, v in kdur.items()}
 
+    cold_ms = time_cold(w, 5, torch)
+    log(f"{args.workload}: cold (Infinity Cache evicted) {cold_ms:.3f} ms/step")
     cpu = None
     if not args.no_cpu_baseline and w.d_host is not None:
         log("timing the CPU oracle on a bounded sample")
         cpu = cpu_baseline(w.d_host, head_cfg, args.seed)
     w = None
     torch.cuda.empty_cache()
+
+    # the same step over further seeds (fresh inputs): median and quartiles
+    seeds = None
+    if not args.no_per_config:
+        per_seed = [ms]
+        for sd in range(args.seed + 1, args.seed + 5):
+            sw = Workload(args.workload, head_cfg, sd, torch, dev)
+            sms = time_steps(sw, 10, 2, torch)[0]
+            per_seed.append(sms)
+            sw = None
+            torch.cuda.empty_cache()
+        q25, q50, q75 = np.percentile(per_seed, [25, 50, 75])
+        seeds = {"seeds": list(range(args.seed, args.seed + 5)), "ms_per_step": per_seed,
+                 "median_ms": float(q50), "q25_ms": float(q25), "q75_ms": float(q75)}
+        log(f"{args.workload}: over 5 seeds median {q50:.3f} ms (IQR {q25:.3f}-{q75:.3f})")
+    ceiling = copy_ceiling(torch)
+    log(f"copy ceiling {ceiling['GB/s']:.0f} GB/s")
 
     per_config = {}
     if not args.no_per_config:
@@ -321,12 +396,16 @@ def main() -> int:
             pms, pwall, pk, pn, pd = time_steps(pw, max(5, args.steps // 2), 2, torch)
             per_config[name] = {
                 "workload": describe(c), "ms_per_step": pms, "input_nnz_per_s": pw.nnz / (pms * 1e-3),
+                "cold_ms_per_step": time_cold(pw, 3, torch),
                 "step_GB/s": pw.step_bytes / (pms * 1e-3) / 1e9,
                 "step_frac_of_hbm_peak": pw.step_bytes / (pms * 1e-3) / 1e9 / HBM_PEAK_GBS,
                 "root_nnz": pn, "root_dense": pd,
                 "kernels": {GROUP_NAMES[g]: {"avg_ms": v, "GB/s": (pw.kernel_bytes[g] / (v * 1e-3) / 1e9)
                                              if pw.kernel_bytes.get(g) else None} for g, v in pk.items()},
             }
+            if c.kind == "topk":
+                tk = sum(pk.get(g, 0.0) for g in (S.TIMER_TOPK_SELECT, S.TIMER_TOPK_WRITE))
+                per_config[name]["topk_input_elems_per_s"] = c.P * c.N / (tk * 1e-3) if tk else None
             log(f"{name}: {pms:.3f} ms/step")
             pw = None
             torch.cuda.empty_cache()
@@ -352,6 +431,9 @@ def main() -> int:
         "kernels": kernels,
         "cpu_baseline": cpu,
         "wall_ms_per_step": wall,
+        "cold_ms_per_step": cold_ms,
+        "seeds": seeds,
+        "copy_ceiling": ceiling,
         "per_config": per_config,
     }
     print(json.dumps(line), flush=True)
