@@ -24,7 +24,11 @@ Besides the headline line the JSON carries:
                 median and quartiles;
   copy_ceiling  a plain 1 GiB device copy's bandwidth, the streaming ceiling;
   per_config    the other configurations (c1..c4; c3 = top-k then reduce,
-                with the top-k input elements per second).
+                with the top-k input elements per second), each timed
+                after at least 0.3 s of warm-up steps, and the split-phase
+                share of c4 and c5 (index range 0 of P equal ones, every
+                rank's stream restricted to it: one node's reduction in the
+                split-allgather allreduce).
 
 Only one GPU is used; --gpus above 1 exits with a message.
 """
@@ -153,7 +157,10 @@ def empty_arena(sizes, dtype, torch, dev, align=256):
 class Workload:
     """Device-resident inputs, prepared calls and byte accounting of one config."""
 
-    def __init__(self, name, cfg, seed, torch, dev):
+    def __init__(self, name, cfg, seed, torch, dev, share=None):
+        """``share`` = (s, S): the s-th of S equal index ranges of the
+        config's vector, each rank's stream restricted to it (one node's
+        work in the split phase of the large-data allreduce)."""
         from paper_1802_08021_amd import inputs
         from paper_1802_08021_amd import sparcml as S
         self.name, self.c = name, cfg
@@ -161,6 +168,15 @@ class Workload:
         t0 = time.time()
         d = inputs.generate(c, seed)
         log(f"{name}: generated inputs in {time.time() - t0:.1f}s")
+        rng = {}
+        self.R = c.N
+        if share is not None:
+            assert c.kind != "topk"
+            lo, hi = c.N * share[0] // share[1], c.N * (share[0] + 1) // share[1]
+            keep = [(a >= lo) & (a < hi) for a in d["idx"]]
+            d = {"idx": [a[m] for a, m in zip(d["idx"], keep)], "val": [v[m] for v, m in zip(d["val"], keep)]}
+            rng = {"lo": lo, "hi": hi}
+            self.R = hi - lo
         self.groups = [S.TIMER_REDUCE_PASS, S.TIMER_REDUCE_SLOW, S.TIMER_REDUCE_WRITE]
         self.kernel_bytes = {}
         if c.kind == "topk":
@@ -188,7 +204,7 @@ class Workload:
                 _, codes = empty_arena(code_bytes, torch.uint8, torch, dev)
                 scale = torch.empty(c.P, dtype=torch.float32, device=dev)
                 self.quant = S.QuantizeCall(vals, codes, scale, c.qbits, inputs.quant_seed(seed, c.cfg))
-                self.reduce = S.ReduceCall(idx, c.N, c.delta, codes=codes, scales=scale, qbits=c.qbits)
+                self.reduce = S.ReduceCall(idx, c.N, c.delta, codes=codes, scales=scale, qbits=c.qbits, **rng)
                 self.groups += [S.TIMER_QUANT_NORM, S.TIMER_QUANT_CODES]
                 cb = sum(code_bytes)
                 self.kernel_bytes[S.TIMER_QUANT_NORM] = self.nnz * 4
@@ -198,11 +214,11 @@ class Workload:
                 self._steps = [self.quant.run, self.reduce.run]
             else:
                 _, vals = arena(d["val"], None, torch, dev)
-                self.reduce = S.ReduceCall(idx, c.N, c.delta, vals=vals)
+                self.reduce = S.ReduceCall(idx, c.N, c.delta, vals=vals, **rng)
                 self.in_bytes = self.nnz * 8
                 self.quant_bytes = 0
                 self._steps = [self.reduce.run]
-        self.d_host = d if cfg.cfg == 5 else None
+        self.d_host = d if cfg.cfg == 5 and share is None else None
 
     def step(self):
         out = None
@@ -214,13 +230,13 @@ class Workload:
         """Algorithmic bytes once the root representation is known."""
         from paper_1802_08021_amd import sparcml as S
         c = self.c
-        out_bytes = c.N * 4 if dense else root_nnz * 8
+        out_bytes = self.R * 4 if dense else root_nnz * 8
         if c.kind == "topk":
             red_in = self.nnz * 8
         else:
             red_in = self.in_bytes
         # first tile pass: reads the streams; a dense root is written there
-        self.kernel_bytes[S.TIMER_REDUCE_PASS] = red_in + (c.N * 4 if dense else 0)
+        self.kernel_bytes[S.TIMER_REDUCE_PASS] = red_in + (self.R * 4 if dense else 0)
         if not dense:
             self.kernel_bytes[S.TIMER_REDUCE_WRITE] = red_in + out_bytes
         if c.kind == "topk":
@@ -229,14 +245,22 @@ class Workload:
             self.step_bytes = self.quant_bytes + red_in + out_bytes
 
 
-def time_steps(w, K, W, torch):
+def time_steps(w, K, W, torch, warm_s=0.0):
+    """W untimed steps (continued until warm_s seconds have passed, so that
+    clocks have ramped after an idle gap), then K timed steps."""
     from paper_1802_08021_amd import sparcml as S
     res = None
-    for _ in range(W):
+    t0 = time.perf_counter()
+    done = 0
+    while done < W or time.perf_counter() - t0 < warm_s:
         res = w.step()
+        done += 1
+        if done % 8 == 0:
+            torch.cuda.synchronize()
     torch.cuda.synchronize()
+    # kernel durations: the library's events around every launch of the
+    # timed steps, read once afterwards
     S.timing_enable(True)
-    durs = {g: [] for g in w.groups}
     start = torch.cuda.Event(enable_timing=True)
     end = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -244,18 +268,15 @@ def time_steps(w, K, W, torch):
     start.record()
     for _ in range(K):
         res = w.step()
-        for g in w.groups:
-            v = S.timing_read(g)
-            if v is not None:
-                durs[g].append(v)
     end.record()
     torch.cuda.synchronize()
     wall = (time.perf_counter() - wall0) * 1e3 / K
+    durs = {g: S.timing_read(g) for g in w.groups}
     S.timing_enable(False)
     ms = start.elapsed_time(end) / K
     nnz, dense = res
     w.finish_bytes(nnz, dense)
-    return ms, wall, {g: float(np.mean(v)) for g, v in durs.items() if v}, nnz, dense
+    return ms, wall, {g: v for g, v in durs.items() if v is not None}, nnz, dense
 
 
 GROUP_NAMES = {0: "reduce_tiles", 1: "reduce_write", 2: "reduce_slow", 3: "qsgd_norm",
@@ -375,7 +396,7 @@ def main() -> int:
         per_seed = [ms]
         for sd in range(args.seed + 1, args.seed + 5):
             sw = Workload(args.workload, head_cfg, sd, torch, dev)
-            sms = time_steps(sw, 10, 2, torch)[0]
+            sms = time_steps(sw, 10, 2, torch, warm_s=0.3)[0]
             per_seed.append(sms)
             sw = None
             torch.cuda.empty_cache()
@@ -388,14 +409,17 @@ def main() -> int:
 
     per_config = {}
     if not args.no_per_config:
-        for name in ("c1", "c2", "c3", "c4", "c5"):
+        for name in ("c1", "c2", "c3", "c4", "c5", "c4/share", "c5/share"):
             if name == args.workload:
                 continue
             c = inputs.config(int(name[1]))
-            pw = Workload(name, c, args.seed, torch, dev)
-            pms, pwall, pk, pn, pd = time_steps(pw, max(5, args.steps // 2), 2, torch)
+            share = (0, c.P) if name.endswith("/share") else None
+            pw = Workload(name, c, args.seed, torch, dev, share=share)
+            pms, pwall, pk, pn, pd = time_steps(pw, max(5, args.steps // 2), 2, torch, warm_s=0.3)
+            desc = describe(c) + (f"; split-phase share [{pw.reduce.rng[0]}, {pw.reduce.rng[1]}) "
+                                  f"(1 of {c.P})" if share else "")
             per_config[name] = {
-                "workload": describe(c), "ms_per_step": pms, "input_nnz_per_s": pw.nnz / (pms * 1e-3),
+                "workload": desc, "ms_per_step": pms, "input_nnz_per_s": pw.nnz / (pms * 1e-3),
                 "cold_ms_per_step": time_cold(pw, 3, torch),
                 "step_GB/s": pw.step_bytes / (pms * 1e-3) / 1e9,
                 "step_frac_of_hbm_peak": pw.step_bytes / (pms * 1e-3) / 1e9 / HBM_PEAK_GBS,

@@ -11,6 +11,9 @@
  *   sparcml_sparse_reduce  -- sum of P sparse streams in recursive-doubling
  *                             order with the sparse->dense switch
  *                             (§5.1, §5.3.1, Fig. 2)
+ *   sparcml_sparse_reduce_range -- the same over one index range: a node's
+ *                             share of the split phase of the large-data
+ *                             allreduce (§5.3.2)
  *   sparcml_densify        -- dense representation of one stream (§5.1)
  *
  * Conventions shared by every call:
@@ -18,12 +21,12 @@
  *     except the descriptor arrays (sparcml_stream[], pointer tables), which
  *     are HOST memory read during the call.
  *   - `stream` is a hipStream_t passed as void*; NULL means the null stream.
- *     Work is enqueued on it in order; sparcml_sparse_reduce additionally
- *     waits for its own result header (see there); the other calls return
- *     without synchronizing.
+ *     Work is enqueued on it in order; sparcml_sparse_reduce(_range)
+ *     additionally waits for its own result header (see there); the other
+ *     calls return without synchronizing.
  *   - The caller owns every buffer.  The library never allocates, frees or
  *     keeps device memory between calls and has no global mutable state
- *     apart from the thread-local last-error message.  Scratch memory comes
+ *     apart from the thread-local last-error message and timing events.  Scratch memory comes
  *     from the caller's workspace (size from sparcml_workspace_size).
  *     Calls on distinct streams with distinct workspaces may run
  *     concurrently.
@@ -186,6 +189,32 @@ SPARCML_API int sparcml_sparse_reduce(int P, const sparcml_stream* streams, uint
                           void* ws, size_t ws_bytes, void* stream);
 
 /*
+ * One GPU's share of the split phase of the large-data allreduce (§5.3.2,
+ * the split-allgather / DSAR scheme): the sum of P streams restricted to
+ * the index range [lo, hi) of a vector of N, with the same recursive-
+ * doubling association and representation switch as sparcml_sparse_reduce
+ * applied to the range as if it were the whole vector: thr =
+ * floor(delta * (hi - lo)), a dense node holds hi - lo values.  Each
+ * stream is the part of a rank's stream whose indices lie in [lo, hi)
+ * (strictly ascending, not checked).  With lo == 0 and hi == N this is
+ * sparcml_sparse_reduce.
+ *   lo, hi   0 <= lo < hi <= N, N < 2^32.
+ *   out      in: as for sparcml_sparse_reduce with hi - lo in place of N
+ *            (out->val holds hi - lo floats).
+ *            out: a sparse root holds absolute indices (in [lo, hi)); a
+ *            dense root holds out->val[i] = sum at index lo + i, i < hi - lo.
+ *   node_nnz, node_dense: as for sparcml_sparse_reduce (dense nodes count
+ *            hi - lo).
+ *   ws       sparcml_workspace_size(SPARCML_OP_REDUCE, P, hi - lo, ...).
+ * Errors: as for sparcml_sparse_reduce; EINVAL also for lo >= hi, hi > N,
+ * or a stream with more than hi - lo entries.
+ */
+SPARCML_API int sparcml_sparse_reduce_range(int P, const sparcml_stream* streams, uint64_t N,
+                                uint64_t lo, uint64_t hi, double delta, sparcml_stream* out,
+                                uint64_t* node_nnz, uint8_t* node_dense, void* ws,
+                                size_t ws_bytes, void* stream);
+
+/*
  * Dense representation of one stream (§5.1): dense[j] = value of index j,
  * +0.0 where absent; dequantizes QSGD codes on the fly.  A dense input is
  * copied (or dequantized).  Writes all N floats.  Indices must be strictly
@@ -197,10 +226,13 @@ SPARCML_API int sparcml_densify(const sparcml_stream* in, uint64_t N, float* den
 
 /*
  * Kernel timing for benchmarks and profiling (off by default; per calling
- * thread).  While enabled, each call records HIP events on its stream
- * around its main kernels; sparcml_timing_read returns the duration (ms) of
- * the most recent launch of one kernel group, waiting for its stop event.
- * Groups: SPARCML_TIMER_*.  Enabling or disabling forgets earlier records.
+ * thread).  While enabled, each call records a pair of HIP events on its
+ * stream around each of its main kernels; sparcml_timing_read returns the
+ * mean duration (ms) over every launch of one kernel group since timing was
+ * enabled, waiting for their stop events (so it can be called once after a
+ * timed loop without synchronizing inside it).  Groups: SPARCML_TIMER_*.
+ * Enabling or disabling forgets earlier records; event pairs are created on
+ * first use and kept for reuse by the calling thread.
  * sparcml_timing_read returns EINVAL when the group has no record.
  */
 #define SPARCML_TIMER_REDUCE_PASS 0  /* first tile pass of sparse_reduce */

@@ -8,6 +8,8 @@ tests, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
 Functions follow the paper:
   * ``sparse_reduce``  -- §5.1 sparse streams, switch rule, pairwise sum;
                           §5.3.1 recursive doubling order.
+  * ``sparse_reduce_range`` -- one node's share of the split phase of the
+                          large-data allreduce (§5.3.2).
   * ``topk``           -- §2.2 Top-k sparsification, Alg. 1 error update.
   * ``quantize``       -- §2.2 / §6 QSGD stochastic quantization.
   * ``dequantize``, ``densify``, ``philox4x32_10``.
@@ -125,6 +127,29 @@ def sparse_reduce(idx_list, val_list, N: int, delta: float):
         "node_nnz": node_nnz[: P - 1].copy(),
         "node_dense": node_dense[: P - 1].copy(),
     }
+
+
+def sparse_reduce_range(idx_list, val_list, N: int, lo: int, hi: int, delta: float):
+    """One node's share of the split phase of the large-data (split-allgather)
+    allreduce, §5.3.2: the node responsible for the index range [lo, hi)
+    reduces the part of every rank's stream that falls in it.  The share is
+    the reduction of those parts as a vector of hi - lo coordinates (index
+    lo + i at i): threshold floor(delta * (hi - lo)), recursive-doubling
+    association as in ``sparse_reduce``.  Entries outside [lo, hi) are
+    dropped.  A sparse root's ``idx`` holds absolute indices; a dense root's
+    ``val`` holds hi - lo values."""
+    if not (0 <= lo < hi <= N):
+        raise OracleError("need 0 <= lo < hi <= N")
+    parts_i, parts_v = [], []
+    for a, v in zip(idx_list, val_list):
+        a = np.asarray(a, dtype=np.uint64)
+        keep = (a >= lo) & (a < hi)
+        parts_i.append((a[keep] - lo).astype(np.uint32))
+        parts_v.append(np.asarray(v, dtype=np.float32)[keep])
+    res = sparse_reduce(parts_i, parts_v, hi - lo, delta)
+    if not res["dense"]:
+        res["idx"] = (res["idx"].astype(np.uint64) + lo).astype(np.uint32)
+    return res
 
 
 def topk(x: np.ndarray, k: int, residual: bool = False):

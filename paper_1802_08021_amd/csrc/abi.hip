@@ -69,6 +69,76 @@ uint64_t threshold(uint64_t N, double delta)
     return t >= 18446744073709551615.0 ? UINT64_MAX : (uint64_t)t;
 }
 
+// The reduction of the index range [lo, hi) of N (the whole vector: [0, N)):
+// every stream's indices lie in the range; a dense result holds hi - lo
+// values (index lo + i at i), a sparse one absolute indices.
+int reduce_impl(int P, const sparcml_stream* streams, uint64_t N, uint64_t lo, uint64_t hi, double delta,
+                sparcml_stream* out, uint64_t* node_nnz, uint8_t* node_dense, void* ws, size_t ws_bytes,
+                void* stream)
+{
+    try {
+        uint32_t qbits;
+        uint64_t max_nnz, sum_nnz;
+        int rc = reduce_validate(P, streams, N, delta, &qbits, &max_nnz, &sum_nnz);
+        if (rc) return rc;
+        const uint64_t R = hi - lo;  // range size
+        if (max_nnz > R) return fail(SPARCML_EINVAL, "a stream has more entries than the range has indices");
+        if (!out || !out->val) return fail(SPARCML_EINVAL, "out / out->val is NULL");
+        if (out->qbits) return fail(SPARCML_EINVAL, "out->qbits must be 0");
+        const uint64_t thr = threshold(R, delta);
+        const hipStream_t s = (hipStream_t)stream;
+        hipError_t e;
+
+        if (P == 1) {
+            const sparcml_stream& a = streams[0];
+            if (a.nnz > thr) {
+                e = densify_run(a.idx, a.val, a.qval, a.qscale, qbits, a.nnz, R, 0, out->val, s, lo);
+                if (e != hipSuccess) return hip_fail(e, "densify");
+                out->nnz = R;
+                out->is_dense = 1;
+                return SPARCML_OK;
+            }
+            if (a.nnz && !out->idx) return fail(SPARCML_EINVAL, "out->idx is NULL");
+            if (out->nnz < a.nnz) return fail(SPARCML_ECAPACITY, "out capacity %llu < %llu",
+                                              (unsigned long long)out->nnz, (unsigned long long)a.nnz);
+            if (a.nnz) {
+                e = hipMemcpyAsync(out->idx, a.idx, a.nnz * sizeof(uint32_t), hipMemcpyDeviceToDevice, s);
+                if (e == hipSuccess)
+                    e = qbits ? dequant_run(a.qval, a.qscale, qbits, a.nnz, out->val, s)
+                              : hipMemcpyAsync(out->val, a.val, a.nnz * sizeof(float),
+                                               hipMemcpyDeviceToDevice, s);
+                if (e != hipSuccess) return hip_fail(e, "copy");
+            }
+            out->nnz = a.nnz;
+            out->is_dense = 0;
+            return SPARCML_OK;
+        }
+
+        const uint64_t cap = std::min(thr, sum_nnz);
+        if (cap && !out->idx) return fail(SPARCML_EINVAL, "out->idx is NULL");
+        if (out->nnz < cap)
+            return fail(SPARCML_ECAPACITY, "out capacity %llu < min(thr, sum nnz) = %llu",
+                        (unsigned long long)out->nnz, (unsigned long long)cap);
+        ReducePlan plan;
+        reduce_plan(P, R, max_nnz, sum_nnz, delta, (int)qbits, &plan, lo);
+        const size_t need = reduce_workspace(plan);
+        if (!ws || ws_bytes < need) return fail(SPARCML_EWORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
+
+        std::vector<StreamDesc> tab(P);
+        for (int r = 0; r < P; ++r)
+            tab[r] = StreamDesc{streams[r].idx, streams[r].val, streams[r].qval, streams[r].qscale,
+                                streams[r].nnz, 0};
+        ReduceResult res{};
+        e = reduce_run(plan, tab.data(), out->idx, out->val, node_nnz, node_dense, ws, s, &res);
+        if (e != hipSuccess) return hip_fail(e, "sparse_reduce");
+        out->nnz = res.nnz;
+        out->is_dense = res.dense;
+        return SPARCML_OK;
+    } catch (const std::exception& ex) {
+        return fail(SPARCML_EHIP, "host exception: %s", ex.what());
+    }
+}
+
 }  // namespace
 
 extern "C" {
@@ -180,65 +250,16 @@ int sparcml_sparse_reduce(int P, const sparcml_stream* streams, uint64_t N, doub
                           sparcml_stream* out, uint64_t* node_nnz, uint8_t* node_dense, void* ws,
                           size_t ws_bytes, void* stream)
 {
-    try {
-        uint32_t qbits;
-        uint64_t max_nnz, sum_nnz;
-        int rc = reduce_validate(P, streams, N, delta, &qbits, &max_nnz, &sum_nnz);
-        if (rc) return rc;
-        if (!out || !out->val) return fail(SPARCML_EINVAL, "out / out->val is NULL");
-        if (out->qbits) return fail(SPARCML_EINVAL, "out->qbits must be 0");
-        const uint64_t thr = threshold(N, delta);
-        const hipStream_t s = (hipStream_t)stream;
-        hipError_t e;
+    return reduce_impl(P, streams, N, 0, N, delta, out, node_nnz, node_dense, ws, ws_bytes, stream);
+}
 
-        if (P == 1) {
-            const sparcml_stream& a = streams[0];
-            if (a.nnz > thr) {
-                e = densify_run(a.idx, a.val, a.qval, a.qscale, qbits, a.nnz, N, 0, out->val, s);
-                if (e != hipSuccess) return hip_fail(e, "densify");
-                out->nnz = N;
-                out->is_dense = 1;
-                return SPARCML_OK;
-            }
-            if (a.nnz && !out->idx) return fail(SPARCML_EINVAL, "out->idx is NULL");
-            if (out->nnz < a.nnz) return fail(SPARCML_ECAPACITY, "out capacity %llu < %llu",
-                                              (unsigned long long)out->nnz, (unsigned long long)a.nnz);
-            if (a.nnz) {
-                e = hipMemcpyAsync(out->idx, a.idx, a.nnz * sizeof(uint32_t), hipMemcpyDeviceToDevice, s);
-                if (e == hipSuccess)
-                    e = qbits ? dequant_run(a.qval, a.qscale, qbits, a.nnz, out->val, s)
-                              : hipMemcpyAsync(out->val, a.val, a.nnz * sizeof(float),
-                                               hipMemcpyDeviceToDevice, s);
-                if (e != hipSuccess) return hip_fail(e, "copy");
-            }
-            out->nnz = a.nnz;
-            out->is_dense = 0;
-            return SPARCML_OK;
-        }
-
-        const uint64_t cap = std::min(thr, sum_nnz);
-        if (cap && !out->idx) return fail(SPARCML_EINVAL, "out->idx is NULL");
-        if (out->nnz < cap)
-            return fail(SPARCML_ECAPACITY, "out capacity %llu < min(thr, sum nnz) = %llu",
-                        (unsigned long long)out->nnz, (unsigned long long)cap);
-        ReducePlan plan;
-        reduce_plan(P, N, max_nnz, sum_nnz, delta, (int)qbits, &plan);
-        const size_t need = reduce_workspace(plan);
-        if (!ws || ws_bytes < need) return fail(SPARCML_EWORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
-
-        std::vector<StreamDesc> tab(P);
-        for (int r = 0; r < P; ++r)
-            tab[r] = StreamDesc{streams[r].idx, streams[r].val, streams[r].qval, streams[r].qscale,
-                                streams[r].nnz, 0};
-        ReduceResult res{};
-        e = reduce_run(plan, tab.data(), out->idx, out->val, node_nnz, node_dense, ws, s, &res);
-        if (e != hipSuccess) return hip_fail(e, "sparse_reduce");
-        out->nnz = res.nnz;
-        out->is_dense = res.dense;
-        return SPARCML_OK;
-    } catch (const std::exception& ex) {
-        return fail(SPARCML_EHIP, "host exception: %s", ex.what());
-    }
+int sparcml_sparse_reduce_range(int P, const sparcml_stream* streams, uint64_t N, uint64_t lo,
+                                uint64_t hi, double delta, sparcml_stream* out, uint64_t* node_nnz,
+                                uint8_t* node_dense, void* ws, size_t ws_bytes, void* stream)
+{
+    if (!valid_n(N)) return fail(SPARCML_EINVAL, "N must be in [1, 2^32)");
+    if (!(lo < hi && hi <= N)) return fail(SPARCML_EINVAL, "need 0 <= lo < hi <= N");
+    return reduce_impl(P, streams, N, lo, hi, delta, out, node_nnz, node_dense, ws, ws_bytes, stream);
 }
 
 int sparcml_densify(const sparcml_stream* in, uint64_t N, float* dense, void* stream)

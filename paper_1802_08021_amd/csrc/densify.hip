@@ -26,13 +26,13 @@ __device__ __forceinline__ uint32_t lower_bound_u32(const uint32_t* a, uint32_t 
 
 __global__ void __launch_bounds__(256) k_densify(const uint32_t* idx, const float* val,
                                                  const uint8_t* qval, const float* qscale,
-                                                 uint32_t qbits, uint32_t nnz, uint64_t N,
+                                                 uint32_t qbits, uint32_t nnz, uint64_t lo, uint64_t N,
                                                  float* out)
 {
     __shared__ float s_tile[kTile];
     __shared__ uint32_t s_rng[2];
-    const uint64_t tlo = (uint64_t)blockIdx.x * kTile;
-    const uint64_t thi = min(tlo + kTile, N);
+    const uint64_t tlo = lo + (uint64_t)blockIdx.x * kTile;  // absolute index of the tile
+    const uint64_t thi = min(tlo + kTile, lo + N);
     for (uint32_t j = threadIdx.x; j < kTile; j += 256) s_tile[j] = 0.0f;
     if (threadIdx.x < 2) s_rng[threadIdx.x] = lower_bound_u32(idx, 0u, nnz, threadIdx.x ? thi : tlo);
     __syncthreads();
@@ -43,7 +43,7 @@ __global__ void __launch_bounds__(256) k_densify(const uint32_t* idx, const floa
     }
     __syncthreads();
     for (uint32_t j = threadIdx.x; j < kTile; j += 256)
-        if (tlo + j < thi) out[tlo + j] = s_tile[j];
+        if (tlo + j < thi) out[tlo - lo + j] = s_tile[j];
 }
 
 __global__ void k_dequant(const uint8_t* qval, const float* qscale, uint32_t qbits, uint64_t n,
@@ -68,7 +68,7 @@ hipError_t dequant_run(const uint8_t* qval, const float* qscale, uint32_t qbits,
 
 hipError_t densify_run(const uint32_t* idx, const float* val, const uint8_t* qval,
                        const float* qscale, uint32_t qbits, uint64_t nnz, uint64_t N,
-                       int is_dense, float* dense, hipStream_t s)
+                       int is_dense, float* dense, hipStream_t s, uint64_t lo)
 {
     if (is_dense) {
         if (qbits) return dequant_run(qval, qscale, qbits, N, dense, s);
@@ -77,7 +77,7 @@ hipError_t densify_run(const uint32_t* idx, const float* val, const uint8_t* qva
     const uint64_t tiles = (N + kTile - 1) / kTile;
     timer_begin(kTDensify, s);
     hipLaunchKernelGGL(k_densify, dim3((uint32_t)tiles), dim3(256), 0, s, idx, val, qval, qscale,
-                       qbits, (uint32_t)nnz, N, dense);
+                       qbits, (uint32_t)nnz, lo, N, dense);
     timer_end(kTDensify, s);
     return hipGetLastError();
 }

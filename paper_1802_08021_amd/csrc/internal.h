@@ -74,13 +74,14 @@ struct Carve {
 };
 
 // ---------------------------------------------------------------- reduce
+// The reduction covers the index range [lo, lo + N); stream indices lie in it.
 struct ReducePlan {
     uint32_t P, L, PK, T, ntiles, nchunks, tiles_per_chunk, qbits;  // PK: rank class 16/32/64/128/256
-    uint64_t N, thr, sum_nnz;
+    uint64_t N, lo, thr, sum_nnz;
     int speculate_dense;
 };
 int reduce_plan(int P, uint64_t N, uint64_t max_nnz, uint64_t sum_nnz, double delta, int qbits,
-                ReducePlan* plan);
+                ReducePlan* plan, uint64_t lo = 0);
 size_t reduce_workspace(const ReducePlan& p);
 
 struct ReduceResult {
@@ -95,9 +96,10 @@ hipError_t reduce_run(const ReducePlan& p, const StreamDesc* host_tab, uint32_t*
                       hipStream_t s, ReduceResult* res);
 
 // ---------------------------------------------------------------- densify
+// dense[i] = the stream's value at index lo + i, i < N (+0.0 where it has none).
 hipError_t densify_run(const uint32_t* idx, const float* val, const uint8_t* qval,
                        const float* qscale, uint32_t qbits, uint64_t nnz, uint64_t N,
-                       int is_dense, float* dense, hipStream_t s);
+                       int is_dense, float* dense, hipStream_t s, uint64_t lo = 0);
 // out[i] = dequantized code i, i < n.
 hipError_t dequant_run(const uint8_t* qval, const float* qscale, uint32_t qbits, uint64_t n,
                        float* out, hipStream_t s);

@@ -92,6 +92,7 @@ struct Args {
     float* out_val;
     uint32_t P, L, N, T, ntiles, nchunks, tpc, qbits;
     uint32_t out_vec;          // out_val is 16-byte aligned
+    uint32_t lo;               // first index of the range [lo, lo + N); dense output is relative
 };
 
 __device__ __forceinline__ uint32_t lower_bound(const uint32_t* a, uint32_t lo, uint32_t hi,
@@ -369,8 +370,8 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
     for (int s = 0; s < SLMAX; ++s) load_win_at(sw[3 * s + 1], sw[3 * s].w, sw[3 * s].x, xr[s], vr[s]);
 
     for (uint32_t tile = t0; tile < t1; ++tile) {
-        const uint32_t tlo = tile * T;
-        const uint32_t TT = (uint32_t)min((uint64_t)T, (uint64_t)a.N - tlo);  // tile width
+        const uint32_t trel = tile * T, tlo = a.lo + trel;  // tile start, in the range and absolute
+        const uint32_t TT = (uint32_t)min((uint64_t)T, (uint64_t)a.N - trel);  // tile width
         const uint32_t toff = MODE == kSparseWrite ? a.tile_off[tile] : 0u;
 
         // P1w: the in-tile entries of every window, compacted into this
@@ -788,7 +789,7 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
                 if (MODE == kDense) {
                     const float4 v = *reinterpret_cast<const float4*>(&s_out[c]);
                     *reinterpret_cast<float4*>(&s_out[c]) = make_float4(0.f, 0.f, 0.f, 0.f);
-                    const uint64_t g = (uint64_t)tlo + c;
+                    const uint64_t g = (uint64_t)trel + c;
                     if (a.out_vec && c + 4u <= TT) {
                         *reinterpret_cast<float4*>(a.out_val + g) = v;
                     } else {
@@ -855,8 +856,8 @@ __global__ void __launch_bounds__(kSlowNT) k_slow(Args a)
 
     for (uint32_t k = blockIdx.x; k < nslow; k += gridDim.x) {
         const uint32_t tile = a.slow_list[k];
-        const uint32_t tlo = tile * a.T;
-        const uint32_t thi = (uint32_t)min((uint64_t)tlo + a.T, (uint64_t)a.N);
+        const uint32_t tlo = a.lo + tile * a.T;
+        const uint32_t thi = (uint32_t)min((uint64_t)tlo + a.T, (uint64_t)a.lo + a.N);
         __syncthreads();
         for (uint32_t r = tid; r < P; r += NT)
             s_lo[r] = lower_bound(a.tab[r].idx, 0u, (uint32_t)a.tab[r].nnz, tlo);
@@ -949,7 +950,7 @@ __global__ void __launch_bounds__(kSlowNT) k_slow(Args a)
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
                     const uint32_t j = tid * 4 + q;
-                    if (j < width) a.out_val[sub + j] = ((nzbits >> q) & 1u) ? vals[q] + 0.0f : 0.0f;
+                    if (j < width) a.out_val[sub - a.lo + j] = ((nzbits >> q) & 1u) ? vals[q] + 0.0f : 0.0f;
                 }
             } else if (MODE == kSparseWrite) {
                 uint32_t o = a.tile_off[tile] + tile_nz + excl;
@@ -974,7 +975,7 @@ __global__ void __launch_bounds__(kSlowNT) k_slow(Args a)
 // Per-chunk start offsets of every stream (binary search) and zeroing of the
 // counters the passes accumulate into.
 __global__ void k_partition(const StreamDesc* tab, uint32_t* off, uint32_t P, uint32_t nchunks,
-                            uint64_t chunk_coords, uint64_t N, uint32_t* zero, uint32_t nzero)
+                            uint64_t chunk_coords, uint64_t lo, uint64_t N, uint32_t* zero, uint32_t nzero)
 {
     const uint32_t gid = blockIdx.x * blockDim.x + threadIdx.x;
     if (gid < nzero) zero[gid] = 0u;
@@ -983,7 +984,7 @@ __global__ void k_partition(const StreamDesc* tab, uint32_t* off, uint32_t P, ui
     const uint32_t r = gid / stride, c = gid % stride;
     const uint32_t nnz = (uint32_t)tab[r].nnz;
     uint32_t res = nnz;
-    if (c < nchunks) res = lower_bound(tab[r].idx, 0u, nnz, min((uint64_t)c * chunk_coords, N));
+    if (c < nchunks) res = lower_bound(tab[r].idx, 0u, nnz, lo + min((uint64_t)c * chunk_coords, N));
     off[gid] = res;
 }
 
@@ -1176,9 +1177,10 @@ Layout layout(const ReducePlan& p, void* ws)
 }  // namespace
 
 int reduce_plan(int P, uint64_t N, uint64_t max_nnz, uint64_t sum_nnz, double delta, int qbits,
-                ReducePlan* plan)
+                ReducePlan* plan, uint64_t lo)
 {
     ReducePlan p{};
+    p.lo = lo;
     p.P = (uint32_t)P;
     p.L = 0;
     while ((1u << p.L) < p.P) ++p.L;
@@ -1212,7 +1214,7 @@ hipError_t reduce_run(const ReducePlan& p, const StreamDesc* host_tab, uint32_t*
 
     const uint32_t nthreads = std::max<uint32_t>(p.P * (p.nchunks + 1), p.P + 1);
     hipLaunchKernelGGL(k_partition, dim3((nthreads + 255) / 256), dim3(256), 0, s, l.tab, l.off,
-                       p.P, p.nchunks, (uint64_t)p.tiles_per_chunk * p.T, p.N, l.zero, p.P + 1);
+                       p.P, p.nchunks, (uint64_t)p.tiles_per_chunk * p.T, p.lo, p.N, l.zero, p.P + 1);
     if ((e = hipGetLastError()) != hipSuccess) return e;
 
     Args a{};
@@ -1228,6 +1230,7 @@ hipError_t reduce_run(const ReducePlan& p, const StreamDesc* host_tab, uint32_t*
     a.P = p.P;
     a.L = p.L;
     a.N = (uint32_t)p.N;
+    a.lo = (uint32_t)p.lo;
     a.T = p.T;
     a.ntiles = p.ntiles;
     a.nchunks = p.nchunks;

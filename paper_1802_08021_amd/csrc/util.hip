@@ -5,6 +5,8 @@
 #include <string.h>
 
 #include <algorithm>
+#include <utility>
+#include <vector>
 
 namespace sparcml {
 namespace {
@@ -38,13 +40,38 @@ hipError_t upload(void* dst, const void* src, size_t bytes, hipStream_t s)
 
 namespace {
 
+// Every launch of a group between enabling and reading gets its own event
+// pair, so that reading once after many calls averages all of them without
+// synchronizing in between.  Pairs are kept for reuse; past kMaxPairs a
+// group's finished pairs are folded into a running sum.
+constexpr size_t kMaxPairs = 4096;
+
+struct Group {
+    std::vector<std::pair<hipEvent_t, hipEvent_t>> pool;  // created events, reused
+    size_t used = 0;                                      // pairs recorded since enabling
+    double folded_ms = 0.0;                               // folded pairs' total
+    uint64_t folded_n = 0;
+};
+
 struct Timers {
     bool enabled = false;
-    bool created = false;
-    hipEvent_t ev[kTSlots][2];
-    bool recorded[kTSlots] = {};
+    Group g[kTSlots];
 };
 thread_local Timers g_timers;
+
+// Total ms and count of the first `used` pairs of a group (waits for them).
+bool sum_pairs(Group& g, double* ms, uint64_t* n)
+{
+    for (size_t i = 0; i < g.used; ++i) {
+        float t = 0.0f;
+        if (hipEventSynchronize(g.pool[i].second) != hipSuccess ||
+            hipEventElapsedTime(&t, g.pool[i].first, g.pool[i].second) != hipSuccess)
+            return false;
+        *ms += t;
+        ++*n;
+    }
+    return true;
+}
 
 }  // namespace
 
@@ -52,36 +79,54 @@ void timer_begin(int slot, hipStream_t s)
 {
     Timers& t = g_timers;
     if (!t.enabled) return;
-    if (!t.created) {
-        for (int i = 0; i < kTSlots; ++i)
-            for (int j = 0; j < 2; ++j)
-                if (hipEventCreate(&t.ev[i][j]) != hipSuccess) return;
-        t.created = true;
+    Group& g = t.g[slot];
+    if (g.used == kMaxPairs) {
+        if (!sum_pairs(g, &g.folded_ms, &g.folded_n)) return;
+        g.used = 0;
     }
-    hipEventRecord(t.ev[slot][0], s);
+    if (g.used == g.pool.size()) {
+        hipEvent_t a, b;
+        if (hipEventCreate(&a) != hipSuccess) return;
+        if (hipEventCreate(&b) != hipSuccess) {
+            hipEventDestroy(a);
+            return;
+        }
+        g.pool.emplace_back(a, b);
+    }
+    hipEventRecord(g.pool[g.used].first, s);
 }
 
 void timer_end(int slot, hipStream_t s)
 {
     Timers& t = g_timers;
-    if (!t.enabled || !t.created) return;
-    hipEventRecord(t.ev[slot][1], s);
-    t.recorded[slot] = true;
+    if (!t.enabled) return;
+    Group& g = t.g[slot];
+    if (g.used == g.pool.size()) return;  // begin failed
+    hipEventRecord(g.pool[g.used].second, s);
+    ++g.used;
 }
 
 int timer_enable(int on)
 {
     g_timers.enabled = on != 0;
-    for (bool& r : g_timers.recorded) r = false;
+    for (Group& g : g_timers.g) {
+        g.used = 0;
+        g.folded_ms = 0.0;
+        g.folded_n = 0;
+    }
     return 0;
 }
 
 int timer_read(int slot, float* ms)
 {
-    Timers& t = g_timers;
-    if (slot < 0 || slot >= kTSlots || !ms || !t.created || !t.recorded[slot]) return -1;
-    if (hipEventSynchronize(t.ev[slot][1]) != hipSuccess) return -5;
-    return hipEventElapsedTime(ms, t.ev[slot][0], t.ev[slot][1]) == hipSuccess ? 0 : -5;
+    if (slot < 0 || slot >= kTSlots || !ms) return -1;
+    Group& g = g_timers.g[slot];
+    double sum = g.folded_ms;
+    uint64_t n = g.folded_n;
+    if (!sum_pairs(g, &sum, &n)) return -5;
+    if (n == 0) return -1;
+    *ms = (float)(sum / (double)n);
+    return 0;
 }
 
 }  // namespace sparcml

@@ -62,6 +62,9 @@ def lib() -> ctypes.CDLL:
     L.sparcml_sparse_reduce.argtypes = [i32, ctypes.POINTER(Stream), u64, ctypes.c_double,
                                         ctypes.POINTER(Stream), vp, vp, vp, ctypes.c_size_t, vp]
     L.sparcml_sparse_reduce.restype = i32
+    L.sparcml_sparse_reduce_range.argtypes = [i32, ctypes.POINTER(Stream), u64, u64, u64, ctypes.c_double,
+                                              ctypes.POINTER(Stream), vp, vp, vp, ctypes.c_size_t, vp]
+    L.sparcml_sparse_reduce_range.restype = i32
     L.sparcml_densify.argtypes = [ctypes.POINTER(Stream), u64, vp, vp]
     L.sparcml_densify.restype = i32
     L.sparcml_timing_enable.argtypes = [i32]
@@ -85,7 +88,8 @@ def timing_enable(on: bool) -> None:
 
 
 def timing_read(group: int):
-    """Duration (ms) of the last launch of a kernel group, or None."""
+    """Mean duration (ms) of a kernel group's launches since timing was
+    enabled, or None."""
     ms = ctypes.c_float(0.0)
     rc = lib().sparcml_timing_read(group, ctypes.byref(ms))
     return float(ms.value) if rc == OK else None
@@ -220,6 +224,19 @@ def sparse_reduce(idx, vals, N: int, delta: float, codes=None, scales=None, qbit
     switch.  ``scales`` is a device fp32 tensor [P] (one scale per stream)
     when ``qbits`` != 0.  Returns dict(idx, val, nnz, dense, node_nnz,
     node_dense); ``idx`` is None for a dense root."""
+    return _reduce(idx, vals, N, None, delta, codes, scales, qbits, node_info, ws, out_idx, out_val)
+
+
+def sparse_reduce_range(idx, vals, N: int, lo: int, hi: int, delta: float, codes=None, scales=None,
+                        qbits: int = 0, node_info: bool = False, ws=None, out_idx=None, out_val=None):
+    """One share of the split phase: the sum of P streams whose indices lie
+    in [lo, hi), reduced as a vector of hi - lo (threshold floor(delta *
+    (hi - lo))).  A dense root's ``val`` holds hi - lo values (index lo + i
+    at i); a sparse root's ``idx`` holds absolute indices."""
+    return _reduce(idx, vals, N, (lo, hi), delta, codes, scales, qbits, node_info, ws, out_idx, out_val)
+
+
+def _reduce(idx, vals, N, rng, delta, codes, scales, qbits, node_info, ws, out_idx, out_val):
     torch = _torch()
     P = len(idx)
     dev = idx[0].device
@@ -229,24 +246,30 @@ def sparse_reduce(idx, vals, N: int, delta: float, codes=None, scales=None, qbit
     else:
         arr = make_streams(idx, vals)
     nnz = [t.numel() for t in idx]
-    thr = int(float(delta) * float(N) // 1)
+    R = N if rng is None else rng[1] - rng[0]
+    thr = int(float(delta) * float(R) // 1)
     cap = max(1, min(thr, sum(nnz)) if P > 1 else max(nnz[0], 1))
     if out_idx is None:
         out_idx = torch.empty(cap, dtype=torch.int32, device=dev)
     if out_val is None:
-        out_val = torch.empty(N, dtype=torch.float32, device=dev)
+        out_val = torch.empty(R, dtype=torch.float32, device=dev)
     out = Stream(_ptr(out_idx), _ptr(out_val), None, None, out_idx.numel(), 0, 0)
     node_nnz = node_dense = None
     if node_info and P > 1:
         node_nnz = torch.empty(P - 1, dtype=torch.int64, device=dev)
         node_dense = torch.empty(P - 1, dtype=torch.uint8, device=dev)
-    nbytes = workspace_size(OP_REDUCE, P, N, max(nnz), delta)
+    nbytes = workspace_size(OP_REDUCE, P, R, min(max(nnz), R), delta)
     if ws is None or ws.numel() < nbytes:
         ws = alloc_workspace(nbytes, dev)
-    _check(lib().sparcml_sparse_reduce(P, arr, N, float(delta), ctypes.byref(out),
-                                       _ptr(node_nnz), _ptr(node_dense), _ptr(ws), ws.numel(),
-                                       _stream_ptr(dev)),
-           "sparcml_sparse_reduce")
+    if rng is None:
+        rc = lib().sparcml_sparse_reduce(P, arr, N, float(delta), ctypes.byref(out), _ptr(node_nnz),
+                                         _ptr(node_dense), _ptr(ws), ws.numel(), _stream_ptr(dev))
+        _check(rc, "sparcml_sparse_reduce")
+    else:
+        rc = lib().sparcml_sparse_reduce_range(P, arr, N, rng[0], rng[1], float(delta), ctypes.byref(out),
+                                               _ptr(node_nnz), _ptr(node_dense), _ptr(ws), ws.numel(),
+                                               _stream_ptr(dev))
+        _check(rc, "sparcml_sparse_reduce_range")
     n = int(out.nnz)
     dense = bool(out.is_dense)
     return {
@@ -306,9 +329,13 @@ class ReduceCall:
     """Repeated sparse reduce of fixed device streams into fixed outputs."""
 
     def __init__(self, idx, N: int, delta: float, vals=None, codes=None, scales=None,
-                 qbits: int = 0, node_info: bool = False):
+                 qbits: int = 0, node_info: bool = False, lo: int | None = None, hi: int | None = None):
+        """``lo``, ``hi``: reduce the index range [lo, hi) (the split-phase
+        share) instead of the whole vector."""
         self.P = len(idx)
         self.N, self.delta = N, float(delta)
+        self.rng = None if lo is None else (int(lo), int(hi))
+        R = N if self.rng is None else self.rng[1] - self.rng[0]
         self.dev = idx[0].device
         torch = _torch()
         if qbits:
@@ -317,15 +344,15 @@ class ReduceCall:
         else:
             self.arr = make_streams(idx, vals)
         nnz = [t.numel() for t in idx]
-        thr = int(self.delta * float(N) // 1)
+        thr = int(self.delta * float(R) // 1)
         cap = max(1, min(thr, sum(nnz)) if self.P > 1 else max(nnz[0], 1))
         self.out_idx = torch.empty(cap, dtype=torch.int32, device=self.dev)
-        self.out_val = torch.empty(N, dtype=torch.float32, device=self.dev)
+        self.out_val = torch.empty(R, dtype=torch.float32, device=self.dev)
         self.node_nnz = self.node_dense = None
         if node_info and self.P > 1:
             self.node_nnz = torch.empty(self.P - 1, dtype=torch.int64, device=self.dev)
             self.node_dense = torch.empty(self.P - 1, dtype=torch.uint8, device=self.dev)
-        nbytes = workspace_size(OP_REDUCE, self.P, N, max(nnz), self.delta)
+        nbytes = workspace_size(OP_REDUCE, self.P, R, min(max(nnz), R), self.delta)
         self.ws = alloc_workspace(nbytes, self.dev)
         self.out = Stream(_ptr(self.out_idx), _ptr(self.out_val), None, None, self.out_idx.numel(), 0, 0)
         self._keep = (idx, vals, codes, scales)
@@ -333,10 +360,16 @@ class ReduceCall:
     def run(self):
         """Returns (nnz, dense)."""
         self.out.nnz = self.out_idx.numel()
-        _check(lib().sparcml_sparse_reduce(
-            self.P, self.arr, self.N, self.delta, ctypes.byref(self.out), _ptr(self.node_nnz),
-            _ptr(self.node_dense), _ptr(self.ws), self.ws.numel(), _stream_ptr(self.dev)),
-            "sparcml_sparse_reduce")
+        if self.rng is None:
+            _check(lib().sparcml_sparse_reduce(
+                self.P, self.arr, self.N, self.delta, ctypes.byref(self.out), _ptr(self.node_nnz),
+                _ptr(self.node_dense), _ptr(self.ws), self.ws.numel(), _stream_ptr(self.dev)),
+                "sparcml_sparse_reduce")
+        else:
+            _check(lib().sparcml_sparse_reduce_range(
+                self.P, self.arr, self.N, self.rng[0], self.rng[1], self.delta, ctypes.byref(self.out),
+                _ptr(self.node_nnz), _ptr(self.node_dense), _ptr(self.ws), self.ws.numel(),
+                _stream_ptr(self.dev)), "sparcml_sparse_reduce_range")
         return int(self.out.nnz), bool(self.out.is_dense)
 
 

@@ -36,16 +36,18 @@ def to_np(t, dtype=None) -> np.ndarray:
     return a
 
 
-def gpu_reduce(idx, val, N, delta, qbits=0, codes=None, scales=None, ws=None):
+def gpu_reduce(idx, val, N, delta, qbits=0, codes=None, scales=None, ws=None, rng=None):
+    """HIP sparse reduce through the C ABI; ``rng`` = (lo, hi) calls the
+    range entry point."""
     from paper_1802_08021_amd import sparcml as S
     torch, dev = torch_dev()
     ti = [to_dev(a) for a in idx]
-    if qbits:
-        r = S.sparse_reduce(ti, None, N, delta, codes=codes, scales=scales, qbits=qbits,
-                            node_info=True, ws=ws)
+    tv = None if qbits else [to_dev(v) for v in val]
+    kw = dict(codes=codes, scales=scales, qbits=qbits, node_info=True, ws=ws)
+    if rng is None:
+        r = S.sparse_reduce(ti, tv, N, delta, **kw)
     else:
-        tv = [to_dev(v) for v in val]
-        r = S.sparse_reduce(ti, tv, N, delta, node_info=True, ws=ws)
+        r = S.sparse_reduce_range(ti, tv, N, rng[0], rng[1], delta, **kw)
     torch.cuda.synchronize()
     P = len(idx)
     return {

@@ -22,7 +22,7 @@ def declared_symbols():
 def test_header_declares_the_boundary():
     syms = declared_symbols()
     for name in ("sparcml_topk_sparsify", "sparcml_quantize", "sparcml_sparse_reduce",
-                 "sparcml_densify", "sparcml_workspace_size", "sparcml_strerror",
+                 "sparcml_sparse_reduce_range", "sparcml_densify", "sparcml_workspace_size", "sparcml_strerror",
                  "sparcml_last_error"):
         assert name in syms
 
@@ -112,6 +112,28 @@ def test_reduce_argument_errors():
     out = S.Stream(FAKE, None, None, None, 100, 0, 0)
     assert reduce_rc(4, streams(4), out=out) == S.EINVAL  # out->val NULL
     assert "val" in S.last_error()
+
+
+def range_rc(P, arr, N=100, lo=0, hi=100, delta=0.5, out=None, ws=FAKE, ws_bytes=1 << 40):
+    if out is None:
+        out = S.Stream(FAKE, FAKE, None, None, 1 << 30, 0, 0)
+    return S.lib().sparcml_sparse_reduce_range(P, arr, N, lo, hi, delta, ctypes.byref(out), None,
+                                               None, ws, ws_bytes, None)
+
+
+def test_reduce_range_argument_errors():
+    assert range_rc(4, streams(4), lo=10, hi=10) == S.EINVAL   # empty range
+    assert range_rc(4, streams(4), lo=20, hi=10) == S.EINVAL
+    assert range_rc(4, streams(4), lo=0, hi=101) == S.EINVAL   # hi > N
+    assert range_rc(4, streams(4), N=0, lo=0, hi=0) == S.EINVAL
+    assert range_rc(4, streams(4), N=2**32, lo=0, hi=5) == S.EINVAL
+    assert range_rc(4, streams(4, nnz=11), lo=40, hi=50) == S.EINVAL  # nnz > hi - lo
+    assert "range" in S.last_error()
+    assert range_rc(3, streams(3), lo=0, hi=50) == S.EINVAL
+    # the capacity bound uses the range's threshold: floor(0.5 * 40) = 20 >= 16 entries
+    small = S.Stream(FAKE, FAKE, None, None, 15, 0, 0)
+    assert range_rc(4, streams(4), lo=30, hi=70, out=small) == S.ECAPACITY
+    assert range_rc(4, streams(4), lo=30, hi=70, ws_bytes=16) == S.EWORKSPACE
 
 
 def test_reduce_capacity_and_workspace_errors():

@@ -325,6 +325,73 @@ def test_reduce_single_rank():
     np.testing.assert_array_equal(r["val"], ref)
 
 
+def test_reduce_range_vs_brute_force():
+    """§5.3.2 split phase: a share is the tree sum of the full P x N matrix
+    restricted to the columns [lo, hi), with the switch rule applied to the
+    range's own index sets and threshold floor(delta * (hi - lo))."""
+    rng = np.random.default_rng(21)
+    for case in range(300):
+        P = int(rng.choice([1, 2, 4, 8]))
+        N = int(rng.integers(1, 80))
+        lo = int(rng.integers(0, N))
+        hi = int(rng.integers(lo + 1, N + 1))
+        delta = float(rng.choice([1e-9, 0.1, 0.3, 0.6, 1.0, 2.0]))
+        idx, val = [], []
+        for r in range(P):
+            k = int(rng.integers(0, N + 1))
+            idx.append(np.sort(rng.choice(N, size=k, replace=False)).astype(np.uint32))
+            val.append(inputs.normal(rng, k))
+        res = oracle.sparse_reduce_range(idx, val, N, lo, hi, delta)
+        full, _ = brute_tree(idx, val, N)
+        R = hi - lo
+        sets = [a[(a >= lo) & (a < hi)].astype(np.int64) - lo for a in idx]
+        bn, bd, broot = brute_decisions(sets, R, math.floor(delta * R))
+        assert res["dense"] == broot
+        assert res["node_nnz"].tolist() == bn
+        assert [bool(x) for x in res["node_dense"]] == bd
+        support = np.unique(np.concatenate(sets)) if P else np.zeros(0, np.int64)
+        if res["dense"]:
+            assert res["nnz"] == R and res["val"].size == R
+            np.testing.assert_array_equal(res["val"].view(np.uint32), full[lo:hi].view(np.uint32))
+        else:
+            np.testing.assert_array_equal(res["idx"].astype(np.int64), support + lo)
+            np.testing.assert_array_equal(res["val"].view(np.uint32),
+                                          full[support + lo].view(np.uint32))
+
+
+def test_split_allgather_equals_full_reduce():
+    """§5.3.2: gathering the P shares of an equal split of [0, N) gives the
+    allreduce result (as a dense vector; a sparse node stores no +0.0 for
+    absent indices, so values are compared with +0.0 == -0.0)."""
+    rng = np.random.default_rng(22)
+    for case in range(40):
+        P = int(rng.choice([2, 4, 8, 16]))
+        N = int(rng.integers(P, 400))
+        delta = float(rng.choice([0.01, 0.1, 0.5, 2.0]))
+        idx = [inputs.uniform_subset(rng, N, int(rng.integers(0, N // 2 + 1))) for _ in range(P)]
+        val = [inputs.normal(rng, a.size) for a in idx]
+        full = oracle.sparse_reduce(idx, val, N, delta)
+        ref = full["val"] if full["dense"] else oracle.densify(full["idx"], full["val"], N)
+        bounds = [N * s // P for s in range(P + 1)]
+        got = np.zeros(N, np.float32)
+        for s in range(P):
+            lo, hi = bounds[s], bounds[s + 1]
+            if lo == hi:
+                continue
+            sh = oracle.sparse_reduce_range(idx, val, N, lo, hi, delta)
+            if sh["dense"]:
+                got[lo:hi] = sh["val"]
+            else:
+                assert np.all((sh["idx"] >= lo) & (sh["idx"] < hi))
+                got[sh["idx"].astype(np.int64)] = sh["val"]
+        np.testing.assert_array_equal(got + np.float32(0), ref + np.float32(0))
+    # the whole range is the plain allreduce
+    r1 = oracle.sparse_reduce(idx, val, N, delta)
+    r2 = oracle.sparse_reduce_range(idx, val, N, 0, N, delta)
+    assert r1["dense"] == r2["dense"] and r1["nnz"] == r2["nnz"]
+    np.testing.assert_array_equal(r1["val"], r2["val"])
+
+
 def test_reduce_rejects_bad_input():
     N = 10
     good = [np.array([1, 2], np.uint32)] * 2
