@@ -8,12 +8,15 @@
  *   sparcml_topk_sparsify  -- top-k sparsification of dense gradients
  *                             (§2.2 "Structured Sparsification", Alg. 1)
  *   sparcml_quantize       -- QSGD stochastic quantization (§2.2, §6)
+ *   sparcml_quantize_bucketed -- QSGD in buckets of B entries (§6)
  *   sparcml_sparse_reduce  -- sum of P sparse streams in recursive-doubling
  *                             order with the sparse->dense switch
  *                             (§5.1, §5.3.1, Fig. 2)
  *   sparcml_sparse_reduce_range -- the same over one index range: a node's
  *                             share of the split phase of the large-data
  *                             allreduce (§5.3.2)
+ *   sparcml_concat         -- gathered shares summed as a concatenation
+ *                             (§5.1 case (2), §5.3.2), QSGD parts decoded
  *   sparcml_densify        -- dense representation of one stream (§5.1)
  *
  * Conventions shared by every call:
@@ -63,6 +66,8 @@ extern "C" {
 #define SPARCML_OP_QUANTIZE 2
 #define SPARCML_OP_REDUCE 3
 #define SPARCML_OP_DENSIFY 4
+#define SPARCML_OP_QUANTIZE_BUCKETED 5
+#define SPARCML_OP_CONCAT 6
 
 /*
  * Sparse stream (§5.1 "Vector Representations" and "Switching to a Dense
@@ -94,7 +99,7 @@ typedef struct sparcml_stream {
  *   P        number of ranks (streams / rows).
  *   N        dimension.
  *   max_nnz  TOPK: k; QUANTIZE: largest stream length; REDUCE: largest
- *            input stream nnz; DENSIFY: ignored.
+ *            input stream nnz; DENSIFY, QUANTIZE_BUCKETED, CONCAT: ignored.
  *   delta    REDUCE only (switch threshold as a fraction of N).
  * A workspace sized with max_nnz >= the actual largest nnz is sufficient.
  * Returns SPARCML_OK and *bytes, or SPARCML_EINVAL.
@@ -150,6 +155,27 @@ SPARCML_API int sparcml_topk_sparsify(int P, const float* x, uint64_t N, uint64_
 SPARCML_API int sparcml_quantize(int P, const sparcml_stream* in, int bits, uint64_t seed,
                      uint8_t* const* out_q, float* out_scale, float* const* out_deq,
                      void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Bucketed QSGD (§6 "Supporting Low-Precision Communication": a stream is
+ * split into buckets of B consecutive entries, each quantized on its own
+ * with a full-precision scale; the paper uses B in the order of 1024 and
+ * applies it to the dense stage of the split-allgather allreduce).  Per
+ * bucket exactly as sparcml_quantize per stream: scale = the bucket's L2
+ * norm (fp64 adjacent-pair tree over its B entries, zeros past the stream's
+ * end, one rounding to fp32), the same levels, codes and random draws
+ * (element j of stream r: Philox word j&3 of counter (j>>2, r, 0, 0)).
+ * One pass: each value is read once and its code written once.
+ *   bucket   B, a power of two in [4, 8192].
+ *   out_scale device fp32 array, flat: stream r's ceil(nnz_r / B) scales
+ *            (in bucket order) follow those of streams 0..r-1.
+ *   Other arguments as for sparcml_quantize.
+ *   ws       sparcml_workspace_size(SPARCML_OP_QUANTIZE_BUCKETED, P, ...).
+ * Errors: EINVAL (also for a bad bucket), EWORKSPACE, EHIP.
+ */
+SPARCML_API int sparcml_quantize_bucketed(int P, const sparcml_stream* in, int bits, uint64_t bucket,
+                              uint64_t seed, uint8_t* const* out_q, float* out_scale,
+                              float* const* out_deq, void* ws, size_t ws_bytes, void* stream);
 
 /*
  * Sparse allreduce of P streams, one GPU's share: the sum of all ranks'
@@ -215,6 +241,40 @@ SPARCML_API int sparcml_sparse_reduce_range(int P, const sparcml_stream* streams
                                 size_t ws_bytes, void* stream);
 
 /*
+ * The allgather phase of the split-allgather allreduce (§5.3.2), the local
+ * part: the sum of P parts with disjoint index ranges, which is their
+ * concatenation (§5.1, case (2)).  Part s covers [bounds[s], bounds[s+1]).
+ * The result is dense if a part is dense or the parts hold more than
+ * thr = floor(delta * N) entries together (the representation rule of
+ * §5.1); a dense result is +0.0 where no part has an entry.  QSGD-coded
+ * parts (§6: DSAR's dense stage is sent quantized) are dequantized.
+ *   P        1 <= P <= 65535.
+ *   parts    host array of P descriptors, all with the same qbits.  Sparse
+ *            part: nnz <= its range's length, absolute indices strictly
+ *            ascending inside the range (not checked).  Dense part
+ *            (is_dense): nnz == its range's length, value i is index
+ *            bounds[s] + i.  qbits != 0: codes in qval; qscale holds one
+ *            scale (bucket == 0) or ceil(nnz / bucket) scales, entry i of
+ *            the part using scale i / bucket.
+ *   bounds   host array of P + 1: bounds[0] == 0, bounds[P] == N, not
+ *            decreasing (empty ranges allowed).
+ *   N, delta 1 <= N < 2^32, delta > 0.
+ *   bucket   0 or a power of two in [4, 8192] (read only when qbits != 0).
+ *   out      in: out->val (N floats), out->idx (capacity out->nnz entries,
+ *            at least the parts' total when the result stays sparse),
+ *            out->qbits == 0.  out: out->nnz (N if dense), out->is_dense; a
+ *            sparse result is the parts' entries in part order (ascending),
+ *            values in fp32.
+ *   ws       sparcml_workspace_size(SPARCML_OP_CONCAT, P, ...).
+ * The representation is decided on the host from the descriptors; the call
+ * does not synchronize.
+ * Errors: EINVAL, ECAPACITY, EWORKSPACE, EHIP.
+ */
+SPARCML_API int sparcml_concat(int P, const sparcml_stream* parts, const uint64_t* bounds, uint64_t N,
+                   double delta, uint64_t bucket, sparcml_stream* out, void* ws, size_t ws_bytes,
+                   void* stream);
+
+/*
  * Dense representation of one stream (§5.1): dense[j] = value of index j,
  * +0.0 where absent; dequantizes QSGD codes on the fly.  A dense input is
  * copied (or dequantized).  Writes all N floats.  Indices must be strictly
@@ -243,6 +303,7 @@ SPARCML_API int sparcml_densify(const sparcml_stream* in, uint64_t N, float* den
 #define SPARCML_TIMER_TOPK_SELECT 5  /* top-k radix-select histogram passes */
 #define SPARCML_TIMER_TOPK_WRITE 6   /* top-k count, scan and write */
 #define SPARCML_TIMER_DENSIFY 7
+#define SPARCML_TIMER_CONCAT 8
 SPARCML_API int sparcml_timing_enable(int on);
 SPARCML_API int sparcml_timing_read(int group, float* ms);
 

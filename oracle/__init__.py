@@ -10,6 +10,9 @@ Functions follow the paper:
                           §5.3.1 recursive doubling order.
   * ``sparse_reduce_range`` -- one node's share of the split phase of the
                           large-data allreduce (§5.3.2).
+  * ``concat``         -- the gathered shares summed as a concatenation
+                          (§5.1 case (2), §5.3.2 allgather phase, §6 dense
+                          stage in QSGD buckets).
   * ``topk``           -- §2.2 Top-k sparsification, Alg. 1 error update.
   * ``quantize``       -- §2.2 / §6 QSGD stochastic quantization.
   * ``dequantize``, ``densify``, ``philox4x32_10``.
@@ -62,6 +65,11 @@ def lib():
         L.orc_quantize.restype = ctypes.c_int
         L.orc_dequantize.argtypes = [vp, ctypes.c_float, ctypes.c_int, ctypes.c_uint64, vp]
         L.orc_dequantize.restype = ctypes.c_int
+        L.orc_quantize_bucketed.argtypes = [ctypes.c_int, vp, vp, ctypes.c_int, ctypes.c_uint64,
+                                            ctypes.c_uint64, vp, vp, vp]
+        L.orc_quantize_bucketed.restype = ctypes.c_int
+        L.orc_dequantize_bucketed.argtypes = [vp, vp, ctypes.c_int, ctypes.c_uint64, ctypes.c_uint64, vp]
+        L.orc_dequantize_bucketed.restype = ctypes.c_int
         L.orc_densify.argtypes = [vp, vp, ctypes.c_uint64, ctypes.c_uint64, vp]
         L.orc_densify.restype = ctypes.c_int
         _lib = L
@@ -152,6 +160,60 @@ def sparse_reduce_range(idx_list, val_list, N: int, lo: int, hi: int, delta: flo
     return res
 
 
+def part_values(part) -> np.ndarray:
+    """Stored values of one part: fp32 as given, or QSGD codes dequantized
+    with one scale (``bucket`` 0) or one per ``bucket`` entries (§6)."""
+    if part.get("qbits", 0):
+        n = part["n"]
+        return dequantize(part["codes"], part["scales"] if part.get("bucket", 0) else part["scales"][0],
+                          part["qbits"], n, bucket=part.get("bucket", 0))
+    return np.asarray(part["val"], dtype=np.float32)
+
+
+def concat(parts, bounds, N: int, delta: float):
+    """Sum of P vectors with disjoint index ranges, part s covering
+    [bounds[s], bounds[s+1]) -- the gathered shares of the split-allgather
+    allreduce (§5.3.2).  Disjoint index sets make the sum a concatenation
+    (§5.1, case (2)).  A part is sparse (``idx`` absolute, ascending, in its
+    range; values) or dense (its range's values, ``idx`` None), with fp32
+    values or QSGD codes (§6).  The result is dense if a part is dense or
+    the parts hold more than thr = floor(delta * N) entries together (the
+    representation rule of §5.1); then every index without an entry is
+    +0.0.  Returns dict(idx, val, nnz, dense)."""
+    P = len(parts)
+    if len(bounds) != P + 1 or bounds[0] != 0 or bounds[-1] != N or any(
+            bounds[s] > bounds[s + 1] for s in range(P)):
+        raise OracleError("bounds must rise from 0 to N")
+    total = 0
+    any_dense = False
+    for s, part in enumerate(parts):
+        lo, hi = bounds[s], bounds[s + 1]
+        if part["idx"] is None:
+            any_dense = True
+            if len(part_values(part)) != hi - lo:
+                raise OracleError(f"dense part {s} must hold {hi - lo} values")
+        else:
+            a = np.asarray(part["idx"], dtype=np.int64)
+            if a.size and (a[0] < lo or a[-1] >= hi or np.any(np.diff(a) <= 0)):
+                raise OracleError(f"part {s}: indices must ascend inside [{lo}, {hi})")
+            total += a.size
+    thr = threshold(N, delta)
+    if any_dense or total > thr:
+        out = np.zeros(N, dtype=np.float32)
+        for s, part in enumerate(parts):
+            v = part_values(part)
+            if part["idx"] is None:
+                out[bounds[s]: bounds[s + 1]] = v
+            else:
+                out[np.asarray(part["idx"], dtype=np.int64)] = v
+        return {"idx": None, "val": out, "nnz": N, "dense": True}
+    idx = [np.asarray(p["idx"], dtype=np.uint32) for p in parts]
+    val = [part_values(p) for p in parts]
+    return {"idx": np.concatenate(idx) if idx else np.zeros(0, np.uint32),
+            "val": np.concatenate(val) if val else np.zeros(0, np.float32),
+            "nnz": total, "dense": False}
+
+
 def topk(x: np.ndarray, k: int, residual: bool = False):
     """Exact per-row top-k by magnitude of x[P, N] by a full sort."""
     x = np.ascontiguousarray(x, dtype=np.float32)
@@ -166,28 +228,43 @@ def topk(x: np.ndarray, k: int, residual: bool = False):
     return out_idx[:, :k].copy(), out_val[:, :k].copy(), res
 
 
-def quantize(val_list, bits: int, seed: int):
-    """QSGD per stream.  Returns (codes list, scales[P], dequantized list)."""
+def scale_counts(sizes, bucket: int):
+    """Scales per stream: ceil(n / bucket), or 1 when bucket == 0."""
+    return [(n + bucket - 1) // bucket if bucket else 1 for n in sizes]
+
+
+def quantize(val_list, bits: int, seed: int, bucket: int = 0):
+    """QSGD per stream (bucket = 0: one scale per stream) or in buckets of
+    ``bucket`` consecutive entries (§6).  Returns (codes list, flat scales,
+    dequantized list); stream r's scales follow those of streams 0..r-1."""
     P = len(val_list)
     val_list = [np.ascontiguousarray(a, dtype=np.float32) for a in val_list]
     nnz = np.array([a.size for a in val_list], dtype=np.uint64)
     per_byte = 8 // bits
     q = [np.zeros(max((a.size + per_byte - 1) // per_byte, 1), dtype=np.uint8) for a in val_list]
     deq = [np.zeros(max(a.size, 1), dtype=np.float32) for a in val_list]
-    scale = np.zeros(P, dtype=np.float32)
-    rc = lib().orc_quantize(P, _ptr_table(val_list), nnz.ctypes.data, bits, seed & (2**64 - 1),
-                            _ptr_table(q), scale.ctypes.data, _ptr_table(deq))
+    scale = np.zeros(max(sum(scale_counts([a.size for a in val_list], bucket)), 1), dtype=np.float32)
+    rc = lib().orc_quantize_bucketed(P, _ptr_table(val_list), nnz.ctypes.data, bits, bucket,
+                                     seed & (2**64 - 1), _ptr_table(q), scale.ctypes.data,
+                                     _ptr_table(deq))
     if rc != 0:
-        raise OracleError(f"orc_quantize returned {rc}")
+        raise OracleError(f"orc_quantize_bucketed returned {rc}")
+    scale = scale[: sum(scale_counts([a.size for a in val_list], bucket))]
     nb = [(a.size + per_byte - 1) // per_byte for a in val_list]
     return ([qq[:n].copy() for qq, n in zip(q, nb)], scale,
             [d[: a.size].copy() for d, a in zip(deq, val_list)])
 
 
-def dequantize(q: np.ndarray, scale: float, bits: int, n: int) -> np.ndarray:
+def dequantize(q: np.ndarray, scale, bits: int, n: int, bucket: int = 0) -> np.ndarray:
+    """Values of n packed codes: one scale (bucket = 0) or scales[j // bucket]."""
     q = np.ascontiguousarray(q, dtype=np.uint8)
     out = np.zeros(max(n, 1), dtype=np.float32)
-    rc = lib().orc_dequantize(_ptr(q), ctypes.c_float(scale), bits, n, out.ctypes.data)
+    if bucket:
+        sc = np.ascontiguousarray(scale, dtype=np.float32)
+        rc = lib().orc_dequantize_bucketed(_ptr(q), _ptr(sc), bits, bucket, n, out.ctypes.data)
+    else:
+        rc = lib().orc_dequantize(_ptr(q), ctypes.c_float(float(np.float32(scale))), bits, n,
+                                  out.ctypes.data)
     if rc != 0:
         raise OracleError(f"orc_dequantize returned {rc}")
     return out[:n].copy()

@@ -310,80 +310,116 @@ int orc_topk(int P, const float* x, uint64_t N, uint64_t k,
 
 static int valid_bits(int bits) { return bits == 2 || bits == 4 || bits == 8; }
 
-int orc_quantize(int P, const float* const* val, const uint64_t* nnz, int bits,
-                 uint64_t seed, uint8_t* const* out_q, float* out_scale,
-                 float* const* out_deq)
+/* L2 norm of v[0..n): squares summed by an adjacent-pair binary tree in
+ * fp64, zero-padded to a power of two, rounded once to fp32. */
+static int l2_scale(const float* v, uint64_t n, float* scale)
 {
-    if (P < 1 || !valid_bits(bits) || !val || !nnz || !out_q || !out_scale) return -1;
+    uint64_t m = 1;
+    while (m < n) m <<= 1;
+    double* t = (double*)calloc(m, sizeof(double));
+    if (!t) return -4;
+    for (uint64_t j = 0; j < n; ++j) t[j] = (double)v[j] * (double)v[j];
+    for (uint64_t w = m; w > 1; w >>= 1)
+        for (uint64_t i = 0; i < w / 2; ++i) t[i] = t[2 * i] + t[2 * i + 1];
+    double norm2 = n ? t[0] : 0.0;
+    free(t);
+    *scale = (float)sqrt(norm2);
+    return 0;
+}
+
+/* Quantize elements j0 .. j0+n-1 of stream r (v points at element j0) with
+ * one scale: codes OR-ed into q (zeroed by the caller), deq may be NULL. */
+static void quantize_span(const float* v, uint64_t j0, uint64_t n, int r, int bits,
+                          const uint32_t key[2], float scale, uint8_t* q, float* deq)
+{
     const uint32_t s = (1u << (bits - 1)) - 1u; /* magnitude levels 0..s */
     const int per_byte = 8 / bits;
+    if (scale == 0.0f) {
+        if (deq)
+            for (uint64_t i = 0; i < n; ++i) deq[j0 + i] = 0.0f;
+        return; /* every code is 0 */
+    }
+    const float inv = (float)s / scale;  /* levels per unit of norm */
+    const float unit = scale / (float)s; /* value of one level */
+    for (uint64_t i = 0; i < n; ++i) {
+        const uint64_t j = j0 + i;
+        float a = fabsf(v[i]) * inv;
+        uint32_t l = (uint32_t)a; /* floor, a >= 0 */
+        float f = a - (float)l;   /* exact */
+        uint32_t ctr[4] = {(uint32_t)(j >> 2), (uint32_t)r, 0u, 0u};
+        uint32_t word[4];
+        orc_philox4x32_10(ctr, key, word);
+        float u = (float)(word[j & 3] >> 8) * 0x1p-24f; /* uniform [0,1) */
+        if (u < f) l += 1u; /* round up with probability f */
+        if (l > s) l = s;
+        uint32_t sign = (v[i] < 0.0f && l > 0u) ? 1u : 0u;
+        uint32_t code = (sign << (bits - 1)) | l;
+        q[j / per_byte] |= (uint8_t)(code << ((j % per_byte) * bits));
+        if (deq) {
+            float mag = (float)l * unit;
+            deq[j] = l == 0u ? 0.0f : (sign ? -mag : mag);
+        }
+    }
+}
+
+int orc_quantize_bucketed(int P, const float* const* val, const uint64_t* nnz, int bits,
+                          uint64_t bucket, uint64_t seed, uint8_t* const* out_q,
+                          float* out_scale, float* const* out_deq)
+{
+    if (P < 1 || !valid_bits(bits) || !val || !nnz || !out_q || !out_scale) return -1;
+    const int per_byte = 8 / bits;
     const uint32_t key[2] = {(uint32_t)(seed & 0xFFFFFFFFu), (uint32_t)(seed >> 32)};
+    uint64_t so = 0; /* first scale of stream r */
     for (int r = 0; r < P; ++r) {
         const uint64_t n = nnz[r];
         const float* v = val[r];
         uint8_t* q = out_q[r];
         if (n && (!v || !q)) return -1;
-
-        /* L2 norm: squares summed by an adjacent-pair binary tree in fp64,
-         * zero-padded to a power of two. */
-        uint64_t m = 1;
-        while (m < n) m <<= 1;
-        double* t = (double*)calloc(m, sizeof(double));
-        if (!t) return -4;
-        for (uint64_t j = 0; j < n; ++j) t[j] = (double)v[j] * (double)v[j];
-        for (uint64_t w = m; w > 1; w >>= 1)
-            for (uint64_t i = 0; i < w / 2; ++i) t[i] = t[2 * i] + t[2 * i + 1];
-        double norm2 = n ? t[0] : 0.0;
-        free(t);
-        float scale = (float)sqrt(norm2);
-        out_scale[r] = scale;
-
-        uint64_t nbytes = (n + per_byte - 1) / per_byte;
+        const uint64_t nbytes = (n + per_byte - 1) / per_byte;
         if (nbytes) memset(q, 0, nbytes);
         float* deq = out_deq ? out_deq[r] : NULL;
-        if (scale == 0.0f) {
-            if (deq)
-                for (uint64_t j = 0; j < n; ++j) deq[j] = 0.0f;
-            continue;
+        const uint64_t B = bucket ? bucket : (n ? n : 1);
+        const uint64_t nb = bucket ? (n + B - 1) / B : 1;
+        for (uint64_t b = 0; b < nb; ++b) {
+            const uint64_t j0 = b * B;
+            const uint64_t len = n - j0 < B ? n - j0 : B;
+            float scale;
+            if (l2_scale(v + j0, len, &scale)) return -4;
+            out_scale[so + b] = scale;
+            quantize_span(v + j0, j0, len, r, bits, key, scale, q, deq);
         }
-        const float inv = (float)s / scale;  /* levels per unit of norm */
-        const float unit = scale / (float)s; /* value of one level */
-        for (uint64_t j = 0; j < n; ++j) {
-            float a = fabsf(v[j]) * inv;
-            uint32_t l = (uint32_t)a; /* floor, a >= 0 */
-            float f = a - (float)l;   /* exact */
-            uint32_t ctr[4] = {(uint32_t)(j >> 2), (uint32_t)r, 0u, 0u};
-            uint32_t word[4];
-            orc_philox4x32_10(ctr, key, word);
-            float u = (float)(word[j & 3] >> 8) * 0x1p-24f; /* uniform [0,1) */
-            if (u < f) l += 1u; /* round up with probability f */
-            if (l > s) l = s;
-            uint32_t sign = (v[j] < 0.0f && l > 0u) ? 1u : 0u;
-            uint32_t code = (sign << (bits - 1)) | l;
-            q[j / per_byte] |= (uint8_t)(code << ((j % per_byte) * bits));
-            if (deq) {
-                float mag = (float)l * unit;
-                deq[j] = l == 0u ? 0.0f : (sign ? -mag : mag);
-            }
-        }
+        so += nb;
     }
     return 0;
 }
 
-int orc_dequantize(const uint8_t* q, float scale, int bits, uint64_t n, float* out)
+int orc_quantize(int P, const float* const* val, const uint64_t* nnz, int bits,
+                 uint64_t seed, uint8_t* const* out_q, float* out_scale,
+                 float* const* out_deq)
 {
-    if (!valid_bits(bits) || (n && (!q || !out))) return -1;
+    return orc_quantize_bucketed(P, val, nnz, bits, 0, seed, out_q, out_scale, out_deq);
+}
+
+int orc_dequantize_bucketed(const uint8_t* q, const float* scales, int bits, uint64_t bucket,
+                            uint64_t n, float* out)
+{
+    if (!valid_bits(bits) || (n && (!q || !out || !scales))) return -1;
     const uint32_t s = (1u << (bits - 1)) - 1u;
     const int per_byte = 8 / bits;
     const uint32_t lmask = s, smask = 1u << (bits - 1);
-    const float unit = scale / (float)s;
     for (uint64_t j = 0; j < n; ++j) {
+        const float unit = scales[bucket ? j / bucket : 0] / (float)s;
         uint32_t code = (q[j / per_byte] >> ((j % per_byte) * bits)) & ((1u << bits) - 1u);
         uint32_t l = code & lmask;
         float mag = (float)l * unit;
         out[j] = l == 0u ? 0.0f : ((code & smask) ? -mag : mag);
     }
     return 0;
+}
+
+int orc_dequantize(const uint8_t* q, float scale, int bits, uint64_t n, float* out)
+{
+    return orc_dequantize_bucketed(q, &scale, bits, 0, n, out);
 }
 
 /* ------------------------------------------------------------------------ */

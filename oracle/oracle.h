@@ -59,8 +59,23 @@ int orc_quantize(int P, const float* const* val, const uint64_t* nnz, int bits,
                  uint64_t seed, uint8_t* const* out_q, float* out_scale,
                  float* const* out_deq);
 
+/* Bucketed QSGD (SparCML §6: each stream split into buckets of B
+ * consecutive entries, each quantized with its own scale, the bucket's L2
+ * norm).  bucket = B >= 1, or 0 for one bucket per stream (orc_quantize).
+ * Scales are flat: stream r's ceil(n_r/B) scales (1 when bucket = 0) follow
+ * those of streams 0..r-1.  Random draws as in orc_quantize (by the
+ * element's position in its stream). */
+int orc_quantize_bucketed(int P, const float* const* val, const uint64_t* nnz, int bits,
+                          uint64_t bucket, uint64_t seed, uint8_t* const* out_q,
+                          float* out_scale, float* const* out_deq);
+
 /* Dequantize n packed codes with the given scale (inverse of the above). */
 int orc_dequantize(const uint8_t* q, float scale, int bits, uint64_t n, float* out);
+
+/* Dequantize n packed codes of one stream quantized in buckets of B (scale
+ * of element j: scales[j / B]; bucket = 0: scales[0] for all). */
+int orc_dequantize_bucketed(const uint8_t* q, const float* scales, int bits, uint64_t bucket,
+                            uint64_t n, float* out);
 
 /* Dense representation of one sparse stream: D = 0, D[idx[i]] = val[i]. */
 int orc_densify(const uint32_t* idx, const float* val, uint64_t nnz, uint64_t N,

@@ -63,6 +63,29 @@ int reduce_validate(int P, const sparcml_stream* streams, uint64_t N, double del
     return SPARCML_OK;
 }
 
+bool valid_bucket(uint64_t b) { return b >= 4 && b <= 8192 && (b & (b - 1)) == 0; }
+
+// Shared argument checks of the QSGD entry points.
+int quant_validate(int P, const sparcml_stream* in, int bits, uint8_t* const* out_q, float* out_scale,
+                   std::vector<const float*>* vals, std::vector<uint64_t>* n, uint64_t* max_n)
+{
+    if (P < 1) return fail(SPARCML_EINVAL, "P must be >= 1");
+    if (!valid_bits((uint32_t)bits)) return fail(SPARCML_EINVAL, "bits must be 2, 4 or 8");
+    if (!in || !out_q || !out_scale) return fail(SPARCML_EINVAL, "NULL argument");
+    vals->assign(P, nullptr);
+    n->assign(P, 0);
+    *max_n = 0;
+    for (int r = 0; r < P; ++r) {
+        if (in[r].qbits) return fail(SPARCML_EINVAL, "stream %d: input must hold fp32 values", r);
+        if (in[r].nnz >= (1ull << 40)) return fail(SPARCML_EINVAL, "stream %d: too long", r);
+        if (in[r].nnz && (!in[r].val || !out_q[r])) return fail(SPARCML_EINVAL, "stream %d: NULL pointer", r);
+        (*vals)[r] = in[r].val;
+        (*n)[r] = in[r].nnz;
+        *max_n = std::max(*max_n, (*n)[r]);
+    }
+    return SPARCML_OK;
+}
+
 uint64_t threshold(uint64_t N, double delta)
 {
     const double t = floor(delta * (double)N);
@@ -180,6 +203,14 @@ int sparcml_workspace_size(int op, int P, uint64_t N, uint64_t max_nnz, double d
         if (P < 1) return fail(SPARCML_EINVAL, "P must be >= 1");
         *bytes = quant_workspace(P, max_nnz);
         return SPARCML_OK;
+    case SPARCML_OP_QUANTIZE_BUCKETED:
+        if (P < 1) return fail(SPARCML_EINVAL, "P must be >= 1");
+        *bytes = quant_buckets_workspace(P);
+        return SPARCML_OK;
+    case SPARCML_OP_CONCAT:
+        if (P < 1 || P > 65535) return fail(SPARCML_EINVAL, "P must be in [1, 65535]");
+        *bytes = concat_workspace(P);
+        return SPARCML_OK;
     case SPARCML_OP_REDUCE: {
         if (!is_pow2(P) || P > 256 || !valid_n(N) || !(delta > 0.0) || max_nnz > N)
             return fail(SPARCML_EINVAL, "bad reduce sizes");
@@ -221,25 +252,38 @@ int sparcml_quantize(int P, const sparcml_stream* in, int bits, uint64_t seed, u
                      float* out_scale, float* const* out_deq, void* ws, size_t ws_bytes, void* stream)
 {
     try {
-        if (P < 1) return fail(SPARCML_EINVAL, "P must be >= 1");
-        if (!valid_bits((uint32_t)bits)) return fail(SPARCML_EINVAL, "bits must be 2, 4 or 8");
-        if (!in || !out_q || !out_scale) return fail(SPARCML_EINVAL, "NULL argument");
-        std::vector<const float*> vals(P);
-        std::vector<uint64_t> n(P);
+        std::vector<const float*> vals;
+        std::vector<uint64_t> n;
         uint64_t max_n = 0;
-        for (int r = 0; r < P; ++r) {
-            if (in[r].qbits) return fail(SPARCML_EINVAL, "stream %d: input must hold fp32 values", r);
-            if (in[r].nnz >= (1ull << 40)) return fail(SPARCML_EINVAL, "stream %d: too long", r);
-            if (in[r].nnz && (!in[r].val || !out_q[r])) return fail(SPARCML_EINVAL, "stream %d: NULL pointer", r);
-            vals[r] = in[r].val;
-            n[r] = in[r].nnz;
-            max_n = std::max(max_n, n[r]);
-        }
+        int rc = quant_validate(P, in, bits, out_q, out_scale, &vals, &n, &max_n);
+        if (rc) return rc;
         const size_t need = quant_workspace(P, max_n);
         if (!ws || ws_bytes < need) return fail(SPARCML_EWORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
         hipError_t e = quant_run(P, vals.data(), n.data(), bits, seed, out_q, out_scale, out_deq, ws,
                                  (hipStream_t)stream);
         if (e != hipSuccess) return hip_fail(e, "quantize");
+        return SPARCML_OK;
+    } catch (const std::exception& ex) {
+        return fail(SPARCML_EHIP, "host exception: %s", ex.what());
+    }
+}
+
+int sparcml_quantize_bucketed(int P, const sparcml_stream* in, int bits, uint64_t bucket, uint64_t seed,
+                              uint8_t* const* out_q, float* out_scale, float* const* out_deq, void* ws,
+                              size_t ws_bytes, void* stream)
+{
+    try {
+        std::vector<const float*> vals;
+        std::vector<uint64_t> n;
+        uint64_t max_n = 0;
+        int rc = quant_validate(P, in, bits, out_q, out_scale, &vals, &n, &max_n);
+        if (rc) return rc;
+        if (!valid_bucket(bucket)) return fail(SPARCML_EINVAL, "bucket must be a power of two in [4, 8192]");
+        const size_t need = quant_buckets_workspace(P);
+        if (!ws || ws_bytes < need) return fail(SPARCML_EWORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
+        hipError_t e = quant_buckets_run(P, vals.data(), n.data(), bits, (uint32_t)bucket, seed, out_q,
+                                         out_scale, out_deq, ws, (hipStream_t)stream);
+        if (e != hipSuccess) return hip_fail(e, "quantize_bucketed");
         return SPARCML_OK;
     } catch (const std::exception& ex) {
         return fail(SPARCML_EHIP, "host exception: %s", ex.what());
@@ -260,6 +304,59 @@ int sparcml_sparse_reduce_range(int P, const sparcml_stream* streams, uint64_t N
     if (!valid_n(N)) return fail(SPARCML_EINVAL, "N must be in [1, 2^32)");
     if (!(lo < hi && hi <= N)) return fail(SPARCML_EINVAL, "need 0 <= lo < hi <= N");
     return reduce_impl(P, streams, N, lo, hi, delta, out, node_nnz, node_dense, ws, ws_bytes, stream);
+}
+
+int sparcml_concat(int P, const sparcml_stream* parts, const uint64_t* bounds, uint64_t N, double delta,
+                   uint64_t bucket, sparcml_stream* out, void* ws, size_t ws_bytes, void* stream)
+{
+    try {
+        if (P < 1 || P > 65535) return fail(SPARCML_EINVAL, "P must be in [1, 65535]");
+        if (!valid_n(N)) return fail(SPARCML_EINVAL, "N must be in [1, 2^32)");
+        if (!(delta > 0.0) || isnan(delta)) return fail(SPARCML_EINVAL, "delta must be > 0");
+        if (!parts || !bounds || !out) return fail(SPARCML_EINVAL, "NULL argument");
+        if (bounds[0] != 0 || bounds[P] != N) return fail(SPARCML_EINVAL, "bounds must run from 0 to N");
+        if (bucket && !valid_bucket(bucket)) return fail(SPARCML_EINVAL, "bucket must be 0 or a power of two in [4, 8192]");
+        const uint32_t qbits = parts[0].qbits;
+        std::vector<ConcatPart> cp(P);
+        uint64_t total = 0;
+        bool any_dense = false;
+        for (int p = 0; p < P; ++p) {
+            const sparcml_stream& a = parts[p];
+            if (bounds[p + 1] < bounds[p]) return fail(SPARCML_EINVAL, "bounds must not decrease (part %d)", p);
+            const uint64_t len = bounds[p + 1] - bounds[p];
+            if (a.qbits != qbits) return fail(SPARCML_EINVAL, "part %d: all parts must share qbits", p);
+            if (qbits && !valid_bits(qbits)) return fail(SPARCML_EINVAL, "part %d: qbits must be 0, 2, 4 or 8", p);
+            if (a.is_dense ? a.nnz != len : a.nnz > len)
+                return fail(SPARCML_EINVAL, "part %d: %s", p, a.is_dense ? "a dense part holds its range's values"
+                                                                          : "more entries than its range has indices");
+            if (a.nnz) {
+                if (!a.is_dense && !a.idx) return fail(SPARCML_EINVAL, "part %d: idx is NULL", p);
+                if (qbits ? (!a.qval || !a.qscale) : !a.val) return fail(SPARCML_EINVAL, "part %d: values are NULL", p);
+            }
+            cp[p] = ConcatPart{a.idx, a.val, a.qval, a.qscale, a.nnz, bounds[p], len, a.is_dense ? 1 : 0};
+            any_dense = any_dense || a.is_dense;
+            total += a.nnz;
+        }
+        const bool dense = any_dense || total > threshold(N, delta);
+        if (!out->val) return fail(SPARCML_EINVAL, "out->val is NULL");
+        if (out->qbits) return fail(SPARCML_EINVAL, "out->qbits must be 0");
+        if (!dense) {
+            if (total && !out->idx) return fail(SPARCML_EINVAL, "out->idx is NULL");
+            if (out->nnz < total)
+                return fail(SPARCML_ECAPACITY, "out capacity %llu < %llu entries", (unsigned long long)out->nnz,
+                            (unsigned long long)total);
+        }
+        const size_t need = concat_workspace(P);
+        if (!ws || ws_bytes < need) return fail(SPARCML_EWORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
+        hipError_t e = concat_run(P, cp.data(), qbits, bucket, dense ? 1 : 0, out->idx, out->val, ws,
+                                  (hipStream_t)stream);
+        if (e != hipSuccess) return hip_fail(e, "concat");
+        out->nnz = dense ? N : total;
+        out->is_dense = dense ? 1 : 0;
+        return SPARCML_OK;
+    } catch (const std::exception& ex) {
+        return fail(SPARCML_EHIP, "host exception: %s", ex.what());
+    }
 }
 
 int sparcml_densify(const sparcml_stream* in, uint64_t N, float* dense, void* stream)

@@ -36,7 +36,8 @@ enum TimerSlot {
     kTTopkSelect = 5,   // top-k histogram passes
     kTTopkWrite = 6,    // top-k count + scan + write
     kTDensify = 7,
-    kTSlots = 8
+    kTConcat = 8,       // concatenation of disjoint parts
+    kTSlots = 9
 };
 void timer_begin(int slot, hipStream_t s);
 void timer_end(int slot, hipStream_t s);
@@ -104,6 +105,23 @@ hipError_t densify_run(const uint32_t* idx, const float* val, const uint8_t* qva
 hipError_t dequant_run(const uint8_t* qval, const float* qscale, uint32_t qbits, uint64_t n,
                        float* out, hipStream_t s);
 
+// ---------------------------------------------------------------- concat
+// One part of a concatenation: indices in [lo, lo + len); dense parts hold
+// len values.  qscale: one scale, or one per bucket of stored entries.
+struct ConcatPart {
+    const uint32_t* idx;
+    const float* val;
+    const uint8_t* qval;
+    const float* qscale;
+    uint64_t nnz, lo, len;
+    int dense;
+};
+size_t concat_workspace(int P);
+// bucket: 0 (one scale per part) or a power of two; dense: the result's
+// representation (out_val holds the whole vector).
+hipError_t concat_run(int P, const ConcatPart* parts, uint32_t qbits, uint64_t bucket, int dense,
+                      uint32_t* out_idx, float* out_val, void* ws, hipStream_t s);
+
 // ---------------------------------------------------------------- top-k
 size_t topk_workspace(int P, uint64_t N, uint64_t k);
 hipError_t topk_run(int P, const float* x, uint64_t N, uint64_t k, uint32_t* out_idx,
@@ -114,5 +132,11 @@ size_t quant_workspace(int P, uint64_t max_n);
 hipError_t quant_run(int P, const float* const* vals, const uint64_t* n, int bits, uint64_t seed,
                      uint8_t* const* out_q, float* out_scale, float* const* out_deq, void* ws,
                      hipStream_t s);
+// Buckets of `bucket` entries (a power of two, 4..8192); scales flat, stream
+// r's ceil(n_r / bucket) scales after those of streams 0..r-1.
+size_t quant_buckets_workspace(int P);
+hipError_t quant_buckets_run(int P, const float* const* vals, const uint64_t* n, int bits,
+                             uint32_t bucket, uint64_t seed, uint8_t* const* out_q, float* out_scale,
+                             float* const* out_deq, void* ws, hipStream_t s);
 
 }  // namespace sparcml

@@ -1,6 +1,7 @@
 // QSGD stochastic quantization on gfx950 (§2.2 "Quantization", §6): one
-// bucket per stream, scale = the stream's L2 norm, s = 2^(bits-1)-1 levels
-// plus a sign bit, unbiased stochastic rounding driven by Philox4x32-10.
+// bucket per stream or buckets of B consecutive entries, scale = the
+// bucket's L2 norm, s = 2^(bits-1)-1 levels plus a sign bit, unbiased
+// stochastic rounding driven by Philox4x32-10.
 //
 // The norm is a fixed adjacent-pair tree in fp64 (zero-padded to a power of
 // two), so it is reproducible bit for bit: 64 consecutive squares are summed
@@ -178,6 +179,117 @@ __global__ void __launch_bounds__(256) k_quantize(const QDesc* tab, const float*
     }
 }
 
+// Bucketed QSGD in one pass: a bucket of B (a power of two, 4..8192)
+// consecutive entries is held in the registers of G = B / EPT consecutive
+// threads, EPT = max(4, B / 256) consecutive entries each.  Its norm is the
+// adjacent-pair tree in fp64: each thread's EPT squares, then a lane
+// butterfly over min(G, 64) lanes, then (G > 64) the waves' sums pairwise.
+// The codes are drawn as in the per-stream scheme (Philox word j&3 of
+// counter (j>>2, r, 0, 0) for element j of stream r) and written once.
+struct QBDesc {
+    const float* val;
+    uint8_t* q;
+    float* deq;
+    uint64_t n;
+    uint64_t soff;  // index of the stream's first scale
+};
+
+template <int BITS, int EPT>
+__global__ void __launch_bounds__(256) k_quantize_buckets(const QBDesc* tab, float* scales, uint32_t B,
+                                                          uint32_t k0, uint32_t k1)
+{
+    constexpr uint32_t S = (1u << (BITS - 1)) - 1u;
+    __shared__ double s_w[4];
+    const uint32_t r = blockIdx.y;
+    const QBDesc d = tab[r];
+    const uint64_t blk0 = (uint64_t)blockIdx.x * 256 * EPT;
+    if (blk0 >= d.n) return;  // uniform over the block
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    const uint32_t G = B / EPT;  // threads per bucket (1..256)
+    const uint64_t e0 = blk0 + (uint64_t)threadIdx.x * EPT;
+
+    float x[EPT];
+    const bool full = e0 + EPT <= d.n;
+    if (full && ((reinterpret_cast<uintptr_t>(d.val + e0) & 15u) == 0)) {
+#pragma unroll
+        for (int i = 0; i < EPT; i += 4) {
+            const float4 t = *reinterpret_cast<const float4*>(d.val + e0 + i);
+            x[i] = t.x;
+            x[i + 1] = t.y;
+            x[i + 2] = t.z;
+            x[i + 3] = t.w;
+        }
+    } else {
+#pragma unroll
+        for (int i = 0; i < EPT; ++i) x[i] = e0 + i < d.n ? d.val[e0 + i] : 0.0f;
+    }
+    double t[EPT];
+#pragma unroll
+    for (int i = 0; i < EPT; ++i) t[i] = (double)x[i] * (double)x[i];
+#pragma unroll
+    for (int w = EPT; w > 1; w >>= 1)
+#pragma unroll
+        for (int i = 0; i < w / 2; ++i) t[i] = t[2 * i] + t[2 * i + 1];
+    double sum = t[0];
+    const int width = G < 64u ? (int)G : 64;
+    for (int o = 1; o < width; o <<= 1) sum = sum + __shfl_xor(sum, o);
+    if (G > 64u) {  // (uniform) a bucket spans two or four waves
+        if (lane == 0) s_w[wv] = sum;
+        __syncthreads();
+        if (G == 128u) sum = (wv < 2) ? s_w[0] + s_w[1] : s_w[2] + s_w[3];
+        else sum = (s_w[0] + s_w[1]) + (s_w[2] + s_w[3]);
+    }
+    const float scale = (float)sqrt(sum);
+    if (e0 % B == 0 && e0 < d.n) scales[d.soff + e0 / B] = scale;
+
+    const float inv = scale > 0.0f ? __fdiv_rn((float)S, scale) : 0.0f;
+    const float unit = __fdiv_rn(scale, (float)S);
+    constexpr int NW = (EPT * BITS + 31) / 32;  // code words of this thread
+    uint32_t word[NW];
+#pragma unroll
+    for (int w = 0; w < NW; ++w) word[w] = 0u;
+#pragma unroll
+    for (int g = 0; g < EPT; g += 4) {
+        const uint4 w4 = philox(make_uint4((uint32_t)((e0 + g) >> 2), r, 0u, 0u), k0, k1);
+        const uint32_t wr[4] = {w4.x, w4.y, w4.z, w4.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int ii = g + i;
+            uint32_t l = 0;
+            if (scale > 0.0f) {
+                const float a = __fmul_rn(fabsf(x[ii]), inv);
+                l = (uint32_t)a;
+                const float f = __fsub_rn(a, (float)l);
+                const float u = (float)(wr[i] >> 8) * 0x1p-24f;
+                l += u < f ? 1u : 0u;
+                l = l > S ? S : l;
+            }
+            const uint32_t sign = (x[ii] < 0.0f && l > 0u) ? 1u : 0u;
+            const uint32_t code = (sign << (BITS - 1)) | l;
+            word[(ii * BITS) / 32] |= code << ((ii * BITS) % 32);
+            if (d.deq && e0 + ii < d.n) {
+                const float mag = __fmul_rn((float)l, unit);
+                d.deq[e0 + ii] = l == 0u ? 0.0f : (sign ? -mag : mag);
+            }
+        }
+    }
+    // EPT * BITS / 8 bytes of codes at byte e0 * BITS / 8
+    constexpr int NB = EPT * BITS / 8;
+    const uint64_t byte0 = e0 * BITS / 8;
+    const uint64_t nbytes = (d.n * BITS + 7) / 8;
+    uint8_t* q = d.q + byte0;
+    if (NB >= 4 && byte0 + NB <= nbytes && ((reinterpret_cast<uintptr_t>(q) & 3u) == 0)) {
+#pragma unroll
+        for (int w = 0; w < NW; ++w) reinterpret_cast<uint32_t*>(q)[w] = word[w];
+    } else if (NB == 2 && byte0 + 2 <= nbytes && ((reinterpret_cast<uintptr_t>(q) & 1u) == 0)) {
+        *reinterpret_cast<uint16_t*>(q) = (uint16_t)word[0];
+    } else {
+#pragma unroll
+        for (int i = 0; i < NB; ++i)
+            if (byte0 + i < nbytes) q[i] = (uint8_t)(word[i / 4] >> (8 * (i % 4)));
+    }
+}
+
 struct QLayout {
     QDesc* tab;
     double* part[4];
@@ -207,9 +319,50 @@ QLayout qlayout(int P, uint64_t max_n, void* ws)
     return l;
 }
 
+template <int BITS>
+void launch_buckets(dim3 grid, int ept, hipStream_t s, const QBDesc* tab, float* scales, uint32_t B,
+                    uint32_t k0, uint32_t k1)
+{
+    switch (ept) {
+    case 4: hipLaunchKernelGGL((k_quantize_buckets<BITS, 4>), grid, dim3(256), 0, s, tab, scales, B, k0, k1); break;
+    case 8: hipLaunchKernelGGL((k_quantize_buckets<BITS, 8>), grid, dim3(256), 0, s, tab, scales, B, k0, k1); break;
+    case 16: hipLaunchKernelGGL((k_quantize_buckets<BITS, 16>), grid, dim3(256), 0, s, tab, scales, B, k0, k1); break;
+    default: hipLaunchKernelGGL((k_quantize_buckets<BITS, 32>), grid, dim3(256), 0, s, tab, scales, B, k0, k1); break;
+    }
+}
+
 }  // namespace
 
 size_t quant_workspace(int P, uint64_t max_n) { return qlayout(P, max_n, nullptr).bytes; }
+
+size_t quant_buckets_workspace(int P) { return align_up(sizeof(QBDesc) * (size_t)P, 256); }
+
+hipError_t quant_buckets_run(int P, const float* const* vals, const uint64_t* n, int bits,
+                             uint32_t bucket, uint64_t seed, uint8_t* const* out_q, float* out_scale,
+                             float* const* out_deq, void* ws, hipStream_t s)
+{
+    uint64_t max_n = 0, soff = 0;
+    QBDesc* host = new QBDesc[P];
+    for (int r = 0; r < P; ++r) {
+        host[r] = QBDesc{vals[r], out_q[r], out_deq ? out_deq[r] : nullptr, n[r], soff};
+        soff += (n[r] + bucket - 1) / bucket;
+        max_n = std::max(max_n, n[r]);
+    }
+    QBDesc* tab = static_cast<QBDesc*>(ws);
+    hipError_t e = upload(tab, host, sizeof(QBDesc) * P, s);
+    delete[] host;
+    if (e != hipSuccess || max_n == 0) return e;
+    const int ept = bucket <= 1024u ? 4 : (int)(bucket / 256u);
+    const uint64_t per_block = 256ull * ept;
+    const dim3 grid((uint32_t)((max_n + per_block - 1) / per_block), P);
+    const uint32_t k0 = (uint32_t)(seed & 0xFFFFFFFFu), k1 = (uint32_t)(seed >> 32);
+    timer_begin(kTQuantCodes, s);
+    if (bits == 2) launch_buckets<2>(grid, ept, s, tab, out_scale, bucket, k0, k1);
+    else if (bits == 4) launch_buckets<4>(grid, ept, s, tab, out_scale, bucket, k0, k1);
+    else launch_buckets<8>(grid, ept, s, tab, out_scale, bucket, k0, k1);
+    timer_end(kTQuantCodes, s);
+    return hipGetLastError();
+}
 
 hipError_t quant_run(int P, const float* const* vals, const uint64_t* n, int bits, uint64_t seed,
                      uint8_t* const* out_q, float* out_scale, float* const* out_deq, void* ws,

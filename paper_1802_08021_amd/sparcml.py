@@ -16,7 +16,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "_lib", "libsparcml.so")
 
 OK, EINVAL, ECAPACITY, EWORKSPACE, EUNSORTED, EHIP = 0, -1, -2, -3, -4, -5
-OP_TOPK, OP_QUANTIZE, OP_REDUCE, OP_DENSIFY = 1, 2, 3, 4
+OP_TOPK, OP_QUANTIZE, OP_REDUCE, OP_DENSIFY, OP_QUANTIZE_BUCKETED, OP_CONCAT = 1, 2, 3, 4, 5, 6
 
 
 class Stream(ctypes.Structure):
@@ -59,12 +59,18 @@ def lib() -> ctypes.CDLL:
     L.sparcml_quantize.argtypes = [i32, ctypes.POINTER(Stream), i32, u64, vp, vp, vp, vp,
                                    ctypes.c_size_t, vp]
     L.sparcml_quantize.restype = i32
+    L.sparcml_quantize_bucketed.argtypes = [i32, ctypes.POINTER(Stream), i32, u64, u64, vp, vp, vp, vp,
+                                            ctypes.c_size_t, vp]
+    L.sparcml_quantize_bucketed.restype = i32
     L.sparcml_sparse_reduce.argtypes = [i32, ctypes.POINTER(Stream), u64, ctypes.c_double,
                                         ctypes.POINTER(Stream), vp, vp, vp, ctypes.c_size_t, vp]
     L.sparcml_sparse_reduce.restype = i32
     L.sparcml_sparse_reduce_range.argtypes = [i32, ctypes.POINTER(Stream), u64, u64, u64, ctypes.c_double,
                                               ctypes.POINTER(Stream), vp, vp, vp, ctypes.c_size_t, vp]
     L.sparcml_sparse_reduce_range.restype = i32
+    L.sparcml_concat.argtypes = [i32, ctypes.POINTER(Stream), ctypes.POINTER(u64), u64, ctypes.c_double, u64,
+                                 ctypes.POINTER(Stream), vp, ctypes.c_size_t, vp]
+    L.sparcml_concat.restype = i32
     L.sparcml_densify.argtypes = [ctypes.POINTER(Stream), u64, vp, vp]
     L.sparcml_densify.restype = i32
     L.sparcml_timing_enable.argtypes = [i32]
@@ -81,6 +87,7 @@ def lib() -> ctypes.CDLL:
 
 TIMER_REDUCE_PASS, TIMER_REDUCE_WRITE, TIMER_REDUCE_SLOW = 0, 1, 2
 TIMER_QUANT_NORM, TIMER_QUANT_CODES, TIMER_TOPK_SELECT, TIMER_TOPK_WRITE, TIMER_DENSIFY = 3, 4, 5, 6, 7
+TIMER_CONCAT = 8
 
 
 def timing_enable(on: bool) -> None:
@@ -176,6 +183,17 @@ def topk_sparsify(x, k: int, residual=None, ws=None):
 def quantize(vals, bits: int, seed: int, want_deq: bool = False, ws=None):
     """QSGD of each fp32 tensor in ``vals``.  Returns (codes list of uint8
     tensors, scales fp32 [P], dequantized list or None)."""
+    return _quantize(vals, bits, seed, want_deq, ws, 0)
+
+
+def quantize_bucketed(vals, bits: int, bucket: int, seed: int, want_deq: bool = False, ws=None):
+    """QSGD in buckets of ``bucket`` entries (§6).  Returns (codes list,
+    flat scales fp32 -- stream r's ceil(n_r / bucket) after those of streams
+    0..r-1 --, dequantized list or None)."""
+    return _quantize(vals, bits, seed, want_deq, ws, bucket)
+
+
+def _quantize(vals, bits, seed, want_deq, ws, bucket):
     torch = _torch()
     P = len(vals)
     dev = vals[0].device
@@ -191,16 +209,28 @@ def quantize(vals, bits: int, seed: int, want_deq: bool = False, ws=None):
             deqs.append(torch.empty(max(n, 1), dtype=torch.float32, device=dev))
     qptr = (ctypes.c_void_p * P)(*[_ptr(c) for c in codes])
     dptr = (ctypes.c_void_p * P)(*[_ptr(d) for d in deqs]) if want_deq else None
-    scale = torch.empty(P, dtype=torch.float32, device=dev)
-    nbytes = workspace_size(OP_QUANTIZE, P, 1, max(v.numel() for v in vals))
+    dp = ctypes.cast(dptr, ctypes.c_void_p) if dptr else None
+    if bucket:
+        nscale = sum((v.numel() + bucket - 1) // bucket for v in vals)
+        scale = torch.empty(max(nscale, 1), dtype=torch.float32, device=dev)
+        nbytes = workspace_size(OP_QUANTIZE_BUCKETED, P, 1, 0)
+    else:
+        nscale = P
+        scale = torch.empty(P, dtype=torch.float32, device=dev)
+        nbytes = workspace_size(OP_QUANTIZE, P, 1, max(v.numel() for v in vals))
     if ws is None or ws.numel() < nbytes:
         ws = alloc_workspace(nbytes, dev)
-    _check(lib().sparcml_quantize(P, arr, bits, seed & (2**64 - 1), ctypes.cast(qptr, ctypes.c_void_p),
-                                  _ptr(scale), ctypes.cast(dptr, ctypes.c_void_p) if dptr else None,
-                                  _ptr(ws), ws.numel(), _stream_ptr(dev)),
-           "sparcml_quantize")
+    if bucket:
+        _check(lib().sparcml_quantize_bucketed(P, arr, bits, bucket, seed & (2**64 - 1),
+                                               ctypes.cast(qptr, ctypes.c_void_p), _ptr(scale), dp,
+                                               _ptr(ws), ws.numel(), _stream_ptr(dev)),
+               "sparcml_quantize_bucketed")
+    else:
+        _check(lib().sparcml_quantize(P, arr, bits, seed & (2**64 - 1), ctypes.cast(qptr, ctypes.c_void_p),
+                                      _ptr(scale), dp, _ptr(ws), ws.numel(), _stream_ptr(dev)),
+               "sparcml_quantize")
     nb = [(v.numel() + per - 1) // per for v in vals]
-    return ([c[:m] for c, m in zip(codes, nb)], scale,
+    return ([c[:m] for c, m in zip(codes, nb)], scale[:nscale],
             [d[: v.numel()] for d, v in zip(deqs, vals)] if want_deq else None)
 
 
@@ -280,6 +310,55 @@ def _reduce(idx, vals, N, rng, delta, codes, scales, qbits, node_info, ws, out_i
         "node_nnz": node_nnz,
         "node_dense": node_dense,
     }
+
+
+class ConcatCall:
+    """Repeated concatenation of P parts with disjoint index ranges (the
+    gathered shares of the split-allgather allreduce) into fixed outputs.
+    ``parts``: dicts with ``idx`` (device int32 tensor, or None for a dense
+    part) and ``val`` (fp32) or ``codes`` + ``scales`` (QSGD, ``qbits``)."""
+
+    def __init__(self, parts, bounds, N: int, delta: float, qbits: int = 0, bucket: int = 0):
+        torch = _torch()
+        self.P = len(parts)
+        self.N, self.delta, self.bucket = N, float(delta), bucket
+        self.dev = None
+        self.arr = (Stream * self.P)()
+        total = 0
+        for p, part in enumerate(parts):
+            n = bounds[p + 1] - bounds[p] if part["idx"] is None else part["idx"].numel()
+            ref = part["codes"] if qbits else part["val"]
+            _require_cuda(ref, f"parts[{p}]")
+            self.dev = ref.device
+            self.arr[p] = Stream(None if part["idx"] is None else _ptr(part["idx"]),
+                                 None if qbits else _ptr(part["val"]),
+                                 _ptr(part["codes"]) if qbits else None,
+                                 _ptr(part["scales"]) if qbits else None,
+                                 n, 1 if part["idx"] is None else 0, qbits)
+            total += 0 if part["idx"] is None else n
+        self.bounds = (ctypes.c_uint64 * (self.P + 1))(*[int(b) for b in bounds])
+        self.out_idx = torch.empty(max(total, 1), dtype=torch.int32, device=self.dev)
+        self.out_val = torch.empty(N, dtype=torch.float32, device=self.dev)
+        self.ws = alloc_workspace(workspace_size(OP_CONCAT, self.P, N, 0), self.dev)
+        self.out = Stream(_ptr(self.out_idx), _ptr(self.out_val), None, None, self.out_idx.numel(), 0, 0)
+        self._keep = parts
+
+    def run(self):
+        """Returns (nnz, dense)."""
+        self.out.nnz = self.out_idx.numel()
+        _check(lib().sparcml_concat(self.P, self.arr, self.bounds, self.N, self.delta, self.bucket,
+                                    ctypes.byref(self.out), _ptr(self.ws), self.ws.numel(),
+                                    _stream_ptr(self.dev)), "sparcml_concat")
+        return int(self.out.nnz), bool(self.out.is_dense)
+
+
+def concat(parts, bounds, N: int, delta: float, qbits: int = 0, bucket: int = 0):
+    """Concatenation of parts with disjoint index ranges (see ConcatCall).
+    Returns dict(idx, val, nnz, dense); ``idx`` is None for a dense result."""
+    c = ConcatCall(parts, bounds, N, delta, qbits, bucket)
+    n, dense = c.run()
+    return {"idx": None if dense else c.out_idx[:n], "val": c.out_val if dense else c.out_val[:n],
+            "nnz": n, "dense": dense}
 
 
 def densify(idx, val, N: int, codes=None, scale=None, qbits: int = 0):

@@ -22,7 +22,8 @@ def declared_symbols():
 def test_header_declares_the_boundary():
     syms = declared_symbols()
     for name in ("sparcml_topk_sparsify", "sparcml_quantize", "sparcml_sparse_reduce",
-                 "sparcml_sparse_reduce_range", "sparcml_densify", "sparcml_workspace_size", "sparcml_strerror",
+                 "sparcml_sparse_reduce_range", "sparcml_quantize_bucketed", "sparcml_concat",
+                 "sparcml_densify", "sparcml_workspace_size", "sparcml_strerror",
                  "sparcml_last_error"):
         assert name in syms
 
@@ -166,6 +167,50 @@ def test_quantize_argument_errors():
     assert L.sparcml_quantize(4, arr, 4, 1, ctypes.cast(q, ctypes.c_void_p), None, None, FAKE, 1 << 30, None) == S.EINVAL
     assert L.sparcml_quantize(4, streams(4, qbits=4), 4, 1, ctypes.cast(q, ctypes.c_void_p), FAKE, None, FAKE, 1 << 30, None) == S.EINVAL
     assert L.sparcml_quantize(4, arr, 4, 1, ctypes.cast(q, ctypes.c_void_p), FAKE, None, FAKE, 8, None) == S.EWORKSPACE
+
+
+def test_quantize_bucketed_argument_errors():
+    L = S.lib()
+    q = ctypes.cast((ctypes.c_void_p * 4)(*([FAKE] * 4)), ctypes.c_void_p)
+    arr = streams(4)
+    for bad in (0, 2, 3, 100, 16384):
+        assert L.sparcml_quantize_bucketed(4, arr, 4, bad, 1, q, FAKE, None, FAKE, 1 << 30, None) == S.EINVAL
+    assert "bucket" in S.last_error()
+    assert L.sparcml_quantize_bucketed(4, arr, 5, 1024, 1, q, FAKE, None, FAKE, 1 << 30, None) == S.EINVAL
+    assert L.sparcml_quantize_bucketed(4, arr, 4, 1024, 1, q, FAKE, None, FAKE, 8, None) == S.EWORKSPACE
+    assert ws_size(S.OP_QUANTIZE_BUCKETED, 4, 1, 0) == (S.OK, 256)
+
+
+def concat_rc(parts, bounds, N=100, delta=0.5, bucket=0, out=None, ws=FAKE, ws_bytes=1 << 30):
+    P = len(bounds) - 1
+    b = (ctypes.c_uint64 * len(bounds))(*bounds)
+    if out is None:
+        out = S.Stream(FAKE, FAKE, None, None, 1 << 30, 0, 0)
+    return S.lib().sparcml_concat(P, parts, b, N, delta, bucket, ctypes.byref(out), ws, ws_bytes, None)
+
+
+def test_concat_argument_errors():
+    # every call below fails validation before any device work
+    sp = streams(2, nnz=4)
+    assert concat_rc(sp, [1, 50, 100]) == S.EINVAL       # bounds[0] != 0
+    assert concat_rc(sp, [0, 50, 99]) == S.EINVAL        # bounds[P] != N
+    assert concat_rc(streams(3, nnz=4), [0, 60, 50, 100]) == S.EINVAL  # decreasing bounds
+    assert concat_rc(streams(2, nnz=51), [0, 50, 100]) == S.EINVAL  # more entries than the range
+    dense = streams(2, nnz=49, dense=1)
+    assert concat_rc(dense, [0, 50, 100]) == S.EINVAL    # a dense part must hold its range
+    assert concat_rc(sp, [0, 50, 100], N=0) == S.EINVAL
+    assert concat_rc(sp, [0, 50, 100], delta=0.0) == S.EINVAL
+    assert concat_rc(sp, [0, 50, 100], bucket=3) == S.EINVAL
+    mixed = streams(2, nnz=4)
+    mixed[1] = S.Stream(FAKE, None, FAKE, FAKE, 4, 0, 4)
+    assert concat_rc(mixed, [0, 50, 100]) == S.EINVAL    # mixed qbits
+    noscale = streams(2, nnz=4, qbits=4)
+    noscale[0] = S.Stream(FAKE, None, FAKE, None, 4, 0, 4)
+    assert concat_rc(noscale, [0, 50, 100]) == S.EINVAL
+    # 8 entries, thr = 50: the result stays sparse and needs 8 output entries
+    assert concat_rc(sp, [0, 50, 100], out=S.Stream(FAKE, FAKE, None, None, 7, 0, 0)) == S.ECAPACITY
+    assert concat_rc(sp, [0, 50, 100], ws_bytes=8) == S.EWORKSPACE
+    assert S.lib().sparcml_concat(0, sp, None, 100, 0.5, 0, None, FAKE, 1, None) == S.EINVAL
 
 
 def test_densify_argument_errors():

@@ -392,6 +392,88 @@ def test_split_allgather_equals_full_reduce():
     np.testing.assert_array_equal(r1["val"], r2["val"])
 
 
+def _equal_bounds(N, P):
+    return [N * s // P for s in range(P + 1)]
+
+
+def test_concat_of_disjoint_sparse_parts_is_their_reduce():
+    """§5.1 case (2): summing vectors with disjoint index sets is their
+    concatenation.  With P a power of two the tree reduce of the same parts
+    (pinned by brute force above) must give the same representation, nnz,
+    indices and values: every tree node's size is then the sum of its
+    leaves' sizes, so the root is dense exactly when the total exceeds thr."""
+    rng = np.random.default_rng(23)
+    for case in range(200):
+        P = int(rng.choice([1, 2, 4, 8, 16]))
+        N = int(rng.integers(P, 200))
+        b = _equal_bounds(N, P)
+        delta = float(rng.choice([0.05, 0.2, 0.5, 1.0]))
+        idx, val, parts = [], [], []
+        for s in range(P):
+            k = int(rng.integers(0, b[s + 1] - b[s] + 1))
+            a = (np.sort(rng.choice(b[s + 1] - b[s], size=k, replace=False)) + b[s]).astype(np.uint32)
+            v = inputs.normal(rng, k)
+            idx.append(a)
+            val.append(v)
+            parts.append({"idx": a, "val": v})
+        c = oracle.concat(parts, b, N, delta)
+        r = oracle.sparse_reduce(idx, val, N, delta)
+        assert c["dense"] == r["dense"] and c["nnz"] == r["nnz"]
+        if c["dense"]:
+            np.testing.assert_array_equal(c["val"] + np.float32(0), r["val"] + np.float32(0))
+        else:
+            np.testing.assert_array_equal(c["idx"], r["idx"])
+            np.testing.assert_array_equal(c["val"].view(np.uint32), r["val"].view(np.uint32))
+
+
+def test_concat_threshold_boundary_and_dense_parts():
+    N, P = 40, 4
+    b = _equal_bounds(N, P)
+    parts = [{"idx": np.array([b[s], b[s] + 1], np.uint32), "val": np.ones(2, np.float32) * (s + 1)}
+             for s in range(P)]
+    # 8 entries: thr = 8 stays sparse, thr = 7 turns dense
+    assert not oracle.concat(parts, b, N, 8 / 40)["dense"]
+    d = oracle.concat(parts, b, N, 7 / 40)
+    assert d["dense"] and d["nnz"] == N
+    assert d["val"][b[2] + 1] == 3.0 and d["val"][b[2] + 2] == 0.0
+    # one dense part makes the result dense whatever the threshold
+    parts[1] = {"idx": None, "val": np.arange(b[2] - b[1], dtype=np.float32)}
+    d = oracle.concat(parts, b, N, 100.0)
+    assert d["dense"]
+    np.testing.assert_array_equal(d["val"][b[1]: b[2]], np.arange(b[2] - b[1], dtype=np.float32))
+    with pytest.raises(oracle.OracleError):  # an index outside its part's range
+        oracle.concat([{"idx": np.array([b[1]], np.uint32), "val": np.ones(1, np.float32)}] + parts[1:],
+                      b, N, 0.5)
+
+
+def test_dsar_gathered_quantized_shares_within_one_level():
+    """DSAR with the QSGD dense stage (§5.3.2, §6): each node's dense share
+    is quantized in buckets and the gathered shares are dequantized in
+    place.  Every coordinate is within one level of its bucket of the exact
+    allreduce, and an all-zero bucket comes back as exact zeros."""
+    rng = np.random.default_rng(24)
+    P, N, delta, B = 8, 4000, 0.01, 64
+    idx = [inputs.uniform_subset(rng, N, 300) for _ in range(P)]
+    val = [inputs.normal(rng, 300) for _ in range(P)]
+    full, _ = brute_tree(idx, val, N)
+    b = _equal_bounds(N, P)
+    for bits in (2, 4, 8):
+        parts = []
+        for s in range(P):
+            sh = oracle.sparse_reduce_range(idx, val, N, b[s], b[s + 1], delta)
+            assert sh["dense"]
+            q, sc, _ = oracle.quantize([sh["val"]], bits, seed=100 + s, bucket=B)
+            parts.append({"idx": None, "codes": q[0], "scales": sc, "qbits": bits, "bucket": B,
+                          "n": sh["val"].size})
+            units = np.repeat(sc.astype(np.float64) / (2 ** (bits - 1) - 1), B)[: sh["val"].size]
+            parts[-1]["units"] = units
+        c = oracle.concat(parts, b, N, delta)
+        assert c["dense"]
+        units = np.concatenate([p["units"] for p in parts])
+        assert np.all(np.abs(c["val"].astype(np.float64) - full) <= units * (1 + 2.0**-22))
+        assert np.all(c["val"][units == 0] == 0) and np.all(full[units == 0] == 0)
+
+
 def test_reduce_rejects_bad_input():
     N = 10
     good = [np.array([1, 2], np.uint32)] * 2
@@ -554,6 +636,81 @@ def test_qsgd_random_stream_convention():
             u = np.float32(w >> 8) * np.float32(2.0**-24)
             l = min(l0 + (1 if u < f else 0), 127)
             assert (int(q[r][j]) & 127) == l
+
+
+def test_qsgd_bucketed_scales_bounds_and_draws():
+    """§6 buckets: every bucket of B consecutive entries has its own scale,
+    the bucket's L2 norm (checked against an exactly rounded sum); each
+    element is within one of its bucket's levels, and the draw for element
+    j of stream r is still Philox word j&3 of counter (j>>2, r, 0, 0)."""
+    rng = np.random.default_rng(14)
+    seed = 0xDEAD_BEEF_0BAD_F00D
+    for bits, B in ((2, 64), (4, 1024), (8, 256), (4, 4)):
+        s = 2 ** (bits - 1) - 1
+        per = 8 // bits
+        sizes = (0, 1, B - 1, B, B + 1, 3 * B + 7)
+        vals = [inputs.laplace(rng, 1e-3, n) for n in sizes]
+        vals[3][: min(B, 8)] = 0.0
+        vals.append(np.zeros(2 * B + 3, np.float32))  # all-zero buckets
+        q, scales, deq = oracle.quantize(vals, bits, seed, bucket=B)
+        counts = oracle.scale_counts([v.size for v in vals], B)
+        assert scales.size == sum(counts)
+        so = 0
+        for r, (v, qq, dq) in enumerate(zip(vals, q, deq)):
+            n = v.size
+            sc = scales[so: so + counts[r]]
+            so += counts[r]
+            codes = (qq[np.arange(n) // per] >> ((np.arange(n) % per) * bits)) & ((1 << bits) - 1)
+            lev = codes & s
+            for b in range(counts[r]):
+                seg = slice(b * B, min((b + 1) * B, n))
+                exact = math.sqrt(math.fsum(float(a) * float(a) for a in v[seg]))
+                assert abs(float(sc[b]) - exact) <= 2.0**-23 * exact + 1e-45
+                if sc[b] == 0:
+                    assert np.all(codes[seg] == 0) and np.all(dq[seg] == 0)
+                    continue
+                unit = np.float32(sc[b]) / np.float32(s)
+                assert np.all(np.abs(dq[seg].astype(np.float64) - v[seg]) <= float(unit) * (1 + 2.0**-22))
+                inv = np.float32(s) / np.float32(sc[b])
+                for j in range(seg.start, seg.stop, max(1, (seg.stop - seg.start) // 9)):
+                    a = np.float32(abs(v[j])) * inv
+                    l0 = int(a)
+                    f = a - np.float32(l0)
+                    w = oracle.philox4x32_10([j >> 2, r, 0, 0], [seed & 0xFFFFFFFF, seed >> 32])[j & 3]
+                    u = np.float32(w >> 8) * np.float32(2.0**-24)
+                    assert int(lev[j]) == min(l0 + (1 if u < f else 0), s)
+            assert np.all(lev <= s)
+            np.testing.assert_array_equal(oracle.dequantize(qq, sc, bits, n, bucket=B), dq)
+
+
+def test_qsgd_bucket_covering_the_stream_is_per_stream_qsgd():
+    """Special case: a bucket at least as long as the stream (zero padding to
+    B adds exact zeros to the norm tree) gives the per-stream scheme."""
+    rng = np.random.default_rng(15)
+    vals = [inputs.laplace(rng, 1.0, n) for n in (1, 5, 64, 100, 1000)]
+    for bits in (2, 4, 8):
+        q0, s0, d0 = oracle.quantize(vals, bits, seed=77)
+        q1, s1, d1 = oracle.quantize(vals, bits, seed=77, bucket=1024)
+        np.testing.assert_array_equal(s0, s1)
+        for a, b in zip(q0, q1):
+            np.testing.assert_array_equal(a, b)
+
+
+def test_qsgd_bucketed_unbiased():
+    """Zero-mean noise per element under bucketed scales (§2.2, §6)."""
+    rng = np.random.default_rng(16)
+    v = inputs.laplace(rng, 1.0, 40)
+    v[20:] *= 50.0  # second bucket on a different scale
+    M = 2000
+    acc = np.zeros(v.size)
+    for seed in range(M):
+        _, sc, dq = oracle.quantize([v], 4, seed=seed * 104729 + 3, bucket=20)
+        acc += dq[0]
+    units = np.repeat(sc.astype(np.float64) / 7, 20)
+    a = np.abs(v.astype(np.float64)) / units
+    f = a - np.floor(a)
+    sd = units * np.sqrt(f * (1 - f) / M)
+    assert np.all(np.abs(acc / M - v) <= 5 * sd + units * 2.0**-20 + 1e-12)
 
 
 # ---------------------------------------------------------------------------
