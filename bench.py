@@ -28,7 +28,10 @@ Besides the headline line the JSON carries:
                 after at least 0.3 s of warm-up steps, and the split-phase
                 share of c4 and c5 (index range 0 of P equal ones, every
                 rank's stream restricted to it: one node's reduction in the
-                split-allgather allreduce).
+                split-allgather allreduce), and c5/dsar: one node's compute
+                in DSAR with the QSGD dense stage (its share reduced, the
+                dense share quantized 4-bit in buckets of 1024, all P
+                gathered shares decoded into the full vector).
 
 Only one GPU is used; --gpus above 1 exits with a message.
 """
@@ -245,6 +248,78 @@ class Workload:
             self.step_bytes = self.quant_bytes + red_in + out_bytes
 
 
+class DsarWorkload:
+    """One node's compute in the split-allgather allreduce with QSGD on the
+    dense stage (DSAR, §5.3.2 and §6), on c5's streams in fp32: the node's
+    share (index range 0 of P equal ones) reduced over the P ranks'
+    sub-streams, the dense share quantized in buckets, and the P gathered
+    quantized shares decoded into the full vector.  The other nodes' shares
+    (their own work) are prepared once, untimed."""
+
+    def __init__(self, name, cfg, seed, torch, dev, bits=4, bucket=1024):
+        from paper_1802_08021_amd import inputs
+        from paper_1802_08021_amd import sparcml as S
+        self.name, self.c = name, cfg
+        c = cfg
+        t0 = time.time()
+        d = inputs.generate(c, seed)
+        log(f"{name}: generated inputs in {time.time() - t0:.1f}s")
+        P, N = c.P, c.N
+        self.bits, self.bucket = bits, bucket
+        b = [N * s // P for s in range(P + 1)]
+        _, idx = arena([a.view(np.int32) for a in d["idx"]], None, torch, dev)
+        _, vals = arena(d["val"], None, torch, dev)
+        # sub-stream of rank r for share s: a slice of the sorted stream
+        cuts = [np.searchsorted(a, b) for a in d["idx"]]
+        per = 8 // bits
+        codes, scales, keep = [], [], []
+        self.nnz = 0
+        for sh in range(P):
+            si = [idx[r][int(cuts[r][sh]): int(cuts[r][sh + 1])] for r in range(P)]
+            sv = [vals[r][int(cuts[r][sh]): int(cuts[r][sh + 1])] for r in range(P)]
+            red = S.ReduceCall(si, N, c.delta, vals=sv, lo=b[sh], hi=b[sh + 1])
+            R = b[sh + 1] - b[sh]
+            cq = torch.empty((R + per - 1) // per, dtype=torch.uint8, device=dev)
+            sc = torch.empty((R + bucket - 1) // bucket, dtype=torch.float32, device=dev)
+            qc = S.QuantizeCall([red.out_val], [cq], sc, bits, inputs.quant_seed(seed, c.cfg) + sh,
+                                bucket=bucket)
+            if sh == 0:
+                self.reduce, self.quant = red, qc
+                self.nnz = sum(int(cuts[r][1] - cuts[r][0]) for r in range(P))
+                self.R = R
+            else:
+                _, dense = red.run()
+                assert dense, "a DSAR share is expected to be dense"
+                qc.run()
+                keep.append(red.out_val)
+                red = qc = None
+            codes.append(cq)
+            scales.append(sc)
+        torch.cuda.synchronize()
+        parts = [{"idx": None, "codes": cq, "scales": sc} for cq, sc in zip(codes, scales)]
+        self.concat = S.ConcatCall(parts, b, N, c.delta, qbits=bits, bucket=bucket)
+        self._keep = (idx, vals, codes, scales)
+        self.groups = [S.TIMER_REDUCE_PASS, S.TIMER_REDUCE_SLOW, S.TIMER_QUANT_CODES, S.TIMER_CONCAT]
+        nsc = (N + bucket - 1) // bucket
+        self.kernel_bytes = {
+            S.TIMER_REDUCE_PASS: self.nnz * 8 + self.R * 4,
+            S.TIMER_QUANT_CODES: self.R * 4 + self.R * bits // 8 + (self.R // bucket) * 4,
+            S.TIMER_CONCAT: N * bits // 8 + nsc * 4 + N * 4,
+        }
+        self.step_bytes = sum(self.kernel_bytes.values())
+        self.d_host = None
+        self._steps = [self.reduce.run, self.quant.run, self.concat.run]
+
+    def step(self):
+        out = None
+        for f in self._steps:
+            out = f()
+        return out
+
+    def finish_bytes(self, root_nnz, dense):
+        pass
+
+
 def time_steps(w, K, W, torch, warm_s=0.0):
     """W untimed steps (continued until warm_s seconds have passed, so that
     clocks have ramped after an idle gap), then K timed steps."""
@@ -280,7 +355,7 @@ def time_steps(w, K, W, torch, warm_s=0.0):
 
 
 GROUP_NAMES = {0: "reduce_tiles", 1: "reduce_write", 2: "reduce_slow", 3: "qsgd_norm",
-               4: "qsgd_codes", 5: "topk_select", 6: "topk_write", 7: "densify"}
+               4: "qsgd_codes", 5: "topk_select", 6: "topk_write", 7: "densify", 8: "concat"}
 
 
 def source_hash() -> str:
@@ -409,15 +484,22 @@ def main() -> int:
 
     per_config = {}
     if not args.no_per_config:
-        for name in ("c1", "c2", "c3", "c4", "c5", "c4/share", "c5/share"):
+        for name in ("c1", "c2", "c3", "c4", "c5", "c4/share", "c5/share", "c5/dsar"):
             if name == args.workload:
                 continue
             c = inputs.config(int(name[1]))
             share = (0, c.P) if name.endswith("/share") else None
-            pw = Workload(name, c, args.seed, torch, dev, share=share)
+            if name.endswith("/dsar"):
+                pw = DsarWorkload(name, c, args.seed, torch, dev)
+            else:
+                pw = Workload(name, c, args.seed, torch, dev, share=share)
             pms, pwall, pk, pn, pd = time_steps(pw, max(5, args.steps // 2), 2, torch, warm_s=0.3)
             desc = describe(c) + (f"; split-phase share [{pw.reduce.rng[0]}, {pw.reduce.rng[1]}) "
                                   f"(1 of {c.P})" if share else "")
+            if name.endswith("/dsar"):
+                desc = (f"{c.name} streams in fp32 (P={c.P}, N={c.N}, k={c.k}, delta={c.delta}): "
+                        f"share [0, {pw.R}) reduced, QSGD {pw.bits}-bit in buckets of {pw.bucket}, "
+                        f"{c.P} quantized shares decoded into N")
             per_config[name] = {
                 "workload": desc, "ms_per_step": pms, "input_nnz_per_s": pw.nnz / (pms * 1e-3),
                 "cold_ms_per_step": time_cold(pw, 3, torch),

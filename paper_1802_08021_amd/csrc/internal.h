@@ -57,6 +57,16 @@ __device__ __forceinline__ uint32_t wave_scan(uint32_t v)
     return v;
 }
 
+// 16-byte store marked nontemporal (streamed output that is not read back
+// soon): it does not displace cached inputs, and measured on gfx950 it
+// writes HBM markedly faster than a plain store.
+__device__ __forceinline__ void store_nt(float* p, float4 v)
+{
+    typedef float f4 __attribute__((ext_vector_type(4)));
+    const f4 x = {v.x, v.y, v.z, v.w};
+    __builtin_nontemporal_store(x, reinterpret_cast<f4*>(p));
+}
+
 // Round x up to a multiple of a (a power of two).
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) & ~(a - 1); }
 

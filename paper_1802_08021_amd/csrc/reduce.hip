@@ -791,7 +791,7 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
                     *reinterpret_cast<float4*>(&s_out[c]) = make_float4(0.f, 0.f, 0.f, 0.f);
                     const uint64_t g = (uint64_t)trel + c;
                     if (a.out_vec && c + 4u <= TT) {
-                        *reinterpret_cast<float4*>(a.out_val + g) = v;
+                        store_nt(a.out_val + g, v);
                     } else {
                         if (c < TT) a.out_val[g] = v.x;
                         if (c + 1u < TT) a.out_val[g + 1] = v.y;

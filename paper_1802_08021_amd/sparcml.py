@@ -380,11 +380,12 @@ def densify(idx, val, N: int, codes=None, scale=None, qbits: int = 0):
 # the timed loop).
 
 class QuantizeCall:
-    """Repeated QSGD of fixed device arrays into fixed code buffers."""
+    """Repeated QSGD of fixed device arrays into fixed code buffers
+    (``bucket`` > 0: buckets of that many entries, flat scales)."""
 
-    def __init__(self, vals, codes, scale, bits: int, seed: int, deq=None):
+    def __init__(self, vals, codes, scale, bits: int, seed: int, deq=None, bucket: int = 0):
         self.P = len(vals)
-        self.bits, self.seed = bits, seed & (2**64 - 1)
+        self.bits, self.seed, self.bucket = bits, seed & (2**64 - 1), bucket
         self.dev = vals[0].device
         self.arr = (Stream * self.P)()
         for r, v in enumerate(vals):
@@ -393,15 +394,24 @@ class QuantizeCall:
         self.qptr = (ctypes.c_void_p * self.P)(*[_ptr(c) for c in codes])
         self.dptr = (ctypes.c_void_p * self.P)(*[_ptr(d) for d in deq]) if deq else None
         self.scale = scale
-        nbytes = workspace_size(OP_QUANTIZE, self.P, 1, max(v.numel() for v in vals))
+        if bucket:
+            nbytes = workspace_size(OP_QUANTIZE_BUCKETED, self.P, 1, 0)
+        else:
+            nbytes = workspace_size(OP_QUANTIZE, self.P, 1, max(v.numel() for v in vals))
         self.ws = alloc_workspace(nbytes, self.dev)
         self._keep = (vals, codes, deq)
 
     def run(self) -> None:
-        _check(lib().sparcml_quantize(
-            self.P, self.arr, self.bits, self.seed, ctypes.cast(self.qptr, ctypes.c_void_p),
-            _ptr(self.scale), ctypes.cast(self.dptr, ctypes.c_void_p) if self.dptr else None,
-            _ptr(self.ws), self.ws.numel(), _stream_ptr(self.dev)), "sparcml_quantize")
+        dp = ctypes.cast(self.dptr, ctypes.c_void_p) if self.dptr else None
+        qp = ctypes.cast(self.qptr, ctypes.c_void_p)
+        if self.bucket:
+            _check(lib().sparcml_quantize_bucketed(
+                self.P, self.arr, self.bits, self.bucket, self.seed, qp, _ptr(self.scale), dp,
+                _ptr(self.ws), self.ws.numel(), _stream_ptr(self.dev)), "sparcml_quantize_bucketed")
+        else:
+            _check(lib().sparcml_quantize(
+                self.P, self.arr, self.bits, self.seed, qp, _ptr(self.scale), dp,
+                _ptr(self.ws), self.ws.numel(), _stream_ptr(self.dev)), "sparcml_quantize")
 
 
 class ReduceCall:
