@@ -7,6 +7,8 @@
  *
  *   sparcml_topk_sparsify  -- top-k sparsification of dense gradients
  *                             (§2.2 "Structured Sparsification", Alg. 1)
+ *   sparcml_topk_bucketed  -- kb of every bucket of coordinates with the
+ *                             error feedback of Alg. 1 (§8.4)
  *   sparcml_quantize       -- QSGD stochastic quantization (§2.2, §6)
  *   sparcml_quantize_bucketed -- QSGD in buckets of B entries (§6)
  *   sparcml_sparse_reduce  -- sum of P sparse streams in recursive-doubling
@@ -126,6 +128,34 @@ SPARCML_API int sparcml_workspace_size(int op, int P, uint64_t N, uint64_t max_n
 SPARCML_API int sparcml_topk_sparsify(int P, const float* x, uint64_t N, uint64_t k,
                           uint32_t* out_idx, float* out_val, float* residual,
                           void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Bucketed top-k with error feedback, per rank (§8.4: each group of
+ * `bucket` consecutive coordinates sends its kb largest entries and keeps
+ * the rest locally; Alg. 1: acc = eps + alpha * grad, eps = acc -
+ * TopK(acc)).  acc is formed in fp32 as a product then a sum (two
+ * roundings).  Per bucket the min(kb, len) largest magnitudes (key and
+ * ties as in sparcml_topk_sparsify), listed in ascending index order, so a
+ * rank's output is one sorted sparse stream of K entries,
+ *   K = (nb - 1) * kb + min(kb, N - (nb - 1) * bucket), nb = ceil(N / bucket)
+ * (sparcml_topk_bucketed_count).
+ *   P, N     grad and eps are P rows of N fp32 (row r at r * N), 1 <= P <=
+ *            65535, 1 <= N < 2^32.
+ *   grad     NULL (acc = eps) or the rows of the new gradient.
+ *   eps      in: the accumulated error; out: acc with the selected entries
+ *            set to +0.0.
+ *   alpha    learning rate (finite).
+ *   bucket   a power of two in [64, 4096]; kb in [1, 64].
+ *   out_idx, out_val  [P][K]: rank r's entries at r * K.
+ * No workspace; does not synchronize.
+ * Errors: EINVAL, EHIP.
+ */
+SPARCML_API int sparcml_topk_bucketed(int P, const float* grad, float* eps, uint64_t N, float alpha,
+                          uint64_t bucket, uint64_t kb, uint32_t* out_idx, float* out_val,
+                          void* stream);
+
+/* K of sparcml_topk_bucketed (0 for invalid sizes). */
+SPARCML_API uint64_t sparcml_topk_bucketed_count(uint64_t N, uint64_t bucket, uint64_t kb);
 
 /*
  * QSGD stochastic quantization of each stream's values (§2.2
@@ -304,6 +334,7 @@ SPARCML_API int sparcml_densify(const sparcml_stream* in, uint64_t N, float* den
 #define SPARCML_TIMER_TOPK_WRITE 6   /* top-k count, scan and write */
 #define SPARCML_TIMER_DENSIFY 7
 #define SPARCML_TIMER_CONCAT 8
+#define SPARCML_TIMER_TOPK_BUCKETED 9
 SPARCML_API int sparcml_timing_enable(int on);
 SPARCML_API int sparcml_timing_read(int group, float* ms);
 

@@ -14,6 +14,8 @@ Functions follow the paper:
                           (§5.1 case (2), §5.3.2 allgather phase, §6 dense
                           stage in QSGD buckets).
   * ``topk``           -- §2.2 Top-k sparsification, Alg. 1 error update.
+  * ``topk_bucketed``  -- §8.4 k of every group of consecutive coordinates,
+                          with Alg. 1's accumulate and error update.
   * ``quantize``       -- §2.2 / §6 QSGD stochastic quantization.
   * ``dequantize``, ``densify``, ``philox4x32_10``.
 """
@@ -65,6 +67,9 @@ def lib():
         L.orc_quantize.restype = ctypes.c_int
         L.orc_dequantize.argtypes = [vp, ctypes.c_float, ctypes.c_int, ctypes.c_uint64, vp]
         L.orc_dequantize.restype = ctypes.c_int
+        L.orc_topk_bucketed.argtypes = [ctypes.c_int, vp, vp, ctypes.c_uint64, ctypes.c_float,
+                                        ctypes.c_uint64, ctypes.c_uint64, vp, vp]
+        L.orc_topk_bucketed.restype = ctypes.c_int
         L.orc_quantize_bucketed.argtypes = [ctypes.c_int, vp, vp, ctypes.c_int, ctypes.c_uint64,
                                             ctypes.c_uint64, vp, vp, vp]
         L.orc_quantize_bucketed.restype = ctypes.c_int
@@ -231,6 +236,31 @@ def topk(x: np.ndarray, k: int, residual: bool = False):
 def scale_counts(sizes, bucket: int):
     """Scales per stream: ceil(n / bucket), or 1 when bucket == 0."""
     return [(n + bucket - 1) // bucket if bucket else 1 for n in sizes]
+
+
+def bucketed_count(N: int, bucket: int, kb: int) -> int:
+    """Entries per rank of the bucketed top-k: min(kb, len) per bucket."""
+    nb = (N + bucket - 1) // bucket
+    return (nb - 1) * kb + min(kb, N - (nb - 1) * bucket)
+
+
+def topk_bucketed(eps: np.ndarray, grad, alpha: float, bucket: int, kb: int):
+    """Alg. 1's error-feedback step with bucketed selection (§8.4): acc =
+    eps + alpha * grad in fp32 (grad None: acc = eps); from each bucket of
+    ``bucket`` consecutive coordinates the kb largest magnitudes.  Returns
+    (idx [P, K], val [P, K], new eps [P, N])."""
+    e = np.ascontiguousarray(eps, dtype=np.float32).copy()
+    P, N = e.shape
+    g = None if grad is None else np.ascontiguousarray(grad, dtype=np.float32)
+    K = bucketed_count(N, bucket, kb)
+    out_idx = np.zeros((P, max(K, 1)), dtype=np.uint32)
+    out_val = np.zeros((P, max(K, 1)), dtype=np.float32)
+    rc = lib().orc_topk_bucketed(P, None if g is None else g.ctypes.data, e.ctypes.data, N,
+                                 ctypes.c_float(alpha), bucket, kb, out_idx.ctypes.data,
+                                 out_val.ctypes.data)
+    if rc != 0:
+        raise OracleError(f"orc_topk_bucketed returned {rc}")
+    return out_idx[:, :K].copy(), out_val[:, :K].copy(), e
 
 
 def quantize(val_list, bits: int, seed: int, bucket: int = 0):

@@ -305,6 +305,55 @@ int orc_topk(int P, const float* x, uint64_t N, uint64_t k,
     return 0;
 }
 
+int orc_topk_bucketed(int P, const float* grad, float* eps, uint64_t N, float alpha,
+                      uint64_t bucket, uint64_t kb, uint32_t* out_idx, float* out_val)
+{
+    if (P < 1 || N == 0 || N > 0xFFFFFFFFull || !eps || bucket == 0 || kb == 0 || kb > 64) return -1;
+    if (!out_idx || !out_val) return -1;
+    const uint64_t nb = (N + bucket - 1) / bucket;
+    const uint64_t last = N - (nb - 1) * bucket;
+    const uint64_t K = (nb - 1) * kb + (last < kb ? last : kb); /* entries per rank */
+    okv* b = (okv*)malloc(bucket * sizeof(okv));
+    float* acc = (float*)malloc(bucket * sizeof(float));
+    if (!b || !acc) {
+        free(b);
+        free(acc);
+        return -4;
+    }
+    for (int r = 0; r < P; ++r) {
+        float* e = eps + (uint64_t)r * N;
+        const float* g = grad ? grad + (uint64_t)r * N : NULL;
+        uint64_t o = (uint64_t)r * K;
+        for (uint64_t q = 0; q < nb; ++q) {
+            const uint64_t j0 = q * bucket;
+            const uint64_t len = N - j0 < bucket ? N - j0 : bucket;
+            /* Alg. 1: acc = eps + alpha * grad (fp32, two roundings) */
+            for (uint64_t j = 0; j < len; ++j) {
+                acc[j] = g ? e[j0 + j] + alpha * g[j0 + j] : e[j0 + j];
+                b[j].key = mag_key(acc[j]);
+                b[j].idx = (uint32_t)(j0 + j);
+            }
+            /* the bucket's kb largest magnitudes, lowest index on ties */
+            qsort(b, len, sizeof(okv), cmp_key_desc_idx_asc);
+            const uint64_t take = len < kb ? len : kb;
+            uint32_t sel[64];
+            for (uint64_t i = 0; i < take; ++i) sel[i] = b[i].idx;
+            qsort(sel, take, sizeof(uint32_t), cmp_u32);
+            /* eps = acc - TopK(acc): the selected entries leave, the rest stay */
+            for (uint64_t j = 0; j < len; ++j) e[j0 + j] = acc[j];
+            for (uint64_t i = 0; i < take; ++i) {
+                out_idx[o + i] = sel[i];
+                out_val[o + i] = acc[sel[i] - j0];
+                e[sel[i]] = 0.0f;
+            }
+            o += take;
+        }
+    }
+    free(b);
+    free(acc);
+    return 0;
+}
+
 /* ------------------------------------------------------------------------ */
 /* QSGD stochastic quantization (§2.2, §6).                                  */
 

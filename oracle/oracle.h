@@ -49,6 +49,17 @@ int orc_sparse_reduce(int P, const uint32_t* const* idx, const float* const* val
 int orc_topk(int P, const float* x, uint64_t N, uint64_t k,
              uint32_t* out_idx, float* out_val, float* residual);
 
+/* Bucketed top-k with the error feedback of Alg. 1 (SparCML §8.4: each
+ * group of `bucket` consecutive coordinates sends its kb largest entries;
+ * Alg. 1: acc = eps + alpha * grad, eps = acc - TopK(acc)).  grad and eps
+ * are P rows of N; grad may be NULL (acc = eps).  Per bucket the min(kb,
+ * len) largest magnitudes (key as in orc_topk, lowest index on ties), in
+ * ascending index order; rank r's K = sum over buckets of min(kb, len)
+ * entries start at out_idx/out_val + r*K.  eps is overwritten with acc, the
+ * selected entries set to +0.  kb <= 64. */
+int orc_topk_bucketed(int P, const float* grad, float* eps, uint64_t N, float alpha,
+                      uint64_t bucket, uint64_t kb, uint32_t* out_idx, float* out_val);
+
 /* QSGD stochastic quantization of each stream (SparCML §2.2 "Quantization",
  * §6; scale = the stream's L2 norm).  bits in {2,4,8}; s = 2^(bits-1)-1
  * levels plus a sign bit; codes packed 8/bits per byte, element j in byte

@@ -248,6 +248,32 @@ int sparcml_topk_sparsify(int P, const float* x, uint64_t N, uint64_t k, uint32_
     }
 }
 
+int sparcml_topk_bucketed(int P, const float* grad, float* eps, uint64_t N, float alpha, uint64_t bucket,
+                          uint64_t kb, uint32_t* out_idx, float* out_val, void* stream)
+{
+    try {
+        if (P < 1 || P > 65535) return fail(SPARCML_EINVAL, "P must be in [1, 65535]");
+        if (!valid_n(N)) return fail(SPARCML_EINVAL, "N must be in [1, 2^32)");
+        if (bucket < 64 || bucket > 4096 || (bucket & (bucket - 1)))
+            return fail(SPARCML_EINVAL, "bucket must be a power of two in [64, 4096]");
+        if (kb < 1 || kb > 64) return fail(SPARCML_EINVAL, "kb must be in [1, 64]");
+        if (!eps || !out_idx || !out_val) return fail(SPARCML_EINVAL, "NULL argument");
+        if (isnan(alpha) || isinf(alpha)) return fail(SPARCML_EINVAL, "alpha must be finite");
+        hipError_t e = topk_buckets_run(P, grad, eps, N, alpha, (uint32_t)bucket, (uint32_t)kb, out_idx,
+                                        out_val, (hipStream_t)stream);
+        if (e != hipSuccess) return hip_fail(e, "topk_bucketed");
+        return SPARCML_OK;
+    } catch (const std::exception& ex) {
+        return fail(SPARCML_EHIP, "host exception: %s", ex.what());
+    }
+}
+
+uint64_t sparcml_topk_bucketed_count(uint64_t N, uint64_t bucket, uint64_t kb)
+{
+    if (!valid_n(N) || bucket == 0 || kb == 0) return 0;
+    return topk_buckets_count(N, bucket, kb);
+}
+
 int sparcml_quantize(int P, const sparcml_stream* in, int bits, uint64_t seed, uint8_t* const* out_q,
                      float* out_scale, float* const* out_deq, void* ws, size_t ws_bytes, void* stream)
 {

@@ -37,7 +37,8 @@ enum TimerSlot {
     kTTopkWrite = 6,    // top-k count + scan + write
     kTDensify = 7,
     kTConcat = 8,       // concatenation of disjoint parts
-    kTSlots = 9
+    kTTopkBuckets = 9,  // bucketed top-k with error feedback
+    kTSlots = 10
 };
 void timer_begin(int slot, hipStream_t s);
 void timer_end(int slot, hipStream_t s);
@@ -136,6 +137,11 @@ hipError_t concat_run(int P, const ConcatPart* parts, uint32_t qbits, uint64_t b
 size_t topk_workspace(int P, uint64_t N, uint64_t k);
 hipError_t topk_run(int P, const float* x, uint64_t N, uint64_t k, uint32_t* out_idx,
                     float* out_val, float* residual, void* ws, hipStream_t s);
+
+// Bucketed top-k with error feedback: bucket = 64 * 2^j, 64..4096; kb <= 64.
+uint64_t topk_buckets_count(uint64_t N, uint64_t bucket, uint64_t kb);
+hipError_t topk_buckets_run(int P, const float* grad, float* eps, uint64_t N, float alpha, uint32_t bucket,
+                            uint32_t kb, uint32_t* out_idx, float* out_val, hipStream_t s);
 
 // ---------------------------------------------------------------- QSGD
 size_t quant_workspace(int P, uint64_t max_n);

@@ -56,6 +56,10 @@ def lib() -> ctypes.CDLL:
     L.sparcml_workspace_size.restype = i32
     L.sparcml_topk_sparsify.argtypes = [i32, vp, u64, u64, vp, vp, vp, vp, ctypes.c_size_t, vp]
     L.sparcml_topk_sparsify.restype = i32
+    L.sparcml_topk_bucketed.argtypes = [i32, vp, vp, u64, ctypes.c_float, u64, u64, vp, vp, vp]
+    L.sparcml_topk_bucketed.restype = i32
+    L.sparcml_topk_bucketed_count.argtypes = [u64, u64, u64]
+    L.sparcml_topk_bucketed_count.restype = u64
     L.sparcml_quantize.argtypes = [i32, ctypes.POINTER(Stream), i32, u64, vp, vp, vp, vp,
                                    ctypes.c_size_t, vp]
     L.sparcml_quantize.restype = i32
@@ -87,7 +91,7 @@ def lib() -> ctypes.CDLL:
 
 TIMER_REDUCE_PASS, TIMER_REDUCE_WRITE, TIMER_REDUCE_SLOW = 0, 1, 2
 TIMER_QUANT_NORM, TIMER_QUANT_CODES, TIMER_TOPK_SELECT, TIMER_TOPK_WRITE, TIMER_DENSIFY = 3, 4, 5, 6, 7
-TIMER_CONCAT = 8
+TIMER_CONCAT, TIMER_TOPK_BUCKETED = 8, 9
 
 
 def timing_enable(on: bool) -> None:
@@ -178,6 +182,40 @@ def topk_sparsify(x, k: int, residual=None, ws=None):
                                         _ptr(ws), ws.numel(), _stream_ptr(x.device)),
            "sparcml_topk_sparsify")
     return idx[:, :k], val[:, :k]
+
+
+class TopkBucketedCall:
+    """Repeated bucketed top-k with error feedback (§8.4, Alg. 1) of fixed
+    device rows: eps [P, N] is updated in place; idx / val [P, K]."""
+
+    def __init__(self, eps, grad, alpha: float, bucket: int, kb: int):
+        torch = _torch()
+        _require_cuda(eps, "eps")
+        if eps.dim() != 2 or not eps.is_contiguous() or eps.dtype != torch.float32:
+            raise ValueError("eps must be a contiguous fp32 [P, N] tensor")
+        if grad is not None and (grad.shape != eps.shape or not grad.is_contiguous()
+                                 or grad.dtype != torch.float32):
+            raise ValueError("grad must be a contiguous fp32 tensor shaped like eps")
+        self.P, self.N = eps.shape
+        self.eps, self.grad = eps, grad
+        self.alpha, self.bucket, self.kb = float(alpha), bucket, kb
+        self.K = int(lib().sparcml_topk_bucketed_count(self.N, bucket, kb))
+        self.idx = torch.empty((self.P, max(self.K, 1)), dtype=torch.int32, device=eps.device)
+        self.val = torch.empty((self.P, max(self.K, 1)), dtype=torch.float32, device=eps.device)
+
+    def run(self) -> None:
+        _check(lib().sparcml_topk_bucketed(self.P, _ptr(self.grad), _ptr(self.eps), self.N, self.alpha,
+                                           self.bucket, self.kb, _ptr(self.idx), _ptr(self.val),
+                                           _stream_ptr(self.eps.device)), "sparcml_topk_bucketed")
+
+
+def topk_bucketed(eps, grad, alpha: float, bucket: int, kb: int):
+    """acc = eps + alpha * grad; the kb largest magnitudes of every bucket of
+    ``bucket`` coordinates; eps <- acc with them zeroed (in place).  Returns
+    (idx [P, K] int32, val [P, K] fp32)."""
+    c = TopkBucketedCall(eps, grad, alpha, bucket, kb)
+    c.run()
+    return c.idx[:, : c.K], c.val[:, : c.K]
 
 
 def quantize(vals, bits: int, seed: int, want_deq: bool = False, ws=None):

@@ -23,6 +23,7 @@ def test_header_declares_the_boundary():
     syms = declared_symbols()
     for name in ("sparcml_topk_sparsify", "sparcml_quantize", "sparcml_sparse_reduce",
                  "sparcml_sparse_reduce_range", "sparcml_quantize_bucketed", "sparcml_concat",
+                 "sparcml_topk_bucketed", "sparcml_topk_bucketed_count",
                  "sparcml_densify", "sparcml_workspace_size", "sparcml_strerror",
                  "sparcml_last_error"):
         assert name in syms
@@ -155,6 +156,26 @@ def test_topk_argument_errors():
     assert L.sparcml_topk_sparsify(1, FAKE, 10, 1, None, FAKE, None, FAKE, 1 << 30, None) == S.EINVAL
     assert L.sparcml_topk_sparsify(1, FAKE, 0, 0, FAKE, FAKE, None, FAKE, 1 << 30, None) == S.EINVAL
     assert L.sparcml_topk_sparsify(2, FAKE, 1000, 10, FAKE, FAKE, None, FAKE, 8, None) == S.EWORKSPACE
+
+
+def test_topk_bucketed_argument_errors_and_count():
+    L = S.lib()
+    ok = dict(P=2, g=FAKE, e=FAKE, N=1000, a=0.1, B=512, kb=4, i=FAKE, v=FAKE)
+
+    def rc(**kw):
+        a = dict(ok, **kw)
+        return L.sparcml_topk_bucketed(a["P"], a["g"], a["e"], a["N"], a["a"], a["B"], a["kb"], a["i"], a["v"], None)
+    assert rc(P=0) == S.EINVAL
+    assert rc(N=0) == S.EINVAL
+    assert rc(N=2**32) == S.EINVAL
+    for b in (0, 32, 100, 8192):
+        assert rc(B=b) == S.EINVAL
+    assert rc(kb=0) == S.EINVAL and rc(kb=65) == S.EINVAL
+    assert rc(e=None) == S.EINVAL and rc(i=None) == S.EINVAL
+    assert rc(a=float("nan")) == S.EINVAL
+    cnt = L.sparcml_topk_bucketed_count
+    assert cnt(1000, 512, 4) == 8 and cnt(1000, 512, 500) == 500 + 488 and cnt(3, 512, 4) == 3
+    assert cnt(1 << 24, 512, 4) == (1 << 24) // 128 and cnt(0, 512, 4) == 0
 
 
 def test_quantize_argument_errors():

@@ -555,6 +555,78 @@ def test_topk_special_cases():
 # ---------------------------------------------------------------------------
 # QSGD
 
+def _brute_bucketed(acc, bucket, kb):
+    """Per bucket, numpy lexsort on (index, -|acc| bits): the kb largest
+    magnitudes, lowest index on ties, listed in ascending index order."""
+    P, N = acc.shape
+    keys = (acc.view(np.uint32) & np.uint32(0x7FFFFFFF)).astype(np.int64)
+    idx, val = [], []
+    for r in range(P):
+        ri, rv = [], []
+        for j0 in range(0, N, bucket):
+            j = np.arange(j0, min(j0 + bucket, N))
+            order = np.lexsort((j, -keys[r, j]))
+            sel = np.sort(j[order[:kb]])
+            ri.extend(sel.tolist())
+            rv.extend(acc[r, sel].tolist())
+        idx.append(ri)
+        val.append(rv)
+    return np.array(idx, np.int64), np.array(val, np.float32)
+
+
+def test_topk_bucketed_vs_brute_force():
+    """§8.4 selection with Alg. 1's error feedback: acc = eps + alpha*grad in
+    fp32 (numpy's float32 ops round each step), the kb largest magnitudes of
+    every bucket, and eps' = acc with the selected entries zeroed."""
+    rng = np.random.default_rng(17)
+    for case in range(60):
+        P = int(rng.integers(1, 4))
+        bucket = int(rng.choice([1, 4, 8, 64, 512]))
+        N = int(rng.integers(1, 3 * bucket + 40))
+        kb = int(rng.integers(1, min(bucket, 64) + 1))
+        eps = inputs.laplace(rng, 1.0, P * N).reshape(P, N)
+        grad = inputs.normal(rng, P * N).reshape(P, N)
+        grad[:, : N // 3] = 0.0  # ties at zero magnitude
+        alpha = np.float32(rng.choice([0.0, 0.01, 0.5]))
+        acc = eps + alpha * grad
+        bi, bv = _brute_bucketed(acc, bucket, kb)
+        oi, ov, oe = oracle.topk_bucketed(eps, grad, float(alpha), bucket, kb)
+        assert oi.shape == (P, oracle.bucketed_count(N, bucket, kb))
+        np.testing.assert_array_equal(oi.astype(np.int64), bi)
+        np.testing.assert_array_equal(ov.view(np.uint32), bv.view(np.uint32))
+        want = acc.copy()
+        for r in range(P):
+            want[r, bi[r]] = 0.0
+        np.testing.assert_array_equal(oe.view(np.uint32), want.view(np.uint32))
+
+
+def test_topk_bucketed_one_bucket_is_global_topk_and_feedback_identity():
+    """A bucket covering the row is the global top-k (orc_topk, pinned by
+    numpy above); without a gradient acc = eps; and acc is split exactly
+    into the sent entries plus the new error (Alg. 1)."""
+    rng = np.random.default_rng(18)
+    P, N, kb = 3, 700, 37
+    eps = inputs.laplace(rng, 1.0, P * N).reshape(P, N)
+    oi, ov, oe = oracle.topk_bucketed(eps, None, 1.0, 1024, kb)
+    gi, gv, gres = oracle.topk(eps, kb, residual=True)
+    np.testing.assert_array_equal(oi, gi)
+    np.testing.assert_array_equal(ov, gv)
+    np.testing.assert_array_equal(oe, gres)
+    grad = inputs.normal(rng, P * N).reshape(P, N)
+    oi, ov, oe = oracle.topk_bucketed(eps, grad, 0.1, 64, 4)
+    acc = eps + np.float32(0.1) * grad
+    rebuilt = oe.copy()
+    for r in range(P):
+        assert np.all(oe[r, oi[r].astype(np.int64)] == 0)
+        rebuilt[r, oi[r].astype(np.int64)] = ov[r]
+        # every sent magnitude >= every kept one of the same bucket
+        for j0 in range(0, N, 64):
+            m = (oi[r] >= j0) & (oi[r] < j0 + 64)
+            kept = np.abs(oe[r, j0: j0 + 64])
+            assert np.abs(ov[r][m]).min() >= kept.max()
+    np.testing.assert_array_equal(rebuilt, acc)
+
+
 def test_qsgd_error_bound_levels_and_scale():
     rng = np.random.default_rng(11)
     for bits in (2, 4, 8):
