@@ -28,7 +28,9 @@ Besides the headline line the JSON carries:
                 after at least 0.3 s of warm-up steps, and the split-phase
                 share of c4 and c5 (index range 0 of P equal ones, every
                 rank's stream restricted to it: one node's reduction in the
-                split-allgather allreduce), and c5/dsar: one node's compute
+                split-allgather allreduce), c3/bucketed: c3 with Alg. 1's
+                error feedback and 4 of every 512 coordinates selected
+                (§8.4), and c5/dsar: one node's compute
                 in DSAR with the QSGD dense stage (its share reduced, the
                 dense share quantized 4-bit in buckets of 1024, all P
                 gathered shares decoded into the full vector).
@@ -160,7 +162,7 @@ def empty_arena(sizes, dtype, torch, dev, align=256):
 class Workload:
     """Device-resident inputs, prepared calls and byte accounting of one config."""
 
-    def __init__(self, name, cfg, seed, torch, dev, share=None):
+    def __init__(self, name, cfg, seed, torch, dev, share=None, bucketed=None):
         """``share`` = (s, S): the s-th of S equal index ranges of the
         config's vector, each rank's stream restricted to it (one node's
         work in the split phase of the large-data allreduce)."""
@@ -182,9 +184,29 @@ class Workload:
             self.R = hi - lo
         self.groups = [S.TIMER_REDUCE_PASS, S.TIMER_REDUCE_SLOW, S.TIMER_REDUCE_WRITE]
         self.kernel_bytes = {}
-        if c.kind == "topk":
+        if c.kind == "topk" and bucketed:
+            # Alg. 1 with §8.4's selection: acc = eps + alpha * grad, kb of
+            # every bucket; eps starts at zero and carries over between steps
+            B, kb = bucketed
             x = torch.from_numpy(d["x"]).to(dev)
             del d
+            eps = torch.zeros_like(x)
+            self.topk = S.TopkBucketedCall(eps, x, 0.1, B, kb)
+            K = self.topk.K
+            idx = [self.topk.idx[r, :K] for r in range(c.P)]
+            vals = [self.topk.val[r, :K] for r in range(c.P)]
+            self.nnz = c.P * K
+            self.reduce = S.ReduceCall(idx, c.N, c.delta, vals=vals)
+            self.groups += [S.TIMER_TOPK_BUCKETED]
+            # grad read, eps read and written, K pairs written per rank
+            self.kernel_bytes[S.TIMER_TOPK_BUCKETED] = c.P * c.N * 12 + c.P * K * 8
+            self._steps = [self.topk.run, self.reduce.run]
+            self.topk_step_bytes = self.kernel_bytes[S.TIMER_TOPK_BUCKETED]
+            self._keep = (x, eps)
+        elif c.kind == "topk":
+            x = torch.from_numpy(d["x"]).to(dev)
+            del d
+            self.topk_step_bytes = c.P * c.N * 4 + c.P * c.k * 8
             self.topk = S.TopkCall(x, c.k)
             idx = [self.topk.idx[r] for r in range(c.P)]
             vals = [self.topk.val[r] for r in range(c.P)]
@@ -243,7 +265,7 @@ class Workload:
         if not dense:
             self.kernel_bytes[S.TIMER_REDUCE_WRITE] = red_in + out_bytes
         if c.kind == "topk":
-            self.step_bytes = c.P * c.N * 4 + c.P * c.k * 8 + red_in + out_bytes
+            self.step_bytes = self.topk_step_bytes + red_in + out_bytes
         else:
             self.step_bytes = self.quant_bytes + red_in + out_bytes
 
@@ -355,7 +377,8 @@ def time_steps(w, K, W, torch, warm_s=0.0):
 
 
 GROUP_NAMES = {0: "reduce_tiles", 1: "reduce_write", 2: "reduce_slow", 3: "qsgd_norm",
-               4: "qsgd_codes", 5: "topk_select", 6: "topk_write", 7: "densify", 8: "concat"}
+               4: "qsgd_codes", 5: "topk_select", 6: "topk_write", 7: "densify", 8: "concat",
+               9: "topk_bucketed"}
 
 
 def source_hash() -> str:
@@ -484,7 +507,7 @@ def main() -> int:
 
     per_config = {}
     if not args.no_per_config:
-        for name in ("c1", "c2", "c3", "c4", "c5", "c4/share", "c5/share", "c5/dsar"):
+        for name in ("c1", "c2", "c3", "c4", "c5", "c3/bucketed", "c4/share", "c5/share", "c5/dsar"):
             if name == args.workload:
                 continue
             c = inputs.config(int(name[1]))
@@ -492,10 +515,14 @@ def main() -> int:
             if name.endswith("/dsar"):
                 pw = DsarWorkload(name, c, args.seed, torch, dev)
             else:
-                pw = Workload(name, c, args.seed, torch, dev, share=share)
+                pw = Workload(name, c, args.seed, torch, dev, share=share,
+                              bucketed=(512, 4) if name.endswith("/bucketed") else None)
             pms, pwall, pk, pn, pd = time_steps(pw, max(5, args.steps // 2), 2, torch, warm_s=0.3)
             desc = describe(c) + (f"; split-phase share [{pw.reduce.rng[0]}, {pw.reduce.rng[1]}) "
                                   f"(1 of {c.P})" if share else "")
+            if name.endswith("/bucketed"):
+                desc = (describe(c) + "; Alg. 1 error feedback (acc = eps + 0.1 grad) with 4 of every "
+                        f"512 coordinates ({pw.topk.K} per rank) in place of the global top-k")
             if name.endswith("/dsar"):
                 desc = (f"{c.name} streams in fp32 (P={c.P}, N={c.N}, k={c.k}, delta={c.delta}): "
                         f"share [0, {pw.R}) reduced, QSGD {pw.bits}-bit in buckets of {pw.bucket}, "
@@ -510,7 +537,8 @@ def main() -> int:
                                              if pw.kernel_bytes.get(g) else None} for g, v in pk.items()},
             }
             if c.kind == "topk":
-                tk = sum(pk.get(g, 0.0) for g in (S.TIMER_TOPK_SELECT, S.TIMER_TOPK_WRITE))
+                tk = sum(pk.get(g, 0.0) for g in (S.TIMER_TOPK_SELECT, S.TIMER_TOPK_WRITE,
+                                                  S.TIMER_TOPK_BUCKETED))
                 per_config[name]["topk_input_elems_per_s"] = c.P * c.N / (tk * 1e-3) if tk else None
             log(f"{name}: {pms:.3f} ms/step")
             pw = None

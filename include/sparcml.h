@@ -218,8 +218,11 @@ SPARCML_API int sparcml_quantize_bucketed(int P, const sparcml_stream* in, int b
  * sorted union with values summed (fp32) where indices coincide.  Entries
  * whose sum is zero are kept.  A dense node holds the sum at every index
  * (+0.0 where no rank contributes).  For P == 1 the root is the single
- * stream, dense iff its nnz > thr.
- *   P        power of two, 1 <= P <= 256.
+ * stream, dense iff its nnz > thr.  For P not a power of two (App. A), with
+ * P2 the largest power of two below P, a step in front sums rank P2+i into
+ * rank i (i < P - P2; a tree node under the same rule), then recursive
+ * doubling runs over the P2 participants.
+ *   P        1 <= P <= 256.
  *   streams  host array of P sparse descriptors (is_dense == 0) with the
  *            same qbits (0 = fp32 val, or 2/4/8 = QSGD codes dequantized on
  *            the fly).  Indices strictly ascending and < N (not checked).
@@ -232,11 +235,12 @@ SPARCML_API int sparcml_quantize_bucketed(int P, const sparcml_stream* in, int b
  *            root out->val[0..N).
  *   node_nnz   NULL or device uint64[P-1]: union size of every internal
  *              node (N for dense nodes), level order: level-1 nodes first
- *              (g ascending), root last.
+ *              (g ascending), root last; for P not a power of two the
+ *              P - P2 nodes of the step in front come first.
  *   node_dense NULL or device uint8[P-1]: switch decision per node.
  * Synchronization: the call reads back a 16-byte result header from the
  * device and therefore waits for its own work on `stream`.
- * Errors: EINVAL (including P > 256 or mixed qbits), ECAPACITY (out->nnz
+ * Errors: EINVAL (including P outside [1, 256] or mixed qbits), ECAPACITY (out->nnz
  * below the capacity stated above), EWORKSPACE, EHIP; all but EHIP are
  * detected before any device work is enqueued.
  */

@@ -156,7 +156,7 @@ int orc_sparse_reduce(int P, const uint32_t* const* idx, const float* const* val
                       uint64_t* out_nnz, int* out_dense,
                       uint64_t* node_nnz, uint8_t* node_dense)
 {
-    if (!is_pow2(P) || N == 0 || N > 0xFFFFFFFFull || !(delta > 0.0)) return -1;
+    if (P < 1 || N == 0 || N > 0xFFFFFFFFull || !(delta > 0.0)) return -1;
     if (!idx || !val || !nnz || !out_val || !out_nnz || !out_dense) return -1;
     /* threshold on the number of sparse items (§5.1), as a fraction of N */
     double t = floor(delta * (double)N);
@@ -190,11 +190,38 @@ int orc_sparse_reduce(int P, const uint32_t* const* idx, const float* const* val
         cur[0] = d;
     }
 
+    /* P not a power of two (App. A): a step in front reduces the
+     * participants to the largest power of two P2 <= P -- rank P2 + i sends
+     * its stream to rank i, which sums the two (a tree node under the same
+     * switch rule), for i < P - P2; the other ranks take part unchanged. */
+    int width = P;
+    uint64_t node_base = 0;
+    if (!is_pow2(P)) {
+        int P2 = 1;
+        while (2 * P2 <= P) P2 *= 2;
+        const int rem = P - P2;
+        for (int i = 0; i < rem && rc == 0; ++i) {
+            onode f;
+            rc = sum_pair(&cur[i], &cur[P2 + i], N, thr, &f);
+            if (rc) break;
+            if (node_nnz) node_nnz[i] = f.nnz;
+            if (node_dense) node_dense[i] = (uint8_t)f.dense;
+            node_free(&cur[i]);
+            node_free(&cur[P2 + i]);
+            cur[i] = f;
+        }
+        if (rc) {
+            for (int r = 0; r < P; ++r) node_free(&cur[r]);
+            free(cur);
+            return rc;
+        }
+        width = P2;
+        node_base = (uint64_t)rem;
+    }
+
     /* Recursive doubling (§5.3.1): in round t the partners at distance
      * 2^(t-1) hold the sums of adjacent blocks of 2^(t-1) ranks; their sum is
      * node g of level t, made of nodes 2g and 2g+1 of level t-1. */
-    int width = P;
-    uint64_t node_base = 0;
     while (width > 1) {
         int half = width / 2;
         onode* next = (onode*)calloc((size_t)half, sizeof(onode));

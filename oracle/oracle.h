@@ -32,6 +32,10 @@ void orc_philox4x32_10(const uint32_t ctr[4], const uint32_t key[2], uint32_t ou
  *   node_nnz / node_dense (P-1 entries each, may be NULL): per internal tree
  *   node in level order (level 1 groups first, root last), the union size
  *   (N for a dense node) and the switch decision.
+ *   P need not be a power of two (App. A): with P2 the largest power of two
+ *   <= P, a step in front sums rank P2+i into rank i for i < P-P2 (these
+ *   P-P2 nodes come first in node_nnz / node_dense), then recursive
+ *   doubling runs over the P2 participants.
  * Returns 0, -1 bad arguments, -2 unsorted / out-of-range input, -3 capacity,
  * -4 out of memory. */
 int orc_sparse_reduce(int P, const uint32_t* const* idx, const float* const* val,

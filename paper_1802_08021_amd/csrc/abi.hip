@@ -39,7 +39,7 @@ bool is_pow2(int p) { return p >= 1 && (p & (p - 1)) == 0; }
 int reduce_validate(int P, const sparcml_stream* streams, uint64_t N, double delta, uint32_t* qbits,
                     uint64_t* max_nnz, uint64_t* sum_nnz)
 {
-    if (!is_pow2(P) || P > 256) return fail(SPARCML_EINVAL, "P must be a power of two in [1, 256] (got %d)", P);
+    if (P < 1 || P > 256) return fail(SPARCML_EINVAL, "P must be in [1, 256] (got %d)", P);
     if (!valid_n(N)) return fail(SPARCML_EINVAL, "N must be in [1, 2^32)");
     if (!(delta > 0.0) || isnan(delta)) return fail(SPARCML_EINVAL, "delta must be > 0");
     if (!streams) return fail(SPARCML_EINVAL, "streams is NULL");
@@ -84,6 +84,21 @@ int quant_validate(int P, const sparcml_stream* in, int bits, uint8_t* const* ou
         *max_n = std::max(*max_n, (*n)[r]);
     }
     return SPARCML_OK;
+}
+
+// Ranks of the power-of-two tree that the kernels reduce.  For P not a
+// power of two (App. A), with P2 the largest power of two below P, rank P2+i
+// is summed into rank i first (i < P - P2), then recursive doubling runs
+// over the P2 participants.  That is the tree over 2*P2 ranks in which
+// participant i sits at 2i and its partner P2+i at 2i+1 (empty for i >=
+// P - P2): level 1 is the step in front, the levels above it recursive
+// doubling.
+int tree_ranks(int P)
+{
+    if (is_pow2(P)) return P;
+    int P2 = 1;
+    while (2 * P2 <= P) P2 *= 2;
+    return 2 * P2;
 }
 
 uint64_t threshold(uint64_t N, double delta)
@@ -142,17 +157,23 @@ int reduce_impl(int P, const sparcml_stream* streams, uint64_t N, uint64_t lo, u
         if (out->nnz < cap)
             return fail(SPARCML_ECAPACITY, "out capacity %llu < min(thr, sum nnz) = %llu",
                         (unsigned long long)out->nnz, (unsigned long long)cap);
+        const int PT = tree_ranks(P);
         ReducePlan plan;
-        reduce_plan(P, R, max_nnz, sum_nnz, delta, (int)qbits, &plan, lo);
+        reduce_plan(PT, R, max_nnz, sum_nnz, delta, (int)qbits, &plan, lo);
         const size_t need = reduce_workspace(plan);
         if (!ws || ws_bytes < need) return fail(SPARCML_EWORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
 
-        std::vector<StreamDesc> tab(P);
-        for (int r = 0; r < P; ++r)
-            tab[r] = StreamDesc{streams[r].idx, streams[r].val, streams[r].qval, streams[r].qscale,
-                                streams[r].nnz, 0};
+        // tree slot of every rank; empty slots keep a readable scale pointer
+        std::vector<StreamDesc> tab(PT, StreamDesc{nullptr, nullptr, nullptr, streams[0].qscale, 0, 0});
+        const int P2 = PT == P ? P : PT / 2;
+        for (int r = 0; r < P; ++r) {
+            const int slot = PT == P ? r : (r < P2 ? 2 * r : 2 * (r - P2) + 1);
+            tab[slot] = StreamDesc{streams[r].idx, streams[r].val, streams[r].qval, streams[r].qscale,
+                                   streams[r].nnz, 0};
+        }
+        const uint32_t nfold = PT == P ? (uint32_t)(P / 2) : (uint32_t)(P - P2);
         ReduceResult res{};
-        e = reduce_run(plan, tab.data(), out->idx, out->val, node_nnz, node_dense, ws, s, &res);
+        e = reduce_run(plan, tab.data(), out->idx, out->val, node_nnz, node_dense, ws, s, &res, nfold);
         if (e != hipSuccess) return hip_fail(e, "sparse_reduce");
         out->nnz = res.nnz;
         out->is_dense = res.dense;
@@ -212,12 +233,12 @@ int sparcml_workspace_size(int op, int P, uint64_t N, uint64_t max_nnz, double d
         *bytes = concat_workspace(P);
         return SPARCML_OK;
     case SPARCML_OP_REDUCE: {
-        if (!is_pow2(P) || P > 256 || !valid_n(N) || !(delta > 0.0) || max_nnz > N)
+        if (P < 1 || P > 256 || !valid_n(N) || !(delta > 0.0) || max_nnz > N)
             return fail(SPARCML_EINVAL, "bad reduce sizes");
         ReducePlan p;
         // the call's sum of nnz is at most P * max_nnz, which never needs a
         // smaller workspace than the call itself
-        reduce_plan(P, N, max_nnz, (uint64_t)P * max_nnz, delta, 0, &p);
+        reduce_plan(tree_ranks(P), N, max_nnz, (uint64_t)P * max_nnz, delta, 0, &p);
         *bytes = P == 1 ? 0 : reduce_workspace(p);
         return SPARCML_OK;
     }

@@ -103,9 +103,11 @@ struct ReduceResult {
 };
 
 // Enqueue the whole reduction; writes the root header into *res (host).
+// node_nnz / node_dense receive the level-1 nodes g < nfold and every node
+// above level 1 (nfold = P/2 reports all P - 1 nodes).
 hipError_t reduce_run(const ReducePlan& p, const StreamDesc* host_tab, uint32_t* out_idx,
                       float* out_val, uint64_t* node_nnz, uint8_t* node_dense, void* ws,
-                      hipStream_t s, ReduceResult* res);
+                      hipStream_t s, ReduceResult* res, uint32_t nfold);
 
 // ---------------------------------------------------------------- densify
 // dense[i] = the stream's value at index lo + i, i < N (+0.0 where it has none).

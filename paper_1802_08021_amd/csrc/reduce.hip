@@ -990,9 +990,12 @@ __global__ void k_partition(const StreamDesc* tab, uint32_t* off, uint32_t P, ui
 
 // Switch rule over the tree (§5.1): node dense iff a child is dense or the
 // children's nnz sum exceeds thr; a sparse node's nnz is its union size.
+// Nodes are reported in level order; only the first nfold nodes of level
+// 1 are reported (all of them for a power-of-two rank count: nfold = P/2),
+// the higher levels follow them.
 __global__ void __launch_bounds__(256) k_decide(const StreamDesc* tab, const uint32_t* node_cnt, uint32_t P,
                                                 uint64_t N, uint64_t thr, uint64_t* node_nnz,
-                                                uint8_t* node_dense, ReduceResult* hdr)
+                                                uint8_t* node_dense, ReduceResult* hdr, uint32_t nfold)
 {
     // Stream sizes and node union sizes are read by all threads at once, the
     // rule is applied level by level in LDS, and all threads store.
@@ -1034,9 +1037,10 @@ __global__ void __launch_bounds__(256) k_decide(const StreamDesc* tab, const uin
         hdr->pad = 0;
     }
     __syncthreads();
-    if (t + 1 < P) {
-        if (node_nnz) node_nnz[t] = s_nn[t];
-        if (node_dense) node_dense[t] = s_nd[t];
+    if (t + 1 < P && (t >= P / 2 || t < nfold)) {
+        const uint32_t o = t < P / 2 ? t : t - P / 2 + nfold;
+        if (node_nnz) node_nnz[o] = s_nn[t];
+        if (node_dense) node_dense[o] = s_nd[t];
     }
 }
 
@@ -1206,7 +1210,7 @@ size_t reduce_workspace(const ReducePlan& p) { return layout(p, nullptr).bytes; 
 
 hipError_t reduce_run(const ReducePlan& p, const StreamDesc* host_tab, uint32_t* out_idx,
                       float* out_val, uint64_t* node_nnz, uint8_t* node_dense, void* ws,
-                      hipStream_t s, ReduceResult* res)
+                      hipStream_t s, ReduceResult* res, uint32_t nfold)
 {
     const Layout l = layout(p, ws);
     hipError_t e = upload(l.tab, host_tab, sizeof(StreamDesc) * p.P, s);
@@ -1243,7 +1247,7 @@ hipError_t reduce_run(const ReducePlan& p, const StreamDesc* host_tab, uint32_t*
                           : launch_pass<kCount>(a, p.PK, quant, s);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(k_decide, dim3(1), dim3(256), 0, s, l.tab, l.node_cnt, p.P, p.N, p.thr,
-                       node_nnz, node_dense, l.hdr);
+                       node_nnz, node_dense, l.hdr, nfold);
     if ((e = hipGetLastError()) != hipSuccess) return e;
 
     if (p.speculate_dense) {

@@ -59,7 +59,9 @@ def test_workspace_size_queries():
     assert rc == 0 and n > 0
     rc2, n2 = ws_size(S.OP_REDUCE, 128, 2**27, 2**27 // 10, 0.1)
     assert rc2 == 0 and n2 >= n  # larger max_nnz never needs less
-    assert ws_size(S.OP_REDUCE, 3, 100, 10)[0] == S.EINVAL
+    assert ws_size(S.OP_REDUCE, 0, 100, 10)[0] == S.EINVAL
+    assert ws_size(S.OP_REDUCE, 3, 100, 10)[0] == S.OK  # a tree over 4 slots
+    assert ws_size(S.OP_REDUCE, 257, 100, 10)[0] == S.EINVAL
     assert ws_size(S.OP_REDUCE, 512, 100, 10)[0] == S.EINVAL
     assert ws_size(S.OP_REDUCE, 4, 0, 0)[0] == S.EINVAL
     assert ws_size(S.OP_REDUCE, 4, 2**32, 1)[0] == S.EINVAL
@@ -91,7 +93,6 @@ def reduce_rc(P, arr, N=100, delta=0.5, out=None, ws=FAKE, ws_bytes=1 << 40):
 
 
 def test_reduce_argument_errors():
-    assert reduce_rc(3, streams(3)) == S.EINVAL          # P not a power of two
     assert reduce_rc(0, streams(1)) == S.EINVAL
     assert reduce_rc(512, streams(512)) == S.EINVAL      # beyond the supported P
     assert reduce_rc(4, streams(4), N=0) == S.EINVAL
@@ -131,7 +132,7 @@ def test_reduce_range_argument_errors():
     assert range_rc(4, streams(4), N=2**32, lo=0, hi=5) == S.EINVAL
     assert range_rc(4, streams(4, nnz=11), lo=40, hi=50) == S.EINVAL  # nnz > hi - lo
     assert "range" in S.last_error()
-    assert range_rc(3, streams(3), lo=0, hi=50) == S.EINVAL
+    assert range_rc(0, streams(1), lo=0, hi=50) == S.EINVAL
     # the capacity bound uses the range's threshold: floor(0.5 * 40) = 20 >= 16 entries
     small = S.Stream(FAKE, FAKE, None, None, 15, 0, 0)
     assert range_rc(4, streams(4), lo=30, hi=70, out=small) == S.ECAPACITY

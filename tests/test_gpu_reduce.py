@@ -214,3 +214,37 @@ def test_wave_regions_near_capacity(P, density, bits):
     else:
         for delta in (1.0, 0.01):
             check(idx, val, N, delta, f"near capacity P={P} delta={delta}")
+
+
+@pytest.mark.parametrize("P", [3, 5, 6, 7, 12, 24, 100, 129, 200, 255])
+def test_non_power_of_two_ranks(P):
+    """App. A: rank P2+i joins rank i in a step in front, then recursive
+    doubling over P2 = the largest power of two <= P participants; node
+    decisions and sizes in that order (the step's nodes first)."""
+    rng = np.random.default_rng(700 + P)
+    for N, kmax, delta in ((9001, 400, 0.3), (70001, 3000, 1e-9), (70001, 3000, 8.0), (300007, 20000, 0.05)):
+        idx, val = rand_streams(rng, P, N, kmax)
+        check(idx, val, N, delta, f"P={P}")
+
+
+def test_non_power_of_two_quantized_and_range():
+    from gpu_util import to_dev, torch_dev
+    rng = np.random.default_rng(720)
+    P, N = 48, 200003
+    idx, val = rand_streams(rng, P, N, 6000, dist="laplace")
+    q, scale, deq = oracle.quantize(val, 4, seed=31)
+    torch, dev = torch_dev()
+    codes = [to_dev(a if a.size else np.zeros(1, np.uint8)) for a in q]
+    scales = to_dev(scale)
+    for delta in (0.02, 5.0):
+        say(f"[reduce] P={P} quantized delta={delta}")
+        o = oracle.sparse_reduce(idx, deq, N, delta)
+        g = gpu_reduce(idx, None, N, delta, qbits=4, codes=codes, scales=scales)
+        assert_reduce_equal(g, o, "non-pow2 q4")
+    lo, hi = 50000, 150001
+    si = [a[(a >= lo) & (a < hi)] for a in idx]
+    sv = [v[(a >= lo) & (a < hi)] for a, v in zip(idx, val)]
+    say(f"[reduce] P={P} range")
+    o = oracle.sparse_reduce_range(si, sv, N, lo, hi, 0.1)
+    g = gpu_reduce(si, sv, N, 0.1, rng=(lo, hi))
+    assert_reduce_equal(g, o, "non-pow2 range")

@@ -25,13 +25,27 @@ GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 # ---------------------------------------------------------------------------
 # brute-force references (independent of the oracle's merge / switch code)
 
+def _fold_width(P):
+    """Largest power of two <= P (App. A's participants)."""
+    P2 = 1
+    while 2 * P2 <= P:
+        P2 *= 2
+    return P2
+
+
 def brute_tree(idx_list, val_list, N):
     """P x N dense matrix (absent entries +0.0) reduced by an adjacent-pair
-    tree in fp32 -- the recursive-doubling association of §5.3.1, Fig. 2."""
+    tree in fp32 -- the recursive-doubling association of §5.3.1, Fig. 2 --
+    after App. A's step in front for P not a power of two (row P2+i added
+    into row i)."""
     P = len(idx_list)
     M = np.zeros((P, N), np.float32)
     for r in range(P):
         M[r, idx_list[r]] = val_list[r]
+    P2 = _fold_width(P) if P else 0
+    if P2 != P:
+        M[: P - P2] = M[: P - P2] + M[P2:]
+        M = M[:P2]
     while M.shape[0] > 1:
         M = M[0::2] + M[1::2]
     support = np.unique(np.concatenate([np.asarray(a, np.int64) for a in idx_list])) \
@@ -48,6 +62,16 @@ def brute_decisions(idx_list, N, thr):
     node_nnz, node_dense = [], []
     if len(sets) == 1:
         return [], [], len(sets[0]) > thr
+    P2 = _fold_width(len(sets))
+    if P2 != len(sets):  # App. A: rank P2+i joins rank i first
+        for i in range(len(sets) - P2):
+            d = sizes[i] + sizes[P2 + i] > thr
+            sets[i] = sets[i] | sets[P2 + i]
+            dense[i] = d
+            sizes[i] = N if d else len(sets[i])
+            node_nnz.append(sizes[i])
+            node_dense.append(d)
+        sets, dense, sizes = sets[:P2], dense[:P2], sizes[:P2]
     while len(sets) > 1:
         ns, nd, nz = [], [], []
         for g in range(len(sets) // 2):
@@ -135,8 +159,8 @@ int main() { K e; unsigned a[6];
 
 def test_reduce_random_tiny_vs_brute_force():
     rng = np.random.default_rng(1)
-    for case in range(400):
-        P = int(rng.choice([1, 2, 4, 8, 16]))
+    for case in range(600):
+        P = int(rng.choice([1, 2, 3, 4, 5, 6, 7, 8, 12, 16, 24]))
         N = int(rng.integers(1, 65))
         delta = float(rng.choice([1e-9, 0.05, 0.25, 0.5, 1.0, 3.0]))
         idx, val = [], []
@@ -474,6 +498,33 @@ def test_dsar_gathered_quantized_shares_within_one_level():
         assert np.all(c["val"][units == 0] == 0) and np.all(full[units == 0] == 0)
 
 
+def test_reduce_non_power_of_two_exhaustive_three_ranks():
+    """App. A with P = 3: rank 2 joins rank 0 first, then the two
+    participants are summed -- every subset pattern of N = 3."""
+    N = 3
+    subsets = [s for n in range(N + 1) for s in itertools.combinations(range(N), n)]
+    rng = np.random.default_rng(19)
+    for combo in itertools.product(subsets, repeat=3):
+        idx = [np.array(s, np.uint32) for s in combo]
+        val = [inputs.normal(rng, len(s)) for s in combo]
+        for delta in (1.0 / 3.0, 2.0 / 3.0, 1.0):
+            check_reduce_against_brute(idx, val, N, delta)
+
+
+def test_reduce_non_power_of_two_association():
+    """Values where the App. A order ((r0 + r2) + r1) differs in fp32 from
+    the rank order ((r0 + r1) + r2)."""
+    a, b, c = np.float32(1.0), np.float32(2.0**-24), np.float32(-1.0)
+    want = (a + c) + b
+    assert want != (a + b) + c
+    idx = [np.array([2], np.uint32)] * 3
+    val = [np.array([v], np.float32) for v in (a, b, c)]
+    for delta in (1e-9, 1.0):
+        r = oracle.sparse_reduce(idx, val, 4, delta)
+        v = r["val"][2] if r["dense"] else r["val"][0]
+        assert v.view(np.uint32) == np.float32(want).view(np.uint32)
+
+
 def test_reduce_rejects_bad_input():
     N = 10
     good = [np.array([1, 2], np.uint32)] * 2
@@ -483,7 +534,7 @@ def test_reduce_rejects_bad_input():
     with pytest.raises(oracle.OracleError):
         oracle.sparse_reduce([np.array([1, 10], np.uint32)] * 2, v, N, 0.5)
     with pytest.raises(oracle.OracleError):
-        oracle.sparse_reduce([good[0]] * 3, [v[0]] * 3, N, 0.5)  # P not a power of two
+        oracle.sparse_reduce([], [], N, 0.5)  # no rank
     with pytest.raises(oracle.OracleError):
         oracle.sparse_reduce(good, v, N, 0.0)
 
