@@ -28,7 +28,8 @@ Besides the headline line the JSON carries:
                 after at least 0.3 s of warm-up steps, and the split-phase
                 share of c4 and c5 (index range 0 of P equal ones, every
                 rank's stream restricted to it: one node's reduction in the
-                split-allgather allreduce), c3/bucketed: c3 with Alg. 1's
+                split-allgather allreduce), c4/p48: c4 with 48 ranks (App.
+                A's step in front), c3/bucketed: c3 with Alg. 1's
                 error feedback and 4 of every 512 coordinates selected
                 (§8.4), and c5/dsar: one node's compute
                 in DSAR with the QSGD dense stage (its share reduced, the
@@ -40,6 +41,7 @@ Only one GPU is used; --gpus above 1 exits with a message.
 from __future__ import annotations
 
 import argparse
+import dataclasses
 import hashlib
 import json
 import os
@@ -69,6 +71,8 @@ def parse():
     p.add_argument("--workload", default="c5", choices=["c1", "c2", "c3", "c4", "c5"])
     p.add_argument("--seed", type=int, default=0)
     p.add_argument("--no-per-config", action="store_true")
+    p.add_argument("--configs", default=None,
+                   help="comma-separated per-config workloads to run (others and the seed sweep skipped)")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--calibrate-copy", action="store_true",
                    help="only run a plain 1 GiB device copy (3 times): the reference for "
@@ -490,7 +494,7 @@ def main() -> int:
 
     # the same step over further seeds (fresh inputs): median and quartiles
     seeds = None
-    if not args.no_per_config:
+    if not args.no_per_config and args.configs is None:
         per_seed = [ms]
         for sd in range(args.seed + 1, args.seed + 5):
             sw = Workload(args.workload, head_cfg, sd, torch, dev)
@@ -507,10 +511,13 @@ def main() -> int:
 
     per_config = {}
     if not args.no_per_config:
-        for name in ("c1", "c2", "c3", "c4", "c5", "c3/bucketed", "c4/share", "c5/share", "c5/dsar"):
-            if name == args.workload:
+        for name in ("c1", "c2", "c3", "c4", "c5", "c3/bucketed", "c4/p48", "c4/share", "c5/share",
+                     "c5/dsar"):
+            if name == args.workload or (args.configs is not None and name not in args.configs.split(",")):
                 continue
             c = inputs.config(int(name[1]))
+            if name.endswith("/p48"):  # a rank count that is not a power of two
+                c = dataclasses.replace(c, P=48)
             share = (0, c.P) if name.endswith("/share") else None
             if name.endswith("/dsar"):
                 pw = DsarWorkload(name, c, args.seed, torch, dev)

@@ -2,14 +2,15 @@
 // consecutive coordinates sends its kb largest entries and keeps the rest;
 // Alg. 1: acc = eps + alpha * grad, eps = acc - TopK(acc)).
 //
-// One wave per bucket, B = 64 * EPT: lane l holds the EPT consecutive
-// coordinates at l * EPT, so a wave reads and writes its bucket with
-// coalesced 16-byte accesses.  Selection is kb rounds of a wave-wide maximum
+// One wave per bucket, B = 64 * EPT: each lane holds EPT coordinates, 4
+// consecutive ones in each 256-coordinate group, so that every wave-wide
+// load or store is one contiguous kilobyte.  Selection is kb rounds of a wave-wide maximum
 // over 64-bit keys (|acc| bits above the complemented index: the largest
 // magnitude wins, the lowest index on ties); each lane then writes its
-// selected entries at its prefix count, which lists the bucket's entries in
-// ascending index order.  The kernel is HBM-bound: acc is formed, selected
-// and written back in registers (grad and eps read once, eps written once).
+// selected entries at its prefix count in LDS, which lists the bucket's
+// entries in ascending index order, and kb lanes store them at once.  The
+// kernel is HBM-bound: acc is formed, selected and written back in
+// registers (grad and eps read once, eps written once).
 #include "internal.h"
 
 #include <algorithm>
@@ -32,46 +33,52 @@ __global__ void __launch_bounds__(256) k_topk_buckets(const float* grad, float* 
                                                       uint32_t nb, uint32_t kb, uint64_t K, uint32_t* out_idx,
                                                       float* out_val)
 {
+    // Lane l holds G = min(EPT, 4) consecutive coordinates in each of NG
+    // groups: coordinate u * 64G + l * G + k, so every wave-wide access of a
+    // group is one contiguous run of 64G floats (whole cache lines).
+    constexpr int G = EPT < 4 ? EPT : 4;
+    constexpr int NG = EPT / G;
     constexpr uint32_t B = 64u * EPT;
     const uint32_t lane = threadIdx.x & 63u;
-    const uint32_t q = blockIdx.x * 4u + (threadIdx.x >> 6);  // bucket
-    if (q >= nb) return;                                    // whole wave
+    const uint32_t wv = threadIdx.x >> 6;
+    const uint32_t q = blockIdx.x * 4u + wv;  // bucket
+    if (q >= nb) return;                      // whole wave
     const uint32_t r = blockIdx.y;
     const uint32_t j0 = q * B;
     const uint32_t len = min(B, N - j0);
     float* e = eps + (uint64_t)r * N + j0;
     const float* g = grad ? grad + (uint64_t)r * N + j0 : nullptr;
-    const uint32_t c0 = lane * EPT;  // this lane's first coordinate in the bucket
-    const bool vec = EPT >= 4 && len == B &&
+    const bool vec = G == 4 && len == B &&
                      ((reinterpret_cast<uintptr_t>(e) | (g ? reinterpret_cast<uintptr_t>(g) : 0u)) & 15u) == 0;
 
-    float acc[EPT];
+    float acc[EPT];  // acc[u * G + k]: coordinate u * 64G + lane * G + k
     if (vec) {
 #pragma unroll
-        for (int i = 0; i < EPT; i += 4) {
-            float4 a = *reinterpret_cast<const float4*>(e + c0 + i);
+        for (int u = 0; u < NG; ++u) {
+            const uint32_t c = u * 256u + lane * 4u;
+            float4 v = *reinterpret_cast<const float4*>(e + c);
             if (g) {
-                const float4 b = *reinterpret_cast<const float4*>(g + c0 + i);
-                a.x = __fadd_rn(a.x, __fmul_rn(alpha, b.x));
-                a.y = __fadd_rn(a.y, __fmul_rn(alpha, b.y));
-                a.z = __fadd_rn(a.z, __fmul_rn(alpha, b.z));
-                a.w = __fadd_rn(a.w, __fmul_rn(alpha, b.w));
+                const float4 w = *reinterpret_cast<const float4*>(g + c);
+                v.x = __fadd_rn(v.x, __fmul_rn(alpha, w.x));
+                v.y = __fadd_rn(v.y, __fmul_rn(alpha, w.y));
+                v.z = __fadd_rn(v.z, __fmul_rn(alpha, w.z));
+                v.w = __fadd_rn(v.w, __fmul_rn(alpha, w.w));
             }
-            acc[i] = a.x;
-            acc[i + 1] = a.y;
-            acc[i + 2] = a.z;
-            acc[i + 3] = a.w;
+            acc[u * 4] = v.x;
+            acc[u * 4 + 1] = v.y;
+            acc[u * 4 + 2] = v.z;
+            acc[u * 4 + 3] = v.w;
         }
     } else {
 #pragma unroll
         for (int i = 0; i < EPT; ++i) {
-            const uint32_t c = c0 + i;
-            float a = 0.0f;
+            const uint32_t c = (i / G) * 64u * G + lane * G + (i % G);
+            float v = 0.0f;
             if (c < len) {
-                a = e[c];
-                if (g) a = __fadd_rn(a, __fmul_rn(alpha, g[c]));
+                v = e[c];
+                if (g) v = __fadd_rn(v, __fmul_rn(alpha, g[c]));
             }
-            acc[i] = a;
+            acc[i] = v;
         }
     }
 
@@ -80,11 +87,11 @@ __global__ void __launch_bounds__(256) k_topk_buckets(const float* grad, float* 
     uint64_t key[EPT];
 #pragma unroll
     for (int i = 0; i < EPT; ++i) {
-        const uint32_t c = c0 + i;
+        const uint32_t c = (i / G) * 64u * G + lane * G + (i % G);
         key[i] = c < len ? ((uint64_t)(__float_as_uint(acc[i]) & 0x7FFFFFFFu) << 32) | (0xFFFFFFFFu - (j0 + c))
                          : 0ull;
     }
-    uint64_t taken = 0;  // bit i: coordinate c0 + i selected
+    uint64_t taken = 0;  // bit i: acc[i] selected
     const uint32_t take = min(kb, len);
     for (uint32_t t = 0; t < take; ++t) {
         uint64_t best = 0;
@@ -100,27 +107,49 @@ __global__ void __launch_bounds__(256) k_topk_buckets(const float* grad, float* 
         }
     }
 
-    // selected entries in ascending index order at the bucket's output
-    // offset (every bucket before the last one contributes kb)
-    const uint32_t cnt = (uint32_t)__popcll(taken);
-    const uint32_t excl = wave_scan(cnt) - cnt;
-    uint64_t o = (uint64_t)r * K + (uint64_t)q * kb + excl;
+    // Selected entries in ascending index order (group, then lane, then k):
+    // each lane stages its own in the wave's LDS row at the count of
+    // selected entries before them, then lanes 0..take-1 write the bucket's
+    // output (offset q * kb: every bucket before the last contributes kb)
+    // with one coalesced store per array.
+    __shared__ uint32_t s_i[4][64];
+    __shared__ float s_v[4][64];
+    uint32_t before = 0;  // selected entries of earlier groups
 #pragma unroll
-    for (int i = 0; i < EPT; ++i) {
-        if ((taken >> i) & 1ull) {
-            out_idx[o] = j0 + c0 + i;
-            out_val[o] = acc[i];
-            ++o;
-            acc[i] = 0.0f;  // eps = acc - TopK(acc)
+    for (int u = 0; u < NG; ++u) {
+        const uint32_t bits = (uint32_t)((taken >> (u * G)) & ((1u << G) - 1u));
+        const uint32_t cnt = (uint32_t)__popc(bits);
+        const uint32_t incl = wave_scan(cnt);
+        uint32_t pos = before + incl - cnt;
+#pragma unroll
+        for (int k = 0; k < G; ++k) {
+            if ((bits >> k) & 1u) {
+                s_i[wv][pos] = j0 + u * 64u * G + lane * G + k;
+                s_v[wv][pos] = acc[u * G + k];
+                ++pos;
+                acc[u * G + k] = 0.0f;  // eps = acc - TopK(acc)
+            }
         }
+        before += (uint32_t)__builtin_amdgcn_readlane((int)incl, 63);
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    if (lane < take) {
+        const uint64_t o = (uint64_t)r * K + (uint64_t)q * kb + lane;
+        out_idx[o] = s_i[wv][lane];
+        out_val[o] = s_v[wv][lane];
     }
     if (vec) {
 #pragma unroll
-        for (int i = 0; i < EPT; i += 4) store_nt(e + c0 + i, make_float4(acc[i], acc[i + 1], acc[i + 2], acc[i + 3]));
+        for (int u = 0; u < NG; ++u)
+            store_nt(e + u * 256u + lane * 4u, make_float4(acc[u * 4], acc[u * 4 + 1], acc[u * 4 + 2], acc[u * 4 + 3]));
     } else {
 #pragma unroll
-        for (int i = 0; i < EPT; ++i)
-            if (c0 + i < len) e[c0 + i] = acc[i];
+        for (int i = 0; i < EPT; ++i) {
+            const uint32_t c = (i / G) * 64u * G + lane * G + (i % G);
+            if (c < len) e[c] = acc[i];
+        }
     }
 }
 
