@@ -17,6 +17,8 @@
  *   sparcml_sparse_reduce_range -- the same over one index range: a node's
  *                             share of the split phase of the large-data
  *                             allreduce (§5.3.2)
+ *   sparcml_sparse_reduce_async -- either reduce without waiting (result
+ *                             header written on the device)
  *   sparcml_concat         -- gathered shares summed as a concatenation
  *                             (§5.1 case (2), §5.3.2), QSGD parts decoded
  *   sparcml_densify        -- dense representation of one stream (§5.1)
@@ -187,6 +189,15 @@ SPARCML_API int sparcml_quantize(int P, const sparcml_stream* in, int bits, uint
                      void* ws, size_t ws_bytes, void* stream);
 
 /*
+ * Root header of an asynchronous reduction, written by the device.
+ */
+typedef struct sparcml_result {
+    uint64_t nnz;      /* root nnz (the range's length if dense) */
+    uint32_t is_dense; /* root representation */
+    uint32_t reserved;
+} sparcml_result;
+
+/*
  * Bucketed QSGD (§6 "Supporting Low-Precision Communication": a stream is
  * split into buckets of B consecutive entries, each quantized on its own
  * with a full-precision scale; the paper uses B in the order of 1024 and
@@ -273,6 +284,27 @@ SPARCML_API int sparcml_sparse_reduce_range(int P, const sparcml_stream* streams
                                 uint64_t lo, uint64_t hi, double delta, sparcml_stream* out,
                                 uint64_t* node_nnz, uint8_t* node_dense, void* ws,
                                 size_t ws_bytes, void* stream);
+
+/*
+ * sparcml_sparse_reduce_range without any host round trip: the same
+ * computation and outputs, but the root header goes to `result` (DEVICE
+ * memory, written in stream order) instead of being read back, and the call
+ * returns once the work is enqueued.  The passes that write a sparse root
+ * are always enqueued and return at once on the device when the root is
+ * dense, so the call enqueues the same work whatever the data, never waits,
+ * and can be captured in a HIP graph (it issues no memset and no host copy;
+ * the descriptor table travels in kernel arguments).  With lo == 0 and
+ * hi == N it is sparcml_sparse_reduce.
+ *   out      read only: out->idx (capacity out->nnz, as for
+ *            sparcml_sparse_reduce) and out->val; out itself is not
+ *            written.
+ *   result   device pointer to one sparcml_result.
+ * Errors: as for sparcml_sparse_reduce_range, EINVAL for a NULL result.
+ */
+SPARCML_API int sparcml_sparse_reduce_async(int P, const sparcml_stream* streams, uint64_t N, uint64_t lo,
+                                uint64_t hi, double delta, const sparcml_stream* out,
+                                uint64_t* node_nnz, uint8_t* node_dense, sparcml_result* result,
+                                void* ws, size_t ws_bytes, void* stream);
 
 /*
  * The allgather phase of the split-allgather allreduce (§5.3.2), the local

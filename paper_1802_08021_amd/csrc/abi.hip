@@ -4,6 +4,7 @@
 #include "internal.h"
 
 #include <math.h>
+#include <stddef.h>
 #include <stdarg.h>
 #include <stdio.h>
 #include <string.h>
@@ -11,6 +12,11 @@
 #include <algorithm>
 #include <exception>
 #include <vector>
+
+static_assert(sizeof(sparcml_result) == sizeof(sparcml::ReduceResult) &&
+                  offsetof(sparcml_result, nnz) == offsetof(sparcml::ReduceResult, nnz) &&
+                  offsetof(sparcml_result, is_dense) == offsetof(sparcml::ReduceResult, dense),
+              "the device writes sparcml_result as a ReduceResult");
 
 using namespace sparcml;
 
@@ -109,10 +115,12 @@ uint64_t threshold(uint64_t N, double delta)
 
 // The reduction of the index range [lo, hi) of N (the whole vector: [0, N)):
 // every stream's indices lie in the range; a dense result holds hi - lo
-// values (index lo + i at i), a sparse one absolute indices.
+// values (index lo + i at i), a sparse one absolute indices.  result ==
+// NULL: the root header is read back into *out; otherwise it is written to
+// result (device) and the call does not wait.
 int reduce_impl(int P, const sparcml_stream* streams, uint64_t N, uint64_t lo, uint64_t hi, double delta,
                 sparcml_stream* out, uint64_t* node_nnz, uint8_t* node_dense, void* ws, size_t ws_bytes,
-                void* stream)
+                void* stream, sparcml_result* result = nullptr)
 {
     try {
         uint32_t qbits;
@@ -127,13 +135,17 @@ int reduce_impl(int P, const sparcml_stream* streams, uint64_t N, uint64_t lo, u
         const hipStream_t s = (hipStream_t)stream;
         hipError_t e;
 
+        ReduceResult* dres = reinterpret_cast<ReduceResult*>(result);
         if (P == 1) {
             const sparcml_stream& a = streams[0];
             if (a.nnz > thr) {
                 e = densify_run(a.idx, a.val, a.qval, a.qscale, qbits, a.nnz, R, 0, out->val, s, lo);
+                if (e == hipSuccess && dres) e = set_result_run(dres, R, 1, s);
                 if (e != hipSuccess) return hip_fail(e, "densify");
-                out->nnz = R;
-                out->is_dense = 1;
+                if (!dres) {
+                    out->nnz = R;
+                    out->is_dense = 1;
+                }
                 return SPARCML_OK;
             }
             if (a.nnz && !out->idx) return fail(SPARCML_EINVAL, "out->idx is NULL");
@@ -147,8 +159,12 @@ int reduce_impl(int P, const sparcml_stream* streams, uint64_t N, uint64_t lo, u
                                                hipMemcpyDeviceToDevice, s);
                 if (e != hipSuccess) return hip_fail(e, "copy");
             }
-            out->nnz = a.nnz;
-            out->is_dense = 0;
+            if (dres) {
+                if ((e = set_result_run(dres, a.nnz, 0, s)) != hipSuccess) return hip_fail(e, "result");
+            } else {
+                out->nnz = a.nnz;
+                out->is_dense = 0;
+            }
             return SPARCML_OK;
         }
 
@@ -173,10 +189,12 @@ int reduce_impl(int P, const sparcml_stream* streams, uint64_t N, uint64_t lo, u
         }
         const uint32_t nfold = PT == P ? (uint32_t)(P / 2) : (uint32_t)(P - P2);
         ReduceResult res{};
-        e = reduce_run(plan, tab.data(), out->idx, out->val, node_nnz, node_dense, ws, s, &res, nfold);
+        e = reduce_run(plan, tab.data(), out->idx, out->val, node_nnz, node_dense, ws, s, &res, nfold, dres);
         if (e != hipSuccess) return hip_fail(e, "sparse_reduce");
-        out->nnz = res.nnz;
-        out->is_dense = res.dense;
+        if (!dres) {
+            out->nnz = res.nnz;
+            out->is_dense = res.dense;
+        }
         return SPARCML_OK;
     } catch (const std::exception& ex) {
         return fail(SPARCML_EHIP, "host exception: %s", ex.what());
@@ -404,6 +422,19 @@ int sparcml_concat(int P, const sparcml_stream* parts, const uint64_t* bounds, u
     } catch (const std::exception& ex) {
         return fail(SPARCML_EHIP, "host exception: %s", ex.what());
     }
+}
+
+int sparcml_sparse_reduce_async(int P, const sparcml_stream* streams, uint64_t N, uint64_t lo, uint64_t hi,
+                                double delta, const sparcml_stream* out, uint64_t* node_nnz,
+                                uint8_t* node_dense, sparcml_result* result, void* ws, size_t ws_bytes,
+                                void* stream)
+{
+    if (!valid_n(N)) return fail(SPARCML_EINVAL, "N must be in [1, 2^32)");
+    if (!(lo < hi && hi <= N)) return fail(SPARCML_EINVAL, "need 0 <= lo < hi <= N");
+    if (!result) return fail(SPARCML_EINVAL, "result is NULL");
+    if (!out) return fail(SPARCML_EINVAL, "out is NULL");
+    sparcml_stream o = *out;  // capacity and pointers only; never written
+    return reduce_impl(P, streams, N, lo, hi, delta, &o, node_nnz, node_dense, ws, ws_bytes, stream, result);
 }
 
 int sparcml_densify(const sparcml_stream* in, uint64_t N, float* dense, void* stream)

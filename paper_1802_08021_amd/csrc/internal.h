@@ -102,12 +102,18 @@ struct ReduceResult {
     uint32_t pad;
 };
 
-// Enqueue the whole reduction; writes the root header into *res (host).
+// *r = {nnz, dense} on the device, in stream order.
+hipError_t set_result_run(ReduceResult* r, uint64_t nnz, uint32_t dense, hipStream_t s);
+
+// Enqueue the whole reduction.  dev_result == NULL: waits for the root
+// header and writes it into *res (host).  Otherwise the header goes to
+// dev_result (device) and nothing waits: the sparse-output passes are
+// enqueued unconditionally and skip themselves on a dense root.
 // node_nnz / node_dense receive the level-1 nodes g < nfold and every node
 // above level 1 (nfold = P/2 reports all P - 1 nodes).
 hipError_t reduce_run(const ReducePlan& p, const StreamDesc* host_tab, uint32_t* out_idx,
                       float* out_val, uint64_t* node_nnz, uint8_t* node_dense, void* ws,
-                      hipStream_t s, ReduceResult* res, uint32_t nfold);
+                      hipStream_t s, ReduceResult* res, uint32_t nfold, ReduceResult* dev_result);
 
 // ---------------------------------------------------------------- densify
 // dense[i] = the stream's value at index lo + i, i < N (+0.0 where it has none).

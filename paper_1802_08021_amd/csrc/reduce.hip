@@ -93,6 +93,7 @@ struct Args {
     uint32_t P, L, N, T, ntiles, nchunks, tpc, qbits;
     uint32_t out_vec;          // out_val is 16-byte aligned
     uint32_t lo;               // first index of the range [lo, lo + N); dense output is relative
+    const ReduceResult* skip;  // sparse-output passes: return at once if skip->dense (NULL: never)
 };
 
 __device__ __forceinline__ uint32_t lower_bound(const uint32_t* a, uint32_t lo, uint32_t hi,
@@ -238,6 +239,7 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
     constexpr int PW = (PMAX + 31) / 32;        // rank-mask words
     constexpr uint32_t RROWS = PMAX >= 256 ? 2u : 4u;  // indices per wave in the row walk
     constexpr uint32_t RK = PMAX / 16;                  // ranks per lane in the row walk
+    if (MODE == kSparseWrite && a.skip && a.skip->dense) return;  // the root is dense: nothing to write
     static_assert(NW * RROWS * (PMAX + PW) <= 2 * NW * (int)ERGN, "walk buffers alias the entry regions");
 
     // Per index: arrivals | (sum of the arrived ranks) << 16 -- the second
@@ -837,6 +839,7 @@ template <int MW, int MODE, bool QUANT>
 __global__ void __launch_bounds__(kSlowNT) k_slow(Args a)
 {
     constexpr int NT = kSlowNT, TS = kSlowTS, LMAX = SlowShape<MW>::LMAX, PMAX = 32 * MW;
+    if (MODE == kSparseWrite && a.skip && a.skip->dense) return;  // the root is dense: nothing to write
     __shared__ float s_slot[LMAX][TS];
     __shared__ float s_curv[TS];
     __shared__ int16_t s_last[TS];
@@ -995,7 +998,8 @@ __global__ void k_partition(const StreamDesc* tab, uint32_t* off, uint32_t P, ui
 // the higher levels follow them.
 __global__ void __launch_bounds__(256) k_decide(const StreamDesc* tab, const uint32_t* node_cnt, uint32_t P,
                                                 uint64_t N, uint64_t thr, uint64_t* node_nnz,
-                                                uint8_t* node_dense, ReduceResult* hdr, uint32_t nfold)
+                                                uint8_t* node_dense, ReduceResult* hdr, uint32_t nfold,
+                                                ReduceResult* result)
 {
     // Stream sizes and node union sizes are read by all threads at once, the
     // rule is applied level by level in LDS, and all threads store.
@@ -1035,6 +1039,7 @@ __global__ void __launch_bounds__(256) k_decide(const StreamDesc* tab, const uin
         hdr->nnz = s_n[0];
         hdr->dense = s_d[0];
         hdr->pad = 0;
+        if (result) *result = ReduceResult{s_n[0], s_d[0], 0u};
     }
     __syncthreads();
     if (t + 1 < P && (t >= P / 2 || t < nfold)) {
@@ -1044,11 +1049,17 @@ __global__ void __launch_bounds__(256) k_decide(const StreamDesc* tab, const uin
     }
 }
 
+__global__ void k_set_result(ReduceResult* r, uint64_t nnz, uint32_t dense)
+{
+    if (threadIdx.x == 0) *r = ReduceResult{nnz, dense, 0u};
+}
+
 // Exclusive scan of the per-tile root union sizes (one workgroup); also
 // clears the deferred-tile counter for the write pass.
 __global__ void __launch_bounds__(1024) k_scan_tiles(const uint32_t* cnt, uint32_t* off, uint32_t n,
-                                                     uint32_t* slow_count)
+                                                     uint32_t* slow_count, const ReduceResult* skip)
 {
+    if (skip && skip->dense) return;  // the root is dense: no sparse output
     __shared__ uint32_t s_wsum[16];
     const uint32_t tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const uint32_t per = (n + 1023) / 1024;
@@ -1208,9 +1219,15 @@ int reduce_plan(int P, uint64_t N, uint64_t max_nnz, uint64_t sum_nnz, double de
 
 size_t reduce_workspace(const ReducePlan& p) { return layout(p, nullptr).bytes; }
 
+hipError_t set_result_run(ReduceResult* r, uint64_t nnz, uint32_t dense, hipStream_t s)
+{
+    hipLaunchKernelGGL(k_set_result, dim3(1), dim3(64), 0, s, r, nnz, dense);
+    return hipGetLastError();
+}
+
 hipError_t reduce_run(const ReducePlan& p, const StreamDesc* host_tab, uint32_t* out_idx,
                       float* out_val, uint64_t* node_nnz, uint8_t* node_dense, void* ws,
-                      hipStream_t s, ReduceResult* res, uint32_t nfold)
+                      hipStream_t s, ReduceResult* res, uint32_t nfold, ReduceResult* dev_result)
 {
     const Layout l = layout(p, ws);
     hipError_t e = upload(l.tab, host_tab, sizeof(StreamDesc) * p.P, s);
@@ -1247,9 +1264,18 @@ hipError_t reduce_run(const ReducePlan& p, const StreamDesc* host_tab, uint32_t*
                           : launch_pass<kCount>(a, p.PK, quant, s);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(k_decide, dim3(1), dim3(256), 0, s, l.tab, l.node_cnt, p.P, p.N, p.thr,
-                       node_nnz, node_dense, l.hdr, nfold);
+                       node_nnz, node_dense, l.hdr, nfold, dev_result);
     if ((e = hipGetLastError()) != hipSuccess) return e;
 
+    if (dev_result) {
+        // No host round trip: the sparse-output passes are always enqueued
+        // and return at once on the device when the root is dense.
+        a.skip = p.speculate_dense ? l.hdr : nullptr;
+        hipLaunchKernelGGL(k_scan_tiles, dim3(1), dim3(1024), 0, s, l.tile_cnt, l.tile_off, p.ntiles,
+                           l.slow_count, a.skip);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        return launch_pass<kSparseWrite>(a, p.PK, quant, s);
+    }
     if (p.speculate_dense) {
         if ((e = hipMemcpyAsync(res, l.hdr, sizeof(ReduceResult), hipMemcpyDeviceToHost, s)) !=
             hipSuccess)
@@ -1259,7 +1285,7 @@ hipError_t reduce_run(const ReducePlan& p, const StreamDesc* host_tab, uint32_t*
     }
     // Sparse root: positions from the per-tile union sizes, then write.
     hipLaunchKernelGGL(k_scan_tiles, dim3(1), dim3(1024), 0, s, l.tile_cnt, l.tile_off, p.ntiles,
-                       l.slow_count);
+                       l.slow_count, nullptr);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if ((e = launch_pass<kSparseWrite>(a, p.PK, quant, s)) != hipSuccess) return e;
     if ((e = hipMemcpyAsync(res, l.hdr, sizeof(ReduceResult), hipMemcpyDeviceToHost, s)) !=

@@ -72,6 +72,9 @@ def lib() -> ctypes.CDLL:
     L.sparcml_sparse_reduce_range.argtypes = [i32, ctypes.POINTER(Stream), u64, u64, u64, ctypes.c_double,
                                               ctypes.POINTER(Stream), vp, vp, vp, ctypes.c_size_t, vp]
     L.sparcml_sparse_reduce_range.restype = i32
+    L.sparcml_sparse_reduce_async.argtypes = [i32, ctypes.POINTER(Stream), u64, u64, u64, ctypes.c_double,
+                                              ctypes.POINTER(Stream), vp, vp, vp, vp, ctypes.c_size_t, vp]
+    L.sparcml_sparse_reduce_async.restype = i32
     L.sparcml_concat.argtypes = [i32, ctypes.POINTER(Stream), ctypes.POINTER(u64), u64, ctypes.c_double, u64,
                                  ctypes.POINTER(Stream), vp, ctypes.c_size_t, vp]
     L.sparcml_concat.restype = i32
@@ -483,6 +486,25 @@ class ReduceCall:
         self.ws = alloc_workspace(nbytes, self.dev)
         self.out = Stream(_ptr(self.out_idx), _ptr(self.out_val), None, None, self.out_idx.numel(), 0, 0)
         self._keep = (idx, vals, codes, scales)
+
+    def run_async(self):
+        """Enqueue the reduction without waiting (capturable in a HIP
+        graph); the root header lands in ``self.result`` (device int64 [2]:
+        nnz, dense flag in the low word of the second)."""
+        if not hasattr(self, "result"):
+            torch = _torch()
+            self.result = torch.zeros(2, dtype=torch.int64, device=self.dev)
+        self.out.nnz = self.out_idx.numel()
+        lo, hi = self.rng if self.rng is not None else (0, self.N)
+        _check(lib().sparcml_sparse_reduce_async(
+            self.P, self.arr, self.N, lo, hi, self.delta, ctypes.byref(self.out), _ptr(self.node_nnz),
+            _ptr(self.node_dense), _ptr(self.result), _ptr(self.ws), self.ws.numel(),
+            _stream_ptr(self.dev)), "sparcml_sparse_reduce_async")
+
+    def result_header(self):
+        """(nnz, dense) from ``self.result`` (synchronizes)."""
+        r = self.result.cpu()
+        return int(r[0]), bool(int(r[1]) & 0xFFFFFFFF)
 
     def run(self):
         """Returns (nnz, dense)."""

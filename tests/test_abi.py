@@ -23,7 +23,7 @@ def test_header_declares_the_boundary():
     syms = declared_symbols()
     for name in ("sparcml_topk_sparsify", "sparcml_quantize", "sparcml_sparse_reduce",
                  "sparcml_sparse_reduce_range", "sparcml_quantize_bucketed", "sparcml_concat",
-                 "sparcml_topk_bucketed", "sparcml_topk_bucketed_count",
+                 "sparcml_topk_bucketed", "sparcml_topk_bucketed_count", "sparcml_sparse_reduce_async",
                  "sparcml_densify", "sparcml_workspace_size", "sparcml_strerror",
                  "sparcml_last_error"):
         assert name in syms
@@ -137,6 +137,22 @@ def test_reduce_range_argument_errors():
     small = S.Stream(FAKE, FAKE, None, None, 15, 0, 0)
     assert range_rc(4, streams(4), lo=30, hi=70, out=small) == S.ECAPACITY
     assert range_rc(4, streams(4), lo=30, hi=70, ws_bytes=16) == S.EWORKSPACE
+
+
+def test_reduce_async_argument_errors():
+    L = S.lib()
+    out = S.Stream(FAKE, FAKE, None, None, 1 << 30, 0, 0)
+
+    def rc(P=4, arr=None, N=100, lo=0, hi=100, result=FAKE, ws_bytes=1 << 40, o=out):
+        return L.sparcml_sparse_reduce_async(P, streams(P) if arr is None else arr, N, lo, hi, 0.5,
+                                             ctypes.byref(o) if o is not None else None, None, None,
+                                             result, FAKE, ws_bytes, None)
+    assert rc(result=None) == S.EINVAL
+    assert rc(lo=5, hi=5) == S.EINVAL and rc(hi=101) == S.EINVAL
+    assert rc(P=0, arr=streams(1)) == S.EINVAL
+    assert rc(o=None) == S.EINVAL
+    assert rc(ws_bytes=16) == S.EWORKSPACE
+    assert rc(o=S.Stream(FAKE, FAKE, None, None, 15, 0, 0)) == S.ECAPACITY
 
 
 def test_reduce_capacity_and_workspace_errors():
