@@ -1,17 +1,18 @@
 // Top-k sparsification by magnitude on gfx950 (§2.2 "Structured
 // Sparsification"; Alg. 1: TopK and the error update eps = acc - TopK(acc)).
 //
-// Exact radix select on the 31-bit magnitude key (IEEE bits, sign cleared),
-// three passes over the data: a histogram of the top 11 key bits finds the
-// bin holding the k-th largest key; a filter pass counts, per 4096-element
-// wave unit, the keys above that bin and gathers the keys inside it; the
-// k-th largest key K* and how many entries equal to it are still needed
-// follow from the gathered keys alone (two more 10-bit histograms), which
-// also complete the unit counts.  A scan over the units gives every unit its
-// output offset, and a write pass compacts the selection in index order
-// (equal keys: lowest index first) with wave ballots, optionally zeroing the
-// residual.  A row with a unit holding more than kSlots keys of the boundary
-// bin takes two more histogram passes and a count pass over its data instead.
+// Exact radix select on the 31-bit magnitude key (IEEE bits, sign cleared)
+// in two passes over the data: a histogram of the top 11 key bits finds the
+// bin holding the k-th largest key; a gather pass collects, per 4096-element
+// wave unit, every entry in that bin or above it as {element, value bits} in
+// index order (a few per unit).  The k-th largest key K* and how many
+// entries equal to it are still needed follow from the gathered keys alone
+// (two more 10-bit histograms), which also give every unit its counts; a
+// scan over the units gives output offsets, and the selection is written
+// from the gathered entries (equal keys: lowest index first), zeroing the
+// residual at the selected positions.  A row with a unit holding more than
+// kSlots such entries takes two more histogram passes, a count pass and a
+// write pass over its data instead.
 #include "internal.h"
 
 #include <algorithm>
@@ -20,7 +21,7 @@ namespace sparcml {
 namespace {
 
 constexpr uint32_t kUnit = 4096;  // elements per wave unit (64 iterations of 64 lanes)
-constexpr uint32_t kSlots = 16;   // gathered keys per unit
+constexpr uint32_t kSlots = 32;   // gathered entries per unit
 constexpr int kHistBlocksPerRank = 64;
 
 __device__ __forceinline__ uint32_t mag_key(float v) { return __float_as_uint(v) & 0x7FFFFFFFu; }
@@ -171,32 +172,35 @@ __device__ __forceinline__ uint32_t block_excl_scan(uint32_t v, uint32_t* s_w, u
     return ex;
 }
 
-// Per wave unit: keys above the boundary bin (top 11 bits) counted, keys in
-// it gathered as {element, key} into the unit's kSlots slots (a unit with
-// more flags its row for the passes over the data); the unit's tie count
-// starts at zero.
-__global__ void __launch_bounds__(256) k_filter(const float* x, uint64_t N, uint32_t U, const RankState* st,
-                                                uint32_t* cgt, uint32_t* ceq, uint2* cand, uint32_t* ccnt,
-                                                uint32_t* overflow)
+// Per wave unit: every entry whose top 11 key bits are at or above the
+// boundary bin gathered as {element, value bits} into the unit's kSlots
+// slots, in index order (a unit with more flags its row for the passes over
+// the data).  A separate residual receives a copy of the row here.
+__global__ void __launch_bounds__(256) k_gather(const float* x, uint64_t N, uint32_t U, const RankState* st,
+                                                uint2* cand, uint32_t* ccnt, uint32_t* overflow, float* residual)
 {
     const uint32_t r = blockIdx.y, lane = threadIdx.x & 63;
     const uint32_t u = blockIdx.x * 4 + (threadIdx.x >> 6);
     if (u >= U) return;
     const uint32_t bin = st[r].prefix;
     const float* row = x + (uint64_t)r * N;
+    float* res = residual && residual != x ? residual + (uint64_t)r * N : nullptr;
     const uint64_t lo = (uint64_t)u * kUnit, hi = min(lo + kUnit, N);
     uint2* cu = cand + ((uint64_t)r * U + u) * kSlots;
-    uint32_t gt = 0, nc = 0;
-    auto gather = [&](bool in, uint64_t e, uint32_t key) {
+    uint32_t nc = 0;
+    auto gather = [&](bool in, uint64_t e, float v) {
         const uint64_t m = __ballot(in);
         if (m) {
             const uint32_t at = nc + (uint32_t)__popcll(m & ((1ull << lane) - 1ull));
-            if (in && at < kSlots) cu[at] = make_uint2((uint32_t)e, key);
+            if (in && at < kSlots) cu[at] = make_uint2((uint32_t)e, __float_as_uint(v));
             nc += (uint32_t)__popcll(m);
         }
     };
-    if ((reinterpret_cast<uintptr_t>(row) & 15u) == 0u && hi - lo == kUnit) {
-        // the unit's 16 float4 per lane, all requested before use
+    const bool rvec = res == nullptr || (reinterpret_cast<uintptr_t>(res) & 15u) == 0u;
+    if ((reinterpret_cast<uintptr_t>(row) & 15u) == 0u && rvec && hi - lo == kUnit) {
+        // the unit's 16 float4 per lane, all requested before use; lane i
+        // holds elements 4i..4i+3 of every 256, so each gather step is in
+        // index order within the step and the steps follow each other
         float4 vs[kUnit / 256];
 #pragma unroll
         for (uint32_t q = 0; q < kUnit / 256; ++q)
@@ -205,25 +209,27 @@ __global__ void __launch_bounds__(256) k_filter(const float* x, uint64_t N, uint
         for (uint32_t q = 0; q < kUnit / 256; ++q) {
             const uint64_t e = lo + 256u * q + 4u * lane;
             const float4 v = vs[q];
-            const uint32_t k0 = mag_key(v.x), k1 = mag_key(v.y), k2 = mag_key(v.z), k3 = mag_key(v.w);
-            gt += ((k0 >> 20) > bin) + ((k1 >> 20) > bin) + ((k2 >> 20) > bin) + ((k3 >> 20) > bin);
-            gather((k0 >> 20) == bin, e, k0);
-            gather((k1 >> 20) == bin, e + 1, k1);
-            gather((k2 >> 20) == bin, e + 2, k2);
-            gather((k3 >> 20) == bin, e + 3, k3);
+            const bool i0 = (mag_key(v.x) >> 20) >= bin, i1 = (mag_key(v.y) >> 20) >= bin;
+            const bool i2 = (mag_key(v.z) >> 20) >= bin, i3 = (mag_key(v.w) >> 20) >= bin;
+            const uint32_t n4 = (uint32_t)i0 + (uint32_t)i1 + (uint32_t)i2 + (uint32_t)i3;
+            const uint32_t incl = wave_scan(n4);
+            uint32_t at = nc + incl - n4;
+            if (i0) { if (at < kSlots) cu[at] = make_uint2((uint32_t)e, __float_as_uint(v.x)); ++at; }
+            if (i1) { if (at < kSlots) cu[at] = make_uint2((uint32_t)e + 1u, __float_as_uint(v.y)); ++at; }
+            if (i2) { if (at < kSlots) cu[at] = make_uint2((uint32_t)e + 2u, __float_as_uint(v.z)); ++at; }
+            if (i3) { if (at < kSlots) cu[at] = make_uint2((uint32_t)e + 3u, __float_as_uint(v.w)); }
+            nc += (uint32_t)__builtin_amdgcn_readlane((int)incl, 63);
+            if (res) store_nt(res + e, v);
         }
     } else {
         for (uint64_t e0 = lo; e0 < hi; e0 += 64) {
             const uint64_t e = e0 + lane;
-            const uint32_t key = e < hi ? mag_key(row[e]) : 0u;
-            gt += e < hi && (key >> 20) > bin;
-            gather(e < hi && (key >> 20) == bin, e, key);
+            const float v = e < hi ? row[e] : 0.0f;
+            gather(e < hi && (mag_key(v) >> 20) >= bin, e, v);
+            if (res && e < hi) res[e] = v;
         }
     }
-    for (int o = 32; o > 0; o >>= 1) gt += __shfl_xor(gt, o);
     if (lane == 0) {
-        cgt[(uint64_t)r * U + u] = gt;
-        ceq[(uint64_t)r * U + u] = 0;
         ccnt[(uint64_t)r * U + u] = nc;
         if (nc > kSlots) atomicOr(&overflow[r], 1u);
     }
@@ -246,9 +252,9 @@ __device__ uint32_t block_find(uint32_t cnt, uint64_t krem, uint32_t NB, uint64_
     return s_res[0];
 }
 
-// K* and the ties still needed from the gathered keys of row r (its
-// boundary bin), then the unit counts of keys above K* and equal to it.
-// Thread t takes units t, t + 1024, ...
+// K* and the ties still needed from the gathered keys of row r that lie in
+// its boundary bin, then the unit counts of keys above K* and equal to it
+// (every such key was gathered).  Thread t takes units t, t + 1024, ...
 __global__ void __launch_bounds__(1024) k_cand_select(uint32_t U, RankState* st, const uint2* cand,
                                                       const uint32_t* ccnt, const uint32_t* overflow,
                                                       uint32_t* cgt, uint32_t* ceq)
@@ -269,7 +275,10 @@ __global__ void __launch_bounds__(1024) k_cand_select(uint32_t U, RankState* st,
     s_h[t] = 0;
     __syncthreads();
     for (uint32_t u = t; u < U; u += 1024)
-        for (uint32_t i = 0; i < cn[u]; ++i) atomicAdd(&s_h[(cr[u * kSlots + i].y >> 10) & 1023u], 1u);
+        for (uint32_t i = 0; i < cn[u]; ++i) {
+            const uint32_t key = cr[u * kSlots + i].y & 0x7FFFFFFFu;
+            if ((key >> 20) == bin) atomicAdd(&s_h[(key >> 10) & 1023u], 1u);
+        }
     __syncthreads();
     const uint32_t b2 = block_find(s_h[1023u - t], krem, 1024u, &krem, s_w, s_res);
     const uint32_t p21 = bin << 10 | b2;
@@ -278,7 +287,7 @@ __global__ void __launch_bounds__(1024) k_cand_select(uint32_t U, RankState* st,
     __syncthreads();
     for (uint32_t u = t; u < U; u += 1024)
         for (uint32_t i = 0; i < cn[u]; ++i) {
-            const uint32_t key = cr[u * kSlots + i].y;
+            const uint32_t key = cr[u * kSlots + i].y & 0x7FFFFFFFu;
             if ((key >> 10) == p21) atomicAdd(&s_h[key & 1023u], 1u);
         }
     __syncthreads();
@@ -287,11 +296,11 @@ __global__ void __launch_bounds__(1024) k_cand_select(uint32_t U, RankState* st,
     for (uint32_t u = t; u < U; u += 1024) {
         uint32_t g = 0, q = 0;
         for (uint32_t i = 0; i < cn[u]; ++i) {
-            const uint32_t key = cr[u * kSlots + i].y;
+            const uint32_t key = cr[u * kSlots + i].y & 0x7FFFFFFFu;
             g += key > K;
             q += key == K;
         }
-        cgt[(uint64_t)r * U + u] += g;
+        cgt[(uint64_t)r * U + u] = g;
         ceq[(uint64_t)r * U + u] = q;
     }
     if (t == 0) {
@@ -368,7 +377,7 @@ __global__ void __launch_bounds__(256) k_write(const float* x, uint64_t N, uint6
 {
     const uint32_t r = blockIdx.y, lane = threadIdx.x & 63;
     const uint32_t u = blockIdx.x * 4 + (threadIdx.x >> 6);
-    if (u >= U) return;
+    if (u >= U || st[r].full == 0u) return;  // written from the gathered entries
     const uint32_t K = st[r].prefix;
     const uint64_t need = st[r].krem;
     const float* row = x + (uint64_t)r * N;
@@ -465,6 +474,37 @@ __global__ void __launch_bounds__(256) k_write(const float* x, uint64_t N, uint6
     }
 }
 
+// Rows settled by their gathered entries: per wave unit, the unit's
+// gathered entries (index order, one per lane) selected if key > K* or,
+// for key == K*, while ties are still needed; written at the unit's
+// offset; the residual is zeroed at the selected positions.
+__global__ void __launch_bounds__(256) k_write_cand(uint64_t N, uint64_t k, uint32_t U, const RankState* st,
+                                                    const uint2* cand, const uint32_t* ccnt,
+                                                    const uint32_t* beq, const uint32_t* bout,
+                                                    uint32_t* out_idx, float* out_val, float* residual)
+{
+    const uint32_t r = blockIdx.y, lane = threadIdx.x & 63;
+    const uint32_t u = blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (u >= U || st[r].full != 0u) return;
+    const uint32_t K = st[r].prefix;
+    const uint64_t need = st[r].krem;
+    const uint32_t n = ccnt[(uint64_t)r * U + u];  // <= kSlots on a settled row
+    const uint2 c = lane < n ? cand[((uint64_t)r * U + u) * kSlots + lane] : make_uint2(0u, 0u);
+    const uint32_t key = c.y & 0x7FFFFFFFu;
+    const uint64_t lt = (1ull << lane) - 1ull;
+    const bool eq = lane < n && key == K;
+    const uint64_t beq_w = __ballot(eq);
+    const bool sel = (lane < n && key > K) ||
+                     (eq && (uint64_t)beq[(uint64_t)r * U + u] + (uint64_t)__popcll(beq_w & lt) < need);
+    const uint64_t bsel = __ballot(sel);
+    if (sel) {
+        const uint64_t o = (uint64_t)r * k + bout[(uint64_t)r * U + u] + (uint32_t)__popcll(bsel & lt);
+        out_idx[o] = c.x;
+        out_val[o] = __uint_as_float(c.y);
+        if (residual) residual[(uint64_t)r * N + c.x] = 0.0f;
+    }
+}
+
 struct TLayout {
     RankState* st;
     uint32_t *hist, *cgt, *ceq, *beq, *bout, *ccnt, *overflow;
@@ -512,8 +552,8 @@ hipError_t topk_run(int P, const float* x, uint64_t N, uint64_t k, uint32_t* out
     timer_begin(kTTopkSelect, s);
     hipLaunchKernelGGL(k_hist<0>, hgrid, dim3(256), 0, s, x, N, l.st, l.hist);
     hipLaunchKernelGGL(k_select<0>, dim3(P), dim3(256), 0, s, l.st, l.hist);
-    hipLaunchKernelGGL(k_filter, ugrid, dim3(256), 0, s, x, N, l.U, l.st, l.cgt, l.ceq, l.cand, l.ccnt,
-                       l.overflow);
+    hipLaunchKernelGGL(k_gather, ugrid, dim3(256), 0, s, x, N, l.U, l.st, l.cand, l.ccnt, l.overflow,
+                       residual);
     hipLaunchKernelGGL(k_cand_select, dim3(P), dim3(1024), 0, s, l.U, l.st, l.cand, l.ccnt, l.overflow,
                        l.cgt, l.ceq);
     // rows whose boundary bin overflowed the gather buffer (the others return at once)
@@ -527,6 +567,8 @@ hipError_t topk_run(int P, const float* x, uint64_t N, uint64_t k, uint32_t* out
     hipLaunchKernelGGL(k_unit_scan, dim3(P), dim3(1024), 0, s, l.U, l.st, l.cgt, l.ceq, l.beq, l.bout);
     hipLaunchKernelGGL(k_write, ugrid, dim3(256), 0, s, x, N, k, l.U, l.st, l.beq, l.bout, out_idx,
                        out_val, residual);
+    hipLaunchKernelGGL(k_write_cand, ugrid, dim3(256), 0, s, N, k, l.U, l.st, l.cand, l.ccnt, l.beq, l.bout,
+                       out_idx, out_val, residual);
     timer_end(kTTopkWrite, s);
     return hipGetLastError();
 }

@@ -74,25 +74,30 @@ def test_topk_all_equal_and_config3_scaled():
 
 
 def test_topk_boundary_bin_at_gather_capacity():
-    """The k-th largest key's 11-bit bin holding 16 keys (as many as a
-    4096-element unit gathers) in every unit of the first row, and 17 in one
-    unit of the second: the first row is settled by its gathered keys, the
-    second by the extra passes over its data."""
+    """Every 4096-element unit of the first row holding exactly as many
+    entries in or above the k-th largest key's 11-bit bin as a unit gathers
+    (32: 8 above the bin, 24 in it), one unit of the second row one more:
+    the first row is settled by its gathered entries, the second by the
+    extra passes over its data."""
     rng = np.random.default_rng(31)
-    N, k, unit = 1 << 18, 500, 4096
+    N, k, unit = 1 << 18, 600, 4096
     x = np.stack([inputs.laplace(rng, 1e-3, N) for _ in range(2)])
     for r in range(2):
         for u in range(N // unit):
-            cnt = 17 if (r == 1 and u == 7) else 16
+            cnt = 33 if (r == 1 and u == 7) else 32
             pos = u * unit + rng.choice(unit, size=cnt, replace=False)
-            x[r, pos] = np.float32(1.0) if r == 0 else np.float32(-1.0)
-            x[r, pos[::5]] = np.float32(1.0009765625)  # same bin, a larger key
+            sign = np.float32(1.0) if r == 0 else np.float32(-1.0)
+            x[r, pos] = sign * np.float32(1.0)
+            x[r, pos[::6]] = sign * np.float32(1.0009765625)  # same bin, a larger key
+            x[r, pos[1::4][:8]] = sign * np.float32(2.0)       # above the bin
     say(f"[topk] gather capacity P=2 N={N} k={k}")
-    oi, ov, orr = oracle.topk(x, k, residual=True)
-    gi, gv, gr = gpu_topk(x, k, "copy")
-    np.testing.assert_array_equal(gi, oi)
-    np.testing.assert_array_equal(gv.view(np.uint32), ov.view(np.uint32))
-    np.testing.assert_array_equal(gr.view(np.uint32), orr.view(np.uint32))
+    for mode in ("copy", "inplace", None):
+        oi, ov, orr = oracle.topk(x, k, residual=True)
+        gi, gv, gr = gpu_topk(x, k, mode)
+        np.testing.assert_array_equal(gi, oi)
+        np.testing.assert_array_equal(gv.view(np.uint32), ov.view(np.uint32))
+        if mode is not None:
+            np.testing.assert_array_equal(gr.view(np.uint32), orr.view(np.uint32))
 
 
 def gpu_quantize(vals, bits, seed):
