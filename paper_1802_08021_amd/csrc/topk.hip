@@ -1,18 +1,22 @@
 // Top-k sparsification by magnitude on gfx950 (§2.2 "Structured
 // Sparsification"; Alg. 1: TopK and the error update eps = acc - TopK(acc)).
 //
-// Exact radix select on the 31-bit magnitude key (IEEE bits, sign cleared)
-// in two passes over the data: a histogram of the top 11 key bits finds the
-// bin holding the k-th largest key; a gather pass collects, per 4096-element
-// wave unit, every entry in that bin or above it as {element, value bits} in
-// index order (a few per unit).  The k-th largest key K* and how many
-// entries equal to it are still needed follow from the gathered keys alone
-// (two more 10-bit histograms), which also give every unit its counts; a
-// scan over the units gives output offsets, and the selection is written
-// from the gathered entries (equal keys: lowest index first), zeroing the
-// residual at the selected positions.  A row with a unit holding more than
-// kSlots such entries takes two more histogram passes, a count pass and a
-// write pass over its data instead.
+// Exact radix select on the 31-bit magnitude key (IEEE bits, sign cleared),
+// normally in one pass over the data.  A histogram of the top 11 key bits
+// over a sample of the row (1024 segments of 256 elements) gives a gather
+// bin safely below the k-th largest key; the gather pass collects, per
+// 4096-element wave unit, every entry in that bin or above it as {element,
+// value bits} in index order (a few per unit).  If the row then holds at
+// least k gathered keys, the k-th largest key K* and how many entries equal
+// to it are still needed follow from the gathered keys alone (11-, 10- and
+// 10-bit histograms), which also give every unit its counts; a scan over
+// the units gives output offsets, and the selection is written from the
+// gathered entries (equal keys: lowest index first), zeroing the residual
+// at the selected positions.  Otherwise the row takes the exact gather bin
+// from a histogram of all its keys and gathers again; a row with a unit
+// holding more than kSlots entries even then takes two more histogram
+// passes, a count pass and a write pass over its data.  Every path is
+// exact: the sample only decides how much data is read.
 #include "internal.h"
 
 #include <algorithm>
@@ -23,13 +27,16 @@ namespace {
 constexpr uint32_t kUnit = 4096;  // elements per wave unit (64 iterations of 64 lanes)
 constexpr uint32_t kSlots = 32;   // gathered entries per unit
 constexpr int kHistBlocksPerRank = 64;
+constexpr uint64_t kSampleSegs = 1024;  // 256-element segments sampled per row
 
 __device__ __forceinline__ uint32_t mag_key(float v) { return __float_as_uint(v) & 0x7FFFFFFFu; }
 
 struct RankState {
-    uint32_t prefix;  // key bits fixed so far
+    uint32_t prefix;  // key bits fixed so far (gather: the lowest 11-bit bin gathered)
     uint32_t full;    // 0: K* from the gathered keys; 1: refined by passes over the data
     uint64_t krem;    // entries still to take from keys matching the prefix
+    uint32_t exact;   // 0: gather bin estimated from a sample; 1: from the full histogram
+    uint32_t pad;
 };
 
 // Keys of row r from element lo to hi (lo a multiple of 4), in float4 loads
@@ -80,7 +87,7 @@ __global__ void __launch_bounds__(256) k_hist(const float* x, uint64_t N, const 
     constexpr int PSHIFT = PASS == 1 ? 20 : 10;
     __shared__ uint32_t s_h[NB];
     const uint32_t r = blockIdx.y;
-    if (PASS != 0 && st[r].full == 0u) return;  // row settled by its gathered keys
+    if (PASS == 0 ? st[r].exact == 0u : st[r].full == 0u) return;  // row not on this path
     for (uint32_t i = threadIdx.x; i < NB; i += 256) s_h[i] = 0;
     __syncthreads();
     const uint32_t prefix = PASS == 0 ? 0u : st[r].prefix;
@@ -104,7 +111,7 @@ __global__ void __launch_bounds__(256) k_select(RankState* st, uint32_t* hist)
     constexpr int BITS = PASS == 0 ? 11 : 10;
     __shared__ uint64_t s_w[4];
     const uint32_t r = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-    if (PASS != 0 && st[r].full == 0u) return;
+    if (PASS == 0 ? st[r].exact == 0u : st[r].full == 0u) return;
     // read the state before the barrier below; one thread rewrites it after
     const uint64_t krem = st[r].krem;
     const uint32_t prefix = st[r].prefix;
@@ -140,14 +147,19 @@ __global__ void __launch_bounds__(256) k_select(RankState* st, uint32_t* hist)
     for (uint32_t i = 0; i < PER; ++i) h[lo + i] = 0;
 }
 
-__global__ void k_init(RankState* st, uint32_t P, uint64_t k, uint32_t* hist, uint32_t* overflow)
+// mode 0: start from a sampled gather bin; 1: from the exact one; 2: more
+// keys per unit than a unit gathers are selected -- straight to the passes
+// over the data (marked as overflowed, so that no gather runs).
+__global__ void k_init(RankState* st, uint32_t P, uint64_t k, uint32_t* hist, uint32_t* overflow, uint32_t mode)
 {
     const uint64_t gid = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (gid < P) {
         st[gid].prefix = 0;
         st[gid].full = 0;
         st[gid].krem = k;
-        overflow[gid] = 0;
+        st[gid].exact = mode >= 1u ? 1u : 0u;
+        st[gid].pad = 0;
+        overflow[gid] = mode == 2u ? 1u : 0u;
     }
     if (gid < (uint64_t)P * 2048) hist[gid] = 0;
 }
@@ -172,16 +184,91 @@ __device__ __forceinline__ uint32_t block_excl_scan(uint32_t v, uint32_t* s_w, u
     return ex;
 }
 
+// Sample histogram of the top 11 key bits: kSampleSegs segments of 256
+// consecutive elements spread evenly over the row (all of a short row).
+__global__ void __launch_bounds__(256) k_sample(const float* x, uint64_t N, uint32_t stride, uint32_t* hist)
+{
+    __shared__ uint32_t s_h[2048];
+    const uint32_t r = blockIdx.y;
+    for (uint32_t i = threadIdx.x; i < 2048; i += 256) s_h[i] = 0;
+    __syncthreads();
+    const float* row = x + (uint64_t)r * N;
+    const uint64_t nseg = (N + 255) / 256;
+    for (uint64_t g = (uint64_t)blockIdx.x * stride; g < nseg; g += (uint64_t)gridDim.x * stride) {
+        const uint64_t e = g * 256 + threadIdx.x;
+        if (e < N) atomicAdd(&s_h[mag_key(row[e]) >> 20], 1u);
+    }
+    __syncthreads();
+    for (uint32_t i = threadIdx.x; i < 2048; i += 256)
+        if (s_h[i]) atomicAdd(&hist[(uint64_t)r * 2048 + i], s_h[i]);
+}
+
+// The gather bin of a row from its sample: the 11-bit bin of the t-th
+// largest sampled key, t = k f + 4 sqrt(k f) + 16 for sample fraction f --
+// low enough that the row holds at least k keys at or above it, barring a
+// sample off by more than four standard deviations (checked after the
+// gather).  Clears the histogram.
+__global__ void __launch_bounds__(256) k_estimate(RankState* st, uint32_t* hist, uint64_t k, double f)
+{
+    __shared__ uint32_t s_w[4];
+    __shared__ uint32_t s_bin;
+    const uint32_t r = blockIdx.x, tid = threadIdx.x;
+    if (st[r].exact != 0u) return;  // the row starts from the exact bin
+    uint32_t* h = hist + (uint64_t)r * 2048;
+    const double kf = (double)k * f;
+    const uint64_t t = (uint64_t)ceil(kf + 4.0 * sqrt(kf) + 16.0);
+    // thread tid owns bins [lo, lo + 8), threads ordered from the top
+    const uint32_t lo = 2048u - (tid + 1u) * 8u;
+    uint32_t cnt[8], mine = 0;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        cnt[i] = h[lo + i];
+        mine += cnt[i];
+    }
+    if (tid == 0) s_bin = 0u;  // the whole row when the sample holds fewer than t keys
+    uint32_t total;
+    uint64_t run = block_excl_scan(mine, s_w, &total);
+    for (int i = 7; i >= 0; --i) {
+        if (run < t && run + cnt[i] >= t) s_bin = lo + (uint32_t)i;
+        run += cnt[i];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < 8; ++i) h[lo + i] = 0;
+    if (tid == 0) st[r].prefix = s_bin;
+}
+
+// After the estimated gather: a row whose units overflowed or whose
+// gathered keys number fewer than k takes the exact path (a histogram of
+// the full row, then a second gather).
+__global__ void __launch_bounds__(1024) k_check(uint32_t U, uint64_t k, RankState* st, const uint32_t* ccnt,
+                                                uint32_t* overflow)
+{
+    __shared__ uint32_t s_w[16];
+    const uint32_t r = blockIdx.x;
+    uint32_t mine = 0;
+    for (uint32_t u = threadIdx.x; u < U; u += 1024) mine += ccnt[(uint64_t)r * U + u];
+    uint32_t total;
+    block_excl_scan(mine, s_w, &total);
+    if (threadIdx.x == 0 && (overflow[r] != 0u || total < k)) {
+        st[r].exact = 1u;
+        st[r].prefix = 0u;
+        st[r].krem = k;
+        overflow[r] = 0u;
+    }
+}
+
 // Per wave unit: every entry whose top 11 key bits are at or above the
 // boundary bin gathered as {element, value bits} into the unit's kSlots
 // slots, in index order (a unit with more flags its row for the passes over
 // the data).  A separate residual receives a copy of the row here.
 __global__ void __launch_bounds__(256) k_gather(const float* x, uint64_t N, uint32_t U, const RankState* st,
-                                                uint2* cand, uint32_t* ccnt, uint32_t* overflow, float* residual)
+                                                uint2* cand, uint32_t* ccnt, uint32_t* overflow, float* residual,
+                                                uint32_t exact)
 {
     const uint32_t r = blockIdx.y, lane = threadIdx.x & 63;
     const uint32_t u = blockIdx.x * 4 + (threadIdx.x >> 6);
-    if (u >= U) return;
+    if (u >= U || st[r].exact != exact || overflow[r] != 0u) return;  // not this path, or gathered too many
     const uint32_t bin = st[r].prefix;
     const float* row = x + (uint64_t)r * N;
     float* res = residual && residual != x ? residual + (uint64_t)r * N : nullptr;
@@ -252,14 +339,14 @@ __device__ uint32_t block_find(uint32_t cnt, uint64_t krem, uint32_t NB, uint64_
     return s_res[0];
 }
 
-// K* and the ties still needed from the gathered keys of row r that lie in
-// its boundary bin, then the unit counts of keys above K* and equal to it
-// (every such key was gathered).  Thread t takes units t, t + 1024, ...
-__global__ void __launch_bounds__(1024) k_cand_select(uint32_t U, RankState* st, const uint2* cand,
+// K* and the ties still needed from the gathered keys of row r, then the
+// unit counts of keys above K* and equal to it (every such key was
+// gathered).  Thread t takes units t, t + 1024, ...
+__global__ void __launch_bounds__(1024) k_cand_select(uint32_t U, uint64_t k, RankState* st, const uint2* cand,
                                                       const uint32_t* ccnt, const uint32_t* overflow,
                                                       uint32_t* cgt, uint32_t* ceq)
 {
-    __shared__ uint32_t s_h[1024];
+    __shared__ uint32_t s_h[1024], s_h2[1024];
     __shared__ uint32_t s_w[16];
     __shared__ uint32_t s_res[2];
     const uint32_t r = blockIdx.x, t = threadIdx.x;
@@ -269,9 +356,37 @@ __global__ void __launch_bounds__(1024) k_cand_select(uint32_t U, RankState* st,
     }
     const uint2* cr = cand + (uint64_t)r * U * kSlots;
     const uint32_t* cn = ccnt + (uint64_t)r * U;
-    const uint32_t bin = st[r].prefix;
-    uint64_t krem = st[r].krem;
-    // bits 19..10, then bits 9..0 among the keys matching so far
+    // the gathered keys are every key at or above the gather bin: the k-th
+    // largest of them is the row's; its 11-bit bin first (2048 bins, two
+    // per thread), then bits 19..10, then bits 9..0
+    uint64_t krem = k;
+    s_h[t] = 0;
+    s_h2[t] = 0;
+    __syncthreads();
+    for (uint32_t u = t; u < U; u += 1024)
+        for (uint32_t i = 0; i < cn[u]; ++i) {
+            const uint32_t b = (cr[u * kSlots + i].y & 0x7FFFFFFFu) >> 20;
+            atomicAdd(b & 1u ? &s_h2[b >> 1] : &s_h[b >> 1], 1u);
+        }
+    __syncthreads();
+    uint32_t bin;
+    {
+        // thread t: bins 2047-2t (odd, in s_h2) and 2046-2t (even, in s_h)
+        const uint32_t hi_b = s_h2[1023u - t], lo_b = s_h[1023u - t];
+        uint32_t total;
+        const uint32_t above = block_excl_scan(hi_b + lo_b, s_w, &total);
+        if (above < krem && above + hi_b >= krem) {
+            s_res[0] = 2047u - 2u * t;
+            s_res[1] = (uint32_t)(krem - above);
+        } else if (above + hi_b < krem && above + hi_b + lo_b >= krem) {
+            s_res[0] = 2046u - 2u * t;
+            s_res[1] = (uint32_t)(krem - above - hi_b);
+        }
+        __syncthreads();
+        bin = s_res[0];
+        krem = s_res[1];
+    }
+    __syncthreads();
     s_h[t] = 0;
     __syncthreads();
     for (uint32_t u = t; u < U; u += 1024)
@@ -544,17 +659,35 @@ hipError_t topk_run(int P, const float* x, uint64_t N, uint64_t k, uint32_t* out
         return hipSuccess;
     }
     const TLayout l = tlayout(P, N, ws);
+    // expected selections per unit decide where a row starts
+    const double per_unit = (double)k * kUnit / (double)N;
+    const uint32_t mode = per_unit > kSlots ? 2u : (per_unit > kSlots / 4 ? 1u : 0u);
     const uint64_t ninit = (uint64_t)P * 2048;
     hipLaunchKernelGGL(k_init, dim3((uint32_t)((ninit + 255) / 256)), dim3(256), 0, s, l.st,
-                       (uint32_t)P, k, l.hist, l.overflow);
+                       (uint32_t)P, k, l.hist, l.overflow, mode);
     const uint32_t hb = (uint32_t)std::min<uint64_t>(kHistBlocksPerRank, (N + 4095) / 4096);
     const dim3 hgrid(hb, P), ugrid((l.U + 3) / 4, P);
+    // sample: every stride-th 256-element segment, about kSampleSegs of them
+    const uint64_t nseg = (N + 255) / 256;
+    const uint64_t stride = std::max<uint64_t>(1, nseg / kSampleSegs);
+    uint64_t sampled = 0;
+    for (uint64_t g = 0; g < nseg; g += stride) sampled += std::min<uint64_t>(256, N - g * 256);
+    const double frac = (double)sampled / (double)N;
+    const uint32_t sb = (uint32_t)std::min<uint64_t>(16, (nseg + stride - 1) / stride);
     timer_begin(kTTopkSelect, s);
+    if (mode == 0) {
+        hipLaunchKernelGGL(k_sample, dim3(sb, P), dim3(256), 0, s, x, N, (uint32_t)stride, l.hist);
+        hipLaunchKernelGGL(k_estimate, dim3(P), dim3(256), 0, s, l.st, l.hist, k, frac);
+        hipLaunchKernelGGL(k_gather, ugrid, dim3(256), 0, s, x, N, l.U, l.st, l.cand, l.ccnt, l.overflow,
+                           residual, 0u);
+        hipLaunchKernelGGL(k_check, dim3(P), dim3(1024), 0, s, l.U, k, l.st, l.ccnt, l.overflow);
+    }
+    // rows whose estimate failed: the exact boundary bin, a second gather
     hipLaunchKernelGGL(k_hist<0>, hgrid, dim3(256), 0, s, x, N, l.st, l.hist);
     hipLaunchKernelGGL(k_select<0>, dim3(P), dim3(256), 0, s, l.st, l.hist);
     hipLaunchKernelGGL(k_gather, ugrid, dim3(256), 0, s, x, N, l.U, l.st, l.cand, l.ccnt, l.overflow,
-                       residual);
-    hipLaunchKernelGGL(k_cand_select, dim3(P), dim3(1024), 0, s, l.U, l.st, l.cand, l.ccnt, l.overflow,
+                       residual, 1u);
+    hipLaunchKernelGGL(k_cand_select, dim3(P), dim3(1024), 0, s, l.U, k, l.st, l.cand, l.ccnt, l.overflow,
                        l.cgt, l.ceq);
     // rows whose boundary bin overflowed the gather buffer (the others return at once)
     hipLaunchKernelGGL(k_hist<1>, hgrid, dim3(256), 0, s, x, N, l.st, l.hist);

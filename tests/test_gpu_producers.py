@@ -100,6 +100,29 @@ def test_topk_boundary_bin_at_gather_capacity():
             np.testing.assert_array_equal(gr.view(np.uint32), orr.view(np.uint32))
 
 
+def test_topk_sampled_gather_bin_paths():
+    """The gather bin comes from a sample of every 16th 256-element segment
+    (N = 2^22).  Row 0: its 200 largest values sit only in sampled segments
+    and k = 1000, so the sample overestimates and the row must fall back to
+    the exact bin.  Row 1: 5000 large values only outside the sample, k =
+    100: the estimate holds and every large value is gathered.  Row 2: plain
+    Laplace values."""
+    rng = np.random.default_rng(32)
+    N, seg, stride = 1 << 22, 256, 16
+    x = np.stack([inputs.laplace(rng, 1e-3, N) for _ in range(3)])
+    sampled = np.arange(0, N // seg, stride) * seg
+    x[0, rng.choice(sampled, 200, replace=False)] = np.float32(1.0)
+    hidden = (np.arange(0, N // seg, stride) + 1) * seg
+    x[1, rng.choice(hidden, 5000, replace=True) + rng.integers(0, seg, 5000)] = np.float32(-3.0)
+    for k in (1000, 100):
+        say(f"[topk] sampled gather paths N={N} k={k}")
+        oi, ov, orr = oracle.topk(x, k, residual=True)
+        gi, gv, gr = gpu_topk(x, k, "copy")
+        np.testing.assert_array_equal(gi, oi)
+        np.testing.assert_array_equal(gv.view(np.uint32), ov.view(np.uint32))
+        np.testing.assert_array_equal(gr.view(np.uint32), orr.view(np.uint32))
+
+
 def gpu_quantize(vals, bits, seed):
     from paper_1802_08021_amd import sparcml as S
     torch, dev = torch_dev()
