@@ -28,6 +28,15 @@ constexpr uint32_t kUnit = 4096;  // elements per wave unit (64 iterations of 64
 constexpr uint32_t kSlots = 32;   // gathered entries per unit
 constexpr int kHistBlocksPerRank = 64;
 constexpr uint64_t kSampleSegs = 1024;  // 256-element segments sampled per row
+// Gathered keys are also listed per row in kSub sub-lists (unit u appends to
+// sub-list u mod kSub, reserving its place with one atomic on that
+// sub-list's counter, each counter on a cache line of its own, so that no
+// counter takes more than a few hundred atomics); a full sub-list counts as
+// an overflow.
+constexpr uint32_t kSub = 64;
+constexpr uint32_t kSubCap = 1024;                     // keys per sub-list
+constexpr uint32_t kList = kSub * kSubCap;             // keys listed per row
+constexpr uint32_t kCntStride = 32;                    // counter words apart (128 B)
 
 __device__ __forceinline__ uint32_t mag_key(float v) { return __float_as_uint(v) & 0x7FFFFFFFu; }
 
@@ -150,9 +159,11 @@ __global__ void __launch_bounds__(256) k_select(RankState* st, uint32_t* hist)
 // mode 0: start from a sampled gather bin; 1: from the exact one; 2: more
 // keys per unit than a unit gathers are selected -- straight to the passes
 // over the data (marked as overflowed, so that no gather runs).
-__global__ void k_init(RankState* st, uint32_t P, uint64_t k, uint32_t* hist, uint32_t* overflow, uint32_t mode)
+__global__ void k_init(RankState* st, uint32_t P, uint64_t k, uint32_t* hist, uint32_t* overflow, uint32_t mode,
+                       uint32_t* kcnt)
 {
     const uint64_t gid = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (gid < (uint64_t)P * kSub) kcnt[gid * kCntStride] = 0;
     if (gid < P) {
         st[gid].prefix = 0;
         st[gid].full = 0;
@@ -193,10 +204,19 @@ __global__ void __launch_bounds__(256) k_sample(const float* x, uint64_t N, uint
     for (uint32_t i = threadIdx.x; i < 2048; i += 256) s_h[i] = 0;
     __syncthreads();
     const float* row = x + (uint64_t)r * N;
-    const uint64_t nseg = (N + 255) / 256;
-    for (uint64_t g = (uint64_t)blockIdx.x * stride; g < nseg; g += (uint64_t)gridDim.x * stride) {
-        const uint64_t e = g * 256 + threadIdx.x;
-        if (e < N) atomicAdd(&s_h[mag_key(row[e]) >> 20], 1u);
+    const uint64_t nseg = (N + 255) / 256, step = (uint64_t)gridDim.x * stride;
+    for (uint64_t g = (uint64_t)blockIdx.x * stride; g < nseg; g += 4 * step) {
+        float v[4];
+        bool ok[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {  // four segments' loads in flight
+            const uint64_t e = (g + q * step) * 256 + threadIdx.x;
+            ok[q] = g + q * step < nseg && e < N;
+            v[q] = ok[q] ? row[e] : 0.0f;
+        }
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+            if (ok[q]) atomicAdd(&s_h[mag_key(v[q]) >> 20], 1u);
     }
     __syncthreads();
     for (uint32_t i = threadIdx.x; i < 2048; i += 256)
@@ -242,7 +262,7 @@ __global__ void __launch_bounds__(256) k_estimate(RankState* st, uint32_t* hist,
 // gathered keys number fewer than k takes the exact path (a histogram of
 // the full row, then a second gather).
 __global__ void __launch_bounds__(1024) k_check(uint32_t U, uint64_t k, RankState* st, const uint32_t* ccnt,
-                                                uint32_t* overflow)
+                                                uint32_t* overflow, uint32_t* kcnt)
 {
     __shared__ uint32_t s_w[16];
     const uint32_t r = blockIdx.x;
@@ -256,15 +276,19 @@ __global__ void __launch_bounds__(1024) k_check(uint32_t U, uint64_t k, RankStat
         st[r].krem = k;
         overflow[r] = 0u;
     }
+    __syncthreads();
+    if (threadIdx.x < kSub && st[r].exact != 0u && st[r].full == 0u)
+        kcnt[((uint64_t)r * kSub + threadIdx.x) * kCntStride] = 0u;
 }
 
 // Per wave unit: every entry whose top 11 key bits are at or above the
-// boundary bin gathered as {element, value bits} into the unit's kSlots
-// slots, in index order (a unit with more flags its row for the passes over
-// the data).  A separate residual receives a copy of the row here.
+// gather bin goes as {element, value bits} into the unit's kSlots slots in
+// index order, and its key into the row's key list (a unit with more, or a
+// full list, flags its row for the next path).  A separate residual
+// receives a copy of the row here.
 __global__ void __launch_bounds__(256) k_gather(const float* x, uint64_t N, uint32_t U, const RankState* st,
                                                 uint2* cand, uint32_t* ccnt, uint32_t* overflow, float* residual,
-                                                uint32_t exact)
+                                                uint32_t exact, uint32_t* klist, uint32_t* kcnt)
 {
     const uint32_t r = blockIdx.y, lane = threadIdx.x & 63;
     const uint32_t u = blockIdx.x * 4 + (threadIdx.x >> 6);
@@ -274,51 +298,92 @@ __global__ void __launch_bounds__(256) k_gather(const float* x, uint64_t N, uint
     float* res = residual && residual != x ? residual + (uint64_t)r * N : nullptr;
     const uint64_t lo = (uint64_t)u * kUnit, hi = min(lo + kUnit, N);
     uint2* cu = cand + ((uint64_t)r * U + u) * kSlots;
-    uint32_t nc = 0;
-    auto gather = [&](bool in, uint64_t e, float v) {
-        const uint64_t m = __ballot(in);
-        if (m) {
-            const uint32_t at = nc + (uint32_t)__popcll(m & ((1ull << lane) - 1ull));
-            if (in && at < kSlots) cu[at] = make_uint2((uint32_t)e, __float_as_uint(v));
-            nc += (uint32_t)__popcll(m);
+    const uint32_t sub = u % kSub;
+    uint32_t* kl = klist + ((uint64_t)r * kSub + sub) * kSubCap;
+    uint32_t* kc = kcnt + ((uint64_t)r * kSub + sub) * kCntStride;
+    // The unit's count first, then its entries: into the unit's slots in
+    // index order and, at a place reserved with one atomic, into the row's
+    // key list.  Returns whether the unit's entries are to be written.
+    auto reserve = [&](uint32_t nc, uint32_t* base) {
+        uint32_t b = kSubCap;
+        if (lane == 0) {
+            ccnt[(uint64_t)r * U + u] = nc;
+            if (nc > kSlots) {
+                atomicOr(&overflow[r], 1u);
+            } else if (nc) {
+                b = atomicAdd(kc, nc);
+                if (b + nc > kSubCap) atomicOr(&overflow[r], 1u);
+            }
         }
+        *base = (uint32_t)__builtin_amdgcn_readfirstlane((int)b);
+        return nc != 0u && nc <= kSlots && *base + nc <= kSubCap;
+    };
+    auto put = [&](uint32_t at, uint32_t base, uint64_t e, float v) {
+        cu[at] = make_uint2((uint32_t)e, __float_as_uint(v));
+        kl[base + at] = mag_key(v);
     };
     const bool rvec = res == nullptr || (reinterpret_cast<uintptr_t>(res) & 15u) == 0u;
     if ((reinterpret_cast<uintptr_t>(row) & 15u) == 0u && rvec && hi - lo == kUnit) {
         // the unit's 16 float4 per lane, all requested before use; lane i
-        // holds elements 4i..4i+3 of every 256, so each gather step is in
-        // index order within the step and the steps follow each other
+        // holds elements 4i..4i+3 of every 256, so entries are placed in
+        // index order by a wave scan per 256 elements
         float4 vs[kUnit / 256];
 #pragma unroll
         for (uint32_t q = 0; q < kUnit / 256; ++q)
             vs[q] = *reinterpret_cast<const float4*>(row + lo + 256u * q + 4u * lane);
+        auto in4 = [&](const float4& v, bool* i) {
+            i[0] = (mag_key(v.x) >> 20) >= bin;
+            i[1] = (mag_key(v.y) >> 20) >= bin;
+            i[2] = (mag_key(v.z) >> 20) >= bin;
+            i[3] = (mag_key(v.w) >> 20) >= bin;
+            return (uint32_t)i[0] + (uint32_t)i[1] + (uint32_t)i[2] + (uint32_t)i[3];
+        };
+        uint32_t mine = 0;
 #pragma unroll
         for (uint32_t q = 0; q < kUnit / 256; ++q) {
-            const uint64_t e = lo + 256u * q + 4u * lane;
-            const float4 v = vs[q];
-            const bool i0 = (mag_key(v.x) >> 20) >= bin, i1 = (mag_key(v.y) >> 20) >= bin;
-            const bool i2 = (mag_key(v.z) >> 20) >= bin, i3 = (mag_key(v.w) >> 20) >= bin;
-            const uint32_t n4 = (uint32_t)i0 + (uint32_t)i1 + (uint32_t)i2 + (uint32_t)i3;
-            const uint32_t incl = wave_scan(n4);
-            uint32_t at = nc + incl - n4;
-            if (i0) { if (at < kSlots) cu[at] = make_uint2((uint32_t)e, __float_as_uint(v.x)); ++at; }
-            if (i1) { if (at < kSlots) cu[at] = make_uint2((uint32_t)e + 1u, __float_as_uint(v.y)); ++at; }
-            if (i2) { if (at < kSlots) cu[at] = make_uint2((uint32_t)e + 2u, __float_as_uint(v.z)); ++at; }
-            if (i3) { if (at < kSlots) cu[at] = make_uint2((uint32_t)e + 3u, __float_as_uint(v.w)); }
-            nc += (uint32_t)__builtin_amdgcn_readlane((int)incl, 63);
-            if (res) store_nt(res + e, v);
+            bool i[4];
+            mine += in4(vs[q], i);
+            if (res) store_nt(res + lo + 256u * q + 4u * lane, vs[q]);
+        }
+        const uint32_t nc = (uint32_t)__builtin_amdgcn_readlane((int)wave_scan(mine), 63);
+        uint32_t base;
+        if (reserve(nc, &base)) {
+            uint32_t run = 0;
+#pragma unroll
+            for (uint32_t q = 0; q < kUnit / 256; ++q) {
+                const uint64_t e = lo + 256u * q + 4u * lane;
+                bool i[4];
+                const uint32_t n4 = in4(vs[q], i);
+                const uint32_t incl = wave_scan(n4);
+                uint32_t at = run + incl - n4;
+                if (i[0]) put(at++, base, e, vs[q].x);
+                if (i[1]) put(at++, base, e + 1, vs[q].y);
+                if (i[2]) put(at++, base, e + 2, vs[q].z);
+                if (i[3]) put(at, base, e + 3, vs[q].w);
+                run += (uint32_t)__builtin_amdgcn_readlane((int)incl, 63);
+            }
         }
     } else {
+        // short or unaligned unit: count (and copy), then read again to place
+        uint32_t nc = 0;
         for (uint64_t e0 = lo; e0 < hi; e0 += 64) {
             const uint64_t e = e0 + lane;
             const float v = e < hi ? row[e] : 0.0f;
-            gather(e < hi && (mag_key(v) >> 20) >= bin, e, v);
+            nc += (uint32_t)__popcll(__ballot(e < hi && (mag_key(v) >> 20) >= bin));
             if (res && e < hi) res[e] = v;
         }
-    }
-    if (lane == 0) {
-        ccnt[(uint64_t)r * U + u] = nc;
-        if (nc > kSlots) atomicOr(&overflow[r], 1u);
+        uint32_t base;
+        if (reserve(nc, &base)) {
+            uint32_t run = 0;
+            for (uint64_t e0 = lo; e0 < hi; e0 += 64) {
+                const uint64_t e = e0 + lane;
+                const float v = e < hi ? row[e] : 0.0f;
+                const bool in = e < hi && (mag_key(v) >> 20) >= bin;
+                const uint64_t m = __ballot(in);
+                if (in) put(run + (uint32_t)__popcll(m & ((1ull << lane) - 1ull)), base, e, v);
+                run += (uint32_t)__popcll(m);
+            }
+        }
     }
 }
 
@@ -339,14 +404,12 @@ __device__ uint32_t block_find(uint32_t cnt, uint64_t krem, uint32_t NB, uint64_
     return s_res[0];
 }
 
-// K* and the ties still needed from the gathered keys of row r, then the
-// unit counts of keys above K* and equal to it (every such key was
-// gathered).  Thread t takes units t, t + 1024, ...
-__global__ void __launch_bounds__(1024) k_cand_select(uint32_t U, uint64_t k, RankState* st, const uint2* cand,
-                                                      const uint32_t* ccnt, const uint32_t* overflow,
-                                                      uint32_t* cgt, uint32_t* ceq)
+// K* and the ties still needed, from the key list of row r (every key at or
+// above its gather bin).
+__global__ void __launch_bounds__(1024) k_cand_select(uint64_t k, RankState* st, const uint32_t* klist,
+                                                      const uint32_t* kcnt, const uint32_t* overflow)
 {
-    __shared__ uint32_t s_h[1024], s_h2[1024];
+    __shared__ uint32_t s_h[2048];
     __shared__ uint32_t s_w[16];
     __shared__ uint32_t s_res[2];
     const uint32_t r = blockIdx.x, t = threadIdx.x;
@@ -354,33 +417,42 @@ __global__ void __launch_bounds__(1024) k_cand_select(uint32_t U, uint64_t k, Ra
         if (t == 0) st[r].full = 1u;
         return;
     }
-    const uint2* cr = cand + (uint64_t)r * U * kSlots;
-    const uint32_t* cn = ccnt + (uint64_t)r * U;
-    // the gathered keys are every key at or above the gather bin: the k-th
-    // largest of them is the row's; its 11-bit bin first (2048 bins, two
-    // per thread), then bits 19..10, then bits 9..0
+    // every listed key: 16 threads per sub-list, four loads per thread in
+    // flight: f(key)
+    const uint32_t sub = t / 16u, j = t % 16u;
+    const uint32_t* kl = klist + ((uint64_t)r * kSub + sub) * kSubCap;
+    const uint32_t n = kcnt[((uint64_t)r * kSub + sub) * kCntStride];
+    auto for_keys = [&](auto&& f) {
+        for (uint32_t i0 = j; i0 < n; i0 += 64u) {
+            uint32_t key[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) key[q] = i0 + 16u * q < n ? kl[i0 + 16u * q] : 0u;
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+                if (i0 + 16u * q < n) f(key[q]);
+        }
+    };
+    // The listed keys are every key at or above the gather bin, so the k-th
+    // largest of them is the row's: its top 11 bits (2048 bins, two per
+    // thread), then bits 19..10, then bits 9..0.
     uint64_t krem = k;
     s_h[t] = 0;
-    s_h2[t] = 0;
+    s_h[t + 1024] = 0;
     __syncthreads();
-    for (uint32_t u = t; u < U; u += 1024)
-        for (uint32_t i = 0; i < cn[u]; ++i) {
-            const uint32_t b = (cr[u * kSlots + i].y & 0x7FFFFFFFu) >> 20;
-            atomicAdd(b & 1u ? &s_h2[b >> 1] : &s_h[b >> 1], 1u);
-        }
+    for_keys([&](uint32_t key) { atomicAdd(&s_h[key >> 20], 1u); });
     __syncthreads();
     uint32_t bin;
     {
-        // thread t: bins 2047-2t (odd, in s_h2) and 2046-2t (even, in s_h)
-        const uint32_t hi_b = s_h2[1023u - t], lo_b = s_h[1023u - t];
+        // thread t: bins 2047-2t and 2046-2t
+        const uint32_t hb = s_h[2047u - 2u * t], lb = s_h[2046u - 2u * t];
         uint32_t total;
-        const uint32_t above = block_excl_scan(hi_b + lo_b, s_w, &total);
-        if (above < krem && above + hi_b >= krem) {
+        const uint32_t above = block_excl_scan(hb + lb, s_w, &total);
+        if (above < krem && above + hb >= krem) {
             s_res[0] = 2047u - 2u * t;
             s_res[1] = (uint32_t)(krem - above);
-        } else if (above + hi_b < krem && above + hi_b + lo_b >= krem) {
+        } else if (above + hb < krem && above + hb + lb >= krem) {
             s_res[0] = 2046u - 2u * t;
-            s_res[1] = (uint32_t)(krem - above - hi_b);
+            s_res[1] = (uint32_t)(krem - above - hb);
         }
         __syncthreads();
         bin = s_res[0];
@@ -389,64 +461,75 @@ __global__ void __launch_bounds__(1024) k_cand_select(uint32_t U, uint64_t k, Ra
     __syncthreads();
     s_h[t] = 0;
     __syncthreads();
-    for (uint32_t u = t; u < U; u += 1024)
-        for (uint32_t i = 0; i < cn[u]; ++i) {
-            const uint32_t key = cr[u * kSlots + i].y & 0x7FFFFFFFu;
-            if ((key >> 20) == bin) atomicAdd(&s_h[(key >> 10) & 1023u], 1u);
-        }
+    for_keys([&](uint32_t key) {
+        if ((key >> 20) == bin) atomicAdd(&s_h[(key >> 10) & 1023u], 1u);
+    });
     __syncthreads();
     const uint32_t b2 = block_find(s_h[1023u - t], krem, 1024u, &krem, s_w, s_res);
     const uint32_t p21 = bin << 10 | b2;
     __syncthreads();
     s_h[t] = 0;
     __syncthreads();
-    for (uint32_t u = t; u < U; u += 1024)
-        for (uint32_t i = 0; i < cn[u]; ++i) {
-            const uint32_t key = cr[u * kSlots + i].y & 0x7FFFFFFFu;
-            if ((key >> 10) == p21) atomicAdd(&s_h[key & 1023u], 1u);
-        }
+    for_keys([&](uint32_t key) {
+        if ((key >> 10) == p21) atomicAdd(&s_h[key & 1023u], 1u);
+    });
     __syncthreads();
     const uint32_t b3 = block_find(s_h[1023u - t], krem, 1024u, &krem, s_w, s_res);
-    const uint32_t K = p21 << 10 | b3;
-    for (uint32_t u = t; u < U; u += 1024) {
-        uint32_t g = 0, q = 0;
-        for (uint32_t i = 0; i < cn[u]; ++i) {
-            const uint32_t key = cr[u * kSlots + i].y & 0x7FFFFFFFu;
-            g += key > K;
-            q += key == K;
-        }
-        cgt[(uint64_t)r * U + u] = g;
-        ceq[(uint64_t)r * U + u] = q;
-    }
     if (t == 0) {
-        st[r].prefix = K;
+        st[r].prefix = p21 << 10 | b3;
         st[r].krem = krem;
     }
 }
 
-// Per wave unit: entries with key > K* and key == K*.
-__global__ void __launch_bounds__(256) k_count(const float* x, uint64_t N, uint32_t U,
-                                               const RankState* st, uint32_t* cgt, uint32_t* ceq)
+
+// Per unit: entries with key > K* and key == K*.  A wave takes kUPW
+// consecutive units: from the gathered entries on a settled row (all loads
+// in flight together), from the data on a row refined over it.
+constexpr uint32_t kUPW = 8;  // units per wave in the count and write kernels
+
+__global__ void __launch_bounds__(256) k_count(const float* x, uint64_t N, uint32_t U, const RankState* st,
+                                               const uint2* cand, const uint32_t* ccnt, uint32_t* cgt,
+                                               uint32_t* ceq)
 {
     const uint32_t r = blockIdx.y, lane = threadIdx.x & 63;
-    const uint32_t u = blockIdx.x * 4 + (threadIdx.x >> 6);
-    if (u >= U || st[r].full == 0u) return;
+    const uint32_t u0 = (blockIdx.x * 4 + (threadIdx.x >> 6)) * kUPW;
+    if (u0 >= U) return;
     const uint32_t K = st[r].prefix;
+    if (st[r].full == 0u) {
+        uint32_t n[kUPW], key[kUPW];
+#pragma unroll
+        for (uint32_t j = 0; j < kUPW; ++j) n[j] = u0 + j < U ? ccnt[(uint64_t)r * U + u0 + j] : 0u;
+#pragma unroll
+        for (uint32_t j = 0; j < kUPW; ++j)
+            key[j] = lane < n[j] ? cand[((uint64_t)r * U + u0 + j) * kSlots + lane].y & 0x7FFFFFFFu : 0u;
+#pragma unroll
+        for (uint32_t j = 0; j < kUPW; ++j) {
+            const uint32_t g = (uint32_t)__popcll(__ballot(lane < n[j] && key[j] > K));
+            const uint32_t q = (uint32_t)__popcll(__ballot(lane < n[j] && key[j] == K));
+            if (lane == 0 && u0 + j < U) {
+                cgt[(uint64_t)r * U + u0 + j] = g;
+                ceq[(uint64_t)r * U + u0 + j] = q;
+            }
+        }
+        return;
+    }
     const float* row = x + (uint64_t)r * N;
-    const uint64_t lo = (uint64_t)u * kUnit, hi = min(lo + kUnit, N);
-    uint32_t gt = 0, eq = 0;
-    for (uint64_t e = lo + lane; e < hi; e += 64) {
-        const uint32_t key = mag_key(row[e]);
-        gt += key > K;
-        eq += key == K;
-    }
-    for (int o = 32; o > 0; o >>= 1) {
-        gt += __shfl_xor(gt, o);
-        eq += __shfl_xor(eq, o);
-    }
-    if (lane == 0) {
-        cgt[(uint64_t)r * U + u] = gt;
-        ceq[(uint64_t)r * U + u] = eq;
+    for (uint32_t u = u0; u < min(u0 + kUPW, U); ++u) {
+        const uint64_t lo = (uint64_t)u * kUnit, hi = min(lo + kUnit, N);
+        uint32_t gt = 0, eq = 0;
+        for (uint64_t e = lo + lane; e < hi; e += 64) {
+            const uint32_t key = mag_key(row[e]);
+            gt += key > K;
+            eq += key == K;
+        }
+        for (int o = 32; o > 0; o >>= 1) {
+            gt += __shfl_xor(gt, o);
+            eq += __shfl_xor(eq, o);
+        }
+        if (lane == 0) {
+            cgt[(uint64_t)r * U + u] = gt;
+            ceq[(uint64_t)r * U + u] = eq;
+        }
     }
 }
 
@@ -485,14 +568,13 @@ __global__ void __launch_bounds__(1024) k_unit_scan(uint32_t U, const RankState*
     }
 }
 
-__global__ void __launch_bounds__(256) k_write(const float* x, uint64_t N, uint64_t k, uint32_t U,
-                                               const RankState* st, const uint32_t* beq,
-                                               const uint32_t* bout, uint32_t* out_idx, float* out_val,
-                                               float* residual)
+// One unit of a row refined over its data: the selection compacted in index
+// order from the data itself.
+__device__ void write_unit(const float* x, uint64_t N, uint64_t k, uint32_t U, uint32_t r, uint32_t u,
+                           const RankState* st, const uint32_t* beq, const uint32_t* bout, uint32_t* out_idx,
+                           float* out_val, float* residual)
 {
-    const uint32_t r = blockIdx.y, lane = threadIdx.x & 63;
-    const uint32_t u = blockIdx.x * 4 + (threadIdx.x >> 6);
-    if (u >= U || st[r].full == 0u) return;  // written from the gathered entries
+    const uint32_t lane = threadIdx.x & 63;
     const uint32_t K = st[r].prefix;
     const uint64_t need = st[r].krem;
     const float* row = x + (uint64_t)r * N;
@@ -589,40 +671,57 @@ __global__ void __launch_bounds__(256) k_write(const float* x, uint64_t N, uint6
     }
 }
 
-// Rows settled by their gathered entries: per wave unit, the unit's
-// gathered entries (index order, one per lane) selected if key > K* or,
-// for key == K*, while ties are still needed; written at the unit's
-// offset; the residual is zeroed at the selected positions.
-__global__ void __launch_bounds__(256) k_write_cand(uint64_t N, uint64_t k, uint32_t U, const RankState* st,
-                                                    const uint2* cand, const uint32_t* ccnt,
-                                                    const uint32_t* beq, const uint32_t* bout,
-                                                    uint32_t* out_idx, float* out_val, float* residual)
+// Per kUPW units of a wave: a row settled by its gathered entries writes
+// its selection from them (a unit's entries in index order, one per lane):
+// key > K*, or key == K* while ties are still needed, at the unit's offset,
+// zeroing the residual there; a row refined over its data compacts it.
+__global__ void __launch_bounds__(256) k_write(const float* x, uint64_t N, uint64_t k, uint32_t U,
+                                               const RankState* st, const uint2* cand, const uint32_t* ccnt,
+                                               const uint32_t* beq, const uint32_t* bout, uint32_t* out_idx,
+                                               float* out_val, float* residual)
 {
     const uint32_t r = blockIdx.y, lane = threadIdx.x & 63;
-    const uint32_t u = blockIdx.x * 4 + (threadIdx.x >> 6);
-    if (u >= U || st[r].full != 0u) return;
+    const uint32_t u0 = (blockIdx.x * 4 + (threadIdx.x >> 6)) * kUPW;
+    if (u0 >= U) return;
+    if (st[r].full != 0u) {
+        for (uint32_t u = u0; u < min(u0 + kUPW, U); ++u)
+            write_unit(x, N, k, U, r, u, st, beq, bout, out_idx, out_val, residual);
+        return;
+    }
     const uint32_t K = st[r].prefix;
     const uint64_t need = st[r].krem;
-    const uint32_t n = ccnt[(uint64_t)r * U + u];  // <= kSlots on a settled row
-    const uint2 c = lane < n ? cand[((uint64_t)r * U + u) * kSlots + lane] : make_uint2(0u, 0u);
-    const uint32_t key = c.y & 0x7FFFFFFFu;
     const uint64_t lt = (1ull << lane) - 1ull;
-    const bool eq = lane < n && key == K;
-    const uint64_t beq_w = __ballot(eq);
-    const bool sel = (lane < n && key > K) ||
-                     (eq && (uint64_t)beq[(uint64_t)r * U + u] + (uint64_t)__popcll(beq_w & lt) < need);
-    const uint64_t bsel = __ballot(sel);
-    if (sel) {
-        const uint64_t o = (uint64_t)r * k + bout[(uint64_t)r * U + u] + (uint32_t)__popcll(bsel & lt);
-        out_idx[o] = c.x;
-        out_val[o] = __uint_as_float(c.y);
-        if (residual) residual[(uint64_t)r * N + c.x] = 0.0f;
+    uint32_t n[kUPW], eqb[kUPW], ob[kUPW];
+    uint2 c[kUPW];
+#pragma unroll
+    for (uint32_t j = 0; j < kUPW; ++j) {
+        const bool in = u0 + j < U;
+        n[j] = in ? ccnt[(uint64_t)r * U + u0 + j] : 0u;  // <= kSlots on a settled row
+        eqb[j] = in ? beq[(uint64_t)r * U + u0 + j] : 0u;
+        ob[j] = in ? bout[(uint64_t)r * U + u0 + j] : 0u;
+    }
+#pragma unroll
+    for (uint32_t j = 0; j < kUPW; ++j)
+        c[j] = lane < n[j] ? cand[((uint64_t)r * U + u0 + j) * kSlots + lane] : make_uint2(0u, 0u);
+#pragma unroll
+    for (uint32_t j = 0; j < kUPW; ++j) {
+        const uint32_t key = c[j].y & 0x7FFFFFFFu;
+        const bool eq = lane < n[j] && key == K;
+        const uint64_t beq_w = __ballot(eq);
+        const bool sel = (lane < n[j] && key > K) || (eq && (uint64_t)eqb[j] + (uint64_t)__popcll(beq_w & lt) < need);
+        const uint64_t bsel = __ballot(sel);
+        if (sel) {
+            const uint64_t o = (uint64_t)r * k + ob[j] + (uint32_t)__popcll(bsel & lt);
+            out_idx[o] = c[j].x;
+            out_val[o] = __uint_as_float(c[j].y);
+            if (residual) residual[(uint64_t)r * N + c[j].x] = 0.0f;
+        }
     }
 }
 
 struct TLayout {
     RankState* st;
-    uint32_t *hist, *cgt, *ceq, *beq, *bout, *ccnt, *overflow;
+    uint32_t *hist, *cgt, *ceq, *beq, *bout, *ccnt, *overflow, *klist, *kcnt;
     uint2* cand;
     uint32_t U;
     size_t bytes;
@@ -635,6 +734,8 @@ TLayout tlayout(int P, uint64_t N, void* ws)
     l.U = (uint32_t)((N + kUnit - 1) / kUnit);
     l.st = c.take<RankState>(P);
     l.overflow = c.take<uint32_t>(P);
+    l.kcnt = c.take<uint32_t>((size_t)P * kSub * kCntStride);
+    l.klist = c.take<uint32_t>((size_t)P * kList);
     l.ccnt = c.take<uint32_t>((size_t)P * l.U);
     l.cand = c.take<uint2>((size_t)P * l.U * kSlots);
     l.hist = c.take<uint32_t>((size_t)P * 2048);
@@ -662,9 +763,9 @@ hipError_t topk_run(int P, const float* x, uint64_t N, uint64_t k, uint32_t* out
     // expected selections per unit decide where a row starts
     const double per_unit = (double)k * kUnit / (double)N;
     const uint32_t mode = per_unit > kSlots ? 2u : (per_unit > kSlots / 4 ? 1u : 0u);
-    const uint64_t ninit = (uint64_t)P * 2048;
+    const uint64_t ninit = (uint64_t)P * 2048;  // covers P * kSub counters too
     hipLaunchKernelGGL(k_init, dim3((uint32_t)((ninit + 255) / 256)), dim3(256), 0, s, l.st,
-                       (uint32_t)P, k, l.hist, l.overflow, mode);
+                       (uint32_t)P, k, l.hist, l.overflow, mode, l.kcnt);
     const uint32_t hb = (uint32_t)std::min<uint64_t>(kHistBlocksPerRank, (N + 4095) / 4096);
     const dim3 hgrid(hb, P), ugrid((l.U + 3) / 4, P);
     // sample: every stride-th 256-element segment, about kSampleSegs of them
@@ -673,22 +774,21 @@ hipError_t topk_run(int P, const float* x, uint64_t N, uint64_t k, uint32_t* out
     uint64_t sampled = 0;
     for (uint64_t g = 0; g < nseg; g += stride) sampled += std::min<uint64_t>(256, N - g * 256);
     const double frac = (double)sampled / (double)N;
-    const uint32_t sb = (uint32_t)std::min<uint64_t>(16, (nseg + stride - 1) / stride);
+    const uint32_t sb = (uint32_t)std::min<uint64_t>(64, (nseg + stride - 1) / stride);
     timer_begin(kTTopkSelect, s);
     if (mode == 0) {
         hipLaunchKernelGGL(k_sample, dim3(sb, P), dim3(256), 0, s, x, N, (uint32_t)stride, l.hist);
         hipLaunchKernelGGL(k_estimate, dim3(P), dim3(256), 0, s, l.st, l.hist, k, frac);
         hipLaunchKernelGGL(k_gather, ugrid, dim3(256), 0, s, x, N, l.U, l.st, l.cand, l.ccnt, l.overflow,
-                           residual, 0u);
-        hipLaunchKernelGGL(k_check, dim3(P), dim3(1024), 0, s, l.U, k, l.st, l.ccnt, l.overflow);
+                           residual, 0u, l.klist, l.kcnt);
+        hipLaunchKernelGGL(k_check, dim3(P), dim3(1024), 0, s, l.U, k, l.st, l.ccnt, l.overflow, l.kcnt);
     }
     // rows whose estimate failed: the exact boundary bin, a second gather
     hipLaunchKernelGGL(k_hist<0>, hgrid, dim3(256), 0, s, x, N, l.st, l.hist);
     hipLaunchKernelGGL(k_select<0>, dim3(P), dim3(256), 0, s, l.st, l.hist);
     hipLaunchKernelGGL(k_gather, ugrid, dim3(256), 0, s, x, N, l.U, l.st, l.cand, l.ccnt, l.overflow,
-                       residual, 1u);
-    hipLaunchKernelGGL(k_cand_select, dim3(P), dim3(1024), 0, s, l.U, k, l.st, l.cand, l.ccnt, l.overflow,
-                       l.cgt, l.ceq);
+                       residual, 1u, l.klist, l.kcnt);
+    hipLaunchKernelGGL(k_cand_select, dim3(P), dim3(1024), 0, s, k, l.st, l.klist, l.kcnt, l.overflow);
     // rows whose boundary bin overflowed the gather buffer (the others return at once)
     hipLaunchKernelGGL(k_hist<1>, hgrid, dim3(256), 0, s, x, N, l.st, l.hist);
     hipLaunchKernelGGL(k_select<1>, dim3(P), dim3(256), 0, s, l.st, l.hist);
@@ -696,11 +796,10 @@ hipError_t topk_run(int P, const float* x, uint64_t N, uint64_t k, uint32_t* out
     hipLaunchKernelGGL(k_select<2>, dim3(P), dim3(256), 0, s, l.st, l.hist);
     timer_end(kTTopkSelect, s);
     timer_begin(kTTopkWrite, s);
-    hipLaunchKernelGGL(k_count, ugrid, dim3(256), 0, s, x, N, l.U, l.st, l.cgt, l.ceq);
+    const dim3 wgrid((l.U + 4 * kUPW - 1) / (4 * kUPW), P);
+    hipLaunchKernelGGL(k_count, wgrid, dim3(256), 0, s, x, N, l.U, l.st, l.cand, l.ccnt, l.cgt, l.ceq);
     hipLaunchKernelGGL(k_unit_scan, dim3(P), dim3(1024), 0, s, l.U, l.st, l.cgt, l.ceq, l.beq, l.bout);
-    hipLaunchKernelGGL(k_write, ugrid, dim3(256), 0, s, x, N, k, l.U, l.st, l.beq, l.bout, out_idx,
-                       out_val, residual);
-    hipLaunchKernelGGL(k_write_cand, ugrid, dim3(256), 0, s, N, k, l.U, l.st, l.cand, l.ccnt, l.beq, l.bout,
+    hipLaunchKernelGGL(k_write, wgrid, dim3(256), 0, s, x, N, k, l.U, l.st, l.cand, l.ccnt, l.beq, l.bout,
                        out_idx, out_val, residual);
     timer_end(kTTopkWrite, s);
     return hipGetLastError();
