@@ -217,11 +217,11 @@ class Workload:
             self.nnz = c.P * c.k
             self.reduce = S.ReduceCall(idx, c.N, c.delta, vals=vals)
             self.groups += [S.TIMER_TOPK_SELECT, S.TIMER_TOPK_WRITE]
-            # compulsory bytes: one read of x (selection), x read + k pairs
-            # written (compaction); the passes re-read x, which the roofline
-            # fraction then shows as lost bandwidth
+            # compulsory bytes: one read of x (the sampled histogram and the
+            # gather pass), the k selected pairs written (from the gathered
+            # entries); any re-read shows as lost bandwidth
             self.kernel_bytes[S.TIMER_TOPK_SELECT] = c.P * c.N * 4
-            self.kernel_bytes[S.TIMER_TOPK_WRITE] = c.P * c.N * 4 + c.P * c.k * 8
+            self.kernel_bytes[S.TIMER_TOPK_WRITE] = c.P * c.k * 8
             self._steps = [self.topk.run, self.reduce.run_async]
         else:
             self.nnz = sum(a.size for a in d["idx"])
