@@ -102,3 +102,74 @@ def test_c3_full_topk_and_reduce():
     o = oracle.sparse_reduce([oi[r] for r in range(c.P)], [ov[r] for r in range(c.P)], c.N, c.delta)
     assert_reduce_equal(g, o, "c3 full")
     assert not g["dense"]
+
+
+@pytest.mark.timeout(900)
+def test_c3_bucketed_full_step():
+    """c3's rows as gradients with Alg. 1's error feedback and 4 of every 512
+    coordinates selected (the c3/bucketed benchmark step): selections, values
+    and the updated error of every row, then the reduce, against the oracle."""
+    import bench
+    torch, dev = torch_dev()
+    c = inputs.config(3)
+    say(f"[full] c3/bucketed: P={c.P} N={c.N}")
+    w = bench.Workload("c3/bucketed", c, 0, torch, dev, bucketed=(512, 4))
+    w.topk.run()
+    torch.cuda.synchronize()
+    gi = to_np(w.topk.idx, np.uint32)[:, : w.topk.K]
+    gv = to_np(w.topk.val)[:, : w.topk.K]
+    ge = to_np(w.topk.eps)
+    g = _gpu_result(w.reduce, torch)
+    say("[full] c3/bucketed: oracle (zero error, alpha 0.1)")
+    x = inputs.generate(c, 0)["x"]
+    oi, ov, oe = oracle.topk_bucketed(np.zeros_like(x), x, 0.1, 512, 4)
+    np.testing.assert_array_equal(gi, oi, err_msg="selected indices")
+    assert_values(gv.ravel(), ov.ravel(), "selected values")
+    assert_values(ge.ravel(), oe.ravel(), "updated error")
+    del x, oe, ge
+    o = oracle.sparse_reduce([oi[r] for r in range(c.P)], [ov[r] for r in range(c.P)], c.N, c.delta)
+    assert_reduce_equal(g, o, "c3/bucketed full")
+
+
+@pytest.mark.timeout(900)
+def test_c4_with_48_ranks_full_reduce():
+    """c4 with a rank count that is not a power of two (App. A's step in
+    front), at full size."""
+    import dataclasses
+    import bench
+    torch, dev = torch_dev()
+    c = dataclasses.replace(inputs.config(4), P=48)
+    say(f"[full] c4/p48: P={c.P} N={c.N}")
+    w = bench.Workload("c4/p48", c, 0, torch, dev)
+    g = _gpu_result(w.reduce, torch)
+    d = inputs.generate(c, 0)
+    o = oracle.sparse_reduce(d["idx"], d["val"], c.N, c.delta)
+    assert_reduce_equal(g, o, "c4/p48 full")
+
+
+@pytest.mark.timeout(900)
+def test_c5_dsar_full_step_sampled_shares():
+    """One DSAR node step at c5's size (the c5/dsar benchmark step): the
+    gathered, decoded vector of 2^27 coordinates compared with the oracle's
+    pipeline (range reduce of the share, bucketed QSGD, decode) on the first,
+    a middle and the last of the 128 shares; the node's own share (0)
+    computed by the timed step itself."""
+    import bench
+    torch, dev = torch_dev()
+    c = inputs.config(5)
+    say(f"[full] c5/dsar: P={c.P} N={c.N} preparing the other nodes' shares")
+    w = bench.DsarWorkload("c5/dsar", c, 0, torch, dev)
+    w.step()
+    torch.cuda.synchronize()
+    got = to_np(w.concat.out_val)
+    d = inputs.generate(c, 0)
+    b = [c.N * s // c.P for s in range(c.P + 1)]
+    for sh in (0, c.P // 2, c.P - 1):
+        lo, hi = b[sh], b[sh + 1]
+        say(f"[full] c5/dsar: oracle share {sh} [{lo}, {hi})")
+        m = [(a >= lo) & (a < hi) for a in d["idx"]]
+        o = oracle.sparse_reduce_range([a[k] for a, k in zip(d["idx"], m)], [v[k] for v, k in zip(d["val"], m)],
+                                       c.N, lo, hi, c.delta)
+        assert o["dense"]
+        q, sc, deq = oracle.quantize([o["val"]], w.bits, inputs.quant_seed(0, c.cfg) + sh, bucket=w.bucket)
+        assert_values(got[lo:hi], deq[0], f"share {sh}")
