@@ -146,6 +146,23 @@ def test_concat_quantized_parts(qbits, bucket):
     check_concat(hp, dp, b, N, 5.0, "sparse quantized", qbits, bucket)
 
 
+def test_concat_unaligned_code_arrays():
+    """Dense QSGD parts whose code arrays start at odd byte addresses (the
+    per-element decode path) next to aligned ones."""
+    torch, dev = torch_dev()
+    rng = np.random.default_rng(414)
+    N, P, B = 100003, 4, 64
+    b = [N * s // P for s in range(P + 1)]
+    for bits in (2, 4, 8):
+        hp, dp = make_parts(rng, b, ["dense"] * P, bits, B, seed=11)
+        for s_, d in enumerate(dp):
+            if s_ % 2:
+                buf = torch.zeros(d["codes"].numel() + 1, dtype=torch.uint8, device=dev)
+                buf[1:] = d["codes"]
+                d["codes"] = buf[1:]  # one byte past an aligned start
+        check_concat(hp, dp, b, N, 0.1, "unaligned codes", bits, B)
+
+
 def test_concat_many_parts_and_single_part():
     rng = np.random.default_rng(413)
     N, P = 2000000, 1000
