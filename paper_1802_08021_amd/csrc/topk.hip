@@ -545,25 +545,53 @@ __global__ void __launch_bounds__(1024) k_unit_scan(uint32_t U, const RankState*
     const uint32_t lo = min(threadIdx.x * per, U), hi = min(lo + per, U);
     const uint32_t* g = cgt + (uint64_t)r * U;
     const uint32_t* q = ceq + (uint64_t)r * U;
+    // the first kScanPer of a thread's units read at once (all of them at the
+    // common sizes), the rest in turn
+    constexpr uint32_t kScanPer = 8;
+    const uint32_t h8 = min(hi, lo + kScanPer);
+    uint32_t gv[kScanPer], qv[kScanPer];
+#pragma unroll
+    for (uint32_t j = 0; j < kScanPer; ++j) {
+        gv[j] = lo + j < h8 ? g[lo + j] : 0u;
+        qv[j] = lo + j < h8 ? q[lo + j] : 0u;
+    }
     uint32_t seq = 0;
-    for (uint32_t i = lo; i < hi; ++i) seq += q[i];
+#pragma unroll
+    for (uint32_t j = 0; j < kScanPer; ++j) seq += qv[j];
+    for (uint32_t i = h8; i < hi; ++i) seq += q[i];
     uint32_t tot;
     uint32_t run_eq = block_excl_scan(seq, s_w, &tot);
+    // selections of a unit: its keys above K*, and its ties while needed
+    auto take = [&](uint32_t re, uint32_t gi, uint32_t qi) {
+        return gi + (re >= need ? 0u : (uint32_t)min<uint64_t>(need - re, qi));
+    };
     uint32_t ssel = 0;
     {
         uint32_t re = run_eq;
-        for (uint32_t i = lo; i < hi; ++i) {
-            const uint64_t take = re >= need ? 0 : min<uint64_t>(need - re, q[i]);
-            ssel += g[i] + (uint32_t)take;
+#pragma unroll
+        for (uint32_t j = 0; j < kScanPer; ++j) {
+            ssel += take(re, gv[j], qv[j]);
+            re += qv[j];
+        }
+        for (uint32_t i = h8; i < hi; ++i) {
+            ssel += take(re, g[i], q[i]);
             re += q[i];
         }
     }
     uint32_t run_out = block_excl_scan(ssel, s_w, &tot);
-    for (uint32_t i = lo; i < hi; ++i) {
+#pragma unroll
+    for (uint32_t j = 0; j < kScanPer; ++j) {
+        if (lo + j < h8) {
+            beq[(uint64_t)r * U + lo + j] = run_eq;
+            bout[(uint64_t)r * U + lo + j] = run_out;
+        }
+        run_out += take(run_eq, gv[j], qv[j]);
+        run_eq += qv[j];
+    }
+    for (uint32_t i = h8; i < hi; ++i) {
         beq[(uint64_t)r * U + i] = run_eq;
         bout[(uint64_t)r * U + i] = run_out;
-        const uint64_t take = run_eq >= need ? 0 : min<uint64_t>(need - run_eq, q[i]);
-        run_out += g[i] + (uint32_t)take;
+        run_out += take(run_eq, g[i], q[i]);
         run_eq += q[i];
     }
 }
