@@ -392,10 +392,15 @@ GROUP_NAMES = {0: "reduce_tiles", 1: "reduce_write", 2: "reduce_slow", 3: "qsgd_
 
 
 def source_hash() -> str:
+    """sha256 of the tile pass's sources without comments and blank lines
+    (a change of code, not of wording, invalidates measured traffic)."""
     h = hashlib.sha256()
     for f in ("reduce.hip", "qsgd_device.h", "internal.h"):
-        with open(os.path.join(ROOT, "paper_1802_08021_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
+        with open(os.path.join(ROOT, "paper_1802_08021_amd", "csrc", f)) as fh:
+            for line in fh:
+                code = line.split("//", 1)[0].rstrip()
+                if code:
+                    h.update(code.encode() + b"\n")
     return h.hexdigest()
 
 

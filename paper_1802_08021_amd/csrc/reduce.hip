@@ -7,12 +7,16 @@
 // the tree (which moves log2(P) times the data), the coordinate space is cut
 // into tiles of T indices and each tile evaluates the whole tree at once:
 //
-//  * a rank bitmask per coordinate (LDS) records which ranks hold it; the
-//    popcount prefix of the mask places each rank's value in rank order;
-//  * a per-coordinate walk over the present ranks sums the values with the
-//    exact association of the tree: two ranks first meet at the level given
-//    by the highest differing bit of their numbers, so a stack keyed by that
-//    level reproduces ((r0+r1)+(r2+r3))... for any subset of ranks;
+//  * every entry of the tile takes an arrival number at its coordinate (an
+//    LDS atomic on a word that also sums the arrived ranks); the first
+//    arrival leaves its value there;
+//  * the later arrivals are summed with the exact association of the tree:
+//    two ranks first meet at the level given by the highest differing bit of
+//    their numbers (their separator), and the root of any subset of ranks
+//    splits at the largest separator between rank-order neighbours -- so two
+//    ranks need one addition, three or four a closed form of the separators,
+//    five a sorting network, and more a walk that reduces the tree level by
+//    level across the lanes of a row;
 //  * the exact union size of every tree node -- what the switch rule needs --
 //    is counted on the side: the entry of rank r whose predecessor (next
 //    lower present rank) differs from r first at bit h opens a new group at
@@ -62,8 +66,9 @@ struct SlowShape {
 // per tile it reads a 64-entry window of each slot's stream (one entry per
 // lane) and compacts the entries inside the tile into its own region of at
 // most ECAP entries.  TMAX coordinates per tile; CAP staged entries (those
-// of indices held by three or more ranks).  Up to 128 ranks: two 512-thread
-// workgroups per CU (LDS), four waves per SIMD.
+// of indices held by three or more ranks).  Above 32 ranks a 1024-thread
+// workgroup holds about 147 KB of LDS, so one runs per CU (four waves per
+// SIMD); up to 32 ranks 512 threads and half the tile.
 template <int PMAX>
 struct Fast {
     static constexpr int NT = PMAX <= 32 ? 512 : 1024;
