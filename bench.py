@@ -17,12 +17,14 @@ Besides the headline line the JSON carries:
                 traffic = measured HBM bytes per launch from rocprofv3
                 FETCH_SIZE/WRITE_SIZE runs (profiles/), or null when the
                 kernel source changed since they were taken;
-  cpu_baseline  the CPU oracle timed on a bounded sample of the workload;
+  cpu_baseline  the CPU oracle timed on the workload's input (one host core);
   cold_ms_per_step  the step with the 256 MB Infinity Cache evicted first
                 (median of 5);
   seeds         the step over seeds s..s+4 (fresh inputs): per-seed ms,
                 median and quartiles;
   copy_ceiling  a plain 1 GiB device copy's bandwidth, the streaming ceiling;
+  parts         the producer (QSGD or top-k) and the reduce apart: summed
+                kernel time and input rate of each;
   per_config    the other configurations (c1..c4; c3 = top-k then reduce,
                 with the top-k input elements per second), each timed
                 after at least 0.3 s of warm-up steps, and the split-phase
@@ -419,9 +421,10 @@ def traffic_for(kernel: str, workload: str):
     return t.get("bytes_per_launch")
 
 
-def cpu_baseline(d, c, seed, frac_log2=2):
+def cpu_baseline(d, c, seed, frac_log2=0):
     """Oracle (quantize + reduce) on the coordinate slice [0, N/2^frac_log2)
-    of the same streams: same P, density, threshold fraction and tree."""
+    of the same streams: same P, density, threshold fraction and tree (the
+    whole workload by default: several seconds on one host core)."""
     import oracle
     from paper_1802_08021_amd import inputs
     Ns = c.N >> frac_log2
@@ -439,7 +442,8 @@ def cpu_baseline(d, c, seed, frac_log2=2):
     oracle.sparse_reduce(idx, deq, Ns, c.delta)
     dt = time.perf_counter() - t0
     return {"value": nnz / dt, "unit": "nnz/s", "cores": 1, "kind": "oracle",
-            "sample": f"{c.name} streams restricted to indices < N/{2**frac_log2} "
+            "sample": (f"{c.name} streams restricted to indices < N/{2**frac_log2} " if frac_log2 else
+                       f"the whole {c.name} input ") +
                       f"({nnz} input nnz, N'={Ns}); quantize + reduce, single thread, {dt:.2f} s; "
                       f"host {cpu_model()}, {os.cpu_count()} logical CPUs"}
 
@@ -494,6 +498,17 @@ def main() -> int:
                                 "GB/s": (w.kernel_bytes[g] / (v * 1e-3) / 1e9) if w.kernel_bytes.get(g) else None}
                for g, v in kdur.items()}
 
+    # the step's producer and reduce apart (kernel timers; launches between
+    # kernels not included), each with its input rate
+    def group_ms(gs):
+        return sum(kdur.get(g, 0.0) for g in gs)
+    prod = [S.TIMER_QUANT_NORM, S.TIMER_QUANT_CODES, S.TIMER_TOPK_SELECT, S.TIMER_TOPK_WRITE]
+    red = [S.TIMER_REDUCE_PASS, S.TIMER_REDUCE_SLOW, S.TIMER_REDUCE_WRITE]
+    parts = {"reduce": {"kernel_ms": group_ms(red), "input_nnz_per_s": w.nnz / (group_ms(red) * 1e-3)}}
+    if group_ms(prod):
+        pn = w.nnz if head_cfg.qbits else head_cfg.P * head_cfg.N
+        parts["producer"] = {"kind": "qsgd" if head_cfg.qbits else "topk", "kernel_ms": group_ms(prod),
+                             "input_elems_per_s": pn / (group_ms(prod) * 1e-3)}
     cold_ms = time_cold(w, 5, torch)
     log(f"{args.workload}: cold (Infinity Cache evicted) {cold_ms:.3f} ms/step")
     cpu = None
@@ -581,6 +596,7 @@ def main() -> int:
         "step_GB/s": step_gbs,
         "roofline": roofline,
         "kernels": kernels,
+        "parts": parts,
         "cpu_baseline": cpu,
         "wall_ms_per_step": wall,
         "cold_ms_per_step": cold_ms,
