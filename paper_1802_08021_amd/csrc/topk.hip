@@ -258,29 +258,6 @@ __global__ void __launch_bounds__(256) k_estimate(RankState* st, uint32_t* hist,
     if (tid == 0) st[r].prefix = s_bin;
 }
 
-// After the estimated gather: a row whose units overflowed or whose
-// gathered keys number fewer than k takes the exact path (a histogram of
-// the full row, then a second gather).
-__global__ void __launch_bounds__(1024) k_check(uint32_t U, uint64_t k, RankState* st, const uint32_t* ccnt,
-                                                uint32_t* overflow, uint32_t* kcnt)
-{
-    __shared__ uint32_t s_w[16];
-    const uint32_t r = blockIdx.x;
-    uint32_t mine = 0;
-    for (uint32_t u = threadIdx.x; u < U; u += 1024) mine += ccnt[(uint64_t)r * U + u];
-    uint32_t total;
-    block_excl_scan(mine, s_w, &total);
-    if (threadIdx.x == 0 && (overflow[r] != 0u || total < k)) {
-        st[r].exact = 1u;
-        st[r].prefix = 0u;
-        st[r].krem = k;
-        overflow[r] = 0u;
-    }
-    __syncthreads();
-    if (threadIdx.x < kSub && st[r].exact != 0u && st[r].full == 0u)
-        kcnt[((uint64_t)r * kSub + threadIdx.x) * kCntStride] = 0u;
-}
-
 // Per wave unit: every entry whose top 11 key bits are at or above the
 // gather bin goes as {element, value bits} into the unit's kSlots slots in
 // index order, and its key into the row's key list (a unit with more, or a
@@ -407,13 +384,30 @@ __device__ uint32_t block_find(uint32_t cnt, uint64_t krem, uint32_t NB, uint64_
 // K* and the ties still needed, from the key list of row r (every key at or
 // above its gather bin).
 __global__ void __launch_bounds__(1024) k_cand_select(uint64_t k, RankState* st, const uint32_t* klist,
-                                                      const uint32_t* kcnt, const uint32_t* overflow)
+                                                      uint32_t* kcnt, uint32_t* overflow, uint32_t exact)
 {
     __shared__ uint32_t s_h[2048];
     __shared__ uint32_t s_w[16];
     __shared__ uint32_t s_res[2];
     const uint32_t r = blockIdx.x, t = threadIdx.x;
-    if (overflow[r]) {  // too many to gather: refine by passes over the data
+    if (st[r].exact != exact || st[r].full != 0u) return;  // row not on this path (whole workgroup)
+    // keys gathered for the row (the sub-list counters) and the overflow flag
+    uint32_t total;
+    block_excl_scan(t < kSub ? kcnt[((uint64_t)r * kSub + t) * kCntStride] : 0u, s_w, &total);
+    const bool ov = overflow[r] != 0u;
+    if (exact == 0u && (ov || total < k)) {
+        // the sampled bin failed: the exact one from a histogram of the row,
+        // then a second gather
+        if (t == 0) {
+            st[r].exact = 1u;
+            st[r].prefix = 0u;
+            st[r].krem = k;
+            overflow[r] = 0u;
+        }
+        if (t < kSub) kcnt[((uint64_t)r * kSub + t) * kCntStride] = 0u;
+        return;
+    }
+    if (ov) {  // too many to gather even from the exact bin: passes over the data
         if (t == 0) st[r].full = 1u;
         return;
     }
@@ -809,14 +803,15 @@ hipError_t topk_run(int P, const float* x, uint64_t N, uint64_t k, uint32_t* out
         hipLaunchKernelGGL(k_estimate, dim3(P), dim3(256), 0, s, l.st, l.hist, k, frac);
         hipLaunchKernelGGL(k_gather, ugrid, dim3(256), 0, s, x, N, l.U, l.st, l.cand, l.ccnt, l.overflow,
                            residual, 0u, l.klist, l.kcnt);
-        hipLaunchKernelGGL(k_check, dim3(P), dim3(1024), 0, s, l.U, k, l.st, l.ccnt, l.overflow, l.kcnt);
+        // settles the rows whose sampled bin held; the others go exact
+        hipLaunchKernelGGL(k_cand_select, dim3(P), dim3(1024), 0, s, k, l.st, l.klist, l.kcnt, l.overflow, 0u);
     }
-    // rows whose estimate failed: the exact boundary bin, a second gather
+    // rows on the exact path: the exact boundary bin, a gather from it
     hipLaunchKernelGGL(k_hist<0>, hgrid, dim3(256), 0, s, x, N, l.st, l.hist);
     hipLaunchKernelGGL(k_select<0>, dim3(P), dim3(256), 0, s, l.st, l.hist);
     hipLaunchKernelGGL(k_gather, ugrid, dim3(256), 0, s, x, N, l.U, l.st, l.cand, l.ccnt, l.overflow,
                        residual, 1u, l.klist, l.kcnt);
-    hipLaunchKernelGGL(k_cand_select, dim3(P), dim3(1024), 0, s, k, l.st, l.klist, l.kcnt, l.overflow);
+    hipLaunchKernelGGL(k_cand_select, dim3(P), dim3(1024), 0, s, k, l.st, l.klist, l.kcnt, l.overflow, 1u);
     // rows whose boundary bin overflowed the gather buffer (the others return at once)
     hipLaunchKernelGGL(k_hist<1>, hgrid, dim3(256), 0, s, x, N, l.st, l.hist);
     hipLaunchKernelGGL(k_select<1>, dim3(P), dim3(256), 0, s, l.st, l.hist);
