@@ -460,7 +460,7 @@ def main() -> int:
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py measures one GPU's share of the reduction; runs on more than one GPU "
-              "are not part of this build (use --gpus 1).", file=sys.stderr)
+              "are not implemented (use --gpus 1).", file=sys.stderr)
         return 2
     import torch
     from paper_1802_08021_amd import inputs, sparcml as S
