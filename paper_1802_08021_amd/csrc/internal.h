@@ -68,6 +68,14 @@ __device__ __forceinline__ void store_nt(float* p, float4 v)
     __builtin_nontemporal_store(x, reinterpret_cast<f4*>(p));
 }
 
+// 16-byte load marked nontemporal (data streamed through once).
+__device__ __forceinline__ float4 load_nt(const float* p)
+{
+    typedef float f4 __attribute__((ext_vector_type(4)));
+    const f4 x = __builtin_nontemporal_load(reinterpret_cast<const f4*>(p));
+    return make_float4(x.x, x.y, x.z, x.w);
+}
+
 // Round x up to a multiple of a (a power of two).
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) & ~(a - 1); }
 

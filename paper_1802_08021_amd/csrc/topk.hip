@@ -301,42 +301,44 @@ __global__ void __launch_bounds__(256) k_gather(const float* x, uint64_t N, uint
     };
     const bool rvec = res == nullptr || (reinterpret_cast<uintptr_t>(res) & 15u) == 0u;
     if ((reinterpret_cast<uintptr_t>(row) & 15u) == 0u && rvec && hi - lo == kUnit) {
-        // the unit's 16 float4 per lane, all requested before use; lane i
-        // holds elements 4i..4i+3 of every 256, so entries are placed in
-        // index order by a wave scan per 256 elements
+        // the unit's 16 float4 per lane, all requested before use (loads
+        // marked nontemporal: the row is streamed once); lane i holds
+        // elements 4i..4i+3 of every 256, so entries are placed in index
+        // order by a wave scan per 256 elements that hold any
         float4 vs[kUnit / 256];
 #pragma unroll
         for (uint32_t q = 0; q < kUnit / 256; ++q)
-            vs[q] = *reinterpret_cast<const float4*>(row + lo + 256u * q + 4u * lane);
-        auto in4 = [&](const float4& v, bool* i) {
-            i[0] = (mag_key(v.x) >> 20) >= bin;
-            i[1] = (mag_key(v.y) >> 20) >= bin;
-            i[2] = (mag_key(v.z) >> 20) >= bin;
-            i[3] = (mag_key(v.w) >> 20) >= bin;
-            return (uint32_t)i[0] + (uint32_t)i[1] + (uint32_t)i[2] + (uint32_t)i[3];
+            vs[q] = load_nt(row + lo + 256u * q + 4u * lane);
+        // in-bin flags of the lane's elements, bit k of nibble q for element
+        // 256q + 4 lane + k (two words of eight nibbles: a handful of
+        // registers instead of 64 lane masks)
+        auto in4 = [&](const float4& v) {
+            return (uint32_t)((mag_key(v.x) >> 20) >= bin) | (uint32_t)((mag_key(v.y) >> 20) >= bin) << 1 |
+                   (uint32_t)((mag_key(v.z) >> 20) >= bin) << 2 | (uint32_t)((mag_key(v.w) >> 20) >= bin) << 3;
         };
-        uint32_t mine = 0;
+        uint32_t fl[2] = {0u, 0u};
 #pragma unroll
         for (uint32_t q = 0; q < kUnit / 256; ++q) {
-            bool i[4];
-            mine += in4(vs[q], i);
+            fl[q / 8] |= in4(vs[q]) << (4 * (q % 8));
             if (res) store_nt(res + lo + 256u * q + 4u * lane, vs[q]);
         }
+        const uint32_t mine = (uint32_t)__popc(fl[0]) + (uint32_t)__popc(fl[1]);
         const uint32_t nc = (uint32_t)__builtin_amdgcn_readlane((int)wave_scan(mine), 63);
         uint32_t base;
         if (reserve(nc, &base)) {
             uint32_t run = 0;
 #pragma unroll
             for (uint32_t q = 0; q < kUnit / 256; ++q) {
+                const uint32_t f = (fl[q / 8] >> (4 * (q % 8))) & 15u;
+                const uint32_t n4 = (uint32_t)__popc(f);
+                if (__ballot(n4 != 0u) == 0ull) continue;  // no entry in these 256 elements
                 const uint64_t e = lo + 256u * q + 4u * lane;
-                bool i[4];
-                const uint32_t n4 = in4(vs[q], i);
                 const uint32_t incl = wave_scan(n4);
                 uint32_t at = run + incl - n4;
-                if (i[0]) put(at++, base, e, vs[q].x);
-                if (i[1]) put(at++, base, e + 1, vs[q].y);
-                if (i[2]) put(at++, base, e + 2, vs[q].z);
-                if (i[3]) put(at, base, e + 3, vs[q].w);
+                if (f & 1u) put(at++, base, e, vs[q].x);
+                if (f & 2u) put(at++, base, e + 1, vs[q].y);
+                if (f & 4u) put(at++, base, e + 2, vs[q].z);
+                if (f & 8u) put(at, base, e + 3, vs[q].w);
                 run += (uint32_t)__builtin_amdgcn_readlane((int)incl, 63);
             }
         }
