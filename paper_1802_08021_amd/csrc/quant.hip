@@ -50,7 +50,7 @@ __global__ void __launch_bounds__(256) k_sumsq_partial(const QDesc* tab, double*
         const uint64_t e = base + (uint64_t)it * 256 + (uint64_t)lane * 4;
         float4 x;
         if (vec && e + 4 <= n) {
-            x = *reinterpret_cast<const float4*>(v + e);
+            x = load_nt(v + e);  // streamed: nontemporal
         } else {
             x.x = e < n ? v[e] : 0.0f;
             x.y = e + 1 < n ? v[e + 1] : 0.0f;
