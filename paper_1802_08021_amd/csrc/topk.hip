@@ -384,7 +384,10 @@ __device__ uint32_t block_find(uint32_t cnt, uint64_t krem, uint32_t NB, uint64_
 }
 
 // K* and the ties still needed, from the key list of row r (every key at or
-// above its gather bin).
+// above its gather bin), for the rows on the path `exact` names.  After the
+// sampled gather (exact = 0) a row that gathered fewer than k keys, or
+// overflowed, is sent to the exact path instead; after the exact gather a row
+// that overflowed is sent to the passes over its data.
 __global__ void __launch_bounds__(1024) k_cand_select(uint64_t k, RankState* st, const uint32_t* klist,
                                                       uint32_t* kcnt, uint32_t* overflow, uint32_t exact)
 {
