@@ -26,8 +26,9 @@
 //
 // Passes: partition (per-chunk stream offsets) -> tile pass (COUNT, or DENSE
 // when the root is likely dense) -> slow pass for tiles that overflow the
-// fast path's LDS budget -> decide (switch rule over the node counts) ->
-// [scan of per-tile union sizes -> SPARSE_WRITE tile and slow passes].
+// fast path's LDS budget -> decide (switch rule over the node counts) and,
+// in the same launch, the scan of per-tile union sizes -> [SPARSE_WRITE tile
+// and slow passes].
 #include "internal.h"
 
 #include <map>
@@ -1001,10 +1002,42 @@ __global__ void k_partition(const StreamDesc* tab, uint32_t* off, uint32_t P, ui
 // Nodes are reported in level order; only the first nfold nodes of level
 // 1 are reported (all of them for a power-of-two rank count: nfold = P/2),
 // the higher levels follow them.
-__global__ void __launch_bounds__(256) k_decide(const StreamDesc* tab, const uint32_t* node_cnt, uint32_t P,
-                                                uint64_t N, uint64_t thr, uint64_t* node_nnz,
-                                                uint8_t* node_dense, ReduceResult* hdr, uint32_t nfold,
-                                                ReduceResult* result)
+// Exclusive scan of the per-tile root union sizes by one 1024-thread
+// workgroup; also clears the deferred-tile counter for the write pass.
+__device__ void scan_tiles(const uint32_t* cnt, uint32_t* off, uint32_t n, uint32_t* slow_count)
+{
+    __shared__ uint32_t s_wsum[16];
+    const uint32_t tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    const uint32_t per = (n + 1023) / 1024;
+    const uint32_t lo = min(tid * per, n), hi = min(lo + per, n);
+    uint32_t acc = 0;
+    for (uint32_t i = lo; i < hi; ++i) acc += cnt[i];
+    uint32_t incl = acc;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const uint32_t y = __shfl_up(incl, o);
+        if (lane >= (uint32_t)o) incl += y;
+    }
+    if (lane == 63) s_wsum[wv] = incl;
+    __syncthreads();
+    uint32_t run = incl - acc;
+    for (uint32_t w = 0; w < wv; ++w) run += s_wsum[w];
+    for (uint32_t i = lo; i < hi; ++i) {
+        off[i] = run;
+        run += cnt[i];
+    }
+    if (tid == 0) *slow_count = 0u;
+}
+
+// The switch rule over the node sizes (threads 0-255), then, unless the root
+// is dense, the exclusive scan of the per-tile root union sizes that gives
+// the sparse write pass its output offsets (all 1024 threads; it also clears
+// the deferred-tile counter for that pass).  One workgroup.
+__global__ void __launch_bounds__(1024) k_decide_scan(const StreamDesc* tab, const uint32_t* node_cnt, uint32_t P,
+                                                      uint64_t N, uint64_t thr, uint64_t* node_nnz,
+                                                      uint8_t* node_dense, ReduceResult* hdr, uint32_t nfold,
+                                                      ReduceResult* result, const uint32_t* cnt, uint32_t* off,
+                                                      uint32_t n, uint32_t* slow_count)
 {
     // Stream sizes and node union sizes are read by all threads at once, the
     // rule is applied level by level in LDS, and all threads store.
@@ -1052,40 +1085,13 @@ __global__ void __launch_bounds__(256) k_decide(const StreamDesc* tab, const uin
         if (node_nnz) node_nnz[o] = s_nn[t];
         if (node_dense) node_dense[o] = s_nd[t];
     }
+    if (s_d[0]) return;  // the root is dense: no sparse output (whole workgroup)
+    scan_tiles(cnt, off, n, slow_count);
 }
 
 __global__ void k_set_result(ReduceResult* r, uint64_t nnz, uint32_t dense)
 {
     if (threadIdx.x == 0) *r = ReduceResult{nnz, dense, 0u};
-}
-
-// Exclusive scan of the per-tile root union sizes (one workgroup); also
-// clears the deferred-tile counter for the write pass.
-__global__ void __launch_bounds__(1024) k_scan_tiles(const uint32_t* cnt, uint32_t* off, uint32_t n,
-                                                     uint32_t* slow_count, const ReduceResult* skip)
-{
-    if (skip && skip->dense) return;  // the root is dense: no sparse output
-    __shared__ uint32_t s_wsum[16];
-    const uint32_t tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-    const uint32_t per = (n + 1023) / 1024;
-    const uint32_t lo = min(tid * per, n), hi = min(lo + per, n);
-    uint32_t acc = 0;
-    for (uint32_t i = lo; i < hi; ++i) acc += cnt[i];
-    uint32_t incl = acc;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-        const uint32_t y = __shfl_up(incl, o);
-        if (lane >= (uint32_t)o) incl += y;
-    }
-    if (lane == 63) s_wsum[wv] = incl;
-    __syncthreads();
-    uint32_t run = incl - acc;
-    for (uint32_t w = 0; w < wv; ++w) run += s_wsum[w];
-    for (uint32_t i = lo; i < hi; ++i) {
-        off[i] = run;
-        run += cnt[i];
-    }
-    if (tid == 0) *slow_count = 0u;
 }
 
 template <int PMAX, int MODE>
@@ -1268,19 +1274,16 @@ hipError_t reduce_run(const ReducePlan& p, const StreamDesc* host_tab, uint32_t*
     e = p.speculate_dense ? launch_pass<kDense>(a, p.PK, quant, s)
                           : launch_pass<kCount>(a, p.PK, quant, s);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_decide, dim3(1), dim3(256), 0, s, l.tab, l.node_cnt, p.P, p.N, p.thr,
-                       node_nnz, node_dense, l.hdr, nfold, dev_result);
+    // the switch rule, then (sparse root) the output offsets of the write pass
+    hipLaunchKernelGGL(k_decide_scan, dim3(1), dim3(1024), 0, s, l.tab, l.node_cnt, p.P, p.N, p.thr,
+                       node_nnz, node_dense, l.hdr, nfold, dev_result, l.tile_cnt, l.tile_off, p.ntiles,
+                       l.slow_count);
     if ((e = hipGetLastError()) != hipSuccess) return e;
+    // the sparse-output passes return at once on the device when the root is
+    // dense (the offsets are then not computed)
+    a.skip = l.hdr;
 
-    if (dev_result) {
-        // No host round trip: the sparse-output passes are always enqueued
-        // and return at once on the device when the root is dense.
-        a.skip = p.speculate_dense ? l.hdr : nullptr;
-        hipLaunchKernelGGL(k_scan_tiles, dim3(1), dim3(1024), 0, s, l.tile_cnt, l.tile_off, p.ntiles,
-                           l.slow_count, a.skip);
-        if ((e = hipGetLastError()) != hipSuccess) return e;
-        return launch_pass<kSparseWrite>(a, p.PK, quant, s);
-    }
+    if (dev_result) return launch_pass<kSparseWrite>(a, p.PK, quant, s);  // no host round trip
     if (p.speculate_dense) {
         if ((e = hipMemcpyAsync(res, l.hdr, sizeof(ReduceResult), hipMemcpyDeviceToHost, s)) !=
             hipSuccess)
@@ -1288,10 +1291,7 @@ hipError_t reduce_run(const ReducePlan& p, const StreamDesc* host_tab, uint32_t*
         if ((e = hipStreamSynchronize(s)) != hipSuccess) return e;
         if (res->dense) return hipSuccess;
     }
-    // Sparse root: positions from the per-tile union sizes, then write.
-    hipLaunchKernelGGL(k_scan_tiles, dim3(1), dim3(1024), 0, s, l.tile_cnt, l.tile_off, p.ntiles,
-                       l.slow_count, nullptr);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
+    // Sparse root: write at the offsets from the per-tile union sizes.
     if ((e = launch_pass<kSparseWrite>(a, p.PK, quant, s)) != hipSuccess) return e;
     if ((e = hipMemcpyAsync(res, l.hdr, sizeof(ReduceResult), hipMemcpyDeviceToHost, s)) !=
         hipSuccess)
