@@ -28,10 +28,11 @@ Besides the headline line the JSON carries:
   per_config    the other configurations (c1..c4; c3 = top-k then reduce,
                 with the top-k input elements per second), each timed
                 after at least 0.3 s of warm-up steps, and the split-phase
-                share of c4 and c5 (index range 0 of P equal ones, every
-                rank's stream restricted to it: one node's reduction in the
-                split-allgather allreduce), c4/p48: c4 with 48 ranks (App.
-                A's step in front), c3/bucketed: c3 with Alg. 1's
+                share of c4 and c5 (index range 0 of App. A's P-way
+                partition, every rank's stream restricted to it: one node's
+                reduction in the split-allgather allreduce), c4/p48: c4
+                with 48 ranks (App. A's step in front), c3/bucketed: c3
+                with Alg. 1's
                 error feedback and 4 of every 512 coordinates selected
                 (§8.4), and c5/dsar: one node's compute
                 in DSAR with the QSGD dense stage (its share reduced, the
@@ -169,9 +170,10 @@ class Workload:
     """Device-resident inputs, prepared calls and byte accounting of one config."""
 
     def __init__(self, name, cfg, seed, torch, dev, share=None, bucketed=None):
-        """``share`` = (s, S): the s-th of S equal index ranges of the
-        config's vector, each rank's stream restricted to it (one node's
-        work in the split phase of the large-data allreduce)."""
+        """``share`` = (s, S): the s-th of S index ranges of the config's
+        vector (App. A's partition: floor(N/S) indices each, the rest to the
+        last), each rank's stream restricted to it (one node's work in the
+        split phase of the large-data allreduce)."""
         from paper_1802_08021_amd import inputs
         from paper_1802_08021_amd import sparcml as S
         self.name, self.c = name, cfg
@@ -183,7 +185,7 @@ class Workload:
         self.R = c.N
         if share is not None:
             assert c.kind != "topk"
-            lo, hi = c.N * share[0] // share[1], c.N * (share[0] + 1) // share[1]
+            lo, hi = S.split_bounds(share[1], c.N)[share[0]: share[0] + 2]  # App. A's partition
             keep = [(a >= lo) & (a < hi) for a in d["idx"]]
             d = {"idx": [a[m] for a, m in zip(d["idx"], keep)], "val": [v[m] for v, m in zip(d["val"], keep)]}
             rng = {"lo": lo, "hi": hi}
@@ -281,7 +283,7 @@ class Workload:
 class DsarWorkload:
     """One node's compute in the split-allgather allreduce with QSGD on the
     dense stage (DSAR, §5.3.2 and §6), on c5's streams in fp32: the node's
-    share (index range 0 of P equal ones) reduced over the P ranks'
+    share (index range 0 of App. A's P-way partition) reduced over the P ranks'
     sub-streams, the dense share quantized in buckets, and the P gathered
     quantized shares decoded into the full vector.  The other nodes' shares
     (their own work) are prepared once, untimed."""
@@ -296,7 +298,8 @@ class DsarWorkload:
         log(f"{name}: generated inputs in {time.time() - t0:.1f}s")
         P, N = c.P, c.N
         self.bits, self.bucket = bits, bucket
-        b = [N * s // P for s in range(P + 1)]
+        b = S.split_bounds(P, N)  # App. A: floor(N/P) per node, the rest to the last
+        self.bounds = b
         _, idx = arena([a.view(np.int32) for a in d["idx"]], None, torch, dev)
         _, vals = arena(d["val"], None, torch, dev)
         # sub-stream of rank r for share s: a slice of the sorted stream

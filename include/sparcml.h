@@ -116,7 +116,7 @@ SPARCML_API int sparcml_workspace_size(int op, int P, uint64_t N, uint64_t max_n
  * Sparsification": each node keeps the k largest-magnitude components;
  * Alg. 1: eps = acc - TopK(acc)).
  *   P, N, k    x is P rows of N fp32 (row r at x + r*N), 1 <= N < 2^32,
- *              0 <= k <= N, P >= 1.
+ *              0 <= k <= N, 1 <= P <= 65535.
  *   out_idx    [P][k] uint32: the selected indices of row r, ascending.
  *   out_val    [P][k] fp32: x[r][out_idx[r][i]] (signed).
  *   residual   NULL, or [P][N] fp32 receiving x with the selected entries
@@ -124,8 +124,8 @@ SPARCML_API int sparcml_workspace_size(int op, int P, uint64_t N, uint64_t max_n
  *              which case only the k selected entries per row are written.
  * Ordering: magnitude = the IEEE bit pattern with the sign cleared; equal
  * magnitudes are taken lowest index first.
- * Errors: EINVAL (P < 1, N == 0 or >= 2^32, k > N, NULL x / outputs with
- * k > 0), EWORKSPACE, EHIP.
+ * Errors: EINVAL (P outside [1, 65535], N == 0 or >= 2^32, k > N, NULL x /
+ * outputs with k > 0), EWORKSPACE, EHIP.
  */
 SPARCML_API int sparcml_topk_sparsify(int P, const float* x, uint64_t N, uint64_t k,
                           uint32_t* out_idx, float* out_val, float* residual,
@@ -165,9 +165,11 @@ SPARCML_API uint64_t sparcml_topk_bucketed_count(uint64_t N, uint64_t bucket, ui
  * the stream's L2 norm (one bucket per stream); s = 2^(bits-1)-1 levels;
  * element v -> level l = floor(|v| s/scale) + [u < frac], u uniform in
  * [0,1), plus a sign bit; the dequantized value is +-l * (scale/s).
- *   P        number of streams (P >= 1).
+ *   P        number of streams, 1 <= P <= 65535.
  *   in       host array of P descriptors; in[r].val holds in[r].nnz fp32
- *            values (qbits must be 0; idx/is_dense are not read).
+ *            values, nnz <= 2^34 (the counter word j >> 2 below is 32 bits
+ *            wide; longer streams would repeat draws); qbits must be 0;
+ *            idx/is_dense are not read.
  *   bits     2, 4 or 8.
  *   seed     key of the Philox4x32-10 generator (Salmon et al., SC'11):
  *            element j of stream r uses word (j & 3) of the block at
@@ -339,6 +341,20 @@ SPARCML_API int sparcml_sparse_reduce_async(int P, const sparcml_stream* streams
 SPARCML_API int sparcml_concat(int P, const sparcml_stream* parts, const uint64_t* bounds, uint64_t N,
                    double delta, uint64_t bucket, sparcml_stream* out, void* ws, size_t ws_bytes,
                    void* stream);
+
+/*
+ * Index ranges of a P-way split of [0, N): which coordinates each node
+ * reduces in the split phase of the large-data allreduce (§5.3.2), with
+ * the rule App. A ("Relaxation of Assumption") gives for N not divisible by
+ * P: every node but the last is responsible for floor(N/P) indices, the
+ * last for the remaining N - (P-1) floor(N/P).  So bounds[s] = s * floor(N/P)
+ * for s < P and bounds[P] = N; node s covers [bounds[s], bounds[s+1]) (empty
+ * ranges when N < P).
+ *   P        1 <= P <= 65535.   N  1 <= N < 2^32.
+ *   bounds   host array of P + 1 uint64 (written).
+ * Host only: no device work.  Errors: EINVAL.
+ */
+SPARCML_API int sparcml_split_bounds(int P, uint64_t N, uint64_t* bounds);
 
 /*
  * Dense representation of one stream (§5.1): dense[j] = value of index j,

@@ -75,7 +75,7 @@ bool valid_bucket(uint64_t b) { return b >= 4 && b <= 8192 && (b & (b - 1)) == 0
 int quant_validate(int P, const sparcml_stream* in, int bits, uint8_t* const* out_q, float* out_scale,
                    std::vector<const float*>* vals, std::vector<uint64_t>* n, uint64_t* max_n)
 {
-    if (P < 1) return fail(SPARCML_EINVAL, "P must be >= 1");
+    if (P < 1 || P > 65535) return fail(SPARCML_EINVAL, "P must be in [1, 65535]");
     if (!valid_bits((uint32_t)bits)) return fail(SPARCML_EINVAL, "bits must be 2, 4 or 8");
     if (!in || !out_q || !out_scale) return fail(SPARCML_EINVAL, "NULL argument");
     vals->assign(P, nullptr);
@@ -83,7 +83,9 @@ int quant_validate(int P, const sparcml_stream* in, int bits, uint8_t* const* ou
     *max_n = 0;
     for (int r = 0; r < P; ++r) {
         if (in[r].qbits) return fail(SPARCML_EINVAL, "stream %d: input must hold fp32 values", r);
-        if (in[r].nnz >= (1ull << 40)) return fail(SPARCML_EINVAL, "stream %d: too long", r);
+        // the random draw of element j comes from counter word j >> 2 (32 bits)
+        if (in[r].nnz > (1ull << 34))
+            return fail(SPARCML_EINVAL, "stream %d: more than 2^34 entries (the Philox counter word is 32 bits)", r);
         if (in[r].nnz && (!in[r].val || !out_q[r])) return fail(SPARCML_EINVAL, "stream %d: NULL pointer", r);
         (*vals)[r] = in[r].val;
         (*n)[r] = in[r].nnz;
@@ -105,6 +107,16 @@ int tree_ranks(int P)
     int P2 = 1;
     while (2 * P2 <= P) P2 *= 2;
     return 2 * P2;
+}
+
+// Workspace of a reduce of P streams over N indices, enough for fp32 values
+// and for QSGD codes alike.
+size_t reduce_ws_any(int P, uint64_t N, uint64_t max_nnz, double delta)
+{
+    ReducePlan p0, pq;
+    reduce_plan(tree_ranks(P), N, max_nnz, (uint64_t)P * max_nnz, delta, 0, &p0);
+    reduce_plan(tree_ranks(P), N, max_nnz, (uint64_t)P * max_nnz, delta, 4, &pq);
+    return std::max(reduce_workspace(p0), reduce_workspace(pq));
 }
 
 uint64_t threshold(uint64_t N, double delta)
@@ -180,7 +192,9 @@ int reduce_impl(int P, const sparcml_stream* streams, uint64_t N, uint64_t lo, u
         if (!ws || ws_bytes < need) return fail(SPARCML_EWORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
 
         // tree slot of every rank; empty slots keep a readable scale pointer
-        std::vector<StreamDesc> tab(PT, StreamDesc{nullptr, nullptr, nullptr, streams[0].qscale, 0, 0});
+        // (a fixed array: the reduce path makes no host allocation)
+        StreamDesc tab[256];
+        for (int r = 0; r < PT; ++r) tab[r] = StreamDesc{nullptr, nullptr, nullptr, streams[0].qscale, 0, 0};
         const int P2 = PT == P ? P : PT / 2;
         for (int r = 0; r < P; ++r) {
             const int slot = PT == P ? r : (r < P2 ? 2 * r : 2 * (r - P2) + 1);
@@ -189,7 +203,7 @@ int reduce_impl(int P, const sparcml_stream* streams, uint64_t N, uint64_t lo, u
         }
         const uint32_t nfold = PT == P ? (uint32_t)(P / 2) : (uint32_t)(P - P2);
         ReduceResult res{};
-        e = reduce_run(plan, tab.data(), out->idx, out->val, node_nnz, node_dense, ws, s, &res, nfold, dres);
+        e = reduce_run(plan, tab, out->idx, out->val, node_nnz, node_dense, ws, s, &res, nfold, dres);
         if (e != hipSuccess) return hip_fail(e, "sparse_reduce");
         if (!dres) {
             out->nnz = res.nnz;
@@ -235,15 +249,15 @@ int sparcml_workspace_size(int op, int P, uint64_t N, uint64_t max_nnz, double d
     if (!bytes) return fail(SPARCML_EINVAL, "bytes is NULL");
     switch (op) {
     case SPARCML_OP_TOPK:
-        if (P < 1 || !valid_n(N) || max_nnz > N) return fail(SPARCML_EINVAL, "bad top-k sizes");
+        if (P < 1 || P > 65535 || !valid_n(N) || max_nnz > N) return fail(SPARCML_EINVAL, "bad top-k sizes");
         *bytes = max_nnz ? topk_workspace(P, N, max_nnz) : 0;
         return SPARCML_OK;
     case SPARCML_OP_QUANTIZE:
-        if (P < 1) return fail(SPARCML_EINVAL, "P must be >= 1");
+        if (P < 1 || P > 65535) return fail(SPARCML_EINVAL, "P must be in [1, 65535]");
         *bytes = quant_workspace(P, max_nnz);
         return SPARCML_OK;
     case SPARCML_OP_QUANTIZE_BUCKETED:
-        if (P < 1) return fail(SPARCML_EINVAL, "P must be >= 1");
+        if (P < 1 || P > 65535) return fail(SPARCML_EINVAL, "P must be in [1, 65535]");
         *bytes = quant_buckets_workspace(P);
         return SPARCML_OK;
     case SPARCML_OP_CONCAT:
@@ -253,11 +267,10 @@ int sparcml_workspace_size(int op, int P, uint64_t N, uint64_t max_nnz, double d
     case SPARCML_OP_REDUCE: {
         if (P < 1 || P > 256 || !valid_n(N) || !(delta > 0.0) || max_nnz > N)
             return fail(SPARCML_EINVAL, "bad reduce sizes");
-        ReducePlan p;
         // the call's sum of nnz is at most P * max_nnz, which never needs a
-        // smaller workspace than the call itself
-        reduce_plan(tree_ranks(P), N, max_nnz, (uint64_t)P * max_nnz, delta, 0, &p);
-        *bytes = P == 1 ? 0 : reduce_workspace(p);
+        // smaller workspace than the call itself; the plan of fp32 values and
+        // that of QSGD codes may differ (kernel occupancy), so the larger
+        *bytes = P == 1 ? 0 : reduce_ws_any(P, N, max_nnz, delta);
         return SPARCML_OK;
     }
     case SPARCML_OP_DENSIFY:
@@ -271,7 +284,7 @@ int sparcml_topk_sparsify(int P, const float* x, uint64_t N, uint64_t k, uint32_
                           float* out_val, float* residual, void* ws, size_t ws_bytes, void* stream)
 {
     try {
-        if (P < 1) return fail(SPARCML_EINVAL, "P must be >= 1");
+        if (P < 1 || P > 65535) return fail(SPARCML_EINVAL, "P must be in [1, 65535]");
         if (!valid_n(N)) return fail(SPARCML_EINVAL, "N must be in [1, 2^32)");
         if (k > N) return fail(SPARCML_EINVAL, "k > N");
         if (!x) return fail(SPARCML_EINVAL, "x is NULL");
@@ -435,6 +448,17 @@ int sparcml_sparse_reduce_async(int P, const sparcml_stream* streams, uint64_t N
     if (!out) return fail(SPARCML_EINVAL, "out is NULL");
     sparcml_stream o = *out;  // capacity and pointers only; never written
     return reduce_impl(P, streams, N, lo, hi, delta, &o, node_nnz, node_dense, ws, ws_bytes, stream, result);
+}
+
+int sparcml_split_bounds(int P, uint64_t N, uint64_t* bounds)
+{
+    if (P < 1 || P > 65535) return fail(SPARCML_EINVAL, "P must be in [1, 65535]");
+    if (!valid_n(N)) return fail(SPARCML_EINVAL, "N must be in [1, 2^32)");
+    if (!bounds) return fail(SPARCML_EINVAL, "bounds is NULL");
+    const uint64_t each = N / (uint64_t)P;  // App. A: floor(N/P) per node, the rest to the last
+    for (int s = 0; s < P; ++s) bounds[s] = (uint64_t)s * each;
+    bounds[P] = N;
+    return SPARCML_OK;
 }
 
 int sparcml_densify(const sparcml_stream* in, uint64_t N, float* dense, void* stream)

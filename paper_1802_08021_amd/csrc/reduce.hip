@@ -31,9 +31,7 @@
 // and slow passes].
 #include "internal.h"
 
-#include <map>
-#include <mutex>
-#include <tuple>
+#include <atomic>
 #include "qsgd_device.h"
 
 #include <algorithm>
@@ -1135,18 +1133,22 @@ int tiles_occupancy()
 // (size queries on a host with no GPU) a fixed 512.
 uint32_t resident_chunks(uint32_t pk, bool quant)
 {
-    static std::mutex mu;
-    static std::map<std::tuple<int, uint32_t, bool>, uint32_t> cache;
+    // per device, rank class and value kind; 0 = not queried yet (a race
+    // between threads only computes the same value twice)
+    constexpr int kCacheDevs = 64;
+    static std::atomic<uint32_t> cache[kCacheDevs][5][2];
     int dev = 0, cus = 0;
     if (hipGetDevice(&dev) != hipSuccess ||
         hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0) {
         (void)hipGetLastError();
         return 512u;
     }
-    std::lock_guard<std::mutex> g(mu);
-    const auto key = std::make_tuple(dev, pk, quant);
-    const auto it = cache.find(key);
-    if (it != cache.end()) return it->second;
+    const int cls = pk == 16 ? 0 : (pk == 32 ? 1 : (pk == 64 ? 2 : (pk == 128 ? 3 : 4)));
+    std::atomic<uint32_t>* slot = dev >= 0 && dev < kCacheDevs ? &cache[dev][cls][quant ? 1 : 0] : nullptr;
+    if (slot) {
+        const uint32_t v = slot->load(std::memory_order_relaxed);
+        if (v) return v;
+    }
     int occ = 0;
     switch (pk) {
     case 16: occ = quant ? tiles_occupancy<16, true>() : tiles_occupancy<16, false>(); break;
@@ -1160,7 +1162,7 @@ uint32_t resident_chunks(uint32_t pk, bool quant)
         occ = 1;
     }
     const uint32_t n = (uint32_t)occ * (uint32_t)cus;
-    cache[key] = n;
+    if (slot) slot->store(n, std::memory_order_relaxed);
     return n;
 }
 

@@ -78,6 +78,8 @@ def lib() -> ctypes.CDLL:
     L.sparcml_concat.argtypes = [i32, ctypes.POINTER(Stream), ctypes.POINTER(u64), u64, ctypes.c_double, u64,
                                  ctypes.POINTER(Stream), vp, ctypes.c_size_t, vp]
     L.sparcml_concat.restype = i32
+    L.sparcml_split_bounds.argtypes = [i32, u64, ctypes.POINTER(u64)]
+    L.sparcml_split_bounds.restype = i32
     L.sparcml_densify.argtypes = [ctypes.POINTER(Stream), u64, vp, vp]
     L.sparcml_densify.restype = i32
     L.sparcml_timing_enable.argtypes = [i32]
@@ -400,6 +402,14 @@ def concat(parts, bounds, N: int, delta: float, qbits: int = 0, bucket: int = 0)
     n, dense = c.run()
     return {"idx": None if dense else c.out_idx[:n], "val": c.out_val if dense else c.out_val[:n],
             "nnz": n, "dense": dense}
+
+
+def split_bounds(P: int, N: int):
+    """Bounds of the P index ranges of the split phase (App. A's rule:
+    floor(N/P) indices per node, the rest to the last).  List of P + 1."""
+    b = (ctypes.c_uint64 * (P + 1))()
+    _check(lib().sparcml_split_bounds(P, N, b), "sparcml_split_bounds")
+    return [int(v) for v in b]
 
 
 def densify(idx, val, N: int, codes=None, scale=None, qbits: int = 0):

@@ -24,7 +24,7 @@ def test_header_declares_the_boundary():
     for name in ("sparcml_topk_sparsify", "sparcml_quantize", "sparcml_sparse_reduce",
                  "sparcml_sparse_reduce_range", "sparcml_quantize_bucketed", "sparcml_concat",
                  "sparcml_topk_bucketed", "sparcml_topk_bucketed_count", "sparcml_sparse_reduce_async",
-                 "sparcml_densify", "sparcml_workspace_size", "sparcml_strerror",
+                 "sparcml_densify", "sparcml_split_bounds", "sparcml_workspace_size", "sparcml_strerror",
                  "sparcml_last_error"):
         assert name in syms
 
@@ -173,6 +173,10 @@ def test_topk_argument_errors():
     assert L.sparcml_topk_sparsify(1, FAKE, 10, 1, None, FAKE, None, FAKE, 1 << 30, None) == S.EINVAL
     assert L.sparcml_topk_sparsify(1, FAKE, 0, 0, FAKE, FAKE, None, FAKE, 1 << 30, None) == S.EINVAL
     assert L.sparcml_topk_sparsify(2, FAKE, 1000, 10, FAKE, FAKE, None, FAKE, 8, None) == S.EWORKSPACE
+    # one row per grid row: more than 65535 rows is refused before any launch
+    assert L.sparcml_topk_sparsify(65536, FAKE, 10, 1, FAKE, FAKE, None, FAKE, 1 << 40, None) == S.EINVAL
+    assert "65535" in S.last_error()
+    assert ws_size(S.OP_TOPK, 65536, 10, 1)[0] == S.EINVAL
 
 
 def test_topk_bucketed_argument_errors_and_count():
@@ -205,6 +209,45 @@ def test_quantize_argument_errors():
     assert L.sparcml_quantize(4, arr, 4, 1, ctypes.cast(q, ctypes.c_void_p), None, None, FAKE, 1 << 30, None) == S.EINVAL
     assert L.sparcml_quantize(4, streams(4, qbits=4), 4, 1, ctypes.cast(q, ctypes.c_void_p), FAKE, None, FAKE, 1 << 30, None) == S.EINVAL
     assert L.sparcml_quantize(4, arr, 4, 1, ctypes.cast(q, ctypes.c_void_p), FAKE, None, FAKE, 8, None) == S.EWORKSPACE
+    # more streams than grid rows
+    big = streams(65536)
+    qb = ctypes.cast((ctypes.c_void_p * 65536)(*([FAKE] * 65536)), ctypes.c_void_p)
+    assert L.sparcml_quantize(65536, big, 4, 1, qb, FAKE, None, FAKE, 1 << 40, None) == S.EINVAL
+    assert ws_size(S.OP_QUANTIZE, 65536, 1, 10)[0] == S.EINVAL
+
+
+def test_quantize_counter_limit():
+    """Element j of a stream draws from Philox counter word j >> 2, which is
+    32 bits wide: a stream of 2^34 entries uses every counter once, a longer
+    one would repeat draws and is refused on the host."""
+    L = S.lib()
+    q = ctypes.cast((ctypes.c_void_p * 2)(FAKE, FAKE), ctypes.c_void_p)
+    ok = streams(2, nnz=1 << 34)
+    bad = streams(2, nnz=(1 << 34) + 1)
+    # at the limit validation passes and only the (too small) workspace fails
+    assert L.sparcml_quantize(2, ok, 4, 1, q, FAKE, None, FAKE, 8, None) == S.EWORKSPACE
+    assert L.sparcml_quantize(2, bad, 4, 1, q, FAKE, None, FAKE, 1 << 40, None) == S.EINVAL
+    assert "2^34" in S.last_error()
+    assert L.sparcml_quantize_bucketed(2, bad, 4, 1024, 1, q, FAKE, None, FAKE, 1 << 40, None) == S.EINVAL
+    # the highest element of a maximal stream uses counter word 2^32 - 1
+    assert ((1 << 34) - 1) >> 2 == 2**32 - 1
+
+
+def test_split_bounds_follow_appendix_a():
+    """App. A: every node but the last gets floor(N/P) indices, the last the
+    remaining N - (P-1) floor(N/P)."""
+    for P, N in ((48, (1 << 20) + 12345), (128, 1 << 27), (7, 100), (5, 3), (1, 9), (65535, 2**32 - 1)):
+        b = S.split_bounds(P, N)
+        assert len(b) == P + 1 and b[0] == 0 and b[-1] == N
+        sizes = [b[s + 1] - b[s] for s in range(P)]
+        assert all(x == N // P for x in sizes[:-1])
+        assert sizes[-1] == N - (P - 1) * (N // P)
+    b = (ctypes.c_uint64 * 3)()
+    assert S.lib().sparcml_split_bounds(0, 10, b) == S.EINVAL
+    assert S.lib().sparcml_split_bounds(65536, 10, None) == S.EINVAL
+    assert S.lib().sparcml_split_bounds(2, 0, b) == S.EINVAL
+    assert S.lib().sparcml_split_bounds(2, 2**32, b) == S.EINVAL
+    assert S.lib().sparcml_split_bounds(2, 10, None) == S.EINVAL
 
 
 def test_quantize_bucketed_argument_errors():

@@ -207,3 +207,48 @@ def test_dsar_node_pipeline(bits):
     torch.cuda.synchronize()
     assert g["dense"] and o["dense"]
     assert_values(to_np(g["val"]), o["val"], "gathered DSAR result")
+
+
+@pytest.mark.parametrize("bits", [4])
+def test_dsar_pipeline_appendix_a_partition(bits):
+    """The DSAR node pipeline over App. A's partition with N not divisible
+    by P (N = 2^20 + 12345, P = 48: 47 ranges of floor(N/P) indices, the
+    last one 45 longer), and with every rank's share taken from the full
+    streams: share reduce, bucketed QSGD, decode of all shares."""
+    from paper_1802_08021_amd import sparcml as S
+    torch, dev = torch_dev()
+    rng = np.random.default_rng(440)
+    P, N, delta, B = 48, (1 << 20) + 12345, 0.05, 1024
+    b = S.split_bounds(P, N)
+    assert b[1] == N // P and b[-1] - b[-2] == N - (P - 1) * (N // P) and (N % P) != 0
+    idx = [inputs.uniform_subset(rng, N, 4000) for _ in range(P)]
+    val = [inputs.laplace(rng, 1e-3, 4000) for _ in range(P)]
+    hp, dp = [], []
+    for s in range(P):
+        lo, hi = b[s], b[s + 1]
+        cut = [np.searchsorted(a, (lo, hi)) for a in idx]
+        si = [a[x:y] for a, (x, y) in zip(idx, cut)]
+        sv = [v[x:y] for v, (x, y) in zip(val, cut)]
+        if s % 12 == 0:
+            say(f"[dsar] App. A partition P={P} N={N} share {s} [{lo}, {hi})")
+        o = oracle.sparse_reduce_range(si, sv, N, lo, hi, delta)
+        g = gpu_reduce(si, sv, N, delta, rng=(lo, hi))
+        assert g["dense"] == o["dense"]
+        assert_values(g["val"], o["val"], f"share {s}")
+        ov = o["val"] if o["dense"] else oracle.densify((o["idx"].astype(np.int64) - lo).astype(np.uint32),
+                                                          o["val"], hi - lo)
+        gv = g["val"] if g["dense"] else None
+        oq, osc, _ = oracle.quantize([ov], bits, seed=2000 + s, bucket=B)
+        if gv is None:
+            gv = to_np(S.densify(to_dev((g["idx"].astype(np.int64) - lo).astype(np.uint32)),
+                                 to_dev(g["val"]), hi - lo))
+        gq, gsc, _ = S.quantize_bucketed([to_dev(gv)], bits, B, 2000 + s)
+        np.testing.assert_array_equal(to_np(gq[0]), oq[0], err_msg=f"share {s} codes")
+        np.testing.assert_array_equal(to_np(gsc).view(np.uint32), osc.view(np.uint32))
+        hp.append({"idx": None, "codes": oq[0], "scales": osc, "qbits": bits, "bucket": B, "n": hi - lo})
+        dp.append({"idx": None, "codes": gq[0], "scales": gsc})
+    o = oracle.concat(hp, b, N, delta)
+    g = S.concat(dp, b, N, delta, qbits=bits, bucket=B)
+    torch.cuda.synchronize()
+    assert g["dense"] and o["dense"]
+    assert_values(to_np(g["val"]), o["val"], "gathered DSAR result, App. A partition")

@@ -30,11 +30,16 @@ def _workload(cfg, seed=0):
 
 
 def _gpu_result(call, torch):
-    """The reduce outputs of one timed step, plus per-node union sizes and
-    decisions from the same prepared inputs."""
+    """The reduce outputs of one timed step -- the call the benchmark times,
+    sparcml_sparse_reduce_async, with its device result header -- plus
+    per-node union sizes and decisions from the synchronous entry point on
+    the same prepared inputs (whose root must agree)."""
     from paper_1802_08021_amd import sparcml as S
-    nnz, dense = call.run()
+    call.run_async()
+    nnz, dense = call.result_header()
     torch.cuda.synchronize()
+    out_idx = None if dense else to_np(call.out_idx, np.uint32)[:nnz].copy()
+    out_val = to_np(call.out_val).copy() if dense else to_np(call.out_val)[:nnz].copy()
     idx, vals, codes, scales = call._keep
     node = S.ReduceCall(idx, call.N, call.delta, vals=vals, codes=codes, scales=scales,
                         qbits=0 if codes is None else call.arr[0].qbits, node_info=True)
@@ -44,8 +49,8 @@ def _gpu_result(call, torch):
     out = {
         "dense": dense,
         "nnz": nnz,
-        "idx": None if dense else to_np(call.out_idx, np.uint32)[:nnz].copy(),
-        "val": to_np(call.out_val).copy() if dense else to_np(call.out_val)[:nnz].copy(),
+        "idx": out_idx,
+        "val": out_val,
         "node_nnz": to_np(node.node_nnz).astype(np.uint64),
         "node_dense": to_np(node.node_dense),
     }
@@ -147,13 +152,13 @@ def test_c4_with_48_ranks_full_reduce():
     assert_reduce_equal(g, o, "c4/p48 full")
 
 
-@pytest.mark.timeout(900)
-def test_c5_dsar_full_step_sampled_shares():
+@pytest.mark.timeout(1200)
+def test_c5_dsar_full_step_all_shares():
     """One DSAR node step at c5's size (the c5/dsar benchmark step): the
-    gathered, decoded vector of 2^27 coordinates compared with the oracle's
-    pipeline (range reduce of the share, bucketed QSGD, decode) on the first,
-    a middle and the last of the 128 shares; the node's own share (0)
-    computed by the timed step itself."""
+    gathered, decoded vector of 2^27 coordinates compared, share by share,
+    with the oracle's pipeline (range reduce of the share, bucketed QSGD,
+    decode) for all 128 shares of App. A's partition; the node's own share
+    (0) is computed by the timed step itself."""
     import bench
     torch, dev = torch_dev()
     c = inputs.config(5)
@@ -163,13 +168,15 @@ def test_c5_dsar_full_step_sampled_shares():
     torch.cuda.synchronize()
     got = to_np(w.concat.out_val)
     d = inputs.generate(c, 0)
-    b = [c.N * s // c.P for s in range(c.P + 1)]
-    for sh in (0, c.P // 2, c.P - 1):
+    b = w.bounds
+    assert b[1] - b[0] == c.N // c.P and b[-1] == c.N
+    for sh in range(c.P):
         lo, hi = b[sh], b[sh + 1]
-        say(f"[full] c5/dsar: oracle share {sh} [{lo}, {hi})")
-        m = [(a >= lo) & (a < hi) for a in d["idx"]]
-        o = oracle.sparse_reduce_range([a[k] for a, k in zip(d["idx"], m)], [v[k] for v, k in zip(d["val"], m)],
-                                       c.N, lo, hi, c.delta)
+        if sh % 16 == 0:
+            say(f"[full] c5/dsar: oracle shares {sh}..{min(sh + 15, c.P - 1)}")
+        cut = [np.searchsorted(a, (lo, hi)) for a in d["idx"]]
+        o = oracle.sparse_reduce_range([a[x:y] for a, (x, y) in zip(d["idx"], cut)],
+                                       [v[x:y] for v, (x, y) in zip(d["val"], cut)], c.N, lo, hi, c.delta)
         assert o["dense"]
         q, sc, deq = oracle.quantize([o["val"]], w.bits, inputs.quant_seed(0, c.cfg) + sh, bucket=w.bucket)
         assert_values(got[lo:hi], deq[0], f"share {sh}")

@@ -118,6 +118,9 @@ def _kat_rows():
 
 
 def test_philox_known_answers():
+    """Regression fixture: rocRAND's answers for three fixed inputs (the
+    file's header gives their provenance; the rocRAND cross-check below is
+    the independent pin, this one needs no compiler)."""
     rows = _kat_rows()
     assert len(rows) == 3
     for ctr, key, out in rows:
@@ -869,3 +872,17 @@ def test_topk_by_threshold_matches_full_sort():
         i2, v2 = oracle.topk_by_threshold(x, k)
         np.testing.assert_array_equal(i1, i2)
         np.testing.assert_array_equal(v1.view(np.uint32), v2.view(np.uint32))
+
+
+def test_oracle_keeps_negative_zero_in_sparse_sums():
+    """Signed zeros (§5.1 sums in fp32): a sparse node keeps what IEEE
+    addition gives (a lone -0 stays -0, -0 + -0 = -0, -0 + +0 = +0); a dense
+    node starts from +0.0, so no dense value is -0.0."""
+    nz = np.float32(-0.0)
+    idx = [np.array([1, 2, 3], np.uint32), np.array([2, 3, 4], np.uint32)]
+    val = [np.array([nz, nz, nz], np.float32), np.array([nz, 0.0, nz], np.float32)]
+    o = oracle.sparse_reduce(idx, val, 16, 10.0)
+    assert not o["dense"]
+    assert o["val"].view(np.uint32).tolist() == [0x80000000, 0x80000000, 0, 0x80000000]
+    d = oracle.sparse_reduce(idx, val, 16, 1e-9)
+    assert d["dense"] and not np.signbit(d["val"]).any()
