@@ -66,7 +66,7 @@ def test_reduce_sparse_and_dense_roots(P):
 def test_reduce_counts_of_ranks_per_index():
     """-0.0 at indices held by exactly 1, 2, 3, 4, 5, 6 and 9 ranks of 16
     (the paths for two, three or four, five and more ranks)."""
-    P, N = 16, 9000
+    P, N = 16, 12000  # indices up to 279 * 37
     sets = [set() for _ in range(P)]
     vals = [dict() for _ in range(P)]
     j = 0
