@@ -19,6 +19,9 @@
  *                             allreduce (§5.3.2)
  *   sparcml_sparse_reduce_async -- either reduce without waiting (result
  *                             header written on the device)
+ *   sparcml_sparse_reduce_async_noalloc -- the same with the library's own
+ *                             fixed scratch array, for callers that cannot
+ *                             allocate
  *   sparcml_concat         -- gathered shares summed as a concatenation
  *                             (§5.1 case (2), §5.3.2), QSGD parts decoded
  *   sparcml_densify        -- dense representation of one stream (§5.1)
@@ -307,6 +310,31 @@ SPARCML_API int sparcml_sparse_reduce_async(int P, const sparcml_stream* streams
                                 uint64_t hi, double delta, const sparcml_stream* out,
                                 uint64_t* node_nnz, uint8_t* node_dense, sparcml_result* result,
                                 void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * sparcml_sparse_reduce_async for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid allocation): the same computation, arguments and outputs, without
+ * a workspace argument.  Its scratch memory is a fixed device array of
+ * SPARCML_NOALLOC_SCRATCH_BYTES inside the library, which each GPU the
+ * library runs on holds until the process ends; the call allocates nothing
+ * (no hipMalloc, no hipFree, no allocating library routine).
+ *   Limit: a reduce whose workspace (sparcml_workspace_size, OP_REDUCE)
+ *   exceeds SPARCML_NOALLOC_SCRATCH_BYTES is rejected with EWORKSPACE
+ *   before any device work (16 MiB covers, e.g., every P <= 256 at
+ *   N <= 2^31 and P >= 33 at any N < 2^32).
+ *   Sharing: every call on one GPU uses that GPU's one array, and the array
+ *   keeps the last call's contents (the call initializes what it reads).
+ *   Calls that overlap on one GPU (concurrent streams, threads or
+ *   processes) race on it; calls in one stream's order do not.
+ * Errors: as for sparcml_sparse_reduce_async, EWORKSPACE for sizes above the
+ * limit, EHIP if the array's address cannot be obtained.
+ */
+#define SPARCML_NOALLOC_SCRATCH_BYTES (16u << 20)
+SPARCML_API int sparcml_sparse_reduce_async_noalloc(int P, const sparcml_stream* streams, uint64_t N,
+                                        uint64_t lo, uint64_t hi, double delta,
+                                        const sparcml_stream* out, uint64_t* node_nnz,
+                                        uint8_t* node_dense, sparcml_result* result, void* stream);
 
 /*
  * The allgather phase of the split-allgather allreduce (§5.3.2), the local

@@ -11,6 +11,7 @@
 
 #include <algorithm>
 #include <exception>
+#include <mutex>
 #include <vector>
 
 static_assert(sizeof(sparcml_result) == sizeof(sparcml::ReduceResult) &&
@@ -130,9 +131,44 @@ uint64_t threshold(uint64_t N, double delta)
 // values (index lo + i at i), a sparse one absolute indices.  result ==
 // NULL: the root header is read back into *out; otherwise it is written to
 // result (device) and the call does not wait.
+// ------------------------------------------------------------------------
+// Scratch memory of sparcml_sparse_reduce_async_noalloc (for callers that
+// cannot allocate): a file-scope device array, which every GPU the library
+// runs on holds until the process ends.  In host code `scratch` names a
+// host-side stand-in, not device memory: host code only ever uses the
+// per-device address hipGetSymbolAddress returns for it.
+static __device__ __align__(256) uint8_t scratch[SPARCML_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kScratchDevs = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kScratchDevs];  // device address of `scratch`, per device
+
+// Address of the current device's `scratch`, looked up on the first call on
+// that device (with it current) and kept.
+int scratch_on_current_device(void** ptr)
+{
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    if (dev < 0 || dev >= kScratchDevs)
+        return fail(SPARCML_EINVAL, "device %d: the scratch table covers devices 0..%d", dev, kScratchDevs - 1);
+    std::lock_guard<std::mutex> g(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+        if (!p) return fail(SPARCML_EHIP, "hipGetSymbolAddress(scratch) returned NULL");
+        g_scratch_ptr[dev] = p;
+    }
+    *ptr = g_scratch_ptr[dev];
+    return SPARCML_OK;
+}
+
+// use_scratch: the workspace is the current device's `scratch` (ws and
+// ws_bytes are ignored); a call that needs more is rejected.
 int reduce_impl(int P, const sparcml_stream* streams, uint64_t N, uint64_t lo, uint64_t hi, double delta,
                 sparcml_stream* out, uint64_t* node_nnz, uint8_t* node_dense, void* ws, size_t ws_bytes,
-                void* stream, sparcml_result* result = nullptr)
+                void* stream, sparcml_result* result = nullptr, bool use_scratch = false)
 {
     try {
         uint32_t qbits;
@@ -189,6 +225,15 @@ int reduce_impl(int P, const sparcml_stream* streams, uint64_t N, uint64_t lo, u
         ReducePlan plan;
         reduce_plan(PT, R, max_nnz, sum_nnz, delta, (int)qbits, &plan, lo);
         const size_t need = reduce_workspace(plan);
+        if (use_scratch) {
+            if (need > (size_t)SPARCML_NOALLOC_SCRATCH_BYTES)
+                return fail(SPARCML_EWORKSPACE,
+                            "this reduce needs %zu bytes of scratch; the allocation-free entry point holds %zu",
+                            need, (size_t)SPARCML_NOALLOC_SCRATCH_BYTES);
+            rc = scratch_on_current_device(&ws);
+            if (rc) return rc;
+            ws_bytes = SPARCML_NOALLOC_SCRATCH_BYTES;
+        }
         if (!ws || ws_bytes < need) return fail(SPARCML_EWORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
 
         // tree slot of every rank; empty slots keep a readable scale pointer
@@ -448,6 +493,20 @@ int sparcml_sparse_reduce_async(int P, const sparcml_stream* streams, uint64_t N
     if (!out) return fail(SPARCML_EINVAL, "out is NULL");
     sparcml_stream o = *out;  // capacity and pointers only; never written
     return reduce_impl(P, streams, N, lo, hi, delta, &o, node_nnz, node_dense, ws, ws_bytes, stream, result);
+}
+
+int sparcml_sparse_reduce_async_noalloc(int P, const sparcml_stream* streams, uint64_t N, uint64_t lo,
+                                        uint64_t hi, double delta, const sparcml_stream* out,
+                                        uint64_t* node_nnz, uint8_t* node_dense, sparcml_result* result,
+                                        void* stream)
+{
+    if (!valid_n(N)) return fail(SPARCML_EINVAL, "N must be in [1, 2^32)");
+    if (!(lo < hi && hi <= N)) return fail(SPARCML_EINVAL, "need 0 <= lo < hi <= N");
+    if (!result) return fail(SPARCML_EINVAL, "result is NULL");
+    if (!out) return fail(SPARCML_EINVAL, "out is NULL");
+    sparcml_stream o = *out;  // capacity and pointers only; never written
+    return reduce_impl(P, streams, N, lo, hi, delta, &o, node_nnz, node_dense, nullptr, 0, stream, result,
+                       /*use_scratch=*/true);
 }
 
 int sparcml_split_bounds(int P, uint64_t N, uint64_t* bounds)

@@ -75,6 +75,9 @@ def lib() -> ctypes.CDLL:
     L.sparcml_sparse_reduce_async.argtypes = [i32, ctypes.POINTER(Stream), u64, u64, u64, ctypes.c_double,
                                               ctypes.POINTER(Stream), vp, vp, vp, vp, ctypes.c_size_t, vp]
     L.sparcml_sparse_reduce_async.restype = i32
+    L.sparcml_sparse_reduce_async_noalloc.argtypes = [i32, ctypes.POINTER(Stream), u64, u64, u64,
+                                                      ctypes.c_double, ctypes.POINTER(Stream), vp, vp, vp, vp]
+    L.sparcml_sparse_reduce_async_noalloc.restype = i32
     L.sparcml_concat.argtypes = [i32, ctypes.POINTER(Stream), ctypes.POINTER(u64), u64, ctypes.c_double, u64,
                                  ctypes.POINTER(Stream), vp, ctypes.c_size_t, vp]
     L.sparcml_concat.restype = i32
@@ -510,6 +513,19 @@ class ReduceCall:
             self.P, self.arr, self.N, lo, hi, self.delta, ctypes.byref(self.out), _ptr(self.node_nnz),
             _ptr(self.node_dense), _ptr(self.result), _ptr(self.ws), self.ws.numel(),
             _stream_ptr(self.dev)), "sparcml_sparse_reduce_async")
+
+    def run_async_noalloc(self):
+        """run_async through the allocation-free entry point (the library's
+        fixed scratch array instead of ``self.ws``)."""
+        if not hasattr(self, "result"):
+            torch = _torch()
+            self.result = torch.zeros(2, dtype=torch.int64, device=self.dev)
+        self.out.nnz = self.out_idx.numel()
+        lo, hi = self.rng if self.rng is not None else (0, self.N)
+        _check(lib().sparcml_sparse_reduce_async_noalloc(
+            self.P, self.arr, self.N, lo, hi, self.delta, ctypes.byref(self.out), _ptr(self.node_nnz),
+            _ptr(self.node_dense), _ptr(self.result), _stream_ptr(self.dev)),
+            "sparcml_sparse_reduce_async_noalloc")
 
     def result_header(self):
         """(nnz, dense) from ``self.result`` (synchronizes)."""
