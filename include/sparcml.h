@@ -25,6 +25,8 @@
  *   sparcml_concat         -- gathered shares summed as a concatenation
  *                             (§5.1 case (2), §5.3.2), QSGD parts decoded
  *   sparcml_densify        -- dense representation of one stream (§5.1)
+ *   sparcml_validate_streams -- input check: indices strictly ascending
+ *                             and in range (§5.1)
  *
  * Conventions shared by every call:
  *   - All data pointers are DEVICE pointers (HBM of the current HIP device),
@@ -75,6 +77,7 @@ extern "C" {
 #define SPARCML_OP_DENSIFY 4
 #define SPARCML_OP_QUANTIZE_BUCKETED 5
 #define SPARCML_OP_CONCAT 6
+#define SPARCML_OP_VALIDATE 7
 
 /*
  * Sparse stream (§5.1 "Vector Representations" and "Switching to a Dense
@@ -106,7 +109,8 @@ typedef struct sparcml_stream {
  *   P        number of ranks (streams / rows).
  *   N        dimension.
  *   max_nnz  TOPK: k; QUANTIZE: largest stream length; REDUCE: largest
- *            input stream nnz; DENSIFY, QUANTIZE_BUCKETED, CONCAT: ignored.
+ *            input stream nnz; DENSIFY, QUANTIZE_BUCKETED, CONCAT, VALIDATE:
+ *            ignored.
  *   delta    REDUCE only (switch threshold as a fraction of N).
  * A workspace sized with max_nnz >= the actual largest nnz is sufficient.
  * Returns SPARCML_OK and *bytes, or SPARCML_EINVAL.
@@ -241,7 +245,8 @@ SPARCML_API int sparcml_quantize_bucketed(int P, const sparcml_stream* in, int b
  *   P        1 <= P <= 256.
  *   streams  host array of P sparse descriptors (is_dense == 0) with the
  *            same qbits (0 = fp32 val, or 2/4/8 = QSGD codes dequantized on
- *            the fly).  Indices strictly ascending and < N (not checked).
+ *            the fly).  Indices strictly ascending and < N (not checked here:
+ *            sparcml_validate_streams checks them).
  *   N        1 <= N < 2^32.   delta > 0 (fraction of N).
  *   out      in: out->idx (capacity out->nnz entries, must be >=
  *            min(thr, sum of input nnz), or >= nnz_0 when P == 1 and the
@@ -369,6 +374,25 @@ SPARCML_API int sparcml_sparse_reduce_async_noalloc(int P, const sparcml_stream*
 SPARCML_API int sparcml_concat(int P, const sparcml_stream* parts, const uint64_t* bounds, uint64_t N,
                    double delta, uint64_t bucket, sparcml_stream* out, void* ws, size_t ws_bytes,
                    void* stream);
+
+/*
+ * Checks what the reduction assumes of its input streams and does not check
+ * itself (§5.1 "Vector Representations": a sparse vector is a list of
+ * index/value pairs; the merges need each list sorted): every sparse stream's
+ * indices strictly ascending (no duplicates) and inside [lo, hi) -- [0, N)
+ * for a whole vector.  A read-only pass over the indices.
+ *   P        1 <= P <= 65535.
+ *   streams  host array of P descriptors; only idx and nnz are read (idx
+ *            may be NULL when nnz == 0); dense descriptors are EINVAL.
+ *   lo, hi   lo < hi <= 2^32.
+ *   ws       sparcml_workspace_size(SPARCML_OP_VALIDATE, P, ...) bytes.
+ * Returns SPARCML_OK, or SPARCML_EUNSORTED with the first offending stream
+ * and position (lowest stream first) in sparcml_last_error().  Waits for
+ * its own work on `stream` (it reads back one 8-byte result).
+ * Errors: EINVAL, EWORKSPACE, EHIP.
+ */
+SPARCML_API int sparcml_validate_streams(int P, const sparcml_stream* streams, uint64_t lo, uint64_t hi,
+                             void* ws, size_t ws_bytes, void* stream);
 
 /*
  * Index ranges of a P-way split of [0, N): which coordinates each node

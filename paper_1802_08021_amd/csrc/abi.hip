@@ -321,6 +321,10 @@ int sparcml_workspace_size(int op, int P, uint64_t N, uint64_t max_nnz, double d
     case SPARCML_OP_DENSIFY:
         *bytes = 0;
         return SPARCML_OK;
+    case SPARCML_OP_VALIDATE:
+        if (P < 1 || P > 65535) return fail(SPARCML_EINVAL, "P must be in [1, 65535]");
+        *bytes = validate_workspace(P);
+        return SPARCML_OK;
     default: return fail(SPARCML_EINVAL, "unknown op %d", op);
     }
 }
@@ -507,6 +511,38 @@ int sparcml_sparse_reduce_async_noalloc(int P, const sparcml_stream* streams, ui
     sparcml_stream o = *out;  // capacity and pointers only; never written
     return reduce_impl(P, streams, N, lo, hi, delta, &o, node_nnz, node_dense, nullptr, 0, stream, result,
                        /*use_scratch=*/true);
+}
+
+int sparcml_validate_streams(int P, const sparcml_stream* streams, uint64_t lo, uint64_t hi, void* ws,
+                             size_t ws_bytes, void* stream)
+{
+    try {
+        if (P < 1 || P > 65535) return fail(SPARCML_EINVAL, "P must be in [1, 65535]");
+        if (!streams) return fail(SPARCML_EINVAL, "streams is NULL");
+        if (!(lo < hi && hi <= (1ull << 32))) return fail(SPARCML_EINVAL, "need lo < hi <= 2^32");
+        std::vector<const uint32_t*> idx(P);
+        std::vector<uint64_t> nnz(P);
+        for (int r = 0; r < P; ++r) {
+            if (streams[r].is_dense) return fail(SPARCML_EINVAL, "stream %d: a dense stream has no indices", r);
+            if (streams[r].nnz && !streams[r].idx) return fail(SPARCML_EINVAL, "stream %d: idx is NULL", r);
+            if (streams[r].nnz >= (1ull << 32)) return fail(SPARCML_EINVAL, "stream %d: nnz >= 2^32", r);
+            idx[r] = streams[r].idx;
+            nnz[r] = streams[r].nnz;
+        }
+        const size_t need = validate_workspace(P);
+        if (!ws || ws_bytes < need) return fail(SPARCML_EWORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
+        int bad_stream = -1;
+        uint64_t bad_pos = 0;
+        hipError_t e = validate_run(P, idx.data(), nnz.data(), lo, hi, ws, (hipStream_t)stream, &bad_stream, &bad_pos);
+        if (e != hipSuccess) return hip_fail(e, "validate");
+        if (bad_stream >= 0)
+            return fail(SPARCML_EUNSORTED,
+                        "stream %d, position %llu: index not strictly above its predecessor or outside [%llu, %llu)",
+                        bad_stream, (unsigned long long)bad_pos, (unsigned long long)lo, (unsigned long long)hi);
+        return SPARCML_OK;
+    } catch (const std::exception& ex) {
+        return fail(SPARCML_EHIP, "host exception: %s", ex.what());
+    }
 }
 
 int sparcml_split_bounds(int P, uint64_t N, uint64_t* bounds)

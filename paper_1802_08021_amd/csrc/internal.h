@@ -171,4 +171,11 @@ hipError_t quant_buckets_run(int P, const float* const* vals, const uint64_t* n,
                              uint32_t bucket, uint64_t seed, uint8_t* const* out_q, float* out_scale,
                              float* const* out_deq, void* ws, hipStream_t s);
 
+// ---------------------------------------------------------------- validate
+// Every stream's indices strictly ascending inside [lo, hi); *bad_stream =
+// -1 if so, else the first offending stream and position.  Synchronizes.
+size_t validate_workspace(int P);
+hipError_t validate_run(int P, const uint32_t* const* idx, const uint64_t* nnz, uint64_t lo, uint64_t hi,
+                        void* ws, hipStream_t s, int* bad_stream, uint64_t* bad_pos);
+
 }  // namespace sparcml

@@ -16,7 +16,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "_lib", "libsparcml.so")
 
 OK, EINVAL, ECAPACITY, EWORKSPACE, EUNSORTED, EHIP = 0, -1, -2, -3, -4, -5
-OP_TOPK, OP_QUANTIZE, OP_REDUCE, OP_DENSIFY, OP_QUANTIZE_BUCKETED, OP_CONCAT = 1, 2, 3, 4, 5, 6
+OP_TOPK, OP_QUANTIZE, OP_REDUCE, OP_DENSIFY, OP_QUANTIZE_BUCKETED, OP_CONCAT, OP_VALIDATE = 1, 2, 3, 4, 5, 6, 7
 
 
 class Stream(ctypes.Structure):
@@ -81,6 +81,8 @@ def lib() -> ctypes.CDLL:
     L.sparcml_concat.argtypes = [i32, ctypes.POINTER(Stream), ctypes.POINTER(u64), u64, ctypes.c_double, u64,
                                  ctypes.POINTER(Stream), vp, ctypes.c_size_t, vp]
     L.sparcml_concat.restype = i32
+    L.sparcml_validate_streams.argtypes = [i32, ctypes.POINTER(Stream), u64, u64, vp, ctypes.c_size_t, vp]
+    L.sparcml_validate_streams.restype = i32
     L.sparcml_split_bounds.argtypes = [i32, u64, ctypes.POINTER(u64)]
     L.sparcml_split_bounds.restype = i32
     L.sparcml_densify.argtypes = [ctypes.POINTER(Stream), u64, vp, vp]
@@ -405,6 +407,23 @@ def concat(parts, bounds, N: int, delta: float, qbits: int = 0, bucket: int = 0)
     n, dense = c.run()
     return {"idx": None if dense else c.out_idx[:n], "val": c.out_val if dense else c.out_val[:n],
             "nnz": n, "dense": dense}
+
+
+def validate_streams(idx, lo: int, hi: int):
+    """Check that every index tensor (device int32 holding uint32 indices)
+    ascends strictly inside [lo, hi).  Returns (True, "") or (False, the
+    library's message naming the first offending stream and position)."""
+    P = len(idx)
+    arr = (Stream * P)()
+    for r, t in enumerate(idx):
+        _require_cuda(t, f"idx[{r}]")
+        arr[r] = Stream(_ptr(t), None, None, None, t.numel(), 0, 0)
+    ws = alloc_workspace(workspace_size(OP_VALIDATE, P, 1, 0), idx[0].device)
+    rc = lib().sparcml_validate_streams(P, arr, lo, hi, _ptr(ws), ws.numel(), _stream_ptr(idx[0].device))
+    if rc == EUNSORTED:
+        return False, last_error()
+    _check(rc, "sparcml_validate_streams")
+    return True, ""
 
 
 def split_bounds(P: int, N: int):

@@ -24,7 +24,8 @@ def test_header_declares_the_boundary():
     for name in ("sparcml_topk_sparsify", "sparcml_quantize", "sparcml_sparse_reduce",
                  "sparcml_sparse_reduce_range", "sparcml_quantize_bucketed", "sparcml_concat",
                  "sparcml_topk_bucketed", "sparcml_topk_bucketed_count", "sparcml_sparse_reduce_async",
-                 "sparcml_densify", "sparcml_split_bounds", "sparcml_workspace_size", "sparcml_strerror",
+                 "sparcml_densify", "sparcml_split_bounds", "sparcml_validate_streams",
+                 "sparcml_workspace_size", "sparcml_strerror",
                  "sparcml_last_error"):
         assert name in syms
 
@@ -313,3 +314,21 @@ def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(S, "_lib", None)
     with pytest.raises(RuntimeError, match="no CPU fallback"):
         S.lib()
+
+
+def test_validate_argument_errors():
+    L = S.lib()
+    assert ws_size(S.OP_VALIDATE, 4, 1, 0)[0] == S.OK
+    assert ws_size(S.OP_VALIDATE, 0, 1, 0)[0] == S.EINVAL
+    assert ws_size(S.OP_VALIDATE, 65536, 1, 0)[0] == S.EINVAL
+
+    def rc(P=4, arr=None, lo=0, hi=100, ws=FAKE, nb=1 << 20):
+        return L.sparcml_validate_streams(P, streams(P) if arr is None else arr, lo, hi, ws, nb, None)
+    assert rc(P=0, arr=streams(1)) == S.EINVAL
+    assert L.sparcml_validate_streams(2, None, 0, 10, FAKE, 1 << 20, None) == S.EINVAL
+    assert rc(lo=10, hi=10) == S.EINVAL and rc(lo=0, hi=2**32 + 1) == S.EINVAL
+    assert rc(arr=streams(4, dense=1)) == S.EINVAL
+    nullidx = streams(4)
+    nullidx[3] = S.Stream(None, FAKE, None, None, 4, 0, 0)
+    assert rc(arr=nullidx) == S.EINVAL
+    assert rc(nb=8) == S.EWORKSPACE and rc(ws=None) == S.EWORKSPACE

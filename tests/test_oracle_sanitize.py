@@ -1,0 +1,28 @@
+"""The oracle built with the address and undefined-behaviour sanitizers
+(gcc -fsanitize=address,undefined, no recovery) and run by a driver that
+calls every oracle function on small random and edge-case inputs: no
+out-of-bounds access, leak or undefined operation in the oracle."""
+import os
+import shutil
+import subprocess
+import tempfile
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.mark.skipif(shutil.which("gcc") is None, reason="gcc not available")
+def test_oracle_under_sanitizers():
+    with tempfile.TemporaryDirectory() as d:
+        exe = os.path.join(d, "oracle_sanitize")
+        cmd = ["gcc", "-O1", "-g", "-std=c11", "-ffp-contract=off", "-fno-fast-math",
+               "-fsanitize=address,undefined", "-fno-sanitize-recover=all", "-fno-omit-frame-pointer",
+               "-I", os.path.join(ROOT, "oracle"), os.path.join(ROOT, "oracle", "oracle.c"),
+               os.path.join(ROOT, "tests", "oracle_sanitize_main.c"), "-o", exe, "-lm"]
+        subprocess.run(cmd, check=True, capture_output=True, text=True)
+        env = dict(os.environ, ASAN_OPTIONS="detect_leaks=1:abort_on_error=1:verify_asan_link_order=0",
+                   UBSAN_OPTIONS="halt_on_error=1:print_stacktrace=1")
+        r = subprocess.run([exe], capture_output=True, text=True, env=env, timeout=600)
+        assert r.returncode == 0, r.stdout + r.stderr
+        assert "ok" in r.stdout
