@@ -17,7 +17,11 @@ Besides the headline line the JSON carries:
                 traffic = measured HBM bytes per launch from rocprofv3
                 FETCH_SIZE/WRITE_SIZE runs (profiles/), or null when the
                 kernel source changed since they were taken;
-  cpu_baseline  the CPU oracle timed on the workload's input (one host core);
+  cpu_baseline  one step of the workload run by the CPU oracle on the same
+                host inputs: value on all usable host threads (the
+                oracle's independent items spread over them, same bits as
+                one thread), with the single-thread time beside it; every
+                per_config entry carries the same as cpu_oracle;
   cold_ms_per_step  the step with the 256 MB Infinity Cache evicted first
                 (median of 5);
   seeds         the step over seeds s..s+4 (fresh inputs): per-seed ms,
@@ -169,7 +173,7 @@ def empty_arena(sizes, dtype, torch, dev, align=256):
 class Workload:
     """Device-resident inputs, prepared calls and byte accounting of one config."""
 
-    def __init__(self, name, cfg, seed, torch, dev, share=None, bucketed=None):
+    def __init__(self, name, cfg, seed, torch, dev, share=None, bucketed=None, keep_host=False):
         """``share`` = (s, S): the s-th of S index ranges of the config's
         vector (App. A's partition: floor(N/S) indices each, the rest to the
         last), each rank's stream restricted to it (one node's work in the
@@ -177,10 +181,12 @@ class Workload:
         from paper_1802_08021_amd import inputs
         from paper_1802_08021_amd import sparcml as S
         self.name, self.c = name, cfg
+        self.seed, self.bucketed = seed, bucketed
         c = cfg
         t0 = time.time()
         d = inputs.generate(c, seed)
         log(f"{name}: generated inputs in {time.time() - t0:.1f}s")
+        self.d_host = d if keep_host else None  # for the CPU oracle leg
         rng = {}
         self.R = c.N
         if share is not None:
@@ -190,6 +196,8 @@ class Workload:
             d = {"idx": [a[m] for a, m in zip(d["idx"], keep)], "val": [v[m] for v, m in zip(d["val"], keep)]}
             rng = {"lo": lo, "hi": hi}
             self.R = hi - lo
+            if keep_host:
+                self.d_host = d
         self.groups = [S.TIMER_REDUCE_PASS, S.TIMER_REDUCE_SLOW, S.TIMER_REDUCE_WRITE]
         self.kernel_bytes = {}
         if c.kind == "topk" and bucketed:
@@ -251,7 +259,8 @@ class Workload:
                 self.in_bytes = self.nnz * 8
                 self.quant_bytes = 0
                 self._steps = [self.reduce.run_async]
-        self.d_host = d if cfg.cfg == 5 and share is None else None
+        self.rng = rng
+        d = None
 
     def step(self):
         """One step, enqueued without waiting; header() reads its root."""
@@ -288,7 +297,7 @@ class DsarWorkload:
     quantized shares decoded into the full vector.  The other nodes' shares
     (their own work) are prepared once, untimed."""
 
-    def __init__(self, name, cfg, seed, torch, dev, bits=4, bucket=1024):
+    def __init__(self, name, cfg, seed, torch, dev, bits=4, bucket=1024, keep_host=False):
         from paper_1802_08021_amd import inputs
         from paper_1802_08021_amd import sparcml as S
         self.name, self.c = name, cfg
@@ -340,7 +349,8 @@ class DsarWorkload:
             S.TIMER_CONCAT: N * bits // 8 + nsc * 4 + N * 4,
         }
         self.step_bytes = sum(self.kernel_bytes.values())
-        self.d_host = None
+        self.seed = seed
+        self.d_host = d if keep_host else None
         self._steps = [self.reduce.run_async, self.quant.run, self._gather]
         self._last = None
 
@@ -424,31 +434,132 @@ def traffic_for(kernel: str, workload: str):
     return t.get("bytes_per_launch")
 
 
-def cpu_baseline(d, c, seed, frac_log2=0):
-    """Oracle (quantize + reduce) on the coordinate slice [0, N/2^frac_log2)
-    of the same streams: same P, density, threshold fraction and tree (the
-    whole workload by default: several seconds on one host core)."""
+def oracle_threads() -> int:
+    """Threads for the oracle's parallel leg: the CPUs this process may run
+    on, capped by OMP_NUM_THREADS when that is set (the host share of one
+    GPU)."""
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:
+        n = os.cpu_count() or 1
+    omp = os.environ.get("OMP_NUM_THREADS", "")
+    if omp.isdigit() and int(omp) > 0:
+        n = min(n, int(omp))
+    return max(1, n)
+
+
+def _mean_seconds(fn, min_s):
+    """fn() repeated until min_s seconds have passed (at least once): mean."""
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        fn()
+        reps += 1
+        dt = time.perf_counter() - t0
+        if dt >= min_s:
+            return dt / reps
+
+
+def oracle_step_times(w, threads):
+    """One step of workload ``w`` run by the CPU oracle on the workload's own
+    host inputs, with the oracle's independent items (tree-level nodes,
+    top-k rows, quantized streams) on 1 and on ``threads`` threads; the
+    results are the same bits either way.  Where a single-thread step would
+    take minutes (top-k over 32 rows of 2^24) only some rows are selected and
+    the time is scaled to all P rows.  Returns (single_s, multi_s, sample)."""
     import oracle
     from paper_1802_08021_amd import inputs
-    Ns = c.N >> frac_log2
-    idx, val = [], []
-    for a, v in zip(d["idx"], d["val"]):
-        n = int(np.searchsorted(a, Ns))
-        idx.append(a[:n])
-        val.append(v[:n])
-    nnz = sum(a.size for a in idx)
-    t0 = time.perf_counter()
-    if c.qbits:
-        _, _, deq = oracle.quantize(val, c.qbits, inputs.quant_seed(seed, c.cfg))
-    else:
-        deq = val
-    oracle.sparse_reduce(idx, deq, Ns, c.delta)
-    dt = time.perf_counter() - t0
-    return {"value": nnz / dt, "unit": "nnz/s", "cores": 1, "kind": "oracle",
-            "sample": (f"{c.name} streams restricted to indices < N/{2**frac_log2} " if frac_log2 else
-                       f"the whole {c.name} input ") +
-                      f"({nnz} input nnz, N'={Ns}); quantize + reduce, single thread, {dt:.2f} s; "
-                      f"host {cpu_model()}, {os.cpu_count()} logical CPUs"}
+    c, d = w.c, w.d_host
+    if isinstance(w, DsarWorkload):
+        return _oracle_dsar(w, threads)
+    if c.kind == "topk":
+        x = d["x"]
+        P = x.shape[0]
+        if w.bucketed:
+            B, kb = w.bucketed
+
+            def select(rows):
+                return oracle.topk_bucketed(np.zeros_like(x[:rows]), x[:rows], 0.1, B, kb)[:2]
+        else:
+            def select(rows):
+                return oracle.topk(x[:rows], c.k)[:2]
+        one_rows = 1
+        with oracle.threads(threads):
+            t0 = time.perf_counter()
+            idx, val = select(P)
+            t_sel_multi = time.perf_counter() - t0
+        with oracle.threads(1):
+            t0 = time.perf_counter()
+            select(one_rows)
+            t_sel_one = (time.perf_counter() - t0) * P / one_rows
+        il, vl = [idx[r] for r in range(P)], [val[r] for r in range(P)]
+        times = []
+        for th in (1, threads):
+            with oracle.threads(th):
+                times.append(_mean_seconds(lambda: oracle.sparse_reduce(il, vl, c.N, c.delta), 0.2))
+        sample = (f"selection: all {P} rows on {threads} threads, {one_rows} row on one thread "
+                  f"(scaled by {P}); reduce: the whole input")
+        return t_sel_one + times[0], t_sel_multi + times[1], sample
+    idx, val = d["idx"], d["val"]
+    qseed = inputs.quant_seed(w.seed, c.cfg)
+    lo, hi = w.rng.get("lo"), w.rng.get("hi")
+
+    def step():
+        deq = oracle.quantize(val, c.qbits, qseed)[2] if c.qbits else val
+        if lo is None:
+            oracle.sparse_reduce(idx, deq, c.N, c.delta)
+        else:
+            oracle.sparse_reduce_range(idx, deq, c.N, lo, hi, c.delta)
+    times = []
+    for th in (1, threads):
+        with oracle.threads(th):
+            times.append(_mean_seconds(step, 0.2))
+    return times[0], times[1], "the whole input" + (", quantize + reduce" if c.qbits else "")
+
+
+def _oracle_dsar(w, threads):
+    """DSAR node step: share 0 reduced (fp32), quantized in buckets, and the
+    P quantized shares decoded into the full vector.  The other P - 1 shares
+    are stand-ins of the right sizes (random codes, unit scales): the decode
+    does the same work for any codes."""
+    import oracle
+    from paper_1802_08021_amd import inputs
+    c, d = w.c, w.d_host
+    b = w.bounds
+    P, N = c.P, c.N
+    lo, hi = b[0], b[1]
+    cut = [int(np.searchsorted(a, hi)) for a in d["idx"]]
+    si = [a[:n] for a, n in zip(d["idx"], cut)]
+    sv = [v[:n] for v, n in zip(d["val"], cut)]
+    rng = np.random.default_rng(7)
+    per = 8 // w.bits
+    others = []
+    for s in range(1, P):
+        R = b[s + 1] - b[s]
+        others.append({"idx": None, "qbits": w.bits, "bucket": w.bucket, "n": R,
+                       "codes": rng.integers(0, 256, size=(R + per - 1) // per, dtype=np.uint8),
+                       "scales": np.ones((R + w.bucket - 1) // w.bucket, np.float32)})
+    qseed = inputs.quant_seed(w.seed, c.cfg)
+
+    def step():
+        red = oracle.sparse_reduce_range(si, sv, N, lo, hi, c.delta)
+        q, sc, _ = oracle.quantize([red["val"]], w.bits, qseed, bucket=w.bucket)
+        mine = {"idx": None, "qbits": w.bits, "bucket": w.bucket, "n": hi - lo, "codes": q[0], "scales": sc}
+        oracle.concat([mine] + others, b, N, c.delta)
+    times = []
+    for th in (1, threads):
+        with oracle.threads(th):
+            times.append(_mean_seconds(step, 0.2))
+    return times[0], times[1], (f"share [0, {hi}) reduced and quantized; the other {P - 1} shares' codes "
+                                "random stand-ins of their sizes; the decode runs on one thread in both legs")
+
+
+def oracle_leg(w, threads):
+    """The CPU oracle's time for one step of ``w``, single-thread and on
+    ``threads`` threads, as step times and input rates."""
+    one, multi, sample = oracle_step_times(w, threads)
+    return {"kind": "oracle", "threads": threads, "ms_per_step": multi * 1e3,
+            "input_nnz_per_s": w.nnz / multi, "single_thread_ms_per_step": one * 1e3,
+            "single_thread_input_nnz_per_s": w.nnz / one, "sample": sample}
 
 
 def describe(c) -> str:
@@ -476,7 +587,7 @@ def main() -> int:
     dev = torch.device("cuda:0")
 
     head_cfg = inputs.config(int(args.workload[1]))
-    w = Workload(args.workload, head_cfg, args.seed, torch, dev)
+    w = Workload(args.workload, head_cfg, args.seed, torch, dev, keep_host=not args.no_cpu_baseline)
     ms, wall, kdur, root_nnz, dense = time_steps(w, args.steps, args.warmup, torch)
     log(f"{args.workload}: {ms:.3f} ms/step (wall {wall:.3f}), kernels {kdur}")
     value = w.nnz / (ms * 1e-3)
@@ -515,9 +626,18 @@ def main() -> int:
     cold_ms = time_cold(w, 5, torch)
     log(f"{args.workload}: cold (Infinity Cache evicted) {cold_ms:.3f} ms/step")
     cpu = None
-    if not args.no_cpu_baseline and w.d_host is not None:
-        log("timing the CPU oracle on a bounded sample")
-        cpu = cpu_baseline(w.d_host, head_cfg, args.seed)
+    threads = oracle_threads()
+    if not args.no_cpu_baseline:
+        log(f"timing the CPU oracle on the workload (1 and {threads} threads)")
+        leg = oracle_leg(w, threads)
+        cpu = {"value": leg["input_nnz_per_s"], "unit": "nnz/s", "cores": threads, "kind": "oracle",
+               "sample": f"{leg['sample']}; one step of {describe(head_cfg)}, "
+                         f"{leg['ms_per_step'] / 1e3:.2f} s on {threads} threads",
+               "single_thread": {"value": leg["single_thread_input_nnz_per_s"], "cores": 1,
+                                 "seconds": leg["single_thread_ms_per_step"] / 1e3},
+               "host": f"{cpu_model()}, {os.cpu_count()} logical CPUs, {threads} usable"}
+        log(f"oracle: {leg['ms_per_step']:.0f} ms on {threads} threads, "
+            f"{leg['single_thread_ms_per_step']:.0f} ms on one")
     w = None
     torch.cuda.empty_cache()
 
@@ -548,11 +668,12 @@ def main() -> int:
             if name.endswith("/p48"):  # a rank count that is not a power of two
                 c = dataclasses.replace(c, P=48)
             share = (0, c.P) if name.endswith("/share") else None
+            keep = not args.no_cpu_baseline
             if name.endswith("/dsar"):
-                pw = DsarWorkload(name, c, args.seed, torch, dev)
+                pw = DsarWorkload(name, c, args.seed, torch, dev, keep_host=keep)
             else:
                 pw = Workload(name, c, args.seed, torch, dev, share=share,
-                              bucketed=(512, 4) if name.endswith("/bucketed") else None)
+                              bucketed=(512, 4) if name.endswith("/bucketed") else None, keep_host=keep)
             pms, pwall, pk, pn, pd = time_steps(pw, max(5, args.steps // 2), 2, torch, warm_s=0.3)
             desc = describe(c) + (f"; split-phase share [{pw.reduce.rng[0]}, {pw.reduce.rng[1]}) "
                                   f"(1 of {c.P})" if share else "")
@@ -576,6 +697,11 @@ def main() -> int:
                 tk = sum(pk.get(g, 0.0) for g in (S.TIMER_TOPK_SELECT, S.TIMER_TOPK_WRITE,
                                                   S.TIMER_TOPK_BUCKETED))
                 per_config[name]["topk_input_elems_per_s"] = c.P * c.N / (tk * 1e-3) if tk else None
+            if keep:
+                leg = oracle_leg(pw, threads)
+                per_config[name]["cpu_oracle"] = leg
+                log(f"{name}: oracle {leg['ms_per_step']:.1f} ms on {threads} threads, "
+                    f"{leg['single_thread_ms_per_step']:.1f} ms on one")
             log(f"{name}: {pms:.3f} ms/step")
             pw = None
             torch.cuda.empty_cache()

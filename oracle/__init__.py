@@ -37,7 +37,7 @@ def build(force: bool = True) -> str:
     if not force and os.path.exists(LIB_PATH):
         return LIB_PATH
     tmp = LIB_PATH + ".tmp"
-    cmd = ["gcc", "-O2", "-std=c11", "-ffp-contract=off", "-fno-fast-math",
+    cmd = ["gcc", "-O2", "-std=c11", "-ffp-contract=off", "-fno-fast-math", "-pthread",
            "-fPIC", "-shared", "-o", tmp] + _SOURCES + ["-lm"]
     subprocess.run(cmd, check=True)
     os.replace(tmp, LIB_PATH)
@@ -57,6 +57,10 @@ def lib():
         vp = ctypes.c_void_p
         L.orc_philox4x32_10.argtypes = [u32p, u32p, u32p]
         L.orc_philox4x32_10.restype = None
+        L.orc_set_threads.argtypes = [ctypes.c_int]
+        L.orc_set_threads.restype = None
+        L.orc_get_threads.argtypes = []
+        L.orc_get_threads.restype = ctypes.c_int
         L.orc_sparse_reduce.argtypes = [
             ctypes.c_int, vp, vp, vp, ctypes.c_uint64, ctypes.c_double,
             vp, ctypes.c_uint64, vp, vp, vp, vp, vp]
@@ -100,6 +104,34 @@ def philox4x32_10(ctr, key):
     o = (ctypes.c_uint32 * 4)()
     lib().orc_philox4x32_10(c, k, o)
     return [int(v) for v in o]
+
+
+def set_threads(n: int) -> None:
+    """Threads for the independent items of a call (the nodes of one tree
+    level, the rows of top-k, the streams of quantization); results are the
+    same bits for any count.  Default 1."""
+    lib().orc_set_threads(int(n))
+
+
+def get_threads() -> int:
+    return int(lib().orc_get_threads())
+
+
+class threads:
+    """``with oracle.threads(n): ...`` -- n threads inside, the previous
+    count restored afterwards."""
+
+    def __init__(self, n: int):
+        self.n, self.prev = int(n), None
+
+    def __enter__(self):
+        self.prev = get_threads()
+        set_threads(self.n)
+        return self
+
+    def __exit__(self, *exc):
+        set_threads(self.prev)
+        return False
 
 
 def threshold(N: int, delta: float) -> int:

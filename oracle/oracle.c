@@ -8,13 +8,69 @@
  * (the value type of the sparse streams, §5.1 "Vector Representations");
  * the QSGD norm, which the paper leaves unspecified, is accumulated in fp64.
  *
- * Build: gcc -O2 -std=c11 -ffp-contract=off -fno-fast-math -shared -fPIC.
+ * Build: gcc -O2 -std=c11 -ffp-contract=off -fno-fast-math -pthread -shared -fPIC.
  */
 #include "oracle.h"
 
 #include <math.h>
+#include <pthread.h>
+#include <stdatomic.h>
 #include <stdlib.h>
 #include <string.h>
+
+/* ------------------------------------------------------------------------ */
+/* Work items that are independent by definition (the nodes of one level of
+ * the reduction tree, the ranks of top-k and quantization) may be spread
+ * over threads; each item reads only its own inputs and writes only its own
+ * outputs, so the results are the same bits for any thread count.  The
+ * default is one thread (a plain loop). */
+
+static int g_threads = 1;
+
+void orc_set_threads(int n) { g_threads = n < 1 ? 1 : (n > 256 ? 256 : n); }
+int orc_get_threads(void) { return g_threads; }
+
+typedef void (*orc_item_fn)(void* ctx, int i);
+
+typedef struct {
+    orc_item_fn fn;
+    void* ctx;
+    int n;
+    atomic_int next;
+} orc_pool;
+
+static void* pool_worker(void* arg)
+{
+    orc_pool* p = (orc_pool*)arg;
+    for (;;) {
+        int i = atomic_fetch_add(&p->next, 1);
+        if (i >= p->n) break;
+        p->fn(p->ctx, i);
+    }
+    return NULL;
+}
+
+/* fn(ctx, i) for i in [0, n): in order on the calling thread, or claimed one
+ * at a time by min(threads, n) threads (the caller is one of them). */
+static void for_each_item(int n, orc_item_fn fn, void* ctx)
+{
+    int t = g_threads < n ? g_threads : n;
+    if (t <= 1) {
+        for (int i = 0; i < n; ++i) fn(ctx, i);
+        return;
+    }
+    orc_pool p;
+    p.fn = fn;
+    p.ctx = ctx;
+    p.n = n;
+    atomic_init(&p.next, 0);
+    pthread_t th[256];
+    int started = 0;
+    for (int k = 1; k < t; ++k, ++started)
+        if (pthread_create(&th[started], NULL, pool_worker, &p) != 0) break;
+    pool_worker(&p); /* also finishes whatever a thread that failed to start would have taken */
+    for (int k = 0; k < started; ++k) pthread_join(th[k], NULL);
+}
 
 /* ------------------------------------------------------------------------ */
 /* Philox4x32-10 (Salmon et al., SC'11).  State: four 32-bit words; key: two.
@@ -150,6 +206,30 @@ static int sum_pair(const onode* L, const onode* R, uint64_t N, uint64_t thr, on
     return 0;
 }
 
+/* One level of the tree as independent items: item g sums node a = g and
+ * b = g + off (App. A's step in front, off = P2) or a = 2g, b = 2g + 1
+ * (recursive doubling, off = 0) into out[g]; its inputs are released once
+ * it succeeds. */
+typedef struct {
+    onode* in;
+    onode* out;
+    int* rc;
+    uint64_t N, thr;
+    int off;
+} pair_level;
+
+static void pair_item(void* ctx, int g)
+{
+    pair_level* lv = (pair_level*)ctx;
+    onode* a = lv->off ? &lv->in[g] : &lv->in[2 * g];
+    onode* b = lv->off ? &lv->in[g + lv->off] : &lv->in[2 * g + 1];
+    lv->rc[g] = sum_pair(a, b, lv->N, lv->thr, &lv->out[g]);
+    if (lv->rc[g] == 0) {
+        node_free(a);
+        node_free(b);
+    }
+}
+
 int orc_sparse_reduce(int P, const uint32_t* const* idx, const float* const* val,
                       const uint64_t* nnz, uint64_t N, double delta,
                       uint32_t* out_idx, uint64_t out_cap, float* out_val,
@@ -200,21 +280,30 @@ int orc_sparse_reduce(int P, const uint32_t* const* idx, const float* const* val
         int P2 = 1;
         while (2 * P2 <= P) P2 *= 2;
         const int rem = P - P2;
-        for (int i = 0; i < rem && rc == 0; ++i) {
-            onode f;
-            rc = sum_pair(&cur[i], &cur[P2 + i], N, thr, &f);
-            if (rc) break;
-            if (node_nnz) node_nnz[i] = f.nnz;
-            if (node_dense) node_dense[i] = (uint8_t)f.dense;
-            node_free(&cur[i]);
-            node_free(&cur[P2 + i]);
-            cur[i] = f;
+        onode* fold = (onode*)calloc((size_t)rem, sizeof(onode));
+        int* frc = (int*)calloc((size_t)rem, sizeof(int));
+        if (!fold || !frc) rc = -4;
+        if (rc == 0) {
+            pair_level lv = {cur, fold, frc, N, thr, P2};
+            for_each_item(rem, pair_item, &lv);
+            for (int i = 0; i < rem; ++i)
+                if (frc[i] && rc == 0) rc = frc[i];
         }
         if (rc) {
+            for (int i = 0; fold && i < rem; ++i) node_free(&fold[i]);
             for (int r = 0; r < P; ++r) node_free(&cur[r]);
+            free(fold);
+            free(frc);
             free(cur);
             return rc;
         }
+        for (int i = 0; i < rem; ++i) {
+            if (node_nnz) node_nnz[i] = fold[i].nnz;
+            if (node_dense) node_dense[i] = (uint8_t)fold[i].dense;
+            cur[i] = fold[i];
+        }
+        free(fold);
+        free(frc);
         width = P2;
         node_base = (uint64_t)rem;
     }
@@ -225,15 +314,22 @@ int orc_sparse_reduce(int P, const uint32_t* const* idx, const float* const* val
     while (width > 1) {
         int half = width / 2;
         onode* next = (onode*)calloc((size_t)half, sizeof(onode));
-        if (!next) { rc = -4; break; }
-        for (int g = 0; g < half && rc == 0; ++g) {
-            rc = sum_pair(&cur[2 * g], &cur[2 * g + 1], N, thr, &next[g]);
-            if (rc) break;
+        int* grc = (int*)calloc((size_t)half, sizeof(int));
+        if (!next || !grc) {
+            free(next);
+            free(grc);
+            rc = -4;
+            break;
+        }
+        /* the nodes of one level are independent of each other */
+        pair_level lv = {cur, next, grc, N, thr, 0};
+        for_each_item(half, pair_item, &lv);
+        for (int g = 0; g < half; ++g) {
+            if (grc[g] && rc == 0) rc = grc[g];
             if (node_nnz) node_nnz[node_base + g] = next[g].nnz;
             if (node_dense) node_dense[node_base + g] = (uint8_t)next[g].dense;
-            node_free(&cur[2 * g]);
-            node_free(&cur[2 * g + 1]);
         }
+        free(grc);
         if (rc) {
             for (int g = 0; g < half; ++g) node_free(&next[g]);
             free(next);
@@ -303,33 +399,115 @@ static int cmp_u32(const void* pa, const void* pb)
     return a < b ? -1 : (a > b ? 1 : 0);
 }
 
+typedef struct {
+    const float* x;
+    uint64_t N, k;
+    uint32_t* out_idx;
+    float* out_val;
+    float* residual;
+    int* rc;
+} topk_rows;
+
+/* Rank r's row: full sort by key, the first k taken, reported in index order. */
+static void topk_row(void* ctx, int r)
+{
+    topk_rows* t = (topk_rows*)ctx;
+    const uint64_t N = t->N, k = t->k;
+    okv* all = (okv*)malloc(N * sizeof(okv));
+    if (!all) {
+        t->rc[r] = -4;
+        return;
+    }
+    const float* row = t->x + (uint64_t)r * N;
+    for (uint64_t j = 0; j < N; ++j) {
+        all[j].key = mag_key(row[j]);
+        all[j].idx = (uint32_t)j;
+    }
+    qsort(all, N, sizeof(okv), cmp_key_desc_idx_asc);
+    uint32_t* sel = t->out_idx + (uint64_t)r * k;
+    for (uint64_t i = 0; i < k; ++i) sel[i] = all[i].idx;
+    qsort(sel, k, sizeof(uint32_t), cmp_u32);
+    float* v = t->out_val + (uint64_t)r * k;
+    for (uint64_t i = 0; i < k; ++i) v[i] = row[sel[i]];
+    if (t->residual) {
+        float* res = t->residual + (uint64_t)r * N;
+        if (res != row) memcpy(res, row, N * sizeof(float));
+        for (uint64_t i = 0; i < k; ++i) res[sel[i]] = 0.0f;
+    }
+    free(all);
+    t->rc[r] = 0;
+}
+
 int orc_topk(int P, const float* x, uint64_t N, uint64_t k,
              uint32_t* out_idx, float* out_val, float* residual)
 {
     if (P < 1 || N == 0 || N > 0xFFFFFFFFull || k > N || !x) return -1;
     if (k && (!out_idx || !out_val)) return -1;
-    okv* all = (okv*)malloc(N * sizeof(okv));
-    if (!all) return -4;
-    for (int r = 0; r < P; ++r) {
-        const float* row = x + (uint64_t)r * N;
-        for (uint64_t j = 0; j < N; ++j) {
-            all[j].key = mag_key(row[j]);
-            all[j].idx = (uint32_t)j;
-        }
-        qsort(all, N, sizeof(okv), cmp_key_desc_idx_asc);
-        uint32_t* sel = out_idx + (uint64_t)r * k;
-        for (uint64_t i = 0; i < k; ++i) sel[i] = all[i].idx;
-        qsort(sel, k, sizeof(uint32_t), cmp_u32);
-        float* v = out_val + (uint64_t)r * k;
-        for (uint64_t i = 0; i < k; ++i) v[i] = row[sel[i]];
-        if (residual) {
-            float* res = residual + (uint64_t)r * N;
-            if (res != row) memcpy(res, row, N * sizeof(float));
-            for (uint64_t i = 0; i < k; ++i) res[sel[i]] = 0.0f;
-        }
+    int* rc = (int*)calloc((size_t)P, sizeof(int));
+    if (!rc) return -4;
+    topk_rows t = {x, N, k, out_idx, out_val, residual, rc};
+    for_each_item(P, topk_row, &t); /* rows are independent */
+    int e = 0;
+    for (int r = 0; r < P; ++r)
+        if (rc[r] && e == 0) e = rc[r];
+    free(rc);
+    return e;
+}
+
+typedef struct {
+    const float* grad;
+    float* eps;
+    uint64_t N, bucket, kb, K;
+    float alpha;
+    uint32_t* out_idx;
+    float* out_val;
+    int* rc;
+} topkb_rows;
+
+/* Rank r's row, bucket by bucket in order. */
+static void topk_bucketed_row(void* ctx, int r)
+{
+    topkb_rows* t = (topkb_rows*)ctx;
+    const uint64_t N = t->N, bucket = t->bucket, kb = t->kb;
+    const uint64_t nb = (N + bucket - 1) / bucket;
+    okv* b = (okv*)malloc(bucket * sizeof(okv));
+    float* acc = (float*)malloc(bucket * sizeof(float));
+    if (!b || !acc) {
+        free(b);
+        free(acc);
+        t->rc[r] = -4;
+        return;
     }
-    free(all);
-    return 0;
+    float* e = t->eps + (uint64_t)r * N;
+    const float* g = t->grad ? t->grad + (uint64_t)r * N : NULL;
+    uint64_t o = (uint64_t)r * t->K;
+    for (uint64_t q = 0; q < nb; ++q) {
+        const uint64_t j0 = q * bucket;
+        const uint64_t len = N - j0 < bucket ? N - j0 : bucket;
+        /* Alg. 1: acc = eps + alpha * grad (fp32, two roundings) */
+        for (uint64_t j = 0; j < len; ++j) {
+            acc[j] = g ? e[j0 + j] + t->alpha * g[j0 + j] : e[j0 + j];
+            b[j].key = mag_key(acc[j]);
+            b[j].idx = (uint32_t)(j0 + j);
+        }
+        /* the bucket's kb largest magnitudes, lowest index on ties */
+        qsort(b, len, sizeof(okv), cmp_key_desc_idx_asc);
+        const uint64_t take = len < kb ? len : kb;
+        uint32_t sel[64];
+        for (uint64_t i = 0; i < take; ++i) sel[i] = b[i].idx;
+        qsort(sel, take, sizeof(uint32_t), cmp_u32);
+        /* eps = acc - TopK(acc): the selected entries leave, the rest stay */
+        for (uint64_t j = 0; j < len; ++j) e[j0 + j] = acc[j];
+        for (uint64_t i = 0; i < take; ++i) {
+            t->out_idx[o + i] = sel[i];
+            t->out_val[o + i] = acc[sel[i] - j0];
+            e[sel[i]] = 0.0f;
+        }
+        o += take;
+    }
+    free(b);
+    free(acc);
+    t->rc[r] = 0;
 }
 
 int orc_topk_bucketed(int P, const float* grad, float* eps, uint64_t N, float alpha,
@@ -340,45 +518,15 @@ int orc_topk_bucketed(int P, const float* grad, float* eps, uint64_t N, float al
     const uint64_t nb = (N + bucket - 1) / bucket;
     const uint64_t last = N - (nb - 1) * bucket;
     const uint64_t K = (nb - 1) * kb + (last < kb ? last : kb); /* entries per rank */
-    okv* b = (okv*)malloc(bucket * sizeof(okv));
-    float* acc = (float*)malloc(bucket * sizeof(float));
-    if (!b || !acc) {
-        free(b);
-        free(acc);
-        return -4;
-    }
-    for (int r = 0; r < P; ++r) {
-        float* e = eps + (uint64_t)r * N;
-        const float* g = grad ? grad + (uint64_t)r * N : NULL;
-        uint64_t o = (uint64_t)r * K;
-        for (uint64_t q = 0; q < nb; ++q) {
-            const uint64_t j0 = q * bucket;
-            const uint64_t len = N - j0 < bucket ? N - j0 : bucket;
-            /* Alg. 1: acc = eps + alpha * grad (fp32, two roundings) */
-            for (uint64_t j = 0; j < len; ++j) {
-                acc[j] = g ? e[j0 + j] + alpha * g[j0 + j] : e[j0 + j];
-                b[j].key = mag_key(acc[j]);
-                b[j].idx = (uint32_t)(j0 + j);
-            }
-            /* the bucket's kb largest magnitudes, lowest index on ties */
-            qsort(b, len, sizeof(okv), cmp_key_desc_idx_asc);
-            const uint64_t take = len < kb ? len : kb;
-            uint32_t sel[64];
-            for (uint64_t i = 0; i < take; ++i) sel[i] = b[i].idx;
-            qsort(sel, take, sizeof(uint32_t), cmp_u32);
-            /* eps = acc - TopK(acc): the selected entries leave, the rest stay */
-            for (uint64_t j = 0; j < len; ++j) e[j0 + j] = acc[j];
-            for (uint64_t i = 0; i < take; ++i) {
-                out_idx[o + i] = sel[i];
-                out_val[o + i] = acc[sel[i] - j0];
-                e[sel[i]] = 0.0f;
-            }
-            o += take;
-        }
-    }
-    free(b);
-    free(acc);
-    return 0;
+    int* rc = (int*)calloc((size_t)P, sizeof(int));
+    if (!rc) return -4;
+    topkb_rows t = {grad, eps, N, bucket, kb, K, alpha, out_idx, out_val, rc};
+    for_each_item(P, topk_bucketed_row, &t); /* rows are independent */
+    int e = 0;
+    for (int r = 0; r < P; ++r)
+        if (rc[r] && e == 0) e = rc[r];
+    free(rc);
+    return e;
 }
 
 /* ------------------------------------------------------------------------ */
@@ -438,35 +586,76 @@ static void quantize_span(const float* v, uint64_t j0, uint64_t n, int r, int bi
     }
 }
 
+typedef struct {
+    const float* const* val;
+    const uint64_t* nnz;
+    int bits;
+    uint64_t bucket;
+    uint32_t key[2];
+    uint8_t* const* out_q;
+    float* out_scale;
+    float* const* out_deq;
+    const uint64_t* first_scale; /* per stream: index of its first scale */
+    int* rc;
+} quant_streams;
+
+/* Stream r: its buckets in order, each with its own L2 scale. */
+static void quantize_stream(void* ctx, int r)
+{
+    quant_streams* t = (quant_streams*)ctx;
+    const int bits = t->bits;
+    const int per_byte = 8 / bits;
+    const uint64_t n = t->nnz[r];
+    const float* v = t->val[r];
+    uint8_t* q = t->out_q[r];
+    const uint64_t nbytes = (n + per_byte - 1) / per_byte;
+    if (nbytes) memset(q, 0, nbytes);
+    float* deq = t->out_deq ? t->out_deq[r] : NULL;
+    const uint64_t B = t->bucket ? t->bucket : (n ? n : 1);
+    const uint64_t nb = t->bucket ? (n + B - 1) / B : 1;
+    for (uint64_t b = 0; b < nb; ++b) {
+        const uint64_t j0 = b * B;
+        const uint64_t len = n - j0 < B ? n - j0 : B;
+        float scale;
+        if (l2_scale(v + j0, len, &scale)) {
+            t->rc[r] = -4;
+            return;
+        }
+        t->out_scale[t->first_scale[r] + b] = scale;
+        quantize_span(v + j0, j0, len, r, bits, t->key, scale, q, deq);
+    }
+    t->rc[r] = 0;
+}
+
 int orc_quantize_bucketed(int P, const float* const* val, const uint64_t* nnz, int bits,
                           uint64_t bucket, uint64_t seed, uint8_t* const* out_q,
                           float* out_scale, float* const* out_deq)
 {
     if (P < 1 || !valid_bits(bits) || !val || !nnz || !out_q || !out_scale) return -1;
-    const int per_byte = 8 / bits;
-    const uint32_t key[2] = {(uint32_t)(seed & 0xFFFFFFFFu), (uint32_t)(seed >> 32)};
-    uint64_t so = 0; /* first scale of stream r */
-    for (int r = 0; r < P; ++r) {
-        const uint64_t n = nnz[r];
-        const float* v = val[r];
-        uint8_t* q = out_q[r];
-        if (n && (!v || !q)) return -1;
-        const uint64_t nbytes = (n + per_byte - 1) / per_byte;
-        if (nbytes) memset(q, 0, nbytes);
-        float* deq = out_deq ? out_deq[r] : NULL;
-        const uint64_t B = bucket ? bucket : (n ? n : 1);
-        const uint64_t nb = bucket ? (n + B - 1) / B : 1;
-        for (uint64_t b = 0; b < nb; ++b) {
-            const uint64_t j0 = b * B;
-            const uint64_t len = n - j0 < B ? n - j0 : B;
-            float scale;
-            if (l2_scale(v + j0, len, &scale)) return -4;
-            out_scale[so + b] = scale;
-            quantize_span(v + j0, j0, len, r, bits, key, scale, q, deq);
-        }
-        so += nb;
+    for (int r = 0; r < P; ++r)
+        if (nnz[r] && (!val[r] || !out_q[r])) return -1;
+    uint64_t* first = (uint64_t*)malloc((size_t)P * sizeof(uint64_t));
+    int* rc = (int*)calloc((size_t)P, sizeof(int));
+    if (!first || !rc) {
+        free(first);
+        free(rc);
+        return -4;
     }
-    return 0;
+    uint64_t so = 0; /* stream r's scales follow those of streams 0..r-1 */
+    for (int r = 0; r < P; ++r) {
+        first[r] = so;
+        so += bucket ? (nnz[r] + bucket - 1) / bucket : 1;
+    }
+    quant_streams t = {val, nnz, bits, bucket,
+                       {(uint32_t)(seed & 0xFFFFFFFFu), (uint32_t)(seed >> 32)},
+                       out_q, out_scale, out_deq, first, rc};
+    for_each_item(P, quantize_stream, &t); /* streams are independent */
+    int e = 0;
+    for (int r = 0; r < P; ++r)
+        if (rc[r] && e == 0) e = rc[r];
+    free(first);
+    free(rc);
+    return e;
 }
 
 int orc_quantize(int P, const float* const* val, const uint64_t* nnz, int bits,

@@ -1,7 +1,7 @@
 /*
  * SparCML reference oracle -- TEST INFRASTRUCTURE ONLY.
  *
- * Plain, sequential, obviously-correct CPU implementation of what the
+ * Plain, obviously-correct CPU implementation of what the
  * SparCML hot path computes (Renggli et al., "SparCML: High-Performance
  * Sparse Communication for Machine Learning", arXiv 1802.08021).  Only the
  * test-suite, the smoke check and the CPU-baseline leg of the benchmark may
@@ -21,6 +21,15 @@ extern "C" {
 /* Philox4x32 with 10 rounds (Salmon, Moraes, Dror, Shaw, SC'11, "Parallel
  * random numbers: as easy as 1, 2, 3"): one block cipher evaluation. */
 void orc_philox4x32_10(const uint32_t ctr[4], const uint32_t key[2], uint32_t out[4]);
+
+/* Threads for work items that are independent by definition: the nodes of
+ * one level of the reduction tree (and of App. A's step in front), the rows
+ * of top-k, the streams of quantization.  Each item reads only its own
+ * inputs and writes only its own outputs, so every result is the same bits
+ * for any count.  Default 1 (plain loops); clamped to [1, 256].  Process-
+ * wide; set it before, not during, calls from several threads. */
+void orc_set_threads(int n);
+int orc_get_threads(void);
 
 /* Sparse allreduce of P sparse streams in recursive-doubling order with the
  * sparse->dense switch (SparCML §5.1 "Switching to a Dense Format" and

@@ -3,7 +3,7 @@
  * inputs; built with the address and undefined-behaviour sanitizers by
  * tests/test_oracle_sanitize.py (so any out-of-bounds access, leak or
  * undefined operation in the oracle aborts the run).  Exit 0 when all calls
- * return as expected.
+ * return as expected.  Argument: the oracle's thread count (default 1).
  */
 #include <stdint.h>
 #include <stdio.h>
@@ -39,8 +39,10 @@ static uint64_t subset(uint32_t* out, uint64_t N, uint64_t k)
         }                                                               \
     } while (0)
 
-int main(void)
+int main(int argc, char** argv)
 {
+    /* optional argument: the oracle's thread count for every call */
+    if (argc > 1) orc_set_threads(atoi(argv[1]));
     for (int it = 0; it < 200; ++it) {
         const int P = 1 + (int)(rnd() % 19);
         const uint64_t N = 1 + rnd() % 300;
