@@ -22,6 +22,9 @@ Besides the headline line the JSON carries:
                 oracle's independent items spread over them, same bits as
                 one thread), with the single-thread time beside it; every
                 per_config entry carries the same as cpu_oracle;
+  ms_per_step   the K timed steps, during which the library records HIP
+                events around its kernels (the durations the roofline uses);
+  ms_per_step_no_events  the same K steps just before, without those events;
   cold_ms_per_step  the step with the 256 MB Infinity Cache evicted first
                 (median of 5);
   seeds         the step over seeds s..s+4 (fresh inputs): per-seed ms,
@@ -29,7 +32,11 @@ Besides the headline line the JSON carries:
   copy_ceiling  a plain 1 GiB device copy's bandwidth, the streaming ceiling;
   parts         the producer (QSGD or top-k) and the reduce apart: summed
                 kernel time and input rate of each;
-  per_config    the other configurations (c1..c4; c3 = top-k then reduce,
+  per_config    the other configurations, each with ms_per_step from steps
+                without the library's kernel events (at tens of microseconds
+                per step their records are a visible share) and
+                ms_per_step_with_kernel_events from the steps whose kernel
+                durations are reported (c1..c4; c3 = top-k then reduce,
                 with the top-k input elements per second), each timed
                 after at least 0.3 s of warm-up steps, and the split-phase
                 share of c4 and c5 (index range 0 of App. A's P-way
@@ -198,7 +205,7 @@ class Workload:
             self.R = hi - lo
             if keep_host:
                 self.d_host = d
-        self.groups = [S.TIMER_REDUCE_PASS, S.TIMER_REDUCE_SLOW, S.TIMER_REDUCE_WRITE]
+        self.groups = [S.TIMER_REDUCE_PASS, S.TIMER_REDUCE_SLOW, S.TIMER_REDUCE_WRITE, S.TIMER_REDUCE_MERGE]
         self.kernel_bytes = {}
         if c.kind == "topk" and bucketed:
             # Alg. 1 with §8.4's selection: acc = eps + alpha * grad, kb of
@@ -283,6 +290,8 @@ class Workload:
         self.kernel_bytes[S.TIMER_REDUCE_PASS] = red_in + (self.R * 4 if dense else 0)
         if not dense:
             self.kernel_bytes[S.TIMER_REDUCE_WRITE] = red_in + out_bytes
+        # small-data path: the streams read once, the root written once
+        self.kernel_bytes[S.TIMER_REDUCE_MERGE] = red_in + out_bytes
         if c.kind == "topk":
             self.step_bytes = self.topk_step_bytes + red_in + out_bytes
         else:
@@ -380,8 +389,18 @@ def time_steps(w, K, W, torch, warm_s=0.0):
         if done % 8 == 0:
             torch.cuda.synchronize()
     torch.cuda.synchronize()
-    # kernel durations: the library's events around every launch of the
-    # timed steps, read once afterwards
+    # the same K steps without the library's kernel events (their records
+    # are extra packets on the stream, visible at microsecond step times)
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(K):
+        w.step()
+    end.record()
+    torch.cuda.synchronize()
+    ms_plain = start.elapsed_time(end) / K
+    # the timed steps: kernel durations from the library's events around
+    # every launch of these steps, read once afterwards
     S.timing_enable(True)
     start = torch.cuda.Event(enable_timing=True)
     end = torch.cuda.Event(enable_timing=True)
@@ -398,12 +417,13 @@ def time_steps(w, K, W, torch, warm_s=0.0):
     ms = start.elapsed_time(end) / K
     nnz, dense = w.header()
     w.finish_bytes(nnz, dense)
+    w.ms_plain = ms_plain
     return ms, wall, {g: v for g, v in durs.items() if v is not None}, nnz, dense
 
 
 GROUP_NAMES = {0: "reduce_tiles", 1: "reduce_write", 2: "reduce_slow", 3: "qsgd_norm",
                4: "qsgd_codes", 5: "topk_select", 6: "topk_write", 7: "densify", 8: "concat",
-               9: "topk_bucketed"}
+               9: "topk_bucketed", 10: "reduce_merge"}
 
 
 def source_hash() -> str:
@@ -589,6 +609,7 @@ def main() -> int:
     head_cfg = inputs.config(int(args.workload[1]))
     w = Workload(args.workload, head_cfg, args.seed, torch, dev, keep_host=not args.no_cpu_baseline)
     ms, wall, kdur, root_nnz, dense = time_steps(w, args.steps, args.warmup, torch)
+    w_ms_plain = w.ms_plain
     log(f"{args.workload}: {ms:.3f} ms/step (wall {wall:.3f}), kernels {kdur}")
     value = w.nnz / (ms * 1e-3)
     step_gbs = w.step_bytes / (ms * 1e-3) / 1e9
@@ -617,7 +638,7 @@ def main() -> int:
     def group_ms(gs):
         return sum(kdur.get(g, 0.0) for g in gs)
     prod = [S.TIMER_QUANT_NORM, S.TIMER_QUANT_CODES, S.TIMER_TOPK_SELECT, S.TIMER_TOPK_WRITE]
-    red = [S.TIMER_REDUCE_PASS, S.TIMER_REDUCE_SLOW, S.TIMER_REDUCE_WRITE]
+    red = [S.TIMER_REDUCE_PASS, S.TIMER_REDUCE_SLOW, S.TIMER_REDUCE_WRITE, S.TIMER_REDUCE_MERGE]
     parts = {"reduce": {"kernel_ms": group_ms(red), "input_nnz_per_s": w.nnz / (group_ms(red) * 1e-3)}}
     if group_ms(prod):
         pn = w.nnz if head_cfg.qbits else head_cfg.P * head_cfg.N
@@ -685,10 +706,11 @@ def main() -> int:
                         f"share [0, {pw.R}) reduced, QSGD {pw.bits}-bit in buckets of {pw.bucket}, "
                         f"{c.P} quantized shares decoded into N")
             per_config[name] = {
-                "workload": desc, "ms_per_step": pms, "input_nnz_per_s": pw.nnz / (pms * 1e-3),
+                "workload": desc, "ms_per_step": pw.ms_plain, "input_nnz_per_s": pw.nnz / (pw.ms_plain * 1e-3),
+                "ms_per_step_with_kernel_events": pms,
                 "cold_ms_per_step": time_cold(pw, 3, torch),
-                "step_GB/s": pw.step_bytes / (pms * 1e-3) / 1e9,
-                "step_frac_of_hbm_peak": pw.step_bytes / (pms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                "step_GB/s": pw.step_bytes / (pw.ms_plain * 1e-3) / 1e9,
+                "step_frac_of_hbm_peak": pw.step_bytes / (pw.ms_plain * 1e-3) / 1e9 / HBM_PEAK_GBS,
                 "root_nnz": pn, "root_dense": pd,
                 "kernels": {GROUP_NAMES[g]: {"avg_ms": v, "GB/s": (pw.kernel_bytes[g] / (v * 1e-3) / 1e9)
                                              if pw.kernel_bytes.get(g) else None} for g, v in pk.items()},
@@ -702,7 +724,7 @@ def main() -> int:
                 per_config[name]["cpu_oracle"] = leg
                 log(f"{name}: oracle {leg['ms_per_step']:.1f} ms on {threads} threads, "
                     f"{leg['single_thread_ms_per_step']:.1f} ms on one")
-            log(f"{name}: {pms:.3f} ms/step")
+            log(f"{name}: {pw.ms_plain:.3f} ms/step ({pms:.3f} with kernel events)")
             pw = None
             torch.cuda.empty_cache()
 
@@ -714,6 +736,7 @@ def main() -> int:
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": ms,
+        "ms_per_step_no_events": w_ms_plain,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,

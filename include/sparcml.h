@@ -439,6 +439,7 @@ SPARCML_API int sparcml_densify(const sparcml_stream* in, uint64_t N, float* den
 #define SPARCML_TIMER_DENSIFY 7
 #define SPARCML_TIMER_CONCAT 8
 #define SPARCML_TIMER_TOPK_BUCKETED 9
+#define SPARCML_TIMER_REDUCE_MERGE 10 /* small-data reduce: the whole merge tree in one workgroup */
 SPARCML_API int sparcml_timing_enable(int on);
 SPARCML_API int sparcml_timing_read(int group, float* ms);
 

@@ -38,7 +38,8 @@ enum TimerSlot {
     kTDensify = 7,
     kTConcat = 8,       // concatenation of disjoint parts
     kTTopkBuckets = 9,  // bucketed top-k with error feedback
-    kTSlots = 10
+    kTReduceMerge = 10, // small-data reduce: the whole merge tree in one workgroup
+    kTSlots = 11
 };
 void timer_begin(int slot, hipStream_t s);
 void timer_end(int slot, hipStream_t s);
@@ -99,6 +100,7 @@ struct ReducePlan {
     uint32_t P, L, PK, T, ntiles, nchunks, tiles_per_chunk, qbits;  // PK: rank class 16/32/64/128/256
     uint64_t N, lo, thr, sum_nnz;
     int speculate_dense;
+    int small;  // few slots, every node sparse, few entries: the one-workgroup merge tree
 };
 int reduce_plan(int P, uint64_t N, uint64_t max_nnz, uint64_t sum_nnz, double delta, int qbits,
                 ReducePlan* plan, uint64_t lo = 0);
@@ -122,6 +124,16 @@ hipError_t set_result_run(ReduceResult* r, uint64_t nnz, uint32_t dense, hipStre
 hipError_t reduce_run(const ReducePlan& p, const StreamDesc* host_tab, uint32_t* out_idx,
                       float* out_val, uint64_t* node_nnz, uint8_t* node_dense, void* ws,
                       hipStream_t s, ReduceResult* res, uint32_t nfold, ReduceResult* dev_result);
+
+// Small-data path: at most 8 slots holding at most thr entries together (so
+// every node stays sparse), few enough that one workgroup's merge tree is
+// faster than the tile pipeline.
+bool merge_small_fits(uint32_t PT, uint64_t sum_nnz, uint64_t thr);
+// The whole tree in one launch: root to out_idx / out_val, node sizes (in
+// the order of reduce_run), header to hdr and, if not NULL, result.
+hipError_t merge_small_run(uint32_t PT, uint32_t L, uint32_t qbits, uint32_t nfold, const StreamDesc* host_tab,
+                           uint32_t* out_idx, float* out_val, uint64_t* node_nnz, uint8_t* node_dense,
+                           ReduceResult* hdr, ReduceResult* result, hipStream_t s);
 
 // ---------------------------------------------------------------- densify
 // dense[i] = the stream's value at index lo + i, i < N (+0.0 where it has none).

@@ -1226,6 +1226,7 @@ int reduce_plan(int P, uint64_t N, uint64_t max_nnz, uint64_t sum_nnz, double de
     p.sum_nnz = sum_nnz;
     p.qbits = (uint32_t)qbits;
     p.speculate_dense = sum_nnz > p.thr ? 1 : 0;
+    p.small = merge_small_fits(p.P, sum_nnz, p.thr) ? 1 : 0;
     *plan = p;
     return 0;
 }
@@ -1243,7 +1244,17 @@ hipError_t reduce_run(const ReducePlan& p, const StreamDesc* host_tab, uint32_t*
                       hipStream_t s, ReduceResult* res, uint32_t nfold, ReduceResult* dev_result)
 {
     const Layout l = layout(p, ws);
-    hipError_t e = upload(l.tab, host_tab, sizeof(StreamDesc) * p.P, s);
+    hipError_t e;
+    if (p.small) {
+        // few slots, every node sparse, few entries: one workgroup, one launch
+        e = merge_small_run(p.P, p.L, p.qbits, nfold, host_tab, out_idx, out_val, node_nnz, node_dense, l.hdr,
+                            dev_result, s);
+        if (e != hipSuccess || dev_result) return e;
+        if ((e = hipMemcpyAsync(res, l.hdr, sizeof(ReduceResult), hipMemcpyDeviceToHost, s)) != hipSuccess)
+            return e;
+        return hipStreamSynchronize(s);
+    }
+    e = upload(l.tab, host_tab, sizeof(StreamDesc) * p.P, s);
     if (e != hipSuccess) return e;
 
     const uint32_t nthreads = std::max<uint32_t>(p.P * (p.nchunks + 1), p.P + 1);

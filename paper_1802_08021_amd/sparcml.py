@@ -101,7 +101,7 @@ def lib() -> ctypes.CDLL:
 
 TIMER_REDUCE_PASS, TIMER_REDUCE_WRITE, TIMER_REDUCE_SLOW = 0, 1, 2
 TIMER_QUANT_NORM, TIMER_QUANT_CODES, TIMER_TOPK_SELECT, TIMER_TOPK_WRITE, TIMER_DENSIFY = 3, 4, 5, 6, 7
-TIMER_CONCAT, TIMER_TOPK_BUCKETED = 8, 9
+TIMER_CONCAT, TIMER_TOPK_BUCKETED, TIMER_REDUCE_MERGE = 8, 9, 10
 
 
 def timing_enable(on: bool) -> None:
