@@ -36,6 +36,8 @@
 
 #include <algorithm>
 #include <cmath>
+#include <cstddef>
+#include <cstring>
 
 namespace sparcml {
 namespace {
@@ -981,17 +983,32 @@ __global__ void __launch_bounds__(kSlowNT) k_slow(Args a)
 // ------------------------------------------------------------------------
 // Per-chunk start offsets of every stream (binary search) and zeroing of the
 // counters the passes accumulate into.
-__global__ void k_partition(const StreamDesc* tab, uint32_t* off, uint32_t P, uint32_t nchunks,
+// When the descriptor table travels in the arguments (tb.nwords > 0, up to
+// kBlobWords / 12 streams) this launch also stores it to `tab` for the later
+// passes, and reads its own descriptors from the arguments.
+static_assert(sizeof(StreamDesc) == 48 && offsetof(StreamDesc, idx) == 0 && offsetof(StreamDesc, nnz) == 32,
+              "descriptor words read by k_partition");
+__global__ void k_partition(StreamDesc* tab, Blob tb, uint32_t* off, uint32_t P, uint32_t nchunks,
                             uint64_t chunk_coords, uint64_t lo, uint64_t N, uint32_t* zero, uint32_t nzero)
 {
+    constexpr uint32_t W = sizeof(StreamDesc) / 4;  // words per descriptor
     const uint32_t gid = blockIdx.x * blockDim.x + threadIdx.x;
     if (gid < nzero) zero[gid] = 0u;
+    if (gid < tb.nwords) reinterpret_cast<uint32_t*>(tab)[gid] = tb.words[gid];
     const uint32_t stride = nchunks + 1;
     if (gid >= P * stride) return;
     const uint32_t r = gid / stride, c = gid % stride;
-    const uint32_t nnz = (uint32_t)tab[r].nnz;
+    const uint32_t* idx;
+    uint32_t nnz;
+    if (tb.nwords) {  // idx: words 0-1 of the descriptor, nnz: words 8-9
+        idx = reinterpret_cast<const uint32_t*>((uint64_t)tb.words[r * W] | (uint64_t)tb.words[r * W + 1] << 32);
+        nnz = tb.words[r * W + 8];
+    } else {
+        idx = tab[r].idx;
+        nnz = (uint32_t)tab[r].nnz;
+    }
     uint32_t res = nnz;
-    if (c < nchunks) res = lower_bound(tab[r].idx, 0u, nnz, lo + min((uint64_t)c * chunk_coords, N));
+    if (c < nchunks) res = lower_bound(idx, 0u, nnz, lo + min((uint64_t)c * chunk_coords, N));
     off[gid] = res;
 }
 
@@ -1254,11 +1271,19 @@ hipError_t reduce_run(const ReducePlan& p, const StreamDesc* host_tab, uint32_t*
             return e;
         return hipStreamSynchronize(s);
     }
-    e = upload(l.tab, host_tab, sizeof(StreamDesc) * p.P, s);
-    if (e != hipSuccess) return e;
-
-    const uint32_t nthreads = std::max<uint32_t>(p.P * (p.nchunks + 1), p.P + 1);
-    hipLaunchKernelGGL(k_partition, dim3((nthreads + 255) / 256), dim3(256), 0, s, l.tab, l.off,
+    // the descriptor table: in the partition launch's arguments when it fits
+    // there, else uploaded first
+    const size_t tab_bytes = sizeof(StreamDesc) * p.P;
+    Blob tb;
+    tb.nwords = 0;
+    if (tab_bytes <= sizeof(tb.words)) {
+        tb.nwords = (uint32_t)(tab_bytes / 4);
+        memcpy(tb.words, host_tab, tab_bytes);
+    } else if ((e = upload(l.tab, host_tab, tab_bytes, s)) != hipSuccess) {
+        return e;
+    }
+    const uint32_t nthreads = std::max<uint32_t>(std::max<uint32_t>(p.P * (p.nchunks + 1), p.P + 1), tb.nwords);
+    hipLaunchKernelGGL(k_partition, dim3((nthreads + 255) / 256), dim3(256), 0, s, l.tab, tb, l.off,
                        p.P, p.nchunks, (uint64_t)p.tiles_per_chunk * p.T, p.lo, p.N, l.zero, p.P + 1);
     if ((e = hipGetLastError()) != hipSuccess) return e;
 

@@ -26,7 +26,7 @@ def _workload(cfg, seed=0):
     torch, dev = torch_dev()
     c = inputs.config(cfg)
     say(f"[full] {c.name}: P={c.P} N={c.N} generating inputs and device buffers")
-    return c, bench.Workload(c.name, c, seed, torch, dev), torch
+    return c, bench.Workload(c.name, c, seed, torch, dev, keep_host=cfg == 5), torch
 
 
 def _gpu_result(call, torch):
