@@ -70,7 +70,7 @@ if ROOT not in sys.path:
 
 METRIC = "sparse-reduce input nnz/s + achieved HBM GB/s (% of MI355X peak)"
 HBM_PEAK_GBS = 8000.0
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "reduce_tiles_c5_traffic.json")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 
 
 def log(msg: str) -> None:
@@ -426,11 +426,28 @@ GROUP_NAMES = {0: "reduce_tiles", 1: "reduce_write", 2: "reduce_slow", 3: "qsgd_
                9: "topk_bucketed", 10: "reduce_merge"}
 
 
-def source_hash() -> str:
-    """sha256 of the tile pass's sources without comments and blank lines
+# the sources each kernel group is built from (a change of code in them
+# invalidates its measured traffic)
+GROUP_SOURCES = {
+    "reduce_tiles": ("reduce.hip", "qsgd_device.h", "internal.h"),
+    "reduce_write": ("reduce.hip", "qsgd_device.h", "internal.h"),
+    "reduce_slow": ("reduce.hip", "qsgd_device.h", "internal.h"),
+    "reduce_merge": ("merge.hip", "qsgd_device.h", "internal.h"),
+    "qsgd_norm": ("quant.hip", "internal.h"),
+    "qsgd_codes": ("quant.hip", "internal.h"),
+    "topk_select": ("topk.hip", "internal.h"),
+    "topk_write": ("topk.hip", "internal.h"),
+    "topk_bucketed": ("topk_buckets.hip", "internal.h"),
+    "concat": ("concat.hip", "qsgd_device.h", "internal.h"),
+    "densify": ("densify.hip", "qsgd_device.h", "internal.h"),
+}
+
+
+def source_hash(group: str = "reduce_tiles") -> str:
+    """sha256 of a kernel group's sources without comments and blank lines
     (a change of code, not of wording, invalidates measured traffic)."""
     h = hashlib.sha256()
-    for f in ("reduce.hip", "qsgd_device.h", "internal.h"):
+    for f in GROUP_SOURCES[group]:
         with open(os.path.join(ROOT, "paper_1802_08021_amd", "csrc", f)) as fh:
             for line in fh:
                 code = line.split("//", 1)[0].rstrip()
@@ -440,18 +457,20 @@ def source_hash() -> str:
 
 
 def traffic_for(kernel: str, workload: str):
-    """Measured HBM bytes per launch from the committed rocprofv3 counters,
-    only while the kernel source is unchanged since they were taken."""
+    """Measured HBM bytes per launch of a kernel group on a workload, from
+    the committed rocprofv3 FETCH_SIZE/WRITE_SIZE runs (profiles/), only
+    while the group's sources are unchanged since they were taken."""
     try:
         with open(TRAFFIC_FILE) as f:
             t = json.load(f)
     except (OSError, ValueError):
         return None
-    if t.get("kernel") != kernel or t.get("workload") != workload:
-        return None
-    if t.get("source_sha256") != source_hash():
-        return None
-    return t.get("bytes_per_launch")
+    for e in t.get("entries", []):
+        if e.get("kernel") == kernel and e.get("workload") == workload:
+            if kernel in GROUP_SOURCES and e.get("source_sha256") == source_hash(kernel):
+                return e.get("bytes_per_launch")
+            return None
+    return None
 
 
 def oracle_threads() -> int:
@@ -630,7 +649,8 @@ def main() -> int:
         "avg_ms": kdur[dom],
     }
     kernels = {GROUP_NAMES[g]: {"avg_ms": v, "bytes": w.kernel_bytes.get(g),
-                                "GB/s": (w.kernel_bytes[g] / (v * 1e-3) / 1e9) if w.kernel_bytes.get(g) else None}
+                                "GB/s": (w.kernel_bytes[g] / (v * 1e-3) / 1e9) if w.kernel_bytes.get(g) else None,
+                                "traffic": traffic_for(GROUP_NAMES[g], args.workload)}
                for g, v in kdur.items()}
 
     # the step's producer and reduce apart (kernel timers; launches between
@@ -713,7 +733,8 @@ def main() -> int:
                 "step_frac_of_hbm_peak": pw.step_bytes / (pw.ms_plain * 1e-3) / 1e9 / HBM_PEAK_GBS,
                 "root_nnz": pn, "root_dense": pd,
                 "kernels": {GROUP_NAMES[g]: {"avg_ms": v, "GB/s": (pw.kernel_bytes[g] / (v * 1e-3) / 1e9)
-                                             if pw.kernel_bytes.get(g) else None} for g, v in pk.items()},
+                                             if pw.kernel_bytes.get(g) else None,
+                                             "traffic": traffic_for(GROUP_NAMES[g], name)} for g, v in pk.items()},
             }
             if c.kind == "topk":
                 tk = sum(pk.get(g, 0.0) for g in (S.TIMER_TOPK_SELECT, S.TIMER_TOPK_WRITE,
