@@ -101,6 +101,9 @@ struct ReducePlan {
     uint64_t N, lo, thr, sum_nnz;
     int speculate_dense;
     int small;  // few slots, every node sparse, few entries: the one-workgroup merge tree
+    int seg;    // every node sparse, up to 64 slots: the segmented merge tree
+    uint32_t nseg;
+    uint64_t segw;
 };
 int reduce_plan(int P, uint64_t N, uint64_t max_nnz, uint64_t sum_nnz, double delta, int qbits,
                 ReducePlan* plan, uint64_t lo = 0);
@@ -134,6 +137,27 @@ bool merge_small_fits(uint32_t PT, uint64_t sum_nnz, uint64_t thr);
 hipError_t merge_small_run(uint32_t PT, uint32_t L, uint32_t qbits, uint32_t nfold, const StreamDesc* host_tab,
                            uint32_t* out_idx, float* out_val, uint64_t* node_nnz, uint8_t* node_dense,
                            ReduceResult* hdr, ReduceResult* result, hipStream_t s);
+
+// Segmented merge path: at most 64 slots, every node sparse, at most
+// kSegMaxEntries entries; the range cut into nseg segments of segw indices
+// (merge_seg_shape), each merged by one workgroup.
+constexpr uint64_t kSegEntries = 2048;                     // expected entries per segment
+constexpr uint32_t kSegMax = 1024;                         // segments at most
+constexpr uint64_t kSegMaxEntries = kSegEntries * kSegMax;  // inputs it takes at most
+bool merge_seg_fits(uint32_t PT, uint64_t sum_nnz, uint64_t thr);
+void merge_seg_shape(uint64_t R, uint64_t sum_nnz, uint32_t* nseg, uint64_t* segw);
+// Counters of one segmented merge, zeroed before it (k_partition): node
+// union sizes [64], ticket, finished workgroups, error flag, look-back words
+// [nseg] (8-byte aligned).
+struct SegState {
+    uint32_t *node_cnt, *ticket, *done, *err;
+    unsigned long long* flags;
+};
+constexpr uint32_t kSegStateWords = 68;  // words before the look-back words
+hipError_t merge_seg_run(uint32_t PT, uint32_t L, uint32_t qbits, uint32_t nfold, const StreamDesc* dev_tab,
+                         const uint32_t* off, const SegState& st, uint32_t nseg, uint64_t lo, uint64_t segw,
+                         uint64_t N, uint32_t* out_idx, float* out_val, uint64_t* node_nnz, uint8_t* node_dense,
+                         ReduceResult* hdr, ReduceResult* result, hipStream_t s);
 
 // ---------------------------------------------------------------- densify
 // dense[i] = the stream's value at index lo + i, i < N (+0.0 where it has none).

@@ -1,14 +1,14 @@
-// Small-data reduction in one launch (§5.3.1: for small messages recursive
-// doubling is the latency-optimal schedule; §5.1 "Efficient Summation").
+// Sparse reduce as a tree of sorted-list merges, for inputs whose tree nodes
+// all stay sparse (§5.1 "Efficient Summation"; §5.3.1 recursive doubling).
 //
-// When the P' tree slots hold at most thr entries together, no tree node can
+// When the P' tree slots hold at most thr entries together, no node can
 // switch to dense (a sparse node's size is at most the sum of its leaves'
-// sizes), so the whole reduction is a tree of sorted-list merges.  When the
-// entries also fit in one workgroup's LDS, that workgroup runs the tree
-// itself, literally in recursive-doubling order:
+// sizes), and the reduction is the paper's merge tree itself.  A workgroup
+// runs it for the entries of an index range, literally in recursive-doubling
+// order:
 //
-//  * the slot streams are loaded side by side into LDS (QSGD codes
-//    dequantized on the way in), slot s at run start S[s];
+//  * the slot streams' entries in the range are loaded side by side into LDS
+//    (QSGD codes dequantized on the way in), slot s at run start S[s];
 //  * level t merges, for every node g at once, its two children -- the runs
 //    at S[g * 2^t] and S[g * 2^t + 2^(t-1)] -- into the node's run at
 //    S[g * 2^t]: an index present in both children gets left + right;
@@ -20,45 +20,79 @@
 //    positions; per-node counts are the nodes' union sizes (what the switch
 //    rule reports per node).
 //
-// The root run is then copied out.  One launch, no counters to clear, no
-// second pass; the slot table travels in the kernel arguments.
-//
-// A level costs about 4.5 us of dependent LDS round trips and barriers even
-// when it holds few entries, while the tile pipeline costs about 23-30 us of
-// launches for any small input (measured on MI355X, P = 4..32, 256..16384
-// entries).  So this path is taken where it is the faster one: at most 8
-// slots (three levels), with at most 16384 / 8192 / 1024 entries for one,
-// two, three levels.
+// Two kernels use it.  k_merge_small: one workgroup takes the whole range
+// (one launch, the slot table in the kernel arguments).  A level costs about
+// 4.5 us of dependent LDS round trips and barriers even when it holds few
+// entries, while the tile pipeline costs about 23-30 us of launches for any
+// small input (measured on MI355X, P = 4..32, 256..16384 entries), so it is
+// taken for at most 8 slots with at most 16384 / 8192 / 1024 entries for
+// one, two, three levels.  k_merge_seg: the range is cut into segments of
+// equal width (about kSegEntries expected entries each), one small workgroup
+// per segment (several per CU), all at once; a segment's output offset comes
+// from a decoupled look-back over the segments' union sizes (a workgroup
+// waits only on segments whose ticket is lower than its own, which have
+// started and publish their sizes before they wait on anyone), and the last
+// workgroup to finish reports the node sizes.  A segment with more entries
+// than the LDS holds is merged piece by piece (its index range halved until
+// each piece fits), once to count and once more to write.
 #include "internal.h"
 #include "qsgd_device.h"
+
+#include <algorithm>
 
 namespace sparcml {
 namespace {
 
-constexpr int kMNT = 1024;          // threads
-constexpr uint32_t kMCap = 16384;   // entries held in LDS (idx + value: 128 KB)
-constexpr int kMV = 9;              // merged positions per unit (odd: adjacent units fall in different LDS banks)
-constexpr int kMUPT = 2;            // units per thread (kMCap / kMV units, one more per node at most)
-constexpr int kMKL = kMCap / kMNT;  // entries loaded per thread
-constexpr int kMKB = 8;             // of which loaded at once
-constexpr uint32_t kMSlots = 8;     // slots (the kernel-argument table)
-static_assert(kMCap / kMV + 1 + kMSlots / 2 <= (uint32_t)kMNT * kMUPT, "too few units for the nodes of a level");
+constexpr int kMV = 9;               // merged positions per unit (odd: adjacent units fall in different LDS banks)
+constexpr uint32_t kMSlots = 64;     // slots the LDS tables hold
+constexpr uint32_t kSmallSlots = 8;  // slots of the one-workgroup path (its argument table)
 
-struct MTable {
-    StreamDesc d[kMSlots];
+// Threads, LDS entries and units per thread of a merge workgroup.
+template <int NT_, uint32_t CAP_, int UPT_>
+struct MCfg {
+    static constexpr int NT = NT_;
+    static constexpr uint32_t CAP = CAP_;
+    static constexpr int UPT = UPT_;
+    static constexpr int KL = (int)(CAP / NT);  // entries loaded per thread
+    static constexpr int KB = KL < 8 ? KL : 8;  // of which loaded at once
+    static_assert(CAP / kMV + 1 + kMSlots / 2 <= (uint32_t)NT * UPT, "too few units for the nodes of a level");
+};
+using SmallCfg = MCfg<1024, 16384, 2>;  // the whole input in one workgroup (128 KB of entries)
+using SegCfg = MCfg<512, 4096, 1>;      // one segment per workgroup (32 KB), several workgroups per CU
+
+template <class C>
+struct MLds {
+    uint32_t idx[C::CAP];
+    float val[C::CAP];
+    uint32_t start[kMSlots + 1];   // run start of each slot; start[PT] = all entries
+    uint32_t len[kMSlots];         // current run length, kept at the node's first slot
+    uint32_t ub[kMSlots / 2 + 1];  // first unit of each node of a level; ub[nodes] = units
+    uint32_t nb[kMSlots / 2];      // scan value at each node's first unit
+    uint32_t lc[kMSlots / 2];      // outputs of each node of the level (its union size)
+    uint32_t cnt[kMSlots - 1];     // union size of every node, level order
+    const uint32_t* pi[kMSlots];   // slot index streams
+    const void* pv[kMSlots];       // slot values, or QSGD codes
+    uint32_t first[kMSlots];       // stream position of the slot's first entry in the range
+    float unit[kMSlots];           // QSGD level unit of the slot
+    uint32_t w[C::NT / 64];
 };
 
-struct MArgs {
-    uint32_t PT, L, qbits, nfold;
-    uint32_t* out_idx;
-    float* out_val;
-    uint64_t* node_nnz;
-    uint8_t* node_dense;
-    ReduceResult* hdr;
-    ReduceResult* result;
-};
+// Past every index: indices lie below 2^32 - 1 (N < 2^32, and a range ends
+// at or below N).
+constexpr uint32_t kNone = 0xFFFFFFFFu;
+
+// Stream pointers kept in LDS are generic; read through them as global
+// memory, so that the reads are not FLAT accesses (which also count against
+// the LDS wait counter).
+typedef const uint32_t __attribute__((address_space(1)))* g_u32p;
+typedef const float __attribute__((address_space(1)))* g_f32p;
+typedef const uint8_t __attribute__((address_space(1)))* g_u8p;
+__device__ __forceinline__ g_u32p as_global(const uint32_t* p) { return (g_u32p)p; }
+__device__ __forceinline__ g_f32p as_global(const float* p) { return (g_f32p)p; }
+__device__ __forceinline__ g_u8p as_global(const uint8_t* p) { return (g_u8p)p; }
 
 // Exclusive scan of v over the workgroup; *total = the sum over all threads.
+template <int NT>
 __device__ __forceinline__ uint32_t wg_excl_scan(uint32_t v, uint32_t* s_w, uint32_t* total)
 {
     const uint32_t lane = threadIdx.x & 63u, wv = threadIdx.x >> 6;
@@ -68,7 +102,7 @@ __device__ __forceinline__ uint32_t wg_excl_scan(uint32_t v, uint32_t* s_w, uint
     __syncthreads();
     uint32_t before = 0, t = 0;
 #pragma unroll
-    for (uint32_t w = 0; w < (uint32_t)kMNT / 64u; ++w) {
+    for (uint32_t w = 0; w < (uint32_t)NT / 64u; ++w) {
         const uint32_t x = s_w[w];
         before += w < wv ? x : 0u;
         t += x;
@@ -92,122 +126,110 @@ __device__ __forceinline__ uint32_t last_at_most(const uint32_t* a, uint32_t n, 
     return pos;
 }
 
-// Past every index: indices lie below 2^32 - 1 (N < 2^32, and a range ends
-// at or below N).
-constexpr uint32_t kNone = 0xFFFFFFFFu;
-
-template <bool QUANT>
-__global__ void __launch_bounds__(kMNT) k_merge_small(MTable kt, MArgs a)
+// Run starts from this thread's slot size n (threads >= PT pass 0); returns
+// the number of entries.
+template <class C>
+__device__ __forceinline__ uint32_t slot_starts(MLds<C>& m, uint32_t PT, uint32_t n)
 {
-    __shared__ uint32_t s_idx[kMCap];
-    __shared__ float s_val[kMCap];
-    __shared__ uint32_t s_start[kMSlots + 1];  // run start of each slot; s_start[PT] = all entries
-    __shared__ uint32_t s_len[kMSlots];    // current run length, kept at the node's first slot
-    __shared__ uint32_t s_ub[kMSlots / 2 + 1];  // first unit of each node of a level; s_ub[nodes] = units
-    __shared__ uint32_t s_nb[kMSlots / 2];  // scan value at each node's first unit
-    __shared__ uint32_t s_lc[kMSlots / 2];  // outputs of each node of the level (its union size)
-    __shared__ uint32_t s_cnt[kMSlots - 1];  // union size of every node, level order
-    __shared__ const uint32_t* s_pi[kMSlots];
-    __shared__ const void* s_pv[kMSlots];  // values, or QSGD codes
-    __shared__ float s_unit[QUANT ? kMSlots : 1];
-    __shared__ uint32_t s_w[kMNT / 64];
-    const uint32_t tid = threadIdx.x, PT = a.PT;
-
-    // the slot table and each slot's run start
-    uint32_t n = 0;
-    if (tid < PT) {
-        const StreamDesc d = kt.d[tid];
-        n = (uint32_t)d.nnz;
-        s_pi[tid] = d.idx;
-        s_pv[tid] = QUANT ? static_cast<const void*>(d.qval) : static_cast<const void*>(d.val);
-        if (QUANT) s_unit[tid] = n ? level_unit(*d.qscale, a.qbits) : 0.0f;
-        s_len[tid] = n;
-    }
     uint32_t total;
-    const uint32_t st = wg_excl_scan(n, s_w, &total);
-    if (tid <= PT) s_start[tid] = st;  // tid == PT: the total
+    const uint32_t st = wg_excl_scan<C::NT>(n, m.w, &total);
+    if (threadIdx.x <= PT) m.start[threadIdx.x] = st;  // thread PT: the total
+    if (threadIdx.x < PT) m.len[threadIdx.x] = n;
     __syncthreads();
+    return total;
+}
 
-    // load: entry e of the concatenation is entry e - S[s] of slot s; in
-    // batches of kMKB entries per thread whose loads are all issued before
-    // any is stored
+// Entry e of the concatenation is entry e - S[s] of slot s, at stream
+// position first[s] + e - S[s]; in batches of KB entries per thread whose
+// loads are all issued before any is stored.
+template <class C, bool QUANT>
+__device__ __forceinline__ void load_runs(MLds<C>& m, uint32_t PT, uint32_t total, uint32_t qbits)
+{
+    const uint32_t tid = threadIdx.x;
     const uint32_t wfirst = (uint32_t)__builtin_amdgcn_readfirstlane((int)(tid & ~63u));  // the wave's lane 0
-    for (int b = 0; b < kMKL; b += kMKB) {
-        if (wfirst + (uint32_t)b * kMNT >= total) break;  // the wave has no entry left
-        uint32_t slot[kMKB], pos[kMKB];
+    for (int b = 0; b < C::KL; b += C::KB) {
+        if (wfirst + (uint32_t)b * C::NT >= total) break;  // the wave has no entry left
+        uint32_t slot[C::KB], pos[C::KB];
 #pragma unroll
-        for (int k = 0; k < kMKB; ++k) {
-            const uint32_t e = tid + (uint32_t)(b + k) * kMNT;
-            slot[k] = e < total ? last_at_most<3>(s_start, PT, e) : 0u;
-            pos[k] = e - s_start[slot[k]];
+        for (int k = 0; k < C::KB; ++k) {
+            const uint32_t e = tid + (uint32_t)(b + k) * C::NT;
+            slot[k] = e < total ? last_at_most<6>(m.start, PT, e) : 0u;
+            pos[k] = m.first[slot[k]] + e - m.start[slot[k]];
         }
-        uint32_t gi[kMKB];
-        float gv[kMKB];
+        uint32_t gi[C::KB];
+        float gv[C::KB];
 #pragma unroll
-        for (int k = 0; k < kMKB; ++k) {
-            const uint32_t e = tid + (uint32_t)(b + k) * kMNT;
+        for (int k = 0; k < C::KB; ++k) {
+            const uint32_t e = tid + (uint32_t)(b + k) * C::NT;
             if (e < total) {
                 const uint32_t s = slot[k];
-                gi[k] = s_pi[s][pos[k]];
+                gi[k] = as_global(m.pi[s])[pos[k]];
                 if (QUANT) {
-                    const uint32_t code = load_code(static_cast<const uint8_t*>(s_pv[s]), pos[k], a.qbits);
-                    gv[k] = dequant(code, a.qbits, s_unit[s]);
+                    const uint32_t code = load_code(as_global(static_cast<const uint8_t*>(m.pv[s])), pos[k], qbits);
+                    gv[k] = dequant(code, qbits, m.unit[s]);
                 } else {
-                    gv[k] = static_cast<const float*>(s_pv[s])[pos[k]];
+                    gv[k] = as_global(static_cast<const float*>(m.pv[s]))[pos[k]];
                 }
             }
         }
 #pragma unroll
-        for (int k = 0; k < kMKB; ++k) {
-            const uint32_t e = tid + (uint32_t)(b + k) * kMNT;
+        for (int k = 0; k < C::KB; ++k) {
+            const uint32_t e = tid + (uint32_t)(b + k) * C::NT;
             if (e < total) {
-                s_idx[e] = gi[k];
-                s_val[e] = gv[k];
+                m.idx[e] = gi[k];
+                m.val[e] = gv[k];
             }
         }
     }
     __syncthreads();
+}
 
-    // the tree, level by level
+// The tree over the loaded runs, level by level; returns the root's length
+// (its run starts at 0) and leaves every node's union size in m.cnt.
+template <class C>
+__device__ __forceinline__ uint32_t merge_levels(MLds<C>& m, uint32_t PT, uint32_t L, uint32_t total)
+{
+    constexpr int NT = C::NT, UPT = C::UPT;
+    const uint32_t tid = threadIdx.x;
+    const uint32_t wfirst = (uint32_t)__builtin_amdgcn_readfirstlane((int)(tid & ~63u));
     uint32_t node_base = 0;  // level-order number of the level's first node
-    for (uint32_t t = 1; t <= a.L; ++t) {
+    for (uint32_t t = 1; t <= L; ++t) {
         const uint32_t nodes = PT >> t, half = 1u << (t - 1u);
         uint32_t units = 0;
         if (tid < nodes) {
             const uint32_t f = tid << t;
-            units = (s_len[f] + s_len[f + half] + (uint32_t)kMV - 1u) / (uint32_t)kMV;
-            s_lc[tid] = 0u;
+            units = (m.len[f] + m.len[f + half] + (uint32_t)kMV - 1u) / (uint32_t)kMV;
+            m.lc[tid] = 0u;
         }
         uint32_t U;
-        const uint32_t ub = wg_excl_scan(units, s_w, &U);
-        if (tid <= nodes) s_ub[tid] = ub;
+        const uint32_t ub = wg_excl_scan<NT>(units, m.w, &U);
+        if (tid <= nodes) m.ub[tid] = ub;
         __syncthreads();
 
         // merge this thread's units into registers, their dependent LDS
-        // reads interleaved; unit q * kMNT + tid, so that the lanes of a
-        // wave work on adjacent units, kMV (odd) entries apart: no LDS bank
+        // reads interleaved; unit q * NT + tid, so that the lanes of a wave
+        // work on adjacent units, kMV (odd) entries apart: no LDS bank
         // conflicts
-        uint32_t key[kMUPT][kMV];
-        float val[kMUPT][kMV];
-        uint32_t valid[kMUPT], cnt[kMUPT], node[kMUPT], sa[kMUPT];
-        uint32_t rem[kMUPT], ia[kMUPT], jb[kMUPT], na[kMUPT], nb[kMUPT], sb[kMUPT], d0[kMUPT], lo[kMUPT],
-            hi[kMUPT];
-        bool wq[kMUPT];  // the wave has a unit q (uniform): the others skip its work
+        uint32_t key[UPT][kMV];
+        float val[UPT][kMV];
+        uint32_t valid[UPT], cnt[UPT], node[UPT], sa[UPT];
+        uint32_t rem[UPT], ia[UPT], jb[UPT], na[UPT], nb[UPT], sb[UPT], d0[UPT], lo[UPT], hi[UPT];
+        bool wq[UPT];  // the wave has a unit q (uniform): the others skip its work
 #pragma unroll
-        for (int q = 0; q < kMUPT; ++q) {
-            const uint32_t u = (uint32_t)q * kMNT + tid;
-            wq[q] = (uint32_t)q * kMNT + wfirst < U;
+        for (int q = 0; q < UPT; ++q) {
+            const uint32_t u = (uint32_t)q * NT + tid;
+            wq[q] = (uint32_t)q * NT + wfirst < U;
             valid[q] = cnt[q] = node[q] = sa[q] = 0u;
             rem[q] = na[q] = nb[q] = sb[q] = d0[q] = lo[q] = hi[q] = ia[q] = jb[q] = 0u;
             if (wq[q] && u < U) {
-                const uint32_t g = last_at_most<2>(s_ub, nodes, u);  // node of the unit (units > 0)
+                const uint32_t g = last_at_most<5>(m.ub, nodes, u);  // node of the unit (units > 0)
                 const uint32_t f = g << t;
                 node[q] = g;
-                sa[q] = s_start[f];
-                na[q] = s_len[f];
-                sb[q] = s_start[f + half];
-                nb[q] = s_len[f + half];
-                d0[q] = (u - s_ub[g]) * (uint32_t)kMV;
+                sa[q] = m.start[f];
+                na[q] = m.len[f];
+                sb[q] = m.start[f + half];
+                nb[q] = m.len[f + half];
+                d0[q] = (u - m.ub[g]) * (uint32_t)kMV;
                 rem[q] = min((uint32_t)kMV, na[q] + nb[q] - d0[q]);
                 lo[q] = d0[q] > nb[q] ? d0[q] - nb[q] : 0u;
                 hi[q] = min(d0[q], na[q]);
@@ -218,36 +240,36 @@ __global__ void __launch_bounds__(kMNT) k_merge_small(MTable kt, MArgs a)
         // largest c in [lo, hi] whose left entry c - 1 is at most the right
         // entry d0 - c, found in fixed steps
 #pragma unroll
-        for (int q = 0; q < kMUPT; ++q) ia[q] = lo[q];
+        for (int q = 0; q < UPT; ++q) ia[q] = lo[q];
         const int top = 31 - __clz(total | 1u);  // hi - lo <= total < 2^(top + 1)
         for (int k = top; k >= 0; --k) {
 #pragma unroll
-            for (int q = 0; q < kMUPT; ++q) {
+            for (int q = 0; q < UPT; ++q) {
                 if (!wq[q]) continue;
                 const uint32_t c = ia[q] + (1u << k);
                 const bool in = c <= hi[q];
-                const uint32_t x = s_idx[in ? sa[q] + c - 1u : 0u], y = s_idx[in ? sb[q] + d0[q] - c : 0u];
+                const uint32_t x = m.idx[in ? sa[q] + c - 1u : 0u], y = m.idx[in ? sb[q] + d0[q] - c : 0u];
                 ia[q] = in && x <= y ? c : ia[q];
             }
         }
-        uint32_t ka[kMUPT], kb[kMUPT];
-        float va[kMUPT], vb[kMUPT];
-        bool skip[kMUPT];
+        uint32_t ka[UPT], kb[UPT];
+        float va[UPT], vb[UPT];
+        bool skip[UPT];
 #pragma unroll
-        for (int q = 0; q < kMUPT; ++q) {
+        for (int q = 0; q < UPT; ++q) {
             ka[q] = kb[q] = kNone;
             va[q] = vb[q] = 0.0f;
             skip[q] = false;
             if (!wq[q]) continue;
             jb[q] = d0[q] - ia[q];
             const bool ina = ia[q] < na[q], inb = jb[q] < nb[q];
-            ka[q] = ina ? s_idx[sa[q] + ia[q]] : kNone;
-            va[q] = ina ? s_val[sa[q] + ia[q]] : 0.0f;
-            kb[q] = inb ? s_idx[sb[q] + jb[q]] : kNone;
-            vb[q] = inb ? s_val[sb[q] + jb[q]] : 0.0f;
+            ka[q] = ina ? m.idx[sa[q] + ia[q]] : kNone;
+            va[q] = ina ? m.val[sa[q] + ia[q]] : 0.0f;
+            kb[q] = inb ? m.idx[sb[q] + jb[q]] : kNone;
+            vb[q] = inb ? m.val[sb[q] + jb[q]] : 0.0f;
             // a right entry equal to the left entry before the split was
             // summed by the unit that took that left entry
-            skip[q] = inb && ia[q] > 0u && rem[q] && s_idx[sa[q] + ia[q] - 1u] == kb[q];
+            skip[q] = inb && ia[q] > 0u && rem[q] && m.idx[sa[q] + ia[q] - 1u] == kb[q];
         }
         // one merged position per step, without branches: take the left
         // head (summed with an equal right head), or the right head, or skip
@@ -256,7 +278,7 @@ __global__ void __launch_bounds__(kMNT) k_merge_small(MTable kt, MArgs a)
 #pragma unroll
         for (int s = 0; s < kMV; ++s) {
 #pragma unroll
-            for (int q = 0; q < kMUPT; ++q) {
+            for (int q = 0; q < UPT; ++q) {
                 key[q][s] = 0u;
                 val[q][s] = 0.0f;
                 if (!wq[q]) continue;
@@ -274,8 +296,8 @@ __global__ void __launch_bounds__(kMNT) k_merge_small(MTable kt, MArgs a)
                 jb[q] += tB ? 1u : 0u;
                 const bool in = tA ? ia[q] < na[q] : jb[q] < nb[q];
                 const uint32_t at = in ? (tA ? sa[q] + ia[q] : sb[q] + jb[q]) : 0u;
-                const uint32_t nk = in ? s_idx[at] : kNone;
-                const float nv = in ? s_val[at] : 0.0f;
+                const uint32_t nk = in ? m.idx[at] : kNone;
+                const float nv = in ? m.val[at] : 0.0f;
                 ka[q] = tA ? nk : ka[q];
                 va[q] = tA ? nv : va[q];
                 kb[q] = tB ? nk : kb[q];
@@ -285,53 +307,97 @@ __global__ void __launch_bounds__(kMNT) k_merge_small(MTable kt, MArgs a)
 
         // output positions: units in order (all q = 0 units, then q = 1, ...),
         // by a scan per q, relative to the node's first unit
-        uint32_t xq[kMUPT], base = 0;
+        uint32_t xq[UPT], base = 0;
 #pragma unroll
-        for (int q = 0; q < kMUPT; ++q) {
+        for (int q = 0; q < UPT; ++q) {
             uint32_t tot;
-            xq[q] = base + wg_excl_scan(cnt[q], s_w, &tot);  // past the first: every read of the level done
+            xq[q] = base + wg_excl_scan<NT>(cnt[q], m.w, &tot);  // past the first: every read of the level done
             base += tot;
         }
 #pragma unroll
-        for (int q = 0; q < kMUPT; ++q) {
-            const uint32_t u = (uint32_t)q * kMNT + tid;
+        for (int q = 0; q < UPT; ++q) {
+            const uint32_t u = (uint32_t)q * NT + tid;
             if (u < U) {
-                if (u == s_ub[node[q]]) s_nb[node[q]] = xq[q];
-                if (cnt[q]) atomicAdd(&s_lc[node[q]], cnt[q]);
+                if (u == m.ub[node[q]]) m.nb[node[q]] = xq[q];
+                if (cnt[q]) atomicAdd(&m.lc[node[q]], cnt[q]);
             }
         }
         __syncthreads();
 #pragma unroll
-        for (int q = 0; q < kMUPT; ++q) {
+        for (int q = 0; q < UPT; ++q) {
             if (!valid[q]) continue;
-            uint32_t p = sa[q] + xq[q] - s_nb[node[q]];  // the node's run starts at its left child's
+            uint32_t p = sa[q] + xq[q] - m.nb[node[q]];  // the node's run starts at its left child's
 #pragma unroll
             for (int s = 0; s < kMV; ++s) {
                 if (valid[q] & (1u << s)) {
-                    s_idx[p] = key[q][s];
-                    s_val[p] = val[q][s];
+                    m.idx[p] = key[q][s];
+                    m.val[p] = val[q][s];
                     ++p;
                 }
             }
         }
         __syncthreads();
         if (tid < nodes) {
-            s_len[tid << t] = s_lc[tid];
-            s_cnt[node_base + tid] = s_lc[tid];
+            m.len[tid << t] = m.lc[tid];
+            m.cnt[node_base + tid] = m.lc[tid];
         }
         node_base += nodes;
         __syncthreads();
     }
+    return m.len[0];
+}
 
-    // the root run, the per-node sizes (all sparse) and the result header
-    const uint32_t root = s_len[0];
-    for (uint32_t e = tid; e < root; e += kMNT) {
-        a.out_idx[e] = s_idx[e];
-        a.out_val[e] = s_val[e];
+// Node t of the P'-slot tree (level order) goes to position o of node_nnz /
+// node_dense: the first nfold level-1 nodes, then every higher node.
+__device__ __forceinline__ bool report_slot(uint32_t t, uint32_t PT, uint32_t nfold, uint32_t* o)
+{
+    if (t + 1u >= PT || (t < PT / 2u && t >= nfold)) return false;
+    *o = t < PT / 2u ? t : t - PT / 2u + nfold;
+    return true;
+}
+
+// ------------------------------------------------------------------------
+// One workgroup, the whole range.
+
+struct MTable {
+    StreamDesc d[kSmallSlots];
+};
+
+struct MArgs {
+    uint32_t PT, L, qbits, nfold;
+    uint32_t* out_idx;
+    float* out_val;
+    uint64_t* node_nnz;
+    uint8_t* node_dense;
+    ReduceResult* hdr;
+    ReduceResult* result;
+};
+
+template <bool QUANT>
+__global__ void __launch_bounds__(SmallCfg::NT) k_merge_small(MTable kt, MArgs a)
+{
+    using C = SmallCfg;
+    __shared__ MLds<C> m;
+    const uint32_t tid = threadIdx.x, PT = a.PT;
+    uint32_t n = 0;
+    if (tid < PT) {
+        const StreamDesc d = kt.d[tid];
+        n = (uint32_t)d.nnz;
+        m.pi[tid] = d.idx;
+        m.pv[tid] = QUANT ? static_cast<const void*>(d.qval) : static_cast<const void*>(d.val);
+        m.first[tid] = 0u;
+        if (QUANT) m.unit[tid] = n ? level_unit(*d.qscale, a.qbits) : 0.0f;
     }
-    if (tid + 1u < PT && (tid >= PT / 2u || tid < a.nfold)) {
-        const uint32_t o = tid < PT / 2u ? tid : tid - PT / 2u + a.nfold;
-        if (a.node_nnz) a.node_nnz[o] = s_cnt[tid];
+    const uint32_t total = slot_starts(m, PT, n);
+    load_runs<C, QUANT>(m, PT, total, a.qbits);
+    const uint32_t root = merge_levels(m, PT, a.L, total);
+    for (uint32_t e = tid; e < root; e += C::NT) {
+        a.out_idx[e] = m.idx[e];
+        a.out_val[e] = m.val[e];
+    }
+    uint32_t o;
+    if (report_slot(tid, PT, a.nfold, &o)) {
+        if (a.node_nnz) a.node_nnz[o] = m.cnt[tid];
         if (a.node_dense) a.node_dense[o] = 0u;
     }
     if (tid == 0) {
@@ -341,12 +407,234 @@ __global__ void __launch_bounds__(kMNT) k_merge_small(MTable kt, MArgs a)
     }
 }
 
+// ------------------------------------------------------------------------
+// One workgroup per segment.
+
+struct SArgs {
+    const StreamDesc* tab;
+    const uint32_t* off;  // [PT][nseg + 1] stream position of each segment's first entry
+    SegState st;
+    uint32_t PT, L, qbits, nfold, nseg;
+    uint64_t lo, segw, N;  // range [lo, lo + N); segment s: [lo + s segw, lo + min((s + 1) segw, N))
+    uint32_t* out_idx;
+    float* out_val;
+    uint64_t* node_nnz;
+    uint8_t* node_dense;
+    ReduceResult* hdr;
+    ReduceResult* result;
+};
+
+// look-back words: status (1 the segment's own size, 2 the sum through it)
+// in the top two bits, the size or sum below
+constexpr unsigned long long kAgg = 1ull << 62, kIncl = 2ull << 62, kValMask = (1ull << 62) - 1ull;
+constexpr uint32_t kSpinLimit = 1u << 24;  // polls of one predecessor before the look-back gives up
+
+// First position in [a, b) of a sorted stream whose index is at least x.
+__device__ __forceinline__ uint32_t first_at_least(const uint32_t* idx, uint32_t a, uint32_t b, uint64_t x)
+{
+    while (a < b) {
+        const uint32_t mid = a + ((b - a) >> 1);
+        if ((uint64_t)as_global(idx)[mid] < x) a = mid + 1u;
+        else b = mid;
+    }
+    return a;
+}
+
+// The pieces of a segment that does not fit, in index order: its range
+// halved until each piece does (one index holds at most PT entries).
+// write = false: count (the pieces' node sizes added to s_acc); true: write
+// the pieces' roots from `at` on.  Returns the entries of the roots.  Whole
+// workgroup; slot r's entries in the segment are at stream positions [ra, rb).
+template <bool QUANT>
+__device__ __forceinline__ unsigned long long seg_pieces(MLds<SegCfg>& m, const SArgs& a, bool write,
+                                                         unsigned long long at, uint32_t ra, uint32_t rb,
+                                                         uint64_t c0, uint64_t c1, uint32_t* s_acc,
+                                                         uint64_t* s_lo, uint64_t* s_hi, uint32_t* s_depth,
+                                                         uint32_t* s_fits)
+{
+    using C = SegCfg;
+    const uint32_t tid = threadIdx.x, PT = a.PT;
+    unsigned long long done = 0;
+    if (tid == 0) {
+        *s_depth = 1u;
+        s_lo[0] = c0;
+        s_hi[0] = c1;
+    }
+    __syncthreads();
+    while (*s_depth) {
+        const uint32_t depth = *s_depth;
+        const uint64_t x0 = s_lo[depth - 1u], x1 = s_hi[depth - 1u];
+        uint32_t n = 0;
+        if (tid < PT) {
+            const uint32_t p0 = first_at_least(m.pi[tid], ra, rb, x0);
+            const uint32_t p1 = first_at_least(m.pi[tid], p0, rb, x1);
+            m.first[tid] = p0;
+            n = p1 - p0;
+        }
+        const uint32_t pt = slot_starts(m, PT, n);  // its barriers follow every read of the stack top
+        if (tid == 0) {
+            *s_fits = pt <= C::CAP || x1 - x0 <= 1u ? 1u : 0u;
+            if (*s_fits) {
+                *s_depth = depth - 1u;
+            } else {  // halves, the lower one on top
+                const uint64_t mid = x0 + (x1 - x0) / 2u;
+                s_lo[depth - 1u] = mid;
+                s_lo[depth] = x0;
+                s_hi[depth] = mid;
+                *s_depth = depth + 1u;
+            }
+        }
+        __syncthreads();
+        if (!*s_fits) continue;
+        load_runs<C, QUANT>(m, PT, pt, a.qbits);
+        const uint32_t root = merge_levels(m, PT, a.L, pt);
+        if (write) {
+            for (uint32_t e = tid; e < root; e += C::NT) {
+                a.out_idx[at + done + e] = m.idx[e];
+                a.out_val[at + done + e] = m.val[e];
+            }
+        } else if (tid + 1u < PT) {
+            s_acc[tid] += m.cnt[tid];
+        }
+        done += root;
+        __syncthreads();
+    }
+    return done;
+}
+
+template <bool QUANT>
+__global__ void __launch_bounds__(SegCfg::NT) k_merge_seg(SArgs a)
+{
+    using C = SegCfg;
+    __shared__ MLds<C> m;
+    __shared__ uint32_t s_seg, s_last, s_ok;
+    __shared__ unsigned long long s_excl;
+    __shared__ uint32_t s_acc[kMSlots - 1];  // node sizes of the segment
+    __shared__ uint64_t s_lo[40], s_hi[40];  // pieces still to do (a stack)
+    __shared__ uint32_t s_depth, s_fits;
+    const uint32_t tid = threadIdx.x, PT = a.PT;
+    if (tid == 0) s_seg = atomicAdd(a.st.ticket, 1u);
+    __syncthreads();
+    const uint32_t s = s_seg, stride = a.nseg + 1u;
+    uint32_t ra = 0, rb = 0;  // this slot's entries in the segment: stream positions [ra, rb)
+    if (tid < PT) {
+        const StreamDesc d = a.tab[tid];
+        ra = a.off[tid * stride + s];
+        rb = a.off[tid * stride + s + 1u];
+        m.pi[tid] = d.idx;
+        m.pv[tid] = QUANT ? static_cast<const void*>(d.qval) : static_cast<const void*>(d.val);
+        m.first[tid] = ra;
+        if (QUANT) m.unit[tid] = d.nnz ? level_unit(*d.qscale, a.qbits) : 0.0f;
+    }
+    if (tid < kMSlots - 1u) s_acc[tid] = 0u;
+    const uint32_t total = slot_starts(m, PT, rb - ra);
+    const uint64_t c0 = a.lo + (uint64_t)s * a.segw, c1 = a.lo + min((uint64_t)(s + 1u) * a.segw, a.N);
+
+    // this segment's union size (and node sizes)
+    unsigned long long R;
+    const bool big = total > C::CAP;  // uniform
+    if (!big) {
+        load_runs<C, QUANT>(m, PT, total, a.qbits);
+        R = merge_levels(m, PT, a.L, total);
+        if (tid + 1u < PT) s_acc[tid] = m.cnt[tid];
+    } else {
+        R = seg_pieces<QUANT>(m, a, false, 0ull, ra, rb, c0, c1, s_acc, s_lo, s_hi, &s_depth, &s_fits);
+    }
+    __syncthreads();
+
+    // its output offset: decoupled look-back over the lower segments, by the
+    // first wave, 64 predecessors at a time (lane l reads segment j0 - 1 - l;
+    // those below segment 0 read as a finished sum of 0): the sizes up to the
+    // nearest finished sum are added once every one of them is there
+    if (tid < 64u) {
+        unsigned long long* f = a.st.flags;
+        const uint32_t lane = tid;
+        if (lane == 0)
+            __hip_atomic_store(&f[s], (s ? kAgg : kIncl) | R, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        unsigned long long excl = 0;
+        uint32_t ok = 1u, spins = 0;
+        int j0 = (int)s;
+        while (j0 > 0) {
+            const int j = j0 - 1 - (int)lane;
+            const unsigned long long v =
+                j >= 0 ? __hip_atomic_load(&f[j], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : kIncl;
+            const uint64_t fin = __ballot((v >> 62) == 2ull), miss = __ballot((v >> 62) == 0ull);
+            const uint32_t upto = fin ? (uint32_t)__builtin_ctzll(fin) : 64u;  // nearest finished sum
+            const uint64_t need = upto >= 63u ? ~0ull : (2ull << upto) - 1ull;
+            if (miss & need) {  // a size still missing: wait and read again
+                if (++spins > kSpinLimit) {
+                    ok = 0u;
+                    break;
+                }
+                __builtin_amdgcn_s_sleep(2);
+                continue;
+            }
+            unsigned long long part = lane <= upto ? (v & kValMask) : 0ull;
+#pragma unroll
+            for (int o = 32; o > 0; o >>= 1) part += __shfl_xor(part, o);
+            excl += part;
+            if (upto < 64u) break;
+            j0 -= 64;
+        }
+        if (lane == 0) {
+            if (ok) {
+                if (s) __hip_atomic_store(&f[s], kIncl | (excl + R), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            } else {
+                atomicOr(a.st.err, 1u);
+            }
+            s_excl = excl;
+            s_ok = ok;
+        }
+    }
+    __syncthreads();
+    if (s_ok) {
+        if (!big) {
+            for (uint32_t e = tid; e < (uint32_t)R; e += C::NT) {
+                a.out_idx[s_excl + e] = m.idx[e];
+                a.out_val[s_excl + e] = m.val[e];
+            }
+        } else {
+            seg_pieces<QUANT>(m, a, true, s_excl, ra, rb, c0, c1, s_acc, s_lo, s_hi, &s_depth, &s_fits);
+        }
+    }
+
+    // node sizes; the last workgroup to finish reports them and the root.
+    // The first wave adds the segment's node sizes (device atomics) and
+    // waits until they are acknowledged before counting itself done, so the
+    // workgroup that counts last finds every size added.  (No release
+    // fence: on this chip that writes back the whole L2, and hundreds of
+    // them stall the look-back of the other segments.)
+    if (tid < 64u) {
+        if (tid + 1u < PT && s_acc[tid]) atomicAdd(&a.st.node_cnt[tid], s_acc[tid]);
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        if (tid == 0) {
+            const uint32_t prev = atomicAdd(a.st.done, 1u);
+            s_last = prev + 1u == a.nseg ? 1u : 0u;
+        }
+    }
+    __syncthreads();
+    if (!s_last) return;
+    uint32_t o;
+    if (report_slot(tid, PT, a.nfold, &o)) {
+        const uint32_t c = __hip_atomic_load(&a.st.node_cnt[tid], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (a.node_nnz) a.node_nnz[o] = c;
+        if (a.node_dense) a.node_dense[o] = 0u;
+    }
+    if (tid == 0) {
+        const uint32_t root = __hip_atomic_load(&a.st.node_cnt[PT - 2u], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const uint32_t err = __hip_atomic_load(a.st.err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const ReduceResult r{root, 0u, err};
+        *a.hdr = r;
+        if (a.result) *a.result = r;
+    }
+}
+
 }  // namespace
 
 bool merge_small_fits(uint32_t PT, uint64_t sum_nnz, uint64_t thr)
 {
-    if (PT < 2 || PT > kMSlots || sum_nnz > thr) return false;  // every node sparse
-    const uint64_t most = PT == 2 ? kMCap : (PT == 4 ? 8192u : 1024u);
+    if (PT < 2 || PT > kSmallSlots || sum_nnz > thr) return false;  // every node sparse
+    const uint64_t most = PT == 2 ? SmallCfg::CAP : (PT == 4 ? 8192u : 1024u);
     return sum_nnz <= most;
 }
 
@@ -354,7 +642,7 @@ hipError_t merge_small_run(uint32_t PT, uint32_t L, uint32_t qbits, uint32_t nfo
                            uint32_t* out_idx, float* out_val, uint64_t* node_nnz, uint8_t* node_dense,
                            ReduceResult* hdr, ReduceResult* result, hipStream_t s)
 {
-    if (PT > kMSlots) return hipErrorInvalidValue;
+    if (PT > kSmallSlots) return hipErrorInvalidValue;
     MTable kt{};
     MArgs a{};
     a.PT = PT;
@@ -369,8 +657,53 @@ hipError_t merge_small_run(uint32_t PT, uint32_t L, uint32_t qbits, uint32_t nfo
     a.result = result;
     for (uint32_t r = 0; r < PT; ++r) kt.d[r] = host_tab[r];
     timer_begin(kTReduceMerge, s);
-    if (qbits) hipLaunchKernelGGL(k_merge_small<true>, dim3(1), dim3(kMNT), 0, s, kt, a);
-    else hipLaunchKernelGGL(k_merge_small<false>, dim3(1), dim3(kMNT), 0, s, kt, a);
+    if (qbits) hipLaunchKernelGGL(k_merge_small<true>, dim3(1), dim3(SmallCfg::NT), 0, s, kt, a);
+    else hipLaunchKernelGGL(k_merge_small<false>, dim3(1), dim3(SmallCfg::NT), 0, s, kt, a);
+    timer_end(kTReduceMerge, s);
+    return hipGetLastError();
+}
+
+bool merge_seg_fits(uint32_t PT, uint64_t sum_nnz, uint64_t thr)
+{
+    return PT >= 2 && PT <= kMSlots && sum_nnz <= thr && sum_nnz <= kSegMaxEntries;
+}
+
+void merge_seg_shape(uint64_t R, uint64_t sum_nnz, uint32_t* nseg, uint64_t* segw)
+{
+    uint64_t n = (sum_nnz + kSegEntries - 1) / kSegEntries;
+    n = std::max<uint64_t>(1, std::min<uint64_t>(std::min<uint64_t>(n, kSegMax), R));
+    const uint64_t w = (R + n - 1) / n;
+    *segw = w;
+    *nseg = (uint32_t)((R + w - 1) / w);
+}
+
+hipError_t merge_seg_run(uint32_t PT, uint32_t L, uint32_t qbits, uint32_t nfold, const StreamDesc* dev_tab,
+                         const uint32_t* off, const SegState& st, uint32_t nseg, uint64_t lo, uint64_t segw,
+                         uint64_t N, uint32_t* out_idx, float* out_val, uint64_t* node_nnz, uint8_t* node_dense,
+                         ReduceResult* hdr, ReduceResult* result, hipStream_t s)
+{
+    if (PT > kMSlots || nseg == 0 || nseg > kSegMax) return hipErrorInvalidValue;
+    SArgs a{};
+    a.tab = dev_tab;
+    a.off = off;
+    a.st = st;
+    a.PT = PT;
+    a.L = L;
+    a.qbits = qbits;
+    a.nfold = nfold;
+    a.nseg = nseg;
+    a.lo = lo;
+    a.segw = segw;
+    a.N = N;
+    a.out_idx = out_idx;
+    a.out_val = out_val;
+    a.node_nnz = node_nnz;
+    a.node_dense = node_dense;
+    a.hdr = hdr;
+    a.result = result;
+    timer_begin(kTReduceMerge, s);
+    if (qbits) hipLaunchKernelGGL(k_merge_seg<true>, dim3(nseg), dim3(SegCfg::NT), 0, s, a);
+    else hipLaunchKernelGGL(k_merge_seg<false>, dim3(nseg), dim3(SegCfg::NT), 0, s, a);
     timer_end(kTReduceMerge, s);
     return hipGetLastError();
 }

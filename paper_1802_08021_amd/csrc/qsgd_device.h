@@ -9,7 +9,9 @@ namespace sparcml {
 
 // Code of element i from a packed array (8/qbits codes per byte, element i
 // at bit (i % (8/qbits)) * qbits of byte i / (8/qbits)).
-__device__ __forceinline__ uint32_t load_code(const uint8_t* q, uint64_t i, uint32_t qbits)
+// (q: any pointer to bytes -- generic, or marked global)
+template <class BytePtr>
+__device__ __forceinline__ uint32_t load_code(BytePtr q, uint64_t i, uint32_t qbits)
 {
     const uint32_t plog = qbits == 8u ? 0u : (qbits == 4u ? 1u : 2u);  // log2(codes per byte)
     const uint32_t byte = q[i >> plog];

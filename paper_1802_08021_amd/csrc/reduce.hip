@@ -1207,8 +1207,10 @@ Layout layout(const ReducePlan& p, void* ws)
     Carve c(ws);
     Layout l;
     l.tab = c.take<StreamDesc>(p.P);
-    l.off = c.take<uint32_t>((size_t)p.P * (p.nchunks + 1));
-    l.zero = c.take<uint32_t>((size_t)p.P + 1);
+    // stream offsets at the tile pass's chunks, or at the merge path's
+    // segments; counters zeroed by the partition launch (either path's)
+    l.off = c.take<uint32_t>((size_t)p.P * (std::max<uint32_t>(p.nchunks, kSegMax) + 1));
+    l.zero = c.take<uint32_t>(std::max<size_t>((size_t)p.P + 1, kSegStateWords + 2 * (size_t)kSegMax));
     l.node_cnt = l.zero;
     l.slow_count = l.zero ? l.zero + p.P : nullptr;
     l.tile_cnt = c.take<uint32_t>(p.ntiles);
@@ -1244,6 +1246,10 @@ int reduce_plan(int P, uint64_t N, uint64_t max_nnz, uint64_t sum_nnz, double de
     p.qbits = (uint32_t)qbits;
     p.speculate_dense = sum_nnz > p.thr ? 1 : 0;
     p.small = merge_small_fits(p.P, sum_nnz, p.thr) ? 1 : 0;
+    p.seg = !p.small && merge_seg_fits(p.P, sum_nnz, p.thr) ? 1 : 0;
+    p.nseg = 0;
+    p.segw = 0;
+    if (p.seg) merge_seg_shape(N, sum_nnz, &p.nseg, &p.segw);
     *plan = p;
     return 0;
 }
@@ -1282,10 +1288,33 @@ hipError_t reduce_run(const ReducePlan& p, const StreamDesc* host_tab, uint32_t*
     } else if ((e = upload(l.tab, host_tab, tab_bytes, s)) != hipSuccess) {
         return e;
     }
-    const uint32_t nthreads = std::max<uint32_t>(std::max<uint32_t>(p.P * (p.nchunks + 1), p.P + 1), tb.nwords);
+    // offsets of every stream at the tile pass's chunks or the merge path's
+    // segments, and that path's counters cleared
+    const uint32_t nparts = p.seg ? p.nseg : p.nchunks;
+    const uint64_t part_coords = p.seg ? p.segw : (uint64_t)p.tiles_per_chunk * p.T;
+    const uint32_t nzero = p.seg ? kSegStateWords + 2u * p.nseg : p.P + 1u;
+    const uint32_t nthreads =
+        std::max<uint32_t>(std::max<uint32_t>(p.P * (nparts + 1), nzero), tb.nwords);
     hipLaunchKernelGGL(k_partition, dim3((nthreads + 255) / 256), dim3(256), 0, s, l.tab, tb, l.off,
-                       p.P, p.nchunks, (uint64_t)p.tiles_per_chunk * p.T, p.lo, p.N, l.zero, p.P + 1);
+                       p.P, nparts, part_coords, p.lo, p.N, l.zero, nzero);
     if ((e = hipGetLastError()) != hipSuccess) return e;
+
+    if (p.seg) {
+        // every node sparse: the merge tree, one workgroup per segment
+        SegState st;
+        st.node_cnt = l.zero;
+        st.ticket = l.zero + 64;
+        st.done = l.zero + 65;
+        st.err = l.zero + 66;
+        st.flags = reinterpret_cast<unsigned long long*>(l.zero + kSegStateWords);
+        e = merge_seg_run(p.P, p.L, p.qbits, nfold, l.tab, l.off, st, p.nseg, p.lo, p.segw, p.N, out_idx,
+                          out_val, node_nnz, node_dense, l.hdr, dev_result, s);
+        if (e != hipSuccess || dev_result) return e;
+        if ((e = hipMemcpyAsync(res, l.hdr, sizeof(ReduceResult), hipMemcpyDeviceToHost, s)) != hipSuccess)
+            return e;
+        if ((e = hipStreamSynchronize(s)) != hipSuccess) return e;
+        return res->pad ? hipErrorLaunchFailure : hipSuccess;  // a look-back that gave up
+    }
 
     Args a{};
     a.tab = l.tab;
