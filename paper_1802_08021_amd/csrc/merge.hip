@@ -187,7 +187,7 @@ __device__ __forceinline__ void load_runs(MLds<C>& m, uint32_t PT, uint32_t tota
 // The tree over the loaded runs, level by level; returns the root's length
 // (its run starts at 0) and leaves every node's union size in m.cnt.
 template <class C>
-__device__ __forceinline__ uint32_t merge_levels(MLds<C>& m, uint32_t PT, uint32_t L, uint32_t total)
+__device__ __forceinline__ uint32_t merge_levels(MLds<C>& m, uint32_t PT, uint32_t L)
 {
     constexpr int NT = C::NT, UPT = C::UPT;
     const uint32_t tid = threadIdx.x;
@@ -239,9 +239,13 @@ __device__ __forceinline__ uint32_t merge_levels(MLds<C>& m, uint32_t PT, uint32
         // one come before position d0 (left first on equal keys): the
         // largest c in [lo, hi] whose left entry c - 1 is at most the right
         // entry d0 - c, found in fixed steps
+        uint32_t span = 0;  // the widest search range of this thread's units
 #pragma unroll
-        for (int q = 0; q < UPT; ++q) ia[q] = lo[q];
-        const int top = 31 - __clz(total | 1u);  // hi - lo <= total < 2^(top + 1)
+        for (int q = 0; q < UPT; ++q) {
+            ia[q] = lo[q];
+            span = max(span, hi[q] - lo[q]);
+        }
+        const int top = 31 - __clz(span | 1u);  // span < 2^(top + 1)
         for (int k = top; k >= 0; --k) {
 #pragma unroll
             for (int q = 0; q < UPT; ++q) {
@@ -390,7 +394,7 @@ __global__ void __launch_bounds__(SmallCfg::NT) k_merge_small(MTable kt, MArgs a
     }
     const uint32_t total = slot_starts(m, PT, n);
     load_runs<C, QUANT>(m, PT, total, a.qbits);
-    const uint32_t root = merge_levels(m, PT, a.L, total);
+    const uint32_t root = merge_levels(m, PT, a.L);
     for (uint32_t e = tid; e < root; e += C::NT) {
         a.out_idx[e] = m.idx[e];
         a.out_val[e] = m.val[e];
@@ -487,7 +491,7 @@ __device__ __forceinline__ unsigned long long seg_pieces(MLds<SegCfg>& m, const 
         __syncthreads();
         if (!*s_fits) continue;
         load_runs<C, QUANT>(m, PT, pt, a.qbits);
-        const uint32_t root = merge_levels(m, PT, a.L, pt);
+        const uint32_t root = merge_levels(m, PT, a.L);
         if (write) {
             for (uint32_t e = tid; e < root; e += C::NT) {
                 a.out_idx[at + done + e] = m.idx[e];
@@ -535,7 +539,7 @@ __global__ void __launch_bounds__(SegCfg::NT) k_merge_seg(SArgs a)
     const bool big = total > C::CAP;  // uniform
     if (!big) {
         load_runs<C, QUANT>(m, PT, total, a.qbits);
-        R = merge_levels(m, PT, a.L, total);
+        R = merge_levels(m, PT, a.L);
         if (tid + 1u < PT) s_acc[tid] = m.cnt[tid];
     } else {
         R = seg_pieces<QUANT>(m, a, false, 0ull, ra, rb, c0, c1, s_acc, s_lo, s_hi, &s_depth, &s_fits);
