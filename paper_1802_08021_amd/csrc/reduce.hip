@@ -1312,8 +1312,7 @@ hipError_t reduce_run(const ReducePlan& p, const StreamDesc* host_tab, uint32_t*
         if (e != hipSuccess || dev_result) return e;
         if ((e = hipMemcpyAsync(res, l.hdr, sizeof(ReduceResult), hipMemcpyDeviceToHost, s)) != hipSuccess)
             return e;
-        if ((e = hipStreamSynchronize(s)) != hipSuccess) return e;
-        return res->pad ? hipErrorLaunchFailure : hipSuccess;  // a look-back that gave up
+        return hipStreamSynchronize(s);  // res->pad nonzero: a look-back gave up (the caller reports it)
     }
 
     Args a{};

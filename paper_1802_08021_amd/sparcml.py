@@ -547,8 +547,12 @@ class ReduceCall:
             "sparcml_sparse_reduce_async_noalloc")
 
     def result_header(self):
-        """(nnz, dense) from ``self.result`` (synchronizes)."""
+        """(nnz, dense) from ``self.result`` (synchronizes); raises if the
+        header's reserved word reports an incomplete reduction."""
         r = self.result.cpu()
+        if (int(r[1]) >> 32) & 0xFFFFFFFF:
+            raise RuntimeError("sparse_reduce_async: a segment of the merge path gave up waiting for its "
+                               "predecessors' sizes; the outputs are incomplete")
         return int(r[0]), bool(int(r[1]) & 0xFFFFFFFF)
 
     def run(self):
