@@ -68,7 +68,7 @@ struct MLds {
     uint32_t len[kMSlots];         // current run length, kept at the node's first slot
     uint32_t ub[kMSlots / 2 + 1];  // first unit of each node of a level; ub[nodes] = units
     uint32_t nb[kMSlots / 2];      // scan value at each node's first unit
-    uint32_t lc[kMSlots / 2];      // outputs of each node of the level (its union size)
+    uint32_t lc[2][kMSlots / 2];   // outputs of each node of a level (its union size), by level parity
     uint32_t cnt[kMSlots - 1];     // union size of every node, level order
     const uint32_t* pi[kMSlots];   // slot index streams
     const void* pv[kMSlots];       // slot values, or QSGD codes
@@ -192,19 +192,27 @@ __device__ __forceinline__ uint32_t merge_levels(MLds<C>& m, uint32_t PT, uint32
     constexpr int NT = C::NT, UPT = C::UPT;
     const uint32_t tid = threadIdx.x;
     const uint32_t wfirst = (uint32_t)__builtin_amdgcn_readfirstlane((int)(tid & ~63u));
+    // Units of the nodes of a level (first wave; at most 32 nodes): node g's
+    // children hold n0(g) and n1(g) entries; ub[g] = its first unit,
+    // ub[nodes] = all; the level's output counters (lc[t & 1]) are cleared.
+    auto level_units = [&](uint32_t t, auto&& n0, auto&& n1) {
+        const uint32_t nodes = PT >> t;
+        uint32_t u = 0;
+        if (tid < nodes) {
+            u = (n0(tid) + n1(tid) + (uint32_t)kMV - 1u) / (uint32_t)kMV;
+            m.lc[t & 1u][tid] = 0u;
+        }
+        const uint32_t incl = wave_scan(u);
+        if (tid <= nodes) m.ub[tid] = incl - u;  // lane `nodes`: the total
+    };
+    if (tid < 64u && L)
+        level_units(1u, [&](uint32_t g) { return m.len[2u * g]; }, [&](uint32_t g) { return m.len[2u * g + 1u]; });
+    __syncthreads();
     uint32_t node_base = 0;  // level-order number of the level's first node
     for (uint32_t t = 1; t <= L; ++t) {
         const uint32_t nodes = PT >> t, half = 1u << (t - 1u);
-        uint32_t units = 0;
-        if (tid < nodes) {
-            const uint32_t f = tid << t;
-            units = (m.len[f] + m.len[f + half] + (uint32_t)kMV - 1u) / (uint32_t)kMV;
-            m.lc[tid] = 0u;
-        }
-        uint32_t U;
-        const uint32_t ub = wg_excl_scan<NT>(units, m.w, &U);
-        if (tid <= nodes) m.ub[tid] = ub;
-        __syncthreads();
+        const uint32_t U = m.ub[nodes];
+        uint32_t* const lc = m.lc[t & 1u];
 
         // merge this thread's units into registers, their dependent LDS
         // reads interleaved; unit q * NT + tid, so that the lanes of a wave
@@ -222,7 +230,8 @@ __device__ __forceinline__ uint32_t merge_levels(MLds<C>& m, uint32_t PT, uint32
             valid[q] = cnt[q] = node[q] = sa[q] = 0u;
             rem[q] = na[q] = nb[q] = sb[q] = d0[q] = lo[q] = hi[q] = ia[q] = jb[q] = 0u;
             if (wq[q] && u < U) {
-                const uint32_t g = last_at_most<5>(m.ub, nodes, u);  // node of the unit (units > 0)
+                uint32_t g = 0;  // node of the unit: nodes whose first unit is at or below u, less one
+                for (uint32_t i = 1; i < nodes; ++i) g += m.ub[i] <= u ? 1u : 0u;
                 const uint32_t f = g << t;
                 node[q] = g;
                 sa[q] = m.start[f];
@@ -323,7 +332,7 @@ __device__ __forceinline__ uint32_t merge_levels(MLds<C>& m, uint32_t PT, uint32
             const uint32_t u = (uint32_t)q * NT + tid;
             if (u < U) {
                 if (u == m.ub[node[q]]) m.nb[node[q]] = xq[q];
-                if (cnt[q]) atomicAdd(&m.lc[node[q]], cnt[q]);
+                if (cnt[q]) atomicAdd(&lc[node[q]], cnt[q]);
             }
         }
         __syncthreads();
@@ -340,11 +349,13 @@ __device__ __forceinline__ uint32_t merge_levels(MLds<C>& m, uint32_t PT, uint32
                 }
             }
         }
-        __syncthreads();
         if (tid < nodes) {
-            m.len[tid << t] = m.lc[tid];
-            m.cnt[node_base + tid] = m.lc[tid];
+            m.len[tid << t] = lc[tid];
+            m.cnt[node_base + tid] = lc[tid];
         }
+        // the next level's units from this level's counts (its children)
+        if (tid < 64u && t < L)
+            level_units(t + 1u, [&](uint32_t g) { return lc[2u * g]; }, [&](uint32_t g) { return lc[2u * g + 1u]; });
         node_base += nodes;
         __syncthreads();
     }
