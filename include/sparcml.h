@@ -203,8 +203,9 @@ SPARCML_API int sparcml_quantize(int P, const sparcml_stream* in, int bits, uint
 typedef struct sparcml_result {
     uint64_t nnz;      /* root nnz (the range's length if dense) */
     uint32_t is_dense; /* root representation */
-    uint32_t reserved; /* 0; nonzero if a workgroup of the all-sparse merge path gave up waiting for
-                          its predecessors' sizes (never expected): the outputs are then incomplete */
+    uint32_t reserved; /* 0; nonzero if the all-sparse merge path could not complete: bit 0, a
+                          workgroup gave up waiting for its predecessors' sizes (never expected);
+                          bit 1, streams that do not ascend were met.  The outputs are then incomplete */
 } sparcml_result;
 
 /*

@@ -250,6 +250,9 @@ int reduce_impl(int P, const sparcml_stream* streams, uint64_t N, uint64_t lo, u
         ReduceResult res{};
         e = reduce_run(plan, tab, out->idx, out->val, node_nnz, node_dense, ws, s, &res, nfold, dres);
         if (e != hipSuccess) return hip_fail(e, "sparse_reduce");
+        if (!dres && (res.pad & 2u))
+            return fail(SPARCML_EUNSORTED, "sparse_reduce: the merge path met streams that do not ascend; "
+                                           "the outputs are incomplete");
         if (!dres && res.pad)
             return fail(SPARCML_EHIP, "sparse_reduce: a segment of the merge path gave up waiting for its "
                                       "predecessors' sizes; the outputs are incomplete");

@@ -488,7 +488,10 @@ __device__ __forceinline__ unsigned long long seg_pieces(MLds<SegCfg>& m, const 
         }
         const uint32_t pt = slot_starts(m, PT, n);  // its barriers follow every read of the stack top
         if (tid == 0) {
-            *s_fits = pt <= C::CAP || x1 - x0 <= 1u ? 1u : 0u;
+            // a single index holds at most PT entries of valid streams; more
+            // (unsorted input) is reported and the index skipped
+            *s_fits = pt <= C::CAP ? 1u : (x1 - x0 <= 1u ? 2u : 0u);
+            if (*s_fits == 2u) atomicOr(a.st.err, 2u);
             if (*s_fits) {
                 *s_depth = depth - 1u;
             } else {  // halves, the lower one on top
@@ -500,7 +503,7 @@ __device__ __forceinline__ unsigned long long seg_pieces(MLds<SegCfg>& m, const 
             }
         }
         __syncthreads();
-        if (!*s_fits) continue;
+        if (*s_fits != 1u) continue;
         load_runs<C, QUANT>(m, PT, pt, a.qbits);
         const uint32_t root = merge_levels(m, PT, a.L);
         if (write) {
@@ -536,6 +539,10 @@ __global__ void __launch_bounds__(SegCfg::NT) k_merge_seg(SArgs a)
         const StreamDesc d = a.tab[tid];
         ra = a.off[tid * stride + s];
         rb = a.off[tid * stride + s + 1u];
+        if (rb < ra) {  // only for streams that do not ascend: reported, the slot skipped
+            atomicOr(a.st.err, 2u);
+            rb = ra;
+        }
         m.pi[tid] = d.idx;
         m.pv[tid] = QUANT ? static_cast<const void*>(d.qval) : static_cast<const void*>(d.val);
         m.first[tid] = ra;
@@ -595,7 +602,7 @@ __global__ void __launch_bounds__(SegCfg::NT) k_merge_seg(SArgs a)
             if (ok) {
                 if (s) __hip_atomic_store(&f[s], kIncl | (excl + R), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             } else {
-                atomicOr(a.st.err, 1u);
+                atomicOr(a.st.err, 1u);  // bit 0: a look-back gave up
             }
             s_excl = excl;
             s_ok = ok;

@@ -550,7 +550,11 @@ class ReduceCall:
         """(nnz, dense) from ``self.result`` (synchronizes); raises if the
         header's reserved word reports an incomplete reduction."""
         r = self.result.cpu()
-        if (int(r[1]) >> 32) & 0xFFFFFFFF:
+        flags = (int(r[1]) >> 32) & 0xFFFFFFFF
+        if flags & 2:
+            raise RuntimeError("sparse_reduce_async: the merge path met streams that do not ascend; "
+                               "the outputs are incomplete")
+        if flags:
             raise RuntimeError("sparse_reduce_async: a segment of the merge path gave up waiting for its "
                                "predecessors' sizes; the outputs are incomplete")
         return int(r[0]), bool(int(r[1]) & 0xFFFFFFFF)
