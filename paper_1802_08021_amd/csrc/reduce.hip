@@ -636,10 +636,11 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
                 vv[y] = sw ? tv : vv[y];
             };
             // Waves 4q + s run on SIMD s (round-robin placement).  The walk of
-            // three or four ranks fills the waves of SIMDs 0-2 from the first,
-            // the row walk takes waves from the other end (those of SIMDs 0-2
-            // from the last, then SIMD 3's), so that the two spread over the
-            // four SIMDs.
+            // three or four ranks fills the waves of SIMDs 0-2 from the first.
+            // The row walk takes the waves of SIMD 3 first when its rows fit
+            // there (those the walk above leaves free), else waves from the
+            // other end (those of SIMDs 0-2 from the last, then SIMD 3's), so
+            // that the two spread over the four SIMDs.
             constexpr uint32_t G3 = (NW / 4) * 3;
             static_assert(NW % 4 == 0, "four SIMDs");
             const uint32_t wslot = (wv & 3u) != 3u ? (wv >> 2) * 3u + (wv & 3u) : G3 + (wv >> 2);
@@ -731,7 +732,10 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
                 float* const rval = s_wv + (wv * RROWS + row) * PMAX;
                 uint32_t* const rpre = s_wp + (wv * RROWS + row) * PW;
                 const uint32_t base = l16 * RK;
-                for (uint32_t b0 = (wslot < G3 ? G3 - 1u - wslot : wslot) * RROWS; b0 < NB; b0 += RROWS * NW) {
+                const bool few = NB <= (uint32_t)(NW / 4) * RROWS;
+                const uint32_t rq = few ? (wslot >= G3 ? wslot - G3 : (uint32_t)NW / 4u + G3 - 1u - wslot)
+                                        : (wslot < G3 ? G3 - 1u - wslot : wslot);
+                for (uint32_t b0 = rq * RROWS; b0 < NB; b0 += RROWS * NW) {
                     const uint32_t i = b0 + row;
                     const bool act = (lane >> 4) < RROWS && i < NB;
                     const uint32_t item = act ? s_listb[i] : 0u;
@@ -756,11 +760,10 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
                         uint32_t prev = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)top, 0x111, 0xF, 0xF, true);
 #pragma unroll
                         for (uint32_t q = 0; q < RK; ++q) {
-                            if ((bits >> q) & 1u) {
-                                const uint32_t r = base + q;
-                                if (prev) atomicAdd(&s_E[sep_level(prev - 1u, r) * PMAX + r], 1u);
-                                prev = r + 1u;
-                            }
+                            const bool pres = (bits >> q) & 1u;
+                            const uint32_t r = base + q;
+                            atomicAdd(&s_E[pres && prev ? sep_level(prev - 1u, r) * PMAX + r : EW + lane], 1u);
+                            prev = pres ? r + 1u : prev;
                         }
                     }
                     if (VALS) {
