@@ -27,8 +27,9 @@
 // small input (measured on MI355X, P = 4..32, 256..16384 entries), so it is
 // taken for at most 8 slots with at most 16384 / 8192 / 1024 entries for
 // one, two, three levels.  k_merge_seg: the range is cut into segments of
-// equal width (about kSegEntries expected entries each), one small workgroup
-// per segment (several per CU), all at once; a segment's output offset comes
+// equal width (about kSegEntries expected entries each, at least kSegMin
+// segments), one small workgroup per segment (several per CU), all at
+// once; a segment's output offset comes
 // from a decoupled look-back over the segments' union sizes (a workgroup
 // waits only on segments whose ticket is lower than its own, which have
 // started and publish their sizes before they wait on anyone), and the last
@@ -692,7 +693,10 @@ bool merge_seg_fits(uint32_t PT, uint64_t sum_nnz, uint64_t thr)
 
 void merge_seg_shape(uint64_t R, uint64_t sum_nnz, uint32_t* nseg, uint64_t* segw)
 {
-    uint64_t n = (sum_nnz + kSegEntries - 1) / kSegEntries;
+    // about kSegEntries expected entries a segment, but at least kSegMin
+    // segments: a smaller segment loads sooner and its merge-path searches
+    // are shorter, and the chip holds far more workgroups than that
+    uint64_t n = std::max<uint64_t>((sum_nnz + kSegEntries - 1) / kSegEntries, kSegMin);
     n = std::max<uint64_t>(1, std::min<uint64_t>(std::min<uint64_t>(n, kSegMax), R));
     const uint64_t w = (R + n - 1) / n;
     *segw = w;
