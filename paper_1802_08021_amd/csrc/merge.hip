@@ -266,29 +266,37 @@ __device__ __forceinline__ uint32_t merge_levels(MLds<C>& m, uint32_t PT, uint32
                 ia[q] = in && x <= y ? c : ia[q];
             }
         }
-        uint32_t ka[UPT], kb[UPT];
-        float va[UPT], vb[UPT];
+        // the heads of both children (ka, kb) and the entries after them
+        // (ka1, kb1; kNone past the end)
+        uint32_t ka[UPT], kb[UPT], ka1[UPT], kb1[UPT];
+        float va[UPT], vb[UPT], va1[UPT], vb1[UPT];
         bool skip[UPT];
+        auto entry = [&](uint32_t base, uint32_t i, uint32_t n, uint32_t& k, float& v) {
+            const bool in = i < n;
+            k = in ? m.idx[base + i] : kNone;
+            v = in ? m.val[base + i] : 0.0f;
+        };
 #pragma unroll
         for (int q = 0; q < UPT; ++q) {
-            ka[q] = kb[q] = kNone;
-            va[q] = vb[q] = 0.0f;
+            ka[q] = kb[q] = ka1[q] = kb1[q] = kNone;
+            va[q] = vb[q] = va1[q] = vb1[q] = 0.0f;
             skip[q] = false;
             if (!wq[q]) continue;
             jb[q] = d0[q] - ia[q];
-            const bool ina = ia[q] < na[q], inb = jb[q] < nb[q];
-            ka[q] = ina ? m.idx[sa[q] + ia[q]] : kNone;
-            va[q] = ina ? m.val[sa[q] + ia[q]] : 0.0f;
-            kb[q] = inb ? m.idx[sb[q] + jb[q]] : kNone;
-            vb[q] = inb ? m.val[sb[q] + jb[q]] : 0.0f;
+            entry(sa[q], ia[q], na[q], ka[q], va[q]);
+            entry(sb[q], jb[q], nb[q], kb[q], vb[q]);
+            entry(sa[q], ia[q] + 1u, na[q], ka1[q], va1[q]);
+            entry(sb[q], jb[q] + 1u, nb[q], kb1[q], vb1[q]);
             // a right entry equal to the left entry before the split was
             // summed by the unit that took that left entry
-            skip[q] = inb && ia[q] > 0u && rem[q] && m.idx[sa[q] + ia[q] - 1u] == kb[q];
+            skip[q] = jb[q] < nb[q] && ia[q] > 0u && rem[q] && m.idx[sa[q] + ia[q] - 1u] == kb[q];
         }
         // one merged position per step, without branches: take the left
         // head (summed with an equal right head), or the right head, or skip
-        // the right twin of a pair summed one step before; then reload the
-        // side that moved
+        // the right twin of a pair summed one step before.  The side that
+        // moved takes its next entry, read one step ahead; then the entries
+        // after both heads are read for the next step, so that no step waits
+        // on a read of its own.
 #pragma unroll
         for (int s = 0; s < kMV; ++s) {
 #pragma unroll
@@ -308,14 +316,14 @@ __device__ __forceinline__ uint32_t merge_levels(MLds<C>& m, uint32_t PT, uint32
                 skip[q] = act ? pair : skip[q];
                 ia[q] += tA ? 1u : 0u;
                 jb[q] += tB ? 1u : 0u;
-                const bool in = tA ? ia[q] < na[q] : jb[q] < nb[q];
-                const uint32_t at = in ? (tA ? sa[q] + ia[q] : sb[q] + jb[q]) : 0u;
-                const uint32_t nk = in ? m.idx[at] : kNone;
-                const float nv = in ? m.val[at] : 0.0f;
-                ka[q] = tA ? nk : ka[q];
-                va[q] = tA ? nv : va[q];
-                kb[q] = tB ? nk : kb[q];
-                vb[q] = tB ? nv : vb[q];
+                ka[q] = tA ? ka1[q] : ka[q];
+                va[q] = tA ? va1[q] : va[q];
+                kb[q] = tB ? kb1[q] : kb[q];
+                vb[q] = tB ? vb1[q] : vb[q];
+                if (s + 1 < kMV) {
+                    entry(sa[q], ia[q] + 1u, na[q], ka1[q], va1[q]);
+                    entry(sb[q], jb[q] + 1u, nb[q], kb1[q], vb1[q]);
+                }
             }
         }
 
