@@ -255,16 +255,30 @@ __device__ __forceinline__ uint32_t merge_levels(MLds<C>& m, uint32_t PT, uint32
             ia[q] = lo[q];
             span = max(span, hi[q] - lo[q]);
         }
+        // (two bits a step: the predicate is monotone in c, so of the three
+        // candidates ia + b, ia + 2b, ia + 3b the ones that hold are a prefix
+        // and their count is the step's pair of bits; the six reads of a step
+        // do not wait on one another)
         const int top = 31 - __clz(span | 1u);  // span < 2^(top + 1)
-        for (int k = top; k >= 0; --k) {
+        auto holds = [&](int q, uint32_t c) -> uint32_t {
+            const bool in = c <= hi[q];
+            const uint32_t x = m.idx[in ? sa[q] + c - 1u : 0u], y = m.idx[in ? sb[q] + d0[q] - c : 0u];
+            return in && x <= y ? 1u : 0u;
+        };
+        int k = top;
+        for (; k >= 1; k -= 2) {
 #pragma unroll
             for (int q = 0; q < UPT; ++q) {
                 if (!wq[q]) continue;
-                const uint32_t c = ia[q] + (1u << k);
-                const bool in = c <= hi[q];
-                const uint32_t x = m.idx[in ? sa[q] + c - 1u : 0u], y = m.idx[in ? sb[q] + d0[q] - c : 0u];
-                ia[q] = in && x <= y ? c : ia[q];
+                const uint32_t b = 1u << (k - 1);
+                const uint32_t n = holds(q, ia[q] + b) + holds(q, ia[q] + 2u * b) + holds(q, ia[q] + 3u * b);
+                ia[q] += n * b;
             }
+        }
+        if (k == 0) {
+#pragma unroll
+            for (int q = 0; q < UPT; ++q)
+                if (wq[q]) ia[q] += holds(q, ia[q] + 1u);
         }
         // the heads of both children (ka, kb) and the entries after them
         // (ka1, kb1; kNone past the end)
