@@ -158,7 +158,9 @@ constexpr uint32_t kSegStateWords = 68;  // words before the look-back words
 hipError_t merge_seg_run(uint32_t PT, uint32_t L, uint32_t qbits, uint32_t nfold, const StreamDesc* dev_tab,
                          const uint32_t* off, const SegState& st, uint32_t nseg, uint64_t lo, uint64_t segw,
                          uint64_t N, uint32_t* out_idx, float* out_val, uint64_t* node_nnz, uint8_t* node_dense,
-                         ReduceResult* hdr, ReduceResult* result, hipStream_t s);
+                         ReduceResult* hdr, ReduceResult* result, bool short_units, hipStream_t s);
+// Whether segments of this many expected entries merge in short units.
+bool merge_seg_short(uint64_t sum_nnz, uint32_t nseg);
 
 // ---------------------------------------------------------------- densify
 // dense[i] = the stream's value at index lo + i, i < N (+0.0 where it has none).

@@ -12,7 +12,7 @@
 //  * level t merges, for every node g at once, its two children -- the runs
 //    at S[g * 2^t] and S[g * 2^t + 2^(t-1)] -- into the node's run at
 //    S[g * 2^t]: an index present in both children gets left + right;
-//  * the merge is cut into units of kMV merged positions (merge path: the
+//  * the merge is cut into units of MV merged positions (merge path: the
 //    split of a unit's first position between the two children is found by
 //    binary search); a unit's outputs stay in registers until every unit has
 //    read its inputs, so the level is merged in place;
@@ -44,22 +44,29 @@
 namespace sparcml {
 namespace {
 
-constexpr int kMV = 9;               // merged positions per unit (odd: adjacent units fall in different LDS banks)
 constexpr uint32_t kMSlots = 64;     // slots the LDS tables hold
 constexpr uint32_t kSmallSlots = 8;  // slots of the one-workgroup path (its argument table)
 
-// Threads, LDS entries and units per thread of a merge workgroup.
-template <int NT_, uint32_t CAP_, int UPT_>
+// Threads, LDS entries, units per thread and merged positions per unit
+// (odd: the units of adjacent lanes start in different LDS banks) of a
+// merge workgroup.  A thread's units merge side by side, so their dependent
+// reads overlap: short units shorten a level when few threads have work.
+template <int NT_, uint32_t CAP_, int UPT_, int MV_>
 struct MCfg {
     static constexpr int NT = NT_;
     static constexpr uint32_t CAP = CAP_;
     static constexpr int UPT = UPT_;
+    static constexpr int MV = MV_;
     static constexpr int KL = (int)(CAP / NT);  // entries loaded per thread
     static constexpr int KB = KL < 8 ? KL : 8;  // of which loaded at once
-    static_assert(CAP / kMV + 1 + kMSlots / 2 <= (uint32_t)NT * UPT, "too few units for the nodes of a level");
+    static_assert(CAP / MV + 1 + kMSlots / 2 <= (uint32_t)NT * UPT, "too few units for the nodes of a level");
+    static_assert(MV % 2 == 1 && MV <= 32, "odd unit, one mask bit per position");
 };
-using SmallCfg = MCfg<1024, 16384, 2>;  // the whole input in one workgroup (128 KB of entries)
-using SegCfg = MCfg<512, 4096, 1>;      // one segment per workgroup (32 KB), several workgroups per CU
+using SmallCfg = MCfg<1024, 16384, 2, 9>;  // the whole input in one workgroup (128 KB of entries)
+// one segment per workgroup (32 KB), several workgroups per CU: units of 9
+// positions, or of 3 for segments whose units fit one a thread
+using SegCfg = MCfg<512, 4096, 1, 9>;
+using SegShortCfg = MCfg<512, 4096, 3, 3>;
 
 template <class C>
 struct MLds {
@@ -76,6 +83,7 @@ struct MLds {
     uint32_t first[kMSlots];       // stream position of the slot's first entry in the range
     float unit[kMSlots];           // QSGD level unit of the slot
     uint32_t w[C::NT / 64];
+    uint2 w2[C::NT / 64];
 };
 
 // Past every index: indices lie below 2^32 - 1 (N < 2^32, and a range ends
@@ -110,6 +118,30 @@ __device__ __forceinline__ uint32_t wg_excl_scan(uint32_t v, uint32_t* s_w, uint
     }
     *total = t;
     return incl - v + before;
+}
+
+// Exclusive scans of a and b over the workgroup (one pair of barriers);
+// *ta, *tb = the sums over all threads.
+template <int NT>
+__device__ __forceinline__ uint2 wg_excl_scan2(uint32_t a, uint32_t b, uint2* s_w, uint32_t* ta, uint32_t* tb)
+{
+    const uint32_t lane = threadIdx.x & 63u, wv = threadIdx.x >> 6;
+    const uint32_t ia = wave_scan(a), ib = wave_scan(b);
+    __syncthreads();  // s_w free from any earlier use
+    if (lane == 63u) s_w[wv] = make_uint2(ia, ib);
+    __syncthreads();
+    uint32_t ba = 0, bb = 0, xa = 0, xb = 0;
+#pragma unroll
+    for (uint32_t w = 0; w < (uint32_t)NT / 64u; ++w) {
+        const uint2 x = s_w[w];
+        ba += w < wv ? x.x : 0u;
+        bb += w < wv ? x.y : 0u;
+        xa += x.x;
+        xb += x.y;
+    }
+    *ta = xa;
+    *tb = xb;
+    return make_uint2(ia - a + ba, ib - b + bb);
 }
 
 // Largest i in [0, n) with a[i] <= x (a ascending, a[0] <= x, n <= 2^LOG
@@ -190,7 +222,7 @@ __device__ __forceinline__ void load_runs(MLds<C>& m, uint32_t PT, uint32_t tota
 template <class C>
 __device__ __forceinline__ uint32_t merge_levels(MLds<C>& m, uint32_t PT, uint32_t L)
 {
-    constexpr int NT = C::NT, UPT = C::UPT;
+    constexpr int NT = C::NT, UPT = C::UPT, MV = C::MV;
     const uint32_t tid = threadIdx.x;
     const uint32_t wfirst = (uint32_t)__builtin_amdgcn_readfirstlane((int)(tid & ~63u));
     // Units of the nodes of a level (first wave; at most 32 nodes): node g's
@@ -200,7 +232,7 @@ __device__ __forceinline__ uint32_t merge_levels(MLds<C>& m, uint32_t PT, uint32
         const uint32_t nodes = PT >> t;
         uint32_t u = 0;
         if (tid < nodes) {
-            u = (n0(tid) + n1(tid) + (uint32_t)kMV - 1u) / (uint32_t)kMV;
+            u = (n0(tid) + n1(tid) + (uint32_t)MV - 1u) / (uint32_t)MV;
             m.lc[t & 1u][tid] = 0u;
         }
         const uint32_t incl = wave_scan(u);
@@ -216,11 +248,10 @@ __device__ __forceinline__ uint32_t merge_levels(MLds<C>& m, uint32_t PT, uint32
         uint32_t* const lc = m.lc[t & 1u];
 
         // merge this thread's units into registers, their dependent LDS
-        // reads interleaved; unit q * NT + tid, so that the lanes of a wave
-        // work on adjacent units, kMV (odd) entries apart: no LDS bank
-        // conflicts
-        uint32_t key[UPT][kMV];
-        float val[UPT][kMV];
+        // reads interleaved; unit q * NT + tid, so that while units are few
+        // each lane of a wave takes one
+        uint32_t key[UPT][MV];
+        float val[UPT][MV];
         uint32_t valid[UPT], cnt[UPT], node[UPT], sa[UPT];
         uint32_t rem[UPT], ia[UPT], jb[UPT], na[UPT], nb[UPT], sb[UPT], d0[UPT], lo[UPT], hi[UPT];
         bool wq[UPT];  // the wave has a unit q (uniform): the others skip its work
@@ -239,8 +270,8 @@ __device__ __forceinline__ uint32_t merge_levels(MLds<C>& m, uint32_t PT, uint32
                 na[q] = m.len[f];
                 sb[q] = m.start[f + half];
                 nb[q] = m.len[f + half];
-                d0[q] = (u - m.ub[g]) * (uint32_t)kMV;
-                rem[q] = min((uint32_t)kMV, na[q] + nb[q] - d0[q]);
+                d0[q] = (u - m.ub[g]) * (uint32_t)MV;
+                rem[q] = min((uint32_t)MV, na[q] + nb[q] - d0[q]);
                 lo[q] = d0[q] > nb[q] ? d0[q] - nb[q] : 0u;
                 hi[q] = min(d0[q], na[q]);
             }
@@ -312,7 +343,7 @@ __device__ __forceinline__ uint32_t merge_levels(MLds<C>& m, uint32_t PT, uint32
         // after both heads are read for the next step, so that no step waits
         // on a read of its own.
 #pragma unroll
-        for (int s = 0; s < kMV; ++s) {
+        for (int s = 0; s < MV; ++s) {
 #pragma unroll
             for (int q = 0; q < UPT; ++q) {
                 key[q][s] = 0u;
@@ -334,7 +365,7 @@ __device__ __forceinline__ uint32_t merge_levels(MLds<C>& m, uint32_t PT, uint32
                 va[q] = tA ? va1[q] : va[q];
                 kb[q] = tB ? kb1[q] : kb[q];
                 vb[q] = tB ? vb1[q] : vb[q];
-                if (s + 1 < kMV) {
+                if (s + 1 < MV) {
                     entry(sa[q], ia[q] + 1u, na[q], ka1[q], va1[q]);
                     entry(sb[q], jb[q] + 1u, nb[q], kb1[q], vb1[q]);
                 }
@@ -342,13 +373,34 @@ __device__ __forceinline__ uint32_t merge_levels(MLds<C>& m, uint32_t PT, uint32
         }
 
         // output positions: units in order (all q = 0 units, then q = 1, ...),
-        // by a scan per q, relative to the node's first unit
-        uint32_t xq[UPT], base = 0;
+        // relative to the node's first unit: one scan of the unit counts
+        // packed two to a word, 16 bits each (a level's count of every q is
+        // at most NT * MV < 2^16), past whose first barrier every read of the
+        // level is done
+        static_assert(NT * MV < 65536 && UPT <= 4, "packed unit counts");
+        uint32_t xq[UPT];
+        {
+            uint32_t p0 = 0, p1 = 0;
 #pragma unroll
-        for (int q = 0; q < UPT; ++q) {
-            uint32_t tot;
-            xq[q] = base + wg_excl_scan<NT>(cnt[q], m.w, &tot);  // past the first: every read of the level done
-            base += tot;
+            for (int q = 0; q < UPT; ++q) {
+                if (q < 2) p0 |= cnt[q] << (16 * q);
+                else p1 |= cnt[q] << (16 * (q - 2));
+            }
+            uint32_t t0 = 0, t1 = 0;
+            uint2 e;
+            if (UPT > 2) {
+                e = wg_excl_scan2<NT>(p0, p1, m.w2, &t0, &t1);
+            } else {
+                e.x = wg_excl_scan<NT>(p0, m.w, &t0);
+                e.y = 0u;
+            }
+            uint32_t base = 0;
+#pragma unroll
+            for (int q = 0; q < UPT; ++q) {
+                const uint32_t ew = q < 2 ? e.x : e.y, tw = q < 2 ? t0 : t1, sh = 16u * (q & 1);
+                xq[q] = base + ((ew >> sh) & 0xFFFFu);
+                base += (tw >> sh) & 0xFFFFu;
+            }
         }
 #pragma unroll
         for (int q = 0; q < UPT; ++q) {
@@ -364,7 +416,7 @@ __device__ __forceinline__ uint32_t merge_levels(MLds<C>& m, uint32_t PT, uint32
             if (!valid[q]) continue;
             uint32_t p = sa[q] + xq[q] - m.nb[node[q]];  // the node's run starts at its left child's
 #pragma unroll
-            for (int s = 0; s < kMV; ++s) {
+            for (int s = 0; s < MV; ++s) {
                 if (valid[q] & (1u << s)) {
                     m.idx[p] = key[q][s];
                     m.val[p] = val[q][s];
@@ -483,14 +535,13 @@ __device__ __forceinline__ uint32_t first_at_least(const uint32_t* idx, uint32_t
 // write = false: count (the pieces' node sizes added to s_acc); true: write
 // the pieces' roots from `at` on.  Returns the entries of the roots.  Whole
 // workgroup; slot r's entries in the segment are at stream positions [ra, rb).
-template <bool QUANT>
-__device__ __forceinline__ unsigned long long seg_pieces(MLds<SegCfg>& m, const SArgs& a, bool write,
+template <bool QUANT, class C>
+__device__ __forceinline__ unsigned long long seg_pieces(MLds<C>& m, const SArgs& a, bool write,
                                                          unsigned long long at, uint32_t ra, uint32_t rb,
                                                          uint64_t c0, uint64_t c1, uint32_t* s_acc,
                                                          uint64_t* s_lo, uint64_t* s_hi, uint32_t* s_depth,
                                                          uint32_t* s_fits)
 {
-    using C = SegCfg;
     const uint32_t tid = threadIdx.x, PT = a.PT;
     unsigned long long done = 0;
     if (tid == 0) {
@@ -543,10 +594,9 @@ __device__ __forceinline__ unsigned long long seg_pieces(MLds<SegCfg>& m, const 
     return done;
 }
 
-template <bool QUANT>
-__global__ void __launch_bounds__(SegCfg::NT) k_merge_seg(SArgs a)
+template <bool QUANT, class C>
+__global__ void __launch_bounds__(C::NT) k_merge_seg(SArgs a)
 {
-    using C = SegCfg;
     __shared__ MLds<C> m;
     __shared__ uint32_t s_seg, s_last, s_ok;
     __shared__ unsigned long long s_excl;
@@ -583,7 +633,7 @@ __global__ void __launch_bounds__(SegCfg::NT) k_merge_seg(SArgs a)
         R = merge_levels(m, PT, a.L);
         if (tid + 1u < PT) s_acc[tid] = m.cnt[tid];
     } else {
-        R = seg_pieces<QUANT>(m, a, false, 0ull, ra, rb, c0, c1, s_acc, s_lo, s_hi, &s_depth, &s_fits);
+        R = seg_pieces<QUANT, C>(m, a, false, 0ull, ra, rb, c0, c1, s_acc, s_lo, s_hi, &s_depth, &s_fits);
     }
     __syncthreads();
 
@@ -639,7 +689,7 @@ __global__ void __launch_bounds__(SegCfg::NT) k_merge_seg(SArgs a)
                 a.out_val[s_excl + e] = m.val[e];
             }
         } else {
-            seg_pieces<QUANT>(m, a, true, s_excl, ra, rb, c0, c1, s_acc, s_lo, s_hi, &s_depth, &s_fits);
+            seg_pieces<QUANT, C>(m, a, true, s_excl, ra, rb, c0, c1, s_acc, s_lo, s_hi, &s_depth, &s_fits);
         }
     }
 
@@ -725,10 +775,16 @@ void merge_seg_shape(uint64_t R, uint64_t sum_nnz, uint32_t* nseg, uint64_t* seg
     *nseg = (uint32_t)((R + w - 1) / w);
 }
 
+bool merge_seg_short(uint64_t sum_nnz, uint32_t nseg)
+{
+    // the units of a segment (its expected entries over 3) fit one a thread
+    return nseg && (sum_nnz + nseg - 1) / nseg <= 3u * (uint64_t)SegShortCfg::NT;
+}
+
 hipError_t merge_seg_run(uint32_t PT, uint32_t L, uint32_t qbits, uint32_t nfold, const StreamDesc* dev_tab,
                          const uint32_t* off, const SegState& st, uint32_t nseg, uint64_t lo, uint64_t segw,
                          uint64_t N, uint32_t* out_idx, float* out_val, uint64_t* node_nnz, uint8_t* node_dense,
-                         ReduceResult* hdr, ReduceResult* result, hipStream_t s)
+                         ReduceResult* hdr, ReduceResult* result, bool short_units, hipStream_t s)
 {
     if (PT > kMSlots || nseg == 0 || nseg > kSegMax) return hipErrorInvalidValue;
     SArgs a{};
@@ -750,8 +806,13 @@ hipError_t merge_seg_run(uint32_t PT, uint32_t L, uint32_t qbits, uint32_t nfold
     a.hdr = hdr;
     a.result = result;
     timer_begin(kTReduceMerge, s);
-    if (qbits) hipLaunchKernelGGL(k_merge_seg<true>, dim3(nseg), dim3(SegCfg::NT), 0, s, a);
-    else hipLaunchKernelGGL(k_merge_seg<false>, dim3(nseg), dim3(SegCfg::NT), 0, s, a);
+    if (short_units) {
+        if (qbits) hipLaunchKernelGGL((k_merge_seg<true, SegShortCfg>), dim3(nseg), dim3(SegShortCfg::NT), 0, s, a);
+        else hipLaunchKernelGGL((k_merge_seg<false, SegShortCfg>), dim3(nseg), dim3(SegShortCfg::NT), 0, s, a);
+    } else {
+        if (qbits) hipLaunchKernelGGL((k_merge_seg<true, SegCfg>), dim3(nseg), dim3(SegCfg::NT), 0, s, a);
+        else hipLaunchKernelGGL((k_merge_seg<false, SegCfg>), dim3(nseg), dim3(SegCfg::NT), 0, s, a);
+    }
     timer_end(kTReduceMerge, s);
     return hipGetLastError();
 }

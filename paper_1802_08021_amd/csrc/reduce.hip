@@ -1311,7 +1311,7 @@ hipError_t reduce_run(const ReducePlan& p, const StreamDesc* host_tab, uint32_t*
         st.err = l.zero + 66;
         st.flags = reinterpret_cast<unsigned long long*>(l.zero + kSegStateWords);
         e = merge_seg_run(p.P, p.L, p.qbits, nfold, l.tab, l.off, st, p.nseg, p.lo, p.segw, p.N, out_idx,
-                          out_val, node_nnz, node_dense, l.hdr, dev_result, s);
+                          out_val, node_nnz, node_dense, l.hdr, dev_result, merge_seg_short(p.sum_nnz, p.nseg), s);
         if (e != hipSuccess || dev_result) return e;
         if ((e = hipMemcpyAsync(res, l.hdr, sizeof(ReduceResult), hipMemcpyDeviceToHost, s)) != hipSuccess)
             return e;
