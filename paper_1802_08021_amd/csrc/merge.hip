@@ -73,10 +73,9 @@ struct MLds {
     uint32_t idx[C::CAP];
     float val[C::CAP];
     uint32_t start[kMSlots + 1];   // run start of each slot; start[PT] = all entries
-    uint32_t len[kMSlots];         // current run length, kept at the node's first slot
-    uint32_t ub[kMSlots / 2 + 1];  // first unit of each node of a level; ub[nodes] = units
-    uint32_t nb[kMSlots / 2];      // scan value at each node's first unit
-    uint32_t lc[2][kMSlots / 2];   // outputs of each node of a level (its union size), by level parity
+    uint32_t len[kMSlots];         // run length of each slot
+    uint32_t rs[2][kMSlots / 2];   // run start of each node of a level, by level parity
+    uint32_t lc[2][kMSlots / 2];   // run length of each node of a level (its union size), by level parity
     uint32_t cnt[kMSlots - 1];     // union size of every node, level order
     const uint32_t* pi[kMSlots];   // slot index streams
     const void* pv[kMSlots];       // slot values, or QSGD codes
@@ -101,12 +100,13 @@ __device__ __forceinline__ g_f32p as_global(const float* p) { return (g_f32p)p; 
 __device__ __forceinline__ g_u8p as_global(const uint8_t* p) { return (g_u8p)p; }
 
 // Exclusive scan of v over the workgroup; *total = the sum over all threads.
-template <int NT>
+// FREE: the caller knows s_w free (a barrier since its last reads).
+template <int NT, bool FREE = false>
 __device__ __forceinline__ uint32_t wg_excl_scan(uint32_t v, uint32_t* s_w, uint32_t* total)
 {
     const uint32_t lane = threadIdx.x & 63u, wv = threadIdx.x >> 6;
     const uint32_t incl = wave_scan(v);
-    __syncthreads();  // s_w free from any earlier use
+    if (!FREE) __syncthreads();  // s_w free from any earlier use
     if (lane == 63u) s_w[wv] = incl;
     __syncthreads();
     uint32_t before = 0, t = 0;
@@ -120,14 +120,14 @@ __device__ __forceinline__ uint32_t wg_excl_scan(uint32_t v, uint32_t* s_w, uint
     return incl - v + before;
 }
 
-// Exclusive scans of a and b over the workgroup (one pair of barriers);
+// Exclusive scans of a and b over the workgroup (the barriers of one);
 // *ta, *tb = the sums over all threads.
-template <int NT>
+template <int NT, bool FREE = false>
 __device__ __forceinline__ uint2 wg_excl_scan2(uint32_t a, uint32_t b, uint2* s_w, uint32_t* ta, uint32_t* tb)
 {
     const uint32_t lane = threadIdx.x & 63u, wv = threadIdx.x >> 6;
     const uint32_t ia = wave_scan(a), ib = wave_scan(b);
-    __syncthreads();  // s_w free from any earlier use
+    if (!FREE) __syncthreads();  // s_w free from any earlier use
     if (lane == 63u) s_w[wv] = make_uint2(ia, ib);
     __syncthreads();
     uint32_t ba = 0, bb = 0, xa = 0, xb = 0;
@@ -218,34 +218,54 @@ __device__ __forceinline__ void load_runs(MLds<C>& m, uint32_t PT, uint32_t tota
 }
 
 // The tree over the loaded runs, level by level; returns the root's length
-// (its run starts at 0) and leaves every node's union size in m.cnt.
+// (its run starts at 0) and leaves every node's union size in m.cnt.  A
+// level's node runs are written one after another, in node order, at their
+// scan positions; a level has two barriers: the scan's, past which every
+// read of the level is done, and the last, past which its runs are written.
 template <class C>
 __device__ __forceinline__ uint32_t merge_levels(MLds<C>& m, uint32_t PT, uint32_t L)
 {
     constexpr int NT = C::NT, UPT = C::UPT, MV = C::MV;
-    const uint32_t tid = threadIdx.x;
+    const uint32_t tid = threadIdx.x, lane = tid & 63u;
     const uint32_t wfirst = (uint32_t)__builtin_amdgcn_readfirstlane((int)(tid & ~63u));
-    // Units of the nodes of a level (first wave; at most 32 nodes): node g's
-    // children hold n0(g) and n1(g) entries; ub[g] = its first unit,
-    // ub[nodes] = all; the level's output counters (lc[t & 1]) are cleared.
-    auto level_units = [&](uint32_t t, auto&& n0, auto&& n1) {
-        const uint32_t nodes = PT >> t;
-        uint32_t u = 0;
-        if (tid < nodes) {
-            u = (n0(tid) + n1(tid) + (uint32_t)MV - 1u) / (uint32_t)MV;
-            m.lc[t & 1u][tid] = 0u;
-        }
-        const uint32_t incl = wave_scan(u);
-        if (tid <= nodes) m.ub[tid] = incl - u;  // lane `nodes`: the total
-    };
-    if (tid < 64u && L)
-        level_units(1u, [&](uint32_t g) { return m.len[2u * g]; }, [&](uint32_t g) { return m.len[2u * g + 1u]; });
-    __syncthreads();
+    if (L == 0u) return m.len[0];
+    // the children of level t's nodes: the slots' runs at level 1, else the
+    // runs of level t - 1's nodes
+    auto cstart = [&](uint32_t t, uint32_t c) -> uint32_t { return t == 1u ? m.start[c] : m.rs[(t - 1u) & 1u][c]; };
+    auto clen = [&](uint32_t t, uint32_t c) -> uint32_t { return t == 1u ? m.len[c] : m.lc[(t - 1u) & 1u][c]; };
+    // level 1's node counters (ordered before its atomics by its scan)
+    if (tid < kMSlots / 2u) m.lc[1][tid] = 0u;
     uint32_t node_base = 0;  // level-order number of the level's first node
     for (uint32_t t = 1; t <= L; ++t) {
-        const uint32_t nodes = PT >> t, half = 1u << (t - 1u);
-        const uint32_t U = m.ub[nodes];
+        const uint32_t nodes = PT >> t;
         uint32_t* const lc = m.lc[t & 1u];
+        // Every wave: the units of the level's nodes (lane g: node g's, for
+        // its children's entries), their first units by a wave scan, and all.
+        uint32_t ug = 0;
+        if (lane < nodes) ug = (clen(t, 2u * lane) + clen(t, 2u * lane + 1u) + (uint32_t)MV - 1u) / (uint32_t)MV;
+        const uint32_t ui = wave_scan(ug), ub_l = ui - ug;  // lane g: node g's first unit
+        const uint32_t U = (uint32_t)__builtin_amdgcn_readlane((int)ui, (int)(nodes - 1u));
+        // the previous level's node sizes, final past its last barrier
+        if (t > 1u && tid < 2u * nodes) m.cnt[node_base - 2u * nodes + tid] = clen(t, tid);
+        // node of each unit q * NT + tid: the nodes whose first unit is at or
+        // below it, less one (gq), and that node's first unit (fq).  Outside
+        // any branch on the unit: a readlane takes the lane's register whether
+        // or not the lane is active, and a value used only in a branch may be
+        // computed there, for the active lanes alone.
+        uint32_t gq[UPT], fq[UPT];
+#pragma unroll
+        for (int q = 0; q < UPT; ++q) gq[q] = fq[q] = 0u;
+        if (wfirst < U) {  // (uniform)
+            for (uint32_t i = 1; i < nodes; ++i) {
+                const uint32_t b = (uint32_t)__builtin_amdgcn_readlane((int)ub_l, (int)i);
+#pragma unroll
+                for (int q = 0; q < UPT; ++q) {
+                    const uint32_t u = (uint32_t)q * NT + tid;
+                    gq[q] += b <= u ? 1u : 0u;
+                    fq[q] = b <= u ? b : fq[q];
+                }
+            }
+        }
 
         // merge this thread's units into registers, their dependent LDS
         // reads interleaved; unit q * NT + tid, so that while units are few
@@ -253,6 +273,7 @@ __device__ __forceinline__ uint32_t merge_levels(MLds<C>& m, uint32_t PT, uint32
         uint32_t key[UPT][MV];
         float val[UPT][MV];
         uint32_t valid[UPT], cnt[UPT], node[UPT], sa[UPT];
+        bool first[UPT];  // the unit is its node's first
         uint32_t rem[UPT], ia[UPT], jb[UPT], na[UPT], nb[UPT], sb[UPT], d0[UPT], lo[UPT], hi[UPT];
         bool wq[UPT];  // the wave has a unit q (uniform): the others skip its work
 #pragma unroll
@@ -260,17 +281,17 @@ __device__ __forceinline__ uint32_t merge_levels(MLds<C>& m, uint32_t PT, uint32
             const uint32_t u = (uint32_t)q * NT + tid;
             wq[q] = (uint32_t)q * NT + wfirst < U;
             valid[q] = cnt[q] = node[q] = sa[q] = 0u;
+            first[q] = false;
             rem[q] = na[q] = nb[q] = sb[q] = d0[q] = lo[q] = hi[q] = ia[q] = jb[q] = 0u;
             if (wq[q] && u < U) {
-                uint32_t g = 0;  // node of the unit: nodes whose first unit is at or below u, less one
-                for (uint32_t i = 1; i < nodes; ++i) g += m.ub[i] <= u ? 1u : 0u;
-                const uint32_t f = g << t;
+                const uint32_t g = gq[q], fu = fq[q];
                 node[q] = g;
-                sa[q] = m.start[f];
-                na[q] = m.len[f];
-                sb[q] = m.start[f + half];
-                nb[q] = m.len[f + half];
-                d0[q] = (u - m.ub[g]) * (uint32_t)MV;
+                first[q] = u == fu;
+                sa[q] = cstart(t, 2u * g);
+                na[q] = clen(t, 2u * g);
+                sb[q] = cstart(t, 2u * g + 1u);
+                nb[q] = clen(t, 2u * g + 1u);
+                d0[q] = (u - fu) * (uint32_t)MV;
                 rem[q] = min((uint32_t)MV, na[q] + nb[q] - d0[q]);
                 lo[q] = d0[q] > nb[q] ? d0[q] - nb[q] : 0u;
                 hi[q] = min(d0[q], na[q]);
@@ -386,12 +407,14 @@ __device__ __forceinline__ uint32_t merge_levels(MLds<C>& m, uint32_t PT, uint32
                 if (q < 2) p0 |= cnt[q] << (16 * q);
                 else p1 |= cnt[q] << (16 * (q - 2));
             }
+            // (the scan words are free: every read of them was before the
+            // previous level's last barrier, or before the caller's)
             uint32_t t0 = 0, t1 = 0;
             uint2 e;
             if (UPT > 2) {
-                e = wg_excl_scan2<NT>(p0, p1, m.w2, &t0, &t1);
+                e = wg_excl_scan2<NT, true>(p0, p1, m.w2, &t0, &t1);
             } else {
-                e.x = wg_excl_scan<NT>(p0, m.w, &t0);
+                e.x = wg_excl_scan<NT, true>(p0, m.w, &t0);
                 e.y = 0u;
             }
             uint32_t base = 0;
@@ -402,19 +425,21 @@ __device__ __forceinline__ uint32_t merge_levels(MLds<C>& m, uint32_t PT, uint32
                 base += (tw >> sh) & 0xFFFFu;
             }
         }
+        // node runs start where their first unit's outputs do; node sizes
+        // add up; the next level's counters (the previous level's sizes,
+        // read by now) are cleared
 #pragma unroll
         for (int q = 0; q < UPT; ++q) {
-            const uint32_t u = (uint32_t)q * NT + tid;
-            if (u < U) {
-                if (u == m.ub[node[q]]) m.nb[node[q]] = xq[q];
+            if ((uint32_t)q * NT + tid < U) {
+                if (first[q]) m.rs[t & 1u][node[q]] = xq[q];
                 if (cnt[q]) atomicAdd(&lc[node[q]], cnt[q]);
             }
         }
-        __syncthreads();
+        if (t < L && tid < (nodes >> 1)) m.lc[(t + 1u) & 1u][tid] = 0u;
 #pragma unroll
         for (int q = 0; q < UPT; ++q) {
             if (!valid[q]) continue;
-            uint32_t p = sa[q] + xq[q] - m.nb[node[q]];  // the node's run starts at its left child's
+            uint32_t p = xq[q];
 #pragma unroll
             for (int s = 0; s < MV; ++s) {
                 if (valid[q] & (1u << s)) {
@@ -424,17 +449,14 @@ __device__ __forceinline__ uint32_t merge_levels(MLds<C>& m, uint32_t PT, uint32
                 }
             }
         }
-        if (tid < nodes) {
-            m.len[tid << t] = lc[tid];
-            m.cnt[node_base + tid] = lc[tid];
-        }
-        // the next level's units from this level's counts (its children)
-        if (tid < 64u && t < L)
-            level_units(t + 1u, [&](uint32_t g) { return lc[2u * g]; }, [&](uint32_t g) { return lc[2u * g + 1u]; });
         node_base += nodes;
         __syncthreads();
     }
-    return m.len[0];
+    // the root (its run starts at 0)
+    const uint32_t root = m.lc[L & 1u][0];
+    if (tid == 0) m.cnt[node_base - 1u] = root;
+    __syncthreads();  // m.cnt whole
+    return root;
 }
 
 // Node t of the P'-slot tree (level order) goes to position o of node_nnz /
