@@ -98,7 +98,7 @@ struct Carve {
 // The reduction covers the index range [lo, lo + N); stream indices lie in it.
 struct ReducePlan {
     uint32_t P, L, PK, T, ntiles, nchunks, tiles_per_chunk, qbits;  // PK: rank class 16/32/64/128/256
-    uint64_t N, lo, thr, sum_nnz;
+    uint64_t N, lo, thr, sum_nnz, max_nnz;
     int speculate_dense;
     int small;  // few slots, every node sparse, few entries: the one-workgroup merge tree
     int seg;    // every node sparse, up to 64 slots: the segmented merge tree

@@ -632,8 +632,11 @@ __global__ void __launch_bounds__(C::NT) k_merge_seg(SArgs a)
     uint32_t ra = 0, rb = 0;  // this slot's entries in the segment: stream positions [ra, rb)
     if (tid < PT) {
         const StreamDesc d = a.tab[tid];
-        ra = a.off[tid * stride + s];
-        rb = a.off[tid * stride + s + 1u];
+        // (offsets clamped to the stream: one that does not ascend leaves
+        // some unwritten)
+        const uint32_t nz = (uint32_t)d.nnz;
+        ra = min(a.off[tid * stride + s], nz);
+        rb = min(a.off[tid * stride + s + 1u], nz);
         if (rb < ra) {  // only for streams that do not ascend: reported, the slot skipped
             atomicOr(a.st.err, 2u);
             rb = ra;

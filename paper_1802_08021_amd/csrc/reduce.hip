@@ -1015,6 +1015,48 @@ __global__ void k_partition(StreamDesc* tab, Blob tb, uint32_t* off, uint32_t P,
     off[gid] = res;
 }
 
+// Per-segment start offsets of every stream by one pass over its entries,
+// for the merge path (whose inputs are few: a pass reads less than the
+// searches wait for), and zeroing of that path's counters; the descriptor
+// table as in k_partition.  Segment s of the range starts at index
+// lo + s segw; for an ascending stream, off[s] = the first position whose
+// index is at least that start, so entry e is the offset of every segment
+// s with k(idx[e - 1]) <= s < k(idx[e]), where k(x) counts the segment
+// starts (of the first nseg) at or below x (k = 0 before the first entry,
+// nseg + 1 past the last).  Grid: x over positions 0..nnz of a stream,
+// y over streams.  A stream that does not ascend leaves some offsets
+// unwritten: the merge path clamps every offset to its stream.
+__global__ void k_partition_pass(StreamDesc* tab, Blob tb, uint32_t* off, uint32_t nseg, uint64_t segw,
+                                 uint64_t lo, uint32_t* zero, uint32_t nzero)
+{
+    constexpr uint32_t W = sizeof(StreamDesc) / 4;  // words per descriptor
+    const uint32_t r = blockIdx.y, e = blockIdx.x * blockDim.x + threadIdx.x;
+    if (r == 0) {
+        if (e < nzero) zero[e] = 0u;
+        if (e < tb.nwords) reinterpret_cast<uint32_t*>(tab)[e] = tb.words[e];
+    }
+    const uint32_t* idx;
+    uint32_t nnz;
+    if (tb.nwords) {  // idx: words 0-1 of the descriptor, nnz: words 8-9
+        idx = reinterpret_cast<const uint32_t*>((uint64_t)tb.words[r * W] | (uint64_t)tb.words[r * W + 1] << 32);
+        nnz = tb.words[r * W + 8];
+    } else {
+        idx = tab[r].idx;
+        nnz = (uint32_t)tab[r].nnz;
+    }
+    if (e > nnz) return;
+    auto k = [&](uint32_t x) -> uint32_t {
+        if ((uint64_t)x < lo) return 0u;
+        const uint64_t d = (uint64_t)x - lo;  // < 2^32
+        const uint64_t q = segw - 1ull >= 0xFFFFFFFFull ? 0ull : (uint64_t)((uint32_t)d / (uint32_t)segw);
+        return (uint32_t)min(q + 1ull, (uint64_t)nseg);
+    };
+    const uint32_t ka = e == 0u ? 0u : k(idx[e - 1u]);
+    const uint32_t kb = e == nnz ? nseg + 1u : k(idx[e]);
+    uint32_t* o = off + (size_t)r * (nseg + 1u);
+    for (uint32_t s = ka; s < kb; ++s) o[s] = e;
+}
+
 // Switch rule over the tree (§5.1): node dense iff a child is dense or the
 // children's nnz sum exceeds thr; a sparse node's nnz is its union size.
 // Nodes are reported in level order; only the first nfold nodes of level
@@ -1246,6 +1288,7 @@ int reduce_plan(int P, uint64_t N, uint64_t max_nnz, uint64_t sum_nnz, double de
     const double t = std::floor(delta * (double)N);
     p.thr = t >= 18446744073709551615.0 ? UINT64_MAX : (uint64_t)t;
     p.sum_nnz = sum_nnz;
+    p.max_nnz = max_nnz;
     p.qbits = (uint32_t)qbits;
     p.speculate_dense = sum_nnz > p.thr ? 1 : 0;
     p.small = merge_small_fits(p.P, sum_nnz, p.thr) ? 1 : 0;
@@ -1291,15 +1334,21 @@ hipError_t reduce_run(const ReducePlan& p, const StreamDesc* host_tab, uint32_t*
     } else if ((e = upload(l.tab, host_tab, tab_bytes, s)) != hipSuccess) {
         return e;
     }
-    // offsets of every stream at the tile pass's chunks or the merge path's
-    // segments, and that path's counters cleared
-    const uint32_t nparts = p.seg ? p.nseg : p.nchunks;
-    const uint64_t part_coords = p.seg ? p.segw : (uint64_t)p.tiles_per_chunk * p.T;
-    const uint32_t nzero = p.seg ? kSegStateWords + 2u * p.nseg : p.P + 1u;
-    const uint32_t nthreads =
-        std::max<uint32_t>(std::max<uint32_t>(p.P * (nparts + 1), nzero), tb.nwords);
-    hipLaunchKernelGGL(k_partition, dim3((nthreads + 255) / 256), dim3(256), 0, s, l.tab, tb, l.off,
-                       p.P, nparts, part_coords, p.lo, p.N, l.zero, nzero);
+    // offsets of every stream at the tile pass's chunks (searches) or the
+    // merge path's segments (one pass over the entries), and that path's
+    // counters cleared
+    if (p.seg) {
+        const uint32_t nzero = kSegStateWords + 2u * p.nseg;
+        const uint64_t nthreads = std::max<uint64_t>(p.max_nnz + 1u, std::max<uint32_t>(nzero, tb.nwords));
+        hipLaunchKernelGGL(k_partition_pass, dim3((uint32_t)((nthreads + 255) / 256), p.P), dim3(256), 0, s, l.tab,
+                           tb, l.off, p.nseg, p.segw, p.lo, l.zero, nzero);
+    } else {
+        const uint32_t nzero = p.P + 1u;
+        const uint32_t nthreads =
+            std::max<uint32_t>(std::max<uint32_t>(p.P * (p.nchunks + 1), nzero), tb.nwords);
+        hipLaunchKernelGGL(k_partition, dim3((nthreads + 255) / 256), dim3(256), 0, s, l.tab, tb, l.off, p.P,
+                           p.nchunks, (uint64_t)p.tiles_per_chunk * p.T, p.lo, p.N, l.zero, nzero);
+    }
     if ((e = hipGetLastError()) != hipSuccess) return e;
 
     if (p.seg) {
