@@ -25,6 +25,18 @@ struct Blob {
 };
 hipError_t upload(void* dst, const void* src, size_t bytes, hipStream_t s);
 
+// A reduce's stream descriptors as kernel arguments: whole descriptors (12
+// words a stream, up to 64 streams), or 5 words a stream {idx, values or
+// codes, nnz} (up to 153 streams) whose level units, for codes, are read
+// at scale0 + r; kDescNone: the table was uploaded.
+enum DescFmt : uint32_t { kDescNone = 0, kDescFull = 1, kDescValues = 2, kDescCodes = 3 };
+struct DescArgs {
+    uint32_t nwords;
+    uint32_t fmt;
+    const float* scale0;
+    uint32_t words[kBlobWords];
+};
+
 // Optional kernel timing (see sparcml_timing_enable): HIP events recorded
 // on the launch stream around the main kernels of each call.
 enum TimerSlot {

@@ -23,6 +23,23 @@ struct QDesc {
     uint64_t n;
 };
 
+// Stream r's descriptor: from the launch's arguments (ARGS: six words a
+// stream, val, q and n; no dequantized copy), else from the uploaded table.
+// A template parameter, not a branch: a descriptor read from either place
+// becomes one generic (vector) load of its fields.
+template <bool ARGS>
+__device__ __forceinline__ QDesc qdesc(const QDesc* tab, const Blob& tb, uint32_t r)
+{
+    if (!ARGS) return tab[r];
+    const uint32_t* w = tb.words + 6u * r;
+    QDesc d;
+    d.val = reinterpret_cast<const float*>((uint64_t)w[0] | (uint64_t)w[1] << 32);
+    d.q = reinterpret_cast<uint8_t*>((uint64_t)w[2] | (uint64_t)w[3] << 32);
+    d.deq = nullptr;
+    d.n = (uint64_t)w[4] | (uint64_t)w[5] << 32;
+    return d;
+}
+
 __device__ __forceinline__ double butterfly_sum(double v, int width)
 {
     for (int o = 1; o < width; o <<= 1) v = v + __shfl_xor(v, o);
@@ -30,18 +47,22 @@ __device__ __forceinline__ double butterfly_sum(double v, int width)
 }
 
 // partial[r][b] = tree sum of v^2 over elements [b*kSeg, (b+1)*kSeg) of
-// stream r (zeros past the end).  A wave covers 2048 consecutive elements
+// stream r (zeros past the end); with one block a stream (scale non-null)
+// that is the norm^2, and scale[r] = its square root.  A wave covers 2048 consecutive elements
 // in eight steps of 256: each lane squares four consecutive elements and
 // adds them pairwise, a lane butterfly joins the 64 lanes' subtrees, and the
 // eight step sums are joined pairwise at the end -- the same adjacent-pair
 // tree, with the eight independent butterflies in flight together.
-__global__ void __launch_bounds__(256) k_sumsq_partial(const QDesc* tab, double* partial, uint32_t Q)
+template <bool ARGS>
+__global__ void __launch_bounds__(256) k_sumsq_partial(const QDesc* tab, Blob tb, double* partial, uint32_t Q,
+                                                       float* scale)
 {
     __shared__ double s_w[4];
     const uint32_t r = blockIdx.y, b = blockIdx.x;
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-    const float* v = tab[r].val;
-    const uint64_t n = tab[r].n;
+    const QDesc d = qdesc<ARGS>(tab, tb, r);
+    const float* v = d.val;
+    const uint64_t n = d.n;
     const uint64_t base = (uint64_t)b * kSeg + (uint64_t)wv * 2048;
     const bool vec = (reinterpret_cast<uintptr_t>(v) & 15u) == 0;
     double part[8];
@@ -64,12 +85,18 @@ __global__ void __launch_bounds__(256) k_sumsq_partial(const QDesc* tab, double*
     const double w = ((part[0] + part[1]) + (part[2] + part[3])) + ((part[4] + part[5]) + (part[6] + part[7]));
     if (lane == 0) s_w[wv] = w;
     __syncthreads();
-    if (threadIdx.x == 0) partial[(uint64_t)r * Q + b] = (s_w[0] + s_w[1]) + (s_w[2] + s_w[3]);
+    if (threadIdx.x == 0) {
+        const double t = (s_w[0] + s_w[1]) + (s_w[2] + s_w[3]);
+        partial[(uint64_t)r * Q + b] = t;
+        if (scale) scale[r] = (float)sqrt(t);
+    }
 }
 
-// out[r][b] = tree sum of in[r][b*1024 .. b*1024+1024) (zeros past count).
+// out[r][b] = tree sum of in[r][b*1024 .. b*1024+1024) (zeros past count);
+// at the last level (scale non-null, one block a stream) also scale[r] =
+// the square root of the norm^2.
 __global__ void __launch_bounds__(1024) k_sum_f64(const double* in, uint32_t count, double* out,
-                                                  uint32_t out_count)
+                                                  uint32_t out_count, float* scale)
 {
     __shared__ double s_w[16];
     const uint32_t r = blockIdx.y, b = blockIdx.x;
@@ -85,13 +112,8 @@ __global__ void __launch_bounds__(1024) k_sum_f64(const double* in, uint32_t cou
         for (int width = 16; width > 1; width >>= 1)
             for (int i = 0; i < width / 2; ++i) t[i] = t[2 * i] + t[2 * i + 1];
         out[(uint64_t)r * out_count + b] = t[0];
+        if (scale) scale[r] = (float)sqrt(t[0]);
     }
-}
-
-__global__ void k_scale(const double* norm2, float* scale, uint32_t P)
-{
-    const uint32_t r = blockIdx.x * blockDim.x + threadIdx.x;
-    if (r < P) scale[r] = (float)sqrt(norm2[r]);
 }
 
 // Philox4x32-10 (Salmon et al., SC'11): ten rounds of two 32x32->64
@@ -117,14 +139,14 @@ __device__ __forceinline__ uint4 philox(uint4 c, uint32_t k0, uint32_t k1)
 
 // Each thread quantizes 32/bits consecutive elements into one 32-bit word
 // of codes (4 elements per Philox block).
-template <int BITS>
-__global__ void __launch_bounds__(256) k_quantize(const QDesc* tab, const float* scales, uint32_t k0,
+template <int BITS, bool ARGS>
+__global__ void __launch_bounds__(256) k_quantize(const QDesc* tab, Blob tb, const float* scales, uint32_t k0,
                                                   uint32_t k1)
 {
     constexpr int EPT = 32 / BITS;
     constexpr uint32_t S = (1u << (BITS - 1)) - 1u;
     const uint32_t r = blockIdx.y;
-    const QDesc d = tab[r];
+    const QDesc d = qdesc<ARGS>(tab, tb, r);
     const uint64_t e0 = ((uint64_t)blockIdx.x * 256 + threadIdx.x) * EPT;
     if (e0 >= d.n) return;
     const float scale = scales[r];
@@ -374,31 +396,60 @@ hipError_t quant_run(int P, const float* const* vals, const uint64_t* n, int bit
     uint64_t max_n = 0;
     for (int r = 0; r < P; ++r) max_n = std::max(max_n, n[r]);
     const QLayout l = qlayout(P, max_n, ws);
-    QDesc* host = new QDesc[P];
-    for (int r = 0; r < P; ++r)
-        host[r] = QDesc{vals[r], out_q[r], out_deq ? out_deq[r] : nullptr, n[r]};
-    hipError_t e = upload(l.tab, host, sizeof(QDesc) * P, s);
-    delete[] host;
-    if (e != hipSuccess) return e;
+    // the descriptor table: in both launches' arguments when it fits there
+    // (no dequantized copies), else uploaded first
+    Blob tb;
+    tb.nwords = 0;
+    hipError_t e = hipSuccess;
+    if (!out_deq && 6u * (uint32_t)P <= (uint32_t)kBlobWords) {
+        tb.nwords = 6u * (uint32_t)P;
+        for (int r = 0; r < P; ++r) {
+            const uint64_t a = reinterpret_cast<uint64_t>(vals[r]), b = reinterpret_cast<uint64_t>(out_q[r]);
+            uint32_t* w = tb.words + 6 * r;
+            w[0] = (uint32_t)a;
+            w[1] = (uint32_t)(a >> 32);
+            w[2] = (uint32_t)b;
+            w[3] = (uint32_t)(b >> 32);
+            w[4] = (uint32_t)n[r];
+            w[5] = (uint32_t)(n[r] >> 32);
+        }
+    } else {
+        QDesc* host = new QDesc[P];
+        for (int r = 0; r < P; ++r)
+            host[r] = QDesc{vals[r], out_q[r], out_deq ? out_deq[r] : nullptr, n[r]};
+        e = upload(l.tab, host, sizeof(QDesc) * P, s);
+        delete[] host;
+        if (e != hipSuccess) return e;
+    }
 
+    // norms; the launch that finishes a stream's norm also writes its scale
     timer_begin(kTQuantNorm, s);
-    hipLaunchKernelGGL(k_sumsq_partial, dim3(l.count[0], P), dim3(256), 0, s, l.tab, l.part[0],
-                       l.count[0]);
+    float* const scale0 = l.levels == 0 ? out_scale : nullptr;
+    if (tb.nwords)
+        hipLaunchKernelGGL(k_sumsq_partial<true>, dim3(l.count[0], P), dim3(256), 0, s, l.tab, tb, l.part[0],
+                           l.count[0], scale0);
+    else
+        hipLaunchKernelGGL(k_sumsq_partial<false>, dim3(l.count[0], P), dim3(256), 0, s, l.tab, tb, l.part[0],
+                           l.count[0], scale0);
     timer_end(kTQuantNorm, s);
     for (int lv = 1; lv <= l.levels; ++lv)
         hipLaunchKernelGGL(k_sum_f64, dim3(l.count[lv], P), dim3(1024), 0, s, l.part[lv - 1],
-                           l.count[lv - 1], l.part[lv], l.count[lv]);
-    hipLaunchKernelGGL(k_scale, dim3((P + 255) / 256), dim3(256), 0, s, l.norm2, out_scale,
-                       (uint32_t)P);
+                           l.count[lv - 1], l.part[lv], l.count[lv], lv == l.levels ? out_scale : nullptr);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (max_n == 0) return hipSuccess;
     const uint32_t k0 = (uint32_t)(seed & 0xFFFFFFFFu), k1 = (uint32_t)(seed >> 32);
     const uint64_t per_block = 256ull * (32 / bits);
     const dim3 grid((uint32_t)((max_n + per_block - 1) / per_block), P);
     timer_begin(kTQuantCodes, s);
-    if (bits == 2) hipLaunchKernelGGL(k_quantize<2>, grid, dim3(256), 0, s, l.tab, out_scale, k0, k1);
-    else if (bits == 4) hipLaunchKernelGGL(k_quantize<4>, grid, dim3(256), 0, s, l.tab, out_scale, k0, k1);
-    else hipLaunchKernelGGL(k_quantize<8>, grid, dim3(256), 0, s, l.tab, out_scale, k0, k1);
+    if (tb.nwords) {
+        if (bits == 2) hipLaunchKernelGGL((k_quantize<2, true>), grid, dim3(256), 0, s, l.tab, tb, out_scale, k0, k1);
+        else if (bits == 4) hipLaunchKernelGGL((k_quantize<4, true>), grid, dim3(256), 0, s, l.tab, tb, out_scale, k0, k1);
+        else hipLaunchKernelGGL((k_quantize<8, true>), grid, dim3(256), 0, s, l.tab, tb, out_scale, k0, k1);
+    } else {
+        if (bits == 2) hipLaunchKernelGGL((k_quantize<2, false>), grid, dim3(256), 0, s, l.tab, tb, out_scale, k0, k1);
+        else if (bits == 4) hipLaunchKernelGGL((k_quantize<4, false>), grid, dim3(256), 0, s, l.tab, tb, out_scale, k0, k1);
+        else hipLaunchKernelGGL((k_quantize<8, false>), grid, dim3(256), 0, s, l.tab, tb, out_scale, k0, k1);
+    }
     timer_end(kTQuantCodes, s);
     return hipGetLastError();
 }

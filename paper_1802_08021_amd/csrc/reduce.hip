@@ -984,28 +984,55 @@ __global__ void __launch_bounds__(kSlowNT) k_slow(Args a)
 }
 
 // ------------------------------------------------------------------------
+// Stream r's descriptor from the launch's arguments (fmt != kDescNone).
+static_assert(sizeof(StreamDesc) == 48 && offsetof(StreamDesc, idx) == 0 && offsetof(StreamDesc, val) == 8 &&
+                  offsetof(StreamDesc, qval) == 16 && offsetof(StreamDesc, qscale) == 24 &&
+                  offsetof(StreamDesc, nnz) == 32,
+              "descriptor words");
+__device__ __forceinline__ StreamDesc arg_desc(const DescArgs& tb, uint32_t r)
+{
+    auto word2 = [&](uint32_t i) -> uint64_t { return (uint64_t)tb.words[i] | (uint64_t)tb.words[i + 1] << 32; };
+    StreamDesc d{};
+    if (tb.fmt == kDescFull) {
+        const uint32_t b = r * (uint32_t)(sizeof(StreamDesc) / 4);
+        d.idx = reinterpret_cast<const uint32_t*>(word2(b));
+        d.val = reinterpret_cast<const float*>(word2(b + 2u));
+        d.qval = reinterpret_cast<const uint8_t*>(word2(b + 4u));
+        d.qscale = reinterpret_cast<const float*>(word2(b + 6u));
+        d.nnz = word2(b + 8u);
+    } else {
+        const uint32_t b = r * 5u;
+        d.idx = reinterpret_cast<const uint32_t*>(word2(b));
+        if (tb.fmt == kDescCodes) {
+            d.qval = reinterpret_cast<const uint8_t*>(word2(b + 2u));
+            d.qscale = tb.scale0 + r;
+        } else {
+            d.val = reinterpret_cast<const float*>(word2(b + 2u));
+        }
+        d.nnz = tb.words[b + 4u];
+    }
+    return d;
+}
+
 // Per-chunk start offsets of every stream (binary search) and zeroing of the
-// counters the passes accumulate into.
-// When the descriptor table travels in the arguments (tb.nwords > 0, up to
-// kBlobWords / 12 streams) this launch also stores it to `tab` for the later
-// passes, and reads its own descriptors from the arguments.
-static_assert(sizeof(StreamDesc) == 48 && offsetof(StreamDesc, idx) == 0 && offsetof(StreamDesc, nnz) == 32,
-              "descriptor words read by k_partition");
-__global__ void k_partition(StreamDesc* tab, Blob tb, uint32_t* off, uint32_t P, uint32_t nchunks,
+// counters the passes accumulate into.  When the descriptors travel in the
+// arguments this launch also stores them to `tab` for the later passes (its
+// first P threads), and reads its own from the arguments.
+__global__ void k_partition(StreamDesc* tab, DescArgs tb, uint32_t* off, uint32_t P, uint32_t nchunks,
                             uint64_t chunk_coords, uint64_t lo, uint64_t N, uint32_t* zero, uint32_t nzero)
 {
-    constexpr uint32_t W = sizeof(StreamDesc) / 4;  // words per descriptor
     const uint32_t gid = blockIdx.x * blockDim.x + threadIdx.x;
     if (gid < nzero) zero[gid] = 0u;
-    if (gid < tb.nwords) reinterpret_cast<uint32_t*>(tab)[gid] = tb.words[gid];
+    if (tb.fmt != kDescNone && gid < P) tab[gid] = arg_desc(tb, gid);
     const uint32_t stride = nchunks + 1;
     if (gid >= P * stride) return;
     const uint32_t r = gid / stride, c = gid % stride;
     const uint32_t* idx;
     uint32_t nnz;
-    if (tb.nwords) {  // idx: words 0-1 of the descriptor, nnz: words 8-9
-        idx = reinterpret_cast<const uint32_t*>((uint64_t)tb.words[r * W] | (uint64_t)tb.words[r * W + 1] << 32);
-        nnz = tb.words[r * W + 8];
+    if (tb.fmt != kDescNone) {
+        const StreamDesc d = arg_desc(tb, r);
+        idx = d.idx;
+        nnz = (uint32_t)d.nnz;
     } else {
         idx = tab[r].idx;
         nnz = (uint32_t)tab[r].nnz;
@@ -1026,20 +1053,20 @@ __global__ void k_partition(StreamDesc* tab, Blob tb, uint32_t* off, uint32_t P,
 // nseg + 1 past the last).  Grid: x over positions 0..nnz of a stream,
 // y over streams.  A stream that does not ascend leaves some offsets
 // unwritten: the merge path clamps every offset to its stream.
-__global__ void k_partition_pass(StreamDesc* tab, Blob tb, uint32_t* off, uint32_t nseg, uint64_t segw,
+__global__ void k_partition_pass(StreamDesc* tab, DescArgs tb, uint32_t* off, uint32_t nseg, uint64_t segw,
                                  uint64_t lo, uint32_t* zero, uint32_t nzero)
 {
-    constexpr uint32_t W = sizeof(StreamDesc) / 4;  // words per descriptor
     const uint32_t r = blockIdx.y, e = blockIdx.x * blockDim.x + threadIdx.x;
     if (r == 0) {
         if (e < nzero) zero[e] = 0u;
-        if (e < tb.nwords) reinterpret_cast<uint32_t*>(tab)[e] = tb.words[e];
+        if (tb.fmt != kDescNone && e < gridDim.y) tab[e] = arg_desc(tb, e);
     }
     const uint32_t* idx;
     uint32_t nnz;
-    if (tb.nwords) {  // idx: words 0-1 of the descriptor, nnz: words 8-9
-        idx = reinterpret_cast<const uint32_t*>((uint64_t)tb.words[r * W] | (uint64_t)tb.words[r * W + 1] << 32);
-        nnz = tb.words[r * W + 8];
+    if (tb.fmt != kDescNone) {
+        const StreamDesc d = arg_desc(tb, r);
+        idx = d.idx;
+        nnz = (uint32_t)d.nnz;
     } else {
         idx = tab[r].idx;
         nnz = (uint32_t)tab[r].nnz;
@@ -1324,13 +1351,34 @@ hipError_t reduce_run(const ReducePlan& p, const StreamDesc* host_tab, uint32_t*
         return hipStreamSynchronize(s);
     }
     // the descriptor table: in the partition launch's arguments when it fits
-    // there, else uploaded first
+    // there (whole, or 5 words a stream when every stream's level unit
+    // follows the previous one's), else uploaded first
     const size_t tab_bytes = sizeof(StreamDesc) * p.P;
-    Blob tb;
+    DescArgs tb;
     tb.nwords = 0;
+    tb.fmt = kDescNone;
+    tb.scale0 = nullptr;
+    bool scales_follow = true;
+    for (uint32_t r = 1; r < p.P && scales_follow; ++r) scales_follow = host_tab[r].qscale == host_tab[0].qscale + r;
     if (tab_bytes <= sizeof(tb.words)) {
+        tb.fmt = kDescFull;
         tb.nwords = (uint32_t)(tab_bytes / 4);
         memcpy(tb.words, host_tab, tab_bytes);
+    } else if (5u * p.P <= (uint32_t)kBlobWords && (!p.qbits || scales_follow)) {
+        tb.fmt = p.qbits ? kDescCodes : kDescValues;
+        tb.nwords = 5u * p.P;
+        tb.scale0 = host_tab[0].qscale;
+        for (uint32_t r = 0; r < p.P; ++r) {
+            const uint64_t a = reinterpret_cast<uint64_t>(host_tab[r].idx);
+            const uint64_t b = reinterpret_cast<uint64_t>(p.qbits ? static_cast<const void*>(host_tab[r].qval)
+                                                                  : static_cast<const void*>(host_tab[r].val));
+            uint32_t* w = tb.words + 5u * r;
+            w[0] = (uint32_t)a;
+            w[1] = (uint32_t)(a >> 32);
+            w[2] = (uint32_t)b;
+            w[3] = (uint32_t)(b >> 32);
+            w[4] = (uint32_t)host_tab[r].nnz;
+        }
     } else if ((e = upload(l.tab, host_tab, tab_bytes, s)) != hipSuccess) {
         return e;
     }
@@ -1339,13 +1387,13 @@ hipError_t reduce_run(const ReducePlan& p, const StreamDesc* host_tab, uint32_t*
     // counters cleared
     if (p.seg) {
         const uint32_t nzero = kSegStateWords + 2u * p.nseg;
-        const uint64_t nthreads = std::max<uint64_t>(p.max_nnz + 1u, std::max<uint32_t>(nzero, tb.nwords));
+        const uint64_t nthreads = std::max<uint64_t>(p.max_nnz + 1u, std::max<uint32_t>(nzero, p.P));
         hipLaunchKernelGGL(k_partition_pass, dim3((uint32_t)((nthreads + 255) / 256), p.P), dim3(256), 0, s, l.tab,
                            tb, l.off, p.nseg, p.segw, p.lo, l.zero, nzero);
     } else {
         const uint32_t nzero = p.P + 1u;
         const uint32_t nthreads =
-            std::max<uint32_t>(std::max<uint32_t>(p.P * (p.nchunks + 1), nzero), tb.nwords);
+            std::max<uint32_t>(p.P * (p.nchunks + 1), nzero);
         hipLaunchKernelGGL(k_partition, dim3((nthreads + 255) / 256), dim3(256), 0, s, l.tab, tb, l.off, p.P,
                            p.nchunks, (uint64_t)p.tiles_per_chunk * p.T, p.lo, p.N, l.zero, nzero);
     }
