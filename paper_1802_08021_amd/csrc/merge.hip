@@ -626,12 +626,19 @@ __global__ void __launch_bounds__(C::NT) k_merge_seg(SArgs a)
     __shared__ uint64_t s_lo[40], s_hi[40];  // pieces still to do (a stack)
     __shared__ uint32_t s_depth, s_fits;
     const uint32_t tid = threadIdx.x, PT = a.PT;
+    // the slot's descriptor (and level unit) are read while the ticket is
+    // taken
+    StreamDesc d{};
+    float unit = 0.0f;
+    if (tid < PT) {
+        d = a.tab[tid];
+        if (QUANT && d.nnz) unit = level_unit(*d.qscale, a.qbits);
+    }
     if (tid == 0) s_seg = atomicAdd(a.st.ticket, 1u);
     __syncthreads();
     const uint32_t s = s_seg, stride = a.nseg + 1u;
     uint32_t ra = 0, rb = 0;  // this slot's entries in the segment: stream positions [ra, rb)
     if (tid < PT) {
-        const StreamDesc d = a.tab[tid];
         // (offsets clamped to the stream: one that does not ascend leaves
         // some unwritten)
         const uint32_t nz = (uint32_t)d.nnz;
@@ -644,7 +651,7 @@ __global__ void __launch_bounds__(C::NT) k_merge_seg(SArgs a)
         m.pi[tid] = d.idx;
         m.pv[tid] = QUANT ? static_cast<const void*>(d.qval) : static_cast<const void*>(d.val);
         m.first[tid] = ra;
-        if (QUANT) m.unit[tid] = d.nnz ? level_unit(*d.qscale, a.qbits) : 0.0f;
+        if (QUANT) m.unit[tid] = unit;
     }
     if (tid < kMSlots - 1u) s_acc[tid] = 0u;
     const uint32_t total = slot_starts(m, PT, rb - ra);
