@@ -123,13 +123,24 @@ def test_topk_sampled_gather_bin_paths():
         np.testing.assert_array_equal(gr.view(np.uint32), orr.view(np.uint32))
 
 
-def gpu_quantize(vals, bits, seed):
+def gpu_quantize(vals, bits, seed, want_deq=True):
     from paper_1802_08021_amd import sparcml as S
     torch, dev = torch_dev()
     tv = [to_dev(v if v.size else np.zeros(0, np.float32)) for v in vals]
-    codes, scale, deq = S.quantize(tv, bits, seed, want_deq=True)
+    codes, scale, deq = S.quantize(tv, bits, seed, want_deq=want_deq)
     torch.cuda.synchronize()
-    return [to_np(c) for c in codes], to_np(scale), [to_np(d) for d in deq]
+    return [to_np(c) for c in codes], to_np(scale), [to_np(d) for d in deq] if want_deq else None
+
+
+def assert_quant_equal(g, o, P, label):
+    gq, gs, gd = g
+    oq, os_, od = o
+    np.testing.assert_array_equal(gs.view(np.uint32), os_.view(np.uint32), err_msg=f"{label}: scales")
+    for r in range(P):
+        np.testing.assert_array_equal(gq[r], oq[r], err_msg=f"{label}: codes of stream {r}")
+        if gd is not None:
+            np.testing.assert_array_equal(gd[r].view(np.uint32), od[r].view(np.uint32),
+                                          err_msg=f"{label}: dequantized stream {r}")
 
 
 @pytest.mark.parametrize("bits", [2, 4, 8])
@@ -140,14 +151,25 @@ def test_quantize_parity(bits):
     vals.append(np.zeros(77, np.float32))
     vals.append(np.float32(3.0) * np.ones(5, np.float32))
     seed = 0xDEADBEEF_12345678 + bits
-    say(f"[quant] bits={bits} streams={len(vals)}")
-    oq, os_, od = oracle.quantize(vals, bits, seed)
-    gq, gs, gd = gpu_quantize(vals, bits, seed)
-    np.testing.assert_array_equal(gs.view(np.uint32), os_.view(np.uint32))
-    for r in range(len(vals)):
-        np.testing.assert_array_equal(gq[r], oq[r], err_msg=f"codes of stream {r}")
-        np.testing.assert_array_equal(gd[r].view(np.uint32), od[r].view(np.uint32),
-                                      err_msg=f"dequantized stream {r}")
+    o = oracle.quantize(vals, bits, seed)
+    # with dequantized copies the table is uploaded; without, it travels in
+    # the kernels' arguments
+    for want_deq in (True, False):
+        say(f"[quant] bits={bits} streams={len(vals)} deq={want_deq}")
+        g = gpu_quantize(vals, bits, seed, want_deq)
+        assert_quant_equal(g, o, len(vals), f"deq={want_deq}")
+
+
+def test_quantize_long_stream():
+    # 2^23 + 5 entries: more than 1024 partial norms, so the partials' tree
+    # takes two summing launches
+    rng = np.random.default_rng(77)
+    vals = [inputs.laplace(rng, 1e-2, (1 << 23) + 5), inputs.laplace(rng, 1e-2, 3000)]
+    seed = 0x0123456789ABCDEF
+    say("[quant] long stream")
+    o = oracle.quantize(vals, 4, seed)
+    g = gpu_quantize(vals, 4, seed, want_deq=False)
+    assert_quant_equal(g, o, len(vals), "long stream")
 
 
 def test_quantize_config5_scaled():
@@ -155,12 +177,10 @@ def test_quantize_config5_scaled():
     d = inputs.generate(c, seed=0)
     seed = inputs.quant_seed(0, 5)
     say(f"[quant] c5/32 P={c.P} k={c.k}")
-    oq, os_, od = oracle.quantize(d["val"], 4, seed)
-    gq, gs, gd = gpu_quantize(d["val"], 4, seed)
-    np.testing.assert_array_equal(gs.view(np.uint32), os_.view(np.uint32))
-    for r in range(c.P):
-        np.testing.assert_array_equal(gq[r], oq[r])
-        np.testing.assert_array_equal(gd[r].view(np.uint32), od[r].view(np.uint32))
+    o = oracle.quantize(d["val"], 4, seed)
+    for want_deq in (True, False):
+        g = gpu_quantize(d["val"], 4, seed, want_deq)
+        assert_quant_equal(g, o, c.P, f"c5/32, deq={want_deq}")
 
 
 def test_densify_parity():
