@@ -9,16 +9,17 @@
 //
 //  * the slot streams' entries in the range are loaded side by side into LDS
 //    (QSGD codes dequantized on the way in), slot s at run start S[s];
-//  * level t merges, for every node g at once, its two children -- the runs
-//    at S[g * 2^t] and S[g * 2^t + 2^(t-1)] -- into the node's run at
-//    S[g * 2^t]: an index present in both children gets left + right;
+//  * level t merges, for every node g at once, its two children (the slots'
+//    runs at level 1, else the runs of level t-1's nodes 2g and 2g+1) into
+//    the node's run: an index present in both children gets left + right;
 //  * the merge is cut into units of MV merged positions (merge path: the
 //    split of a unit's first position between the two children is found by
 //    binary search); a unit's outputs stay in registers until every unit has
 //    read its inputs, so the level is merged in place;
 //  * per-unit output counts, scanned across the workgroup, give the output
-//    positions; per-node counts are the nodes' union sizes (what the switch
-//    rule reports per node).
+//    positions: a level's node runs lie one after another in node order;
+//    per-node counts are the nodes' union sizes (what the switch rule
+//    reports per node).
 //
 // Two kernels use it.  k_merge_small: one workgroup takes the whole range
 // (one launch, the slot table in the kernel arguments).  A level costs about
