@@ -1014,32 +1014,57 @@ __device__ __forceinline__ StreamDesc arg_desc(const DescArgs& tb, uint32_t r)
     return d;
 }
 
-// Per-chunk start offsets of every stream (binary search) and zeroing of the
-// counters the passes accumulate into.  When the descriptors travel in the
-// arguments this launch also stores them to `tab` for the later passes (its
-// first P threads), and reads its own from the arguments.
-__global__ void k_partition(StreamDesc* tab, DescArgs tb, uint32_t* off, uint32_t P, uint32_t nchunks,
-                            uint64_t chunk_coords, uint64_t lo, uint64_t N, uint32_t* zero, uint32_t nzero)
+// Per-chunk start offsets of every stream and zeroing of the counters the
+// passes accumulate into; workgroup r takes stream r.  A sample of the
+// stream (every stride-th index, at most kPartSamples, read at once) narrows
+// each chunk start's search to one stride of positions, so a search waits on
+// about half the dependent loads of a binary search over the whole stream.
+// When the descriptors travel in the arguments this launch also stores them
+// to `tab` for the later passes, and reads its own from the arguments.
+constexpr uint32_t kPartSamples = 1024;
+__global__ void __launch_bounds__(256) k_partition(StreamDesc* tab, DescArgs tb, uint32_t* off, uint32_t nchunks,
+                                                   uint64_t chunk_coords, uint64_t lo, uint64_t N, uint32_t* zero,
+                                                   uint32_t nzero)
 {
-    const uint32_t gid = blockIdx.x * blockDim.x + threadIdx.x;
-    if (gid < nzero) zero[gid] = 0u;
-    if (tb.fmt != kDescNone && gid < P) tab[gid] = arg_desc(tb, gid);
-    const uint32_t stride = nchunks + 1;
-    if (gid >= P * stride) return;
-    const uint32_t r = gid / stride, c = gid % stride;
+    __shared__ uint32_t s_smp[kPartSamples];
+    const uint32_t r = blockIdx.x, tid = threadIdx.x;
+    if (r == 0)
+        for (uint32_t i = tid; i < nzero; i += blockDim.x) zero[i] = 0u;
     const uint32_t* idx;
     uint32_t nnz;
     if (tb.fmt != kDescNone) {
         const StreamDesc d = arg_desc(tb, r);
+        if (tid == 0) tab[r] = d;
         idx = d.idx;
         nnz = (uint32_t)d.nnz;
     } else {
         idx = tab[r].idx;
         nnz = (uint32_t)tab[r].nnz;
     }
-    uint32_t res = nnz;
-    if (c < nchunks) res = lower_bound(idx, 0u, nnz, lo + min((uint64_t)c * chunk_coords, N));
-    off[gid] = res;
+    // samples j < ns: the index at position j * stride
+    const uint32_t stride = nnz > kPartSamples ? (uint32_t)(((uint64_t)nnz + kPartSamples - 1u) / kPartSamples) : 1u;
+    const uint32_t ns = (uint32_t)(((uint64_t)nnz + stride - 1u) / stride);
+    for (uint32_t j = tid; j < ns; j += blockDim.x) s_smp[j] = idx[(uint64_t)j * stride];
+    __syncthreads();
+    uint32_t* const o = off + (uint64_t)r * (nchunks + 1u);
+    for (uint32_t c = tid; c <= nchunks; c += blockDim.x) {
+        uint32_t res = nnz;
+        if (c < nchunks) {
+            const uint64_t x = lo + min((uint64_t)c * chunk_coords, N);
+            // js samples lie below x: the first position at or past x is
+            // above sample js - 1's and at most sample js's
+            uint32_t a = 0u, b = ns;
+            while (a < b) {
+                const uint32_t m = a + ((b - a) >> 1);
+                if ((uint64_t)s_smp[m] < x) a = m + 1u;
+                else b = m;
+            }
+            const uint32_t pa = a ? (a - 1u) * stride + 1u : 0u;
+            const uint32_t pb = (uint32_t)min((uint64_t)a * stride, (uint64_t)nnz);
+            res = lower_bound(idx, min(pa, pb), pb, x);
+        }
+        o[c] = res;
+    }
 }
 
 // Per-segment start offsets of every stream by one pass over its entries,
@@ -1392,10 +1417,8 @@ hipError_t reduce_run(const ReducePlan& p, const StreamDesc* host_tab, uint32_t*
                            tb, l.off, p.nseg, p.segw, p.lo, l.zero, nzero);
     } else {
         const uint32_t nzero = p.P + 1u;
-        const uint32_t nthreads =
-            std::max<uint32_t>(p.P * (p.nchunks + 1), nzero);
-        hipLaunchKernelGGL(k_partition, dim3((nthreads + 255) / 256), dim3(256), 0, s, l.tab, tb, l.off, p.P,
-                           p.nchunks, (uint64_t)p.tiles_per_chunk * p.T, p.lo, p.N, l.zero, nzero);
+        hipLaunchKernelGGL(k_partition, dim3(p.P), dim3(256), 0, s, l.tab, tb, l.off, p.nchunks,
+                           (uint64_t)p.tiles_per_chunk * p.T, p.lo, p.N, l.zero, nzero);
     }
     if ((e = hipGetLastError()) != hipSuccess) return e;
 
