@@ -1,0 +1,82 @@
+"""A seeded random sweep of the sparse reduce against the oracle, across the
+paths the library picks by size (one-workgroup merge tree, segmented merge
+tree, tile pipeline with a sparse or a dense root, deferred tiles) and
+across what the other tests fix one at a time: rank counts that are not
+powers of two, QSGD codes of every width, the range entry point, and index
+sets that are uniform, clustered (heavy overlap between ranks) or runs of
+consecutive indices.  Bar: as for every reduce parity test -- root
+representation, nnz, indices, node decisions and sizes bit-exact, values
+bitwise (assert_reduce_equal)."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_1802_08021_amd import inputs
+from gpu_util import assert_reduce_equal, gpu_reduce, say, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+def _indices(rng, N, k, kind, centers):
+    """k distinct ascending indices below N (fewer if N is small)."""
+    k = min(k, N)
+    if k == 0:
+        return np.zeros(0, np.uint32)
+    if kind == "uniform":
+        return inputs.uniform_subset(rng, N, k)
+    if kind == "runs":  # a few runs of consecutive indices
+        out = set()
+        while len(out) < k:
+            s = int(rng.integers(0, N))
+            out.update(range(s, min(N, s + int(rng.integers(1, 200)))))
+        a = np.array(sorted(out), dtype=np.int64)[:k]
+        return np.sort(a).astype(np.uint32)
+    # clustered: draws around shared centers, so many ranks hit the same indices
+    w = max(1, N // 50)
+    c = centers[rng.integers(0, len(centers), size=4 * k)]
+    a = np.unique(np.clip(c + rng.integers(-w, w + 1, size=4 * k), 0, N - 1))
+    if a.size > k:
+        a = np.sort(rng.choice(a, size=k, replace=False))
+    return a.astype(np.uint32)
+
+
+def _case(rng, case):
+    P = int(rng.choice([1, 2, 3, 5, 8, 13, 16, 31, 33, 48, 64, 65, 100, 128, 129, 200, 256]))
+    N = int(rng.choice([1, 63, 4096, 4097, 50000, 300001]))
+    kind = str(rng.choice(["uniform", "clustered", "runs"]))
+    kmax = int(rng.choice([1, 16, 300, 3000, 20000]))
+    qbits = int(rng.choice([0, 0, 2, 4, 8]))
+    delta = float(10.0 ** rng.uniform(-6, 1))
+    ranged = N > 64 and rng.random() < 0.3
+    centers = rng.integers(0, N, size=int(rng.integers(1, 6)))
+    idx = [_indices(rng, N, int(rng.integers(0, kmax + 1)), kind, centers) for _ in range(P)]
+    lo, hi = 0, N
+    if ranged:
+        lo = int(rng.integers(0, N // 2))
+        hi = int(rng.integers(lo + 1, N + 1))
+        idx = [a[(a >= lo) & (a < hi)] for a in idx]
+    val = [inputs.laplace(rng, 1.0, a.size) for a in idx]
+    label = (f"sweep#{case}: P={P} N={N} {kind} kmax={kmax} q={qbits} delta={delta:.3g}"
+             + (f" range=[{lo},{hi})" if ranged else ""))
+    return P, N, idx, val, qbits, delta, (lo, hi) if ranged else None, label
+
+
+def test_random_sweep():
+    rng = np.random.default_rng(20261202)
+    for case in range(300):
+        P, N, idx, val, qbits, delta, rg, label = _case(rng, case)
+        say(f"[sweep] {label} nnz={sum(a.size for a in idx)}")
+        if qbits:
+            q, scale, deq = oracle.quantize(val, qbits, seed=1000 + case)
+            codes = [to_dev(a if a.size else np.zeros(1, np.uint8)) for a in q]
+            scales = to_dev(scale)
+            vals_o = deq
+        else:
+            codes = scales = None
+            vals_o = val
+        if rg is None:
+            o = oracle.sparse_reduce(idx, vals_o, N, delta)
+        else:
+            o = oracle.sparse_reduce_range(idx, vals_o, N, rg[0], rg[1], delta)
+        g = gpu_reduce(idx, None if qbits else val, N, delta, qbits=qbits, codes=codes, scales=scales, rng=rg)
+        assert_reduce_equal(g, o, label)
