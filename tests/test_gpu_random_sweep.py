@@ -1,12 +1,16 @@
-"""A seeded random sweep of the sparse reduce against the oracle, across the
+"""Seeded random sweeps against the oracle.  The sparse reduce: across the
 paths the library picks by size (one-workgroup merge tree, segmented merge
 tree, tile pipeline with a sparse or a dense root, deferred tiles) and
 across what the other tests fix one at a time: rank counts that are not
 powers of two, QSGD codes of every width, the range entry point, and index
 sets that are uniform, clustered (heavy overlap between ranks) or runs of
-consecutive indices.  Bar: as for every reduce parity test -- root
+consecutive indices; bar as for every reduce parity test -- root
 representation, nnz, indices, node decisions and sizes bit-exact, values
-bitwise (assert_reduce_equal)."""
+bitwise (assert_reduce_equal).  Top-k: row lengths around the kernels'
+block sizes, k from 0 to N, rows of ties across signs and of signed zeros,
+every residual mode; indices, values and residuals bitwise.  QSGD: up to
+139 streams of mixed lengths, every width, with and without dequantized
+copies; codes, scales and dequantized values bitwise."""
 import numpy as np
 import pytest
 
@@ -80,3 +84,70 @@ def test_random_sweep():
             o = oracle.sparse_reduce_range(idx, vals_o, N, rg[0], rg[1], delta)
         g = gpu_reduce(idx, None if qbits else val, N, delta, qbits=qbits, codes=codes, scales=scales, rng=rg)
         assert_reduce_equal(g, o, label)
+
+
+def _row_values(rng, N, kind):
+    """fp32 values of one row: smooth, heavy-tailed, few distinct magnitudes
+    (ties across signs), or mostly zeros (signed)."""
+    if kind == "laplace":
+        return inputs.laplace(rng, 1e-3, N)
+    if kind == "normal":
+        return inputs.normal(rng, N)
+    if kind == "ties":
+        return (rng.choice([-2.0, -0.5, 0.5, 2.0, 0.0, -0.0], size=N)).astype(np.float32)
+    x = np.zeros(N, np.float32)
+    x[rng.random(N) < 0.5] = np.float32(-0.0)
+    m = rng.random(N) < 0.01
+    x[m] = inputs.laplace(rng, 1.0, int(m.sum()))
+    return x
+
+
+def test_random_sweep_topk():
+    import torch
+    from gpu_util import to_np
+    from paper_1802_08021_amd import sparcml as S
+    rng = np.random.default_rng(7042)
+    for case in range(60):
+        P = int(rng.integers(1, 6))
+        N = int(rng.choice([1, 2, 255, 256, 257, 4095, 65536, 65537, 300001]))
+        k = int(min(N, rng.choice([0, 1, 2, 17, N // 100 + 1, N // 7 + 1, N - 1, N])))
+        kinds = [str(rng.choice(["laplace", "normal", "ties", "zeros"])) for _ in range(P)]
+        x = np.stack([_row_values(rng, N, kd) for kd in kinds])
+        residual = str(rng.choice(["none", "copy", "inplace"]))
+        say(f"[sweep topk] #{case}: P={P} N={N} k={k} rows={kinds} residual={residual}")
+        oi, ov, orr = oracle.topk(x, k, residual=residual != "none")
+        tx = to_dev(x)
+        res = None if residual == "none" else ("inplace" if residual == "inplace" else torch.empty_like(tx))
+        gi, gv = S.topk_sparsify(tx, k, residual=res)
+        torch.cuda.synchronize()
+        gi, gv = to_np(gi, np.uint32), to_np(gv)
+        np.testing.assert_array_equal(gi, oi, err_msg=f"#{case} indices")
+        np.testing.assert_array_equal(gv.view(np.uint32), ov.view(np.uint32), err_msg=f"#{case} values")
+        if residual != "none":
+            gr = to_np(tx if residual == "inplace" else res)
+            np.testing.assert_array_equal(gr.view(np.uint32), orr.view(np.uint32), err_msg=f"#{case} residual")
+
+
+def test_random_sweep_quantize():
+    import torch
+    from gpu_util import to_np
+    from paper_1802_08021_amd import sparcml as S
+    rng = np.random.default_rng(9113)
+    for case in range(40):
+        P = int(rng.integers(1, 140))
+        bits = int(rng.choice([2, 4, 8]))
+        lens = [int(rng.choice([0, 1, 3, 4, 5, 8191, 8192, 8193, 20000])) for _ in range(P)]
+        vals = [_row_values(rng, n, str(rng.choice(["laplace", "normal", "ties", "zeros"]))) for n in lens]
+        want_deq = bool(rng.random() < 0.5)
+        seed = int(rng.integers(0, 2**63))
+        say(f"[sweep quant] #{case}: P={P} bits={bits} deq={want_deq}")
+        oq, os_, od = oracle.quantize(vals, bits, seed)
+        tv = [to_dev(v if v.size else np.zeros(0, np.float32)) for v in vals]
+        codes, scale, deq = S.quantize(tv, bits, seed, want_deq=want_deq)
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(to_np(scale).view(np.uint32), os_.view(np.uint32), err_msg=f"#{case} scales")
+        for r in range(P):
+            np.testing.assert_array_equal(to_np(codes[r])[: oq[r].size], oq[r], err_msg=f"#{case} codes {r}")
+            if want_deq:
+                np.testing.assert_array_equal(to_np(deq[r])[: od[r].size].view(np.uint32), od[r].view(np.uint32),
+                                              err_msg=f"#{case} dequantized {r}")
