@@ -151,3 +151,40 @@ def test_random_sweep_quantize():
             if want_deq:
                 np.testing.assert_array_equal(to_np(deq[r])[: od[r].size].view(np.uint32), od[r].view(np.uint32),
                                               err_msg=f"#{case} dequantized {r}")
+
+
+def test_random_sweep_async_reduce():
+    """The entry point the benchmark times (the asynchronous reduce, root
+    header on the device), on the reduce sweep's first cases, each run
+    twice on the same buffers."""
+    import torch
+    from gpu_util import to_np
+    from paper_1802_08021_amd import sparcml as S
+    rng = np.random.default_rng(20261202)
+    for case in range(100):
+        P, N, idx, val, qbits, delta, rg, label = _case(rng, case)
+        say(f"[sweep async] {label}")
+        ti = [to_dev(a) for a in idx]
+        kw = {} if rg is None else {"lo": rg[0], "hi": rg[1]}
+        if qbits:
+            q, scale, deq = oracle.quantize(val, qbits, seed=1000 + case)
+            codes = [to_dev(a if a.size else np.zeros(1, np.uint8)) for a in q]
+            c = S.ReduceCall(ti, N, delta, codes=codes, scales=to_dev(scale), qbits=qbits, node_info=True, **kw)
+            vals_o = deq
+        else:
+            c = S.ReduceCall(ti, N, delta, vals=[to_dev(v) for v in val], node_info=True, **kw)
+            vals_o = val
+        o = oracle.sparse_reduce(idx, vals_o, N, delta) if rg is None else \
+            oracle.sparse_reduce_range(idx, vals_o, N, rg[0], rg[1], delta)
+        for rep in range(2):
+            c.run_async()
+            torch.cuda.synchronize()
+            nnz, dense = c.result_header()
+            g = {
+                "dense": dense, "nnz": nnz,
+                "idx": None if dense else to_np(c.out_idx[:nnz], np.uint32).copy(),
+                "val": to_np(c.out_val if dense else c.out_val[:nnz]).copy(),
+                "node_nnz": to_np(c.node_nnz).astype(np.uint64) if P > 1 else np.zeros(0, np.uint64),
+                "node_dense": to_np(c.node_dense) if P > 1 else np.zeros(0, np.uint8),
+            }
+            assert_reduce_equal(g, o, f"{label} (async, run {rep})")
