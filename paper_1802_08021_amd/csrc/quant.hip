@@ -25,8 +25,9 @@ struct QDesc {
 
 // Stream r's descriptor: from the launch's arguments (ARGS: six words a
 // stream, val, q and n; no dequantized copy), else from the uploaded table.
-// A template parameter, not a branch: a descriptor read from either place
-// becomes one generic (vector) load of its fields.
+// (A template parameter: chosen at run time, the two sources were merged by
+// the compiler into one generic pointer and a vector load per workgroup;
+// each instantiation now reads its own source with scalar loads.)
 template <bool ARGS>
 __device__ __forceinline__ QDesc qdesc(const QDesc* tab, const Blob& tb, uint32_t r)
 {
@@ -48,11 +49,12 @@ __device__ __forceinline__ double butterfly_sum(double v, int width)
 
 // partial[r][b] = tree sum of v^2 over elements [b*kSeg, (b+1)*kSeg) of
 // stream r (zeros past the end); with one block a stream (scale non-null)
-// that is the norm^2, and scale[r] = its square root.  A wave covers 2048 consecutive elements
-// in eight steps of 256: each lane squares four consecutive elements and
-// adds them pairwise, a lane butterfly joins the 64 lanes' subtrees, and the
-// eight step sums are joined pairwise at the end -- the same adjacent-pair
-// tree, with the eight independent butterflies in flight together.
+// that is the norm^2, and scale[r] = its square root.  A wave covers 2048
+// consecutive elements in eight steps of 256: each lane squares four
+// consecutive elements and adds them pairwise, a lane butterfly joins the 64
+// lanes' subtrees, and the eight step sums are joined pairwise at the end --
+// the same adjacent-pair tree, with the eight independent butterflies in
+// flight together.
 template <bool ARGS>
 __global__ void __launch_bounds__(256) k_sumsq_partial(const QDesc* tab, Blob tb, double* partial, uint32_t Q,
                                                        float* scale)
