@@ -733,8 +733,17 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
                 uint32_t* const rpre = s_wp + (wv * RROWS + row) * PW;
                 const uint32_t base = l16 * RK;
                 const bool few = NB <= (uint32_t)(NW / 4) * RROWS;
-                const uint32_t rq = few ? (wslot >= G3 ? wslot - G3 : (uint32_t)NW / 4u + G3 - 1u - wslot)
-                                        : (wslot < G3 ? G3 - 1u - wslot : wslot);
+                // (at 64 ranks, where many rows are common -- about 36 a tile
+                // at c4 -- they go round robin over SIMDs 2, 1, 0, 3, each
+                // from its last wave down, SIMD 3's last wave walking the
+                // five-rank list: 0.279 -> 0.275 ms at c4; the wider kernels
+                // keep the order their register allocation was measured with,
+                // the round robin costing c5 0.3%)
+                const uint32_t rq_many =
+                    PMAX != 64 ? (wslot < G3 ? G3 - 1u - wslot : wslot)
+                               : ((wv & 3u) == 3u ? ((wv >> 2) == 3u ? 3u : 2u - (wv >> 2)) : 3u - (wv >> 2)) * 4u +
+                                     ((wv & 3u) == 3u ? 3u : 2u - (wv & 3u));
+                const uint32_t rq = few ? (wslot >= G3 ? wslot - G3 : (uint32_t)NW / 4u + G3 - 1u - wslot) : rq_many;
                 for (uint32_t b0 = rq * RROWS; b0 < NB; b0 += RROWS * NW) {
                     const uint32_t i = b0 + row;
                     const bool act = (lane >> 4) < RROWS && i < NB;
