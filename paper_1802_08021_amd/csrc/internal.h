@@ -155,7 +155,7 @@ hipError_t merge_small_run(uint32_t PT, uint32_t L, uint32_t qbits, uint32_t nfo
 // (merge_seg_shape), each merged by one workgroup.
 constexpr uint64_t kSegEntries = 2048;                     // expected entries per segment
 constexpr uint32_t kSegMax = 1024;                         // segments at most
-constexpr uint64_t kSegMin = 64;                           // segments at least (when the range has as many indices)
+constexpr uint64_t kSegMin = 128;                          // segments at least (when the range has as many indices)
 constexpr uint64_t kSegMaxEntries = kSegEntries * kSegMax;  // inputs it takes at most
 bool merge_seg_fits(uint32_t PT, uint64_t sum_nnz, uint64_t thr);
 void merge_seg_shape(uint64_t R, uint64_t sum_nnz, uint32_t* nseg, uint64_t* segw);

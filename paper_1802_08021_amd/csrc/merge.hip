@@ -47,6 +47,7 @@ namespace {
 
 constexpr uint32_t kMSlots = 64;     // slots the LDS tables hold
 constexpr uint32_t kSmallSlots = 8;  // slots of the one-workgroup path (its argument table)
+constexpr uint32_t kMaxLevels = 6;   // levels of a kMSlots-slot tree
 
 // Threads, LDS entries, units per thread and merged positions per unit
 // (odd: the units of adjacent lanes start in different LDS banks) of a
@@ -82,6 +83,9 @@ struct MLds {
     const void* pv[kMSlots];       // slot values, or QSGD codes
     uint32_t first[kMSlots];       // stream position of the slot's first entry in the range
     float unit[kMSlots];           // QSGD level unit of the slot
+    uint8_t rk[C::CAP];            // one-pass order: the slot of each entry
+    uint32_t lmax;                 // one-pass order: the longest slot run
+    uint32_t ecnt[(kMaxLevels + 1) * kMSlots];  // one-pass order: entries by level span and slot
     uint32_t w[C::NT / 64];
     uint2 w2[C::NT / 64];
 };
@@ -460,6 +464,232 @@ __device__ __forceinline__ uint32_t merge_levels(MLds<C>& m, uint32_t PT, uint32
     return root;
 }
 
+// The same tree in one pass, for ranges of few entries (at most kSortPer
+// a thread).  The root's entries come in the order of (index, slot), and
+// the node sums at an index follow the tree over the slots present there:
+//
+//  * an entry's place in that order is its position in its own run plus,
+//    for every other slot, the entries of that slot's run that precede it
+//    (indices below its own, and equal ones of lower slots): fixed-step
+//    binary searches, eight slots side by side, and up to eight lanes per
+//    entry (each taking every G-th slot) while entries are few;
+//  * the entries move to their places, with their slots, so an index's
+//    entries are consecutive and in slot order;
+//  * two neighbouring slots r' < r there first share a node at level h + 1,
+//    h the highest bit in which they differ (the separator).  The sum is
+//    taken with a stack: before a value is pushed, the pending sums whose
+//    separator lies below its own are folded (left + right), which adds
+//    exactly the pairs of children that both hold a value, in the tree's
+//    order;
+//  * an entry opens a group of its index at levels 1..h below the node it
+//    shares with its predecessor (the next lower slot present), at every
+//    level if it has none; counts of those spans per slot, summed over a
+//    node's slots (one wave per level), give every node's union size.
+// Returns the root's length (its run at 0) and leaves the node sizes in
+// m.cnt, as merge_levels does.
+constexpr uint32_t kSortPer = 2;
+
+template <class C>
+__device__ __forceinline__ bool sort_fits(uint32_t total)
+{
+    return total <= kSortPer * (uint32_t)C::NT;
+}
+
+template <class C, bool QUANT>
+__device__ __forceinline__ uint32_t sort_merge(MLds<C>& m, uint32_t PT, uint32_t L, uint32_t total, uint32_t qbits)
+{
+    constexpr int NT = C::NT, KR = (int)kSortPer;
+    static_assert(3u * kSortPer * (uint32_t)NT <= C::CAP, "a search reads below 3 kSortPer NT");
+    const uint32_t tid = threadIdx.x, lane = tid & 63u, wv = tid >> 6;
+    const uint32_t wfirst = (uint32_t)__builtin_amdgcn_readfirstlane((int)(tid & ~63u));
+    for (uint32_t i = tid; i < (kMaxLevels + 1u) * kMSlots; i += NT) m.ecnt[i] = 0u;
+    if (wv == 0u) {  // the longest run (PT <= 64: one wave)
+        uint32_t n = lane < PT ? m.len[lane] : 0u;
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) n = max(n, (uint32_t)__shfl_xor((int)n, o));
+        if (lane == 0u) m.lmax = n;
+    }
+
+    // entries tid + k NT in the slots' layout: index, value and slot to LDS
+    {
+        uint32_t sl[KR], pos[KR], xi[KR];
+        float xv[KR];
+#pragma unroll
+        for (int k = 0; k < KR; ++k) {
+            const uint32_t e = tid + (uint32_t)k * NT;
+            sl[k] = pos[k] = xi[k] = 0u;
+            xv[k] = 0.0f;
+            if (e < total) {
+                const uint32_t s = last_at_most<6>(m.start, PT, e);
+                sl[k] = s;
+                pos[k] = m.first[s] + e - m.start[s];
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < KR; ++k) {
+            if (tid + (uint32_t)k * NT < total) {
+                const uint32_t s = sl[k];
+                xi[k] = as_global(m.pi[s])[pos[k]];
+                if (QUANT) {
+                    const uint32_t code = load_code(as_global(static_cast<const uint8_t*>(m.pv[s])), pos[k], qbits);
+                    xv[k] = dequant(code, qbits, m.unit[s]);
+                } else {
+                    xv[k] = as_global(static_cast<const float*>(m.pv[s]))[pos[k]];
+                }
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < KR; ++k) {
+            const uint32_t e = tid + (uint32_t)k * NT;
+            if (e < total) {
+                m.idx[e] = xi[k];
+                m.val[e] = xv[k];
+                m.rk[e] = (uint8_t)sl[k];
+            }
+        }
+    }
+    __syncthreads();
+
+    // places: item it = tid + k NT searches for entry it / G in the slots
+    // it % G, it % G + G, ...; the G lanes' counts are added across lanes.
+    // A count is bounded by its run's length, so a place is below total
+    // whatever the indices.
+    uint32_t lg = 0;  // log2 G (uniform): while items fit the threads and a lane keeps eight slots
+    while (lg < 3u && (total << (lg + 1u)) <= (uint32_t)NT && (8u << (lg + 1u)) <= PT) ++lg;
+    const uint32_t G = 1u << lg;
+    const int steps = 32 - __clz((int)__builtin_amdgcn_readfirstlane((int)m.lmax));
+    uint32_t at[KR], ex[KR], es[KR];
+    float ev[KR];
+#pragma unroll
+    for (int k = 0; k < KR; ++k) {
+        at[k] = ex[k] = es[k] = 0u;
+        ev[k] = 0.0f;
+        if (wfirst + (uint32_t)k * NT >= (total << lg)) continue;  // no item in the wave (uniform)
+        const uint32_t it = tid + (uint32_t)k * NT, e = it >> lg, h = it & (G - 1u);
+        const bool in = e < total;
+        const uint32_t ec = in ? e : 0u;
+        const uint32_t x = m.idx[ec], s = m.rk[ec] & (kMSlots - 1u);
+        ex[k] = x;
+        es[k] = s;
+        ev[k] = m.val[ec];
+        uint32_t cnt = in && h == 0u ? ec - m.start[s] : 0u;  // own position, by the first lane
+        for (uint32_t b0 = 0; b0 < PT; b0 += 8u << lg) {
+            uint32_t c[8], st1[8], n[8], xt[8];
+#pragma unroll
+            for (uint32_t j = 0; j < 8u; ++j) {
+                const uint32_t s2 = b0 + h + (j << lg), s2c = min(s2, kMSlots - 1u);
+                const uint32_t len = m.len[s2c];
+                st1[j] = s2 < PT ? m.start[s2c] - 1u : 0u;
+                n[j] = in && s2 < PT && s2 != s ? len : 0u;
+                xt[j] = s2 < s ? x + 1u : x;  // lower slots: equal indices precede too
+                c[j] = 0u;
+            }
+            for (int t = steps - 1; t >= 0; --t) {
+#pragma unroll
+                for (uint32_t j = 0; j < 8u; ++j) {
+                    // (read whether or not cc lies in the run: start + cc - 1
+                    // < total + 2 lmax, inside the array.  The test is bitwise:
+                    // a short-circuit one would be compiled into a branch
+                    // around the read, with a wait of its own)
+                    const uint32_t cc = c[j] + (1u << t);
+                    const uint32_t y = m.idx[st1[j] + cc];
+                    const uint32_t take = (uint32_t)(y < xt[j]) & (uint32_t)(cc <= n[j]);
+                    c[j] = take ? cc : c[j];
+                }
+            }
+#pragma unroll
+            for (uint32_t j = 0; j < 8u; ++j) cnt += c[j];
+        }
+        for (uint32_t o = 1; o < G; o <<= 1) cnt += (uint32_t)__shfl_xor((int)cnt, (int)o);
+        at[k] = in && h == 0u ? cnt : kNone;
+    }
+    __syncthreads();  // every search read done
+#pragma unroll
+    for (int k = 0; k < KR; ++k) {
+        if (at[k] != kNone && wfirst + (uint32_t)k * NT < (total << lg)) {
+            m.idx[at[k]] = ex[k];
+            m.val[at[k]] = ev[k];
+            m.rk[at[k]] = (uint8_t)es[k];
+        }
+    }
+    __syncthreads();
+
+    // ordered positions tid KR + k: group spans, and the sum of each index
+    // whose first entry is here (the stack in place over the index's values)
+    uint32_t ox[KR], heads = 0, nh = 0;
+    float ov[KR];
+#pragma unroll
+    for (int k = 0; k < KR; ++k) {
+        const uint32_t p = tid * (uint32_t)KR + (uint32_t)k;
+        ox[k] = 0u;
+        ov[k] = 0.0f;
+        if (p >= total) continue;
+        const uint32_t xp = m.idx[p], r = m.rk[p] & (kMSlots - 1u);
+        const bool head = p == 0u || m.idx[p - 1u] != xp;
+        uint32_t span = L;
+        if (!head) {
+            const uint32_t d = r ^ m.rk[p - 1u];
+            span = d ? min(31u - (uint32_t)__clz((int)d), L) : 0u;
+        }
+        if (span) atomicAdd(&m.ecnt[span * kMSlots + r], 1u);
+        if (!head) continue;
+        uint32_t i = p + 1u;
+        if (i < total && m.idx[i] == xp) {
+            // stack: values at p .. p + sp - 1, pending separators as bits
+            // (strictly falling from the bottom: the lowest is the top)
+            uint32_t sp = 1u, pend = 0u, prev = r;
+            auto fold = [&]() {
+                m.val[p + sp - 2u] = m.val[p + sp - 2u] + m.val[p + sp - 1u];
+                --sp;
+                pend &= pend - 1u;
+            };
+            do {
+                const uint32_t ri = m.rk[i];
+                const float vi = m.val[i];
+                const uint32_t d = ri ^ prev;
+                const uint32_t h = d ? 31u - (uint32_t)__clz((int)d) : 0u;
+                while (pend && (uint32_t)__builtin_ctz(pend) < h) fold();
+                pend |= 1u << h;
+                m.val[p + sp] = vi;  // (p + sp <= i: read already)
+                ++sp;
+                prev = ri;
+                ++i;
+            } while (i < total && m.idx[i] == xp);
+            while (pend) fold();
+        }
+        ox[k] = xp;
+        ov[k] = m.val[p];
+        heads |= 1u << k;
+        ++nh;
+    }
+    uint32_t R;
+    uint32_t o = wg_excl_scan<NT>(nh, m.w, &R);  // its first barrier: every read above done
+#pragma unroll
+    for (int k = 0; k < KR; ++k) {
+        if (heads & (1u << k)) {
+            m.idx[o] = ox[k];
+            m.val[o] = ov[k];
+            ++o;
+        }
+    }
+    // node sizes, level order: wave l - 1 takes level l (below the root),
+    // lane r slot r's spans that reach level l, summed over the node's 2^l
+    // slots across lanes; the root holds every index once
+    if (wv + 1u < L) {  // (uniform)
+        const uint32_t l = wv + 1u;
+        uint32_t c = 0;
+        if (lane < PT) {
+#pragma unroll
+            for (uint32_t j = 1; j <= kMaxLevels; ++j) c += j >= l && j <= L ? m.ecnt[j * kMSlots + lane] : 0u;
+        }
+        for (uint32_t d = 1; d < (1u << l); d <<= 1) c += (uint32_t)__shfl_xor((int)c, (int)d);
+        if (lane < PT && (lane & ((1u << l) - 1u)) == 0u) m.cnt[PT - (PT >> (l - 1u)) + (lane >> l)] = c;
+    }
+    if (tid == 0u) m.cnt[PT - 2u] = R;
+    __syncthreads();
+    return R;
+}
+
 // Node t of the P'-slot tree (level order) goes to position o of node_nnz /
 // node_dense: the first nfold level-1 nodes, then every higher node.
 __device__ __forceinline__ bool report_slot(uint32_t t, uint32_t PT, uint32_t nfold, uint32_t* o)
@@ -502,8 +732,13 @@ __global__ void __launch_bounds__(SmallCfg::NT) k_merge_small(MTable kt, MArgs a
         if (QUANT) m.unit[tid] = n ? level_unit(*d.qscale, a.qbits) : 0.0f;
     }
     const uint32_t total = slot_starts(m, PT, n);
-    load_runs<C, QUANT>(m, PT, total, a.qbits);
-    const uint32_t root = merge_levels(m, PT, a.L);
+    uint32_t root;
+    if (sort_fits<C>(total)) {
+        root = sort_merge<C, QUANT>(m, PT, a.L, total, a.qbits);
+    } else {
+        load_runs<C, QUANT>(m, PT, total, a.qbits);
+        root = merge_levels(m, PT, a.L);
+    }
     for (uint32_t e = tid; e < root; e += C::NT) {
         a.out_idx[e] = m.idx[e];
         a.out_val[e] = m.val[e];
@@ -661,7 +896,10 @@ __global__ void __launch_bounds__(C::NT) k_merge_seg(SArgs a)
     // this segment's union size (and node sizes)
     unsigned long long R;
     const bool big = total > C::CAP;  // uniform
-    if (!big) {
+    if (!big && sort_fits<C>(total)) {
+        R = sort_merge<C, QUANT>(m, PT, a.L, total, a.qbits);
+        if (tid + 1u < PT) s_acc[tid] = m.cnt[tid];
+    } else if (!big) {
         load_runs<C, QUANT>(m, PT, total, a.qbits);
         R = merge_levels(m, PT, a.L);
         if (tid + 1u < PT) s_acc[tid] = m.cnt[tid];

@@ -125,3 +125,27 @@ def test_async_entry_point_repeated():
         np.testing.assert_array_equal(to_np(call.out_val)[:nnz].view(np.uint32), o["val"].view(np.uint32))
         np.testing.assert_array_equal(to_np(call.node_nnz).astype(np.uint64), o["node_nnz"])
         assert not to_np(call.node_dense).any()
+
+
+@pytest.mark.parametrize("P", [16, 37, 64])
+def test_one_pass_heavy_overlap(P):
+    """Segments of at most two entries a thread take the one-pass order:
+    every index held by a random half of the ranks (long runs of slots with
+    gaps, the summation stack up to the tree's depth), then by every rank,
+    then QSGD codes."""
+    rng = np.random.default_rng(2600 + P)
+    N = 1 << 16
+    cand = inputs.uniform_subset(rng, N, 1000)
+    idx = [cand[rng.random(cand.size) < 0.5] for _ in range(P)]
+    val = [inputs.normal(rng, a.size) for a in idx]
+    g = check(idx, val, N, 1.0, f"random halves, P={P}")
+    assert not g["dense"]
+    few = cand[::5]
+    check([few.copy() for _ in range(P)], [inputs.normal(rng, few.size) for _ in range(P)], N, 1.0,
+          f"every rank every index, P={P}")
+    q, scale, deq = oracle.quantize([inputs.laplace(rng, 1e-3, a.size) for a in idx], 4, seed=99 + P)
+    say(f"[seg] one pass, QSGD 4-bit, P={P}")
+    o = oracle.sparse_reduce(idx, deq, N, 1.0)
+    codes = [to_dev(c if c.size else np.zeros(1, np.uint8)) for c in q]
+    g = gpu_reduce(idx, None, N, 1.0, qbits=4, codes=codes, scales=to_dev(scale))
+    assert_reduce_equal(g, o, f"one pass q4 P={P}")
