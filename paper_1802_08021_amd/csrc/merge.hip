@@ -21,6 +21,10 @@
 //    per-node counts are the nodes' union sizes (what the switch rule
 //    reports per node).
 //
+// Ranges of few entries (at most kSortPer a thread) take the same tree in
+// one pass instead (sort_merge): every entry's place in the root's order
+// from binary searches, then the sums of each index in the tree's order.
+//
 // Two kernels use it.  k_merge_small: one workgroup takes the whole range
 // (one launch, the slot table in the kernel arguments).  A level costs about
 // 4.5 us of dependent LDS round trips and barriers even when it holds few
