@@ -55,17 +55,15 @@ __device__ __forceinline__ double butterfly_sum(double v, int width)
 // lanes' subtrees, and the eight step sums are joined pairwise at the end --
 // the same adjacent-pair tree, with the eight independent butterflies in
 // flight together.
-template <bool ARGS>
-__global__ void __launch_bounds__(256) k_sumsq_partial(const QDesc* tab, Blob tb, double* partial, uint32_t Q,
-                                                       float* scale)
+// Tree sum of v^2 over the 2048 elements [base, base + 2048) (zeros past
+// n) by one wave, in eight steps of 256: each lane squares four consecutive
+// elements and adds them pairwise, a lane butterfly joins the 64 lanes'
+// subtrees, and the eight step sums are joined pairwise at the end -- the
+// adjacent-pair tree, with the eight independent butterflies in flight
+// together.  STREAM: nontemporal loads (values not read again soon).
+template <bool STREAM>
+__device__ __forceinline__ double wave_sumsq(const float* v, uint64_t n, uint64_t base, int lane)
 {
-    __shared__ double s_w[4];
-    const uint32_t r = blockIdx.y, b = blockIdx.x;
-    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-    const QDesc d = qdesc<ARGS>(tab, tb, r);
-    const float* v = d.val;
-    const uint64_t n = d.n;
-    const uint64_t base = (uint64_t)b * kSeg + (uint64_t)wv * 2048;
     const bool vec = (reinterpret_cast<uintptr_t>(v) & 15u) == 0;
     double part[8];
 #pragma unroll
@@ -73,7 +71,7 @@ __global__ void __launch_bounds__(256) k_sumsq_partial(const QDesc* tab, Blob tb
         const uint64_t e = base + (uint64_t)it * 256 + (uint64_t)lane * 4;
         float4 x;
         if (vec && e + 4 <= n) {
-            x = load_nt(v + e);  // streamed: nontemporal
+            x = STREAM ? load_nt(v + e) : *reinterpret_cast<const float4*>(v + e);
         } else {
             x.x = e < n ? v[e] : 0.0f;
             x.y = e + 1 < n ? v[e + 1] : 0.0f;
@@ -84,7 +82,22 @@ __global__ void __launch_bounds__(256) k_sumsq_partial(const QDesc* tab, Blob tb
                           ((double)x.z * (double)x.z + (double)x.w * (double)x.w);
         part[it] = butterfly_sum(sq, 64);
     }
-    const double w = ((part[0] + part[1]) + (part[2] + part[3])) + ((part[4] + part[5]) + (part[6] + part[7]));
+    return ((part[0] + part[1]) + (part[2] + part[3])) + ((part[4] + part[5]) + (part[6] + part[7]));
+}
+
+// partial[r][b] = tree sum of v^2 over elements [b*kSeg, (b+1)*kSeg) of
+// stream r (zeros past the end), a wave per 2048 elements and the four
+// wave sums pairwise; with one block a stream (scale non-null) that is the
+// norm^2, and scale[r] = its square root.
+template <bool ARGS>
+__global__ void __launch_bounds__(256) k_sumsq_partial(const QDesc* tab, Blob tb, double* partial, uint32_t Q,
+                                                       float* scale)
+{
+    __shared__ double s_w[4];
+    const uint32_t r = blockIdx.y, b = blockIdx.x;
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    const QDesc d = qdesc<ARGS>(tab, tb, r);
+    const double w = wave_sumsq<true>(d.val, d.n, (uint64_t)b * kSeg + (uint64_t)wv * 2048, lane);
     if (lane == 0) s_w[wv] = w;
     __syncthreads();
     if (threadIdx.x == 0) {
@@ -139,19 +152,15 @@ __device__ __forceinline__ uint4 philox(uint4 c, uint32_t k0, uint32_t k1)
     return c;
 }
 
-// Each thread quantizes 32/bits consecutive elements into one 32-bit word
-// of codes (4 elements per Philox block).
-template <int BITS, bool ARGS>
-__global__ void __launch_bounds__(256) k_quantize(const QDesc* tab, Blob tb, const float* scales, uint32_t k0,
-                                                  uint32_t k1)
+// Elements e0 .. e0 + 32/BITS - 1 of stream r quantized into one 32-bit
+// word of codes (4 elements per Philox block), the dequantized values
+// stored too when the stream asks for them.
+template <int BITS>
+__device__ __forceinline__ void quant_word(const QDesc& d, uint32_t r, uint64_t e0, float scale, uint32_t k0,
+                                           uint32_t k1)
 {
     constexpr int EPT = 32 / BITS;
     constexpr uint32_t S = (1u << (BITS - 1)) - 1u;
-    const uint32_t r = blockIdx.y;
-    const QDesc d = qdesc<ARGS>(tab, tb, r);
-    const uint64_t e0 = ((uint64_t)blockIdx.x * 256 + threadIdx.x) * EPT;
-    if (e0 >= d.n) return;
-    const float scale = scales[r];
     const float inv = scale > 0.0f ? __fdiv_rn((float)S, scale) : 0.0f;
     const float unit = __fdiv_rn(scale, (float)S);
     float x[EPT];
@@ -204,6 +213,54 @@ __global__ void __launch_bounds__(256) k_quantize(const QDesc* tab, Blob tb, con
         for (int i = 0; i < 4; ++i)
             if (byte0 + i < nbytes) d.q[byte0 + i] = (uint8_t)(word >> (8 * i));
     }
+}
+
+// Each thread quantizes 32/bits consecutive elements into one word.
+template <int BITS, bool ARGS>
+__global__ void __launch_bounds__(256) k_quantize(const QDesc* tab, Blob tb, const float* scales, uint32_t k0,
+                                                  uint32_t k1)
+{
+    constexpr int EPT = 32 / BITS;
+    const uint32_t r = blockIdx.y;
+    const QDesc d = qdesc<ARGS>(tab, tb, r);
+    const uint64_t e0 = ((uint64_t)blockIdx.x * 256 + threadIdx.x) * EPT;
+    if (e0 >= d.n) return;
+    quant_word<BITS>(d, r, e0, scales[r], k0, k1);
+}
+
+// Streams of at most kSmallQ elements: one 1024-thread workgroup a stream
+// takes both passes, one launch instead of three.  Waves 4b..4b+3 sum block
+// b's squares as k_sumsq_partial does, the four block partials are joined
+// pairwise (the tree k_sum_f64 forms over them: the partials of blocks past
+// the stream are +0.0, and adding +0.0 is exact), then the workgroup codes
+// the stream as k_quantize does (its values read again, now from the cache).
+constexpr uint64_t kSmallQ = 4 * kSeg;
+
+template <int BITS, bool ARGS>
+__global__ void __launch_bounds__(1024) k_quant_small(const QDesc* tab, Blob tb, float* scales, uint32_t k0,
+                                                      uint32_t k1)
+{
+    constexpr int EPT = 32 / BITS;
+    __shared__ double s_w[16];
+    __shared__ float s_scale;
+    const uint32_t r = blockIdx.x;
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    const QDesc d = qdesc<ARGS>(tab, tb, r);
+    const double w = wave_sumsq<false>(d.val, d.n, (uint64_t)(wv >> 2) * kSeg + (uint64_t)(wv & 3) * 2048, lane);
+    if (lane == 0) s_w[wv] = w;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        double p[4];
+#pragma unroll
+        for (int b = 0; b < 4; ++b) p[b] = (s_w[4 * b] + s_w[4 * b + 1]) + (s_w[4 * b + 2] + s_w[4 * b + 3]);
+        const float sc = (float)sqrt((p[0] + p[1]) + (p[2] + p[3]));
+        scales[r] = sc;
+        s_scale = sc;
+    }
+    __syncthreads();
+    const float scale = s_scale;
+    for (uint64_t e0 = (uint64_t)threadIdx.x * EPT; e0 < d.n; e0 += 1024u * EPT)
+        quant_word<BITS>(d, r, e0, scale, k0, k1);
 }
 
 // Bucketed QSGD in one pass: a bucket of B (a power of two, 4..8192)
@@ -424,6 +481,22 @@ hipError_t quant_run(int P, const float* const* vals, const uint64_t* n, int bit
         if (e != hipSuccess) return e;
     }
 
+    const uint32_t k0 = (uint32_t)(seed & 0xFFFFFFFFu), k1 = (uint32_t)(seed >> 32);
+    if (max_n > 0 && max_n <= kSmallQ) {  // short streams: norm and codes in one launch
+        timer_begin(kTQuantCodes, s);
+        const dim3 g((uint32_t)P), blk(1024);
+        if (tb.nwords) {
+            if (bits == 2) hipLaunchKernelGGL((k_quant_small<2, true>), g, blk, 0, s, l.tab, tb, out_scale, k0, k1);
+            else if (bits == 4) hipLaunchKernelGGL((k_quant_small<4, true>), g, blk, 0, s, l.tab, tb, out_scale, k0, k1);
+            else hipLaunchKernelGGL((k_quant_small<8, true>), g, blk, 0, s, l.tab, tb, out_scale, k0, k1);
+        } else {
+            if (bits == 2) hipLaunchKernelGGL((k_quant_small<2, false>), g, blk, 0, s, l.tab, tb, out_scale, k0, k1);
+            else if (bits == 4) hipLaunchKernelGGL((k_quant_small<4, false>), g, blk, 0, s, l.tab, tb, out_scale, k0, k1);
+            else hipLaunchKernelGGL((k_quant_small<8, false>), g, blk, 0, s, l.tab, tb, out_scale, k0, k1);
+        }
+        timer_end(kTQuantCodes, s);
+        return hipGetLastError();
+    }
     // norms; the launch that finishes a stream's norm also writes its scale
     timer_begin(kTQuantNorm, s);
     float* const scale0 = l.levels == 0 ? out_scale : nullptr;
@@ -439,7 +512,6 @@ hipError_t quant_run(int P, const float* const* vals, const uint64_t* n, int bit
                            l.count[lv - 1], l.part[lv], l.count[lv], lv == l.levels ? out_scale : nullptr);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (max_n == 0) return hipSuccess;
-    const uint32_t k0 = (uint32_t)(seed & 0xFFFFFFFFu), k1 = (uint32_t)(seed >> 32);
     const uint64_t per_block = 256ull * (32 / bits);
     const dim3 grid((uint32_t)((max_n + per_block - 1) / per_block), P);
     timer_begin(kTQuantCodes, s);
