@@ -172,6 +172,24 @@ def test_quantize_long_stream():
     assert_quant_equal(g, o, len(vals), "long stream")
 
 
+@pytest.mark.parametrize("bits", [2, 4, 8])
+def test_quantize_short_stream_boundary(bits):
+    """Streams of at most 4 x 8192 elements take norm and codes in one
+    launch; the longest one at that limit and one past it (three launches),
+    with streams that end inside each of the four norm blocks and on their
+    edges."""
+    rng = np.random.default_rng(90 + bits)
+    sizes = [1, 8191, 8192, 8193, 16385, 24575, 24577, 32767]
+    seed = 0xC0FFEE_0000 + bits
+    for longest in (32768, 32769):
+        vals = [inputs.laplace(rng, 1e-3, n) for n in sizes + [longest]]
+        o = oracle.quantize(vals, bits, seed)
+        for want_deq in (True, False):
+            say(f"[quant] short-stream boundary: longest {longest}, bits={bits}, deq={want_deq}")
+            g = gpu_quantize(vals, bits, seed, want_deq)
+            assert_quant_equal(g, o, len(vals), f"longest {longest}, deq={want_deq}")
+
+
 def test_quantize_config5_scaled():
     c = inputs.config(5, scale_log2=5)
     d = inputs.generate(c, seed=0)
