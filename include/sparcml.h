@@ -203,9 +203,11 @@ SPARCML_API int sparcml_quantize(int P, const sparcml_stream* in, int bits, uint
 typedef struct sparcml_result {
     uint64_t nnz;      /* root nnz (the range's length if dense) */
     uint32_t is_dense; /* root representation */
-    uint32_t reserved; /* 0; nonzero if the all-sparse merge path could not complete: bit 0, a
-                          workgroup gave up waiting for its predecessors' sizes (never expected);
-                          bit 1, streams that do not ascend were met.  The outputs are then incomplete */
+    uint32_t reserved; /* 0; nonzero if the reduction could not complete: bit 0, a workgroup of
+                          the all-sparse merge path gave up waiting for its predecessors' sizes
+                          (never expected); bit 1, streams that do not ascend were met (the merge
+                          path, or a sparse root that would not fit out->nnz entries: never
+                          written past them).  The outputs are then incomplete */
 } sparcml_result;
 
 /*
@@ -265,7 +267,10 @@ SPARCML_API int sparcml_quantize_bucketed(int P, const sparcml_stream* in, int b
  * device and therefore waits for its own work on `stream`.
  * Errors: EINVAL (including P outside [1, 256] or mixed qbits), ECAPACITY (out->nnz
  * below the capacity stated above), EWORKSPACE, EHIP; all but EHIP are
- * detected before any device work is enqueued.
+ * detected before any device work is enqueued.  Streams that do not ascend
+ * give undefined sums but no write past the outputs: where the device sees
+ * them (the all-sparse merge path, or a sparse root that would not fit
+ * out->nnz entries) the call returns EUNSORTED.
  */
 SPARCML_API int sparcml_sparse_reduce(int P, const sparcml_stream* streams, uint64_t N, double delta,
                           sparcml_stream* out, uint64_t* node_nnz, uint8_t* node_dense,

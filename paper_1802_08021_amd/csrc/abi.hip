@@ -248,10 +248,10 @@ int reduce_impl(int P, const sparcml_stream* streams, uint64_t N, uint64_t lo, u
         }
         const uint32_t nfold = PT == P ? (uint32_t)(P / 2) : (uint32_t)(P - P2);
         ReduceResult res{};
-        e = reduce_run(plan, tab, out->idx, out->val, node_nnz, node_dense, ws, s, &res, nfold, dres);
+        e = reduce_run(plan, tab, out->idx, out->val, node_nnz, node_dense, ws, s, &res, nfold, dres, out->nnz);
         if (e != hipSuccess) return hip_fail(e, "sparse_reduce");
         if (!dres && (res.pad & 2u))
-            return fail(SPARCML_EUNSORTED, "sparse_reduce: the merge path met streams that do not ascend; "
+            return fail(SPARCML_EUNSORTED, "sparse_reduce: streams that do not ascend were met; "
                                            "the outputs are incomplete");
         if (!dres && res.pad)
             return fail(SPARCML_EHIP, "sparse_reduce: a segment of the merge path gave up waiting for its "

@@ -135,10 +135,13 @@ hipError_t set_result_run(ReduceResult* r, uint64_t nnz, uint32_t dense, hipStre
 // dev_result (device) and nothing waits: the sparse-output passes are
 // enqueued unconditionally and skip themselves on a dense root.
 // node_nnz / node_dense receive the level-1 nodes g < nfold and every node
-// above level 1 (nfold = P/2 reports all P - 1 nodes).
+// above level 1 (nfold = P/2 reports all P - 1 nodes).  out_cap: entries
+// out_idx holds; a sparse root is never written past it (header bit 1 if
+// streams that do not ascend would have done so).
 hipError_t reduce_run(const ReducePlan& p, const StreamDesc* host_tab, uint32_t* out_idx,
                       float* out_val, uint64_t* node_nnz, uint8_t* node_dense, void* ws,
-                      hipStream_t s, ReduceResult* res, uint32_t nfold, ReduceResult* dev_result);
+                      hipStream_t s, ReduceResult* res, uint32_t nfold, ReduceResult* dev_result,
+                      uint64_t out_cap);
 
 // Small-data path: at most 8 slots holding at most thr entries together (so
 // every node stays sparse), few enough that one workgroup's merge tree is

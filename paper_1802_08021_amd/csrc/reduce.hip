@@ -100,7 +100,26 @@ struct Args {
     uint32_t out_vec;          // out_val is 16-byte aligned
     uint32_t lo;               // first index of the range [lo, lo + N); dense output is relative
     const ReduceResult* skip;  // sparse-output passes: return at once if skip->dense (NULL: never)
+    uint32_t out_cap;          // entries out_idx holds: the sparse-output passes write no further
+    uint32_t* err_hdr;         // error bits of the root header (bit 1: a result past out_cap) ...
+    uint32_t* err_res;         // ... and of the caller's device header (NULL: none)
 };
+
+// One entry of a sparse root at position o.  Positions come from per-tile
+// union sizes that the count pass and this pass take alike, so for streams
+// that ascend o < root nnz <= out_cap; streams that do not can make them
+// disagree, and such entries are dropped and reported (bit 1 of the header)
+// instead of written past the caller's buffer.
+__device__ __forceinline__ void put_sparse(const Args& a, uint32_t o, uint32_t index, float v)
+{
+    if (o < a.out_cap) {
+        a.out_idx[o] = index;
+        a.out_val[o] = v;
+    } else {
+        atomicOr(a.err_hdr, 2u);
+        if (a.err_res) atomicOr(a.err_res, 2u);
+    }
+}
 
 __device__ __forceinline__ uint32_t lower_bound(const uint32_t* a, uint32_t lo, uint32_t hi,
                                                 uint64_t x)
@@ -519,8 +538,7 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
                 for (int c = 0; c < CPT; ++c) {
                     const uint32_t m = mc[c] & 0xFFFFu, j = jb + (uint32_t)c;
                     if (m == 1u) {
-                        a.out_idx[toff + nrun] = tlo + j;
-                        a.out_val[toff + nrun] = s_out[j];
+                        put_sparse(a, toff + nrun, tlo + j, s_out[j]);
                     } else if (m != 0u) {
                         s_cnt[j] = m | nrun << 9;
                     }
@@ -588,8 +606,7 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
                         if (MODE == kDense) {
                             s_out[jj] = sum;
                         } else {
-                            a.out_idx[toff + (sc >> 9)] = tlo + jj;
-                            a.out_val[toff + (sc >> 9)] = sum;
+                            put_sparse(a, toff + (sc >> 9), tlo + jj, sum);
                         }
                     }
                 } else {
@@ -621,9 +638,7 @@ __global__ void __launch_bounds__(Fast<PMAX>::NT, Fast<PMAX>::WPE) k_tiles(Args 
                 if (MODE == kDense) {
                     s_out[jj] = sum + 0.0f;
                 } else {
-                    const uint32_t nz = s_cnt[jj] >> 9;
-                    a.out_idx[toff + nz] = tlo + jj;
-                    a.out_val[toff + nz] = sum;
+                    put_sparse(a, toff + (s_cnt[jj] >> 9), tlo + jj, sum);
                 }
             };
             auto cswap_rv = [](uint32_t* rk, float* vv, int x, int y) {
@@ -978,8 +993,7 @@ __global__ void __launch_bounds__(kSlowNT) k_slow(Args a)
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
                     if ((nzbits >> q) & 1u) {
-                        a.out_idx[o] = (uint32_t)sub + tid * 4 + q;
-                        a.out_val[o] = vals[q];
+                        put_sparse(a, o, (uint32_t)sub + tid * 4 + q, vals[q]);
                         ++o;
                     }
                 }
@@ -1371,7 +1385,8 @@ hipError_t set_result_run(ReduceResult* r, uint64_t nnz, uint32_t dense, hipStre
 
 hipError_t reduce_run(const ReducePlan& p, const StreamDesc* host_tab, uint32_t* out_idx,
                       float* out_val, uint64_t* node_nnz, uint8_t* node_dense, void* ws,
-                      hipStream_t s, ReduceResult* res, uint32_t nfold, ReduceResult* dev_result)
+                      hipStream_t s, ReduceResult* res, uint32_t nfold, ReduceResult* dev_result,
+                      uint64_t out_cap)
 {
     const Layout l = layout(p, ws);
     hipError_t e;
@@ -1467,6 +1482,9 @@ hipError_t reduce_run(const ReducePlan& p, const StreamDesc* host_tab, uint32_t*
     a.tpc = p.tiles_per_chunk;
     a.qbits = p.qbits;
     a.out_vec = (reinterpret_cast<uintptr_t>(out_val) & 15u) == 0 ? 1u : 0u;
+    a.out_cap = (uint32_t)std::min<uint64_t>(out_cap, 0xFFFFFFFFull);
+    a.err_hdr = &l.hdr->pad;
+    a.err_res = dev_result ? &dev_result->pad : nullptr;
     const bool quant = p.qbits != 0;
 
     e = p.speculate_dense ? launch_pass<kDense>(a, p.PK, quant, s)
