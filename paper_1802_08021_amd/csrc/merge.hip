@@ -475,8 +475,9 @@ __device__ __forceinline__ uint32_t merge_levels(MLds<C>& m, uint32_t PT, uint32
 //  * an entry's place in that order is its position in its own run plus,
 //    for every other slot, the entries of that slot's run that precede it
 //    (indices below its own, and equal ones of lower slots): fixed-step
-//    binary searches, eight slots side by side, and up to eight lanes per
-//    entry (each taking every G-th slot) while entries are few;
+//    binary searches, eight slots side by side, and G lanes per entry
+//    (each taking every G-th slot; G up to 8 while entries are few, and at
+//    most PT / 8 so that a lane keeps eight slots);
 //  * the entries move to their places, with their slots, so an index's
 //    entries are consecutive and in slot order;
 //  * two neighbouring slots r' < r there first share a node at level h + 1,
