@@ -27,6 +27,7 @@ namespace {
 constexpr uint32_t kUnit = 4096;  // elements per wave unit (64 iterations of 64 lanes)
 constexpr uint32_t kSlots = 32;   // gathered entries per unit
 constexpr int kHistBlocksPerRank = 64;
+constexpr uint32_t kExactGatherBlocks = 64;  // workgroups per row of the exact path's gather (grid-stride)
 constexpr uint64_t kSampleSegs = 1024;  // 256-element segments sampled per row
 // Gathered keys are also listed per row in kSub sub-lists (unit u appends to
 // sub-list u mod kSub, reserving its place with one atomic on that
@@ -268,99 +269,103 @@ __global__ void __launch_bounds__(256) k_gather(const float* x, uint64_t N, uint
                                                 uint32_t exact, uint32_t* klist, uint32_t* kcnt)
 {
     const uint32_t r = blockIdx.y, lane = threadIdx.x & 63;
-    const uint32_t u = blockIdx.x * 4 + (threadIdx.x >> 6);
-    if (u >= U || st[r].exact != exact || overflow[r] != 0u) return;  // not this path, or gathered too many
-    const uint32_t bin = st[r].prefix;
-    const float* row = x + (uint64_t)r * N;
-    float* res = residual && residual != x ? residual + (uint64_t)r * N : nullptr;
-    const uint64_t lo = (uint64_t)u * kUnit, hi = min(lo + kUnit, N);
-    uint2* cu = cand + ((uint64_t)r * U + u) * kSlots;
-    const uint32_t sub = u % kSub;
-    uint32_t* kl = klist + ((uint64_t)r * kSub + sub) * kSubCap;
-    uint32_t* kc = kcnt + ((uint64_t)r * kSub + sub) * kCntStride;
-    // The unit's count first, then its entries: into the unit's slots in
-    // index order and, at a place reserved with one atomic, into the row's
-    // key list.  Returns whether the unit's entries are to be written.
-    auto reserve = [&](uint32_t nc, uint32_t* base) {
-        uint32_t b = kSubCap;
-        if (lane == 0) {
-            ccnt[(uint64_t)r * U + u] = nc;
-            if (nc > kSlots) {
-                atomicOr(&overflow[r], 1u);
-            } else if (nc) {
-                b = atomicAdd(kc, nc);
-                if (b + nc > kSubCap) atomicOr(&overflow[r], 1u);
+    if (st[r].exact != exact) return;  // not this path
+    // units one a wave, grid-stride: the fallback launch takes a grid
+    // smaller than the row's units (most rows skip it at once)
+    for (uint32_t u = blockIdx.x * 4 + (threadIdx.x >> 6); u < U; u += gridDim.x * 4) {
+        if (overflow[r] != 0u) return;  // gathered too many
+        const uint32_t bin = st[r].prefix;
+        const float* row = x + (uint64_t)r * N;
+        float* res = residual && residual != x ? residual + (uint64_t)r * N : nullptr;
+        const uint64_t lo = (uint64_t)u * kUnit, hi = min(lo + kUnit, N);
+        uint2* cu = cand + ((uint64_t)r * U + u) * kSlots;
+        const uint32_t sub = u % kSub;
+        uint32_t* kl = klist + ((uint64_t)r * kSub + sub) * kSubCap;
+        uint32_t* kc = kcnt + ((uint64_t)r * kSub + sub) * kCntStride;
+        // The unit's count first, then its entries: into the unit's slots in
+        // index order and, at a place reserved with one atomic, into the row's
+        // key list.  Returns whether the unit's entries are to be written.
+        auto reserve = [&](uint32_t nc, uint32_t* base) {
+            uint32_t b = kSubCap;
+            if (lane == 0) {
+                ccnt[(uint64_t)r * U + u] = nc;
+                if (nc > kSlots) {
+                    atomicOr(&overflow[r], 1u);
+                } else if (nc) {
+                    b = atomicAdd(kc, nc);
+                    if (b + nc > kSubCap) atomicOr(&overflow[r], 1u);
+                }
             }
-        }
-        *base = (uint32_t)__builtin_amdgcn_readfirstlane((int)b);
-        return nc != 0u && nc <= kSlots && *base + nc <= kSubCap;
-    };
-    auto put = [&](uint32_t at, uint32_t base, uint64_t e, float v) {
-        cu[at] = make_uint2((uint32_t)e, __float_as_uint(v));
-        kl[base + at] = mag_key(v);
-    };
-    const bool rvec = res == nullptr || (reinterpret_cast<uintptr_t>(res) & 15u) == 0u;
-    if ((reinterpret_cast<uintptr_t>(row) & 15u) == 0u && rvec && hi - lo == kUnit) {
-        // the unit's 16 float4 per lane, all requested before use (loads
-        // marked nontemporal: the row is streamed once); lane i holds
-        // elements 4i..4i+3 of every 256, so entries are placed in index
-        // order by a wave scan per 256 elements that hold any
-        float4 vs[kUnit / 256];
-#pragma unroll
-        for (uint32_t q = 0; q < kUnit / 256; ++q)
-            vs[q] = load_nt(row + lo + 256u * q + 4u * lane);
-        // in-bin flags of the lane's elements, bit k of nibble q for element
-        // 256q + 4 lane + k (two words of eight nibbles: a handful of
-        // registers instead of 64 lane masks)
-        auto in4 = [&](const float4& v) {
-            return (uint32_t)((mag_key(v.x) >> 20) >= bin) | (uint32_t)((mag_key(v.y) >> 20) >= bin) << 1 |
-                   (uint32_t)((mag_key(v.z) >> 20) >= bin) << 2 | (uint32_t)((mag_key(v.w) >> 20) >= bin) << 3;
+            *base = (uint32_t)__builtin_amdgcn_readfirstlane((int)b);
+            return nc != 0u && nc <= kSlots && *base + nc <= kSubCap;
         };
-        uint32_t fl[2] = {0u, 0u};
-#pragma unroll
-        for (uint32_t q = 0; q < kUnit / 256; ++q) {
-            fl[q / 8] |= in4(vs[q]) << (4 * (q % 8));
-            if (res) store_nt(res + lo + 256u * q + 4u * lane, vs[q]);
-        }
-        const uint32_t mine = (uint32_t)__popc(fl[0]) + (uint32_t)__popc(fl[1]);
-        const uint32_t nc = (uint32_t)__builtin_amdgcn_readlane((int)wave_scan(mine), 63);
-        uint32_t base;
-        if (reserve(nc, &base)) {
-            uint32_t run = 0;
-#pragma unroll
+        auto put = [&](uint32_t at, uint32_t base, uint64_t e, float v) {
+            cu[at] = make_uint2((uint32_t)e, __float_as_uint(v));
+            kl[base + at] = mag_key(v);
+        };
+        const bool rvec = res == nullptr || (reinterpret_cast<uintptr_t>(res) & 15u) == 0u;
+        if ((reinterpret_cast<uintptr_t>(row) & 15u) == 0u && rvec && hi - lo == kUnit) {
+            // the unit's 16 float4 per lane, all requested before use (loads
+            // marked nontemporal: the row is streamed once); lane i holds
+            // elements 4i..4i+3 of every 256, so entries are placed in index
+            // order by a wave scan per 256 elements that hold any
+            float4 vs[kUnit / 256];
+    #pragma unroll
+            for (uint32_t q = 0; q < kUnit / 256; ++q)
+                vs[q] = load_nt(row + lo + 256u * q + 4u * lane);
+            // in-bin flags of the lane's elements, bit k of nibble q for element
+            // 256q + 4 lane + k (two words of eight nibbles: a handful of
+            // registers instead of 64 lane masks)
+            auto in4 = [&](const float4& v) {
+                return (uint32_t)((mag_key(v.x) >> 20) >= bin) | (uint32_t)((mag_key(v.y) >> 20) >= bin) << 1 |
+                       (uint32_t)((mag_key(v.z) >> 20) >= bin) << 2 | (uint32_t)((mag_key(v.w) >> 20) >= bin) << 3;
+            };
+            uint32_t fl[2] = {0u, 0u};
+    #pragma unroll
             for (uint32_t q = 0; q < kUnit / 256; ++q) {
-                const uint32_t f = (fl[q / 8] >> (4 * (q % 8))) & 15u;
-                const uint32_t n4 = (uint32_t)__popc(f);
-                if (__ballot(n4 != 0u) == 0ull) continue;  // no entry in these 256 elements
-                const uint64_t e = lo + 256u * q + 4u * lane;
-                const uint32_t incl = wave_scan(n4);
-                uint32_t at = run + incl - n4;
-                if (f & 1u) put(at++, base, e, vs[q].x);
-                if (f & 2u) put(at++, base, e + 1, vs[q].y);
-                if (f & 4u) put(at++, base, e + 2, vs[q].z);
-                if (f & 8u) put(at, base, e + 3, vs[q].w);
-                run += (uint32_t)__builtin_amdgcn_readlane((int)incl, 63);
+                fl[q / 8] |= in4(vs[q]) << (4 * (q % 8));
+                if (res) store_nt(res + lo + 256u * q + 4u * lane, vs[q]);
             }
-        }
-    } else {
-        // short or unaligned unit: count (and copy), then read again to place
-        uint32_t nc = 0;
-        for (uint64_t e0 = lo; e0 < hi; e0 += 64) {
-            const uint64_t e = e0 + lane;
-            const float v = e < hi ? row[e] : 0.0f;
-            nc += (uint32_t)__popcll(__ballot(e < hi && (mag_key(v) >> 20) >= bin));
-            if (res && e < hi) res[e] = v;
-        }
-        uint32_t base;
-        if (reserve(nc, &base)) {
-            uint32_t run = 0;
+            const uint32_t mine = (uint32_t)__popc(fl[0]) + (uint32_t)__popc(fl[1]);
+            const uint32_t nc = (uint32_t)__builtin_amdgcn_readlane((int)wave_scan(mine), 63);
+            uint32_t base;
+            if (reserve(nc, &base)) {
+                uint32_t run = 0;
+    #pragma unroll
+                for (uint32_t q = 0; q < kUnit / 256; ++q) {
+                    const uint32_t f = (fl[q / 8] >> (4 * (q % 8))) & 15u;
+                    const uint32_t n4 = (uint32_t)__popc(f);
+                    if (__ballot(n4 != 0u) == 0ull) continue;  // no entry in these 256 elements
+                    const uint64_t e = lo + 256u * q + 4u * lane;
+                    const uint32_t incl = wave_scan(n4);
+                    uint32_t at = run + incl - n4;
+                    if (f & 1u) put(at++, base, e, vs[q].x);
+                    if (f & 2u) put(at++, base, e + 1, vs[q].y);
+                    if (f & 4u) put(at++, base, e + 2, vs[q].z);
+                    if (f & 8u) put(at, base, e + 3, vs[q].w);
+                    run += (uint32_t)__builtin_amdgcn_readlane((int)incl, 63);
+                }
+            }
+        } else {
+            // short or unaligned unit: count (and copy), then read again to place
+            uint32_t nc = 0;
             for (uint64_t e0 = lo; e0 < hi; e0 += 64) {
                 const uint64_t e = e0 + lane;
                 const float v = e < hi ? row[e] : 0.0f;
-                const bool in = e < hi && (mag_key(v) >> 20) >= bin;
-                const uint64_t m = __ballot(in);
-                if (in) put(run + (uint32_t)__popcll(m & ((1ull << lane) - 1ull)), base, e, v);
-                run += (uint32_t)__popcll(m);
+                nc += (uint32_t)__popcll(__ballot(e < hi && (mag_key(v) >> 20) >= bin));
+                if (res && e < hi) res[e] = v;
+            }
+            uint32_t base;
+            if (reserve(nc, &base)) {
+                uint32_t run = 0;
+                for (uint64_t e0 = lo; e0 < hi; e0 += 64) {
+                    const uint64_t e = e0 + lane;
+                    const float v = e < hi ? row[e] : 0.0f;
+                    const bool in = e < hi && (mag_key(v) >> 20) >= bin;
+                    const uint64_t m = __ballot(in);
+                    if (in) put(run + (uint32_t)__popcll(m & ((1ull << lane) - 1ull)), base, e, v);
+                    run += (uint32_t)__popcll(m);
+                }
             }
         }
     }
@@ -814,7 +819,8 @@ hipError_t topk_run(int P, const float* x, uint64_t N, uint64_t k, uint32_t* out
     // rows on the exact path: the exact boundary bin, a gather from it
     hipLaunchKernelGGL(k_hist<0>, hgrid, dim3(256), 0, s, x, N, l.st, l.hist);
     hipLaunchKernelGGL(k_select<0>, dim3(P), dim3(256), 0, s, l.st, l.hist);
-    hipLaunchKernelGGL(k_gather, ugrid, dim3(256), 0, s, x, N, l.U, l.st, l.cand, l.ccnt, l.overflow,
+    const dim3 xgrid(std::min<uint32_t>((l.U + 3) / 4, kExactGatherBlocks), P);
+    hipLaunchKernelGGL(k_gather, xgrid, dim3(256), 0, s, x, N, l.U, l.st, l.cand, l.ccnt, l.overflow,
                        residual, 1u, l.klist, l.kcnt);
     hipLaunchKernelGGL(k_cand_select, dim3(P), dim3(1024), 0, s, k, l.st, l.klist, l.kcnt, l.overflow, 1u);
     // rows whose boundary bin overflowed the gather buffer (the others return at once)
